@@ -1,0 +1,483 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix (no GPU).
+
+Each test names the passage of TurboAngle (arXiv 2603.27467) or the mathematical fact it
+checks.  The checks are chosen so that a dropped term, a wrong sign, index or ordering, or a
+transposed operand in the oracle fails at least one of them.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy import stats
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# --------------------------------------------------------------------------- sign diagonal
+def test_splitmix64_published_stream(orc):
+    """SplitMix64 (Steele, Lea, Flood 2014): outputs for seed 0 from the published stream."""
+    vals = [int(l, 16) for l in open(os.path.join(GOLDEN, "splitmix64_seed0.txt"))
+            if l.strip() and not l.startswith("#")]
+    gamma = 0x9E3779B97F4A7C15
+    state = 0
+    for v in vals:
+        state = (state + gamma) % 2**64
+        assert orc.splitmix64_mix(state) == v
+
+
+def test_signs_are_the_stream_top_bits(orc):
+    """Section 3.1 'Implementation': D drawn once from a seeded PRNG.  Row l is the top bits of
+    the SplitMix64 stream keyed by mix(seed ^ (l+1)*C); balanced and different per layer."""
+    d = 4096
+    rows = [orc.signs(7, l, d) for l in range(4)]
+    for r in rows:
+        assert set(np.unique(r)) <= {-1, 1}
+        assert abs(int(r.sum())) < 4 * math.sqrt(d)          # fair coin
+    assert not np.array_equal(rows[0], rows[1])
+    key = orc.splitmix64_mix(7 ^ ((0 + 1) * 0xD1B54A32D192ED03 % 2**64))
+    first = orc.splitmix64_mix((key + 0x9E3779B97F4A7C15) % 2**64)
+    assert rows[0][0] == (-1 if first >> 63 else 1)
+
+
+# --------------------------------------------------------------------------- Hadamard
+@pytest.mark.parametrize("d", [2, 4, 8, 16, 64, 128])
+def test_hadamard_orthonormal_symmetric(orc, d):
+    """Section 2: H has entries +-1/sqrt(d), is symmetric and orthonormal, hence H^-1 = H."""
+    H = orc.hadamard(d)
+    assert np.allclose(np.abs(H), 1 / math.sqrt(d), rtol=0, atol=1e-15)
+    assert np.array_equal(H, H.T)
+    assert np.abs(H @ H - np.eye(d)).max() < 1e-13
+    x = np.random.default_rng(d).standard_normal(d)
+    assert abs(np.linalg.norm(H @ x) - np.linalg.norm(x)) < 1e-12 * np.linalg.norm(x)
+
+
+@pytest.mark.parametrize("d", [2, 4, 8, 16])
+def test_butterfly_equals_explicit_matrix(orc, d):
+    """The O(d log d) butterfly is the Sylvester matrix product: fp64 to rounding, and the fp32
+    butterfly exactly for small-integer inputs (all partial sums are exact integers)."""
+    rng = np.random.default_rng(100 + d)
+    H = orc.hadamard(d) * math.sqrt(d)     # unnormalized +-1 matrix
+    for _ in range(20):
+        x = rng.standard_normal(d)
+        assert np.abs(orc.fwht_f64(x) - H @ x).max() < 1e-12
+        xi = rng.integers(-1000, 1000, d).astype(np.float32)
+        assert np.array_equal(orc.fwht_f32(xi), (H @ xi.astype(np.float64)).astype(np.float32))
+
+
+def test_butterfly_sylvester_not_sequency_order(orc):
+    """Reading of 'consecutive pairs': natural (Sylvester) order.  Row 1 of the Sylvester
+    matrix alternates sign; e_1 maps to (+1, -1, +1, -1, ...)."""
+    e1 = np.zeros(8, np.float32)
+    e1[1] = 1
+    assert list(orc.fwht_f32(e1)) == [1, -1, 1, -1, 1, -1, 1, -1]
+    e2 = np.zeros(8, np.float32)
+    e2[2] = 1
+    assert list(orc.fwht_f32(e2)) == [1, 1, -1, -1, 1, 1, -1, -1]
+
+
+def test_fp32_butterfly_close_to_fp64(orc):
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal(128).astype(np.float32)
+    z32 = orc.fwht_f32(x).astype(np.float64)
+    z64 = orc.fwht_f64(x.astype(np.float64))
+    assert np.abs(z32 - z64).max() < 1e-5 * np.abs(z64).max()
+
+
+# --------------------------------------------------------------------------- worked examples
+def test_worked_example_d2(orc):
+    """Algorithm 1 by hand: d=2, D=I, x=(1,0) -> y=(1/sqrt2, 1/sqrt2), theta=pi/4, r=1;
+    n=8 gives k=1 (pi/4 = 2 pi * 1/8); reconstruction returns (1, 0)."""
+    s = np.array([1, 1], np.int8)
+    vc = orc.encode_vector(np.array([1, 0], np.float32), s, orc.Kind(8))
+    assert vc.k.tolist() == [1]
+    assert abs(vc.rn[0] - 1.0) < 1e-7
+    assert abs(vc.u[0] - 1.0) < 1e-12
+    x = orc.decode_vector(orc.Kind(8), s, vc.k, None, vc.rn, None)
+    assert np.abs(x - [1, 0]).max() < 1e-7
+
+
+def test_worked_example_d4_onehot(orc):
+    """d=4, x=e0: y=(1/2,1/2,1/2,1/2); both pairs at theta=pi/4 with r=sqrt(1/2)."""
+    s = np.ones(4, np.int8)
+    vc = orc.encode_vector(np.array([1, 0, 0, 0], np.float32), s, orc.Kind(64))
+    assert vc.k.tolist() == [8, 8]
+    assert np.allclose(vc.rn, math.sqrt(0.5), rtol=1e-7)
+
+
+def test_sign_flip_enters_before_transform(orc):
+    """y = H D x: encoding x under D equals encoding D x under the identity.  With
+    D = diag(1, -1) and x = (0, 1): D x = (0, -1), y = (-1, 1)/sqrt2, theta = 3pi/4, k = 3 at
+    n = 8; without the flip y = (1, -1)/sqrt2, theta = -pi/4, k = 7."""
+    s = np.array([1, -1], np.int8)
+    ident = np.array([1, 1], np.int8)
+    a = orc.encode_vector(np.array([0, 1], np.float32), s, orc.Kind(8))
+    b = orc.encode_vector(np.array([0, -1], np.float32), ident, orc.Kind(8))
+    c = orc.encode_vector(np.array([0, 1], np.float32), ident, orc.Kind(8))
+    assert a.k.tolist() == b.k.tolist() == [3]
+    assert c.k.tolist() == [7]
+
+
+@pytest.mark.parametrize("n", [8, 16, 64, 256])
+@pytest.mark.parametrize("m", [0, 1, 6, 127])
+def test_onehot_closed_form(orc, n, m):
+    """x = c e_m: every |y_i| = |c|/sqrt(d), so every r_i = |c| sqrt(2/d); the pair angles are
+    +-pi/4 or +-3pi/4, i.e. codes in {n/8, 3n/8, 5n/8, 7n/8}; equal norms make the linear and
+    log quantizers degenerate (codes 0) and the fp32-norm round trip exact to rounding."""
+    d = 128
+    c = np.float32(3.5)
+    x = np.zeros(d, np.float32)
+    x[m] = c
+    s = orc.signs(11, 0, d)
+    vc = orc.encode_vector(x, s, orc.Kind(n))
+    assert set(vc.k.tolist()) <= {n // 8, 3 * n // 8, 5 * n // 8, 7 * n // 8}
+    assert np.allclose(vc.rn, float(c) * math.sqrt(2 / d), rtol=1e-6)
+    xr = orc.decode_vector(orc.Kind(n), s, vc.k, None, vc.rn, None)
+    assert np.abs(xr - x).max() < 1e-5
+    for mode in (orc.NORM_LINEAR, orc.NORM_LOG):
+        vq = orc.encode_vector(x, s, orc.Kind(n, mode, 4))
+        assert vq.hdr[0] == vq.hdr[1]
+        assert not vq.q.any() and np.isnan(vq.t).all()
+        xr = orc.decode_vector(orc.Kind(n, mode, 4), s, vq.k, vq.q, None, vq.hdr)
+        assert np.abs(xr - x).max() < 1e-5
+
+
+def test_zero_vector(orc):
+    """Zero pairs have angle 0 (reading of atan2(0,0)); the zero vector encodes to all-zero codes
+    and decodes to exact zeros."""
+    d = 64
+    s = orc.signs(3, 0, d)
+    for mode in (orc.NORM_F32, orc.NORM_LINEAR, orc.NORM_LOG):
+        kd = orc.Kind(64, mode, 8)
+        vc = orc.encode_vector(np.zeros(d, np.float32), s, kd)
+        assert not vc.k.any() and not vc.q.any()
+        x = orc.decode_vector(kd, s, vc.k, vc.q, vc.rn, vc.hdr)
+        assert not x.any()
+
+
+# --------------------------------------------------------------------------- angle quantizer
+def test_angle_code_rounding_and_mod(orc):
+    """Algorithm 1: k = round(u) mod n with u = n theta / 2pi; nearest bin centred at 2pi k/n,
+    half-up at ties, Euclidean mod for negative angles (atan2 in (-pi, pi])."""
+    n = 64
+    assert orc.angle_code(0.49, n) == 0
+    assert orc.angle_code(0.5, n) == 1
+    assert orc.angle_code(-0.49, n) == 0
+    assert orc.angle_code(-0.51, n) == n - 1
+    assert orc.angle_code(-n / 2, n) == n // 2
+    assert orc.angle_code(n / 2, n) == n // 2
+    assert orc.angle_code(n / 2 - 0.2, n) == n // 2
+    assert orc.angle_code(-1.4, 5) == 4
+    assert orc.angle_code(2.5, 5) == 3 % 5
+
+
+@pytest.mark.parametrize("n", [8, 48, 64, 256])
+def test_angle_error_bound(orc, n):
+    """Per-pair angle error is at most pi/n before norm quantization (bins of width 2pi/n)."""
+    rng = np.random.default_rng(n)
+    d = 128
+    s = orc.signs(1, 0, d)
+    worst = 0.0
+    for _ in range(200):
+        x = rng.standard_normal(d).astype(np.float32)
+        vc = orc.encode_vector(x, s, orc.Kind(n))
+        theta = 2 * np.pi * vc.u / n
+        err = np.angle(np.exp(1j * (theta - 2 * np.pi * vc.k / n)))
+        worst = max(worst, np.abs(err).max())
+        # also from the rebuilt pairs of the fp64 decode
+    assert worst <= np.pi / n + 1e-12
+    assert worst > 0.9 * np.pi / n       # the bound is attained in the limit
+
+
+@pytest.mark.parametrize("n", [16, 64])
+def test_reconstructed_pair_angle(orc, n):
+    """Reconstruction puts pair i at angle 2 pi k_i / n with radius r_i (fp32 norms)."""
+    d = 64
+    rng = np.random.default_rng(9)
+    s = orc.signs(2, 0, d)
+    x = rng.standard_normal(d).astype(np.float32)
+    vc = orc.encode_vector(x, s, orc.Kind(n))
+    xr = orc.decode_vector(orc.Kind(n), s, vc.k, None, vc.rn, None)
+    # forward-transform the reconstruction back to the pair domain
+    y = orc.hadamard(d) @ (s * xr)
+    ang = np.arctan2(y[1::2], y[0::2])
+    rad = np.hypot(y[0::2], y[1::2])
+    assert np.allclose(rad, vc.rn, rtol=1e-6, atol=1e-9)
+    assert np.abs(np.angle(np.exp(1j * (ang - 2 * np.pi * vc.k / n)))).max() < 1e-6
+
+
+# --------------------------------------------------------------------------- statistics
+@pytest.mark.parametrize("n", [16, 64])
+def test_angle_uniform_on_isotropic_gaussian(orc, n):
+    """Section 2: after D and H, pairs of an isotropic Gaussian input are isotropic, so angle
+    codes are uniform -- chi-square with n-1 degrees of freedom, p >= 1e-3."""
+    rng = np.random.default_rng(1234 + n)
+    d = 128
+    s = orc.signs(21, 0, d)
+    counts = np.zeros(n, np.int64)
+    for _ in range(1500):
+        vc = orc.encode_vector(rng.standard_normal(d).astype(np.float32), s, orc.Kind(n))
+        counts += np.bincount(vc.k, minlength=n)
+    chi2, p = stats.chisquare(counts)
+    assert p >= 1e-3, (chi2, p)
+
+
+def test_angle_density_for_unequal_channel_variances(orc):
+    """For independent channels with variances sigma^2, every transformed pair has correlation
+    rho = sum_m (-1)^m sigma_m^2 / sum_m sigma_m^2 (independent of D), and its angle density is
+    sqrt(1-rho^2) / (2 pi (1 - rho sin 2theta)).  The oracle's bin counts follow it."""
+    rng = np.random.default_rng(77)
+    d, n = 64, 32
+    sig = np.exp(rng.standard_normal(d)).astype(np.float64)
+    sig[::2] *= 1.6                       # make the even/odd energy imbalance clear
+    rho = float(np.sum(sig**2 * (-1.0) ** np.arange(d)) / np.sum(sig**2))
+    s = orc.signs(5, 0, d)
+    counts = np.zeros(n, np.int64)
+    N = 3000
+    for _ in range(N):
+        x = (rng.standard_normal(d) * sig).astype(np.float32)
+        counts += np.bincount(orc.encode_vector(x, s, orc.Kind(n)).k, minlength=n)
+    # expected bin masses by integrating the density over each bin
+    edges = (np.arange(n + 1) - 0.5) * 2 * np.pi / n
+    th = np.linspace(edges[0], edges[-1], 200001)
+    dens = np.sqrt(1 - rho**2) / (2 * np.pi * (1 - rho * np.sin(2 * th)))
+    cdf = np.concatenate([[0], np.cumsum((dens[1:] + dens[:-1]) / 2 * np.diff(th))])
+    mass = np.diff(np.interp(edges, th, cdf))
+    mass /= mass.sum()
+    chi2, p = stats.chisquare(counts, mass * counts.sum())
+    assert p >= 1e-3, (rho, chi2, p)
+    # and the uniform null is rejected for this input
+    assert stats.chisquare(counts)[1] < 1e-6
+
+
+@pytest.mark.parametrize("n", [32, 64])
+def test_mse_closed_form_fp32_norms(orc, n):
+    """With fp32 norms and an isotropic Gaussian input, HD is orthogonal and the angle error is
+    uniform on [-pi/n, pi/n], so E|x - x^|^2 / E|x|^2 = 2 (1 - sin(pi/n) / (pi/n))."""
+    rng = np.random.default_rng(31 + n)
+    d = 128
+    s = orc.signs(8, 0, d)
+    num = den = 0.0
+    for _ in range(600):
+        x = rng.standard_normal(d).astype(np.float32)
+        vc = orc.encode_vector(x, s, orc.Kind(n))
+        xr = orc.decode_vector(orc.Kind(n), s, vc.k, None, vc.rn, None)
+        num += float(np.sum((xr - x) ** 2))
+        den += float(np.sum(x.astype(np.float64) ** 2))
+    a = np.pi / n
+    expect = 2 * (1 - np.sin(a) / a)
+    assert abs(num / den / expect - 1) < 0.03, (num / den, expect)
+
+
+# --------------------------------------------------------------------------- equivariances
+def test_scale_equivariance(orc):
+    """encode(2^j x): identical angle and norm codes, header scaled by exactly 2^j (both
+    quantizers use only ratios of norms); decode scales by exactly 2^j."""
+    rng = np.random.default_rng(3)
+    d = 128
+    s = orc.signs(4, 0, d)
+    for mode, bits in ((orc.NORM_LINEAR, 8), (orc.NORM_LOG, 4)):
+        kd = orc.Kind(64, mode, bits)
+        for _ in range(20):
+            x = rng.standard_normal(d).astype(np.float32)
+            a = orc.encode_vector(x, s, kd)
+            b = orc.encode_vector(x * np.float32(8.0), s, kd)
+            assert np.array_equal(a.k, b.k) and np.array_equal(a.q, b.q)
+            assert np.array_equal(a.hdr * 8, b.hdr)
+            xa = orc.decode_vector(kd, s, a.k, a.q, None, a.hdr, "f32")
+            xb = orc.decode_vector(kd, s, b.k, b.q, None, b.hdr, "f32")
+            assert np.array_equal(xa * 8, xb)
+
+
+def test_negation_rotates_codes_by_half_turn(orc):
+    """encode(-x): each pair rotates by pi, so k -> k + n/2 mod n (even n), away from flags."""
+    rng = np.random.default_rng(4)
+    d, n = 128, 64
+    s = orc.signs(6, 0, d)
+    for _ in range(30):
+        x = rng.standard_normal(d).astype(np.float32)
+        a = orc.encode_vector(x, s, orc.Kind(n))
+        b = orc.encode_vector(-x, s, orc.Kind(n))
+        ok = ~orc.angle_flags(a.u, n)
+        assert np.array_equal(b.k[ok], (a.k[ok] + n // 2) % n)
+        assert np.array_equal(a.rn, b.rn)
+
+
+# --------------------------------------------------------------------------- norm quantizers
+@pytest.mark.parametrize("bits", [4, 8])
+def test_linear_norm_bounds(orc, bits):
+    """Eq. (2): codes span [0, 2^b-1], extremes map to 0 and 2^b-1, and the code-centre
+    reconstruction is within half a step (Rmax-Rmin)/(2(2^b-1)) of the norm."""
+    rng = np.random.default_rng(bits)
+    d = 128
+    s = orc.signs(9, 0, d)
+    kd = orc.Kind(64, orc.NORM_LINEAR, bits)
+    for _ in range(50):
+        x = (rng.standard_normal(d) * np.exp(rng.standard_normal(d))).astype(np.float32)
+        vc = orc.encode_vector(x, s, kd)
+        r = np.hypot(vc.z[0::2].astype(np.float64), vc.z[1::2].astype(np.float64)) / np.sqrt(d)
+        assert vc.q.min() == 0 and vc.q.max() == 2**bits - 1
+        assert vc.q[np.argmin(r)] == 0 and vc.q[np.argmax(r)] == 2**bits - 1
+        rh = orc.dequant_norms_f64(kd, vc.q, None, vc.hdr, d // 2)
+        step = (float(vc.hdr[1]) - float(vc.hdr[0])) / (2**bits - 1)
+        assert np.abs(rh - r).max() <= step / 2 * (1 + 1e-6) + 1e-7 * r.max()
+        # monotone: larger norm never gets a smaller code
+        o = np.argsort(r)
+        assert np.all(np.diff(vc.q[o].astype(np.int64)) >= 0)
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_log_norm_bounds(orc, bits):
+    """Log-space variant: half a step in log r, (ln Rmax - ln Rmin)/(2(2^b-1))."""
+    rng = np.random.default_rng(40 + bits)
+    d = 128
+    s = orc.signs(10, 0, d)
+    kd = orc.Kind(64, orc.NORM_LOG, bits)
+    for _ in range(50):
+        x = rng.standard_normal(d).astype(np.float32)
+        vc = orc.encode_vector(x, s, kd)
+        r = np.hypot(vc.z[0::2].astype(np.float64), vc.z[1::2].astype(np.float64)) / np.sqrt(d)
+        assert vc.q.min() == 0 and vc.q.max() == 2**bits - 1
+        rh = orc.dequant_norms_f64(kd, vc.q, None, vc.hdr, d // 2)
+        step = (np.log(float(vc.hdr[1])) - np.log(float(vc.hdr[0]))) / (2**bits - 1)
+        assert np.abs(np.log(rh) - np.log(r)).max() <= step / 2 * (1 + 1e-6) + 1e-7
+
+
+def test_log_levels_are_geometric(orc):
+    """Log-space codes decode to a geometric ladder from Rmin to Rmax."""
+    kd = orc.Kind(8, orc.NORM_LOG, 4)
+    hdr = np.array([0.5, 8.0], np.float32)
+    q = np.arange(16, dtype=np.uint32)
+    rh = orc.dequant_norms_f64(kd, q, None, hdr, 16)
+    assert np.allclose(rh, 0.5 * 16.0 ** (np.arange(16) / 15), rtol=1e-14)
+    kl = orc.Kind(8, orc.NORM_LINEAR, 4)
+    assert np.allclose(orc.dequant_norms_f64(kl, q, None, hdr, 16), 0.5 + 7.5 * np.arange(16) / 15,
+                       rtol=1e-14)
+
+
+def test_norm_codes_use_stored_header(orc):
+    """Codes are computed against the stored fp32 (Rmin, Rmax): the maximal pair gets the top
+    code even though fp32 rounding can put Rmax below the exact maximum."""
+    rng = np.random.default_rng(12)
+    s = orc.signs(1, 0, 64)
+    kd = orc.Kind(64, orc.NORM_LINEAR, 16)
+    for _ in range(100):
+        vc = orc.encode_vector(rng.standard_normal(64).astype(np.float32), s, kd)
+        assert vc.q.max() == 65535 and vc.q.min() == 0
+        assert np.nanmax(vc.t) == pytest.approx(65535, abs=0.01)
+
+
+# --------------------------------------------------------------------------- decode variants
+def test_decode_f32_matches_f64(orc):
+    rng = np.random.default_rng(13)
+    d = 128
+    s = orc.signs(3, 0, d)
+    for mode, bits in ((orc.NORM_F32, 0), (orc.NORM_LINEAR, 8), (orc.NORM_LOG, 4)):
+        kd = orc.Kind(64, mode, bits)
+        for _ in range(30):
+            x = (rng.standard_normal(d) * 3).astype(np.float32)
+            vc = orc.encode_vector(x, s, kd)
+            a = orc.decode_vector(kd, s, vc.k, vc.q, vc.rn, vc.hdr, "f64")
+            b = orc.decode_vector(kd, s, vc.k, vc.q, vc.rn, vc.hdr, "f32")
+            assert np.linalg.norm(a - b) <= 1e-6 * np.linalg.norm(a)
+
+
+@pytest.mark.parametrize("n", [2, 3, 8, 48, 56, 64, 100, 256, 4096])
+def test_trig_table(orc, n):
+    """cos/sin(2 pi k / n) rounded to fp32; exact 0 and +-1 at quarter turns, symmetric."""
+    c, s = orc.trig_table(n)
+    k = np.arange(n)
+    ang = 2 * np.pi * k / n
+    assert np.abs(c - np.cos(ang)).max() <= 6e-8
+    assert np.abs(s - np.sin(ang)).max() <= 6e-8
+    assert c[0] == 1 and s[0] == 0
+    if n % 4 == 0:
+        q = n // 4
+        assert (c[q], s[q]) == (0, 1) and (c[2 * q], s[2 * q]) == (-1, 0)
+        assert (c[3 * q], s[3 * q]) == (0, -1)
+    assert np.array_equal(c[1:], c[1:][::-1])        # cos(2pi(n-k)/n) = cos(2pi k/n)
+    assert np.array_equal(s[1:], -s[1:][::-1])
+    assert np.array_equal(c, c.astype(np.float64).astype(np.float32))
+
+
+# --------------------------------------------------------------------------- packing/layout
+def test_pack_bits_hand_example(orc):
+    """LSB-first bitstream: codes (5, 3, 1) at 3 bits = bits 101 110 100 -> bytes 0x5D, 0x00."""
+    out = orc.pack_bits([5, 3, 1], 3)
+    assert out.tolist() == [0x5D, 0x00]
+    assert orc.unpack_bits(out, 3, 3).tolist() == [5, 3, 1]
+    out = orc.pack_bits([0x3F, 0, 0x3F, 1], 6)       # 24 bits
+    assert out.tolist() == [0x3F, 0xF0, 0x07]
+
+
+@pytest.mark.parametrize("w", [1, 3, 5, 6, 7, 8, 12, 16])
+def test_pack_roundtrip(orc, w):
+    rng = np.random.default_rng(w)
+    c = rng.integers(0, 2**w, 64).astype(np.uint32)
+    assert np.array_equal(orc.unpack_bits(orc.pack_bits(c, w), 64, w), c)
+
+
+def test_cache_layout_sizes(orc):
+    """Planes back to back in (layer, kind, plane) order: d=128 K n=64 8-bit linear is
+    48 + 64 + 8 = 120 bytes per vector, V n=64 4-bit log 48 + 32 + 8 = 88."""
+    L, H, d, B, T = 2, 3, 128, 2, 5
+    kinds = [orc.Kind(64, orc.NORM_LINEAR, 8), orc.Kind(64, orc.NORM_LOG, 4),
+             orc.Kind(256, orc.NORM_F32, 0), orc.Kind(48, orc.NORM_LINEAR, 5)]
+    c = orc.Codec(L, H, d, kinds, np.ones((L, d), np.int8))
+    assert c.record_bytes(0, 0) == [48, 64, 8]
+    assert c.record_bytes(0, 1) == [48, 32, 8]
+    assert c.record_bytes(1, 0) == [64, 256, 0]
+    assert c.record_bytes(1, 1) == [48, 40, 8]
+    total, off = c.layout(B, T)
+    slots = B * H * T
+    assert total == slots * (120 + 88 + 320 + 96)
+    assert off[0, 1, 0] == slots * 120
+    assert off[1, 1, 2] == slots * (120 + 88 + 320 + 48 + 40)
+
+
+# --------------------------------------------------------------------------- rate accounting
+def _parse_rates():
+    rows = []
+    for line in open(os.path.join(GOLDEN, "paper_rates.txt")):
+        if not line.strip() or line.startswith("#"):
+            continue
+        f = [x.strip() for x in line.split("|")]
+
+        def groups(spec):
+            out = []
+            for g in spec.split():
+                v, cnt = g.split("x")
+                out += [int(v)] * int(cnt)
+            return out
+        rows.append((f[0], groups(f[1]), groups(f[2]), int(f[3]), int(f[4]), int(f[5]),
+                     float(f[6]), f[7]))
+    return rows
+
+
+@pytest.mark.parametrize("row", _parse_rates(), ids=lambda r: r[0])
+def test_paper_bit_rates(orc, row):
+    """Eq. (1) mean angle bits and eq. (3) totals reproduce the bits printed in Tables 1, 2, 4,
+    5, 6 and in the eq. (3) worked example, to their printed two decimals."""
+    label, nk, nv, bk, bv, d, printed, what = row
+    ang = orc.mean_angle_bits(nk, nv)
+    if what == "angle":
+        val = ang
+    elif what == "total":
+        val = (orc.total_bits(ang, bk, d) + orc.total_bits(ang, bv, d)) / 2
+    elif what == "totalK":
+        val = orc.total_bits(ang, bk, d)
+    else:
+        val = orc.total_bits(ang, bv, d)
+    assert abs(val - printed) <= 0.005 + 1e-9, (label, val, printed)
+
+
+def test_f32_to_bf16_rounding(orc):
+    """Round to nearest even on the 16 dropped bits; ties go to the even bf16."""
+    assert orc.f32_to_bf16_scalar(1.0) == 0x3F80
+    tie_down = np.array([0x3F808000], np.uint32).view(np.float32)[0]   # halfway, even below
+    tie_up = np.array([0x3F818000], np.uint32).view(np.float32)[0]     # halfway, odd below
+    assert orc.f32_to_bf16_scalar(tie_down) == 0x3F80
+    assert orc.f32_to_bf16_scalar(tie_up) == 0x3F82
+    x = np.random.default_rng(0).standard_normal(5000).astype(np.float32)
+    vec = orc.f32_to_bf16(x)
+    assert all(int(vec[i]) == orc.f32_to_bf16_scalar(float(x[i])) for i in range(0, 5000, 7))
