@@ -1,0 +1,178 @@
+/*
+ * tvq.h -- C ABI of the TurboAngle KV-cache codec for AMD Instinct MI355X (gfx950).
+ *
+ * Method: TurboAngle (arXiv 2603.27467).  Each (token, head) K or V vector x of length d is
+ *   1. sign-flipped by a random +-1 diagonal D and transformed by the normalized fast
+ *      Walsh-Hadamard transform H (section 2; Algorithm 1, first step);
+ *   2. split into d/2 consecutive pairs, each written in polar form (r_i, theta_i) with
+ *      theta_i quantized to one of n uniform bins (Algorithm 1), n chosen per layer and
+ *      separately for K and V (section 3.2, per-layer MixedKV / early-boost);
+ *   3. its pair norms kept in fp32 or quantized per vector by min-max scalar quantization,
+ *      linear (eq. (2)) or in log space (section 3.3), with the vector's min and max stored
+ *      as two fp32 values;
+ *   4. bit-packed into the compressed cache.
+ * Decoding rebuilds y^ = r^ (cos 2 pi k/n, sin 2 pi k/n) and x^ = D H y^ (section 3.1,
+ * reconstruction), using H^-1 = H and D^-1 = D.
+ *
+ * Conventions for every entry point:
+ *   - Plain C types only.  Device pointers are HIP device memory owned by the caller.
+ *     `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   - Nothing here allocates device memory except tvq_create; tvq_encode / tvq_decode only
+ *     validate on the host and enqueue kernels on `stream`, then return without waiting.
+ *   - Argument errors are reported synchronously by the return value and nothing is
+ *     launched.  A launch failure returns TVQ_ERR_HIP.  Faults inside a kernel surface at the
+ *     caller's next synchronization, as for any HIP work.
+ *   - A codec handle is immutable after tvq_create; concurrent calls on different streams are
+ *     safe.  Ordering an encode and a decode that touch the same cache tokens is the caller's
+ *     job (stream order or events).
+ */
+#ifndef TVQ_H
+#define TVQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TVQ_ABI_VERSION 1
+#define TVQ_MAX_LAYERS 256
+
+typedef enum {
+  TVQ_OK = 0,
+  TVQ_ERR_INVALID_ARG = -1,  /* a pointer, size, stride, alignment or config value is bad */
+  TVQ_ERR_UNSUPPORTED = -2,  /* valid for the method but not built for the GPU (e.g. d=32) */
+  TVQ_ERR_HIP = -3,          /* a HIP runtime call or kernel launch failed */
+  TVQ_ERR_ALLOC = -4         /* tvq_create could not allocate its device tables */
+} tvq_status;
+
+typedef enum { TVQ_BF16 = 0, TVQ_F32 = 1 } tvq_dtype;
+
+/* Norm storage (section 3.3): fp32 norms (16 bits per element, section 3.1 "Rate
+ * accounting"), per-vector min-max linear (eq. (2)), or min-max on log r (log-space variant). */
+typedef enum { TVQ_NORM_F32 = 0, TVQ_NORM_LINEAR = 1, TVQ_NORM_LOG = 2 } tvq_norm_mode;
+
+/* One layer of the per-layer codebook table (section 3.2: an independent (n_K, n_V) per
+ * layer; section 3.3: K and V norm bits, e.g. K 8-bit linear / V 4-bit log).
+ *   n_k, n_v           angle bins, 2..4096 (stored in ceil(log2 n) bits per pair)
+ *   norm_bits_k/_v     1..16 for LINEAR/LOG; ignored (32) for F32
+ *   norm_mode_k/_v     tvq_norm_mode                                                  */
+typedef struct {
+  uint16_t n_k, n_v;
+  uint8_t norm_bits_k, norm_bits_v;
+  uint8_t norm_mode_k, norm_mode_v;
+} tvq_layer_cfg;
+
+/* Codec configuration.
+ *   num_layers  L, 1..TVQ_MAX_LAYERS;  num_heads  H (KV heads) >= 1;
+ *   head_dim    d; the GPU kernels are built for d = 64 and d = 128
+ *   layers      [L] table, copied by tvq_create
+ *   signs       optional host array of +-1 (int8): [L][d], or [d] when shared_signs != 0.
+ *               NULL: drawn from `seed` with SplitMix64 (Steele, Lea and Flood 2014) as
+ *               tvq_make_signs describes.  The paper samples D once from a seeded PRNG and
+ *               shares it across layers (section 3.1 "Implementation"); shared_signs = 1 gives
+ *               that, shared_signs = 0 draws an independent D per layer.               */
+typedef struct {
+  int32_t num_layers, num_heads, head_dim;
+  int32_t shared_signs;
+  uint64_t seed;
+  const tvq_layer_cfg* layers;
+  const int8_t* signs;
+} tvq_config;
+
+/* A strided [L][B][H][T][d] view of K and V (the same strides for both), in elements, with
+ * d contiguous.  `batch` = B, `tokens` = T of this call.  Every vector must start on a 16-byte
+ * boundary (base pointers and strides x element size multiples of 16).                    */
+typedef struct {
+  int64_t batch, tokens;
+  int64_t stride_l, stride_b, stride_h, stride_t;
+} tvq_tensor_desc;
+
+/* Compressed cache layout (this project's; the paper only counts bits, section 3.1 "Rate
+ * accounting" and eq. (3)).  For each layer l and kind (0 = K, 1 = V) there are three planes:
+ *   plane 0  angle codes   P*ceil(log2 n)/8 bytes per vector (P = d/2 pairs)
+ *   plane 1  norm data     P*b/8 bytes (LINEAR/LOG codes) or 4P bytes (fp32 norms)
+ *   plane 2  header        8 bytes (fp32 r_min, r_max), absent (0 bytes) for fp32 norms
+ * Each plane holds B*H*capacity records indexed ((b*H + h)*capacity + t).  Planes follow each
+ * other in (layer, kind, plane) order with no padding.  Inside a record, code i occupies bits
+ * [i*w, (i+1)*w) of an LSB-first bitstream (bit j is bit j%8 of byte j/8).                */
+typedef struct {
+  int64_t total_bytes;
+  int64_t batch, capacity_tokens;
+  int64_t off[TVQ_MAX_LAYERS][2][3];        /* byte offset of each plane */
+  int32_t rec_bytes[TVQ_MAX_LAYERS][2][3];  /* bytes per vector in each plane */
+} tvq_layout;
+
+typedef struct tvq_codec tvq_codec;
+
+/* Create a codec: validates `cfg`, builds the sign table, the per-(layer, kind) parameters
+ * and the reconstruction cos/sin tables (section 3.1, "trigonometric lookup") and uploads
+ * them to the current HIP device.  *out receives the handle (NULL on error).
+ * Returns TVQ_ERR_INVALID_ARG (bad config), TVQ_ERR_UNSUPPORTED (d not 64/128),
+ * TVQ_ERR_ALLOC or TVQ_ERR_HIP. */
+tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out);
+
+/* Free a codec and its device tables (NULL is ignored).  Waits for nothing: the caller must
+ * not destroy a codec while its kernels may still run. */
+void tvq_destroy(tvq_codec* c);
+
+/* Fill *out with the layout of a cache for `batch` sequences of `capacity_tokens` slots.
+ * Host-only; the caller allocates out->total_bytes of device memory (any 16-byte aligned
+ * buffer) and passes the same layout to tvq_encode / tvq_decode. */
+tvq_status tvq_cache_layout(const tvq_codec* c, int64_t batch, int64_t capacity_tokens,
+                            tvq_layout* out);
+
+/* Encode (Algorithm 1 + section 3.3) K and V, each described by `in` with `in_dtype`
+ * elements, into cache slots [t_begin, t_begin + in->tokens) of every (layer, batch, head).
+ * Requires in->batch == lay->batch and t_begin + in->tokens <= lay->capacity_tokens.
+ * k, v: device pointers; cache: device pointer to lay->total_bytes bytes.
+ * Launches one kernel on `stream`; in->tokens == 0 launches nothing. */
+tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, const void* v,
+                      const tvq_tensor_desc* in, int64_t t_begin, void* cache,
+                      const tvq_layout* lay, void* stream);
+
+/* Decode (section 3.1, reconstruction) cache slots [t_begin, t_end) of every (layer, batch,
+ * head) into k_out / v_out, described by `out` (out->tokens == t_end - t_begin,
+ * out->batch == lay->batch), as `out_dtype` (bf16 rounded to nearest even, or fp32).
+ * Launches one kernel on `stream`; an empty range launches nothing. */
+tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* lay,
+                      int64_t t_begin, int64_t t_end, tvq_dtype out_dtype, void* k_out,
+                      void* v_out, const tvq_tensor_desc* out, void* stream);
+
+/* Bits per element of the codec, averaged over layers and over K and V.
+ * accounting 0: the paper's -- eq. (1) angle bits (log2 n)/2 (fractional for non-power-of-
+ *               two n) plus, per eq. (3), b_norm/2 + 64/d for quantized norms or 16 for
+ *               fp32 norms (section 3.1 "Rate accounting");
+ * accounting 1: actual storage of the layout above (ceil(log2 n) bits per angle code).
+ * Returns a negative value for a NULL codec or an unknown accounting. */
+double tvq_bits_per_element(const tvq_codec* c, int accounting);
+
+/* Static description of a status code. */
+const char* tvq_status_string(tvq_status s);
+
+/* ---- host-only helpers (no GPU needed) ---- */
+
+/* The sign row of `layer` drawn from `seed`: out[i] = +1 iff the top bit of
+ * SplitMix64 output i+1 of the stream keyed by mix(seed ^ (layer+1)*0xD1B54A32D192ED03)
+ * is 0 (mix = the SplitMix64 finalizer; stream output j = mix(key + j*0x9E3779B97F4A7C15)). */
+tvq_status tvq_make_signs(uint64_t seed, int32_t layer, int32_t head_dim, int8_t* out);
+
+/* The reconstruction lookup table of an n-bin codebook (section 3.1): cos_out[k], sin_out[k]
+ * = fp32 roundings of cos(2 pi k/n), sin(2 pi k/n), exact at multiples of pi/4. */
+tvq_status tvq_make_trig_table(int32_t n, float* cos_out, float* sin_out);
+
+/* Layout of a configuration without creating a codec (same result as tvq_cache_layout). */
+tvq_status tvq_layout_for_config(const tvq_config* cfg, int64_t batch, int64_t capacity_tokens,
+                                 tvq_layout* out);
+
+/* tvq_bits_per_element for a configuration without creating a codec.  Returns a negative
+ * value for an invalid configuration or accounting. */
+double tvq_bits_per_element_config(const tvq_config* cfg, int accounting);
+
+/* TVQ_ABI_VERSION of the built library. */
+int32_t tvq_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TVQ_H */

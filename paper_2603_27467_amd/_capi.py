@@ -1,0 +1,176 @@
+"""ctypes declarations of the C ABI in include/tvq.h (same names, same argument order)."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+TVQ_ABI_VERSION = 1
+TVQ_MAX_LAYERS = 256
+TVQ_OK, TVQ_ERR_INVALID_ARG, TVQ_ERR_UNSUPPORTED, TVQ_ERR_HIP, TVQ_ERR_ALLOC = 0, -1, -2, -3, -4
+TVQ_BF16, TVQ_F32 = 0, 1
+TVQ_NORM_F32, TVQ_NORM_LINEAR, TVQ_NORM_LOG = 0, 1, 2
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def library_path() -> str:
+    return os.path.join(_HERE, "libtvq.so")
+
+
+class TvqError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {tvq_status_string(status)} ({status})")
+
+
+class tvq_layer_cfg(ctypes.Structure):
+    _fields_ = [("n_k", ctypes.c_uint16), ("n_v", ctypes.c_uint16),
+                ("norm_bits_k", ctypes.c_uint8), ("norm_bits_v", ctypes.c_uint8),
+                ("norm_mode_k", ctypes.c_uint8), ("norm_mode_v", ctypes.c_uint8)]
+
+
+class tvq_config(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("shared_signs", ctypes.c_int32),
+                ("seed", ctypes.c_uint64), ("layers", ctypes.POINTER(tvq_layer_cfg)),
+                ("signs", ctypes.POINTER(ctypes.c_int8))]
+
+
+class tvq_tensor_desc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int64), ("tokens", ctypes.c_int64),
+                ("stride_l", ctypes.c_int64), ("stride_b", ctypes.c_int64),
+                ("stride_h", ctypes.c_int64), ("stride_t", ctypes.c_int64)]
+
+
+class tvq_layout(ctypes.Structure):
+    _fields_ = [("total_bytes", ctypes.c_int64), ("batch", ctypes.c_int64),
+                ("capacity_tokens", ctypes.c_int64),
+                ("off", ((ctypes.c_int64 * 3) * 2) * TVQ_MAX_LAYERS),
+                ("rec_bytes", ((ctypes.c_int32 * 3) * 2) * TVQ_MAX_LAYERS)]
+
+
+_lib = None
+
+
+def load_library():
+    """Load libtvq.so; raises if it has not been built (no fallback exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = library_path()
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2603_27467_amd.build`")
+    L = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    L.tvq_create.restype = ctypes.c_int
+    L.tvq_create.argtypes = [ctypes.POINTER(tvq_config), ctypes.POINTER(vp)]
+    L.tvq_destroy.restype = None
+    L.tvq_destroy.argtypes = [vp]
+    L.tvq_cache_layout.restype = ctypes.c_int
+    L.tvq_cache_layout.argtypes = [vp, i64, i64, ctypes.POINTER(tvq_layout)]
+    L.tvq_encode.restype = ctypes.c_int
+    L.tvq_encode.argtypes = [vp, ctypes.c_int, vp, vp, ctypes.POINTER(tvq_tensor_desc), i64, vp,
+                             ctypes.POINTER(tvq_layout), vp]
+    L.tvq_decode.restype = ctypes.c_int
+    L.tvq_decode.argtypes = [vp, vp, ctypes.POINTER(tvq_layout), i64, i64, ctypes.c_int, vp, vp,
+                             ctypes.POINTER(tvq_tensor_desc), vp]
+    L.tvq_bits_per_element.restype = ctypes.c_double
+    L.tvq_bits_per_element.argtypes = [vp, ctypes.c_int]
+    L.tvq_status_string.restype = ctypes.c_char_p
+    L.tvq_status_string.argtypes = [ctypes.c_int]
+    L.tvq_make_signs.restype = ctypes.c_int
+    L.tvq_make_signs.argtypes = [ctypes.c_uint64, i32, i32, vp]
+    L.tvq_make_trig_table.restype = ctypes.c_int
+    L.tvq_make_trig_table.argtypes = [i32, vp, vp]
+    L.tvq_layout_for_config.restype = ctypes.c_int
+    L.tvq_layout_for_config.argtypes = [ctypes.POINTER(tvq_config), i64, i64,
+                                        ctypes.POINTER(tvq_layout)]
+    L.tvq_bits_per_element_config.restype = ctypes.c_double
+    L.tvq_bits_per_element_config.argtypes = [ctypes.POINTER(tvq_config), ctypes.c_int]
+    L.tvq_abi_version.restype = i32
+    L.tvq_abi_version.argtypes = []
+    if L.tvq_abi_version() != TVQ_ABI_VERSION:
+        raise ImportError("libtvq.so ABI version mismatch; rebuild it")
+    _lib = L
+    return L
+
+
+def _check(status: int, what: str):
+    if status != TVQ_OK:
+        raise TvqError(status, what)
+
+
+def tvq_status_string(status: int) -> str:
+    return load_library().tvq_status_string(status).decode()
+
+
+def tvq_abi_version() -> int:
+    return int(load_library().tvq_abi_version())
+
+
+def tvq_create(cfg: tvq_config) -> int:
+    h = ctypes.c_void_p()
+    _check(load_library().tvq_create(ctypes.byref(cfg), ctypes.byref(h)), "tvq_create")
+    return int(h.value)
+
+
+def tvq_destroy(handle: int) -> None:
+    if handle:
+        load_library().tvq_destroy(ctypes.c_void_p(handle))
+
+
+def tvq_cache_layout(handle: int, batch: int, capacity_tokens: int) -> tvq_layout:
+    lay = tvq_layout()
+    _check(load_library().tvq_cache_layout(ctypes.c_void_p(handle), batch, capacity_tokens,
+                                           ctypes.byref(lay)), "tvq_cache_layout")
+    return lay
+
+
+def tvq_layout_for_config(cfg: tvq_config, batch: int, capacity_tokens: int) -> tvq_layout:
+    lay = tvq_layout()
+    _check(load_library().tvq_layout_for_config(ctypes.byref(cfg), batch, capacity_tokens,
+                                                ctypes.byref(lay)), "tvq_layout_for_config")
+    return lay
+
+
+def tvq_encode(handle: int, in_dtype: int, k_ptr: int, v_ptr: int, desc: tvq_tensor_desc,
+               t_begin: int, cache_ptr: int, lay: tvq_layout, stream: int = 0) -> None:
+    _check(load_library().tvq_encode(ctypes.c_void_p(handle), in_dtype, ctypes.c_void_p(k_ptr),
+                                     ctypes.c_void_p(v_ptr), ctypes.byref(desc), t_begin,
+                                     ctypes.c_void_p(cache_ptr), ctypes.byref(lay),
+                                     ctypes.c_void_p(stream)), "tvq_encode")
+
+
+def tvq_decode(handle: int, cache_ptr: int, lay: tvq_layout, t_begin: int, t_end: int,
+               out_dtype: int, k_ptr: int, v_ptr: int, desc: tvq_tensor_desc,
+               stream: int = 0) -> None:
+    _check(load_library().tvq_decode(ctypes.c_void_p(handle), ctypes.c_void_p(cache_ptr),
+                                     ctypes.byref(lay), t_begin, t_end, out_dtype,
+                                     ctypes.c_void_p(k_ptr), ctypes.c_void_p(v_ptr),
+                                     ctypes.byref(desc), ctypes.c_void_p(stream)), "tvq_decode")
+
+
+def tvq_bits_per_element(handle: int, accounting: int) -> float:
+    return float(load_library().tvq_bits_per_element(ctypes.c_void_p(handle), accounting))
+
+
+def tvq_bits_per_element_config(cfg: tvq_config, accounting: int) -> float:
+    return float(load_library().tvq_bits_per_element_config(ctypes.byref(cfg), accounting))
+
+
+def tvq_make_signs(seed: int, layer: int, head_dim: int) -> np.ndarray:
+    out = np.zeros(head_dim, np.int8)
+    _check(load_library().tvq_make_signs(seed & (2**64 - 1), layer, head_dim,
+                                         out.ctypes.data_as(ctypes.c_void_p)), "tvq_make_signs")
+    return out
+
+
+def tvq_make_trig_table(n: int):
+    c = np.zeros(n, np.float32)
+    s = np.zeros(n, np.float32)
+    _check(load_library().tvq_make_trig_table(n, c.ctypes.data_as(ctypes.c_void_p),
+                                              s.ctypes.data_as(ctypes.c_void_p)),
+           "tvq_make_trig_table")
+    return c, s

@@ -1,0 +1,469 @@
+// tvq_api.hip -- host side of libtvq: the C ABI declared in include/tvq.h.
+//
+// tvq_create validates the configuration and uploads three small device tables (segment
+// parameters, sign masks, cos/sin lookup); tvq_encode / tvq_decode validate their arguments
+// on the host and enqueue exactly one kernel each, with no allocation and no synchronization.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/tvq.h"
+#include "tvq_internal.h"
+
+struct tvq_codec {
+  int32_t L = 0, H = 0, d = 0;
+  std::vector<tvq_layer_cfg> layers;
+  std::vector<int8_t> signs;                 // [L][d]
+  std::vector<tvq::SegParams> segs;          // [2L]
+  uint64_t rec_total = 0;                    // record bytes of all planes, per slot
+  int device = 0;
+  tvq::SegParams* d_segs = nullptr;
+  uint32_t* d_sign_masks = nullptr;
+  float* d_lut = nullptr;
+};
+
+namespace {
+
+constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ULL;
+
+uint64_t splitmix64_finalize(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+int width_of(uint32_t n) {
+  int w = 0;
+  while ((1u << w) < n) ++w;
+  return w;
+}
+
+bool kind_valid(uint32_t n, uint32_t bits, uint32_t mode) {
+  if (n < 2 || n > 4096) return false;
+  if (mode == TVQ_NORM_F32) return true;
+  if (mode != TVQ_NORM_LINEAR && mode != TVQ_NORM_LOG) return false;
+  return bits >= 1 && bits <= 16;
+}
+
+tvq_status validate_config(const tvq_config* cfg) {
+  if (!cfg || !cfg->layers) return TVQ_ERR_INVALID_ARG;
+  if (cfg->num_layers < 1 || cfg->num_layers > TVQ_MAX_LAYERS) return TVQ_ERR_INVALID_ARG;
+  if (cfg->num_heads < 1 || cfg->num_heads > (1 << 20)) return TVQ_ERR_INVALID_ARG;
+  const int d = cfg->head_dim;
+  if (d < 2 || d > 4096 || (d & (d - 1))) return TVQ_ERR_INVALID_ARG;
+  for (int l = 0; l < cfg->num_layers; ++l) {
+    const tvq_layer_cfg& c = cfg->layers[l];
+    if (!kind_valid(c.n_k, c.norm_bits_k, c.norm_mode_k)) return TVQ_ERR_INVALID_ARG;
+    if (!kind_valid(c.n_v, c.norm_bits_v, c.norm_mode_v)) return TVQ_ERR_INVALID_ARG;
+  }
+  if (cfg->signs) {
+    const int rows = cfg->shared_signs ? 1 : cfg->num_layers;
+    for (int i = 0; i < rows * d; ++i)
+      if (cfg->signs[i] != 1 && cfg->signs[i] != -1) return TVQ_ERR_INVALID_ARG;
+  }
+  return TVQ_OK;
+}
+
+// record bytes (angle, norm, header) of one kind
+void kind_records(int d, uint32_t n, uint32_t bits, uint32_t mode, uint32_t rec[3]) {
+  const uint32_t P = (uint32_t)d / 2;
+  rec[0] = (P * (uint32_t)width_of(n) + 7) / 8;
+  if (mode == TVQ_NORM_F32) {
+    rec[1] = 4 * P;
+    rec[2] = 0;
+  } else {
+    rec[1] = (P * bits + 7) / 8;
+    rec[2] = 8;
+  }
+}
+
+void fill_layout(const tvq_config* cfg, int64_t batch, int64_t cap, tvq_layout* out) {
+  std::memset(out, 0, sizeof(*out));
+  out->batch = batch;
+  out->capacity_tokens = cap;
+  const int64_t slots = batch * cfg->num_heads * cap;
+  int64_t pos = 0;
+  for (int l = 0; l < cfg->num_layers; ++l) {
+    const tvq_layer_cfg& c = cfg->layers[l];
+    for (int kind = 0; kind < 2; ++kind) {
+      uint32_t rec[3];
+      if (kind == 0) kind_records(cfg->head_dim, c.n_k, c.norm_bits_k, c.norm_mode_k, rec);
+      else kind_records(cfg->head_dim, c.n_v, c.norm_bits_v, c.norm_mode_v, rec);
+      for (int p = 0; p < 3; ++p) {
+        out->off[l][kind][p] = pos;
+        out->rec_bytes[l][kind][p] = (int32_t)rec[p];
+        pos += slots * rec[p];
+      }
+    }
+  }
+  out->total_bytes = pos;
+}
+
+tvq::FastDiv make_div(uint32_t div) {
+  tvq::FastDiv f;
+  uint32_t l = 0;
+  while ((1ull << l) < div) ++l;
+  f.s = 32 + l;
+  f.m = (uint64_t)((((unsigned __int128)1 << f.s) + div - 1) / div);
+  f.div = div;
+  return f;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool layout_matches(const tvq_codec* c, const tvq_layout* lay) {
+  if (!lay || lay->batch < 1 || lay->capacity_tokens < 1) return false;
+  const int64_t slots = lay->batch * c->H * lay->capacity_tokens;
+  if (lay->total_bytes != slots * (int64_t)c->rec_total) return false;
+  for (int l = 0; l < c->L; ++l)
+    for (int kind = 0; kind < 2; ++kind)
+      for (int p = 0; p < 3; ++p) {
+        const tvq::SegParams& s = c->segs[2 * l + kind];
+        if (lay->off[l][kind][p] != slots * (int64_t)s.pre[p]) return false;
+        if (lay->rec_bytes[l][kind][p] != (int32_t)s.rec[p]) return false;
+      }
+  return true;
+}
+
+// strided view [L][B][H][T][d]: every vector start 16-byte aligned and all addressed
+// elements inside int64 range
+bool desc_valid(const tvq_codec* c, const tvq_tensor_desc* t, int elem_bytes) {
+  if (!t || t->batch < 1 || t->tokens < 0) return false;
+  if (t->stride_l < 0 || t->stride_b < 0 || t->stride_h < 0 || t->stride_t < 0) return false;
+  const int64_t strides[4] = {t->stride_l, t->stride_b, t->stride_h, t->stride_t};
+  for (int64_t s : strides)
+    if ((s * elem_bytes) % 16 != 0) return false;
+  if (t->tokens > 1 && t->stride_t < c->d) return false;
+  const int64_t vec = t->batch * c->H * t->tokens;
+  if (vec >= (1ll << 31)) return false;
+  return true;
+}
+
+unsigned plan_grid(uint32_t nvec, uint32_t vpw, uint32_t num_segs, uint32_t* waves_per_seg,
+                   uint32_t* tiles_per_wave) {
+  const uint64_t tiles_per_seg = (nvec + vpw - 1) / vpw;
+  const uint64_t total_tiles = tiles_per_seg * num_segs;
+  // aim for at least ~32 waves per compute unit of a 256-CU part before grouping tiles
+  uint64_t tpw = total_tiles / (256ull * 32ull);
+  if (tpw < 1) tpw = 1;
+  if (tpw > 8) tpw = 8;
+  const uint64_t wps = (tiles_per_seg + tpw - 1) / tpw;
+  *waves_per_seg = (uint32_t)wps;
+  *tiles_per_wave = (uint32_t)tpw;
+  const uint64_t waves = wps * num_segs;
+  return (unsigned)((waves + tvq::kWavesPerBlock - 1) / tvq::kWavesPerBlock);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tvq_status_string(tvq_status s) {
+  switch (s) {
+    case TVQ_OK: return "ok";
+    case TVQ_ERR_INVALID_ARG: return "invalid argument";
+    case TVQ_ERR_UNSUPPORTED: return "unsupported configuration";
+    case TVQ_ERR_HIP: return "HIP runtime error";
+    case TVQ_ERR_ALLOC: return "device allocation failed";
+  }
+  return "unknown status";
+}
+
+int32_t tvq_abi_version(void) { return TVQ_ABI_VERSION; }
+
+tvq_status tvq_make_signs(uint64_t seed, int32_t layer, int32_t head_dim, int8_t* out) {
+  if (!out || layer < 0 || head_dim < 1) return TVQ_ERR_INVALID_ARG;
+  const uint64_t key = splitmix64_finalize(seed ^ ((uint64_t)(layer + 1) * 0xD1B54A32D192ED03ULL));
+  for (int32_t i = 0; i < head_dim; ++i) {
+    const uint64_t word = splitmix64_finalize(key + (uint64_t)(i + 1) * kGamma);
+    out[i] = (word >> 63) ? (int8_t)-1 : (int8_t)1;
+  }
+  return TVQ_OK;
+}
+
+tvq_status tvq_make_trig_table(int32_t n, float* cos_out, float* sin_out) {
+  if (n < 2 || n > 4096 || !cos_out || !sin_out) return TVQ_ERR_INVALID_ARG;
+  const double half_pi = 1.5707963267948966;  // fp64 rounding of pi/2
+  for (int32_t k = 0; k < n; ++k) {
+    // 2 pi k / n = (quarter turns) * pi/2 + (pi/2) * rem/n with 4k = quarter*n + rem
+    const int64_t m = 4ll * k;
+    const int64_t quarter = m / n;
+    const int64_t rem = m % n;
+    double c, s;
+    if (rem == 0) {
+      c = 1.0;
+      s = 0.0;
+    } else if (2 * rem == n) {
+      c = std::sqrt(0.5);
+      s = c;
+    } else if (2 * rem < n) {
+      const double ang = half_pi * ((double)rem / (double)n);
+      c = std::cos(ang);
+      s = std::sin(ang);
+    } else {
+      const double ang = half_pi * ((double)(n - rem) / (double)n);
+      c = std::sin(ang);
+      s = std::cos(ang);
+    }
+    double cr = c, sr = s;
+    switch (quarter & 3) {
+      case 1: cr = -s; sr = c; break;
+      case 2: cr = -c; sr = -s; break;
+      case 3: cr = s; sr = -c; break;
+      default: break;
+    }
+    cos_out[k] = (float)cr;
+    sin_out[k] = (float)sr;
+  }
+  return TVQ_OK;
+}
+
+tvq_status tvq_layout_for_config(const tvq_config* cfg, int64_t batch, int64_t capacity_tokens,
+                                 tvq_layout* out) {
+  const tvq_status st = validate_config(cfg);
+  if (st != TVQ_OK) return st;
+  if (!out || batch < 1 || capacity_tokens < 1) return TVQ_ERR_INVALID_ARG;
+  if (batch * cfg->num_heads * capacity_tokens >= (1ll << 31)) return TVQ_ERR_INVALID_ARG;
+  fill_layout(cfg, batch, capacity_tokens, out);
+  return TVQ_OK;
+}
+
+tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out) {
+  if (!out) return TVQ_ERR_INVALID_ARG;
+  *out = nullptr;
+  tvq_status st = validate_config(cfg);
+  if (st != TVQ_OK) return st;
+  if (cfg->head_dim != 64 && cfg->head_dim != 128) return TVQ_ERR_UNSUPPORTED;
+
+  tvq_codec* c = new (std::nothrow) tvq_codec();
+  if (!c) return TVQ_ERR_ALLOC;
+  c->L = cfg->num_layers;
+  c->H = cfg->num_heads;
+  c->d = cfg->head_dim;
+  c->layers.assign(cfg->layers, cfg->layers + c->L);
+  const int d = c->d;
+
+  // sign diagonal D, one row per layer
+  c->signs.resize((size_t)c->L * d);
+  for (int l = 0; l < c->L; ++l) {
+    int8_t* row = c->signs.data() + (size_t)l * d;
+    if (cfg->signs) {
+      const int8_t* srcrow = cfg->signs + (cfg->shared_signs ? 0 : (size_t)l * d);
+      std::memcpy(row, srcrow, d);
+    } else {
+      tvq_make_signs(cfg->seed, cfg->shared_signs ? 0 : l, d, row);
+    }
+  }
+
+  // XOR masks per bf16 word (element pair 2m, 2m+1)
+  std::vector<uint32_t> masks((size_t)c->L * (d / 2));
+  for (int l = 0; l < c->L; ++l)
+    for (int m = 0; m < d / 2; ++m) {
+      const int8_t* row = c->signs.data() + (size_t)l * d;
+      masks[(size_t)l * (d / 2) + m] =
+          (row[2 * m] < 0 ? 0x00008000u : 0u) | (row[2 * m + 1] < 0 ? 0x80000000u : 0u);
+    }
+
+  // per-segment parameters and the concatenated cos/sin table
+  std::vector<float> lut;
+  c->segs.resize((size_t)2 * c->L);
+  uint64_t prefix = 0;
+  for (int l = 0; l < c->L; ++l)
+    for (int kind = 0; kind < 2; ++kind) {
+      const tvq_layer_cfg& lc = c->layers[l];
+      const uint32_t n = kind ? lc.n_v : lc.n_k;
+      const uint32_t mode = kind ? lc.norm_mode_v : lc.norm_mode_k;
+      const uint32_t bits = mode == TVQ_NORM_F32 ? 32u : (kind ? lc.norm_bits_v : lc.norm_bits_k);
+      tvq::SegParams& s = c->segs[2 * l + kind];
+      std::memset(&s, 0, sizeof(s));
+      s.nf = (float)n;
+      s.n = n;
+      s.mask = (n & (n - 1)) == 0 ? n - 1 : 0u;
+      s.w = (uint32_t)width_of(n);
+      s.mode = mode;
+      s.bits = bits;
+      kind_records(d, n, bits, mode, s.rec);
+      s.layer = (uint32_t)l;
+      s.kind = (uint32_t)kind;
+      s.lut_off = (uint32_t)(lut.size() / 2);
+      for (int p = 0; p < 3; ++p) {
+        s.pre[p] = prefix;
+        prefix += s.rec[p];
+      }
+      std::vector<float> cs(n), sn(n);
+      tvq_make_trig_table((int32_t)n, cs.data(), sn.data());
+      for (uint32_t k = 0; k < n; ++k) {
+        lut.push_back(cs[k]);
+        lut.push_back(sn[k]);
+      }
+    }
+  c->rec_total = prefix;
+
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return TVQ_ERR_HIP;
+  }
+  const size_t seg_bytes = c->segs.size() * sizeof(tvq::SegParams);
+  const size_t mask_bytes = masks.size() * sizeof(uint32_t);
+  const size_t lut_bytes = lut.size() * sizeof(float);
+  if (hipMalloc((void**)&c->d_segs, seg_bytes) != hipSuccess ||
+      hipMalloc((void**)&c->d_sign_masks, mask_bytes) != hipSuccess ||
+      hipMalloc((void**)&c->d_lut, lut_bytes) != hipSuccess) {
+    tvq_destroy(c);
+    return TVQ_ERR_ALLOC;
+  }
+  if (hipMemcpy(c->d_segs, c->segs.data(), seg_bytes, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(c->d_sign_masks, masks.data(), mask_bytes, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(c->d_lut, lut.data(), lut_bytes, hipMemcpyHostToDevice) != hipSuccess) {
+    tvq_destroy(c);
+    return TVQ_ERR_HIP;
+  }
+  *out = c;
+  return TVQ_OK;
+}
+
+void tvq_destroy(tvq_codec* c) {
+  if (!c) return;
+  if (c->d_segs) (void)hipFree(c->d_segs);
+  if (c->d_sign_masks) (void)hipFree(c->d_sign_masks);
+  if (c->d_lut) (void)hipFree(c->d_lut);
+  delete c;
+}
+
+tvq_status tvq_cache_layout(const tvq_codec* c, int64_t batch, int64_t capacity_tokens,
+                            tvq_layout* out) {
+  if (!c || !out || batch < 1 || capacity_tokens < 1) return TVQ_ERR_INVALID_ARG;
+  if (batch * c->H * capacity_tokens >= (1ll << 31)) return TVQ_ERR_INVALID_ARG;
+  tvq_config cfg;
+  std::memset(&cfg, 0, sizeof(cfg));
+  cfg.num_layers = c->L;
+  cfg.num_heads = c->H;
+  cfg.head_dim = c->d;
+  cfg.layers = c->layers.data();
+  fill_layout(&cfg, batch, capacity_tokens, out);
+  return TVQ_OK;
+}
+
+tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, const void* v,
+                      const tvq_tensor_desc* in, int64_t t_begin, void* cache,
+                      const tvq_layout* lay, void* stream) {
+  if (!c || !in || !lay) return TVQ_ERR_INVALID_ARG;
+  if (in_dtype != TVQ_BF16 && in_dtype != TVQ_F32) return TVQ_ERR_INVALID_ARG;
+  const int eb = in_dtype == TVQ_F32 ? 4 : 2;
+  if (!desc_valid(c, in, eb) || !layout_matches(c, lay)) return TVQ_ERR_INVALID_ARG;
+  if (in->batch != lay->batch) return TVQ_ERR_INVALID_ARG;
+  if (t_begin < 0 || t_begin + in->tokens > lay->capacity_tokens) return TVQ_ERR_INVALID_ARG;
+  if (in->tokens == 0) return TVQ_OK;
+  if (!k || !v || !cache || !aligned16(k) || !aligned16(v) || !aligned16(cache))
+    return TVQ_ERR_INVALID_ARG;
+
+  tvq::EncodeArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.k = k;
+  a.v = v;
+  a.stride_l = in->stride_l;
+  a.stride_b = in->stride_b;
+  a.stride_h = in->stride_h;
+  a.stride_t = in->stride_t;
+  a.cache = (uint8_t*)cache;
+  a.n_slots = lay->batch * c->H * lay->capacity_tokens;
+  a.cap = lay->capacity_tokens;
+  a.t_begin = t_begin;
+  a.segs = c->d_segs;
+  a.sign_masks = c->d_sign_masks;
+  a.div_t = make_div((uint32_t)in->tokens);
+  a.div_h = make_div((uint32_t)c->H);
+  a.H = (uint32_t)c->H;
+  a.nvec = (uint32_t)(in->batch * c->H * in->tokens);
+  a.num_segs = (uint32_t)(2 * c->L);
+  a.inv_d = 1.0f / (float)c->d;
+  const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
+  const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave);
+  const int rc = tvq_launch_encode(a, c->d, in_dtype == TVQ_F32, grid, stream);
+  if (rc == -1) return TVQ_ERR_UNSUPPORTED;
+  return rc == 0 ? TVQ_OK : TVQ_ERR_HIP;
+}
+
+tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* lay,
+                      int64_t t_begin, int64_t t_end, tvq_dtype out_dtype, void* k_out,
+                      void* v_out, const tvq_tensor_desc* out, void* stream) {
+  if (!c || !lay || !out) return TVQ_ERR_INVALID_ARG;
+  if (out_dtype != TVQ_BF16 && out_dtype != TVQ_F32) return TVQ_ERR_INVALID_ARG;
+  const int eb = out_dtype == TVQ_F32 ? 4 : 2;
+  if (!desc_valid(c, out, eb) || !layout_matches(c, lay)) return TVQ_ERR_INVALID_ARG;
+  if (out->batch != lay->batch) return TVQ_ERR_INVALID_ARG;
+  if (t_begin < 0 || t_end < t_begin || t_end > lay->capacity_tokens) return TVQ_ERR_INVALID_ARG;
+  if (out->tokens != t_end - t_begin) return TVQ_ERR_INVALID_ARG;
+  if (out->tokens == 0) return TVQ_OK;
+  if (!k_out || !v_out || !cache || !aligned16(k_out) || !aligned16(v_out) || !aligned16(cache))
+    return TVQ_ERR_INVALID_ARG;
+
+  tvq::DecodeArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.cache = (const uint8_t*)cache;
+  a.k_out = k_out;
+  a.v_out = v_out;
+  a.stride_l = out->stride_l;
+  a.stride_b = out->stride_b;
+  a.stride_h = out->stride_h;
+  a.stride_t = out->stride_t;
+  a.n_slots = lay->batch * c->H * lay->capacity_tokens;
+  a.cap = lay->capacity_tokens;
+  a.t_begin = t_begin;
+  a.segs = c->d_segs;
+  a.sign_masks = c->d_sign_masks;
+  a.lut = c->d_lut;
+  a.div_t = make_div((uint32_t)out->tokens);
+  a.div_h = make_div((uint32_t)c->H);
+  a.H = (uint32_t)c->H;
+  a.nvec = (uint32_t)(out->batch * c->H * out->tokens);
+  a.num_segs = (uint32_t)(2 * c->L);
+  a.c_d = (float)(1.0 / std::sqrt((double)c->d));
+  const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
+  const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave);
+  const int rc = tvq_launch_decode(a, c->d, out_dtype == TVQ_F32, grid, stream);
+  if (rc == -1) return TVQ_ERR_UNSUPPORTED;
+  return rc == 0 ? TVQ_OK : TVQ_ERR_HIP;
+}
+
+double tvq_bits_per_element_config(const tvq_config* cfg, int accounting) {
+  if (validate_config(cfg) != TVQ_OK || (accounting != 0 && accounting != 1)) return -1.0;
+  const int d = cfg->head_dim;
+  double total = 0.0;
+  for (int l = 0; l < cfg->num_layers; ++l)
+    for (int kind = 0; kind < 2; ++kind) {
+      const tvq_layer_cfg& lc = cfg->layers[l];
+      const uint32_t n = kind ? lc.n_v : lc.n_k;
+      const uint32_t mode = kind ? lc.norm_mode_v : lc.norm_mode_k;
+      const uint32_t bits = kind ? lc.norm_bits_v : lc.norm_bits_k;
+      double b;
+      if (accounting == 0) {
+        b = std::log2((double)n) / 2.0;                             // eq. (1) term
+        if (mode == TVQ_NORM_F32) b += 16.0;                        // fp32 norms
+        else b += (double)bits / 2.0 + 64.0 / (double)d;            // eq. (3)
+      } else {
+        uint32_t rec[3];
+        kind_records(d, n, bits, mode, rec);
+        b = 8.0 * (double)(rec[0] + rec[1] + rec[2]) / (double)d;
+      }
+      total += b;
+    }
+  return total / (2.0 * cfg->num_layers);
+}
+
+double tvq_bits_per_element(const tvq_codec* c, int accounting) {
+  if (!c) return -1.0;
+  tvq_config cfg;
+  std::memset(&cfg, 0, sizeof(cfg));
+  cfg.num_layers = c->L;
+  cfg.num_heads = c->H;
+  cfg.head_dim = c->d;
+  cfg.layers = c->layers.data();
+  return tvq_bits_per_element_config(&cfg, accounting);
+}
+
+}  // extern "C"

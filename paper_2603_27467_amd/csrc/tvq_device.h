@@ -1,0 +1,182 @@
+// tvq_device.h -- device helpers shared by the encode and decode kernels (gfx950).
+//
+// Thread mapping used by both kernels: a vector of d elements is owned by d/32 consecutive
+// lanes of a wavefront, lane `sub` holding elements [32*sub, 32*sub + 32), i.e. pairs
+// [16*sub, 16*sub + 16).  d = 128 puts one vector on each lane quad (16 vectors per wave),
+// d = 64 one on each lane pair (32 per wave).  Butterfly stages h = 1..16 of the Walsh-
+// Hadamard transform are in-lane; h = 32 and h = 64 pair lanes sub ^ 1 and sub ^ 2, which a
+// DPP quad permutation reaches without LDS.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tvq_internal.h"
+
+namespace tvq {
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2), aligned(4)));
+typedef uint32_t u32x3 __attribute__((ext_vector_type(3), aligned(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4), aligned(4)));
+
+__device__ __forceinline__ uint32_t fast_div(uint32_t x, const FastDiv& d) {
+  return (uint32_t)(((uint64_t)x * d.m) >> d.s);
+}
+
+// DPP quad permutations: 0xB1 = [1,0,3,2] (lane ^ 1), 0x4E = [2,3,0,1] (lane ^ 2).
+template <int CTRL>
+__device__ __forceinline__ float quad_perm(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t quad_perm_u(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+// In-lane butterfly stages h = 1, 2, 4, 8, 16 over the lane's 32 elements.  Each stage maps
+// (z_j, z_j+h) to (z_j + z_j+h, z_j - z_j+h), every result rounded once (no contraction).
+__device__ __forceinline__ void fwht_in_lane(float (&x)[kElemsPerLane]) {
+#pragma unroll
+  for (int h = 1; h < kElemsPerLane; h <<= 1) {
+#pragma unroll
+    for (int j = 0; j < kElemsPerLane; ++j) {
+      if ((j & h) == 0) {
+        const float a = x[j];
+        const float b = x[j + h];
+        x[j] = a + b;
+        x[j + h] = a - b;
+      }
+    }
+  }
+}
+
+// Cross-lane stages h = 32 (lanes sub, sub^1) and h = 64 (lanes sub, sub^2).  The lane that
+// holds z_j computes z_j + partner, the lane that holds z_j+h computes partner - z_j+h; both
+// are one correctly rounded fma with a +-1 multiplier, identical to the plain add/sub.
+template <int LPV>
+__device__ __forceinline__ void fwht_cross_lane(float (&x)[kElemsPerLane], int sub) {
+  if constexpr (LPV >= 2) {
+    const float c = (sub & 1) ? -1.0f : 1.0f;
+#pragma unroll
+    for (int j = 0; j < kElemsPerLane; ++j) x[j] = __builtin_fmaf(c, x[j], quad_perm<0xB1>(x[j]));
+  }
+  if constexpr (LPV >= 4) {
+    const float c = (sub & 2) ? -1.0f : 1.0f;
+#pragma unroll
+    for (int j = 0; j < kElemsPerLane; ++j) x[j] = __builtin_fmaf(c, x[j], quad_perm<0x4E>(x[j]));
+  }
+  static_assert(LPV == 1 || LPV == 2 || LPV == 4, "d must be 32, 64 or 128");
+}
+
+template <int LPV>
+__device__ __forceinline__ float vec_min(float v) {
+  if constexpr (LPV >= 2) v = fminf(v, quad_perm<0xB1>(v));
+  if constexpr (LPV >= 4) v = fminf(v, quad_perm<0x4E>(v));
+  return v;
+}
+
+template <int LPV>
+__device__ __forceinline__ float vec_max(float v) {
+  if constexpr (LPV >= 2) v = fmaxf(v, quad_perm<0xB1>(v));
+  if constexpr (LPV >= 4) v = fmaxf(v, quad_perm<0x4E>(v));
+  return v;
+}
+
+// ---- bit packing: 16 codes of W bits -> LSB-first bitstream of 2W bytes -------------------
+template <int W>
+struct Chunk {
+  static constexpr int kWords = (16 * W + 31) / 32;
+  uint32_t w[kWords];
+};
+
+template <int W>
+__device__ __forceinline__ Chunk<W> pack16(const uint32_t (&c)[kPairsPerLane]) {
+  Chunk<W> o;
+#pragma unroll
+  for (int i = 0; i < Chunk<W>::kWords; ++i) o.w[i] = 0u;
+  constexpr uint32_t m = (W == 32) ? 0xFFFFFFFFu : ((1u << W) - 1u);
+#pragma unroll
+  for (int i = 0; i < kPairsPerLane; ++i) {
+    const uint32_t v = c[i] & m;
+    const int bit = i * W;
+    const int wd = bit >> 5;
+    const int sh = bit & 31;
+    o.w[wd] |= v << sh;
+    if (sh + W > 32) o.w[wd + 1] |= v >> (32 - sh);
+  }
+  return o;
+}
+
+template <int W>
+__device__ __forceinline__ void unpack16(const Chunk<W>& o, uint32_t (&c)[kPairsPerLane]) {
+  constexpr uint32_t m = (W == 32) ? 0xFFFFFFFFu : ((1u << W) - 1u);
+#pragma unroll
+  for (int i = 0; i < kPairsPerLane; ++i) {
+    const int bit = i * W;
+    const int wd = bit >> 5;
+    const int sh = bit & 31;
+    uint32_t v = o.w[wd] >> sh;
+    if (sh + W > 32) v |= o.w[wd + 1] << (32 - sh);
+    c[i] = v & m;
+  }
+}
+
+template <int N>
+__device__ __forceinline__ void store_words(uint32_t* p, const uint32_t* v) {
+  int i = 0;
+#pragma unroll
+  for (; i + 4 <= N; i += 4) *(u32x4*)(p + i) = u32x4{v[i], v[i + 1], v[i + 2], v[i + 3]};
+  if constexpr (N % 4 == 3) *(u32x3*)(p + i) = u32x3{v[i], v[i + 1], v[i + 2]};
+  if constexpr (N % 4 == 2) *(u32x2*)(p + i) = u32x2{v[i], v[i + 1]};
+  if constexpr (N % 4 == 1) p[i] = v[i];
+}
+
+template <int N>
+__device__ __forceinline__ void load_words(const uint32_t* p, uint32_t* v) {
+  int i = 0;
+#pragma unroll
+  for (; i + 4 <= N; i += 4) {
+    const u32x4 t = *(const u32x4*)(p + i);
+    v[i] = t.x; v[i + 1] = t.y; v[i + 2] = t.z; v[i + 3] = t.w;
+  }
+  if constexpr (N % 4 == 3) {
+    const u32x3 t = *(const u32x3*)(p + i);
+    v[i] = t.x; v[i + 1] = t.y; v[i + 2] = t.z;
+  }
+  if constexpr (N % 4 == 2) {
+    const u32x2 t = *(const u32x2*)(p + i);
+    v[i] = t.x; v[i + 1] = t.y;
+  }
+  if constexpr (N % 4 == 1) v[i] = p[i];
+}
+
+// A lane's chunk is 2W bytes at byte offset 2W*sub of its record: 4-byte aligned for even W
+// (stored as dwords), 2-byte aligned for odd W (stored as 16-bit halves).
+template <int W>
+__device__ __forceinline__ void store_chunk(uint8_t* p, const Chunk<W>& o) {
+  if constexpr (W % 2 == 0) {
+    store_words<W / 2>((uint32_t*)p, o.w);
+  } else {
+    uint16_t* q = (uint16_t*)p;
+#pragma unroll
+    for (int i = 0; i < W; ++i) q[i] = (uint16_t)(o.w[i >> 1] >> (16 * (i & 1)));
+  }
+}
+
+template <int W>
+__device__ __forceinline__ Chunk<W> load_chunk(const uint8_t* p) {
+  Chunk<W> o;
+  if constexpr (W % 2 == 0) {
+    load_words<W / 2>((const uint32_t*)p, o.w);
+  } else {
+#pragma unroll
+    for (int i = 0; i < Chunk<W>::kWords; ++i) o.w[i] = 0u;
+    const uint16_t* q = (const uint16_t*)p;
+#pragma unroll
+    for (int i = 0; i < W; ++i) o.w[i >> 1] |= (uint32_t)q[i] << (16 * (i & 1));
+  }
+  return o;
+}
+
+}  // namespace tvq

@@ -1,0 +1,88 @@
+// tvq_internal.h -- structures shared by the host side of libtvq and its gfx950 kernels.
+//
+// Data layout of the device tables built by tvq_create:
+//   SegParams  [2L]        one per (layer, kind), index 2*layer + kind (0 = K, 1 = V)
+//   sign masks [L][d/2]    u32 XOR masks of the sign diagonal D for element pairs (2m, 2m+1)
+//                          of a bf16 word: bit 15 flips element 2m, bit 31 flips element 2m+1
+//   trig LUT   sum_s n_s   float2 (cos, sin)(2 pi k / n) per codebook, segment s at lut_off
+#pragma once
+
+#include <stdint.h>
+
+namespace tvq {
+
+constexpr int kWave = 64;            // CDNA wavefront width
+constexpr int kElemsPerLane = 32;    // each lane owns 32 consecutive elements of a vector
+constexpr int kPairsPerLane = 16;
+constexpr int kBlockThreads = 256;   // 4 waves per workgroup
+constexpr int kWavesPerBlock = kBlockThreads / kWave;
+
+// Per-(layer, kind) parameters.  Plane p of a segment starts at n_slots * pre[p] bytes,
+// where n_slots = B * H * capacity: the layout puts planes back to back, so the prefix of
+// record bytes over all earlier planes scales to the byte offset for any (B, capacity).
+struct SegParams {
+  float nf;            // n as float
+  uint32_t n;          // angle bins
+  uint32_t mask;       // n - 1 when n is a power of two, else 0
+  uint32_t w;          // angle code width ceil(log2 n)
+  uint32_t mode;       // tvq_norm_mode
+  uint32_t bits;       // norm code width (32 for fp32 norms)
+  uint32_t rec[3];     // bytes per vector of the angle, norm and header planes
+  uint32_t layer;
+  uint32_t kind;
+  uint32_t lut_off;    // first entry of this codebook in the trig LUT
+  uint64_t pre[3];     // record-byte prefix of the three planes
+};
+
+// Unsigned division by a runtime constant for numerators below 2^31:
+// q = (x * m) >> s with m = ceil(2^s / div), s = 32 + ceil(log2 div).
+struct FastDiv {
+  uint64_t m;
+  uint32_t s;
+  uint32_t div;
+};
+
+struct EncodeArgs {
+  const void* k;
+  const void* v;
+  int64_t stride_l, stride_b, stride_h, stride_t;  // elements
+  uint8_t* cache;
+  int64_t n_slots;      // B * H * capacity
+  int64_t cap;          // capacity tokens
+  int64_t t_begin;
+  const SegParams* segs;
+  const uint32_t* sign_masks;
+  FastDiv div_t, div_h;  // by T (tokens in the call) and by H
+  uint32_t H;
+  uint32_t nvec;         // B * H * T vectors per segment
+  uint32_t waves_per_seg;
+  uint32_t tiles_per_wave;
+  uint32_t num_segs;
+  float inv_d;           // 1/d (exact)
+};
+
+struct DecodeArgs {
+  const uint8_t* cache;
+  void* k_out;
+  void* v_out;
+  int64_t stride_l, stride_b, stride_h, stride_t;  // elements of the output view
+  int64_t n_slots;
+  int64_t cap;
+  int64_t t_begin;
+  const SegParams* segs;
+  const uint32_t* sign_masks;
+  const float* lut;      // float2 entries
+  FastDiv div_t, div_h;
+  uint32_t H;
+  uint32_t nvec;
+  uint32_t waves_per_seg;
+  uint32_t tiles_per_wave;
+  uint32_t num_segs;
+  float c_d;             // fp32 rounding of 1/sqrt(d)
+};
+
+}  // namespace tvq
+
+// Kernel launchers (defined in the .hip kernel files).
+int tvq_launch_encode(const tvq::EncodeArgs& a, int d, int in_f32, unsigned grid, void* stream);
+int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, unsigned grid, void* stream);

@@ -1,0 +1,205 @@
+"""Host-side checks of the C ABI library (no GPU): it loads, exports everything include/tvq.h
+declares, and its host-only helpers agree with the independently written oracle."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def tvq():
+    import paper_2603_27467_amd as tvq
+    tvq.load_library()
+    return tvq
+
+
+def _declared_symbols():
+    src = open(os.path.join(ROOT, "include", "tvq.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tvq_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol(tvq):
+    syms = _declared_symbols()
+    assert {"tvq_create", "tvq_destroy", "tvq_cache_layout", "tvq_encode", "tvq_decode",
+            "tvq_bits_per_element", "tvq_status_string"} <= set(syms)
+    lib = ctypes.CDLL(tvq.library_path())
+    missing = [s for s in syms if not hasattr(lib, s)]
+    assert not missing, missing
+    assert tvq.tvq_abi_version() == 1
+
+
+def test_status_strings(tvq):
+    assert tvq.tvq_status_string(0) == "ok"
+    assert "invalid" in tvq.tvq_status_string(-1)
+    assert tvq.tvq_status_string(-99) == "unknown status"
+
+
+@pytest.mark.parametrize("seed", [0, 1, 102, 2**63 + 5])
+def test_signs_agree_with_oracle(tvq, orc, seed):
+    """Both sides implement SplitMix64 from its published definition; they must agree."""
+    for layer in (0, 1, 31):
+        for d in (64, 128):
+            assert np.array_equal(tvq.tvq_make_signs(seed, layer, d), orc.signs(seed, layer, d))
+
+
+def test_trig_table_agrees_with_oracle(tvq, orc):
+    """The reconstruction lookup (section 3.1) of every codebook size 2..4096, bit for bit."""
+    for n in range(2, 4097):
+        c1, s1 = tvq.tvq_make_trig_table(n)
+        c2, s2 = orc.trig_table(n)
+        assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32)), n
+        assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32)), n
+
+
+def _cfg(tvq, table, L, H, d, seed=0, shared=0, signs=None):
+    arr = (tvq.tvq_layer_cfg * max(len(table), 1))()
+    for i, t in enumerate(table):
+        arr[i] = tvq.tvq_layer_cfg(*t)
+    sp = None
+    if signs is not None:
+        signs = np.ascontiguousarray(signs, np.int8)
+        sp = signs.ctypes.data_as(ctypes.POINTER(ctypes.c_int8))
+    cfg = tvq.tvq_config(L, H, d, shared, seed, arr, sp)
+    cfg._keep = (arr, signs)
+    return cfg
+
+
+def _random_table(rng, L):
+    out = []
+    for _ in range(L):
+        row = []
+        for _kind in range(2):
+            n = int(rng.choice([2, 3, 8, 32, 48, 56, 64, 100, 128, 256, 4096]))
+            mode = int(rng.integers(0, 3))
+            bits = 32 if mode == 0 else int(rng.integers(1, 17))
+            row.append((n, bits, mode))
+        (nk, bk, mk), (nv, bv, mv) = row
+        out.append((nk, nv, bk, bv, mk, mv))
+    return out
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_layout_agrees_with_oracle(tvq, orc, seed):
+    rng = np.random.default_rng(seed)
+    L = int(rng.integers(1, 9))
+    H = int(rng.integers(1, 9))
+    d = int(rng.choice([64, 128]))
+    B = int(rng.integers(1, 4))
+    T = int(rng.integers(1, 300))
+    table = _random_table(rng, L)
+    lay = tvq.tvq_layout_for_config(_cfg(tvq, table, L, H, d), B, T)
+    kinds = []
+    for (nk, nv, bk, bv, mk, mv) in table:
+        kinds += [orc.Kind(nk, mk, bk), orc.Kind(nv, mv, bv)]
+    oc = orc.Codec(L, H, d, kinds, np.ones((L, d), np.int8))
+    total, off = oc.layout(B, T)
+    assert lay.total_bytes == total
+    assert lay.batch == B and lay.capacity_tokens == T
+    for l in range(L):
+        for k in range(2):
+            assert list(lay.off[l][k]) == list(off[l, k])
+            assert list(lay.rec_bytes[l][k]) == oc.record_bytes(l, k)
+
+
+def _expand(spec):
+    out = []
+    for g in spec.split():
+        v, c = g.split("x")
+        out += [int(v)] * int(c)
+    return out
+
+
+def test_bits_per_element_matches_paper_rates(tvq):
+    """tvq_bits_per_element_config, accounting 0, against the rates printed in the paper."""
+    rows = []
+    for line in open(os.path.join(ROOT, "tests", "golden", "paper_rates.txt")):
+        if line.strip() and not line.startswith("#"):
+            rows.append([x.strip() for x in line.split("|")])
+    checked = 0
+    for label, nk, nv, bk, bv, d, printed, what in rows:
+        nk, nv = _expand(nk), _expand(nv)
+        L, bk, bv, d, printed = len(nk), int(bk), int(bv), int(d), float(printed)
+        if what == "angle":
+            # angle-only rates: fp32 norms add exactly 16 bits (section 3.1 "Rate accounting")
+            table = [(a, b, 32, 32, 0, 0) for a, b in zip(nk, nv)]
+            got = tvq.tvq_bits_per_element_config(_cfg(tvq, table, L, 8, d), 0) - 16.0
+        elif what == "total":
+            table = [(a, b, bk, bv, 1, 2) for a, b in zip(nk, nv)]
+            got = tvq.tvq_bits_per_element_config(_cfg(tvq, table, L, 8, d), 0)
+        else:
+            continue
+        assert abs(got - printed) <= 0.005 + 1e-9, (label, got, printed)
+        checked += 1
+    assert checked >= 20
+
+
+def test_bits_per_element_storage(tvq):
+    """Accounting 1 is the real layout: Mistral-shaped K8 linear / V4 log at n=64 stores
+    120 + 88 bytes per (K, V) vector pair of d=128, i.e. 6.5 bits per element."""
+    table = [(64, 64, 8, 4, 1, 2)] * 32
+    cfg = _cfg(tvq, table, 32, 8, 128)
+    assert tvq.tvq_bits_per_element_config(cfg, 1) == pytest.approx((120 + 88) * 8 / 256)
+    assert tvq.tvq_bits_per_element_config(cfg, 0) == pytest.approx(6.5)
+    # non-power-of-two n is fractional in the paper's accounting, whole bits in storage
+    cfg48 = _cfg(tvq, [(48, 48, 32, 32, 0, 0)], 1, 1, 128)
+    assert tvq.tvq_bits_per_element_config(cfg48, 0) == pytest.approx(np.log2(48) / 2 + 16)
+    assert tvq.tvq_bits_per_element_config(cfg48, 1) == pytest.approx(3.0 + 16)
+    assert tvq.tvq_bits_per_element_config(cfg48, 7) < 0
+
+
+@pytest.mark.parametrize("bad", [
+    dict(L=0), dict(L=257), dict(H=0), dict(d=48), dict(d=0), dict(nk=1), dict(nk=4097),
+    dict(bk=0, mk=1), dict(bk=17, mk=1), dict(mk=3), dict(signs_bad=True),
+])
+def test_invalid_configs_rejected_before_gpu(tvq, bad):
+    """Config validation is host-only: bad values return TVQ_ERR_INVALID_ARG without a GPU."""
+    L = bad.get("L", 2)
+    d = bad.get("d", 128)
+    nk = bad.get("nk", 64)
+    table = [(nk, 64, bad.get("bk", 8), 4, bad.get("mk", 1), 2)] * max(L, 1)
+    if L > 256:
+        table = table[:256]   # the count is rejected before the table is read
+    signs = None
+    if bad.get("signs_bad"):
+        signs = np.ones((L, d), np.int8)
+        signs[1, 3] = 0
+    cfg = _cfg(tvq, table, L, bad.get("H", 8), d, signs=signs)
+    h = ctypes.c_void_p()
+    assert tvq.load_library().tvq_create(ctypes.byref(cfg), ctypes.byref(h)) == -1
+    assert not h.value
+    lay = tvq.tvq_layout()
+    assert tvq.load_library().tvq_layout_for_config(ctypes.byref(cfg), 1, 16, ctypes.byref(lay)) == -1
+
+
+def test_unsupported_head_dim(tvq):
+    """d = 32 and 256 are valid for the method but the GPU kernels are built for 64 and 128."""
+    for d in (32, 256):
+        cfg = _cfg(tvq, [(64, 64, 8, 4, 1, 2)], 1, 1, d)
+        h = ctypes.c_void_p()
+        assert tvq.load_library().tvq_create(ctypes.byref(cfg), ctypes.byref(h)) == -2
+        assert tvq.tvq_layout_for_config(cfg, 1, 4).total_bytes > 0
+
+
+def test_null_codec_calls_rejected(tvq):
+    lib = tvq.load_library()
+    desc = tvq.tvq_tensor_desc(1, 1, 0, 0, 0, 128)
+    lay = tvq.tvq_layout()
+    assert lib.tvq_encode(None, 0, None, None, ctypes.byref(desc), 0, None, ctypes.byref(lay), None) == -1
+    assert lib.tvq_decode(None, None, ctypes.byref(lay), 0, 1, 0, None, None, ctypes.byref(desc), None) == -1
+    assert lib.tvq_cache_layout(None, 1, 1, ctypes.byref(lay)) == -1
+    assert lib.tvq_bits_per_element(None, 0) < 0
+    lib.tvq_destroy(None)
+
+
+def test_layout_limits(tvq):
+    cfg = _cfg(tvq, [(64, 64, 8, 4, 1, 2)], 1, 8, 128)
+    lib = tvq.load_library()
+    lay = tvq.tvq_layout()
+    assert lib.tvq_layout_for_config(ctypes.byref(cfg), 0, 16, ctypes.byref(lay)) == -1
+    assert lib.tvq_layout_for_config(ctypes.byref(cfg), 1, 0, ctypes.byref(lay)) == -1
+    assert lib.tvq_layout_for_config(ctypes.byref(cfg), 1 << 20, 1 << 12, ctypes.byref(lay)) == -1

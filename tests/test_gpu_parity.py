@@ -1,0 +1,295 @@
+"""GPU parity: the HIP encode/decode kernels, called through the C ABI, against the CPU oracle
+on the same seeded inputs.
+
+Bars (each asserted below):
+  - angle and norm codes bit-exact, except pairs whose oracle angle coordinate n*theta/2pi (or
+    norm coordinate t) lies within 1e-6 of the code range of a bin boundary -- those are
+    counted and reported, never asserted;
+  - stored fp32 values (the per-vector min/max header, fp32 norms) within 2 ulp;
+  - decode of the GPU cache bit-exact against the oracle's fixed-order fp32 decode of the same
+    bytes (fp32 and bf16 outputs; the bf16 bar of 1 ulp is therefore met with 0), and within
+    1e-5 relative L2 per vector of the oracle's fp64 decode;
+  - cache slots outside the written token range keep their previous bytes.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from workloads import LayerCfg, NORM_F32, NORM_LINEAR, NORM_LOG
+
+from parity import (Setup, bf16_bits_to_torch, compare_decode, compare_encode, run_encode,
+                    setup_from_workload, torch_to_np, untouched_outside)
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _check_encode(rep, name):
+    _say(f"[{name}] pairs={rep.pairs} angle mismatch={rep.angle_mismatch} "
+         f"(flagged pairs {rep.angle_flagged}, unflagged mismatches {rep.angle_unflagged_mismatch}) "
+         f"norm mismatch={rep.norm_mismatch} (flagged {rep.norm_flagged}, unflagged "
+         f"{rep.norm_unflagged_mismatch}) header<= {rep.header_max_ulp} ulp, fp32 norms <= "
+         f"{rep.f32norm_max_ulp} ulp")
+    for note in rep.notes[:40]:
+        _say("   " + note)
+    assert rep.angle_unflagged_mismatch == 0
+    assert rep.norm_unflagged_mismatch == 0
+    assert rep.header_max_ulp <= 2
+    assert rep.f32norm_max_ulp <= 2
+
+
+def _check_decode(rep, name):
+    _say(f"[{name}] decode vectors={rep.vectors} fp32 bit-mismatch vectors="
+         f"{rep.f32_bit_mismatch_vectors} max rel L2 vs fp64={rep.f32_max_rel_l2_vs_f64:.3e} "
+         f"bf16 max ulp={rep.bf16_max_ulp} ({rep.bf16_mismatch_elems} elems differ)")
+    assert rep.f32_bit_mismatch_vectors == 0
+    assert rep.bf16_max_ulp == 0
+    assert rep.f32_max_rel_l2_vs_f64 <= 1e-5
+
+
+def _draw(w, L, B, H, T, d, dtype, seed):
+    """Small draw with the distributions of workload `w` but custom shape."""
+    ww = workloads.Workload(w.name, L, B, H, T, d, dtype, w.table[:L], seed, w.sign_seed,
+                            w.k_dist, w.v_dist, w.n_outlier, w.outlier_scale)
+    return workloads.generate(ww, "K"), workloads.generate(ww, "V")
+
+
+def _roundtrip(s, k, v, B, T, T_cap, t_begin, name):
+    gcache, ocache, u, t, lay, cache_dev = run_encode(s, k, v, B, T, T_cap, t_begin)
+    assert untouched_outside(gcache, s, B, T, T_cap, t_begin, 0xAB)
+    _check_encode(compare_encode(s, gcache, ocache, u, t, B, T, T_cap, t_begin), name)
+    _check_decode(compare_decode(s, cache_dev, lay, B, t_begin, t_begin + T), name)
+
+
+# ---------------------------------------------------------------------------- workloads
+def test_tiny_f32_workload_full(gpu):
+    """1 layer, 4 heads, d=64, 256 tokens, fp32 inputs with 2 outlier channels x20, n=64,
+    fp32 norms: the whole encode + decode round trip."""
+    w = workloads.get("C1")
+    s = setup_from_workload(w)
+    k, v = workloads.generate(w, "K"), workloads.generate(w, "V")
+    _roundtrip(s, k, v, w.B, w.T, w.T, 0, "tiny-f32")
+
+
+def test_mistral_shaped_small(gpu):
+    """d=128 bf16, K 8-bit linear / V 4-bit log norms, per-layer tables mixing n=64, 256, the
+    non-power-of-two 48 and the odd-width 128 (7 bits); 37 tokens = 2 tiles + a ragged tail."""
+    w = workloads.get("C2")
+    table = [LayerCfg(64, 64), LayerCfg(256, 256), LayerCfg(48, 128)]
+    s = Setup(3, 3, 128, table, workloads.sign_table(5, 3, 128)).build()
+    k, v = _draw(w, 3, 2, 3, 37, 128, "bf16", 11)
+    _roundtrip(s, k, v, 2, 37, 37, 0, "mistral-small")
+
+
+def test_early_boost_table_d128(gpu):
+    """The 4-layer early-boost table of the Mistral-shaped workload (n=256 on layers 0-3, 64
+    after) at a reduced token count."""
+    w = workloads.get("C3")
+    s = Setup(6, 2, 128, w.table[:6], workloads.sign_table(w.sign_seed, 6, 128)).build()
+    k, v = _draw(w, 6, 1, 2, 70, 128, "bf16", 3)
+    _roundtrip(s, k, v, 1, 70, 96, 0, "early-boost-d128")
+
+
+def test_d64_batched_k_boost(gpu):
+    """d=64 (two lanes per vector), batch 3, K-only boost (n_K=256, n_V=64), ragged tokens."""
+    w = workloads.get("C4")
+    s = Setup(3, 2, 64, w.table[2:5], workloads.sign_table(w.sign_seed, 3, 64)).build()
+    k, v = _draw(w, 3, 3, 2, 45, 64, "bf16", 4)
+    _roundtrip(s, k, v, 3, 45, 45, 0, "d64-batched")
+
+
+def test_long_context_append_one_token(gpu):
+    """Append one token per (sequence, layer, head) at position 9 of a 16-slot cache (the
+    per-step encode of the long-context workload), then decode that single slot."""
+    w = workloads.get("C5")
+    s = Setup(4, 8, 128, w.table[:4], workloads.sign_table(w.sign_seed, 4, 128)).build()
+    k, v = _draw(w, 4, 16, 8, 1, 128, "bf16", 5)
+    _roundtrip(s, k, v, 16, 1, 16, 9, "append-1")
+
+
+# ---------------------------------------------------------------------------- coverage
+@pytest.mark.parametrize("d", [64, 128])
+def test_odd_widths_and_norm_modes(gpu, d):
+    """Odd code widths (n=32 -> 5 bits, n=100 -> 7 bits non-power-of-two, n=3 -> 2 bits),
+    5-, 3-, 16- and 1-bit norm codes, fp32 norms, fp32 input."""
+    table = [LayerCfg(32, 100, 5, 3, NORM_LINEAR, NORM_LOG),
+             LayerCfg(3, 4096, 16, 1, NORM_LOG, NORM_LINEAR),
+             LayerCfg(56, 8, 32, 12, NORM_F32, NORM_LOG)]
+    s = Setup(3, 2, d, table, workloads.sign_table(9, 3, d)).build()
+    w = workloads.get("C2")
+    k, v = _draw(w, 3, 1, 2, 33, d, "f32", 6)
+    _roundtrip(s, k, v, 1, 33, 40, 3, f"odd-widths-d{d}")
+
+
+def test_seeded_signs(gpu):
+    """The codec draws D itself from a seed (per layer, and shared across layers as the paper
+    does); the oracle draws it with its own SplitMix64."""
+    w = workloads.get("C2")
+    k, v = _draw(w, 2, 1, 2, 20, 128, "bf16", 7)
+    for shared in (False, True):
+        s = Setup(2, 2, 128, [LayerCfg(64, 64)] * 2, None, seed_mode=True, seed=1234,
+                  shared=shared).build()
+        _roundtrip(s, k, v, 1, 20, 20, 0, f"seeded-signs-shared{int(shared)}")
+
+
+def test_strided_input_view(gpu):
+    """Input stored [L][B][T][H][d] in memory and passed as a permuted [L,B,H,T,d] view."""
+    import torch
+    w = workloads.get("C2")
+    s = Setup(2, 4, 128, [LayerCfg(64, 64), LayerCfg(256, 64)],
+              workloads.sign_table(3, 2, 128)).build()
+    k, v = _draw(w, 2, 2, 4, 19, 128, "bf16", 8)
+    kd = bf16_bits_to_torch(np.ascontiguousarray(k.transpose(0, 1, 3, 2, 4))).cuda().permute(0, 1, 3, 2, 4)
+    vd = bf16_bits_to_torch(np.ascontiguousarray(v.transpose(0, 1, 3, 2, 4))).cuda().permute(0, 1, 3, 2, 4)
+    assert not kd.is_contiguous()
+    gcache, ocache, u, t, lay, cache_dev = run_encode(s, k, v, 2, 19, 19, 0, k_dev=kd, v_dev=vd)
+    _check_encode(compare_encode(s, gcache, ocache, u, t, 2, 19, 19, 0), "strided")
+    # decode into a strided output view too
+    ko = torch.empty((2, 2, 19, 4, 128), dtype=torch.float32, device="cuda").permute(0, 1, 3, 2, 4)
+    vo = torch.empty_like(ko)
+    s.gpu.decode(cache_dev, lay, 0, 19, ko, vo)
+    torch.cuda.synchronize()
+    ref = s.orc.decode_cache(gcache, 2, 19, 0, 19, "f32")
+    assert np.array_equal(torch_to_np(ko).view(np.uint32), ref[:, 0].view(np.uint32))
+    assert np.array_equal(torch_to_np(vo).view(np.uint32), ref[:, 1].view(np.uint32))
+
+
+def test_edge_vectors(gpu):
+    """Zero vectors, one-hot vectors (degenerate min = max), constant-norm vectors, values near
+    the bottom of the fp32 range (the careful path), and large values, in one batch."""
+    d, T = 128, 24
+    rng = np.random.default_rng(42)
+    x = rng.standard_normal((1, 1, 2, T, d)).astype(np.float32)
+    x[0, 0, :, 0] = 0.0                                # zero vector
+    x[0, 0, :, 1] = 0.0
+    x[0, 0, 0, 1, 5] = 3.0                             # one-hot
+    x[0, 0, 1, 1, 64] = -0.25
+    x[0, 0, :, 2] *= np.float32(1e-35)                 # deep in the small range
+    x[0, 0, :, 3] *= np.float32(1e30)                  # large but finite after the transform
+    x[0, 0, :, 4, :] = 0.0
+    x[0, 0, :, 4, 0:2] = [1e-40, -3e-41]               # fp32 subnormals, one nonzero pair
+    x[0, 0, :, 5, :] = 1.0                             # constant vector
+    x[0, 0, :, 6, :] = 0.0
+    x[0, 0, :, 6, 7] = 1e-38                           # one-hot near the normal minimum
+    table = [LayerCfg(64, 48, 8, 4, NORM_LINEAR, NORM_LOG)]
+    s = Setup(1, 2, d, table, workloads.sign_table(1, 1, d)).build()
+    _roundtrip(s, x, x * np.float32(-0.5), 1, T, T, 0, "edge-f32")
+    xb = (x.view(np.uint32) >> 16).astype(np.uint16)   # bf16 truncations of the same values
+    _roundtrip(s, xb, xb ^ np.uint16(0x8000), 1, T, T, 0, "edge-bf16")
+
+
+def test_scale_equivariance_on_gpu(gpu):
+    """encode(2^j x) on the GPU: identical codes, header and fp32 norms scaled exactly."""
+    import torch
+    w = workloads.get("C2")
+    table = [LayerCfg(64, 64), LayerCfg(64, 64, 32, 32, NORM_F32, NORM_F32)]
+    s = Setup(2, 2, 128, table, workloads.sign_table(4, 2, 128)).build()
+    k, v = _draw(w, 2, 1, 2, 32, 128, "f32", 9)
+    lay = s.gpu.layout(1, 32)
+    c1 = torch.zeros(lay.total_bytes, dtype=torch.uint8, device="cuda")
+    c2 = torch.zeros_like(c1)
+    kd, vd = torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda()
+    s.gpu.encode(kd, vd, c1, lay)
+    s.gpu.encode(kd * 16, vd * 16, c2, lay)
+    torch.cuda.synchronize()
+    a, b = torch_to_np(c1), torch_to_np(c2)
+    total, off = s.orc.layout(1, 32)
+    for l in range(2):
+        for kind in range(2):
+            rec = s.orc.record_bytes(l, kind)
+            n = 64 * rec[0]
+            assert np.array_equal(a[off[l, kind, 0]:off[l, kind, 0] + n], b[off[l, kind, 0]:off[l, kind, 0] + n])
+            if rec[2]:
+                n1 = 64 * rec[1]
+                assert np.array_equal(a[off[l, kind, 1]:off[l, kind, 1] + n1], b[off[l, kind, 1]:off[l, kind, 1] + n1])
+                ha = a[off[l, kind, 2]:off[l, kind, 2] + 64 * 8].view(np.float32)
+                hb = b[off[l, kind, 2]:off[l, kind, 2] + 64 * 8].view(np.float32)
+                assert np.array_equal(ha * 16, hb)
+            else:
+                fa = a[off[l, kind, 1]:off[l, kind, 1] + 64 * rec[1]].view(np.float32)
+                fb = b[off[l, kind, 1]:off[l, kind, 1] + 64 * rec[1]].view(np.float32)
+                assert np.array_equal(fa * 16, fb)
+
+
+def test_api_errors_with_live_codec(gpu):
+    """Argument errors return TVQ_ERR_INVALID_ARG synchronously and launch nothing."""
+    import torch
+    import paper_2603_27467_amd as tvq
+    s = Setup(1, 2, 128, [LayerCfg(64, 64)], workloads.sign_table(1, 1, 128)).build()
+    lay = s.gpu.layout(1, 8)
+    cache = torch.zeros(lay.total_bytes + 64, dtype=torch.uint8, device="cuda")
+    k = torch.zeros((1, 1, 2, 8, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(tvq.TvqError):                      # past the capacity
+        s.gpu.encode(k, k, cache, lay, t_begin=1)
+    with pytest.raises(tvq.TvqError):                      # misaligned cache pointer
+        s.gpu.encode(k, k, cache[4:], lay)
+    other = s.gpu.layout(2, 8)
+    with pytest.raises(tvq.TvqError):                      # batch differs from the layout
+        s.gpu.encode(k, k, cache, other)
+    out = torch.zeros_like(k)
+    with pytest.raises(tvq.TvqError):                      # token count differs from range
+        s.gpu.decode(cache, lay, 0, 7, out, out)
+    s.gpu.encode(k[:, :, :, :0], k[:, :, :, :0], cache, lay)   # empty range: nothing to do
+    torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------------------- full size
+def test_mistral_cache_full_size_sampled(gpu):
+    """The full Mistral-7B-shaped cache (32 layers, 8 heads, 4096 tokens, d=128, bf16) in the
+    launch configuration the benchmark times; 3000 sampled vectors compared with the oracle
+    one by one, plus whole-cache properties (every slot written, decode finite)."""
+    import torch
+    w = workloads.get("C2")
+    s = setup_from_workload(w)
+    k, v = workloads.generate(w, "K"), workloads.generate(w, "V")
+    lay = s.gpu.layout(w.B, w.T)
+    cache = torch.full((lay.total_bytes,), 0xAB, dtype=torch.uint8, device="cuda")
+    kd, vd = bf16_bits_to_torch(k).cuda(), bf16_bits_to_torch(v).cuda()
+    s.gpu.encode(kd, vd, cache, lay)
+    ko = torch.empty_like(kd)
+    vo = torch.empty_like(vd)
+    s.gpu.decode(cache, lay, 0, w.T, ko, vo)
+    torch.cuda.synchronize()
+    host = torch_to_np(cache)
+    kout, vout = torch_to_np(ko), torch_to_np(vo)
+    rng = np.random.default_rng(0)
+    P = w.d // 2
+    stats = dict(angle_mismatch=0, angle_unflagged=0, norm_mismatch=0, norm_unflagged=0,
+                 hdr_ulp=0, dec_mismatch=0)
+    for _ in range(3000):
+        l, kind, h, t = (int(rng.integers(0, w.L)), int(rng.integers(0, 2)),
+                         int(rng.integers(0, w.H)), int(rng.integers(0, w.T)))
+        src = k if kind == 0 else v
+        x = (src[l, 0, h, t].astype(np.uint32) << 16).view(np.float32)
+        kd_ = s.orc.kinds[2 * l + kind]
+        ref = oracle.encode_vector(x, s.signs[l], kd_)
+        kg, qg, rng_, hg = s.orc.read_vector(host, w.B, w.T, l, kind, 0, h, t)
+        fa = oracle.angle_flags(ref.u, kd_.n)
+        fn = oracle.norm_flags(ref.t, kd_.norm_bits)
+        stats["angle_mismatch"] += int((kg != ref.k).sum())
+        stats["angle_unflagged"] += int(((kg != ref.k) & ~fa).sum())
+        stats["norm_mismatch"] += int((qg != ref.q).sum())
+        stats["norm_unflagged"] += int(((qg != ref.q) & ~fn).sum())
+        du = np.abs(hg.view(np.int32).astype(np.int64) - ref.hdr.view(np.int32).astype(np.int64))
+        stats["hdr_ulp"] = max(stats["hdr_ulp"], int(du.max()))
+        dec = oracle.decode_vector(kd_, s.signs[l], kg, qg, None, hg, "f32")
+        got = (kout if kind == 0 else vout)[l, 0, h, t]
+        stats["dec_mismatch"] += int((oracle.f32_to_bf16(dec) != got).sum())
+    _say(f"[mistral-full sampled 3000] {stats}")
+    assert stats["angle_unflagged"] == 0 and stats["norm_unflagged"] == 0
+    assert stats["hdr_ulp"] <= 2 and stats["dec_mismatch"] == 0
+    # whole-cache properties: every header plane slot overwritten, outputs finite
+    total, off = s.orc.layout(w.B, w.T)
+    nslot = w.B * w.H * w.T
+    for l in (0, w.L - 1):
+        for kind in range(2):
+            hdr = host[off[l, kind, 2]: off[l, kind, 2] + nslot * 8].view(np.float32).reshape(-1, 2)
+            assert np.all(hdr[:, 0] <= hdr[:, 1]) and np.all(hdr[:, 0] > 0)
+    assert torch.isfinite(ko.float()).all() and torch.isfinite(vo.float()).all()
