@@ -144,13 +144,13 @@ bool desc_valid(const tvq_codec* c, const tvq_tensor_desc* t, int elem_bytes) {
 }
 
 unsigned plan_grid(uint32_t nvec, uint32_t vpw, uint32_t num_segs, uint32_t* waves_per_seg,
-                   uint32_t* tiles_per_wave) {
+                   uint32_t* tiles_per_wave, uint32_t max_tiles_per_wave) {
   const uint64_t tiles_per_seg = (nvec + vpw - 1) / vpw;
   const uint64_t total_tiles = tiles_per_seg * num_segs;
   // aim for at least ~32 waves per compute unit of a 256-CU part before grouping tiles
   uint64_t tpw = total_tiles / (256ull * 32ull);
   if (tpw < 1) tpw = 1;
-  if (tpw > 8) tpw = 8;
+  if (tpw > max_tiles_per_wave) tpw = max_tiles_per_wave;
   const uint64_t wps = (tiles_per_seg + tpw - 1) / tpw;
   *waves_per_seg = (uint32_t)wps;
   *tiles_per_wave = (uint32_t)tpw;
@@ -382,7 +382,7 @@ tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, con
   a.num_segs = (uint32_t)(2 * c->L);
   a.inv_d = 1.0f / (float)c->d;
   const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
-  const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave);
+  const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave, 1);
   const int rc = tvq_launch_encode(a, c->d, in_dtype == TVQ_F32, grid, stream);
   if (rc == -1) return TVQ_ERR_UNSUPPORTED;
   return rc == 0 ? TVQ_OK : TVQ_ERR_HIP;
@@ -424,7 +424,7 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
   a.num_segs = (uint32_t)(2 * c->L);
   a.c_d = (float)(1.0 / std::sqrt((double)c->d));
   const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
-  const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave);
+  const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave, 1);
   const int rc = tvq_launch_decode(a, c->d, out_dtype == TVQ_F32, grid, stream);
   if (rc == -1) return TVQ_ERR_UNSUPPORTED;
   return rc == 0 ? TVQ_OK : TVQ_ERR_HIP;

@@ -23,15 +23,12 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t x, const FastDiv& d) {
   return (uint32_t)(((uint64_t)x * d.m) >> d.s);
 }
 
-// DPP quad permutations: 0xB1 = [1,0,3,2] (lane ^ 1), 0x4E = [2,3,0,1] (lane ^ 2).
+// DPP quad permutations: 0xB1 = [1,0,3,2] (lane ^ 1), 0x4E = [2,3,0,1] (lane ^ 2).  The old
+// value is left undefined (bound_ctrl on, every quad lane is in range), which lets the
+// compiler fold the permutation into the consuming v_add/v_min/v_max as a DPP operand.
 template <int CTRL>
 __device__ __forceinline__ float quad_perm(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
-}
-
-template <int CTRL>
-__device__ __forceinline__ uint32_t quad_perm_u(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
 }
 
 // In-lane butterfly stages h = 1, 2, 4, 8, 16 over the lane's 32 elements.  Each stage maps
@@ -67,6 +64,51 @@ __device__ __forceinline__ void fwht_cross_lane(float (&x)[kElemsPerLane], int s
     for (int j = 0; j < kElemsPerLane; ++j) x[j] = __builtin_fmaf(c, x[j], quad_perm<0x4E>(x[j]));
   }
   static_assert(LPV == 1 || LPV == 2 || LPV == 4, "d must be 32, 64 or 128");
+}
+
+// Cross-lane stages in one instruction per element: x_j <- partner_j * c + x_j as
+// v_fmac_f32 with the DPP-permuted partner as multiplicand (c = +1 on the lane holding z_j,
+// -1 on the lane holding z_j+h).  The first lane gets z_j + z_j+h; the second gets
+// -(z_j - z_j+h), the exact negation of the butterfly output (up to the sign of an exact
+// zero).  After the stages each lane holds sigma * z with sigma = (-1)^popcount(sub), which
+// the caller accounts for.  The DPP source must not be written by either of the two
+// preceding VALU instructions; each group of eight starts with s_nop 1 and writes only its
+// own registers, so that holds inside the group and at its start.
+#define TVQ_FMAC_DPP_1(P, I) "v_fmac_f32_dpp %" #I ", %" #I ", %8 " P " row_mask:0xf bank_mask:0xf\n\t"
+#define TVQ_FMAC_DPP_8(P)                                                                   \
+  "s_nop 1\n\t" TVQ_FMAC_DPP_1(P, 0) TVQ_FMAC_DPP_1(P, 1) TVQ_FMAC_DPP_1(P, 2)           \
+      TVQ_FMAC_DPP_1(P, 3) TVQ_FMAC_DPP_1(P, 4) TVQ_FMAC_DPP_1(P, 5) TVQ_FMAC_DPP_1(P, 6)  \
+          TVQ_FMAC_DPP_1(P, 7)
+
+__device__ __forceinline__ void fmac_dpp_xor1(float (&x)[kElemsPerLane], float c) {
+#pragma unroll
+  for (int g = 0; g < kElemsPerLane; g += 8)
+    asm volatile(TVQ_FMAC_DPP_8("quad_perm:[1,0,3,2]")
+                 : "+v"(x[g]), "+v"(x[g + 1]), "+v"(x[g + 2]), "+v"(x[g + 3]), "+v"(x[g + 4]),
+                   "+v"(x[g + 5]), "+v"(x[g + 6]), "+v"(x[g + 7])
+                 : "v"(c));
+}
+
+__device__ __forceinline__ void fmac_dpp_xor2(float (&x)[kElemsPerLane], float c) {
+#pragma unroll
+  for (int g = 0; g < kElemsPerLane; g += 8)
+    asm volatile(TVQ_FMAC_DPP_8("quad_perm:[2,3,0,1]")
+                 : "+v"(x[g]), "+v"(x[g + 1]), "+v"(x[g + 2]), "+v"(x[g + 3]), "+v"(x[g + 4]),
+                   "+v"(x[g + 5]), "+v"(x[g + 6]), "+v"(x[g + 7])
+                 : "v"(c));
+}
+
+template <int LPV>
+__device__ __forceinline__ void fwht_cross_lane_signed(float (&x)[kElemsPerLane], int sub) {
+  if constexpr (LPV >= 2) fmac_dpp_xor1(x, (sub & 1) ? -1.0f : 1.0f);
+  if constexpr (LPV >= 4) fmac_dpp_xor2(x, (sub & 2) ? -1.0f : 1.0f);
+  static_assert(LPV == 1 || LPV == 2 || LPV == 4, "d must be 32, 64 or 128");
+}
+
+// sigma of fwht_cross_lane_signed: true when the lane holds the negated butterfly output
+template <int LPV>
+__device__ __forceinline__ bool lane_negated(int sub) {
+  return (__builtin_popcount((unsigned)sub & (unsigned)(LPV - 1)) & 1) != 0;
 }
 
 template <int LPV>

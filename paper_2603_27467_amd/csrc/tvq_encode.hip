@@ -4,9 +4,17 @@
 // Walsh-Hadamard butterfly (the 1/sqrt(d) factor of H only scales the norms), polar form of
 // consecutive pairs, uniform angle bins, per-vector min-max norm codes, bit-packing.
 //
-// Work split: a wave takes `tiles_per_wave` tiles of 64/(d/32) consecutive vectors of one
-// (layer, kind) segment, so the segment's parameters and sign masks stay in scalar and vector
-// registers for all its tiles.  No LDS, no barriers: every wave is independent.
+// Work split: a wave takes one tile of 64/(d/32) consecutive vectors of one (layer, kind)
+// segment.  Memory latency is hidden by occupancy (4 waves per SIMD at this register count);
+// a loop over several tiles per wave would hoist loop invariants into ~40 more registers.
+// No LDS, no barriers: every wave is independent.
+//
+// The kernel is bound by VALU issue, so the per-pair path is kept branch-free and short:
+// codes are rounded by the 1.5*2^23 shift and handed to the packer as raw float bits, whose
+// low bits are the code (the packer masks them to the code width, which is the "mod n" for n
+// a power of two).  The two cross-lane butterfly stages take one instruction per element and
+// leave some lanes holding the negated transform; for the angle that is a half-turn rotation,
+// folded into the rounding shift.
 #include <float.h>
 #include <hip/hip_runtime.h>
 
@@ -16,61 +24,70 @@
 namespace tvq {
 namespace {
 
-// atan(t) / (2 pi) for t in [0, 1] as t * p(t^2), degree-13 odd polynomial fitted for
-// minimum maximum error (5.4e-8 of a turn when evaluated in fp32, against 1e-6 of a turn
-// that separates an unflagged pair from a bin boundary).
+constexpr float kRoundShift = 12582912.0f;    // 1.5 * 2^23
+constexpr uint32_t kRoundShiftBits = 0x4B400000u;
+
+// atan(t) / (2 pi) for t in [0, 1] as t * p(t^2), degree-11 odd polynomial fitted for minimum
+// maximum error: 2.8e-7 of a turn when evaluated in fp32, inside the 1e-6 of a turn that
+// separates an unflagged pair from a bin boundary.
 __device__ __forceinline__ float atan_turns01(float t) {
   const float s = t * t;
-  float p = 1.084129326e-03f;
-  p = __builtin_fmaf(p, s, -5.348274019e-03f);
-  p = __builtin_fmaf(p, s, 1.267249696e-02f);
-  p = __builtin_fmaf(p, s, -2.106151544e-02f);
-  p = __builtin_fmaf(p, s, 3.152511641e-02f);
-  p = __builtin_fmaf(p, s, -5.302623659e-02f);
-  p = __builtin_fmaf(p, s, 1.591543257e-01f);
+  float p = -1.865156344e-03f;
+  p = __builtin_fmaf(p, s, 8.379081264e-03f);
+  p = __builtin_fmaf(p, s, -1.852984540e-02f);
+  p = __builtin_fmaf(p, s, 3.080290556e-02f);
+  p = __builtin_fmaf(p, s, -5.293856561e-02f);
+  p = __builtin_fmaf(p, s, 1.591513157e-01f);
   return t * p;
 }
 
-// Signed angle bin of the pair (a, b): round(n * atan2(b, a) / 2pi) before the "mod n".
-// Octant reduction: t = min(|a|,|b|) / max(|a|,|b|) in [0, 1], then reflect by the octant.
-// Requires max(|a|, |b|) in [2^-61, 2^61] (the caller checks) so rcp stays normal.
-__device__ __forceinline__ int angle_bin_signed(float a, float b, float nf) {
+// Angle bin of the pair (a, b) as the bits of round(n * atan2(b, a) / 2pi) + `shift`, where
+// shift = 1.5*2^23 (+ a whole number of bins): the low bits hold the signed bin (two's
+// complement), so masking them to ceil(log2 n) bits gives the bin mod n when n is a power
+// of two.  Reduction: in the first quadrant the angle is pi/4 + atan(t) with
+// t = (|b| - |a|) / (|b| + |a|) in [-1, 1]; the reflection into the left half plane flips the
+// sign of (angle - 1/4 turn), and the sign of b gives the lower half plane.  Requires
+// |a| + |b| in [2^-61, 2^62] (the caller checks) so rcp stays normal.
+__device__ __forceinline__ uint32_t angle_bits(float a, float b, float nf, float shift) {
   const float ax = fabsf(a), ay = fabsf(b);
-  const float mn = fminf(ax, ay), mx = fmaxf(ax, ay);
-  const float t = mn * __builtin_amdgcn_rcpf(mx);
-  float f = atan_turns01(t);          // angle from the nearer axis, turns, [0, 1/8]
-  f = (ay > ax) ? 0.25f - f : f;      // first quadrant
-  f = (a < 0.0f) ? 0.5f - f : f;      // upper half plane
-  f = copysignf(f, b);                // (-1/2, 1/2]
-  const float u = f * nf;             // |u| <= n/2 <= 2048
-  // round half to even by the 1.5*2^23 shift: the integer lands in the low mantissa bits
-  const float r = u + 12582912.0f;
-  return __float_as_int(r) - 0x4B400000;
+  const float t = (ay - ax) * __builtin_amdgcn_rcpf(ay + ax);
+  const float s = t * t;
+  float p = -1.865156344e-03f;
+  p = __builtin_fmaf(p, s, 8.379081264e-03f);
+  p = __builtin_fmaf(p, s, -1.852984540e-02f);
+  p = __builtin_fmaf(p, s, 3.080290556e-02f);
+  p = __builtin_fmaf(p, s, -5.293856561e-02f);
+  p = __builtin_fmaf(p, s, 1.591513157e-01f);
+  const float g = __builtin_fmaf(t, p, -0.125f);            // first-quadrant angle - 1/4, turns
+  const float gr = __uint_as_float(__float_as_uint(g) ^ (__float_as_uint(a) & 0x80000000u));
+  const float h = 0.25f + gr;                                // upper half plane, [0, 1/2]
+  return __float_as_uint(__builtin_fmaf(copysignf(h, b), nf, shift));
 }
 
-__device__ __forceinline__ uint32_t angle_mod(int k, uint32_t n, uint32_t mask) {
-  if (mask) return (uint32_t)k & mask;            // n a power of two
-  return (uint32_t)(k + ((k >> 31) & (int)n));    // k in [-n/2, n/2]
+// Code in [0, n) from angle_bits with shift = 1.5*2^23 + off, off in {0, -n/2}: the signed
+// bin plus n lies in [0, 3n/2], and one conditional subtraction of n (as an unsigned min)
+// wraps it.
+__device__ __forceinline__ uint32_t angle_code_wrap(uint32_t bits, uint32_t n) {
+  const uint32_t k = bits - kRoundShiftBits + n;
+  return min(k, k - n);
 }
 
-// Angle bin for pairs outside the range the fast formula assumes: zero pairs get bin 0; other
-// finite pairs are scaled by an exact power of two first.  Non-finite pairs get bin 0.
-__device__ __noinline__ uint32_t angle_code_careful(float a, float b, float nf, uint32_t n,
-                                                    uint32_t mask) {
+// Angle code for pairs outside the range the fast formula assumes: zero pairs get bin 0;
+// other finite pairs are scaled by an exact power of two first.  Non-finite pairs get bin 0.
+__device__ __noinline__ uint32_t angle_code_careful(float a, float b, float nf, uint32_t n) {
   if (a == 0.0f && b == 0.0f) return 0u;
   const float mx = fmaxf(fabsf(a), fabsf(b));
   if (!(mx <= FLT_MAX)) return 0u;
   int e;
   (void)frexpf(mx, &e);
-  const float as = ldexpf(a, -e), bs = ldexpf(b, -e);
-  return angle_mod(angle_bin_signed(as, bs, nf), n, mask);
+  return angle_code_wrap(angle_bits(ldexpf(a, -e), ldexpf(b, -e), nf, kRoundShift), n);
 }
 
-// r_i = |(a, b)| / sqrt(d) in fp64, rounded once to fp32 -- the same fp64 operation sequence
-// the definition uses, so fp32 norms come out as the correctly rounded value.
-__device__ __forceinline__ float pair_norm_f64(float a, float b, double inv_sqrt_d) {
+// r_i = |(a, b)| / sqrt(d) in fp64: the fp64 operation sequence of the definition, so a
+// single rounding to fp32 gives the correctly rounded norm.
+__device__ __forceinline__ double pair_norm_f64(float a, float b, double inv_sqrt_d) {
   const double ad = (double)a, bd = (double)b;
-  return (float)(sqrt(ad * ad + bd * bd) * inv_sqrt_d);
+  return sqrt(ad * ad + bd * bd) * inv_sqrt_d;
 }
 
 template <int W>
@@ -79,16 +96,13 @@ __device__ __forceinline__ void store_codes(uint8_t* rec, int sub, const uint32_
 }
 
 __device__ __forceinline__ void store_codes_w(uint8_t* rec, int sub, uint32_t w,
-                                           const uint32_t (&c)[kPairsPerLane]) {
+                                              const uint32_t (&c)[kPairsPerLane]) {
   switch (w) {
     case 1: store_codes<1>(rec, sub, c); break;
     case 2: store_codes<2>(rec, sub, c); break;
     case 3: store_codes<3>(rec, sub, c); break;
-    case 4: store_codes<4>(rec, sub, c); break;
     case 5: store_codes<5>(rec, sub, c); break;
-    case 6: store_codes<6>(rec, sub, c); break;
     case 7: store_codes<7>(rec, sub, c); break;
-    case 8: store_codes<8>(rec, sub, c); break;
     case 9: store_codes<9>(rec, sub, c); break;
     case 10: store_codes<10>(rec, sub, c); break;
     case 11: store_codes<11>(rec, sub, c); break;
@@ -101,13 +115,44 @@ __device__ __forceinline__ void store_codes_w(uint8_t* rec, int sub, uint32_t w,
   }
 }
 
-// Codes of the common widths are stored inline; the rest go through the out-of-line switch.
+// Codes of the common widths are packed inline; the rest through the switch.
 __device__ __forceinline__ void store_codes_any(uint8_t* rec, int sub, uint32_t w,
                                                 const uint32_t (&c)[kPairsPerLane]) {
   if (w == 6) store_codes<6>(rec, sub, c);
   else if (w == 8) store_codes<8>(rec, sub, c);
   else if (w == 4) store_codes<4>(rec, sub, c);
   else store_codes_w(rec, sub, w, c);
+}
+
+// One tile's raw input of one lane: 32 bf16 (16 words) or 32 fp32 (32 words).
+template <bool F32IN>
+struct Raw {
+  uint32_t w[F32IN ? 32 : 16];
+};
+
+template <bool F32IN>
+__device__ __forceinline__ Raw<F32IN> load_raw(const void* src, int64_t elem) {
+  Raw<F32IN> r;
+  if constexpr (F32IN) load_words<32>((const uint32_t*)src + elem, r.w);
+  else load_words<16>((const uint32_t*)((const uint16_t*)src + elem), r.w);
+  return r;
+}
+
+struct TilePos {
+  uint32_t bh, t, b, h;
+  bool valid;
+};
+
+__device__ __forceinline__ TilePos tile_pos(const EncodeArgs& a, uint32_t j0, int vslot) {
+  TilePos p;
+  const uint32_t j = j0 + vslot;
+  p.valid = j < a.nvec;
+  const uint32_t jj = p.valid ? j : j0;    // invalid lanes read a valid vector, store nothing
+  p.bh = fast_div(jj, a.div_t);
+  p.t = jj - p.bh * a.div_t.div;
+  p.b = fast_div(p.bh, a.div_h);
+  p.h = p.bh - p.b * a.H;
+  return p;
 }
 
 template <int D, bool F32IN>
@@ -125,6 +170,8 @@ __global__ __launch_bounds__(kBlockThreads) void encode_kernel(EncodeArgs a) {
   const SegParams sp = a.segs[seg];
   const void* src = sp.kind ? a.v : a.k;
   const float nf = sp.nf;
+  const bool pow2 = sp.mask != 0;
+  const int64_t layer_off = (int64_t)sp.layer * a.stride_l + sub * kElemsPerLane;
 
   // sign masks of this lane's 32 elements: 16 words, one per element pair
   uint32_t sm[16];
@@ -134,44 +181,32 @@ __global__ __launch_bounds__(kBlockThreads) void encode_kernel(EncodeArgs a) {
   uint8_t* plane_nrm = a.cache + a.n_slots * sp.pre[1];
   uint8_t* plane_hdr = a.cache + a.n_slots * sp.pre[2];
   const double inv_sqrt_d = 1.0 / sqrt((double)D);
+  const float levels = (float)((1u << (sp.bits & 31u)) - 1u);
+  // lane sign of the cross-lane butterfly and the rounding shift that absorbs it
+  const bool negated = lane_negated<LPV>(sub);
+  const bool odd_n = (sp.n & 1u) != 0;
+  const float shift = (negated && !odd_n) ? kRoundShift - 0.5f * nf : kRoundShift;
+  const uint32_t unneg = (negated && odd_n) ? 0x80000000u : 0u;
 
-  for (uint32_t it = 0; it < a.tiles_per_wave; ++it) {
-    const uint32_t j0 = (wseg * a.tiles_per_wave + it) * VPW;
-    if (j0 >= a.nvec) break;
-    const uint32_t j = j0 + vslot;
-    const bool valid = j < a.nvec;
-    const uint32_t jj = valid ? j : j0;
-    const uint32_t bh = fast_div(jj, a.div_t);
-    const uint32_t t = jj - bh * a.div_t.div;
-    const uint32_t b = fast_div(bh, a.div_h);
-    const uint32_t h = bh - b * a.H;
-    const int64_t elem = (int64_t)sp.layer * a.stride_l + (int64_t)b * a.stride_b +
-                         (int64_t)h * a.stride_h + (int64_t)t * a.stride_t + sub * kElemsPerLane;
-
-    // ---- load, sign flip (sign-bit XOR, exact), widen to fp32 ----
+  const uint32_t j0 = wseg * VPW;
+  if (j0 >= a.nvec) return;
+  const TilePos pos = tile_pos(a, j0, vslot);
+  const Raw<F32IN> raw = load_raw<F32IN>(src, layer_off + (int64_t)pos.b * a.stride_b +
+                                               (int64_t)pos.h * a.stride_h +
+                                               (int64_t)pos.t * a.stride_t);
+  {
+    // ---- sign flip (sign-bit XOR, exact), widen to fp32 ----
     float x[kElemsPerLane];
     if constexpr (F32IN) {
-      uint32_t raw[32];
-      if (valid) load_words<32>((const uint32_t*)src + elem, raw);
-      else {
-#pragma unroll
-        for (int i = 0; i < 32; ++i) raw[i] = 0u;
-      }
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
-        x[2 * m] = __uint_as_float(raw[2 * m] ^ (sm[m] << 16));
-        x[2 * m + 1] = __uint_as_float(raw[2 * m + 1] ^ (sm[m] & 0x80000000u));
+        x[2 * m] = __uint_as_float(raw.w[2 * m] ^ (sm[m] << 16));
+        x[2 * m + 1] = __uint_as_float(raw.w[2 * m + 1] ^ (sm[m] & 0x80000000u));
       }
     } else {
-      uint32_t raw[16];
-      if (valid) load_words<16>((const uint32_t*)((const uint16_t*)src + elem), raw);
-      else {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) raw[i] = 0u;
-      }
 #pragma unroll
       for (int m = 0; m < 16; ++m) {
-        const uint32_t wv = raw[m] ^ sm[m];
+        const uint32_t wv = raw.w[m] ^ sm[m];
         x[2 * m] = __uint_as_float(wv << 16);
         x[2 * m + 1] = __uint_as_float(wv & 0xFFFF0000u);
       }
@@ -179,7 +214,7 @@ __global__ __launch_bounds__(kBlockThreads) void encode_kernel(EncodeArgs a) {
 
     // ---- Walsh-Hadamard butterfly, stages h = 1 .. d/2 in ascending order ----
     fwht_in_lane(x);
-    fwht_cross_lane<LPV>(x, sub);
+    fwht_cross_lane_signed<LPV>(x, sub);   // this lane now holds sigma * z
 
     // ---- squared pair norms and the vector's extremes ----
     float s2[kPairsPerLane];
@@ -193,24 +228,37 @@ __global__ __launch_bounds__(kBlockThreads) void encode_kernel(EncodeArgs a) {
     }
     const float smin = vec_min<LPV>(lmin);
     const float smax = vec_max<LPV>(lmax);
-    // fast formulas need every pair's max(|a|,|b|) inside [2^-61, 2^60]
-    const bool in_range = !valid || (smin >= 0x1p-120f && smax <= 0x1p120f);
-    const bool fast = __all(in_range);
+    // the fast formulas need every pair's max(|a|,|b|) inside [2^-61, 2^60]
+    const bool fast = __all(!pos.valid || (smin >= 0x1p-120f && smax <= 0x1p120f));
 
     // ---- angle codes ----
+    // A lane holding -z sees every pair rotated by half a turn: for even n that is n/2 bins,
+    // removed by starting the rounding shift n/2 lower; for odd n the pair is negated back.
     uint32_t kc[kPairsPerLane];
     if (fast) {
+      if (pow2) {
 #pragma unroll
-      for (int i = 0; i < kPairsPerLane; ++i)
-        kc[i] = angle_mod(angle_bin_signed(x[2 * i], x[2 * i + 1], nf), sp.n, sp.mask);
+        for (int i = 0; i < kPairsPerLane; ++i)
+          kc[i] = angle_bits(x[2 * i], x[2 * i + 1], nf, shift);
+      } else {
+#pragma unroll
+        for (int i = 0; i < kPairsPerLane; ++i)
+          kc[i] = angle_code_wrap(angle_bits(__uint_as_float(__float_as_uint(x[2 * i]) ^ unneg),
+                                             __uint_as_float(__float_as_uint(x[2 * i + 1]) ^ unneg),
+                                             nf, shift),
+                                  sp.n);
+      }
     } else {
+      const uint32_t flip = negated ? 0x80000000u : 0u;
 #pragma unroll
       for (int i = 0; i < kPairsPerLane; ++i)
-        kc[i] = angle_code_careful(x[2 * i], x[2 * i + 1], nf, sp.n, sp.mask);
+        kc[i] = angle_code_careful(__uint_as_float(__float_as_uint(x[2 * i]) ^ flip),
+                                   __uint_as_float(__float_as_uint(x[2 * i + 1]) ^ flip), nf,
+                                   sp.n);
     }
 
-    const int64_t slot = (int64_t)bh * a.cap + a.t_begin + t;
-    if (valid) store_codes_any(plane_ang + slot * sp.rec[0], sub, sp.w, kc);
+    const int64_t slot = (int64_t)pos.bh * a.cap + a.t_begin + pos.t;
+    if (pos.valid) store_codes_any(plane_ang + slot * sp.rec[0], sub, sp.w, kc);
 
     // ---- norms ----
     if (sp.mode == 0) {
@@ -218,74 +266,71 @@ __global__ __launch_bounds__(kBlockThreads) void encode_kernel(EncodeArgs a) {
       uint32_t rn[kPairsPerLane];
 #pragma unroll
       for (int i = 0; i < kPairsPerLane; ++i)
-        rn[i] = __float_as_uint(pair_norm_f64(x[2 * i], x[2 * i + 1], inv_sqrt_d));
-      if (valid) store_words<16>((uint32_t*)(plane_nrm + slot * sp.rec[1]) + 16 * sub, rn);
-      continue;
-    }
-
-    // keys: values whose affine map onto [0, 2^b - 1] gives the code (r for linear, log r
-    // in any base for log-space), plus the stored header (Rmin, Rmax)
-    float key[kPairsPerLane];
-    float kmin, kmax, rmin, rmax;
-    if (fast) {
-      rmin = __builtin_amdgcn_sqrtf(smin * a.inv_d);
-      rmax = __builtin_amdgcn_sqrtf(smax * a.inv_d);
-      if (sp.mode == 1) {
-#pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i) key[i] = __builtin_amdgcn_sqrtf(s2[i] * a.inv_d);
-        kmin = rmin;
-        kmax = rmax;
-      } else {
-        // log2 of s2 / smin: the keys start near 0, so the fp32 spacing of the log results
-        // stays far below the code step (log2 of s2 itself would sit near 10 and lose ~1e-6
-        // to the output rounding before the subtraction)
-        const float rs = __builtin_amdgcn_rcpf(smin);
-#pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i) key[i] = __builtin_amdgcn_logf(s2[i] * rs);
-        kmin = __builtin_amdgcn_logf(smin * rs);
-        kmax = __builtin_amdgcn_logf(smax * rs);
-      }
+        rn[i] = __float_as_uint((float)pair_norm_f64(x[2 * i], x[2 * i + 1], inv_sqrt_d));
+      if (pos.valid) store_words<16>((uint32_t*)(plane_nrm + slot * sp.rec[1]) + 16 * sub, rn);
     } else {
-      float r[kPairsPerLane];
-      float l0 = FLT_MAX, l1 = 0.0f;
+      // qc: bits of t + 1.5*2^23, t the code coordinate of each pair (eq. (2) or its log
+      // variant); t stays within [-eps, 2^b - 1 + eps], so the low b bits are the code
+      uint32_t qc[kPairsPerLane];
+      float rmin, rmax;
+      if (fast) {
+        rmin = __builtin_amdgcn_sqrtf(smin * a.inv_d);
+        rmax = __builtin_amdgcn_sqrtf(smax * a.inv_d);
+        const bool degenerate = rmax == rmin;
+        if (sp.mode == 1) {
+          // linear in r: sqrt(s2) is r * sqrt(d), the same affine map up to a common factor
+          const float k0 = __builtin_amdgcn_sqrtf(smin), k1 = __builtin_amdgcn_sqrtf(smax);
+          const float scale = (degenerate || !(k1 > k0)) ? 0.0f : levels / (k1 - k0);
 #pragma unroll
-      for (int i = 0; i < kPairsPerLane; ++i) {
-        r[i] = pair_norm_f64(x[2 * i], x[2 * i + 1], inv_sqrt_d);
-        l0 = fminf(l0, r[i]);
-        l1 = fmaxf(l1, r[i]);
-      }
-      rmin = vec_min<LPV>(l0);
-      rmax = vec_max<LPV>(l1);
-      if (sp.mode == 1) {
+          for (int i = 0; i < kPairsPerLane; ++i)
+            qc[i] = __float_as_uint(
+                __builtin_fmaf(__builtin_amdgcn_sqrtf(s2[i]) - k0, scale, kRoundShift));
+        } else {
+          // log space: log2(s2 / smin) = 2 log2(r / Rmin) starts near 0, so the fp32 log
+          // outputs keep their precision (no cancellation against a large log of smin)
+          const float rs = __builtin_amdgcn_rcpf(smin);
+          const float k0 = __builtin_amdgcn_logf(smin * rs);   // ~0: rcp is not exact
+          const float k1 = __builtin_amdgcn_logf(smax * rs);
+          const float scale = (degenerate || !(k1 > k0)) ? 0.0f : levels / (k1 - k0);
 #pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i) key[i] = r[i];
-        kmin = rmin;
-        kmax = rmax;
+          for (int i = 0; i < kPairsPerLane; ++i)
+            qc[i] = __float_as_uint(
+                __builtin_fmaf(__builtin_amdgcn_logf(s2[i] * rs) - k0, scale, kRoundShift));
+        }
       } else {
+        // careful path: norms from fp64 (no overflow or underflow of a^2 + b^2), rounded once
+        // to fp32; the affine maps on r and on log r (as a ratio to the minimum, so the log
+        // input is >= 1) in fp32
+        float rf[kPairsPerLane];
+        float l0 = FLT_MAX, l1 = 0.0f;
 #pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i) key[i] = log2f(fmaxf(r[i], FLT_MIN));
-        kmin = log2f(fmaxf(rmin, FLT_MIN));
-        kmax = log2f(fmaxf(rmax, FLT_MIN));
+        for (int i = 0; i < kPairsPerLane; ++i) {
+          rf[i] = (float)pair_norm_f64(x[2 * i], x[2 * i + 1], inv_sqrt_d);
+          l0 = fminf(l0, rf[i]);
+          l1 = fmaxf(l1, rf[i]);
+        }
+        rmin = vec_min<LPV>(l0);
+        rmax = vec_max<LPV>(l1);
+        if (sp.mode == 1) {
+          const float scale = (rmax == rmin) ? 0.0f : levels / (rmax - rmin);
+#pragma unroll
+          for (int i = 0; i < kPairsPerLane; ++i)
+            qc[i] = __float_as_uint(__builtin_fmaf(rf[i] - rmin, scale, kRoundShift));
+        } else {
+          const float c0 = fmaxf(rmin, FLT_MIN);
+          const float rc = 1.0f / c0;
+          const float k1 = log2f(fmaxf(rmax, FLT_MIN) * rc);
+          const float scale = (fmaxf(rmax, FLT_MIN) == c0 || !(k1 > 0.0f)) ? 0.0f : levels / k1;
+#pragma unroll
+          for (int i = 0; i < kPairsPerLane; ++i)
+            qc[i] = __float_as_uint(
+                __builtin_fmaf(fmaxf(log2f(fmaxf(rf[i], FLT_MIN) * rc), 0.0f), scale, kRoundShift));
+        }
       }
-    }
-    const float levels = (float)((1u << sp.bits) - 1u);
-    const bool degenerate = (sp.mode == 1) ? (rmax == rmin)
-                                           : (fmaxf(rmax, FLT_MIN) == fmaxf(rmin, FLT_MIN));
-    const float scale = degenerate ? 0.0f : levels / (kmax - kmin);
-    uint32_t qc[kPairsPerLane];
-    const uint32_t qmax = (1u << sp.bits) - 1u;
-#pragma unroll
-    for (int i = 0; i < kPairsPerLane; ++i) {
-      const float tq = (key[i] - kmin) * scale;
-      const float rr = tq + 12582912.0f;
-      const uint32_t qi = __float_as_uint(rr) - 0x4B400000u;
-      qc[i] = qi > qmax ? qmax : qi;
-    }
-    if (valid) {
-      store_codes_any(plane_nrm + slot * sp.rec[1], sub, sp.bits, qc);
-      if (sub == 0) {
-        float* hp = (float*)(plane_hdr + slot * 8);
-        *(u32x2*)hp = u32x2{__float_as_uint(rmin), __float_as_uint(rmax)};
+      if (pos.valid) {
+        store_codes_any(plane_nrm + slot * sp.rec[1], sub, sp.bits, qc);
+        if (sub == 0) *(u32x2*)(plane_hdr + slot * 8) = u32x2{__float_as_uint(rmin),
+                                                              __float_as_uint(rmax)};
       }
     }
   }
