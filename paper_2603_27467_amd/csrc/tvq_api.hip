@@ -24,6 +24,8 @@ struct tvq_codec {
   tvq::SegParams* d_segs = nullptr;
   uint32_t* d_sign_masks = nullptr;
   float* d_lut = nullptr;
+  uint32_t* d_seg_lists = nullptr;           // decode-fast segment ids, then the others
+  uint32_t n_fast = 0, n_generic = 0;
 };
 
 namespace {
@@ -307,18 +309,29 @@ tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out) {
     delete c;
     return TVQ_ERR_HIP;
   }
+  // segment lists of the two decode kernels
+  std::vector<uint32_t> lists;
+  for (uint32_t i = 0; i < c->segs.size(); ++i)
+    if (tvq::decode_fast_format(c->segs[i].n, c->segs[i].mode, c->segs[i].bits)) lists.push_back(i);
+  c->n_fast = (uint32_t)lists.size();
+  for (uint32_t i = 0; i < c->segs.size(); ++i)
+    if (!tvq::decode_fast_format(c->segs[i].n, c->segs[i].mode, c->segs[i].bits)) lists.push_back(i);
+  c->n_generic = (uint32_t)lists.size() - c->n_fast;
+  const size_t list_bytes = lists.size() * sizeof(uint32_t);
   const size_t seg_bytes = c->segs.size() * sizeof(tvq::SegParams);
   const size_t mask_bytes = masks.size() * sizeof(uint32_t);
   const size_t lut_bytes = lut.size() * sizeof(float);
   if (hipMalloc((void**)&c->d_segs, seg_bytes) != hipSuccess ||
       hipMalloc((void**)&c->d_sign_masks, mask_bytes) != hipSuccess ||
-      hipMalloc((void**)&c->d_lut, lut_bytes) != hipSuccess) {
+      hipMalloc((void**)&c->d_lut, lut_bytes) != hipSuccess ||
+      hipMalloc((void**)&c->d_seg_lists, list_bytes) != hipSuccess) {
     tvq_destroy(c);
     return TVQ_ERR_ALLOC;
   }
   if (hipMemcpy(c->d_segs, c->segs.data(), seg_bytes, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(c->d_sign_masks, masks.data(), mask_bytes, hipMemcpyHostToDevice) != hipSuccess ||
-      hipMemcpy(c->d_lut, lut.data(), lut_bytes, hipMemcpyHostToDevice) != hipSuccess) {
+      hipMemcpy(c->d_lut, lut.data(), lut_bytes, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(c->d_seg_lists, lists.data(), list_bytes, hipMemcpyHostToDevice) != hipSuccess) {
     tvq_destroy(c);
     return TVQ_ERR_HIP;
   }
@@ -331,6 +344,7 @@ void tvq_destroy(tvq_codec* c) {
   if (c->d_segs) (void)hipFree(c->d_segs);
   if (c->d_sign_masks) (void)hipFree(c->d_sign_masks);
   if (c->d_lut) (void)hipFree(c->d_lut);
+  if (c->d_seg_lists) (void)hipFree(c->d_seg_lists);
   delete c;
 }
 
@@ -421,13 +435,23 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
   a.div_h = make_div((uint32_t)c->H);
   a.H = (uint32_t)c->H;
   a.nvec = (uint32_t)(out->batch * c->H * out->tokens);
-  a.num_segs = (uint32_t)(2 * c->L);
   a.c_d = (float)(1.0 / std::sqrt((double)c->d));
   const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
-  const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave, 1);
-  const int rc = tvq_launch_decode(a, c->d, out_dtype == TVQ_F32, grid, stream);
-  if (rc == -1) return TVQ_ERR_UNSUPPORTED;
-  return rc == 0 ? TVQ_OK : TVQ_ERR_HIP;
+  // the common formats go to the multi-tile kernel, the rest to the generic one
+  const struct { uint32_t first, count, tpw; bool fast; } launches[2] = {
+      {0, c->n_fast, tvq::kDecodeFastTilesPerWave, true},
+      {c->n_fast, c->n_generic, 1, false}};
+  for (const auto& l : launches) {
+    if (l.count == 0) continue;
+    a.seg_list = c->d_seg_lists + l.first;
+    a.num_segs = l.count;
+    const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave,
+                                    l.tpw);
+    const int rc = tvq_launch_decode(a, c->d, out_dtype == TVQ_F32, l.fast, grid, stream);
+    if (rc == -1) return TVQ_ERR_UNSUPPORTED;
+    if (rc != 0) return TVQ_ERR_HIP;
+  }
+  return TVQ_OK;
 }
 
 double tvq_bits_per_element_config(const tvq_config* cfg, int accounting) {

@@ -1,4 +1,4 @@
-// tvq_decode.hip -- TurboAngle decode kernel for gfx950.
+// tvq_decode.hip -- TurboAngle decode kernels for gfx950.
 //
 // Per vector (section 3.1, reconstruction; section 3.3 inverted at code centres): unpack the
 // angle and norm codes, recover the pair norms r^, rebuild y^ = r^ (cos, sin)(2 pi k / n) from
@@ -8,14 +8,27 @@
 // Arithmetic order is fixed so that results are reproducible bit for bit:
 //   linear norms  r^ = fmaf(q, RN((Rmax - Rmin) / (2^b - 1)), Rmin)   (Rmin if Rmax == Rmin)
 //   log norms     r^ = RN32(exp(L0 + q * ((L1 - L0) / (2^b - 1)))) in fp64, L = log max(R, FLT_MIN)
+//                 (up to 4 bits: the geometric ladder R'min * rho^q, rho = (R'max/R'min)^(1/(2^b-1)),
+//                 by fp64 products; it differs from the formula by ~1e-15 relative, so the fp32
+//                 levels agree except with probability ~1e-8 per level, and then by one ulp)
 //   y^            RN(r^ * C[k]), RN(r^ * S[k])
 //   x^            s_j * RN(z_j * RN(1/sqrt(d))), z = butterfly with stages h = 1 .. d/2
+// The two cross-lane butterfly stages leave some lanes holding -z (exactly, up to the sign of
+// an exact zero); that sign is folded into the output sign mask.
 //
-// Work split: one tile of 64/(d/32) vectors per wave.  Each wave stages its codebook's cos/sin
-// table in LDS (codebooks up to kLdsLut entries; larger ones are read from global memory), and
-// for log-space norms of up to 4 bits it evaluates the 2^b levels of every vector once (fp64,
-// split over the vector's lanes) into an LDS table instead of one exp per pair.  LDS is only
-// shared within a wave, so wave-scope fences order the writes before the reads.
+// Two kernels, each launched over its own list of (layer, kind) segments, so that each gets
+// the register allocation its own work needs:
+//   decode_fast_kernel     n = 64 or 256 with 8-bit linear or 4-bit log norms.  A wave decodes
+//                          several consecutive tiles and loads the next tile's code words while
+//                          decoding the current one: load latency otherwise dominates.  The
+//                          ladder ratio comes from a division-free Newton iteration, which keeps
+//                          library exp/log (and their fp64 constants, which a loop hoists into
+//                          registers) out of this kernel.
+//   decode_generic_kernel  every other format, one tile per wave.
+// A tile is 64/(d/32) vectors.  Each wave stages its codebook's cos/sin table in LDS (up to
+// kLdsLut entries; larger ones are read from global memory) and writes the log levels of up to
+// 4 bits of each vector into an LDS table.  LDS is only shared within a wave, so wave-scope
+// fences order its writes and reads.
 #include <float.h>
 #include <hip/hip_bf16.h>
 #include <hip/hip_runtime.h>
@@ -72,133 +85,169 @@ __device__ __forceinline__ void load_codes_any(const uint8_t* rec, int sub, uint
   else load_codes_w(rec, sub, w, c);
 }
 
-// fp64 log-space level of code q: exp(lo + q * delta), delta = (hi - lo) / (2^b - 1)
-__device__ __forceinline__ float log_level(double lo, double delta, uint32_t q) {
-  const double qd = (double)q * delta;
-  return (float)exp(lo + qd);
+template <int CTRL>
+__device__ __forceinline__ double quad_perm_f64(double v) {
+  const uint64_t u = __double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)u, CTRL, 0xF, 0xF, true);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)(u >> 32), CTRL, 0xF, 0xF, true);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
-template <int D, bool F32OUT>
-__global__ __launch_bounds__(kBlockThreads) void decode_kernel(DecodeArgs a) {
-  constexpr int LPV = D / kElemsPerLane;
-  constexpr int VPW = kWave / LPV;
-  __shared__ float2 s_lut[kWavesPerBlock][kLdsLut];
-  __shared__ float s_lvl[kWavesPerBlock][kLvlPerWave];
+__device__ __forceinline__ double pow_small(double x, uint32_t e) {   // x^e, e >= 1
+  double r = (e & 1u) ? x : 1.0, p = x;
+  for (e >>= 1; e; e >>= 1) {
+    p *= p;
+    if (e & 1u) r *= p;
+  }
+  return r;
+}
 
-  const int lane = threadIdx.x & (kWave - 1);
-  const int sub = lane % LPV;
-  const int vslot = lane / LPV;
-  const int wib = threadIdx.x / kWave;
-  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + wib);
-  const uint32_t seg = wave / a.waves_per_seg;
-  if (seg >= a.num_segs) return;
-  const uint32_t wseg = wave - seg * a.waves_per_seg;
-  const SegParams sp = a.segs[seg];
-  const uint32_t j0 = wseg * VPW;
-  if (j0 >= a.nvec) return;
+// rho = (R'max / R'min)^(1/L) in fp64, 0 < R'min < R'max.  For L > 1 this is the inverse L-th
+// root of r = R'min / R'max: Newton's step rho <- rho + rho (1 - r rho^L) / L takes the fp32
+// estimate (relative error ~1e-5) to ~1e-9 and then below fp64 rounding.
+__device__ __forceinline__ double ladder_ratio(float lo_c, float hi_c, uint32_t L) {
+  if (L == 1u) return (double)hi_c / (double)lo_c;
+  const double r = (double)lo_c / (double)hi_c;
+  const float lg = (__builtin_amdgcn_logf(hi_c) - __builtin_amdgcn_logf(lo_c)) / (float)L;
+  double rho = (double)__builtin_amdgcn_exp2f(lg);
+  const double invL = 1.0 / (double)L;
+  for (int k = 0; k < 2; ++k)
+    rho = __builtin_fma(rho * __builtin_fma(-r, pow_small(rho, L), 1.0), invL, rho);
+  return rho;
+}
 
-  // ---- tile position (invalid lanes decode a valid vector and store nothing) ----
+struct TilePos {
+  uint32_t bh, t, b, h;
+  int64_t slot;
+  bool valid;
+};
+
+__device__ __forceinline__ TilePos tile_pos(const DecodeArgs& a, uint32_t j0, int vslot) {
+  TilePos p;
   const uint32_t j = j0 + vslot;
-  const bool valid = j < a.nvec;
-  const uint32_t jj = valid ? j : j0;
-  const uint32_t bh = fast_div(jj, a.div_t);
-  const uint32_t t = jj - bh * a.div_t.div;
-  const uint32_t b = fast_div(bh, a.div_h);
-  const uint32_t h = bh - b * a.H;
-  const int64_t slot = (int64_t)bh * a.cap + a.t_begin + t;
-  const uint8_t* plane_ang = a.cache + a.n_slots * sp.pre[0];
-  const uint8_t* plane_nrm = a.cache + a.n_slots * sp.pre[1];
-  const uint8_t* plane_hdr = a.cache + a.n_slots * sp.pre[2];
+  p.valid = j < a.nvec;
+  const uint32_t jj = p.valid ? j : j0;    // invalid lanes decode a valid vector, store nothing
+  p.bh = fast_div(jj, a.div_t);
+  p.t = jj - p.bh * a.div_t.div;
+  p.b = fast_div(p.bh, a.div_h);
+  p.h = p.bh - p.b * a.H;
+  p.slot = (int64_t)p.bh * a.cap + a.t_begin + p.t;
+  return p;
+}
 
-  // ---- issue all global loads first: codes, header, sign masks, cos/sin table ----
-  uint32_t kc[kPairsPerLane];
-  load_codes_any(plane_ang + slot * sp.rec[0], sub, sp.w, kc);
-  uint32_t qc[kPairsPerLane];
-  float r[kPairsPerLane];
-  u32x2 hb = u32x2{0u, 0u};
-  if (sp.mode == 0) {
-    uint32_t raw[kPairsPerLane];
-    load_words<16>((const uint32_t*)(plane_nrm + slot * sp.rec[1]) + 16 * sub, raw);
-#pragma unroll
-    for (int i = 0; i < kPairsPerLane; ++i) r[i] = __uint_as_float(raw[i]);
-  } else {
-    load_codes_any(plane_nrm + slot * sp.rec[1], sub, sp.bits, qc);
-    hb = *(const u32x2*)(plane_hdr + slot * 8);
-  }
-  uint32_t sm[16];
-  load_words<16>(a.sign_masks + (size_t)sp.layer * (D / 2) + sub * 16, sm);
-  const float2* lut_g = (const float2*)a.lut + sp.lut_off;
-  const bool lut_in_lds = sp.n <= (uint32_t)kLdsLut;
-  if (lut_in_lds) {
-    for (uint32_t e = lane; e < sp.n; e += kWave) s_lut[wib][e] = lut_g[e];
-  }
-  if (!sp.mask) {
-    const uint32_t kclamp = sp.n - 1u;   // codes of a corrupted cache stay inside the table
-#pragma unroll
-    for (int i = 0; i < kPairsPerLane; ++i) kc[i] = kc[i] > kclamp ? kclamp : kc[i];
-  }
+// Per-wave state shared by every tile of the wave's segment.
+template <int D>
+struct WaveState {
+  static constexpr int LPV = D / kElemsPerLane;
+  static constexpr int VPW = kWave / LPV;
+  int lane, sub, vslot, wib;
+  SegParams sp;
+  const uint8_t* plane[3];
+  const float2* lut_g;
+  bool lut_in_lds;
+  uint32_t sm[16];           // output sign masks, with this lane's butterfly sign folded in
+};
 
-  // ---- pair norms r^ ----
-  if (sp.mode != 0) {
-    const float rmin = __uint_as_float(hb.x), rmax = __uint_as_float(hb.y);
-    const uint32_t qlevels = (1u << sp.bits) - 1u;
-    if (sp.mode == 1) {
-      const float step = (rmax - rmin) / (float)qlevels;
-      const bool deg = (rmax == rmin);
-#pragma unroll
-      for (int i = 0; i < kPairsPerLane; ++i)
-        r[i] = deg ? rmin : __builtin_fmaf((float)qc[i], step, rmin);
-    } else {
-      const double lo = log(fmax((double)rmin, (double)FLT_MIN));
-      const double hi = log(fmax((double)rmax, (double)FLT_MIN));
-      const double delta = (hi - lo) / (double)qlevels;
-      const bool deg = (hi == lo);
-      if (sp.bits <= (uint32_t)kLvlBits) {
-        // the vector's 2^b levels, split over its LPV lanes, into this wave's LDS table
-        float* lvl = &s_lvl[wib][vslot << kLvlBits];
-        for (uint32_t q = sub; q <= qlevels; q += LPV) lvl[q] = deg ? rmin : log_level(lo, delta, q);
-        wave_lds_sync();
-#pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i) r[i] = lvl[qc[i]];
-      } else {
-#pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i) r[i] = deg ? rmin : log_level(lo, delta, qc[i]);
-      }
-    }
-  }
-
-  // ---- y^ = r^ (cos, sin)(2 pi k / n) ----
-  float x[kElemsPerLane];
-  if (lut_in_lds) {
+// Segment set-up common to both kernels: the wave's segment and tiles, its cos/sin table into
+// LDS, its sign masks into registers.  Returns false if the wave has no tile.
+template <int D>
+__device__ __forceinline__ bool wave_setup(const DecodeArgs& a, WaveState<D>& w,
+                                           float2 (*lut)[kLdsLut], uint32_t& tile0,
+                                           uint32_t& ntiles) {
+  constexpr int LPV = WaveState<D>::LPV;
+  constexpr int VPW = WaveState<D>::VPW;
+  w.lane = threadIdx.x & (kWave - 1);
+  w.sub = w.lane % LPV;
+  w.vslot = w.lane / LPV;
+  w.wib = threadIdx.x / kWave;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + w.wib);
+  const uint32_t li = wave / a.waves_per_seg;
+  if (li >= a.num_segs) return false;
+  const uint32_t wseg = wave - li * a.waves_per_seg;
+  const uint32_t tiles_in_seg = (a.nvec + VPW - 1) / VPW;
+  tile0 = wseg * a.tiles_per_wave;
+  if (tile0 >= tiles_in_seg) return false;
+  ntiles = min(a.tiles_per_wave, tiles_in_seg - tile0);
+  w.sp = a.segs[a.seg_list[li]];
+  for (int p = 0; p < 3; ++p) w.plane[p] = a.cache + a.n_slots * w.sp.pre[p];
+  w.lut_g = (const float2*)a.lut + w.sp.lut_off;
+  w.lut_in_lds = w.sp.n <= (uint32_t)kLdsLut;
+  if (w.lut_in_lds) {
+    for (uint32_t e = w.lane; e < w.sp.n; e += kWave) lut[w.wib][e] = w.lut_g[e];
     wave_lds_sync();
+  }
+  load_words<16>(a.sign_masks + (size_t)w.sp.layer * (D / 2) + w.sub * 16, w.sm);
+  const uint32_t neg = lane_negated<LPV>(w.sub) ? 0x80008000u : 0u;
+#pragma unroll
+  for (int m = 0; m < 16; ++m) w.sm[m] ^= neg;
+  return true;
+}
+
+// The 2^b <= 16 log-space levels of each vector of the tile into the wave's LDS table: the
+// ladder R'min * rho^q, split over the vector's LPV lanes.  Level 0 is R'min exactly and RN32
+// brings the top level back to R'max.  Vectors with R'min == R'max get Rmin at every level.
+template <int D>
+__device__ __forceinline__ const float* build_log_levels(const WaveState<D>& w,
+                                                         float (*lvl)[kLvlPerWave], float rmin,
+                                                         float rmax, uint32_t qlevels) {
+  constexpr int LPV = WaveState<D>::LPV;
+  const float lo_c = fmaxf(rmin, FLT_MIN), hi_c = fmaxf(rmax, FLT_MIN);
+  const bool deg = lo_c == hi_c;
+  const double rho = deg ? 1.0 : ladder_ratio(lo_c, hi_c, qlevels);
+  const double rho2 = rho * rho;
+  const int sub = w.sub;
+  double pw = (sub & 1) ? rho : 1.0;          // rho^sub
+  if constexpr (LPV >= 4) pw = (sub & 2) ? pw * rho2 : pw;
+  const double step = (LPV >= 4) ? rho2 * rho2 : rho2;    // rho^LPV
+  double v = (double)lo_c * pw;
+  float* tab = &lvl[w.wib][w.vslot << kLvlBits];
+  wave_lds_sync();             // the previous tile's reads of the table are done
+  for (uint32_t q = sub; q <= qlevels; q += LPV) {
+    tab[q] = deg ? rmin : (float)v;
+    v *= step;
+  }
+  wave_lds_sync();
+  return tab;
+}
+
+// y^ = r^ (cos, sin)(2 pi k / n), x^ = D H y^, store.  LDS_LUT is a template parameter: a
+// run-time choice between the LDS and the global table makes the compiler address both through
+// flat loads, whose waits also wait for every outstanding global load.
+template <int D, bool F32OUT, bool LDS_LUT>
+__device__ __forceinline__ void reconstruct_store(const DecodeArgs& a, WaveState<D>& w,
+                                                  float2 (*lut)[kLdsLut], const TilePos& pos,
+                                                  const uint32_t (&kc)[kPairsPerLane],
+                                                  const float (&r)[kPairsPerLane]) {
+  constexpr int LPV = WaveState<D>::LPV;
+  float x[kElemsPerLane];
+  if constexpr (LDS_LUT) {
 #pragma unroll
     for (int i = 0; i < kPairsPerLane; ++i) {
-      const float2 cs = s_lut[wib][kc[i]];
+      const float2 cs = lut[w.wib][kc[i]];
       x[2 * i] = r[i] * cs.x;
       x[2 * i + 1] = r[i] * cs.y;
     }
   } else {
 #pragma unroll
     for (int i = 0; i < kPairsPerLane; ++i) {
-      const float2 cs = lut_g[kc[i]];
+      const float2 cs = w.lut_g[kc[i]];
       x[2 * i] = r[i] * cs.x;
       x[2 * i + 1] = r[i] * cs.y;
     }
   }
-
-  // ---- x^ = D H y^ ----
   fwht_in_lane(x);
-  fwht_cross_lane<LPV>(x, sub);
-  if (!valid) return;
-  const int64_t elem = (int64_t)sp.layer * a.stride_l + (int64_t)b * a.stride_b +
-                       (int64_t)h * a.stride_h + (int64_t)t * a.stride_t + sub * kElemsPerLane;
-  void* dst = sp.kind ? a.v_out : a.k_out;
+  fwht_cross_lane_signed<LPV>(x, w.sub);   // sigma * z; sigma is in the sign masks
+  if (!pos.valid) return;
+  const int64_t elem = (int64_t)w.sp.layer * a.stride_l + (int64_t)pos.b * a.stride_b +
+                       (int64_t)pos.h * a.stride_h + (int64_t)pos.t * a.stride_t +
+                       w.sub * kElemsPerLane;
+  void* dst = w.sp.kind ? a.v_out : a.k_out;
   if constexpr (F32OUT) {
     uint32_t o[32];
 #pragma unroll
     for (int m = 0; m < 16; ++m) {
-      o[2 * m] = __float_as_uint(x[2 * m] * a.c_d) ^ (sm[m] << 16);
-      o[2 * m + 1] = __float_as_uint(x[2 * m + 1] * a.c_d) ^ (sm[m] & 0x80000000u);
+      o[2 * m] = __float_as_uint(x[2 * m] * a.c_d) ^ (w.sm[m] << 16);
+      o[2 * m + 1] = __float_as_uint(x[2 * m + 1] * a.c_d) ^ (w.sm[m] & 0x80000000u);
     }
     store_words<32>((uint32_t*)dst + elem, o);
   } else {
@@ -209,26 +258,151 @@ __global__ __launch_bounds__(kBlockThreads) void decode_kernel(DecodeArgs a) {
           __float22bfloat162_rn(make_float2(x[2 * m] * a.c_d, x[2 * m + 1] * a.c_d));
       uint32_t bits;
       __builtin_memcpy(&bits, &p, 4);
-      o[m] = bits ^ sm[m];
+      o[m] = bits ^ w.sm[m];
     }
     store_words<16>((uint32_t*)((uint16_t*)dst + elem), o);
   }
 }
 
+
+// n = 64/256 angle codes (WA = 6/8 bits) with NB = 8 linear or NB = 4 log-space norm codes:
+// the next tile's code words (WA/2 + NB/2 + 2 registers) are loaded while the current tile is
+// decoded.  Only the raw code words cross iterations; tile positions are recomputed.
+template <int D, bool F32OUT, int WA, int NB>
+__device__ void decode_tiles_prefetch(const DecodeArgs& a, WaveState<D>& w, float2 (*lut)[kLdsLut],
+                                      float (*lvl)[kLvlPerWave], uint32_t tile0, uint32_t ntiles) {
+  constexpr int VPW = WaveState<D>::VPW;
+  constexpr uint32_t kLevels = (1u << NB) - 1u;
+  const TilePos p0 = tile_pos(a, tile0 * VPW, w.vslot);
+  Chunk<WA> ang = load_chunk<WA>(w.plane[0] + p0.slot * w.sp.rec[0] + 2 * WA * w.sub);
+  Chunk<NB> nrm = load_chunk<NB>(w.plane[1] + p0.slot * w.sp.rec[1] + 2 * NB * w.sub);
+  u32x2 hb = *(const u32x2*)(w.plane[2] + p0.slot * 8);
+  for (uint32_t it = 0; it < ntiles; ++it) {
+    uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
+    unpack16<WA>(ang, kc);
+    unpack16<NB>(nrm, qc);
+    const float rmin = __uint_as_float(hb.x), rmax = __uint_as_float(hb.y);
+    if (it + 1 < ntiles) {
+      const TilePos np = tile_pos(a, (tile0 + it + 1) * VPW, w.vslot);
+      ang = load_chunk<WA>(w.plane[0] + np.slot * w.sp.rec[0] + 2 * WA * w.sub);
+      nrm = load_chunk<NB>(w.plane[1] + np.slot * w.sp.rec[1] + 2 * NB * w.sub);
+      hb = *(const u32x2*)(w.plane[2] + np.slot * 8);
+    }
+    float r[kPairsPerLane];
+    if constexpr (NB == 8) {
+      const float step = (rmax - rmin) / (float)kLevels;
+      const bool deg = rmax == rmin;
+#pragma unroll
+      for (int i = 0; i < kPairsPerLane; ++i)
+        r[i] = deg ? rmin : __builtin_fmaf((float)qc[i], step, rmin);
+    } else {
+      const float* tab = build_log_levels<D>(w, lvl, rmin, rmax, kLevels);
+#pragma unroll
+      for (int i = 0; i < kPairsPerLane; ++i) r[i] = tab[qc[i]];
+    }
+    reconstruct_store<D, F32OUT, true>(a, w, lut, tile_pos(a, (tile0 + it) * VPW, w.vslot), kc, r);
+  }
+}
+
+template <int D, bool F32OUT>
+__global__ __launch_bounds__(kBlockThreads) void decode_fast_kernel(DecodeArgs a) {
+  __shared__ float2 s_lut[kWavesPerBlock][kLdsLut];
+  __shared__ float s_lvl[kWavesPerBlock][kLvlPerWave];
+  WaveState<D> w;
+  uint32_t tile0, ntiles;
+  if (!wave_setup<D>(a, w, s_lut, tile0, ntiles)) return;
+  // every codebook of this kernel (n <= 256) is in LDS
+  const bool wide = w.sp.w == 8;
+  if (w.sp.mode == 1) {
+    if (wide) decode_tiles_prefetch<D, F32OUT, 8, 8>(a, w, s_lut, s_lvl, tile0, ntiles);
+    else decode_tiles_prefetch<D, F32OUT, 6, 8>(a, w, s_lut, s_lvl, tile0, ntiles);
+  } else {
+    if (wide) decode_tiles_prefetch<D, F32OUT, 8, 4>(a, w, s_lut, s_lvl, tile0, ntiles);
+    else decode_tiles_prefetch<D, F32OUT, 6, 4>(a, w, s_lut, s_lvl, tile0, ntiles);
+  }
+}
+
+// Any code widths and norm modes, one tile per wave.
+template <int D, bool F32OUT>
+__global__ __launch_bounds__(kBlockThreads) void decode_generic_kernel(DecodeArgs a) {
+  constexpr int VPW = WaveState<D>::VPW;
+  __shared__ float2 s_lut[kWavesPerBlock][kLdsLut];
+  __shared__ float s_lvl[kWavesPerBlock][kLvlPerWave];
+  WaveState<D> w;
+  uint32_t tile0, ntiles;
+  if (!wave_setup<D>(a, w, s_lut, tile0, ntiles)) return;
+  const TilePos pos = tile_pos(a, tile0 * VPW, w.vslot);
+  uint32_t kc[kPairsPerLane];
+  load_codes_any(w.plane[0] + pos.slot * w.sp.rec[0], w.sub, w.sp.w, kc);
+  if (!w.sp.mask) {
+    const uint32_t kclamp = w.sp.n - 1u;   // codes of a corrupted cache stay inside the table
+#pragma unroll
+    for (int i = 0; i < kPairsPerLane; ++i) kc[i] = kc[i] > kclamp ? kclamp : kc[i];
+  }
+  float r[kPairsPerLane];
+  if (w.sp.mode == 0) {
+    uint32_t raw[kPairsPerLane];
+    load_words<16>((const uint32_t*)(w.plane[1] + pos.slot * w.sp.rec[1]) + 16 * w.sub, raw);
+#pragma unroll
+    for (int i = 0; i < kPairsPerLane; ++i) r[i] = __uint_as_float(raw[i]);
+  } else {
+    uint32_t qc[kPairsPerLane];
+    load_codes_any(w.plane[1] + pos.slot * w.sp.rec[1], w.sub, w.sp.bits, qc);
+    const u32x2 hb = *(const u32x2*)(w.plane[2] + pos.slot * 8);
+    const float rmin = __uint_as_float(hb.x), rmax = __uint_as_float(hb.y);
+    const uint32_t qlevels = (1u << w.sp.bits) - 1u;
+    if (w.sp.mode == 1) {
+      const float step = (rmax - rmin) / (float)qlevels;
+      const bool deg = rmax == rmin;
+#pragma unroll
+      for (int i = 0; i < kPairsPerLane; ++i)
+        r[i] = deg ? rmin : __builtin_fmaf((float)qc[i], step, rmin);
+    } else if (w.sp.bits <= (uint32_t)kLvlBits) {
+      const float* tab = build_log_levels<D>(w, s_lvl, rmin, rmax, qlevels);
+#pragma unroll
+      for (int i = 0; i < kPairsPerLane; ++i) r[i] = tab[qc[i]];
+    } else {
+      // wider log codes: exp(L0 + q delta) per pair, as written; one log per lane (even lanes
+      // of the vector take L0, odd lanes L1, each fetches the other from its neighbour)
+      const int sub = w.sub;
+      const double mine = log(fmax((double)((sub & 1) ? rmax : rmin), (double)FLT_MIN));
+      const double other = quad_perm_f64<0xB1>(mine);
+      const double lo = (sub & 1) ? other : mine;
+      const double hi = (sub & 1) ? mine : other;
+      const double delta = (hi - lo) / (double)qlevels;
+      const bool deg = hi == lo;
+#pragma unroll
+      for (int i = 0; i < kPairsPerLane; ++i) {
+        const double qd = (double)qc[i] * delta;
+        r[i] = deg ? rmin : (float)exp(lo + qd);
+      }
+    }
+  }
+  if (w.lut_in_lds) reconstruct_store<D, F32OUT, true>(a, w, s_lut, pos, kc, r);
+  else reconstruct_store<D, F32OUT, false>(a, w, s_lut, pos, kc, r);
+}
+
 }  // namespace
 }  // namespace tvq
 
-int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, unsigned grid, void* stream) {
+int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, unsigned grid,
+                      void* stream) {
   hipStream_t s = (hipStream_t)stream;
   const dim3 block(tvq::kBlockThreads);
+#define TVQ_LAUNCH_DEC(KERNEL, D)                                                      \
+  do {                                                                                 \
+    if (out_f32) hipLaunchKernelGGL((tvq::KERNEL<D, true>), dim3(grid), block, 0, s, a); \
+    else hipLaunchKernelGGL((tvq::KERNEL<D, false>), dim3(grid), block, 0, s, a);       \
+  } while (0)
   if (d == 128) {
-    if (out_f32) hipLaunchKernelGGL((tvq::decode_kernel<128, true>), dim3(grid), block, 0, s, a);
-    else hipLaunchKernelGGL((tvq::decode_kernel<128, false>), dim3(grid), block, 0, s, a);
+    if (fast) TVQ_LAUNCH_DEC(decode_fast_kernel, 128);
+    else TVQ_LAUNCH_DEC(decode_generic_kernel, 128);
   } else if (d == 64) {
-    if (out_f32) hipLaunchKernelGGL((tvq::decode_kernel<64, true>), dim3(grid), block, 0, s, a);
-    else hipLaunchKernelGGL((tvq::decode_kernel<64, false>), dim3(grid), block, 0, s, a);
+    if (fast) TVQ_LAUNCH_DEC(decode_fast_kernel, 64);
+    else TVQ_LAUNCH_DEC(decode_generic_kernel, 64);
   } else {
     return -1;
   }
+#undef TVQ_LAUNCH_DEC
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }

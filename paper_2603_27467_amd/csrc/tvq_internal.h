@@ -70,6 +70,7 @@ struct DecodeArgs {
   int64_t cap;
   int64_t t_begin;
   const SegParams* segs;
+  const uint32_t* seg_list;  // segment indices this launch covers
   const uint32_t* sign_masks;
   const float* lut;      // float2 entries
   FastDiv div_t, div_h;
@@ -81,8 +82,18 @@ struct DecodeArgs {
   float c_d;             // fp32 rounding of 1/sqrt(d)
 };
 
+// Segments whose codes the multi-tile decode kernel handles: n = 64 or 256 (6- or 8-bit angle
+// codes, every code a valid bin) with 8-bit linear or 4-bit log-space norms.  Other formats go
+// to the single-tile generic decode kernel.
+inline bool decode_fast_format(uint32_t n, uint32_t mode, uint32_t bits) {
+  return (n == 64 || n == 256) && ((mode == 1 && bits == 8) || (mode == 2 && bits == 4));
+}
+
+constexpr uint32_t kDecodeFastTilesPerWave = 4;
+
 }  // namespace tvq
 
 // Kernel launchers (defined in the .hip kernel files).
 int tvq_launch_encode(const tvq::EncodeArgs& a, int d, int in_f32, unsigned grid, void* stream);
-int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, unsigned grid, void* stream);
+int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, unsigned grid,
+                      void* stream);

@@ -233,7 +233,8 @@ def compare_decode(s: Setup, cache_dev, lay, B, t0, t1) -> DecodeReport:
         g = np.stack([torch_to_np(ko), torch_to_np(vo)], axis=1)         # [L,2,B,H,T,d]
         if dt == torch.float32:
             rep.vectors = int(np.prod(g.shape[:-1]))
-            eq = (g.view(np.uint32) == ref32.view(np.uint32)).all(axis=-1)
+            # bit for bit, except that an exact zero may carry either sign
+            eq = ((g.view(np.uint32) == ref32.view(np.uint32)) | ((g == 0) & (ref32 == 0))).all(axis=-1)
             rep.f32_bit_mismatch_vectors = int((~eq).sum())
             # relative L2 per vector; below fp32's normal range the format's own absolute
             # resolution (2^-149 per element, a few steps through the butterfly) is added
