@@ -82,7 +82,8 @@ typedef struct {
 
 /* A strided [L][B][H][T][d] view of K and V (the same strides for both), in elements, with
  * d contiguous.  `batch` = B, `tokens` = T of this call.  Every vector must start on a 16-byte
- * boundary (base pointers and strides x element size multiples of 16).                    */
+ * boundary (base pointers and strides x element size multiples of 16).  Strides are
+ * non-negative; stride_b, stride_h and stride_t are below 2^32, and B*H*T below 2^31.     */
 typedef struct {
   int64_t batch, tokens;
   int64_t stride_l, stride_b, stride_h, stride_t;
@@ -134,7 +135,8 @@ tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, con
 /* Decode (section 3.1, reconstruction) cache slots [t_begin, t_end) of every (layer, batch,
  * head) into k_out / v_out, described by `out` (out->tokens == t_end - t_begin,
  * out->batch == lay->batch), as `out_dtype` (bf16 rounded to nearest even, or fp32).
- * Launches one kernel on `stream`; an empty range launches nothing. */
+ * Launches up to two kernels on `stream` (one for the layers whose formats have a dedicated
+ * kernel, one for the rest); an empty range launches nothing. */
 tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* lay,
                       int64_t t_begin, int64_t t_end, tvq_dtype out_dtype, void* k_out,
                       void* v_out, const tvq_tensor_desc* out, void* stream);

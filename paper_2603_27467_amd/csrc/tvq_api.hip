@@ -109,8 +109,8 @@ tvq::FastDiv make_div(uint32_t div) {
   tvq::FastDiv f;
   uint32_t l = 0;
   while ((1ull << l) < div) ++l;
-  f.s = 32 + l;
-  f.m = (uint64_t)((((unsigned __int128)1 << f.s) + div - 1) / div);
+  f.s = 31 + l;
+  f.m = (uint32_t)(((1ull << f.s) + div - 1) / div);
   f.div = div;
   return f;
 }
@@ -139,6 +139,8 @@ bool desc_valid(const tvq_codec* c, const tvq_tensor_desc* t, int elem_bytes) {
   const int64_t strides[4] = {t->stride_l, t->stride_b, t->stride_h, t->stride_t};
   for (int64_t s : strides)
     if ((s * elem_bytes) % 16 != 0) return false;
+  if (t->stride_b >= (1ll << 32) || t->stride_h >= (1ll << 32) || t->stride_t >= (1ll << 32))
+    return false;
   if (t->tokens > 1 && t->stride_t < c->d) return false;
   const int64_t vec = t->batch * c->H * t->tokens;
   if (vec >= (1ll << 31)) return false;
@@ -380,13 +382,13 @@ tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, con
   a.k = k;
   a.v = v;
   a.stride_l = in->stride_l;
-  a.stride_b = in->stride_b;
-  a.stride_h = in->stride_h;
-  a.stride_t = in->stride_t;
+  a.stride_b = (uint32_t)in->stride_b;
+  a.stride_h = (uint32_t)in->stride_h;
+  a.stride_t = (uint32_t)in->stride_t;
   a.cache = (uint8_t*)cache;
   a.n_slots = lay->batch * c->H * lay->capacity_tokens;
-  a.cap = lay->capacity_tokens;
-  a.t_begin = t_begin;
+  a.cap = (uint32_t)lay->capacity_tokens;
+  a.t_begin = (uint32_t)t_begin;
   a.segs = c->d_segs;
   a.sign_masks = c->d_sign_masks;
   a.div_t = make_div((uint32_t)in->tokens);
@@ -422,12 +424,12 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
   a.k_out = k_out;
   a.v_out = v_out;
   a.stride_l = out->stride_l;
-  a.stride_b = out->stride_b;
-  a.stride_h = out->stride_h;
-  a.stride_t = out->stride_t;
+  a.stride_b = (uint32_t)out->stride_b;
+  a.stride_h = (uint32_t)out->stride_h;
+  a.stride_t = (uint32_t)out->stride_t;
   a.n_slots = lay->batch * c->H * lay->capacity_tokens;
-  a.cap = lay->capacity_tokens;
-  a.t_begin = t_begin;
+  a.cap = (uint32_t)lay->capacity_tokens;
+  a.t_begin = (uint32_t)t_begin;
   a.segs = c->d_segs;
   a.sign_masks = c->d_sign_masks;
   a.lut = c->d_lut;

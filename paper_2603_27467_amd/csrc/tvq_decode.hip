@@ -16,21 +16,23 @@
 // The two cross-lane butterfly stages leave some lanes holding -z (exactly, up to the sign of
 // an exact zero); that sign is folded into the output sign mask.
 //
-// Two kernels, each launched over its own list of (layer, kind) segments, so that each gets
-// the register allocation its own work needs:
+// A lane computes 32 consecutive elements of a vector (d/32 lanes per vector, 64/(d/32)
+// vectors per wave, a "tile").  Two kernels, each launched over its own list of (layer, kind)
+// segments so that each gets the register allocation its own work needs:
 //   decode_fast_kernel     n = 64 or 256 with 8-bit linear or 4-bit log norms.  A wave decodes
 //                          several consecutive tiles and loads the next tile's code words while
 //                          decoding the current one: load latency otherwise dominates.  The
 //                          ladder ratio comes from a division-free Newton iteration, which keeps
 //                          library exp/log (and their fp64 constants, which a loop hoists into
-//                          registers) out of this kernel.
-//   decode_generic_kernel  every other format, one tile per wave.
-// A tile is 64/(d/32) vectors.  Each wave stages its codebook's cos/sin table in LDS (up to
-// kLdsLut entries; larger ones are read from global memory) and writes the log levels of up to
-// 4 bits of each vector into an LDS table.  LDS is only shared within a wave, so wave-scope
-// fences order its writes and reads.
+//                          registers) out of this kernel.  Outputs go through LDS so that each
+//                          store instruction writes whole 64-byte runs (1 KiB runs when the
+//                          tile's vectors are contiguous in memory): with each lane storing its
+//                          own 64 bytes, every store would touch 64 lines 16 bytes at a time.
+//   decode_generic_kernel  every other format, one tile per wave, direct stores.
+// Each wave stages its codebook's cos/sin table in LDS (larger ones are read from global
+// memory) and writes the log levels of up to 4 bits of each vector into an LDS table.  LDS is
+// only shared within a wave, so wave-scope fences order its writes and reads.
 #include <float.h>
-#include <hip/hip_bf16.h>
 #include <hip/hip_runtime.h>
 
 #include "tvq_device.h"
@@ -39,9 +41,24 @@
 namespace tvq {
 namespace {
 
-constexpr int kLdsLut = 512;                 // cos/sin entries staged per wave (4 KiB)
-constexpr int kLvlBits = 4;                  // log-norm widths up to this use the level table
-constexpr int kLvlPerWave = 32 * (1 << kLvlBits);   // vectors per wave (d=64) x levels
+constexpr int kLutGeneric = 512;   // cos/sin entries a generic-kernel wave stages in LDS (4 KiB)
+constexpr int kLutFast = 256;      // largest codebook of the multi-tile kernel (2 KiB)
+constexpr int kLvlBits = 4;        // log-norm widths up to this use the level table
+constexpr int kLvlPerWave = 32 * (1 << kLvlBits);   // vectors per wave (d = 64) x levels
+
+typedef uint32_t u32x4a __attribute__((ext_vector_type(4)));   // 16-byte aligned
+
+// Two fp32 values to a packed bf16 pair, each rounded to nearest even (one v_cvt_pk_bf16_f32;
+// element 0 in the low half).  Converting the pair as a vector keeps the compiler from
+// converting each value alone and re-packing the halves.
+__device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 p = __builtin_convertvector((f32x2){lo, hi}, bf16x2);
+  uint32_t bits;
+  __builtin_memcpy(&bits, &p, 4);
+  return bits;
+}
 
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -118,7 +135,7 @@ __device__ __forceinline__ double ladder_ratio(float lo_c, float hi_c, uint32_t 
 
 struct TilePos {
   uint32_t bh, t, b, h;
-  int64_t slot;
+  uint32_t slot;             // (b*H + h)*capacity + t_begin + t < 2^31
   bool valid;
 };
 
@@ -131,7 +148,7 @@ __device__ __forceinline__ TilePos tile_pos(const DecodeArgs& a, uint32_t j0, in
   p.t = jj - p.bh * a.div_t.div;
   p.b = fast_div(p.bh, a.div_h);
   p.h = p.bh - p.b * a.H;
-  p.slot = (int64_t)p.bh * a.cap + a.t_begin + p.t;
+  p.slot = p.bh * a.cap + a.t_begin + p.t;
   return p;
 }
 
@@ -143,17 +160,17 @@ struct WaveState {
   int lane, sub, vslot, wib;
   SegParams sp;
   const uint8_t* plane[3];
-  const float2* lut_g;
-  bool lut_in_lds;
+  const float2* lut_g;       // the codebook's table in global memory
+  float2* lut_s;             // this wave's LDS copy, or null when it does not fit
   uint32_t sm[16];           // output sign masks, with this lane's butterfly sign folded in
 };
 
 // Segment set-up common to both kernels: the wave's segment and tiles, its cos/sin table into
-// LDS, its sign masks into registers.  Returns false if the wave has no tile.
+// the wave's LDS row of `lut_cap` entries, its sign masks into registers.  Returns false if the
+// wave has no tile.
 template <int D>
-__device__ __forceinline__ bool wave_setup(const DecodeArgs& a, WaveState<D>& w,
-                                           float2 (*lut)[kLdsLut], uint32_t& tile0,
-                                           uint32_t& ntiles) {
+__device__ __forceinline__ bool wave_setup(const DecodeArgs& a, WaveState<D>& w, float2* lut_rows,
+                                           int lut_cap, uint32_t& tile0, uint32_t& ntiles) {
   constexpr int LPV = WaveState<D>::LPV;
   constexpr int VPW = WaveState<D>::VPW;
   w.lane = threadIdx.x & (kWave - 1);
@@ -171,9 +188,10 @@ __device__ __forceinline__ bool wave_setup(const DecodeArgs& a, WaveState<D>& w,
   w.sp = a.segs[a.seg_list[li]];
   for (int p = 0; p < 3; ++p) w.plane[p] = a.cache + a.n_slots * w.sp.pre[p];
   w.lut_g = (const float2*)a.lut + w.sp.lut_off;
-  w.lut_in_lds = w.sp.n <= (uint32_t)kLdsLut;
-  if (w.lut_in_lds) {
-    for (uint32_t e = w.lane; e < w.sp.n; e += kWave) lut[w.wib][e] = w.lut_g[e];
+  w.lut_s = nullptr;
+  if (w.sp.n <= (uint32_t)lut_cap) {
+    w.lut_s = lut_rows + w.wib * lut_cap;
+    for (uint32_t e = w.lane; e < w.sp.n; e += kWave) w.lut_s[e] = w.lut_g[e];
     wave_lds_sync();
   }
   load_words<16>(a.sign_masks + (size_t)w.sp.layer * (D / 2) + w.sub * 16, w.sm);
@@ -183,13 +201,13 @@ __device__ __forceinline__ bool wave_setup(const DecodeArgs& a, WaveState<D>& w,
   return true;
 }
 
-// The 2^b <= 16 log-space levels of each vector of the tile into the wave's LDS table: the
-// ladder R'min * rho^q, split over the vector's LPV lanes.  Level 0 is R'min exactly and RN32
-// brings the top level back to R'max.  Vectors with R'min == R'max get Rmin at every level.
+// The 2^b <= 16 log-space levels of each vector of the tile into the wave's LDS table `lvl`
+// (16 per vector): the ladder R'min * rho^q, split over the vector's LPV lanes.  Level 0 is
+// R'min exactly and RN32 brings the top level back to R'max.  Vectors with R'min == R'max get
+// Rmin at every level.
 template <int D>
-__device__ __forceinline__ const float* build_log_levels(const WaveState<D>& w,
-                                                         float (*lvl)[kLvlPerWave], float rmin,
-                                                         float rmax, uint32_t qlevels) {
+__device__ __forceinline__ const float* build_log_levels(const WaveState<D>& w, float* lvl,
+                                                         float rmin, float rmax, uint32_t qlevels) {
   constexpr int LPV = WaveState<D>::LPV;
   const float lo_c = fmaxf(rmin, FLT_MIN), hi_c = fmaxf(rmax, FLT_MIN);
   const bool deg = lo_c == hi_c;
@@ -200,8 +218,8 @@ __device__ __forceinline__ const float* build_log_levels(const WaveState<D>& w,
   if constexpr (LPV >= 4) pw = (sub & 2) ? pw * rho2 : pw;
   const double step = (LPV >= 4) ? rho2 * rho2 : rho2;    // rho^LPV
   double v = (double)lo_c * pw;
-  float* tab = &lvl[w.wib][w.vslot << kLvlBits];
-  wave_lds_sync();             // the previous tile's reads of the table are done
+  float* tab = lvl + (w.vslot << kLvlBits);
+  wave_lds_sync();             // earlier reads of this LDS area are done
   for (uint32_t q = sub; q <= qlevels; q += LPV) {
     tab[q] = deg ? rmin : (float)v;
     v *= step;
@@ -210,115 +228,197 @@ __device__ __forceinline__ const float* build_log_levels(const WaveState<D>& w,
   return tab;
 }
 
-// y^ = r^ (cos, sin)(2 pi k / n), x^ = D H y^, store.  LDS_LUT is a template parameter: a
-// run-time choice between the LDS and the global table makes the compiler address both through
-// flat loads, whose waits also wait for every outstanding global load.
+template <bool F32OUT>
+struct OutWords {
+  static constexpr int NW = F32OUT ? 32 : 16;   // 32-bit words a lane stores per tile
+  static constexpr int NBL = NW / 4;            // 16-byte blocks a lane stores per tile
+  static constexpr int EB = F32OUT ? 4 : 2;     // bytes per element
+  static constexpr int PITCH = NW + 4;          // LDS words per lane row: the 4-word pad puts
+                                                // the rows of 8 consecutive lanes on distinct
+                                                // banks for 16-byte accesses
+};
+
+// y^ = r^ (cos, sin)(2 pi k / n), x^ = D H y^ as the words this lane stores: 32 fp32 values or
+// 16 bf16 pairs.  LDS_LUT is a template parameter: a run-time choice between the LDS and the
+// global table makes the compiler address both through flat loads, whose waits also wait for
+// every outstanding global load.
 template <int D, bool F32OUT, bool LDS_LUT>
-__device__ __forceinline__ void reconstruct_store(const DecodeArgs& a, WaveState<D>& w,
-                                                  float2 (*lut)[kLdsLut], const TilePos& pos,
-                                                  const uint32_t (&kc)[kPairsPerLane],
-                                                  const float (&r)[kPairsPerLane]) {
+__device__ __forceinline__ void reconstruct(const DecodeArgs& a, const WaveState<D>& w,
+                                            const uint32_t (&kc)[kPairsPerLane],
+                                            const float (&r)[kPairsPerLane],
+                                            uint32_t (&o)[OutWords<F32OUT>::NW]) {
   constexpr int LPV = WaveState<D>::LPV;
+  const float2* lut = LDS_LUT ? w.lut_s : w.lut_g;
   float x[kElemsPerLane];
-  if constexpr (LDS_LUT) {
 #pragma unroll
-    for (int i = 0; i < kPairsPerLane; ++i) {
-      const float2 cs = lut[w.wib][kc[i]];
-      x[2 * i] = r[i] * cs.x;
-      x[2 * i + 1] = r[i] * cs.y;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < kPairsPerLane; ++i) {
-      const float2 cs = w.lut_g[kc[i]];
-      x[2 * i] = r[i] * cs.x;
-      x[2 * i + 1] = r[i] * cs.y;
-    }
+  for (int i = 0; i < kPairsPerLane; ++i) {
+    const float2 cs = lut[kc[i]];
+    x[2 * i] = r[i] * cs.x;
+    x[2 * i + 1] = r[i] * cs.y;
   }
   fwht_in_lane(x);
   fwht_cross_lane_signed<LPV>(x, w.sub);   // sigma * z; sigma is in the sign masks
-  if (!pos.valid) return;
-  const int64_t elem = (int64_t)w.sp.layer * a.stride_l + (int64_t)pos.b * a.stride_b +
-                       (int64_t)pos.h * a.stride_h + (int64_t)pos.t * a.stride_t +
-                       w.sub * kElemsPerLane;
-  void* dst = w.sp.kind ? a.v_out : a.k_out;
   if constexpr (F32OUT) {
-    uint32_t o[32];
 #pragma unroll
     for (int m = 0; m < 16; ++m) {
       o[2 * m] = __float_as_uint(x[2 * m] * a.c_d) ^ (w.sm[m] << 16);
       o[2 * m + 1] = __float_as_uint(x[2 * m + 1] * a.c_d) ^ (w.sm[m] & 0x80000000u);
     }
-    store_words<32>((uint32_t*)dst + elem, o);
   } else {
-    uint32_t o[16];
 #pragma unroll
-    for (int m = 0; m < 16; ++m) {
-      const __hip_bfloat162 p =
-          __float22bfloat162_rn(make_float2(x[2 * m] * a.c_d, x[2 * m + 1] * a.c_d));
-      uint32_t bits;
-      __builtin_memcpy(&bits, &p, 4);
-      o[m] = bits ^ w.sm[m];
-    }
-    store_words<16>((uint32_t*)((uint16_t*)dst + elem), o);
+    for (int m = 0; m < 16; ++m) o[m] = bf16x2_rne(x[2 * m] * a.c_d, x[2 * m + 1] * a.c_d) ^ w.sm[m];
   }
 }
 
+__device__ __forceinline__ uint64_t out_elem(const DecodeArgs& a, uint32_t layer, const TilePos& p) {
+  return (uint64_t)layer * a.stride_l + (uint64_t)p.b * a.stride_b + (uint64_t)p.h * a.stride_h +
+         (uint64_t)p.t * a.stride_t;
+}
 
-// n = 64/256 angle codes (WA = 6/8 bits) with NB = 8 linear or NB = 4 log-space norm codes:
-// the next tile's code words (WA/2 + NB/2 + 2 registers) are loaded while the current tile is
-// decoded.  Only the raw code words cross iterations; tile positions are recomputed.
-template <int D, bool F32OUT, int WA, int NB>
-__device__ void decode_tiles_prefetch(const DecodeArgs& a, WaveState<D>& w, float2 (*lut)[kLdsLut],
-                                      float (*lvl)[kLvlPerWave], uint32_t tile0, uint32_t ntiles) {
+// Each lane stores its own 32 elements.
+template <int D, bool F32OUT>
+__device__ __forceinline__ void store_direct(const DecodeArgs& a, const WaveState<D>& w,
+                                             const TilePos& pos,
+                                             const uint32_t (&o)[OutWords<F32OUT>::NW]) {
+  if (!pos.valid) return;
+  constexpr int EB = OutWords<F32OUT>::EB;
+  uint8_t* dst = (uint8_t*)(w.sp.kind ? a.v_out : a.k_out) +
+                 (out_elem(a, w.sp.layer, pos) + w.sub * kElemsPerLane) * EB;
+  store_words<OutWords<F32OUT>::NW>((uint32_t*)dst, o);
+}
+
+// The tile's words go to the wave's LDS rows (lane-major, PITCH words per lane) and come back
+// in store order.  When the tile's vectors are contiguous in memory (same (b, h), consecutive
+// tokens, stride_t == d, none past the end), store k of lane L writes 16-byte block 64 k + L of
+// the tile; otherwise it writes block k * LPV + sub of the lane's own vector.  Both orders are
+// a per-lane base plus a per-k constant, so the choice is a select, not a branch: the tile
+// loop then has the same stores on every path, and the wait for the next tile's prefetched
+// codes can leave this tile's stores in flight.  A lane past the end (its position is that of
+// the tile's first vector) stores the first vector's block again: the same bytes to the same
+// address.
+template <int D, bool F32OUT>
+__device__ __forceinline__ void store_staged(const DecodeArgs& a, const WaveState<D>& w,
+                                             const TilePos& pos,
+                                             const uint32_t (&o)[OutWords<F32OUT>::NW],
+                                             uint32_t* stg) {
+  constexpr int LPV = WaveState<D>::LPV;
   constexpr int VPW = WaveState<D>::VPW;
+  constexpr int NBL = OutWords<F32OUT>::NBL;
+  constexpr int PITCH = OutWords<F32OUT>::PITCH;
+  constexpr int EB = OutWords<F32OUT>::EB;
+  static_assert(NBL % LPV == 0 && kWave % NBL == 0, "block orders below assume these");
+  wave_lds_sync();             // earlier reads of this LDS area are done
+  uint32_t* row = stg + w.lane * PITCH;
+#pragma unroll
+  for (int q = 0; q < NBL; ++q)
+    *(u32x4a*)(row + 4 * q) = u32x4a{o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]};
+  wave_lds_sync();
+  const bool lane_ok = pos.valid && pos.t >= (uint32_t)w.vslot &&
+                       pos.t - w.vslot + VPW <= a.div_t.div;
+  const bool contig = a.stride_t == (uint32_t)D && __all(lane_ok);
+  const int vs = pos.valid ? w.vslot : 0;
+  uint8_t* vec = (uint8_t*)(w.sp.kind ? a.v_out : a.k_out) + out_elem(a, w.sp.layer, pos) * EB;
+  // contiguous: block 64 k + L is word (64 k + L) % NBL * 4 of lane (64 k + L) / NBL;
+  // per vector: block k LPV + sub is word ((k LPV) % NBL + sub) * 4 of lane
+  // vs LPV + k LPV / NBL
+  const uint32_t lds0 = contig ? (w.lane / NBL) * PITCH + (w.lane % NBL) * 4
+                               : vs * LPV * PITCH + w.sub * 4;
+  uint8_t* dst0 = contig ? vec - (size_t)w.vslot * D * EB + w.lane * 16 : vec + w.sub * 16;
+  const size_t dst_step = contig ? kWave * 16 : LPV * 16;
+#pragma unroll
+  for (int k = 0; k < NBL; ++k) {
+    const uint32_t off = contig ? k * (kWave / NBL) * PITCH
+                                : (k * LPV / NBL) * PITCH + ((k * LPV) % NBL) * 4;
+    *(u32x4a*)(dst0 + k * dst_step) = *(const u32x4a*)(stg + lds0 + off);
+  }
+}
+
+// Raw code words of one tile for n = 64/256 angle codes (WA = 6/8 bits) and NB = 8 linear or
+// NB = 4 log-space norm codes: WA/2 + NB/2 + 2 registers.
+template <int WA, int NB>
+struct TileCodes {
+  Chunk<WA> ang;
+  Chunk<NB> nrm;
+  u32x2 hdr;
+};
+
+template <int D, int WA, int NB>
+__device__ __forceinline__ TileCodes<WA, NB> load_tile_codes(const DecodeArgs& a,
+                                                              const WaveState<D>& w, uint32_t tile) {
+  const TilePos p = tile_pos(a, tile * WaveState<D>::VPW, w.vslot);
+  TileCodes<WA, NB> c;
+  c.ang = load_chunk<WA>(w.plane[0] + (uint64_t)p.slot * w.sp.rec[0] + 2 * WA * w.sub);
+  c.nrm = load_chunk<NB>(w.plane[1] + (uint64_t)p.slot * w.sp.rec[1] + 2 * NB * w.sub);
+  c.hdr = *(const u32x2*)(w.plane[2] + (uint64_t)p.slot * 8);
+  return c;
+}
+
+template <int D, bool F32OUT, int WA, int NB>
+__device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState<D>& w,
+                                            uint32_t* stg, const TileCodes<WA, NB>& c,
+                                            uint32_t tile) {
   constexpr uint32_t kLevels = (1u << NB) - 1u;
-  const TilePos p0 = tile_pos(a, tile0 * VPW, w.vslot);
-  Chunk<WA> ang = load_chunk<WA>(w.plane[0] + p0.slot * w.sp.rec[0] + 2 * WA * w.sub);
-  Chunk<NB> nrm = load_chunk<NB>(w.plane[1] + p0.slot * w.sp.rec[1] + 2 * NB * w.sub);
-  u32x2 hb = *(const u32x2*)(w.plane[2] + p0.slot * 8);
-  for (uint32_t it = 0; it < ntiles; ++it) {
-    uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
-    unpack16<WA>(ang, kc);
-    unpack16<NB>(nrm, qc);
-    const float rmin = __uint_as_float(hb.x), rmax = __uint_as_float(hb.y);
-    if (it + 1 < ntiles) {
-      const TilePos np = tile_pos(a, (tile0 + it + 1) * VPW, w.vslot);
-      ang = load_chunk<WA>(w.plane[0] + np.slot * w.sp.rec[0] + 2 * WA * w.sub);
-      nrm = load_chunk<NB>(w.plane[1] + np.slot * w.sp.rec[1] + 2 * NB * w.sub);
-      hb = *(const u32x2*)(w.plane[2] + np.slot * 8);
-    }
-    float r[kPairsPerLane];
-    if constexpr (NB == 8) {
-      const float step = (rmax - rmin) / (float)kLevels;
-      const bool deg = rmax == rmin;
+  uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
+  unpack16<WA>(c.ang, kc);
+  unpack16<NB>(c.nrm, qc);
+  const float rmin = __uint_as_float(c.hdr.x), rmax = __uint_as_float(c.hdr.y);
+  float r[kPairsPerLane];
+  if constexpr (NB == 8) {
+    // R^max == R^min (also both infinite) decodes to R^min: q * 0 + R^min
+    const float step = rmax == rmin ? 0.0f : (rmax - rmin) / (float)kLevels;
 #pragma unroll
-      for (int i = 0; i < kPairsPerLane; ++i)
-        r[i] = deg ? rmin : __builtin_fmaf((float)qc[i], step, rmin);
-    } else {
-      const float* tab = build_log_levels<D>(w, lvl, rmin, rmax, kLevels);
+    for (int i = 0; i < kPairsPerLane; ++i) r[i] = __builtin_fmaf((float)qc[i], step, rmin);
+  } else {
+    const float* tab = build_log_levels<D>(w, (float*)stg, rmin, rmax, kLevels);
 #pragma unroll
-      for (int i = 0; i < kPairsPerLane; ++i) r[i] = tab[qc[i]];
-    }
-    reconstruct_store<D, F32OUT, true>(a, w, lut, tile_pos(a, (tile0 + it) * VPW, w.vslot), kc, r);
+    for (int i = 0; i < kPairsPerLane; ++i) r[i] = tab[qc[i]];
+  }
+  uint32_t o[OutWords<F32OUT>::NW];
+  reconstruct<D, F32OUT, true>(a, w, kc, r, o);
+  store_staged<D, F32OUT>(a, w, tile_pos(a, tile * WaveState<D>::VPW, w.vslot), o, stg);
+}
+
+// Tiles tile0 .. tile0 + ntiles - 1, two per iteration from two code buffers: each tile's
+// codes are loaded while the tile before it is decoded.  Tile indices are clamped to the last
+// tile, so an odd count decodes the last tile twice (the same bytes to the same addresses) and
+// the loads past the end read lines already in cache; in exchange the loop has no branch
+// around a load or a store, and nothing has to wait for a load before its data is used.
+template <int D, bool F32OUT, int WA, int NB>
+__device__ void decode_tiles_prefetch(const DecodeArgs& a, const WaveState<D>& w, uint32_t* stg,
+                                      uint32_t tile0, uint32_t ntiles) {
+  const uint32_t last = tile0 + ntiles - 1;
+  TileCodes<WA, NB> ca = load_tile_codes<D, WA, NB>(a, w, tile0);
+  if (ntiles == 1) {
+    decode_tile<D, F32OUT>(a, w, stg, ca, tile0);
+    return;
+  }
+  for (uint32_t t = tile0; t <= last; t += 2) {
+    const uint32_t t1 = min(t + 1, last);
+    const TileCodes<WA, NB> cb = load_tile_codes<D, WA, NB>(a, w, t1);
+    decode_tile<D, F32OUT>(a, w, stg, ca, t);
+    ca = load_tile_codes<D, WA, NB>(a, w, min(t + 2, last));
+    decode_tile<D, F32OUT>(a, w, stg, cb, t1);
   }
 }
 
 template <int D, bool F32OUT>
 __global__ __launch_bounds__(kBlockThreads) void decode_fast_kernel(DecodeArgs a) {
-  __shared__ float2 s_lut[kWavesPerBlock][kLdsLut];
-  __shared__ float s_lvl[kWavesPerBlock][kLvlPerWave];
+  constexpr int kStageWords = kWave * OutWords<F32OUT>::PITCH;
+  static_assert(kStageWords >= kLvlPerWave, "the level table shares the staging area");
+  __shared__ float2 s_lut[kWavesPerBlock * kLutFast];
+  __shared__ __attribute__((aligned(16))) uint32_t s_stg[kWavesPerBlock][kStageWords];
   WaveState<D> w;
   uint32_t tile0, ntiles;
-  if (!wave_setup<D>(a, w, s_lut, tile0, ntiles)) return;
+  if (!wave_setup<D>(a, w, s_lut, kLutFast, tile0, ntiles)) return;
   // every codebook of this kernel (n <= 256) is in LDS
+  uint32_t* stg = s_stg[w.wib];
   const bool wide = w.sp.w == 8;
   if (w.sp.mode == 1) {
-    if (wide) decode_tiles_prefetch<D, F32OUT, 8, 8>(a, w, s_lut, s_lvl, tile0, ntiles);
-    else decode_tiles_prefetch<D, F32OUT, 6, 8>(a, w, s_lut, s_lvl, tile0, ntiles);
+    if (wide) decode_tiles_prefetch<D, F32OUT, 8, 8>(a, w, stg, tile0, ntiles);
+    else decode_tiles_prefetch<D, F32OUT, 6, 8>(a, w, stg, tile0, ntiles);
   } else {
-    if (wide) decode_tiles_prefetch<D, F32OUT, 8, 4>(a, w, s_lut, s_lvl, tile0, ntiles);
-    else decode_tiles_prefetch<D, F32OUT, 6, 4>(a, w, s_lut, s_lvl, tile0, ntiles);
+    if (wide) decode_tiles_prefetch<D, F32OUT, 8, 4>(a, w, stg, tile0, ntiles);
+    else decode_tiles_prefetch<D, F32OUT, 6, 4>(a, w, stg, tile0, ntiles);
   }
 }
 
@@ -326,14 +426,14 @@ __global__ __launch_bounds__(kBlockThreads) void decode_fast_kernel(DecodeArgs a
 template <int D, bool F32OUT>
 __global__ __launch_bounds__(kBlockThreads) void decode_generic_kernel(DecodeArgs a) {
   constexpr int VPW = WaveState<D>::VPW;
-  __shared__ float2 s_lut[kWavesPerBlock][kLdsLut];
+  __shared__ float2 s_lut[kWavesPerBlock * kLutGeneric];
   __shared__ float s_lvl[kWavesPerBlock][kLvlPerWave];
   WaveState<D> w;
   uint32_t tile0, ntiles;
-  if (!wave_setup<D>(a, w, s_lut, tile0, ntiles)) return;
+  if (!wave_setup<D>(a, w, s_lut, kLutGeneric, tile0, ntiles)) return;
   const TilePos pos = tile_pos(a, tile0 * VPW, w.vslot);
   uint32_t kc[kPairsPerLane];
-  load_codes_any(w.plane[0] + pos.slot * w.sp.rec[0], w.sub, w.sp.w, kc);
+  load_codes_any(w.plane[0] + (uint64_t)pos.slot * w.sp.rec[0], w.sub, w.sp.w, kc);
   if (!w.sp.mask) {
     const uint32_t kclamp = w.sp.n - 1u;   // codes of a corrupted cache stay inside the table
 #pragma unroll
@@ -342,23 +442,21 @@ __global__ __launch_bounds__(kBlockThreads) void decode_generic_kernel(DecodeArg
   float r[kPairsPerLane];
   if (w.sp.mode == 0) {
     uint32_t raw[kPairsPerLane];
-    load_words<16>((const uint32_t*)(w.plane[1] + pos.slot * w.sp.rec[1]) + 16 * w.sub, raw);
+    load_words<16>((const uint32_t*)(w.plane[1] + (uint64_t)pos.slot * w.sp.rec[1]) + 16 * w.sub, raw);
 #pragma unroll
     for (int i = 0; i < kPairsPerLane; ++i) r[i] = __uint_as_float(raw[i]);
   } else {
     uint32_t qc[kPairsPerLane];
-    load_codes_any(w.plane[1] + pos.slot * w.sp.rec[1], w.sub, w.sp.bits, qc);
-    const u32x2 hb = *(const u32x2*)(w.plane[2] + pos.slot * 8);
+    load_codes_any(w.plane[1] + (uint64_t)pos.slot * w.sp.rec[1], w.sub, w.sp.bits, qc);
+    const u32x2 hb = *(const u32x2*)(w.plane[2] + (uint64_t)pos.slot * 8);
     const float rmin = __uint_as_float(hb.x), rmax = __uint_as_float(hb.y);
     const uint32_t qlevels = (1u << w.sp.bits) - 1u;
     if (w.sp.mode == 1) {
-      const float step = (rmax - rmin) / (float)qlevels;
-      const bool deg = rmax == rmin;
+      const float step = rmax == rmin ? 0.0f : (rmax - rmin) / (float)qlevels;
 #pragma unroll
-      for (int i = 0; i < kPairsPerLane; ++i)
-        r[i] = deg ? rmin : __builtin_fmaf((float)qc[i], step, rmin);
+      for (int i = 0; i < kPairsPerLane; ++i) r[i] = __builtin_fmaf((float)qc[i], step, rmin);
     } else if (w.sp.bits <= (uint32_t)kLvlBits) {
-      const float* tab = build_log_levels<D>(w, s_lvl, rmin, rmax, qlevels);
+      const float* tab = build_log_levels<D>(w, s_lvl[w.wib], rmin, rmax, qlevels);
 #pragma unroll
       for (int i = 0; i < kPairsPerLane; ++i) r[i] = tab[qc[i]];
     } else {
@@ -378,8 +476,10 @@ __global__ __launch_bounds__(kBlockThreads) void decode_generic_kernel(DecodeArg
       }
     }
   }
-  if (w.lut_in_lds) reconstruct_store<D, F32OUT, true>(a, w, s_lut, pos, kc, r);
-  else reconstruct_store<D, F32OUT, false>(a, w, s_lut, pos, kc, r);
+  uint32_t o[OutWords<F32OUT>::NW];
+  if (w.lut_s) reconstruct<D, F32OUT, true>(a, w, kc, r, o);
+  else reconstruct<D, F32OUT, false>(a, w, kc, r, o);
+  store_direct<D, F32OUT>(a, w, pos, o);
 }
 
 }  // namespace
@@ -389,10 +489,10 @@ int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, u
                       void* stream) {
   hipStream_t s = (hipStream_t)stream;
   const dim3 block(tvq::kBlockThreads);
-#define TVQ_LAUNCH_DEC(KERNEL, D)                                                      \
-  do {                                                                                 \
-    if (out_f32) hipLaunchKernelGGL((tvq::KERNEL<D, true>), dim3(grid), block, 0, s, a); \
-    else hipLaunchKernelGGL((tvq::KERNEL<D, false>), dim3(grid), block, 0, s, a);       \
+#define TVQ_LAUNCH_DEC(KERNEL, D)                                                        \
+  do {                                                                                   \
+    if (out_f32) hipLaunchKernelGGL((tvq::KERNEL<D, true>), dim3(grid), block, 0, s, a);  \
+    else hipLaunchKernelGGL((tvq::KERNEL<D, false>), dim3(grid), block, 0, s, a);         \
   } while (0)
   if (d == 128) {
     if (fast) TVQ_LAUNCH_DEC(decode_fast_kernel, 128);

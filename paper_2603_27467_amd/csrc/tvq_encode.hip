@@ -191,9 +191,9 @@ __global__ __launch_bounds__(kBlockThreads) void encode_kernel(EncodeArgs a) {
   const uint32_t j0 = wseg * VPW;
   if (j0 >= a.nvec) return;
   const TilePos pos = tile_pos(a, j0, vslot);
-  const Raw<F32IN> raw = load_raw<F32IN>(src, layer_off + (int64_t)pos.b * a.stride_b +
-                                               (int64_t)pos.h * a.stride_h +
-                                               (int64_t)pos.t * a.stride_t);
+  const Raw<F32IN> raw = load_raw<F32IN>(src, layer_off + (uint64_t)pos.b * a.stride_b +
+                                               (uint64_t)pos.h * a.stride_h +
+                                               (uint64_t)pos.t * a.stride_t);
   {
     // ---- sign flip (sign-bit XOR, exact), widen to fp32 ----
     float x[kElemsPerLane];
@@ -257,8 +257,8 @@ __global__ __launch_bounds__(kBlockThreads) void encode_kernel(EncodeArgs a) {
                                    sp.n);
     }
 
-    const int64_t slot = (int64_t)pos.bh * a.cap + a.t_begin + pos.t;
-    if (pos.valid) store_codes_any(plane_ang + slot * sp.rec[0], sub, sp.w, kc);
+    const uint32_t slot = pos.bh * a.cap + a.t_begin + pos.t;   // < B*H*capacity < 2^31
+    if (pos.valid) store_codes_any(plane_ang + (uint64_t)slot * sp.rec[0], sub, sp.w, kc);
 
     // ---- norms ----
     if (sp.mode == 0) {
@@ -267,7 +267,7 @@ __global__ __launch_bounds__(kBlockThreads) void encode_kernel(EncodeArgs a) {
 #pragma unroll
       for (int i = 0; i < kPairsPerLane; ++i)
         rn[i] = __float_as_uint((float)pair_norm_f64(x[2 * i], x[2 * i + 1], inv_sqrt_d));
-      if (pos.valid) store_words<16>((uint32_t*)(plane_nrm + slot * sp.rec[1]) + 16 * sub, rn);
+      if (pos.valid) store_words<16>((uint32_t*)(plane_nrm + (uint64_t)slot * sp.rec[1]) + 16 * sub, rn);
     } else {
       // qc: bits of t + 1.5*2^23, t the code coordinate of each pair (eq. (2) or its log
       // variant); t stays within [-eps, 2^b - 1 + eps], so the low b bits are the code
@@ -328,8 +328,8 @@ __global__ __launch_bounds__(kBlockThreads) void encode_kernel(EncodeArgs a) {
         }
       }
       if (pos.valid) {
-        store_codes_any(plane_nrm + slot * sp.rec[1], sub, sp.bits, qc);
-        if (sub == 0) *(u32x2*)(plane_hdr + slot * 8) = u32x2{__float_as_uint(rmin),
+        store_codes_any(plane_nrm + (uint64_t)slot * sp.rec[1], sub, sp.bits, qc);
+        if (sub == 0) *(u32x2*)(plane_hdr + (uint64_t)slot * 8) = u32x2{__float_as_uint(rmin),
                                                               __float_as_uint(rmax)};
       }
     }

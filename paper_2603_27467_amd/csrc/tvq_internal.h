@@ -34,10 +34,12 @@ struct SegParams {
   uint64_t pre[3];     // record-byte prefix of the three planes
 };
 
-// Unsigned division by a runtime constant for numerators below 2^31:
-// q = (x * m) >> s with m = ceil(2^s / div), s = 32 + ceil(log2 div).
+// Unsigned division by a runtime constant for numerators x below 2^31:
+// q = (x * m) >> s with s = 31 + ceil(log2 div) and m = ceil(2^s / div) < 2^32.  With
+// e = m * div - 2^s < div <= 2^(s-31), x * e < 2^s, so the product never reaches the next
+// multiple of 2^s and q = floor(x / div).
 struct FastDiv {
-  uint64_t m;
+  uint32_t m;
   uint32_t s;
   uint32_t div;
 };
@@ -45,11 +47,12 @@ struct FastDiv {
 struct EncodeArgs {
   const void* k;
   const void* v;
-  int64_t stride_l, stride_b, stride_h, stride_t;  // elements
+  int64_t stride_l;                      // elements
+  uint32_t stride_b, stride_h, stride_t;  // elements, below 2^32
   uint8_t* cache;
-  int64_t n_slots;      // B * H * capacity
-  int64_t cap;          // capacity tokens
-  int64_t t_begin;
+  int64_t n_slots;      // B * H * capacity, below 2^31
+  uint32_t cap;         // capacity tokens
+  uint32_t t_begin;
   const SegParams* segs;
   const uint32_t* sign_masks;
   FastDiv div_t, div_h;  // by T (tokens in the call) and by H
@@ -65,10 +68,11 @@ struct DecodeArgs {
   const uint8_t* cache;
   void* k_out;
   void* v_out;
-  int64_t stride_l, stride_b, stride_h, stride_t;  // elements of the output view
-  int64_t n_slots;
-  int64_t cap;
-  int64_t t_begin;
+  int64_t stride_l;                      // elements of the output view
+  uint32_t stride_b, stride_h, stride_t;  // elements, below 2^32
+  int64_t n_slots;      // below 2^31
+  uint32_t cap;
+  uint32_t t_begin;
   const SegParams* segs;
   const uint32_t* seg_list;  // segment indices this launch covers
   const uint32_t* sign_masks;

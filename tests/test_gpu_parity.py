@@ -241,6 +241,53 @@ def test_api_errors_with_live_codec(gpu):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("d,L,B,T", [(128, 4, 1, 8197), (64, 2, 2, 8197)])
+def test_multi_tile_decode_ragged(gpu, d, L, B, T):
+    """Shapes large enough that the decode gives each wave 4 (d=128) or 2 (d=64) tiles of the
+    common formats (n = 64/256 with 8-bit linear K and 4-bit log V norms), with T = 8197 so
+    that the last tile of every (layer, kind) is ragged, the last wave of a segment gets fewer
+    tiles (3 at d=128, 1 at d=64) and tiles both stay within and cross (batch, head) rows.
+    Every vector of the last tiles of each segment and 600 random ones, decoded to fp32 and
+    bf16, against the oracle's decode of the same cache bytes; every output element written."""
+    import torch
+    w = workloads.get("C2")
+    table = [LayerCfg(64, 64), LayerCfg(256, 256), LayerCfg(64, 256), LayerCfg(256, 64)][:L]
+    s = Setup(L, 8, d, table, workloads.sign_table(11, L, d)).build()
+    k, v = _draw(w, L, B, 8, T, d, "bf16", 12)
+    lay = s.gpu.layout(B, T)
+    cache = torch.zeros((lay.total_bytes,), dtype=torch.uint8, device="cuda")
+    s.gpu.encode(bf16_bits_to_torch(k).cuda(), bf16_bits_to_torch(v).cuda(), cache, lay)
+    outs = {}
+    for dt in (torch.float32, torch.bfloat16):
+        ko = torch.full((L, B, 8, T, d), float("nan"), dtype=dt, device="cuda")
+        vo = torch.full_like(ko, float("nan"))
+        s.gpu.decode(cache, lay, 0, T, ko, vo)
+        torch.cuda.synchronize()
+        assert torch.isfinite(ko.float()).all() and torch.isfinite(vo.float()).all()
+        outs[dt] = (torch_to_np(ko), torch_to_np(vo))
+    host = torch_to_np(cache)
+    nvec = B * 8 * T
+    vpw = 64 // (d // 32)
+    tail = range(max(0, (nvec - 1) // vpw - 2) * vpw, nvec)     # the last three tiles
+    rng = np.random.default_rng(1)
+    picks = [(l, kind, j) for l in range(L) for kind in range(2) for j in tail]
+    picks += [(int(rng.integers(0, L)), int(rng.integers(0, 2)), int(rng.integers(0, nvec)))
+              for _ in range(600)]
+    bad32 = bad16 = 0
+    for l, kind, j in picks:
+        bh, t = divmod(j, T)
+        b, h = divmod(bh, 8)
+        kg, qg, rn, hg = s.orc.read_vector(host, B, T, l, kind, b, h, t)
+        ref = oracle.decode_vector(s.orc.kinds[2 * l + kind], s.signs[l], kg, qg, rn, hg, "f32")
+        g32 = outs[torch.float32][kind][l, b, h, t]
+        g16 = outs[torch.bfloat16][kind][l, b, h, t]
+        bad32 += int(np.any((g32.view(np.uint32) != ref.view(np.uint32)) & ~((g32 == 0) & (ref == 0))))
+        bad16 += int(np.any(oracle.f32_to_bf16(ref) != g16))
+    _say(f"[multi-tile d={d}] {len(picks)} vectors: fp32 mismatching vectors {bad32}, "
+         f"bf16 mismatching vectors {bad16}")
+    assert bad32 == 0 and bad16 == 0
+
+
 # ---------------------------------------------------------------------------- full size
 def test_mistral_cache_full_size_sampled(gpu):
     """The full Mistral-7B-shaped cache (32 layers, 8 heads, 4096 tokens, d=128, bf16) in the
