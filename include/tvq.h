@@ -127,7 +127,8 @@ tvq_status tvq_cache_layout(const tvq_codec* c, int64_t batch, int64_t capacity_
  * elements, into cache slots [t_begin, t_begin + in->tokens) of every (layer, batch, head).
  * Requires in->batch == lay->batch and t_begin + in->tokens <= lay->capacity_tokens.
  * k, v: device pointers; cache: device pointer to lay->total_bytes bytes.
- * Launches one kernel on `stream`; in->tokens == 0 launches nothing. */
+ * Launches up to two kernels on `stream` (one for bf16 input of the layers whose formats have a
+ * dedicated kernel, one for the rest); in->tokens == 0 launches nothing. */
 tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, const void* v,
                       const tvq_tensor_desc* in, int64_t t_begin, void* cache,
                       const tvq_layout* lay, void* stream);

@@ -24,7 +24,7 @@ struct tvq_codec {
   tvq::SegParams* d_segs = nullptr;
   uint32_t* d_sign_masks = nullptr;
   float* d_lut = nullptr;
-  uint32_t* d_seg_lists = nullptr;           // decode-fast segment ids, then the others
+  uint32_t* d_seg_lists = nullptr;           // fast-format segment ids, then the others
   uint32_t n_fast = 0, n_generic = 0;
 };
 
@@ -314,10 +314,10 @@ tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out) {
   // segment lists of the two decode kernels
   std::vector<uint32_t> lists;
   for (uint32_t i = 0; i < c->segs.size(); ++i)
-    if (tvq::decode_fast_format(c->segs[i].n, c->segs[i].mode, c->segs[i].bits)) lists.push_back(i);
+    if (tvq::fast_format(c->segs[i].n, c->segs[i].mode, c->segs[i].bits)) lists.push_back(i);
   c->n_fast = (uint32_t)lists.size();
   for (uint32_t i = 0; i < c->segs.size(); ++i)
-    if (!tvq::decode_fast_format(c->segs[i].n, c->segs[i].mode, c->segs[i].bits)) lists.push_back(i);
+    if (!tvq::fast_format(c->segs[i].n, c->segs[i].mode, c->segs[i].bits)) lists.push_back(i);
   c->n_generic = (uint32_t)lists.size() - c->n_fast;
   const size_t list_bytes = lists.size() * sizeof(uint32_t);
   const size_t seg_bytes = c->segs.size() * sizeof(tvq::SegParams);
@@ -395,13 +395,26 @@ tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, con
   a.div_h = make_div((uint32_t)c->H);
   a.H = (uint32_t)c->H;
   a.nvec = (uint32_t)(in->batch * c->H * in->tokens);
-  a.num_segs = (uint32_t)(2 * c->L);
   a.inv_d = 1.0f / (float)c->d;
   const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
-  const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave, 1);
-  const int rc = tvq_launch_encode(a, c->d, in_dtype == TVQ_F32, grid, stream);
-  if (rc == -1) return TVQ_ERR_UNSUPPORTED;
-  return rc == 0 ? TVQ_OK : TVQ_ERR_HIP;
+  // bf16 input of the common formats goes to the multi-tile kernel, the rest to the generic
+  // one (the segment list holds the common formats first, so all of it is every segment)
+  const bool f32 = in_dtype == TVQ_F32;
+  const uint32_t n_fast = f32 ? 0u : c->n_fast;
+  const struct { uint32_t first, count, tpw; bool fast; } launches[2] = {
+      {0, n_fast, tvq::kFastTilesPerWave, true},
+      {n_fast, c->n_fast + c->n_generic - n_fast, 1, false}};
+  for (const auto& l : launches) {
+    if (l.count == 0) continue;
+    a.seg_list = c->d_seg_lists + l.first;
+    a.num_segs = l.count;
+    const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave,
+                                    l.tpw);
+    const int rc = tvq_launch_encode(a, c->d, f32, l.fast, grid, stream);
+    if (rc == -1) return TVQ_ERR_UNSUPPORTED;
+    if (rc != 0) return TVQ_ERR_HIP;
+  }
+  return TVQ_OK;
 }
 
 tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* lay,
@@ -441,7 +454,7 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
   const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
   // the common formats go to the multi-tile kernel, the rest to the generic one
   const struct { uint32_t first, count, tpw; bool fast; } launches[2] = {
-      {0, c->n_fast, tvq::kDecodeFastTilesPerWave, true},
+      {0, c->n_fast, tvq::kFastTilesPerWave, true},
       {c->n_fast, c->n_generic, 1, false}};
   for (const auto& l : launches) {
     if (l.count == 0) continue;

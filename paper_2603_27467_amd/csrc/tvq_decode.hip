@@ -46,7 +46,6 @@ constexpr int kLutFast = 256;      // largest codebook of the multi-tile kernel 
 constexpr int kLvlBits = 4;        // log-norm widths up to this use the level table
 constexpr int kLvlPerWave = 32 * (1 << kLvlBits);   // vectors per wave (d = 64) x levels
 
-typedef uint32_t u32x4a __attribute__((ext_vector_type(4)));   // 16-byte aligned
 
 // Two fp32 values to a packed bf16 pair, each rounded to nearest even (one v_cvt_pk_bf16_f32;
 // element 0 in the low half).  Converting the pair as a vector keeps the compiler from
@@ -60,11 +59,6 @@ __device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi) {
   return bits;
 }
 
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
 
 template <int W>
 __device__ __forceinline__ void load_codes(const uint8_t* rec, int sub, uint32_t (&c)[kPairsPerLane]) {
@@ -378,17 +372,19 @@ __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState
   store_staged<D, F32OUT>(a, w, tile_pos(a, tile * WaveState<D>::VPW, w.vslot), o, stg);
 }
 
-// Tiles tile0 .. tile0 + ntiles - 1, two per iteration from two code buffers: each tile's
-// codes are loaded while the tile before it is decoded.  Tile indices are clamped to the last
-// tile, so an odd count decodes the last tile twice (the same bytes to the same addresses) and
-// the loads past the end read lines already in cache; in exchange the loop has no branch
-// around a load or a store, and nothing has to wait for a load before its data is used.
-template <int D, bool F32OUT, int WA, int NB>
+// Tiles tile0 .. tile0 + ntiles - 1.  MULTI: two per iteration from two code buffers, each
+// tile's codes loaded while the tile before it is decoded.  Tile indices are clamped to the
+// last tile, so an odd count decodes the last tile twice (the same bytes to the same
+// addresses) and the loads past the end read lines already in cache; in exchange the loop
+// has no branch around a load or a store, and nothing has to wait for a load before its data
+// is used.  Launches of one tile per wave use the instantiation without the loop (a separate
+// copy of the tile code inside the same kernel would raise its register count).
+template <int D, bool F32OUT, bool MULTI, int WA, int NB>
 __device__ void decode_tiles_prefetch(const DecodeArgs& a, const WaveState<D>& w, uint32_t* stg,
                                       uint32_t tile0, uint32_t ntiles) {
   const uint32_t last = tile0 + ntiles - 1;
   TileCodes<WA, NB> ca = load_tile_codes<D, WA, NB>(a, w, tile0);
-  if (ntiles == 1) {
+  if constexpr (!MULTI) {
     decode_tile<D, F32OUT>(a, w, stg, ca, tile0);
     return;
   }
@@ -401,7 +397,7 @@ __device__ void decode_tiles_prefetch(const DecodeArgs& a, const WaveState<D>& w
   }
 }
 
-template <int D, bool F32OUT>
+template <int D, bool F32OUT, bool MULTI>
 __global__ __launch_bounds__(kBlockThreads) void decode_fast_kernel(DecodeArgs a) {
   constexpr int kStageWords = kWave * OutWords<F32OUT>::PITCH;
   static_assert(kStageWords >= kLvlPerWave, "the level table shares the staging area");
@@ -414,11 +410,11 @@ __global__ __launch_bounds__(kBlockThreads) void decode_fast_kernel(DecodeArgs a
   uint32_t* stg = s_stg[w.wib];
   const bool wide = w.sp.w == 8;
   if (w.sp.mode == 1) {
-    if (wide) decode_tiles_prefetch<D, F32OUT, 8, 8>(a, w, stg, tile0, ntiles);
-    else decode_tiles_prefetch<D, F32OUT, 6, 8>(a, w, stg, tile0, ntiles);
+    if (wide) decode_tiles_prefetch<D, F32OUT, MULTI, 8, 8>(a, w, stg, tile0, ntiles);
+    else decode_tiles_prefetch<D, F32OUT, MULTI, 6, 8>(a, w, stg, tile0, ntiles);
   } else {
-    if (wide) decode_tiles_prefetch<D, F32OUT, 8, 4>(a, w, stg, tile0, ntiles);
-    else decode_tiles_prefetch<D, F32OUT, 6, 4>(a, w, stg, tile0, ntiles);
+    if (wide) decode_tiles_prefetch<D, F32OUT, MULTI, 8, 4>(a, w, stg, tile0, ntiles);
+    else decode_tiles_prefetch<D, F32OUT, MULTI, 6, 4>(a, w, stg, tile0, ntiles);
   }
 }
 
@@ -489,17 +485,22 @@ int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, u
                       void* stream) {
   hipStream_t s = (hipStream_t)stream;
   const dim3 block(tvq::kBlockThreads);
-#define TVQ_LAUNCH_DEC(KERNEL, D)                                                        \
-  do {                                                                                   \
-    if (out_f32) hipLaunchKernelGGL((tvq::KERNEL<D, true>), dim3(grid), block, 0, s, a);  \
-    else hipLaunchKernelGGL((tvq::KERNEL<D, false>), dim3(grid), block, 0, s, a);         \
+  const bool multi = a.tiles_per_wave > 1;
+#define TVQ_LAUNCH_DEC(D, F32)                                                                  \
+  do {                                                                                          \
+    if (fast && multi)                                                                          \
+      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true>), dim3(grid), block, 0, s, a);  \
+    else if (fast)                                                                              \
+      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, false>), dim3(grid), block, 0, s, a); \
+    else                                                                                        \
+      hipLaunchKernelGGL((tvq::decode_generic_kernel<D, F32>), dim3(grid), block, 0, s, a);     \
   } while (0)
   if (d == 128) {
-    if (fast) TVQ_LAUNCH_DEC(decode_fast_kernel, 128);
-    else TVQ_LAUNCH_DEC(decode_generic_kernel, 128);
+    if (out_f32) TVQ_LAUNCH_DEC(128, true);
+    else TVQ_LAUNCH_DEC(128, false);
   } else if (d == 64) {
-    if (fast) TVQ_LAUNCH_DEC(decode_fast_kernel, 64);
-    else TVQ_LAUNCH_DEC(decode_generic_kernel, 64);
+    if (out_f32) TVQ_LAUNCH_DEC(64, true);
+    else TVQ_LAUNCH_DEC(64, false);
   } else {
     return -1;
   }

@@ -19,6 +19,16 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2), aligned(4)));
 typedef uint32_t u32x3 __attribute__((ext_vector_type(3), aligned(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4), aligned(4)));
 
+typedef uint32_t u32x4a __attribute__((ext_vector_type(4)));   // 16-byte aligned
+
+// Order this wave's LDS writes before its later LDS reads by other lanes (LDS here is only
+// ever shared within one wave).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 __device__ __forceinline__ uint32_t fast_div(uint32_t x, const FastDiv& d) {
   return (uint32_t)(((uint64_t)x * d.m) >> d.s);
 }

@@ -1,20 +1,27 @@
-// tvq_encode.hip -- TurboAngle encode kernel for gfx950.
+// tvq_encode.hip -- TurboAngle encode kernels for gfx950.
 //
 // Per vector (Algorithm 1 and section 3.3 of the paper): sign flip by D, unnormalized
 // Walsh-Hadamard butterfly (the 1/sqrt(d) factor of H only scales the norms), polar form of
 // consecutive pairs, uniform angle bins, per-vector min-max norm codes, bit-packing.
 //
-// Work split: a wave takes one tile of 64/(d/32) consecutive vectors of one (layer, kind)
-// segment.  Memory latency is hidden by occupancy (4 waves per SIMD at this register count);
-// a loop over several tiles per wave would hoist loop invariants into ~40 more registers.
-// No LDS, no barriers: every wave is independent.
+// A lane computes 32 consecutive elements of a vector (d/32 lanes per vector, 64/(d/32)
+// vectors per wave, a "tile").  No LDS, no barriers: every wave is independent.  Two kernels,
+// each launched over its own list of (layer, kind) segments:
+//   encode_fast_kernel     bf16 input, n = 64 or 256 with 8-bit linear or 4-bit log norms,
+//                          every format constant known at compile time.  A wave encodes
+//                          several consecutive tiles, loading the next tile's input while it
+//                          encodes the current one, and amortizes its set-up over them.
+//   encode_generic_kernel  every other format and fp32 input, one tile per wave.
 //
-// The kernel is bound by VALU issue, so the per-pair path is kept branch-free and short:
+// The kernels are bound by VALU issue, so the per-pair path is kept branch-free and short:
 // codes are rounded by the 1.5*2^23 shift and handed to the packer as raw float bits, whose
 // low bits are the code (the packer masks them to the code width, which is the "mod n" for n
 // a power of two).  The two cross-lane butterfly stages take one instruction per element and
 // leave some lanes holding the negated transform; for the angle that is a half-turn rotation,
-// folded into the rounding shift.
+// folded into the rounding shift.  Stores are unconditional: a lane past the end of the
+// segment works on the tile's first vector and stores the same bytes as that vector's own
+// lane, so no path of a tile loop skips a store (which would make the compiler wait for every
+// outstanding store before using a prefetched load).
 #include <float.h>
 #include <hip/hip_runtime.h>
 
@@ -72,15 +79,16 @@ __device__ __forceinline__ uint32_t angle_code_wrap(uint32_t bits, uint32_t n) {
   return min(k, k - n);
 }
 
-// Angle code for pairs outside the range the fast formula assumes: zero pairs get bin 0;
-// other finite pairs are scaled by an exact power of two first.  Non-finite pairs get bin 0.
-__device__ __noinline__ uint32_t angle_code_careful(float a, float b, float nf, uint32_t n) {
-  if (a == 0.0f && b == 0.0f) return 0u;
+// Angle code for pairs outside the range the fast formula assumes: the pair is scaled by the
+// exact power of two that brings max(|a|, |b|) into [1/2, 1) (the angle is unchanged), zero
+// pairs get bin 0, and so do non-finite pairs.  Plain instructions, no call: the encode loop
+// keeps its registers.
+__device__ __forceinline__ uint32_t angle_code_careful(float a, float b, float nf, uint32_t n) {
   const float mx = fmaxf(fabsf(a), fabsf(b));
-  if (!(mx <= FLT_MAX)) return 0u;
-  int e;
-  (void)frexpf(mx, &e);
-  return angle_code_wrap(angle_bits(ldexpf(a, -e), ldexpf(b, -e), nf, kRoundShift), n);
+  const int e = __builtin_amdgcn_frexp_expf(mx);
+  const uint32_t k = angle_code_wrap(
+      angle_bits(__builtin_amdgcn_ldexpf(a, -e), __builtin_amdgcn_ldexpf(b, -e), nf, kRoundShift), n);
+  return (mx == 0.0f || !(mx <= FLT_MAX)) ? 0u : k;
 }
 
 // r_i = |(a, b)| / sqrt(d) in fp64: the fp64 operation sequence of the definition, so a
@@ -138,218 +146,317 @@ __device__ __forceinline__ Raw<F32IN> load_raw(const void* src, int64_t elem) {
   return r;
 }
 
-struct TilePos {
-  uint32_t bh, t, b, h;
-  bool valid;
+// Per-wave state: the segment, its planes and sign masks, the lane's rounding shift.
+template <int D>
+struct EncWave {
+  static constexpr int LPV = D / kElemsPerLane;
+  static constexpr int VPW = kWave / LPV;
+  int sub, vslot;
+  SegParams sp;
+  const void* src;
+  int64_t layer_off;          // element offset of the layer and of the lane's 32 elements
+  uint8_t* plane[3];
+  const uint32_t* sm;         // the lane's 16 sign-mask words, in this wave's LDS
+  bool negated;               // the lane holds -z after the butterfly
+  float shift;                // rounding shift with the half-turn of a negated lane removed
+  uint32_t unneg;             // sign flip that undoes the negation (odd n)
 };
 
-__device__ __forceinline__ TilePos tile_pos(const EncodeArgs& a, uint32_t j0, int vslot) {
-  TilePos p;
-  const uint32_t j = j0 + vslot;
-  p.valid = j < a.nvec;
-  const uint32_t jj = p.valid ? j : j0;    // invalid lanes read a valid vector, store nothing
-  p.bh = fast_div(jj, a.div_t);
-  p.t = jj - p.bh * a.div_t.div;
-  p.b = fast_div(p.bh, a.div_h);
-  p.h = p.bh - p.b * a.H;
-  return p;
-}
-
-template <int D, bool F32IN>
-__global__ __launch_bounds__(kBlockThreads) void encode_kernel(EncodeArgs a) {
-  constexpr int LPV = D / kElemsPerLane;  // lanes per vector
-  constexpr int VPW = kWave / LPV;        // vectors per wave
+template <int D>
+__device__ __forceinline__ bool enc_wave_setup(const EncodeArgs& a, EncWave<D>& w,
+                                               uint32_t (*sm_rows)[D / 2], uint32_t& tile0,
+                                               uint32_t& ntiles) {
+  constexpr int LPV = EncWave<D>::LPV;
+  constexpr int VPW = EncWave<D>::VPW;
   const int lane = threadIdx.x & (kWave - 1);
-  const int sub = lane % LPV;
-  const int vslot = lane / LPV;
+  w.sub = lane % LPV;
+  w.vslot = lane / LPV;
   const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock +
                                                         (threadIdx.x / kWave));
-  const uint32_t seg = wave / a.waves_per_seg;
-  if (seg >= a.num_segs) return;
-  const uint32_t wseg = wave - seg * a.waves_per_seg;
-  const SegParams sp = a.segs[seg];
-  const void* src = sp.kind ? a.v : a.k;
-  const float nf = sp.nf;
-  const bool pow2 = sp.mask != 0;
-  const int64_t layer_off = (int64_t)sp.layer * a.stride_l + sub * kElemsPerLane;
+  const uint32_t li = wave / a.waves_per_seg;
+  if (li >= a.num_segs) return false;
+  const uint32_t wseg = wave - li * a.waves_per_seg;
+  const uint32_t tiles_in_seg = (a.nvec + VPW - 1) / VPW;
+  tile0 = wseg * a.tiles_per_wave;
+  if (tile0 >= tiles_in_seg) return false;
+  ntiles = min(a.tiles_per_wave, tiles_in_seg - tile0);
+  w.sp = a.segs[a.seg_list[li]];
+  w.src = w.sp.kind ? a.v : a.k;
+  w.layer_off = (int64_t)w.sp.layer * a.stride_l + w.sub * kElemsPerLane;
+  for (int p = 0; p < 3; ++p) w.plane[p] = a.cache + a.n_slots * w.sp.pre[p];
+  // the layer's sign masks into LDS (registers would hold them through the whole tile loop)
+  uint32_t* row = sm_rows[threadIdx.x / kWave];
+  if (lane < D / 2) row[lane] = a.sign_masks[(size_t)w.sp.layer * (D / 2) + lane];
+  wave_lds_sync();
+  w.sm = row + w.sub * 16;
+  w.negated = lane_negated<LPV>(w.sub);
+  const bool odd_n = (w.sp.n & 1u) != 0;
+  w.shift = (w.negated && !odd_n) ? kRoundShift - 0.5f * w.sp.nf : kRoundShift;
+  w.unneg = (w.negated && odd_n) ? 0x80000000u : 0u;
+  return true;
+}
 
-  // sign masks of this lane's 32 elements: 16 words, one per element pair
+// A tile's input for one lane and the lane's cache slot.  A lane past the end of the segment
+// takes the tile's first vector.
+template <bool F32IN>
+struct TileIn {
+  Raw<F32IN> raw;
+  uint32_t slot;              // (b*H + h)*capacity + t_begin + t < 2^31
+};
+
+template <int D, bool F32IN>
+__device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const EncWave<D>& w,
+                                                   uint32_t tile) {
+  const uint32_t j0 = tile * EncWave<D>::VPW;
+  const uint32_t j = j0 + w.vslot;
+  const uint32_t jj = j < a.nvec ? j : j0;
+  const uint32_t bh = fast_div(jj, a.div_t);
+  const uint32_t t = jj - bh * a.div_t.div;
+  const uint32_t b = fast_div(bh, a.div_h);
+  const uint32_t h = bh - b * a.H;
+  TileIn<F32IN> in;
+  in.raw = load_raw<F32IN>(w.src, w.layer_off + (uint64_t)b * a.stride_b +
+                                      (uint64_t)h * a.stride_h + (uint64_t)t * a.stride_t);
+  in.slot = bh * a.cap + a.t_begin + t;
+  return in;
+}
+
+// Encode one tile.  WA = angle code width and NB = norm code width of a format fixed at
+// compile time (NB = 8: linear norms, NB = 4: log-space norms; the angle codebook is then
+// n = 2^WA), or WA = NB = 0 for the segment's run-time format.
+template <int D, bool F32IN, int WA, int NB>
+__device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D>& w,
+                                            const TileIn<F32IN>& in) {
+  constexpr int LPV = EncWave<D>::LPV;
+  constexpr bool kFixed = WA != 0;
+  static_assert(!kFixed || ((WA == 6 || WA == 8) && (NB == 8 || NB == 4)), "fixed formats");
+  const SegParams& sp = w.sp;
+  const float nf = kFixed ? (float)(1u << WA) : sp.nf;
+  const uint32_t n = kFixed ? (1u << WA) : sp.n;
+  const bool pow2 = kFixed || sp.mask != 0;
+  const uint32_t mode = kFixed ? (NB == 8 ? 1u : 2u) : sp.mode;
+  const uint32_t nbits = kFixed ? (uint32_t)NB : sp.bits;
+  const float levels = (float)((1u << (nbits & 31u)) - 1u);
+
+  // ---- sign flip (sign-bit XOR, exact), widen to fp32 ----
   uint32_t sm[16];
-  load_words<16>(a.sign_masks + (size_t)sp.layer * (D / 2) + sub * 16, sm);
-
-  uint8_t* plane_ang = a.cache + a.n_slots * sp.pre[0];
-  uint8_t* plane_nrm = a.cache + a.n_slots * sp.pre[1];
-  uint8_t* plane_hdr = a.cache + a.n_slots * sp.pre[2];
-  const double inv_sqrt_d = 1.0 / sqrt((double)D);
-  const float levels = (float)((1u << (sp.bits & 31u)) - 1u);
-  // lane sign of the cross-lane butterfly and the rounding shift that absorbs it
-  const bool negated = lane_negated<LPV>(sub);
-  const bool odd_n = (sp.n & 1u) != 0;
-  const float shift = (negated && !odd_n) ? kRoundShift - 0.5f * nf : kRoundShift;
-  const uint32_t unneg = (negated && odd_n) ? 0x80000000u : 0u;
-
-  const uint32_t j0 = wseg * VPW;
-  if (j0 >= a.nvec) return;
-  const TilePos pos = tile_pos(a, j0, vslot);
-  const Raw<F32IN> raw = load_raw<F32IN>(src, layer_off + (uint64_t)pos.b * a.stride_b +
-                                               (uint64_t)pos.h * a.stride_h +
-                                               (uint64_t)pos.t * a.stride_t);
-  {
-    // ---- sign flip (sign-bit XOR, exact), widen to fp32 ----
-    float x[kElemsPerLane];
-    if constexpr (F32IN) {
 #pragma unroll
-      for (int m = 0; m < 16; ++m) {
-        x[2 * m] = __uint_as_float(raw.w[2 * m] ^ (sm[m] << 16));
-        x[2 * m + 1] = __uint_as_float(raw.w[2 * m + 1] ^ (sm[m] & 0x80000000u));
-      }
-    } else {
+  for (int q = 0; q < 4; ++q) {
+    const u32x4a v = *(const u32x4a*)(w.sm + 4 * q);
+    sm[4 * q] = v.x, sm[4 * q + 1] = v.y, sm[4 * q + 2] = v.z, sm[4 * q + 3] = v.w;
+  }
+  float x[kElemsPerLane];
+  if constexpr (F32IN) {
 #pragma unroll
-      for (int m = 0; m < 16; ++m) {
-        const uint32_t wv = raw.w[m] ^ sm[m];
-        x[2 * m] = __uint_as_float(wv << 16);
-        x[2 * m + 1] = __uint_as_float(wv & 0xFFFF0000u);
-      }
+    for (int m = 0; m < 16; ++m) {
+      x[2 * m] = __uint_as_float(in.raw.w[2 * m] ^ (sm[m] << 16));
+      x[2 * m + 1] = __uint_as_float(in.raw.w[2 * m + 1] ^ (sm[m] & 0x80000000u));
     }
-
-    // ---- Walsh-Hadamard butterfly, stages h = 1 .. d/2 in ascending order ----
-    fwht_in_lane(x);
-    fwht_cross_lane_signed<LPV>(x, sub);   // this lane now holds sigma * z
-
-    // ---- squared pair norms and the vector's extremes ----
-    float s2[kPairsPerLane];
-    float lmin = FLT_MAX, lmax = 0.0f;
+  } else {
 #pragma unroll
-    for (int i = 0; i < kPairsPerLane; ++i) {
-      const float p = x[2 * i], q = x[2 * i + 1];
-      s2[i] = __builtin_fmaf(p, p, q * q);
-      lmin = fminf(lmin, s2[i]);
-      lmax = fmaxf(lmax, s2[i]);
-    }
-    const float smin = vec_min<LPV>(lmin);
-    const float smax = vec_max<LPV>(lmax);
-    // the fast formulas need every pair's max(|a|,|b|) inside [2^-61, 2^60]
-    const bool fast = __all(!pos.valid || (smin >= 0x1p-120f && smax <= 0x1p120f));
-
-    // ---- angle codes ----
-    // A lane holding -z sees every pair rotated by half a turn: for even n that is n/2 bins,
-    // removed by starting the rounding shift n/2 lower; for odd n the pair is negated back.
-    uint32_t kc[kPairsPerLane];
-    if (fast) {
-      if (pow2) {
-#pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i)
-          kc[i] = angle_bits(x[2 * i], x[2 * i + 1], nf, shift);
-      } else {
-#pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i)
-          kc[i] = angle_code_wrap(angle_bits(__uint_as_float(__float_as_uint(x[2 * i]) ^ unneg),
-                                             __uint_as_float(__float_as_uint(x[2 * i + 1]) ^ unneg),
-                                             nf, shift),
-                                  sp.n);
-      }
-    } else {
-      const uint32_t flip = negated ? 0x80000000u : 0u;
-#pragma unroll
-      for (int i = 0; i < kPairsPerLane; ++i)
-        kc[i] = angle_code_careful(__uint_as_float(__float_as_uint(x[2 * i]) ^ flip),
-                                   __uint_as_float(__float_as_uint(x[2 * i + 1]) ^ flip), nf,
-                                   sp.n);
-    }
-
-    const uint32_t slot = pos.bh * a.cap + a.t_begin + pos.t;   // < B*H*capacity < 2^31
-    if (pos.valid) store_codes_any(plane_ang + (uint64_t)slot * sp.rec[0], sub, sp.w, kc);
-
-    // ---- norms ----
-    if (sp.mode == 0) {
-      // fp32 norms, rounded once from the fp64 value
-      uint32_t rn[kPairsPerLane];
-#pragma unroll
-      for (int i = 0; i < kPairsPerLane; ++i)
-        rn[i] = __float_as_uint((float)pair_norm_f64(x[2 * i], x[2 * i + 1], inv_sqrt_d));
-      if (pos.valid) store_words<16>((uint32_t*)(plane_nrm + (uint64_t)slot * sp.rec[1]) + 16 * sub, rn);
-    } else {
-      // qc: bits of t + 1.5*2^23, t the code coordinate of each pair (eq. (2) or its log
-      // variant); t stays within [-eps, 2^b - 1 + eps], so the low b bits are the code
-      uint32_t qc[kPairsPerLane];
-      float rmin, rmax;
-      if (fast) {
-        rmin = __builtin_amdgcn_sqrtf(smin * a.inv_d);
-        rmax = __builtin_amdgcn_sqrtf(smax * a.inv_d);
-        const bool degenerate = rmax == rmin;
-        if (sp.mode == 1) {
-          // linear in r: sqrt(s2) is r * sqrt(d), the same affine map up to a common factor
-          const float k0 = __builtin_amdgcn_sqrtf(smin), k1 = __builtin_amdgcn_sqrtf(smax);
-          const float scale = (degenerate || !(k1 > k0)) ? 0.0f : levels / (k1 - k0);
-#pragma unroll
-          for (int i = 0; i < kPairsPerLane; ++i)
-            qc[i] = __float_as_uint(
-                __builtin_fmaf(__builtin_amdgcn_sqrtf(s2[i]) - k0, scale, kRoundShift));
-        } else {
-          // log space: log2(s2 / smin) = 2 log2(r / Rmin) starts near 0, so the fp32 log
-          // outputs keep their precision (no cancellation against a large log of smin)
-          const float rs = __builtin_amdgcn_rcpf(smin);
-          const float k0 = __builtin_amdgcn_logf(smin * rs);   // ~0: rcp is not exact
-          const float k1 = __builtin_amdgcn_logf(smax * rs);
-          const float scale = (degenerate || !(k1 > k0)) ? 0.0f : levels / (k1 - k0);
-#pragma unroll
-          for (int i = 0; i < kPairsPerLane; ++i)
-            qc[i] = __float_as_uint(
-                __builtin_fmaf(__builtin_amdgcn_logf(s2[i] * rs) - k0, scale, kRoundShift));
-        }
-      } else {
-        // careful path: norms from fp64 (no overflow or underflow of a^2 + b^2), rounded once
-        // to fp32; the affine maps on r and on log r (as a ratio to the minimum, so the log
-        // input is >= 1) in fp32
-        float rf[kPairsPerLane];
-        float l0 = FLT_MAX, l1 = 0.0f;
-#pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i) {
-          rf[i] = (float)pair_norm_f64(x[2 * i], x[2 * i + 1], inv_sqrt_d);
-          l0 = fminf(l0, rf[i]);
-          l1 = fmaxf(l1, rf[i]);
-        }
-        rmin = vec_min<LPV>(l0);
-        rmax = vec_max<LPV>(l1);
-        if (sp.mode == 1) {
-          const float scale = (rmax == rmin) ? 0.0f : levels / (rmax - rmin);
-#pragma unroll
-          for (int i = 0; i < kPairsPerLane; ++i)
-            qc[i] = __float_as_uint(__builtin_fmaf(rf[i] - rmin, scale, kRoundShift));
-        } else {
-          const float c0 = fmaxf(rmin, FLT_MIN);
-          const float rc = 1.0f / c0;
-          const float k1 = log2f(fmaxf(rmax, FLT_MIN) * rc);
-          const float scale = (fmaxf(rmax, FLT_MIN) == c0 || !(k1 > 0.0f)) ? 0.0f : levels / k1;
-#pragma unroll
-          for (int i = 0; i < kPairsPerLane; ++i)
-            qc[i] = __float_as_uint(
-                __builtin_fmaf(fmaxf(log2f(fmaxf(rf[i], FLT_MIN) * rc), 0.0f), scale, kRoundShift));
-        }
-      }
-      if (pos.valid) {
-        store_codes_any(plane_nrm + (uint64_t)slot * sp.rec[1], sub, sp.bits, qc);
-        if (sub == 0) *(u32x2*)(plane_hdr + (uint64_t)slot * 8) = u32x2{__float_as_uint(rmin),
-                                                              __float_as_uint(rmax)};
-      }
+    for (int m = 0; m < 16; ++m) {
+      const uint32_t wv = in.raw.w[m] ^ sm[m];
+      x[2 * m] = __uint_as_float(wv << 16);
+      x[2 * m + 1] = __uint_as_float(wv & 0xFFFF0000u);
     }
   }
+
+  // ---- Walsh-Hadamard butterfly, stages h = 1 .. d/2 in ascending order ----
+  fwht_in_lane(x);
+  fwht_cross_lane_signed<LPV>(x, w.sub);   // this lane now holds sigma * z
+
+  // ---- squared pair norms and the vector's extremes ----
+  float s2[kPairsPerLane];
+  float lmin = FLT_MAX, lmax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kPairsPerLane; ++i) {
+    const float p = x[2 * i], q = x[2 * i + 1];
+    s2[i] = __builtin_fmaf(p, p, q * q);
+    lmin = fminf(lmin, s2[i]);
+    lmax = fmaxf(lmax, s2[i]);
+  }
+  const float smin = vec_min<LPV>(lmin);
+  const float smax = vec_max<LPV>(lmax);
+  // the fast formulas need every pair's max(|a|,|b|) inside [2^-61, 2^60]
+  const bool fast = __all(smin >= 0x1p-120f && smax <= 0x1p120f);
+
+  // ---- norms (first: the squared norms are then dead before the angle codes exist) ----
+  uint8_t* rec_nrm = w.plane[1] + (uint64_t)in.slot * sp.rec[1];
+  if (!kFixed && mode == 0) {
+    // fp32 norms, rounded once from the fp64 value
+    const double inv_sqrt_d = 1.0 / sqrt((double)D);
+    uint32_t rn[kPairsPerLane];
+#pragma unroll
+    for (int i = 0; i < kPairsPerLane; ++i)
+      rn[i] = __float_as_uint((float)pair_norm_f64(x[2 * i], x[2 * i + 1], inv_sqrt_d));
+    store_words<16>((uint32_t*)rec_nrm + 16 * w.sub, rn);
+  } else {
+    // qc: bits of t + 1.5*2^23, t the code coordinate of each pair (eq. (2) or its log
+    // variant); t stays within [-eps, 2^b - 1 + eps], so the low b bits are the code
+    uint32_t qc[kPairsPerLane];
+    float rmin, rmax;
+    if (fast) {
+      rmin = __builtin_amdgcn_sqrtf(smin * a.inv_d);
+      rmax = __builtin_amdgcn_sqrtf(smax * a.inv_d);
+      const bool degenerate = rmax == rmin;
+      if (mode == 1) {
+        // linear in r: sqrt(s2) is r * sqrt(d), the same affine map up to a common factor
+        const float k0 = __builtin_amdgcn_sqrtf(smin), k1 = __builtin_amdgcn_sqrtf(smax);
+        const float scale = (degenerate || !(k1 > k0)) ? 0.0f : levels / (k1 - k0);
+#pragma unroll
+        for (int i = 0; i < kPairsPerLane; ++i)
+          qc[i] = __float_as_uint(
+              __builtin_fmaf(__builtin_amdgcn_sqrtf(s2[i]) - k0, scale, kRoundShift));
+      } else {
+        // log space: log2(s2 / smin) = 2 log2(r / Rmin) starts near 0, so the fp32 log
+        // outputs keep their precision (no cancellation against a large log of smin)
+        const float rs = __builtin_amdgcn_rcpf(smin);
+        const float k0 = __builtin_amdgcn_logf(smin * rs);   // ~0: rcp is not exact
+        const float k1 = __builtin_amdgcn_logf(smax * rs);
+        const float scale = (degenerate || !(k1 > k0)) ? 0.0f : levels / (k1 - k0);
+#pragma unroll
+        for (int i = 0; i < kPairsPerLane; ++i)
+          qc[i] = __float_as_uint(
+              __builtin_fmaf(__builtin_amdgcn_logf(s2[i] * rs) - k0, scale, kRoundShift));
+      }
+    } else {
+      // careful path: norms from fp64 (no overflow or underflow of a^2 + b^2), rounded once
+      // to fp32; the affine maps on r and on log r (as a ratio to the minimum, so the log
+      // input is >= 1) in fp32
+      const double inv_sqrt_d = 1.0 / sqrt((double)D);
+      float rf[kPairsPerLane];
+      float l0 = FLT_MAX, l1 = 0.0f;
+#pragma unroll
+      for (int i = 0; i < kPairsPerLane; ++i) {
+        rf[i] = (float)pair_norm_f64(x[2 * i], x[2 * i + 1], inv_sqrt_d);
+        l0 = fminf(l0, rf[i]);
+        l1 = fmaxf(l1, rf[i]);
+      }
+      rmin = vec_min<LPV>(l0);
+      rmax = vec_max<LPV>(l1);
+      if (mode == 1) {
+        const float scale = (rmax == rmin) ? 0.0f : levels / (rmax - rmin);
+#pragma unroll
+        for (int i = 0; i < kPairsPerLane; ++i)
+          qc[i] = __float_as_uint(__builtin_fmaf(rf[i] - rmin, scale, kRoundShift));
+      } else {
+        const float c0 = fmaxf(rmin, FLT_MIN);
+        const float rc = 1.0f / c0;
+        const float k1 = log2f(fmaxf(rmax, FLT_MIN) * rc);
+        const float scale = (fmaxf(rmax, FLT_MIN) == c0 || !(k1 > 0.0f)) ? 0.0f : levels / k1;
+#pragma unroll
+        for (int i = 0; i < kPairsPerLane; ++i)
+          qc[i] = __float_as_uint(
+              __builtin_fmaf(fmaxf(log2f(fmaxf(rf[i], FLT_MIN) * rc), 0.0f), scale, kRoundShift));
+      }
+    }
+    if constexpr (kFixed) store_codes<NB>(rec_nrm, w.sub, qc);
+    else store_codes_any(rec_nrm, w.sub, nbits, qc);
+    // every lane of the vector writes the same header bytes
+    *(u32x2*)(w.plane[2] + (uint64_t)in.slot * 8) = u32x2{__float_as_uint(rmin), __float_as_uint(rmax)};
+  }
+
+  // ---- angle codes ----
+  // A lane holding -z sees every pair rotated by half a turn: for even n that is n/2 bins,
+  // removed by starting the rounding shift n/2 lower; for odd n the pair is negated back.
+  uint32_t kc[kPairsPerLane];
+  if (fast) {
+    if (pow2) {
+#pragma unroll
+      for (int i = 0; i < kPairsPerLane; ++i)
+        kc[i] = angle_bits(x[2 * i], x[2 * i + 1], nf, w.shift);
+    } else {
+#pragma unroll
+      for (int i = 0; i < kPairsPerLane; ++i)
+        kc[i] = angle_code_wrap(angle_bits(__uint_as_float(__float_as_uint(x[2 * i]) ^ w.unneg),
+                                           __uint_as_float(__float_as_uint(x[2 * i + 1]) ^ w.unneg),
+                                           nf, w.shift),
+                                n);
+    }
+  } else {
+    const uint32_t flip = w.negated ? 0x80000000u : 0u;
+#pragma unroll
+    for (int i = 0; i < kPairsPerLane; ++i)
+      kc[i] = angle_code_careful(__uint_as_float(__float_as_uint(x[2 * i]) ^ flip),
+                                 __uint_as_float(__float_as_uint(x[2 * i + 1]) ^ flip), nf, n);
+  }
+  uint8_t* rec_ang = w.plane[0] + (uint64_t)in.slot * sp.rec[0];
+  if constexpr (kFixed) store_codes<WA>(rec_ang, w.sub, kc);
+  else store_codes_any(rec_ang, w.sub, sp.w, kc);
+}
+
+// Tiles tile0 .. tile0 + ntiles - 1.  MULTI: two per iteration from two input buffers, each
+// tile's input loaded while the tile before it is encoded; tile indices are clamped to the
+// last tile, so an odd count encodes the last tile twice (the same bytes to the same
+// addresses) and the loads past the end read lines already in cache.  Launches of one tile
+// per wave use the instantiation without the loop (a separate copy of the tile code inside
+// the same kernel would raise its register count).
+template <int D, bool MULTI, int WA, int NB>
+__device__ void encode_tiles_fast(const EncodeArgs& a, const EncWave<D>& w, uint32_t tile0,
+                                  uint32_t ntiles) {
+  const uint32_t last = tile0 + ntiles - 1;
+  TileIn<false> ia = load_tile<D, false>(a, w, tile0);
+  if constexpr (!MULTI) {
+    encode_tile<D, false, WA, NB>(a, w, ia);
+    return;
+  }
+  for (uint32_t t = tile0; t <= last; t += 2) {
+    const TileIn<false> ib = load_tile<D, false>(a, w, min(t + 1, last));
+    encode_tile<D, false, WA, NB>(a, w, ia);
+    ia = load_tile<D, false>(a, w, min(t + 2, last));
+    encode_tile<D, false, WA, NB>(a, w, ib);
+  }
+}
+
+template <int D, bool MULTI>
+__global__ __launch_bounds__(kBlockThreads) void encode_fast_kernel(EncodeArgs a) {
+  __shared__ __attribute__((aligned(16))) uint32_t s_sm[kWavesPerBlock][D / 2];
+  EncWave<D> w;
+  uint32_t tile0, ntiles;
+  if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles)) return;
+  const bool wide = w.sp.w == 8;
+  if (w.sp.mode == 1) {
+    if (wide) encode_tiles_fast<D, MULTI, 8, 8>(a, w, tile0, ntiles);
+    else encode_tiles_fast<D, MULTI, 6, 8>(a, w, tile0, ntiles);
+  } else {
+    if (wide) encode_tiles_fast<D, MULTI, 8, 4>(a, w, tile0, ntiles);
+    else encode_tiles_fast<D, MULTI, 6, 4>(a, w, tile0, ntiles);
+  }
+}
+
+// Any format, bf16 or fp32 input; one tile per wave.
+template <int D, bool F32IN>
+__global__ __launch_bounds__(kBlockThreads) void encode_generic_kernel(EncodeArgs a) {
+  __shared__ __attribute__((aligned(16))) uint32_t s_sm[kWavesPerBlock][D / 2];
+  EncWave<D> w;
+  uint32_t tile0, ntiles;
+  if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles)) return;
+  encode_tile<D, F32IN, 0, 0>(a, w, load_tile<D, F32IN>(a, w, tile0));
 }
 
 }  // namespace
 }  // namespace tvq
 
-int tvq_launch_encode(const tvq::EncodeArgs& a, int d, int in_f32, unsigned grid, void* stream) {
+int tvq_launch_encode(const tvq::EncodeArgs& a, int d, int in_f32, bool fast, unsigned grid,
+                      void* stream) {
   hipStream_t s = (hipStream_t)stream;
   const dim3 block(tvq::kBlockThreads);
-  if (d == 128) {
-    if (in_f32) hipLaunchKernelGGL((tvq::encode_kernel<128, true>), dim3(grid), block, 0, s, a);
-    else hipLaunchKernelGGL((tvq::encode_kernel<128, false>), dim3(grid), block, 0, s, a);
-  } else if (d == 64) {
-    if (in_f32) hipLaunchKernelGGL((tvq::encode_kernel<64, true>), dim3(grid), block, 0, s, a);
-    else hipLaunchKernelGGL((tvq::encode_kernel<64, false>), dim3(grid), block, 0, s, a);
-  } else {
-    return -1;
-  }
+  if (fast && in_f32) return -1;      // the multi-tile kernel reads bf16 only
+  const bool multi = a.tiles_per_wave > 1;
+#define TVQ_LAUNCH_ENC(D)                                                                    \
+  do {                                                                                       \
+    if (fast && multi)                                                                       \
+      hipLaunchKernelGGL((tvq::encode_fast_kernel<D, true>), dim3(grid), block, 0, s, a);    \
+    else if (fast)                                                                           \
+      hipLaunchKernelGGL((tvq::encode_fast_kernel<D, false>), dim3(grid), block, 0, s, a);   \
+    else if (in_f32)                                                                         \
+      hipLaunchKernelGGL((tvq::encode_generic_kernel<D, true>), dim3(grid), block, 0, s, a); \
+    else                                                                                     \
+      hipLaunchKernelGGL((tvq::encode_generic_kernel<D, false>), dim3(grid), block, 0, s, a);\
+  } while (0)
+  if (d == 128) TVQ_LAUNCH_ENC(128);
+  else if (d == 64) TVQ_LAUNCH_ENC(64);
+  else return -1;
+#undef TVQ_LAUNCH_ENC
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }

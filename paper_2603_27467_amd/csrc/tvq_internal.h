@@ -54,6 +54,7 @@ struct EncodeArgs {
   uint32_t cap;         // capacity tokens
   uint32_t t_begin;
   const SegParams* segs;
+  const uint32_t* seg_list;  // segment indices this launch covers
   const uint32_t* sign_masks;
   FastDiv div_t, div_h;  // by T (tokens in the call) and by H
   uint32_t H;
@@ -86,18 +87,19 @@ struct DecodeArgs {
   float c_d;             // fp32 rounding of 1/sqrt(d)
 };
 
-// Segments whose codes the multi-tile decode kernel handles: n = 64 or 256 (6- or 8-bit angle
+// Segments the multi-tile encode and decode kernels handle: n = 64 or 256 (6- or 8-bit angle
 // codes, every code a valid bin) with 8-bit linear or 4-bit log-space norms.  Other formats go
-// to the single-tile generic decode kernel.
-inline bool decode_fast_format(uint32_t n, uint32_t mode, uint32_t bits) {
+// to the single-tile generic kernels.
+inline bool fast_format(uint32_t n, uint32_t mode, uint32_t bits) {
   return (n == 64 || n == 256) && ((mode == 1 && bits == 8) || (mode == 2 && bits == 4));
 }
 
-constexpr uint32_t kDecodeFastTilesPerWave = 4;
+constexpr uint32_t kFastTilesPerWave = 4;
 
 }  // namespace tvq
 
 // Kernel launchers (defined in the .hip kernel files).
-int tvq_launch_encode(const tvq::EncodeArgs& a, int d, int in_f32, unsigned grid, void* stream);
+int tvq_launch_encode(const tvq::EncodeArgs& a, int d, int in_f32, bool fast, unsigned grid,
+                      void* stream);
 int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, unsigned grid,
                       void* stream);
