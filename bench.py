@@ -2,14 +2,21 @@
 
 One step = one pass of the whole hot path over the Mistral-7B-shaped cache (32 layers, 8 KV
 heads, 4096 tokens, d = 128, bf16, n = 64 angle bins, K 8-bit linear / V 4-bit log norms):
-encode all of K and V into the compressed cache, then decode the whole cache back to bf16.
-Inputs are seeded synthetic tensors resident in HBM before the timed region.
+encode all of K and V into the compressed cache, then decode a whole compressed cache back to
+bf16.  Inputs are seeded synthetic tensors resident in HBM before the timed region.  Two caches
+and two output sets alternate between steps, so a decode never reads the cache the encode
+before it has just written (the working set of a step exceeds the last-level cache, and the
+cache a decode reads was written a full step earlier).
 
     python bench.py [--steps K] [--warmup W] [--workload C2|C3|C4] [--no-cpu-baseline]
+    python bench.py --summarize-profiles TRACE FETCH WRITE SQ VALU --commands ...
 
 Prints one JSON line.  `value` is bf16 KV bytes through the codec per second, counting the
 bytes encoded and the bytes decoded in a step (2 x 512 MiB at the default workload), divided
-by the step time.
+by the step time.  The roofline object is the HBM roofline of the slower direction, with the
+algorithmic bytes of one launch (every bf16 element and every cache byte once); the counter
+evidence it quotes (HBM bytes per launch, VALU instructions and busy fraction) comes from the
+rocprofv3 summary committed under profiles/ for the same kernel sources.
 """
 from __future__ import annotations
 
@@ -29,7 +36,10 @@ import workloads  # noqa: E402
 
 METRIC = "encode+decode GB/s of bf16 KV and % of HBM peak, d=128, 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
-PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "mistral7b_c2_encode_decode_counters.json")
+# fp32 VALU issue peak without packed-fp32 instructions: 256 CUs x 4 SIMDs, one wave64
+# instruction per SIMD every 4 cycles, 2.4 GHz
+VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4
 KERNEL_SOURCES = ["tvq_encode.hip", "tvq_decode.hip", "tvq_device.h", "tvq_internal.h"]
 
 
@@ -58,10 +68,11 @@ def algorithmic_bytes(w: workloads.Workload) -> dict:
             "vectors": 2 * w.L * w.B * w.H * w.T}
 
 
-def traffic_from_profiles(kernel: str):
-    """HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE and scaled by the
-    same counters on a copy of known size; None when absent or when the kernel sources have
-    changed since the counters were taken."""
+def profile_entry(kernel: str):
+    """The committed counter summary of `kernel` ("tvq_encode" / "tvq_decode"): HBM bytes per
+    launch from rocprofv3 FETCH_SIZE / WRITE_SIZE scaled by the same counters on a copy of known
+    size, VALU instructions per launch and VALU busy.  None when absent or when the kernel
+    sources have changed since the counters were taken."""
     try:
         with open(PROFILE_COUNTERS) as f:
             d = json.load(f)
@@ -69,8 +80,7 @@ def traffic_from_profiles(kernel: str):
         return None
     if d.get("kernel_source_hash") != kernel_source_hash():
         return None
-    ent = d.get("kernels", {}).get(kernel)
-    return None if ent is None else ent.get("hbm_bytes_per_launch")
+    return d.get("kernels", {}).get(kernel)
 
 
 def cpu_baseline(w: workloads.Workload, budget_s: float = 15.0) -> dict:
@@ -142,6 +152,125 @@ def cpu_baseline(w: workloads.Workload, budget_s: float = 15.0) -> dict:
                       f"threads; same unit as value (bf16 KV bytes encoded + decoded per second)"}
 
 
+def _csv(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def _short(name: str) -> str:
+    """Map a rocprofv3 kernel name to the entry point it belongs to."""
+    if "encode_" in name and "tvq" in name:
+        return "tvq_encode"
+    if "decode_" in name and "tvq" in name:
+        return "tvq_decode"
+    if "copyBuffer" in name:
+        return "copy"
+    return name
+
+
+def _kernel_label(name: str) -> str:
+    """"void tvq::(anonymous namespace)::encode_fast_kernel<128, true>(tvq::EncodeArgs)" ->
+    "encode_fast_kernel<128, true>"."""
+    name = name.split("(tvq::")[0]
+    return name.split("::")[-1]
+
+
+def _find(dirpath: str, suffix: str) -> str:
+    for root, _, files in os.walk(dirpath):
+        for f in files:
+            if f.endswith(suffix):
+                return os.path.join(root, f)
+    raise FileNotFoundError(f"no *{suffix} under {dirpath}")
+
+
+def summarize_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, commands) -> int:
+    """Turn the rocprofv3 output of the profiling runs (kernel trace, FETCH_SIZE, WRITE_SIZE,
+    SQ instruction counts, VALU busy) into the counter summary bench.py reads and a readable
+    table, both under profiles/.  FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are scaled by
+    what they read for the 1 GiB device copy the profiled runs include (--copy-calibration)."""
+    w = workloads.get("C2")
+    ab = algorithmic_bytes(w)
+    per = {}
+
+    def add(kind, rows, counter):
+        for r in rows:
+            if r["Counter_Name"] != counter:
+                continue
+            k = _short(r["Kernel_Name"])
+            per.setdefault(k, {}).setdefault(kind, []).append(float(r["Counter_Value"]))
+
+    add("fetch_kib", _csv(_find(fetch_dir, "counter_collection.csv")), "FETCH_SIZE")
+    add("write_kib", _csv(_find(write_dir, "counter_collection.csv")), "WRITE_SIZE")
+    sq = _csv(_find(sq_dir, "counter_collection.csv"))
+    for c in ("SQ_INSTS_VALU", "SQ_INSTS_SALU", "SQ_INSTS_LDS", "SQ_INSTS_VMEM_RD",
+              "SQ_INSTS_VMEM_WR", "SQ_WAVES"):
+        add(c, sq, c)
+    add("VALUBusy", _csv(_find(valu_dir, "counter_collection.csv")), "VALUBusy")
+    stats = {}
+    for r in _csv(_find(trace_dir, "kernel_stats.csv")):
+        k = _short(r["Name"])
+        if k in ("tvq_encode", "tvq_decode"):
+            stats.setdefault(k, []).append(r)
+    # the calibration copy is the largest copy dispatch (the others stage a few bytes)
+    copy_bytes = float(1 << 30)
+    fetch_scale = copy_bytes / 1024.0 / max(per["copy"]["fetch_kib"])
+    write_scale = copy_bytes / 1024.0 / max(per["copy"]["write_kib"])
+    out = {"kernel_source_hash": kernel_source_hash(), "workload": w.name,
+           "algorithmic_bytes_per_launch": ab["per_launch"],
+           "fetch_scale_from_copy": round(fetch_scale, 4),
+           "write_scale_from_copy": round(write_scale, 4),
+           "copy_bytes": int(copy_bytes), "commands": commands, "kernels": {}}
+    lines = [f"# Counter summary: {w.name} (L={w.L}, B={w.B}, H={w.H}, T={w.T}, d={w.d}, bf16)",
+             "", "Commands (run from /tmp, repository root $R):", ""]
+    lines += [f"    {c}" for c in commands]
+    lines += ["", f"FETCH_SIZE scale from the 1 GiB copy: {fetch_scale:.4f}; WRITE_SIZE scale: "
+              f"{write_scale:.4f}", "",
+              "| entry point | kernels (calls, avg ns, min ns) | HBM bytes/launch (counters) | "
+              "algorithmic bytes/launch | VALU instr/launch | VALU instr/tile | VALUBusy % |",
+              "|---|---|---|---|---|---|---|"]
+    for k in ("tvq_encode", "tvq_decode"):
+        d = per.get(k, {})
+        # one launch of the entry point = one dispatch per kernel it starts; the profiled runs
+        # start one kernel per call at this workload
+        fetch = float(np.median(d["fetch_kib"])) * 1024.0 * fetch_scale
+        write = float(np.median(d["write_kib"])) * 1024.0 * write_scale
+        valu = float(np.median(d["SQ_INSTS_VALU"]))
+        tiles = ab["vectors"] / (64 // (w.d // 32))
+        ent = {"hbm_bytes_per_launch": int(round(fetch + write)),
+               "fetch_bytes_per_launch": int(round(fetch)),
+               "write_bytes_per_launch": int(round(write)),
+               "valu_insts_per_launch": int(valu),
+               "valu_insts_per_tile": round(valu / tiles, 1),
+               "salu_insts_per_launch": int(np.median(d["SQ_INSTS_SALU"])),
+               "lds_insts_per_launch": int(np.median(d["SQ_INSTS_LDS"])),
+               "vmem_rd_insts_per_launch": int(np.median(d["SQ_INSTS_VMEM_RD"])),
+               "vmem_wr_insts_per_launch": int(np.median(d["SQ_INSTS_VMEM_WR"])),
+               "waves_per_launch": int(np.median(d["SQ_WAVES"])),
+               "valu_busy_pct": round(float(np.median(d["VALUBusy"])), 2),
+               "trace": [{"kernel": r["Name"], "calls": int(r["Calls"]),
+                          "avg_ns": float(r["AverageNs"]), "min_ns": float(r["MinNs"]),
+                          "max_ns": float(r["MaxNs"])} for r in stats.get(k, [])]}
+        out["kernels"][k] = ent
+        ks = "; ".join(f"{_kernel_label(t['kernel'])} ({t['calls']}, {t['avg_ns']:.0f}, "
+                       f"{t['min_ns']:.0f})" for t in ent["trace"])
+        lines.append(f"| {k} | {ks} | {ent['hbm_bytes_per_launch']} | {ab['per_launch']} | "
+                     f"{ent['valu_insts_per_launch']} | {ent['valu_insts_per_tile']} | "
+                     f"{ent['valu_busy_pct']} |")
+    lines += ["", "rocprofv3 --kernel-trace --stats summary of the first command "
+              "(kernel_stats.csv):", "", "```"]
+    with open(_find(trace_dir, "kernel_stats.csv")) as f:
+        lines += [ln.rstrip("\n") for ln in f]
+    lines += ["```"]
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(PROFILE_COUNTERS, "w") as f:
+        json.dump(out, f, indent=1)
+    with open(PROFILE_COUNTERS.replace("_counters.json", "_counters.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -150,8 +279,15 @@ def main() -> int:
     ap.add_argument("--workload", default="C2")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="also run a plain device copy of known size (for counter scaling)")
+                    help="also run a plain 1 GiB device copy (for counter scaling)")
+    ap.add_argument("--summarize-profiles", nargs=5,
+                    metavar=("TRACE", "FETCH", "WRITE", "SQ", "VALU"),
+                    help="write the profiles/ counter summary from rocprofv3 output dirs")
+    ap.add_argument("--commands", nargs="*", default=[],
+                    help="the profiling commands, recorded in the summary")
     args = ap.parse_args()
+    if args.summarize_profiles:
+        return summarize_profiles(*args.summarize_profiles, args.commands)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the codec is per-vector and this build measures "
               "one GPU's share; --gpus above 1 is not supported", file=sys.stderr)
@@ -177,17 +313,26 @@ def main() -> int:
     codec = tvq.Codec(w.L, w.H, w.d, layers,
                       signs=workloads.sign_table(w.sign_seed, w.L, w.d))
     lay = codec.layout(w.B, w.T)
-    cache = torch.empty(lay.total_bytes, dtype=torch.uint8, device="cuda")
-    ko, vo = torch.empty_like(kd), torch.empty_like(vd)
+    caches = [torch.empty(lay.total_bytes, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    outs = [(torch.empty_like(kd), torch.empty_like(vd)) for _ in range(2)]
     stream = torch.cuda.current_stream()
+    for c in caches:                        # both caches hold the encoded workload
+        codec.encode(kd, vd, c, lay, 0, stream)
 
-    def step():
-        codec.encode(kd, vd, cache, lay, 0, stream)
-        codec.decode(cache, lay, 0, w.T, ko, vo, stream)
+    def step(i, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        codec.encode(kd, vd, caches[i % 2], lay, 0, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        ko, vo = outs[i % 2]
+        codec.decode(caches[(i + 1) % 2], lay, 0, w.T, ko, vo, stream)
+        if ev is not None:
+            ev[2].record(stream)
 
     print(f"# warmup {args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        step()
+    for i in range(args.warmup):
+        step(i)
     torch.cuda.synchronize()
 
     if args.copy_calibration:
@@ -195,35 +340,46 @@ def main() -> int:
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
+        del src, dst
 
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     print(f"# timing {args.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     for i in range(args.steps):
-        ev[i][0].record(stream)
-        codec.encode(kd, vd, cache, lay, 0, stream)
-        ev[i][1].record(stream)
-        codec.decode(cache, lay, 0, w.T, ko, vo, stream)
-        ev[i][2].record(stream)
+        step(args.warmup + i, ev[i])
     torch.cuda.synchronize()
     wall_s = time.perf_counter() - t_wall
-    enc_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-    dec_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    enc = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    dec = np.array([e[1].elapsed_time(e[2]) for e in ev])
     span_ms = ev[0][0].elapsed_time(ev[-1][2]) / args.steps
-    ms_per_step = max(span_ms, enc_ms + dec_ms)
+    ms_per_step = max(span_ms, float(enc.mean() + dec.mean()))
 
-    def leg(ms, name):
+    def leg(ms_all, name):
         kern = f"tvq_{name}"
-        bytes_per = ab["per_launch"]
-        gbs = bytes_per / (ms * 1e-3) / 1e9
-        return {"ms": round(ms, 5), "kv_GBps": round(ab["kv"] / (ms * 1e-3) / 1e9, 2),
-                "hbm_GBps_algorithmic": round(gbs, 2), "frac_of_peak": round(gbs / HBM_PEAK_GBPS, 4),
-                "vectors_per_s": round(ab["vectors"] / (ms * 1e-3), 1),
-                "traffic_bytes_per_launch": traffic_from_profiles(kern)}
+        ms = float(ms_all.mean())
+        gbs = ab["per_launch"] / (ms * 1e-3) / 1e9
+        prof = profile_entry(kern)
+        out = {"ms": round(ms, 5), "ms_median": round(float(np.median(ms_all)), 5),
+               "ms_min": round(float(ms_all.min()), 5),
+               "kv_GBps": round(ab["kv"] / (ms * 1e-3) / 1e9, 2),
+               "hbm_GBps_algorithmic": round(gbs, 2),
+               "frac_of_peak": round(gbs / HBM_PEAK_GBPS, 4),
+               "frac_of_peak_at_min": round(ab["per_launch"] / (ms_all.min() * 1e-3) / 1e9
+                                            / HBM_PEAK_GBPS, 4),
+               "vectors_per_s": round(ab["vectors"] / (ms * 1e-3), 1),
+               "traffic_bytes_per_launch": None if prof is None else prof["hbm_bytes_per_launch"]}
+        if prof is not None:
+            # VALU issue: instructions of one launch (counters) over this run's launch time
+            out["valu"] = {"insts_per_launch": prof["valu_insts_per_launch"],
+                           "insts_per_tile": prof["valu_insts_per_tile"],
+                           "busy_pct_profiled": prof["valu_busy_pct"],
+                           "issue_frac": round(prof["valu_insts_per_launch"] / (ms * 1e-3)
+                                               / VALU_ISSUE_PEAK, 4)}
+        return out
 
-    enc, dec = leg(enc_ms, "encode"), leg(dec_ms, "decode")
-    dom_name, dom = ("encode", enc) if enc_ms >= dec_ms else ("decode", dec)
+    e_leg, d_leg = leg(enc, "encode"), leg(dec, "decode")
+    dom_name, dom = ("encode", e_leg) if e_leg["ms"] >= d_leg["ms"] else ("decode", d_leg)
     value = 2 * ab["kv"] / (ms_per_step * 1e-3) / 1e9
     out = {
         "metric": METRIC,
@@ -247,11 +403,13 @@ def main() -> int:
                      "unit": "GB/s", "frac": dom["frac_of_peak"],
                      "traffic": dom["traffic_bytes_per_launch"],
                      "algorithmic_bytes_per_launch": ab["per_launch"]},
-        "encode": enc,
-        "decode": dec,
+        "encode": e_leg,
+        "decode": d_leg,
         "wall_s_timed": round(wall_s, 4),
         "kernel_source_hash": kernel_source_hash(),
     }
+    if "valu" in dom:
+        out["roofline"]["valu_issue_frac"] = dom["valu"]["issue_frac"]
     if not args.no_cpu_baseline:
         print("# cpu baseline (oracle on host cores)", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w)
