@@ -29,7 +29,10 @@
  *   - The sign diagonal comes from SplitMix64 (Steele, Lea and Flood, OOPSLA 2014)
  *     used counter-style, unless the caller passes the signs explicitly.
  *
- * Functions whose parity has no pin from the paper or from mathematics say so.
+ * Functions whose parity has no pin from the paper or from mathematics say so
+ * ("parity unpinned"): their exact output is this project's definition, checked only
+ * against hand-worked cases of that definition or against a pinned function within
+ * rounding.
  */
 #ifndef TVQ_ORACLE_H
 #define TVQ_ORACLE_H
@@ -47,7 +50,9 @@ enum { OR_NORM_F32 = 0, OR_NORM_LINEAR = 1, OR_NORM_LOG = 2 };
  *      section 3.1 "Implementation": sampled once from a seeded PRNG) ---- */
 uint64_t or_splitmix64_mix(uint64_t z);
 /* Signs of layer `layer`: out[i] = +1 iff the top bit of
- * mix(key + (i+1)*0x9E3779B97F4A7C15) is 0, key = mix(seed ^ (layer+1)*0xD1B54A32D192ED03). */
+ * mix(key + (i+1)*0x9E3779B97F4A7C15) is 0, key = mix(seed ^ (layer+1)*0xD1B54A32D192ED03).
+ * Parity unpinned: the paper names no generator; the SplitMix64 finalizer itself is pinned
+ * to its published output stream, the per-layer key derivation is this project's. */
 void or_signs(uint64_t seed, int layer, int d, int8_t* out);
 
 /* ---- Walsh-Hadamard transform (section 2, "Fast Walsh-Hadamard Transform") ---- */
@@ -113,6 +118,8 @@ void or_decode_vector_f64(int d, const or_kind* kind, const int8_t* signs,
  *   y^_{2i} = RN(r^ * C[k]), y^_{2i+1} = RN(r^ * S[k])   (C, S from or_trig_table)
  *   z = or_fwht_f32(y^);  x^_j = s_j * RN(z_j * RN(1/sqrt(d))).
  */
+/* Parity unpinned: the paper gives the reconstruction formula, not an fp32 operation order;
+ * these bits are this project's fixed order, pinned only to the fp64 decode within rounding. */
 void or_decode_vector_f32(int d, const or_kind* kind, const int8_t* signs,
                           const uint32_t* k, const uint32_t* q, const float* rn,
                           const float* hdr, float* x_out);
@@ -120,7 +127,8 @@ void or_decode_vector_f32(int d, const or_kind* kind, const int8_t* signs,
 /* ---- bit packing of the compressed cache (the paper only counts bits; the byte layout
  *      is this project's and is stated in the design notes) ---- */
 /* LSB-first bitstream: code i occupies bits [i*w, (i+1)*w), bit j of the stream is bit
- * (j mod 8) of byte (j div 8). */
+ * (j mod 8) of byte (j div 8).  Parity unpinned (layout is this project's): checked against a
+ * hand-packed example and by round trip. */
 void or_pack_bits(const uint32_t* codes, int count, int w, uint8_t* out);
 void or_unpack_bits(const uint8_t* in, int count, int w, uint32_t* codes);
 
@@ -135,7 +143,8 @@ typedef struct {
  * plane 0 angle codes P*w/8, plane 1 norm data P*b/8 (4P for F32), plane 2 header 8 (0 for F32). */
 void or_record_bytes(const or_codec* c, int layer, int kind, int64_t rec[3]);
 /* Byte offset of every plane: planes follow each other in (layer, kind, plane) order with no
- * padding; plane size = B * H * T_cap * record.  Returns the total size. */
+ * padding; plane size = B * H * T_cap * record.  Returns the total size.  Parity unpinned
+ * (layout is this project's): checked against sizes worked out by hand and against eq. (3). */
 int64_t or_cache_layout(const or_codec* c, int64_t B, int64_t T_cap, int64_t* off /*[L][2][3]*/);
 
 /*
