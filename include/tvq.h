@@ -164,6 +164,11 @@ tvq_status tvq_make_signs(uint64_t seed, int32_t layer, int32_t head_dim, int8_t
  * = fp32 roundings of cos(2 pi k/n), sin(2 pi k/n), exact at multiples of pi/4. */
 tvq_status tvq_make_trig_table(int32_t n, float* cos_out, float* sin_out);
 
+/* The table the decode kernels read for an n-bin codebook at head dimension d: the same fp64
+ * values divided by sqrt(d) (the normalization of H, section 2) and rounded once to fp32,
+ * cos_out[k] = RN32(cos(2 pi k/n) / sqrt(d)), sin_out[k] likewise.  Host-only. */
+tvq_status tvq_make_decode_table(int32_t n, int32_t head_dim, float* cos_out, float* sin_out);
+
 /* Layout of a configuration without creating a codec (same result as tvq_cache_layout). */
 tvq_status tvq_layout_for_config(const tvq_config* cfg, int64_t batch, int64_t capacity_tokens,
                                  tvq_layout* out);

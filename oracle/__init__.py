@@ -65,6 +65,7 @@ def lib():
         L.or_angle_code.argtypes = [ctypes.c_double, ctypes.c_int]
         L.or_angle_width.argtypes = [ctypes.c_int]
         L.or_trig_table.argtypes = [ctypes.c_int, vp, vp]
+        L.or_decode_table.argtypes = [ctypes.c_int, ctypes.c_int, vp, vp]
         L.or_encode_vector.argtypes = [vp, vp, ctypes.c_int, ctypes.POINTER(_Kind)] + [vp] * 7
         L.or_dequant_norms_f64.argtypes = [ctypes.c_int, ctypes.POINTER(_Kind), vp, vp, vp, vp]
         L.or_decode_vector_f64.argtypes = [ctypes.c_int, ctypes.POINTER(_Kind)] + [vp] * 6
@@ -137,6 +138,13 @@ def trig_table(n: int):
     c = np.empty(n, np.float32)
     s = np.empty(n, np.float32)
     lib().or_trig_table(n, _p(c), _p(s))
+    return c, s
+
+
+def decode_table(n: int, d: int):
+    c = np.empty(n, np.float32)
+    s = np.empty(n, np.float32)
+    lib().or_decode_table(n, d, _p(c), _p(s))
     return c, s
 
 

@@ -104,30 +104,49 @@ int or_angle_width(int n) {
 /* Write 4k = qd*n + rem; the angle is qd quarter turns plus (pi/2)(rem/n).  The small    */
 /* part is folded into [0, pi/4] so that exact multiples of pi/4 are exact.               */
 /* ------------------------------------------------------------------------------------ */
+/* cos and sin of 2 pi k / n in fp64: with 4k = qd*n + rem, the angle is qd quarter turns plus
+ * (pi/2)*rem/n, folded to at most pi/4 (exact at multiples of pi/4). */
+static void trig64(int n, int k, double* c_out, double* s_out) {
+  long long m = 4LL * k;
+  long long qd = m / n, rem = m % n;
+  double c, s;
+  if (rem == 0) {
+    c = 1.0; s = 0.0;
+  } else if (2 * rem == n) {
+    c = sqrt(0.5); s = c;
+  } else if (2 * rem < n) {
+    double a = (M_PI / 2.0) * ((double)rem / (double)n);
+    c = cos(a); s = sin(a);
+  } else {
+    double a = (M_PI / 2.0) * ((double)(n - rem) / (double)n);
+    c = sin(a); s = cos(a);
+  }
+  /* rotate (c, s) by qd quarter turns: each turn maps (c, s) to (-s, c) */
+  for (long long j = 0; j < (qd & 3); j++) {
+    double tmp = c;
+    c = -s;
+    s = tmp;
+  }
+  *c_out = c;
+  *s_out = s;
+}
+
 void or_trig_table(int n, float* cos_out, float* sin_out) {
   for (int k = 0; k < n; k++) {
-    long long m = 4LL * k;
-    long long qd = m / n, rem = m % n;
     double c, s;
-    if (rem == 0) {
-      c = 1.0; s = 0.0;
-    } else if (2 * rem == n) {
-      c = sqrt(0.5); s = c;
-    } else if (2 * rem < n) {
-      double a = (M_PI / 2.0) * ((double)rem / (double)n);
-      c = cos(a); s = sin(a);
-    } else {
-      double a = (M_PI / 2.0) * ((double)(n - rem) / (double)n);
-      c = sin(a); s = cos(a);
-    }
-    /* rotate (c, s) by qd quarter turns: each turn maps (c, s) to (-s, c) */
-    for (long long j = 0; j < (qd & 3); j++) {
-      double tmp = c;
-      c = -s;
-      s = tmp;
-    }
+    trig64(n, k, &c, &s);
     cos_out[k] = (float)c;
     sin_out[k] = (float)s;
+  }
+}
+
+void or_decode_table(int n, int d, float* cos_out, float* sin_out) {
+  double root = sqrt((double)d);
+  for (int k = 0; k < n; k++) {
+    double c, s;
+    trig64(n, k, &c, &s);
+    cos_out[k] = (float)(c / root);
+    sin_out[k] = (float)(s / root);
   }
 }
 
@@ -278,7 +297,7 @@ void or_decode_vector_f32(int d, const or_kind* kind, const int8_t* signs,
   float* C = (float*)malloc(sizeof(float) * (size_t)n);
   float* S = (float*)malloc(sizeof(float) * (size_t)n);
   float* r = (float*)malloc(sizeof(float) * (size_t)P);
-  or_trig_table(n, C, S);
+  or_decode_table(n, d, C, S);     /* cos, sin of the bins with 1/sqrt(d) of H folded in */
 
   if (kind->norm_mode == OR_NORM_F32) {
     for (int i = 0; i < P; i++) r[i] = rn[i];
@@ -307,11 +326,7 @@ void or_decode_vector_f32(int d, const or_kind* kind, const int8_t* signs,
     x_out[2 * i + 1] = r[i] * S[k[i]];
   }
   or_fwht_f32(x_out, d);
-  const float c_d = (float)(1.0 / sqrt((double)d));
-  for (int j = 0; j < d; j++) {
-    float v = x_out[j] * c_d;
-    x_out[j] = signs[j] < 0 ? -v : v;
-  }
+  for (int j = 0; j < d; j++) x_out[j] = signs[j] < 0 ? -x_out[j] : x_out[j];
   free(C);
   free(S);
   free(r);

@@ -73,6 +73,11 @@ int or_angle_width(int n);
  * cos_out[k], sin_out[k] = fp32 roundings of cos(2 pi k/n), sin(2 pi k/n), k < n, with the
  * argument reduced exactly on the integer k so that multiples of pi/2 give exact 0/+-1. */
 void or_trig_table(int n, float* cos_out, float* sin_out);
+/* The same fp64 values divided by sqrt(d), the normalization of H (section 2), each rounded
+ * once to fp32: the table the fixed-order fp32 decode reads.  Parity unpinned beyond that
+ * definition (checked against or_trig_table: exact division by 8 at d = 64, within an ulp of
+ * the scaled value otherwise). */
+void or_decode_table(int n, int d, float* cos_out, float* sin_out);
 
 /* ---- one vector ---- */
 typedef struct {
@@ -115,8 +120,9 @@ void or_decode_vector_f64(int d, const or_kind* kind, const int8_t* signs,
  *          fmaf(q, RN((Rmax - Rmin) / (2^b - 1)), Rmin) with fp32 correctly rounded ops.
  *       LOG: Rmin if max(Rmax,FLT_MIN) == max(Rmin,FLT_MIN), else RN32 of the fp64 value
  *          exp(L0 + q*((L1 - L0)/(2^b - 1))), L0/L1 = log of the clamped min/max.
- *   y^_{2i} = RN(r^ * C[k]), y^_{2i+1} = RN(r^ * S[k])   (C, S from or_trig_table)
- *   z = or_fwht_f32(y^);  x^_j = s_j * RN(z_j * RN(1/sqrt(d))).
+ *   y^_{2i} = RN(r^ * C'[k]), y^_{2i+1} = RN(r^ * S'[k])   (C', S' from or_decode_table:
+ *          the 1/sqrt(d) of H = W/sqrt(d) rides in the table)
+ *   z = or_fwht_f32(y^);  x^_j = s_j * z_j.
  */
 /* Parity unpinned: the paper gives the reconstruction formula, not an fp32 operation order;
  * these bits are this project's fixed order, pinned only to the fp64 decode within rounding. */

@@ -84,6 +84,8 @@ def load_library():
     L.tvq_make_signs.argtypes = [ctypes.c_uint64, i32, i32, vp]
     L.tvq_make_trig_table.restype = ctypes.c_int
     L.tvq_make_trig_table.argtypes = [i32, vp, vp]
+    L.tvq_make_decode_table.restype = ctypes.c_int
+    L.tvq_make_decode_table.argtypes = [i32, i32, vp, vp]
     L.tvq_layout_for_config.restype = ctypes.c_int
     L.tvq_layout_for_config.argtypes = [ctypes.POINTER(tvq_config), i64, i64,
                                         ctypes.POINTER(tvq_layout)]
@@ -165,6 +167,15 @@ def tvq_make_signs(seed: int, layer: int, head_dim: int) -> np.ndarray:
     _check(load_library().tvq_make_signs(seed & (2**64 - 1), layer, head_dim,
                                          out.ctypes.data_as(ctypes.c_void_p)), "tvq_make_signs")
     return out
+
+
+def tvq_make_decode_table(n: int, head_dim: int):
+    c = np.zeros(n, np.float32)
+    s = np.zeros(n, np.float32)
+    _check(load_library().tvq_make_decode_table(n, head_dim, c.ctypes.data_as(ctypes.c_void_p),
+                                                s.ctypes.data_as(ctypes.c_void_p)),
+           "tvq_make_decode_table")
+    return c, s
 
 
 def tvq_make_trig_table(n: int):

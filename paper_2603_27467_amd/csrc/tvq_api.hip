@@ -162,6 +162,40 @@ unsigned plan_grid(uint32_t nvec, uint32_t vpw, uint32_t num_segs, uint32_t* wav
   return (unsigned)((waves + tvq::kWavesPerBlock - 1) / tvq::kWavesPerBlock);
 }
 
+// cos and sin of 2 pi k / n in fp64: 4k = quarter*n + rem, the angle (pi/2)*rem/n is at most
+// pi/4 after folding (exact at multiples of pi/4), then rotated by whole quarter turns.
+void trig_fp64(int32_t n, int32_t k, double* c_out, double* s_out) {
+  const double half_pi = 1.5707963267948966;  // fp64 rounding of pi/2
+  const int64_t m = 4ll * k;
+  const int64_t quarter = m / n;
+  const int64_t rem = m % n;
+  double c, s;
+  if (rem == 0) {
+    c = 1.0;
+    s = 0.0;
+  } else if (2 * rem == n) {
+    c = std::sqrt(0.5);
+    s = c;
+  } else if (2 * rem < n) {
+    const double ang = half_pi * ((double)rem / (double)n);
+    c = std::cos(ang);
+    s = std::sin(ang);
+  } else {
+    const double ang = half_pi * ((double)(n - rem) / (double)n);
+    c = std::sin(ang);
+    s = std::cos(ang);
+  }
+  double cr = c, sr = s;
+  switch (quarter & 3) {
+    case 1: cr = -s; sr = c; break;
+    case 2: cr = -c; sr = -s; break;
+    case 3: cr = s; sr = -c; break;
+    default: break;
+  }
+  *c_out = cr;
+  *s_out = sr;
+}
+
 }  // namespace
 
 extern "C" {
@@ -191,37 +225,23 @@ tvq_status tvq_make_signs(uint64_t seed, int32_t layer, int32_t head_dim, int8_t
 
 tvq_status tvq_make_trig_table(int32_t n, float* cos_out, float* sin_out) {
   if (n < 2 || n > 4096 || !cos_out || !sin_out) return TVQ_ERR_INVALID_ARG;
-  const double half_pi = 1.5707963267948966;  // fp64 rounding of pi/2
   for (int32_t k = 0; k < n; ++k) {
-    // 2 pi k / n = (quarter turns) * pi/2 + (pi/2) * rem/n with 4k = quarter*n + rem
-    const int64_t m = 4ll * k;
-    const int64_t quarter = m / n;
-    const int64_t rem = m % n;
     double c, s;
-    if (rem == 0) {
-      c = 1.0;
-      s = 0.0;
-    } else if (2 * rem == n) {
-      c = std::sqrt(0.5);
-      s = c;
-    } else if (2 * rem < n) {
-      const double ang = half_pi * ((double)rem / (double)n);
-      c = std::cos(ang);
-      s = std::sin(ang);
-    } else {
-      const double ang = half_pi * ((double)(n - rem) / (double)n);
-      c = std::sin(ang);
-      s = std::cos(ang);
-    }
-    double cr = c, sr = s;
-    switch (quarter & 3) {
-      case 1: cr = -s; sr = c; break;
-      case 2: cr = -c; sr = -s; break;
-      case 3: cr = s; sr = -c; break;
-      default: break;
-    }
-    cos_out[k] = (float)cr;
-    sin_out[k] = (float)sr;
+    trig_fp64(n, k, &c, &s);
+    cos_out[k] = (float)c;
+    sin_out[k] = (float)s;
+  }
+  return TVQ_OK;
+}
+
+tvq_status tvq_make_decode_table(int32_t n, int32_t head_dim, float* cos_out, float* sin_out) {
+  if (n < 2 || n > 4096 || head_dim < 1 || !cos_out || !sin_out) return TVQ_ERR_INVALID_ARG;
+  const double root = std::sqrt((double)head_dim);
+  for (int32_t k = 0; k < n; ++k) {
+    double c, s;
+    trig_fp64(n, k, &c, &s);
+    cos_out[k] = (float)(c / root);
+    sin_out[k] = (float)(s / root);
   }
   return TVQ_OK;
 }
@@ -299,7 +319,7 @@ tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out) {
         prefix += s.rec[p];
       }
       std::vector<float> cs(n), sn(n);
-      tvq_make_trig_table((int32_t)n, cs.data(), sn.data());
+      tvq_make_decode_table((int32_t)n, d, cs.data(), sn.data());   // 1/sqrt(d) folded in
       for (uint32_t k = 0; k < n; ++k) {
         lut.push_back(cs[k]);
         lut.push_back(sn[k]);
@@ -450,7 +470,6 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
   a.div_h = make_div((uint32_t)c->H);
   a.H = (uint32_t)c->H;
   a.nvec = (uint32_t)(out->batch * c->H * out->tokens);
-  a.c_d = (float)(1.0 / std::sqrt((double)c->d));
   const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
   // the common formats go to the multi-tile kernel, the rest to the generic one
   const struct { uint32_t first, count, tpw; bool fast; } launches[2] = {

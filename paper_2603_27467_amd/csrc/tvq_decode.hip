@@ -2,8 +2,9 @@
 //
 // Per vector (section 3.1, reconstruction; section 3.3 inverted at code centres): unpack the
 // angle and norm codes, recover the pair norms r^, rebuild y^ = r^ (cos, sin)(2 pi k / n) from
-// the codebook's lookup table, apply the self-inverse Walsh-Hadamard butterfly, the 1/sqrt(d)
-// factor and the sign diagonal (D^-1 = D), and store bf16 (round to nearest even) or fp32.
+// the codebook's lookup table (which carries the 1/sqrt(d) factor of H), apply the
+// self-inverse Walsh-Hadamard butterfly and the sign diagonal (D^-1 = D), and store bf16
+// (round to nearest even) or fp32.
 //
 // Arithmetic order is fixed so that results are reproducible bit for bit:
 //   linear norms  r^ = fmaf(q, RN((Rmax - Rmin) / (2^b - 1)), Rmin)   (Rmin if Rmax == Rmin)
@@ -11,8 +12,9 @@
 //                 (up to 4 bits: the geometric ladder R'min * rho^q, rho = (R'max/R'min)^(1/(2^b-1)),
 //                 by fp64 products; it differs from the formula by ~1e-15 relative, so the fp32
 //                 levels agree except with probability ~1e-8 per level, and then by one ulp)
-//   y^            RN(r^ * C[k]), RN(r^ * S[k])
-//   x^            s_j * RN(z_j * RN(1/sqrt(d))), z = butterfly with stages h = 1 .. d/2
+//   y^            RN(r^ * C'[k]), RN(r^ * S'[k]) with C'[k] = RN(cos(2 pi k/n) / sqrt(d)) and
+//                 S'[k] likewise, from fp64 (the 1/sqrt(d) of H rides in the table)
+//   x^            s_j * z_j, z = butterfly with stages h = 1 .. d/2
 // The two cross-lane butterfly stages leave some lanes holding -z (exactly, up to the sign of
 // an exact zero); that sign is folded into the output sign mask.
 //
@@ -255,12 +257,12 @@ __device__ __forceinline__ void reconstruct(const DecodeArgs& a, const WaveState
   if constexpr (F32OUT) {
 #pragma unroll
     for (int m = 0; m < 16; ++m) {
-      o[2 * m] = __float_as_uint(x[2 * m] * a.c_d) ^ (w.sm[m] << 16);
-      o[2 * m + 1] = __float_as_uint(x[2 * m + 1] * a.c_d) ^ (w.sm[m] & 0x80000000u);
+      o[2 * m] = __float_as_uint(x[2 * m]) ^ (w.sm[m] << 16);
+      o[2 * m + 1] = __float_as_uint(x[2 * m + 1]) ^ (w.sm[m] & 0x80000000u);
     }
   } else {
 #pragma unroll
-    for (int m = 0; m < 16; ++m) o[m] = bf16x2_rne(x[2 * m] * a.c_d, x[2 * m + 1] * a.c_d) ^ w.sm[m];
+    for (int m = 0; m < 16; ++m) o[m] = bf16x2_rne(x[2 * m], x[2 * m + 1]) ^ w.sm[m];
   }
 }
 

@@ -160,6 +160,20 @@ __device__ __forceinline__ Chunk<W> pack16(const uint32_t (&c)[kPairsPerLane]) {
   return o;
 }
 
+// 8-bit codes whose low byte is the code (the rounded float bits of the encoder, or clean
+// integers): three instructions per word, two byte gathers and a shift-or.
+template <>
+__device__ __forceinline__ Chunk<8> pack16<8>(const uint32_t (&c)[kPairsPerLane]) {
+  Chunk<8> o;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t lo = __builtin_amdgcn_perm(c[4 * j + 1], c[4 * j], 0x0c0c0400u);
+    const uint32_t hi = __builtin_amdgcn_perm(c[4 * j + 3], c[4 * j + 2], 0x0c0c0400u);
+    o.w[j] = (hi << 16) | lo;
+  }
+  return o;
+}
+
 template <int W>
 __device__ __forceinline__ void unpack16(const Chunk<W>& o, uint32_t (&c)[kPairsPerLane]) {
   constexpr uint32_t m = (W == 32) ? 0xFFFFFFFFu : ((1u << W) - 1u);

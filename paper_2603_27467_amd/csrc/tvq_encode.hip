@@ -301,8 +301,10 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
       const bool degenerate = rmax == rmin;
       if (mode == 1) {
         // linear in r: sqrt(s2) is r * sqrt(d), the same affine map up to a common factor
+        // scale by rcp (1 ulp): t moves by < 2^-22 * levels, a tenth of the flag zone
         const float k0 = __builtin_amdgcn_sqrtf(smin), k1 = __builtin_amdgcn_sqrtf(smax);
-        const float scale = (degenerate || !(k1 > k0)) ? 0.0f : levels / (k1 - k0);
+        const float scale =
+            (degenerate || !(k1 > k0)) ? 0.0f : levels * __builtin_amdgcn_rcpf(k1 - k0);
 #pragma unroll
         for (int i = 0; i < kPairsPerLane; ++i)
           qc[i] = __float_as_uint(
@@ -313,7 +315,8 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
         const float rs = __builtin_amdgcn_rcpf(smin);
         const float k0 = __builtin_amdgcn_logf(smin * rs);   // ~0: rcp is not exact
         const float k1 = __builtin_amdgcn_logf(smax * rs);
-        const float scale = (degenerate || !(k1 > k0)) ? 0.0f : levels / (k1 - k0);
+        const float scale =
+            (degenerate || !(k1 > k0)) ? 0.0f : levels * __builtin_amdgcn_rcpf(k1 - k0);
 #pragma unroll
         for (int i = 0; i < kPairsPerLane; ++i)
           qc[i] = __float_as_uint(

@@ -4,7 +4,8 @@
 //   SegParams  [2L]        one per (layer, kind), index 2*layer + kind (0 = K, 1 = V)
 //   sign masks [L][d/2]    u32 XOR masks of the sign diagonal D for element pairs (2m, 2m+1)
 //                          of a bf16 word: bit 15 flips element 2m, bit 31 flips element 2m+1
-//   trig LUT   sum_s n_s   float2 (cos, sin)(2 pi k / n) per codebook, segment s at lut_off
+//   trig LUT   sum_s n_s   float2 (cos, sin)(2 pi k / n) / sqrt(d) per codebook (each value
+//                          rounded once from fp64), segment s at lut_off
 #pragma once
 
 #include <stdint.h>
@@ -84,7 +85,6 @@ struct DecodeArgs {
   uint32_t waves_per_seg;
   uint32_t tiles_per_wave;
   uint32_t num_segs;
-  float c_d;             // fp32 rounding of 1/sqrt(d)
 };
 
 // Segments the multi-tile encode and decode kernels handle: n = 64 or 256 (6- or 8-bit angle

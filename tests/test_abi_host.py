@@ -56,6 +56,16 @@ def test_trig_table_agrees_with_oracle(tvq, orc):
         assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32)), n
 
 
+def test_decode_table_agrees_with_oracle(tvq, orc):
+    """The table the decode kernels read (1/sqrt(d) folded in), bit for bit, d = 64 and 128."""
+    for d in (64, 128):
+        for n in list(range(2, 300)) + [384, 512, 1000, 2048, 4095, 4096]:
+            c1, s1 = tvq.tvq_make_decode_table(n, d)
+            c2, s2 = orc.decode_table(n, d)
+            assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32)), (n, d)
+            assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32)), (n, d)
+
+
 def _cfg(tvq, table, L, H, d, seed=0, shared=0, signs=None):
     arr = (tvq.tvq_layer_cfg * max(len(table), 1))()
     for i, t in enumerate(table):

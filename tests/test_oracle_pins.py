@@ -400,6 +400,22 @@ def test_trig_table(orc, n):
     assert np.array_equal(c, c.astype(np.float64).astype(np.float32))
 
 
+@pytest.mark.parametrize("n", [2, 3, 48, 64, 256, 4096])
+def test_decode_table_is_the_scaled_trig_table(orc, n):
+    """The fixed-order fp32 decode reads cos/sin(2 pi k/n) / sqrt(d), rounded once: at d = 64
+    that is the fp32 table divided by 8 exactly; at d = 128 it is within half an ulp of the
+    fp64 value cos(2 pi k/n) / sqrt(128)."""
+    c, s = orc.trig_table(n)
+    c64, s64 = orc.decode_table(n, 64)
+    assert np.array_equal(c64, c / np.float32(8)) and np.array_equal(s64, s / np.float32(8))
+    c128, s128 = orc.decode_table(n, 128)
+    ang = 2 * np.pi * np.arange(n) / n
+    for got, want in ((c128, np.cos(ang) / np.sqrt(128.0)), (s128, np.sin(ang) / np.sqrt(128.0))):
+        ulp = np.spacing(np.abs(got).astype(np.float32)).astype(np.float64)
+        # numpy's fp64 reference is itself off by ~1e-16 (sin(pi) is not 0), hence the slack
+        assert np.all(np.abs(got.astype(np.float64) - want) <= 0.5 * ulp + 2e-16)
+
+
 # --------------------------------------------------------------------------- packing/layout
 def test_pack_bits_hand_example(orc):
     """LSB-first bitstream: codes (5, 3, 1) at 3 bits = bits 101 110 100 -> bytes 0x5D, 0x00."""
