@@ -8,7 +8,7 @@ and two output sets alternate between steps, so a decode never reads the cache t
 before it has just written (the working set of a step exceeds the last-level cache, and the
 cache a decode reads was written a full step earlier).
 
-    python bench.py [--steps K] [--warmup W] [--workload C2|C3|C4] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload C2|C3|C4|C5] [--no-cpu-baseline]
     python bench.py --summarize-profiles TRACE FETCH WRITE SQ VALU --commands ...
 
 Prints one JSON line.  `value` is bf16 KV bytes through the codec per second, counting the
@@ -271,6 +271,116 @@ def summarize_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, comman
     return 0
 
 
+def run_longctx(w: workloads.Workload, args) -> dict:
+    """Long-context step: the cache already holds T tokens of B sequences (every layer, K and
+    V); one step encodes one new token per sequence and layer into slot T + i and decodes
+    slots [0, T + i + 1) of the whole cache back to bf16.  Inputs are drawn on the GPU
+    (workloads.fill_device); the initial draw is freed before the outputs are allocated."""
+    import torch
+    import paper_2603_27467_amd as tvq
+
+    layers = [tvq.LayerCfg(t.n_k, t.n_v, t.norm_bits_k, t.norm_bits_v, t.norm_mode_k,
+                           t.norm_mode_v) for t in w.table]
+    codec = tvq.Codec(w.L, w.H, w.d, layers,
+                      signs=workloads.sign_table(w.sign_seed, w.L, w.d))
+    n_new = args.warmup + args.steps
+    cap = w.T + n_new
+    lay = codec.layout(w.B, cap)
+    shape = (w.L, w.B, w.H, w.T, w.d)
+    print(f"# workload {w.name}: drawing {2 * np.prod(shape) * 2 / 1e9:.1f} GB of bf16 on the "
+          f"GPU, cache {lay.total_bytes / 1e9:.1f} GB", file=sys.stderr, flush=True)
+    cache = torch.empty(lay.total_bytes, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    k = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    workloads.fill_device(w, "K", k)
+    v = torch.empty_like(k)
+    workloads.fill_device(w, "V", v)
+    codec.encode(k, v, cache, lay, 0, stream)
+    torch.cuda.synchronize()
+    del k, v
+    torch.cuda.empty_cache()
+    kn = torch.empty((w.L, w.B, w.H, n_new, w.d), dtype=torch.bfloat16, device="cuda")
+    workloads.fill_device(w, "K", kn, token_part=1)
+    vn = torch.empty_like(kn)
+    workloads.fill_device(w, "V", vn, token_part=1)
+    ko = torch.empty((w.L, w.B, w.H, cap, w.d), dtype=torch.bfloat16, device="cuda")
+    vo = torch.empty_like(ko)
+
+    def step(i, ev=None):
+        t = w.T + i
+        if ev is not None:
+            ev[0].record(stream)
+        codec.encode(kn[:, :, :, i:i + 1], vn[:, :, :, i:i + 1], cache, lay, t, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        codec.decode(cache, lay, 0, t + 1, ko[:, :, :, :t + 1], vo[:, :, :, :t + 1], stream)
+        if ev is not None:
+            ev[2].record(stream)
+
+    print(f"# warmup {args.warmup}", file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    print(f"# timing {args.steps} steps", file=sys.stderr, flush=True)
+    t_wall = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, ev[i])
+    torch.cuda.synchronize()
+    wall_s = time.perf_counter() - t_wall
+    enc = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    dec = np.array([e[1].elapsed_time(e[2]) for e in ev])
+    span_ms = ev[0][0].elapsed_time(ev[-1][2]) / args.steps
+    ms_per_step = max(span_ms, float(enc.mean() + dec.mean()))
+    # bytes of the timed steps, per step on average (the decoded range grows by one token)
+    P = w.d // 2
+    rec_tok = 0                       # compressed bytes of one token position, all (b, h)
+    for t in w.table:
+        for n, mode, bits in ((t.n_k, t.norm_mode_k, t.norm_bits_k),
+                              (t.n_v, t.norm_mode_v, t.norm_bits_v)):
+            wbits = int(np.ceil(np.log2(n)))
+            rec_tok += (P * wbits // 8 + (4 * P if mode == 0 else P * bits // 8 + 8)) * w.B * w.H
+    kv_tok = 2 * w.L * w.B * w.H * w.d * 2          # bf16 K + V bytes of one token position
+    t_mean = w.T + args.warmup + (args.steps - 1) / 2 + 1    # tokens decoded per step, mean
+    dec_bytes = (rec_tok + kv_tok) * t_mean
+    enc_bytes = rec_tok + kv_tok
+    dec_ms = float(dec.mean())
+    dec_gbs = dec_bytes / (dec_ms * 1e-3) / 1e9
+    value = (kv_tok + kv_tok * t_mean) / (ms_per_step * 1e-3) / 1e9
+    return {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "layers": w.L, "batch": w.B, "kv_heads": w.H,
+                   "tokens_cached": w.T, "head_dim": w.d, "io_dtype": w.dtype,
+                   "table": w.notes, "step": "encode 1 token per sequence and layer, then "
+                                             "decode the whole cache",
+                   "compressed_bytes_per_token": rec_tok},
+        "roofline": {"bound": "hbm", "kernel": "tvq_decode",
+                     "achieved": round(dec_gbs, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(dec_gbs / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": int(dec_bytes)},
+        "encode": {"ms": round(float(enc.mean()), 5), "ms_min": round(float(enc.min()), 5),
+                   "vectors": 2 * w.L * w.B * w.H, "algorithmic_bytes": enc_bytes},
+        "decode": {"ms": round(dec_ms, 5), "ms_median": round(float(np.median(dec)), 5),
+                   "ms_min": round(float(dec.min()), 5),
+                   "hbm_GBps_algorithmic": round(dec_gbs, 2),
+                   "frac_of_peak": round(dec_gbs / HBM_PEAK_GBPS, 4),
+                   "vectors_per_s": round(2 * w.L * w.B * w.H * t_mean / (dec_ms * 1e-3), 1)},
+        "wall_s_timed": round(wall_s, 4),
+        "kernel_source_hash": kernel_source_hash(),
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -300,6 +410,13 @@ def main() -> int:
         print("no GPU visible", file=sys.stderr)
         return 1
     w = workloads.get(args.workload)
+    if args.workload == "C5":
+        out = run_longctx(w, args)
+        if not args.no_cpu_baseline:
+            print("# cpu baseline (oracle on host cores)", file=sys.stderr, flush=True)
+            out["cpu_baseline"] = cpu_baseline(w)
+        print(json.dumps(out), flush=True)
+        return 0
     ab = algorithmic_bytes(w)
     print(f"# workload {w.name}: generating inputs", file=sys.stderr, flush=True)
     k = workloads.generate(w, "K")

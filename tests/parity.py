@@ -34,6 +34,13 @@ def ordered_bf16(a: np.ndarray) -> np.ndarray:
     return np.where(b >= 0x8000, -(b & 0x7FFF), b)
 
 
+def bf16_differ(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """Elementwise: the bf16 bit patterns a and b are different values (an exact zero of
+    either sign equals the other: the decode's cross-lane butterfly computes a - b as
+    -(b - a), which cannot keep the sign of an exact zero)."""
+    return ordered_bf16(a) != ordered_bf16(b)
+
+
 @dataclass
 class Setup:
     """One codec configuration on both sides: the GPU codec and the oracle's description."""

@@ -186,3 +186,28 @@ def sign_table(seed: int, L: int, d: int) -> np.ndarray:
     diagonal in as an input rather than asking either side to derive it from a seed)."""
     rng = np.random.default_rng([seed, 99])
     return np.where(rng.integers(0, 2, (L, d)) == 1, 1, -1).astype(np.int8)
+
+
+# ----------------------------------------------------------------------------- on the device
+def _device_seed(w: Workload, which: str, part: int) -> int:
+    """Seed of one torch stream: (data seed, kind, part) mixed into 63 bits."""
+    x = (w.data_seed * 0x9E3779B1 + (0 if which == "K" else 1) * 0x85EBCA77 + part * 0xC2B2AE3D)
+    return x & 0x7FFFFFFFFFFFFFFF
+
+
+def fill_device(w: Workload, which: str, out, token_part: int = 0) -> None:
+    """Fill `out`, a bf16 [L, B, H, T', d] tensor on the GPU, with the recipe of `which` (the
+    same distributions and channel profile as `generate`, drawn by torch's seeded device
+    generator, one stream per layer; `token_part` selects an independent draw, e.g. the tokens
+    appended at one step).  For caches too large to draw on the host; values differ from
+    `generate`'s, so parity tests copy the device tensors they check back to the host."""
+    import torch
+    prof = torch.from_numpy(channel_profile(w, which)).to(out.device)     # [L, H, d]
+    L = out.shape[0]
+    g = torch.Generator(device=out.device)
+    for l in range(L):
+        g.manual_seed(_device_seed(w, which, (token_part << 16) + l))
+        x = torch.randn(out.shape[1:], generator=g, device=out.device, dtype=torch.float32)
+        x *= prof[l][None, :, None, :]
+        out[l].copy_(x.to(torch.bfloat16))       # round to nearest even
+        del x
