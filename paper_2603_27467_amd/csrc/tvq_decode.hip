@@ -355,8 +355,9 @@ __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState
                                             uint32_t tile) {
   constexpr uint32_t kLevels = (1u << NB) - 1u;
   uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
-  unpack16<WA>(c.ang, kc);
-  unpack16<NB>(c.nrm, qc);
+  unpack16_index<WA>(c.ang, kc);
+  if constexpr (NB == 8) unpack16<NB>(c.nrm, qc);    // bytes convert to float in one instruction
+  else unpack16_index<NB>(c.nrm, qc);                // level-table indices
   const float rmin = __uint_as_float(c.hdr.x), rmax = __uint_as_float(c.hdr.y);
   float r[kPairsPerLane];
   if constexpr (NB == 8) {

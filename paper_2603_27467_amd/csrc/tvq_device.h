@@ -188,6 +188,28 @@ __device__ __forceinline__ void unpack16(const Chunk<W>& o, uint32_t (&c)[kPairs
   }
 }
 
+// Table indices of 16 codes (decode): v_bfe_u32 per code, v_alignbit first across a word
+// boundary.  The extract is kept as one instruction (the compiler otherwise rewrites
+// extract-then-scale into shift, mask and add), so an LDS table address is bfe + lshl_add.
+template <int W>
+__device__ __forceinline__ void unpack16_index(const Chunk<W>& o, uint32_t (&c)[kPairsPerLane]) {
+  static_assert(W >= 1 && W < 32, "index widths");
+#pragma unroll
+  for (int i = 0; i < kPairsPerLane; ++i) {
+    const int bit = i * W;
+    const int wd = bit >> 5;
+    const int sh = bit & 31;
+    uint32_t v;
+    if (sh + W <= 32) {
+      asm("v_bfe_u32 %0, %1, %2, %3" : "=v"(v) : "v"(o.w[wd]), "i"(sh), "i"(W));
+    } else {
+      const uint32_t t = __builtin_amdgcn_alignbit(o.w[wd + 1], o.w[wd], sh);
+      asm("v_bfe_u32 %0, %1, 0, %2" : "=v"(v) : "v"(t), "i"(W));
+    }
+    c[i] = v;
+  }
+}
+
 template <int N>
 __device__ __forceinline__ void store_words(uint32_t* p, const uint32_t* v) {
   int i = 0;
