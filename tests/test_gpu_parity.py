@@ -289,12 +289,15 @@ def test_multi_tile_decode_ragged(gpu, d, L, B, T):
 
 
 # ---------------------------------------------------------------------------- full size
-def test_mistral_cache_full_size_sampled(gpu):
-    """The full Mistral-7B-shaped cache (32 layers, 8 heads, 4096 tokens, d=128, bf16) in the
-    launch configuration the benchmark times; 3000 sampled vectors compared with the oracle
-    one by one, plus whole-cache properties (every slot written, decode finite)."""
+@pytest.mark.parametrize("cfg", ["C2", "C3", "C4"])
+def test_cache_full_size_sampled(gpu, cfg):
+    """A benchmark workload at full size in the launch configuration the benchmark times:
+    C2 the Mistral-7B-shaped cache (32 layers, 8 heads, 4096 tokens, d=128), C3 the same with
+    layers 0-3 at n=256, C4 the d=64 cache of 16 layers, batch 8, 8192 tokens with K-only
+    boost.  3000 sampled vectors compared with the oracle one by one (codes, header, bf16
+    output), plus whole-cache properties (every header written, decode finite)."""
     import torch
-    w = workloads.get("C2")
+    w = workloads.get(cfg)
     s = setup_from_workload(w)
     k, v = workloads.generate(w, "K"), workloads.generate(w, "V")
     lay = s.gpu.layout(w.B, w.T)
@@ -312,13 +315,14 @@ def test_mistral_cache_full_size_sampled(gpu):
     stats = dict(angle_mismatch=0, angle_unflagged=0, norm_mismatch=0, norm_unflagged=0,
                  hdr_ulp=0, dec_mismatch=0)
     for _ in range(3000):
-        l, kind, h, t = (int(rng.integers(0, w.L)), int(rng.integers(0, 2)),
-                         int(rng.integers(0, w.H)), int(rng.integers(0, w.T)))
+        l, kind, b, h, t = (int(rng.integers(0, w.L)), int(rng.integers(0, 2)),
+                            int(rng.integers(0, w.B)), int(rng.integers(0, w.H)),
+                            int(rng.integers(0, w.T)))
         src = k if kind == 0 else v
-        x = (src[l, 0, h, t].astype(np.uint32) << 16).view(np.float32)
+        x = (src[l, b, h, t].astype(np.uint32) << 16).view(np.float32)
         kd_ = s.orc.kinds[2 * l + kind]
         ref = oracle.encode_vector(x, s.signs[l], kd_)
-        kg, qg, rng_, hg = s.orc.read_vector(host, w.B, w.T, l, kind, 0, h, t)
+        kg, qg, rng_, hg = s.orc.read_vector(host, w.B, w.T, l, kind, b, h, t)
         fa = oracle.angle_flags(ref.u, kd_.n)
         fn = oracle.norm_flags(ref.t, kd_.norm_bits)
         stats["angle_mismatch"] += int((kg != ref.k).sum())
@@ -328,9 +332,9 @@ def test_mistral_cache_full_size_sampled(gpu):
         du = np.abs(hg.view(np.int32).astype(np.int64) - ref.hdr.view(np.int32).astype(np.int64))
         stats["hdr_ulp"] = max(stats["hdr_ulp"], int(du.max()))
         dec = oracle.decode_vector(kd_, s.signs[l], kg, qg, None, hg, "f32")
-        got = (kout if kind == 0 else vout)[l, 0, h, t]
+        got = (kout if kind == 0 else vout)[l, b, h, t]
         stats["dec_mismatch"] += int(bf16_differ(oracle.f32_to_bf16(dec), got).sum())
-    _say(f"[mistral-full sampled 3000] {stats}")
+    _say(f"[{w.name} full size, 3000 sampled vectors] {stats}")
     assert stats["angle_unflagged"] == 0 and stats["norm_unflagged"] == 0
     assert stats["hdr_ulp"] <= 2 and stats["dec_mismatch"] == 0
     # whole-cache properties: every header plane slot overwritten, outputs finite
