@@ -83,6 +83,10 @@ def lib():
                                      ctypes.c_int64, vp, vp, vp, vp]
         L.or_decode_cache.argtypes = [ctypes.POINTER(_Codec), vp, ctypes.c_int64, ctypes.c_int64,
                                       ctypes.c_int64, ctypes.c_int64, ctypes.c_int, vp]
+        L.or_attention_decode.restype = ctypes.c_int
+        L.or_attention_decode.argtypes = [ctypes.POINTER(_Codec), vp, ctypes.c_int64,
+                                          ctypes.c_int64, ctypes.c_int, ctypes.c_int64,
+                                          ctypes.c_int, ctypes.c_double, vp, vp]
         L.or_f32_to_bf16.restype = ctypes.c_uint16
         L.or_f32_to_bf16.argtypes = [ctypes.c_float]
         L.or_mean_angle_bits.restype = ctypes.c_double
@@ -323,6 +327,18 @@ class Codec:
                                    0 if precision == "f64" else 1, _p(out))
         if rc != 0:
             raise ValueError("oracle decode_cache rejected the arguments")
+        return out
+
+    def attention_decode(self, cache, B, T_cap, layer, t_end, q, scale) -> np.ndarray:
+        """Attention of q ([B][Hq][d], any float dtype) over tokens [0, t_end) of `layer`,
+        in fp64 (see or_attention_decode)."""
+        q = np.ascontiguousarray(q, np.float64)
+        Hq = q.shape[1]
+        out = np.zeros_like(q)
+        rc = lib().or_attention_decode(ctypes.byref(self._c), _p(cache), B, T_cap, layer, t_end,
+                                       Hq, float(scale), _p(q), _p(out))
+        if rc != 0:
+            raise ValueError("oracle attention_decode rejected the arguments")
         return out
 
 

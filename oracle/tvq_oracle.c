@@ -513,6 +513,59 @@ int or_decode_cache(const or_codec* c, const uint8_t* cache, int64_t B, int64_t 
 }
 
 /* ------------------------------------------------------------------------------------ */
+/* Attention of one query token over the decoded cache (standard definition).            */
+/* ------------------------------------------------------------------------------------ */
+int or_attention_decode(const or_codec* c, const uint8_t* cache, int64_t B, int64_t T_cap,
+                        int layer, int64_t t_end, int Hq, double scale, const double* q,
+                        double* out) {
+  const int d = c->d, P = d / 2, H = c->H;
+  if (layer < 0 || layer >= c->L || t_end < 1 || t_end > T_cap || Hq < H || Hq % H != 0)
+    return -1;
+  const int G = Hq / H;
+  uint32_t* kc = (uint32_t*)malloc(sizeof(uint32_t) * (size_t)P);
+  uint32_t* qc = (uint32_t*)malloc(sizeof(uint32_t) * (size_t)P);
+  float* rn = (float*)malloc(sizeof(float) * (size_t)P);
+  double* K = (double*)malloc(sizeof(double) * (size_t)(t_end * d));
+  double* V = (double*)malloc(sizeof(double) * (size_t)(t_end * d));
+  double* s = (double*)malloc(sizeof(double) * (size_t)t_end);
+  const int8_t* sg = c->signs + (size_t)layer * d;
+  for (int64_t b = 0; b < B; b++)
+    for (int h = 0; h < H; h++) {
+      /* decoded keys and values of this (batch, KV head): x^ = D H y^ in fp64 */
+      for (int64_t t = 0; t < t_end; t++) {
+        float hdr[2] = {0.0f, 0.0f};
+        or_read_vector(c, cache, B, T_cap, layer, 0, b, h, t, kc, qc, rn, hdr);
+        or_decode_vector_f64(d, &c->kinds[2 * layer], sg, kc, qc, rn, hdr, K + t * d);
+        hdr[0] = hdr[1] = 0.0f;
+        or_read_vector(c, cache, B, T_cap, layer, 1, b, h, t, kc, qc, rn, hdr);
+        or_decode_vector_f64(d, &c->kinds[2 * layer + 1], sg, kc, qc, rn, hdr, V + t * d);
+      }
+      for (int g = 0; g < G; g++) {
+        const int hq = h * G + g;                 /* query heads grouped over KV heads */
+        const double* qv = q + ((size_t)b * Hq + hq) * d;
+        double* ov = out + ((size_t)b * Hq + hq) * d;
+        double smax = -INFINITY;
+        for (int64_t t = 0; t < t_end; t++) {
+          double acc = 0.0;
+          for (int j = 0; j < d; j++) acc += qv[j] * K[t * d + j];
+          s[t] = scale * acc;
+          if (s[t] > smax) smax = s[t];
+        }
+        double sum = 0.0;
+        for (int j = 0; j < d; j++) ov[j] = 0.0;
+        for (int64_t t = 0; t < t_end; t++) {
+          const double p = exp(s[t] - smax);
+          sum += p;
+          for (int j = 0; j < d; j++) ov[j] += p * V[t * d + j];
+        }
+        for (int j = 0; j < d; j++) ov[j] /= sum;
+      }
+    }
+  free(kc); free(qc); free(rn); free(K); free(V); free(s);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------------------ */
 /* Rate accounting: eq. (1) and eq. (3).                                                 */
 /* ------------------------------------------------------------------------------------ */
 double or_mean_angle_bits(int L, const int* n_k, const int* n_v) {

@@ -174,6 +174,18 @@ int or_read_vector(const or_codec* c, const uint8_t* cache, int64_t B, int64_t T
 int or_decode_cache(const or_codec* c, const uint8_t* cache, int64_t B, int64_t T_cap,
                     int64_t t0, int64_t t1, int precision, void* out);
 
+/*
+ * Attention of one query token per sequence over the compressed cache of one layer: the
+ * consumer of the decoded keys and values (not part of the paper; the standard definition).
+ *   o[b][g] = sum_{t < t_end} p_t v^_t / sum_t p_t,  p_t = exp(s_t - max s),
+ *   s_t = scale * (q[b][g] . k^_t),  k^, v^ of (b, KV head g / (Hq/H), t) decoded in fp64.
+ * q and out are double [B][Hq][d]; Hq is a multiple of H (query heads grouped over the KV
+ * heads in order).  Returns -1 on bad arguments.
+ */
+int or_attention_decode(const or_codec* c, const uint8_t* cache, int64_t B, int64_t T_cap,
+                        int layer, int64_t t_end, int Hq, double scale, const double* q,
+                        double* out);
+
 /* fp32 -> bf16 round to nearest even (bit pattern). */
 uint16_t or_f32_to_bf16(float x);
 

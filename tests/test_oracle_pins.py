@@ -497,3 +497,127 @@ def test_f32_to_bf16_rounding(orc):
     x = np.random.default_rng(0).standard_normal(5000).astype(np.float32)
     vec = orc.f32_to_bf16(x)
     assert all(int(vec[i]) == orc.f32_to_bf16_scalar(float(x[i])) for i in range(0, 5000, 7))
+
+
+# --------------------------------------------------------------------------- attention over the cache
+# The consumer of decode: one query token per sequence attending over the compressed cache.
+# Standard attention is not part of the paper; these pin the oracle's definition to closed
+# forms and limits, and pin the rotated-domain identity the GPU kernel relies on (H D is
+# orthogonal, section 2: q . x^ = (W D q) . y', x^ = D W y' for the unnormalized W and
+# y' = y^ / sqrt(d)).
+def _attn_cache(orc, L=2, B=2, H=2, T=9, d=16, seed=3, same_k=False):
+    rng = np.random.default_rng(seed)
+    kinds = []
+    for _ in range(L):
+        kinds += [orc.Kind(64, orc.NORM_LINEAR, 8), orc.Kind(256, orc.NORM_LOG, 4)]
+    sgn = np.where(rng.integers(0, 2, (L, d)) == 1, 1, -1).astype(np.int8)
+    c = orc.Codec(L, H, d, kinds, sgn)
+    k = rng.standard_normal((L, B, H, T, d)).astype(np.float32)
+    if same_k:
+        k[:] = k[:, :, :, :1]
+    v = rng.standard_normal((L, B, H, T, d)).astype(np.float32)
+    total, _ = c.layout(B, T)
+    cache = np.zeros(total, np.uint8)
+    c.encode_cache(np.ascontiguousarray(k), v, 0, T, cache, want_coords=False)
+    dec = c.decode_cache(cache, B, T, 0, T, "f64")          # [L, 2, B, H, T, d]
+    return c, cache, dec, sgn, rng
+
+
+def test_attention_single_token_is_its_value(orc):
+    """softmax over one token is 1: the output is that token's decoded value, exactly."""
+    c, cache, dec, _, rng = _attn_cache(orc)
+    q = rng.standard_normal((2, 4, 16))
+    out = c.attention_decode(cache, 2, 9, 1, 1, q, 0.25)
+    for b in range(2):
+        for hq in range(4):
+            assert np.array_equal(out[b, hq], dec[1, 1, b, hq // 2, 0])
+
+
+def test_attention_zero_scale_is_the_mean(orc):
+    """scale 0 makes every weight equal: the output is the mean of the decoded values."""
+    c, cache, dec, _, rng = _attn_cache(orc)
+    q = rng.standard_normal((2, 2, 16))
+    out = c.attention_decode(cache, 2, 9, 0, 7, q, 0.0)
+    for b in range(2):
+        for h in range(2):
+            assert np.allclose(out[b, h], dec[0, 1, b, h, :7].mean(axis=0), rtol=0, atol=1e-13)
+
+
+def test_attention_identical_keys_give_the_mean(orc):
+    """All keys equal: every score is equal whatever the query, the output is the mean."""
+    c, cache, dec, _, rng = _attn_cache(orc, same_k=True)
+    q = 3.0 * rng.standard_normal((2, 2, 16))
+    out = c.attention_decode(cache, 2, 9, 1, 9, q, 1.0)
+    for b in range(2):
+        for h in range(2):
+            assert np.allclose(out[b, h], dec[1, 1, b, h].mean(axis=0), rtol=0, atol=1e-12)
+
+
+def test_attention_hard_limit_selects_the_best_key(orc):
+    """A large scale concentrates the weight on the best-scoring key: the output tends to
+    that key's value (here the runner-up weight is below exp(-60))."""
+    c, cache, dec, _, rng = _attn_cache(orc, T=6)
+    checked = 0
+    for trial in range(20):
+        q = rng.standard_normal((2, 2, 16))
+        sc = np.einsum("bhd,bhtd->bht", q, dec[0, 0, :, :, :6])
+        srt = np.sort(sc, axis=-1)
+        gap = (srt[..., -1] - srt[..., -2]).min()
+        if gap < 1e-3:
+            continue
+        scale = 60.0 / gap
+        out = c.attention_decode(cache, 2, 6, 0, 6, q, scale)
+        best = sc.argmax(axis=-1)
+        for b in range(2):
+            for h in range(2):
+                want = dec[0, 1, b, h, best[b, h]]
+                # the other T-1 weights are each below exp(-60) of the best one's
+                bound = 6 * np.abs(dec[0, 1, b, h]).max() * np.exp(-60) + 1e-15 * np.abs(want).max()
+                assert np.allclose(out[b, h], want, rtol=0, atol=bound)
+        checked += 1
+    assert checked >= 5
+
+
+def test_attention_query_heads_grouped_over_kv_heads(orc):
+    """Query heads are grouped over the KV heads in order: with Hq = 3H and the same query in
+    every head, heads 3h, 3h+1, 3h+2 all equal the single-head result of KV head h."""
+    c, cache, dec, _, rng = _attn_cache(orc)
+    q1 = rng.standard_normal((2, 2, 16))
+    one = c.attention_decode(cache, 2, 9, 1, 9, q1, 0.5)
+    q3 = np.repeat(q1, 3, axis=1)
+    three = c.attention_decode(cache, 2, 9, 1, 9, q3, 0.5)
+    for h in range(2):
+        for i in range(3):
+            assert np.array_equal(three[:, 3 * h + i], one[:, h])
+
+
+def test_attention_in_the_rotated_domain(orc):
+    """The identity the GPU kernel uses: scores q . k^ = (W D q) . y'_K and output
+    D W (sum_t p_t y'_V,t) / sum_t p_t, with y'_2i = r^_i cos(2 pi k_i/n) / sqrt(d),
+    y'_2i+1 = r^_i sin(2 pi k_i/n) / sqrt(d) built from the codes and W the unnormalized
+    butterfly -- against the oracle's original-domain attention."""
+    c, cache, dec, sgn, rng = _attn_cache(orc, d=32, T=11)
+    L, B, H, T, d, layer = 2, 2, 2, 11, 32, 1
+    q = rng.standard_normal((B, H, d))
+    scale = 0.3
+    out = c.attention_decode(cache, B, T, layer, T, q, scale)
+
+    def ydash(kind, b, h, t):
+        kg, qg, rn, hg = c.read_vector(cache, B, T, layer, kind, b, h, t)
+        kd = c.kinds[2 * layer + kind]
+        r = orc.dequant_norms_f64(kd, qg, rn, hg, d // 2)
+        ang = 2 * np.pi * kg.astype(np.float64) / kd.n
+        y = np.empty(d)
+        y[0::2], y[1::2] = r * np.cos(ang), r * np.sin(ang)
+        return y / np.sqrt(d)
+
+    for b in range(B):
+        for h in range(H):
+            qt = orc.fwht_f64(sgn[layer] * q[b, h])                      # W D q
+            s = np.array([scale * qt @ ydash(0, b, h, t) for t in range(T)])
+            s_orig = np.array([scale * q[b, h] @ dec[layer, 0, b, h, t] for t in range(T)])
+            assert np.allclose(s, s_orig, rtol=1e-12, atol=1e-12)
+            p = np.exp(s - s.max())
+            a = sum(p[t] * ydash(1, b, h, t) for t in range(T)) / p.sum()
+            o = sgn[layer] * orc.fwht_f64(a)                              # D W a
+            assert np.allclose(o, out[b, h], rtol=1e-12, atol=1e-12)
