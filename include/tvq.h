@@ -142,6 +142,30 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
                       int64_t t_begin, int64_t t_end, tvq_dtype out_dtype, void* k_out,
                       void* v_out, const tvq_tensor_desc* out, void* stream);
 
+/* Attention of one query token per sequence over one layer of the cache -- the consumer of
+ * the decoded keys and values, computed from the codes without writing them (standard
+ * attention, not part of the paper):
+ *   o[b][h*G + g] = sum_{t < t_end} p_t v^_t / sum_t p_t,   p_t = exp(s_t - max_t s_t),
+ *   s_t = scale * (q[b][h*G + g] . k^_t),
+ * where k^_t, v^_t are the vectors tvq_decode would return for (layer, b, KV head h, t) and
+ * G = num_q_heads / H query heads share each KV head.  Because H D is orthogonal (section 2),
+ * s_t = scale * (W D q) . y'_t and o = D W (sum_t p_t y'_t) / sum_t p_t with y' the
+ * reconstructed pair coordinates (section 3.1): one transform per query and per output.
+ *   q, o       device [B][num_q_heads][d], contiguous, bf16 or fp32, 16-byte aligned;
+ *              B = lay->batch
+ *   t_end      1 .. lay->capacity_tokens tokens attended (slots [0, t_end))
+ *   workspace  device scratch of at least tvq_attention_workspace(...) bytes, 16-byte
+ *              aligned, owned by the caller; its contents are overwritten
+ * Arithmetic is fp32 (expect ~1e-5 relative to an fp64 evaluation).  Supported: d = 64 or
+ * 128, G <= 8, and for both K and V of the layer n = 64 or 256 with 8-bit linear or 4-bit
+ * log-space norms (TVQ_ERR_UNSUPPORTED otherwise).  Launches two kernels on `stream`. */
+tvq_status tvq_attention_workspace(const tvq_codec* c, int64_t batch, int32_t num_q_heads,
+                                   int64_t t_end, int64_t* bytes);
+tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq_layout* lay,
+                                int32_t layer, int64_t t_end, int32_t num_q_heads, float scale,
+                                tvq_dtype q_dtype, const void* q, tvq_dtype o_dtype, void* o,
+                                void* workspace, int64_t workspace_bytes, void* stream);
+
 /* Bits per element of the codec, averaged over layers and over K and V.
  * accounting 0: the paper's -- eq. (1) angle bits (log2 n)/2 (fractional for non-power-of-
  *               two n) plus, per eq. (3), b_norm/2 + 64/d for quantized norms or 16 for

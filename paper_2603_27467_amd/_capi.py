@@ -76,6 +76,12 @@ def load_library():
     L.tvq_decode.restype = ctypes.c_int
     L.tvq_decode.argtypes = [vp, vp, ctypes.POINTER(tvq_layout), i64, i64, ctypes.c_int, vp, vp,
                              ctypes.POINTER(tvq_tensor_desc), vp]
+    L.tvq_attention_workspace.restype = ctypes.c_int
+    L.tvq_attention_workspace.argtypes = [vp, i64, i32, i64, ctypes.POINTER(i64)]
+    L.tvq_attention_decode.restype = ctypes.c_int
+    L.tvq_attention_decode.argtypes = [vp, vp, ctypes.POINTER(tvq_layout), i32, i64, i32,
+                                       ctypes.c_float, ctypes.c_int, vp, ctypes.c_int, vp, vp, i64,
+                                       vp]
     L.tvq_bits_per_element.restype = ctypes.c_double
     L.tvq_bits_per_element.argtypes = [vp, ctypes.c_int]
     L.tvq_status_string.restype = ctypes.c_char_p
@@ -152,6 +158,24 @@ def tvq_decode(handle: int, cache_ptr: int, lay: tvq_layout, t_begin: int, t_end
                                      ctypes.byref(lay), t_begin, t_end, out_dtype,
                                      ctypes.c_void_p(k_ptr), ctypes.c_void_p(v_ptr),
                                      ctypes.byref(desc), ctypes.c_void_p(stream)), "tvq_decode")
+
+
+def tvq_attention_workspace(handle: int, batch: int, num_q_heads: int, t_end: int) -> int:
+    out = ctypes.c_int64(0)
+    _check(load_library().tvq_attention_workspace(ctypes.c_void_p(handle), batch, num_q_heads,
+                                                  t_end, ctypes.byref(out)),
+           "tvq_attention_workspace")
+    return int(out.value)
+
+
+def tvq_attention_decode(handle: int, cache_ptr: int, lay: tvq_layout, layer: int, t_end: int,
+                         num_q_heads: int, scale: float, q_dtype: int, q_ptr: int, o_dtype: int,
+                         o_ptr: int, ws_ptr: int, ws_bytes: int, stream: int = 0) -> None:
+    _check(load_library().tvq_attention_decode(
+        ctypes.c_void_p(handle), ctypes.c_void_p(cache_ptr), ctypes.byref(lay), layer, t_end,
+        num_q_heads, ctypes.c_float(scale), q_dtype, ctypes.c_void_p(q_ptr), o_dtype,
+        ctypes.c_void_p(o_ptr), ctypes.c_void_p(ws_ptr), ws_bytes, ctypes.c_void_p(stream)),
+        "tvq_attention_decode")
 
 
 def tvq_bits_per_element(handle: int, accounting: int) -> float:

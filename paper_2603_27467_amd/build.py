@@ -15,7 +15,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libtvq.so")
-SOURCES = ["tvq_api.hip", "tvq_encode.hip", "tvq_decode.hip"]
+SOURCES = ["tvq_api.hip", "tvq_encode.hip", "tvq_decode.hip", "tvq_attention.hip"]
 ARCH = os.environ.get("TVQ_OFFLOAD_ARCH", "gfx950")
 
 HIPCC_FLAGS = [

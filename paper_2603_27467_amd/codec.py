@@ -98,5 +98,27 @@ class Codec:
         C.tvq_decode(self.handle, cache.data_ptr(), lay, t_begin, t_end, dt, k_out.data_ptr(),
                      v_out.data_ptr(), desc_of(k_out), _stream_handle(stream))
 
+    def attention_workspace_bytes(self, batch: int, num_q_heads: int, t_end: int) -> int:
+        return C.tvq_attention_workspace(self.handle, batch, num_q_heads, t_end)
+
+    def attention(self, cache, lay: C.tvq_layout, layer: int, t_end: int, q, out,
+                  scale: float, workspace=None, stream=None) -> None:
+        """Attention of q ([B][Hq][d]) over tokens [0, t_end) of `layer` into out, from the
+        codes (tvq_attention_decode).  `workspace` (a uint8 device tensor) is allocated when
+        not given."""
+        import torch
+        if q.dim() != 3 or out.shape != q.shape or not q.is_contiguous() or \
+                not out.is_contiguous():
+            raise ValueError("q and out must be contiguous [B, Hq, d] tensors")
+        dts = {torch.bfloat16: C.TVQ_BF16, torch.float32: C.TVQ_F32}
+        if q.dtype not in dts or out.dtype not in dts:
+            raise ValueError("q/out must be bf16 or fp32")
+        need = self.attention_workspace_bytes(q.shape[0], q.shape[1], t_end)
+        if workspace is None:
+            workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        C.tvq_attention_decode(self.handle, cache.data_ptr(), lay, layer, t_end, q.shape[1],
+                               scale, dts[q.dtype], q.data_ptr(), dts[out.dtype], out.data_ptr(),
+                               workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
+
     def bits_per_element(self, accounting: int = 0) -> float:
         return C.tvq_bits_per_element(self.handle, accounting)

@@ -488,6 +488,90 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
   return TVQ_OK;
 }
 
+// Tokens per chunk wave of the attention kernels: chunk_tokens * G <= kAttnChunkHeadTokens,
+// a multiple of the tile (64 / (d/32) tokens), at least one tile.
+static uint32_t attn_chunk_tokens(int d, uint32_t G) {
+  const uint32_t vpw = (uint32_t)(tvq::kWave / (d / tvq::kElemsPerLane));
+  uint32_t ch = tvq::kAttnChunkHeadTokens / G;
+  ch -= ch % vpw;
+  return ch < vpw ? vpw : ch;
+}
+
+static tvq_status attn_plan(const tvq_codec* c, int64_t batch, int32_t num_q_heads,
+                            int64_t t_end, uint32_t* chunk, uint32_t* n_chunks,
+                            int64_t* ws_bytes) {
+  if (!c || batch < 1 || t_end < 1 || num_q_heads < c->H || num_q_heads % c->H != 0)
+    return TVQ_ERR_INVALID_ARG;
+  if (c->d != 64 && c->d != 128) return TVQ_ERR_UNSUPPORTED;
+  const uint32_t G = (uint32_t)(num_q_heads / c->H);
+  if (G > tvq::kAttnMaxGroup) return TVQ_ERR_UNSUPPORTED;
+  *chunk = attn_chunk_tokens(c->d, G);
+  *n_chunks = (uint32_t)((t_end + *chunk - 1) / *chunk);
+  const int64_t parts = batch * num_q_heads * (int64_t)*n_chunks;
+  const int64_t acc_bytes = (parts * c->d * 4 + 255) / 256 * 256;
+  *ws_bytes = acc_bytes + parts * 2 * 4;
+  return TVQ_OK;
+}
+
+tvq_status tvq_attention_workspace(const tvq_codec* c, int64_t batch, int32_t num_q_heads,
+                                   int64_t t_end, int64_t* bytes) {
+  if (!bytes) return TVQ_ERR_INVALID_ARG;
+  uint32_t chunk, n_chunks;
+  return attn_plan(c, batch, num_q_heads, t_end, &chunk, &n_chunks, bytes);
+}
+
+tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq_layout* lay,
+                                int32_t layer, int64_t t_end, int32_t num_q_heads, float scale,
+                                tvq_dtype q_dtype, const void* q, tvq_dtype o_dtype, void* o,
+                                void* workspace, int64_t workspace_bytes, void* stream) {
+  if (!c || !lay || !layout_matches(c, lay)) return TVQ_ERR_INVALID_ARG;
+  if (layer < 0 || layer >= c->L || t_end > lay->capacity_tokens) return TVQ_ERR_INVALID_ARG;
+  if ((q_dtype != TVQ_BF16 && q_dtype != TVQ_F32) || (o_dtype != TVQ_BF16 && o_dtype != TVQ_F32))
+    return TVQ_ERR_INVALID_ARG;
+  if (!(scale == scale) || scale > 3.0e38f || scale < -3.0e38f) return TVQ_ERR_INVALID_ARG;
+  uint32_t chunk, n_chunks;
+  int64_t need;
+  const tvq_status st = attn_plan(c, lay->batch, num_q_heads, t_end, &chunk, &n_chunks, &need);
+  if (st != TVQ_OK) return st;
+  for (int kind = 0; kind < 2; ++kind) {
+    const tvq::SegParams& sp = c->segs[2 * layer + kind];
+    if (!tvq::fast_format(sp.n, sp.mode, sp.bits)) return TVQ_ERR_UNSUPPORTED;
+  }
+  if (!cache || !q || !o || !workspace || !aligned16(cache) || !aligned16(q) || !aligned16(o) ||
+      !aligned16(workspace) || workspace_bytes < need)
+    return TVQ_ERR_INVALID_ARG;
+  if ((int64_t)lay->batch * num_q_heads * n_chunks * c->d >= (1ll << 31))
+    return TVQ_ERR_INVALID_ARG;
+
+  tvq::AttnArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.cache = (const uint8_t*)cache;
+  a.n_slots = lay->batch * c->H * lay->capacity_tokens;
+  a.cap = (uint32_t)lay->capacity_tokens;
+  a.segs = c->d_segs;
+  a.sign_masks = c->d_sign_masks;
+  a.lut = c->d_lut;
+  a.q = q;
+  a.o = o;
+  const int64_t parts = lay->batch * num_q_heads * (int64_t)n_chunks;
+  a.ws_acc = (float*)workspace;
+  a.ws_ml = (float*)((char*)workspace + (parts * c->d * 4 + 255) / 256 * 256);
+  a.layer = (uint32_t)layer;
+  a.B = (uint32_t)lay->batch;
+  a.H = (uint32_t)c->H;
+  a.G = (uint32_t)(num_q_heads / c->H);
+  a.Hq = (uint32_t)num_q_heads;
+  a.t_end = (uint32_t)t_end;
+  a.chunk_tokens = chunk;
+  a.n_chunks = n_chunks;
+  const uint32_t vpw = (uint32_t)(tvq::kWave / (c->d / tvq::kElemsPerLane));
+  a.lds_floats_per_wave = 4 * 256 + a.G * c->d + a.G * chunk + vpw * 16;
+  a.qscale = scale * 1.4426950408889634f;          // scores in log2 units
+  const int rc = tvq_launch_attention(a, c->d, q_dtype == TVQ_F32, o_dtype == TVQ_F32, stream);
+  if (rc == -1) return TVQ_ERR_UNSUPPORTED;
+  return rc == 0 ? TVQ_OK : TVQ_ERR_HIP;
+}
+
 double tvq_bits_per_element_config(const tvq_config* cfg, int accounting) {
   if (validate_config(cfg) != TVQ_OK || (accounting != 0 && accounting != 1)) return -1.0;
   const int d = cfg->head_dim;

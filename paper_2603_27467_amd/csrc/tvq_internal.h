@@ -87,6 +87,31 @@ struct DecodeArgs {
   uint32_t num_segs;
 };
 
+// Attention of one query token per sequence over one layer of the cache (tvq_attention_decode).
+// Query heads are grouped over the KV heads: query head h*G + g uses KV head h.  A chunk wave
+// covers `chunk_tokens` tokens of one (batch, KV head) for all G query heads and writes, per
+// query head, the running maximum m (log2 units), the sum l of 2^(s - m) and the accumulated
+// rotated-domain value vector acc[d]; the merge kernel combines the chunks.
+struct AttnArgs {
+  const uint8_t* cache;
+  int64_t n_slots;       // B * H * capacity
+  uint32_t cap;
+  const SegParams* segs;
+  const uint32_t* sign_masks;
+  const float* lut;      // float2 entries, 1/sqrt(d) folded in
+  const void* q;         // [B][Hq][d]
+  void* o;               // [B][Hq][d]
+  float* ws_acc;         // [B*Hq][n_chunks][d]
+  float* ws_ml;          // [B*Hq][n_chunks][2]
+  uint32_t layer, B, H, G, Hq;
+  uint32_t t_end, chunk_tokens, n_chunks;
+  uint32_t lds_floats_per_wave;
+  float qscale;          // scale * log2(e): scores in log2 units
+};
+
+constexpr uint32_t kAttnMaxGroup = 8;         // query heads per KV head (LDS: 52 KiB per block)
+constexpr uint32_t kAttnChunkHeadTokens = 1024;   // chunk_tokens * G
+
 // Segments the multi-tile encode and decode kernels handle: n = 64 or 256 (6- or 8-bit angle
 // codes, every code a valid bin) with 8-bit linear or 4-bit log-space norms.  Other formats go
 // to the single-tile generic kernels.
@@ -103,3 +128,4 @@ int tvq_launch_encode(const tvq::EncodeArgs& a, int d, int in_f32, bool fast, un
                       void* stream);
 int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, unsigned grid,
                       void* stream);
+int tvq_launch_attention(const tvq::AttnArgs& a, int d, int q_f32, int o_f32, void* stream);

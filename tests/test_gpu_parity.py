@@ -447,3 +447,121 @@ def test_long_context_full_size_sampled(gpu):
     assert stats["nonfinite"] == 0
     assert stats["angle_unflagged"] == 0 and stats["norm_unflagged"] == 0
     assert stats["hdr_ulp"] <= 2 and stats["dec_mismatch"] == 0
+
+
+# ---------------------------------------------------------------------------- attention
+def _attention_case(d, G, T, table, seed, q_bf16=False):
+    """Cache of 2 layers, 2 sequences, 2 KV heads, T tokens, encoded on the GPU; queries for
+    G query heads per KV head (bf16-representable when q_bf16)."""
+    import torch
+    L, B, H = 2, 2, 2
+    w = workloads.get("C2")
+    s = Setup(L, H, d, table, workloads.sign_table(seed, L, d)).build()
+    k, v = _draw(w, L, B, H, T, d, "bf16", seed)
+    lay = s.gpu.layout(B, T)
+    cache = torch.zeros((lay.total_bytes,), dtype=torch.uint8, device="cuda")
+    s.gpu.encode(bf16_bits_to_torch(k).cuda(), bf16_bits_to_torch(v).cuda(), cache, lay)
+    rng = np.random.default_rng(seed + 1)
+    q = rng.standard_normal((B, H * G, d)).astype(np.float32) * 2.0
+    if q_bf16:
+        q = (oracle.f32_to_bf16(q).astype(np.uint32) << 16).view(np.float32)
+    torch.cuda.synchronize()
+    return s, lay, cache, q
+
+
+def _attention_check(s, lay, cache, q, layer, t_end, scale, name, q_dtype=None, o_dtype=None):
+    """GPU attention against the oracle's fp64 attention over the same cache bytes.
+
+    Bar, per output vector o of query q (u = 2^-24, fp32 unit roundoff):
+      |o_gpu - o_ref| <= (2 ds + 64 u) max_t |v^_t|  (+ 2^-9 |o_ref| for a bf16 output)
+    where ds = 4 u sqrt(d) |scale| |q| max_t |k^_t| bounds the score error: the fp32 decode of
+    k^ and the d-term dot product each round ~sqrt(d) times at u relative to |q||k^| (random
+    walk, x4 margin).  A score error ds moves the normalized weights by <= 2 ds relative, i.e.
+    o by <= 2 ds max|v^|; the weighted sums and the chunk merge add a few u each.  Normalizing
+    by max|v^| rather than |o| keeps the bar meaningful where the average cancels."""
+    import torch
+    q_dtype = q_dtype or torch.float32
+    o_dtype = o_dtype or torch.float32
+    B, Hq, d = q.shape
+    G = Hq // s.H
+    qd = torch.from_numpy(q).to(q_dtype).cuda()
+    out = torch.full((B, Hq, d), float("nan"), dtype=o_dtype, device="cuda")
+    s.gpu.attention(cache, lay, layer, t_end, qd, out, scale)
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy().astype(np.float64)
+    host = torch_to_np(cache)
+    q64 = qd.float().cpu().numpy().astype(np.float64)
+    ref = s.orc.attention_decode(host, B, lay.capacity_tokens, layer, t_end, q64, scale)
+    dec = s.orc.decode_cache(host, B, lay.capacity_tokens, 0, t_end)[layer]   # [2][B][H][t][d]
+    kmax = np.linalg.norm(dec[0], axis=-1).max(axis=-1)                      # [B][H]
+    vmax = np.linalg.norm(dec[1], axis=-1).max(axis=-1)
+    kmax = np.repeat(kmax, G, axis=1)                                         # [B][Hq]
+    vmax = np.repeat(vmax, G, axis=1)
+    u = 2.0 ** -24
+    ds = 4 * u * np.sqrt(d) * abs(scale) * np.linalg.norm(q64, axis=-1) * kmax
+    bar = (2 * ds + 64 * u) * vmax
+    if o_dtype != torch.float32:
+        bar = bar + 2.0 ** -9 * np.linalg.norm(ref, axis=-1)
+    err = np.linalg.norm(got - ref, axis=-1)
+    rel = err / np.linalg.norm(ref, axis=-1)
+    _say(f"[{name}] t_end={t_end} max |err|/bar = {(err / bar).max():.3f}, max rel L2 "
+         f"= {rel.max():.3e}")
+    assert np.isfinite(got).all()
+    assert (err <= bar).all()
+
+
+@pytest.mark.parametrize("d,G,T,fmt", [
+    (128, 4, 600, "n64-k8lin-v4log"),
+    (128, 4, 600, "n256-k4log-v8lin"),
+    (128, 8, 300, "k256-v64"),
+    (128, 1, 1100, "n64-k8lin-v4log"),
+    (64, 2, 700, "k256-v64"),
+    (64, 3, 200, "n256-k4log-v8lin"),
+])
+def test_attention_matches_oracle(gpu, d, G, T, fmt):
+    """Attention of one query token over the compressed cache (query heads grouped over the
+    KV heads), from the codes, against the oracle's fp64 attention over the decoded cache:
+    several chunks with a ragged last one, one token, and a short range."""
+    tables = {
+        "n64-k8lin-v4log": [LayerCfg(64, 64), LayerCfg(64, 64)],
+        "n256-k4log-v8lin": [LayerCfg(64, 64), LayerCfg(256, 256, 4, 8, NORM_LOG, NORM_LINEAR)],
+        "k256-v64": [LayerCfg(64, 64), LayerCfg(256, 64)],
+    }
+    s, lay, cache, q = _attention_case(d, G, T, tables[fmt], seed=21 + G)
+    scale = 1.0 / np.sqrt(d)
+    for t_end in (1, 17, T):
+        _attention_check(s, lay, cache, q, 1, t_end, scale, f"attn d={d} G={G} {fmt}")
+
+
+def test_attention_dtypes_and_layers(gpu):
+    """bf16 queries and outputs, both layers, a large scale (peaked weights)."""
+    import torch
+    s, lay, cache, q = _attention_case(128, 4, 530, [LayerCfg(256, 256), LayerCfg(64, 64)],
+                                       seed=41, q_bf16=True)
+    for layer in (0, 1):
+        _attention_check(s, lay, cache, q, layer, 530, 0.5, f"attn layer {layer} bf16 q",
+                         q_dtype=torch.bfloat16)
+        _attention_check(s, lay, cache, q, layer, 530, 1.0 / np.sqrt(128), "attn bf16 out",
+                         o_dtype=torch.bfloat16)
+
+
+def test_attention_api_errors(gpu):
+    """Invalid arguments are rejected before any launch; unsupported formats say so."""
+    import torch
+    import paper_2603_27467_amd as tvq
+    s, lay, cache, q = _attention_case(128, 2, 40, [LayerCfg(64, 64), LayerCfg(48, 64)], seed=5)
+    qd = torch.from_numpy(q).cuda()
+    out = torch.empty_like(qd)
+    with pytest.raises(tvq.TvqError, match="unsupported"):
+        s.gpu.attention(cache, lay, 1, 40, qd, out, 0.1)           # n = 48 keys
+    with pytest.raises(tvq.TvqError):
+        s.gpu.attention(cache, lay, 2, 40, qd, out, 0.1)           # no layer 2
+    with pytest.raises(tvq.TvqError):
+        s.gpu.attention(cache, lay, 0, 41, qd, out, 0.1)           # past the capacity
+    with pytest.raises(tvq.TvqError):
+        s.gpu.attention(cache, lay, 0, 0, qd, out, 0.1)            # empty range
+    with pytest.raises(tvq.TvqError):
+        s.gpu.attention(cache, lay, 0, 40, qd[:, :3].contiguous(), out[:, :3].contiguous(), 0.1)
+    small = torch.empty(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(tvq.TvqError):
+        s.gpu.attention(cache, lay, 0, 40, qd, out, 0.1, workspace=small)
