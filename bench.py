@@ -40,12 +40,18 @@ PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "mistral7b_c2_encode_decode_co
 # fp32 VALU issue peak without packed-fp32 instructions: 256 CUs x 4 SIMDs, one wave64
 # instruction per SIMD every 4 cycles, 2.4 GHz
 VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4
-KERNEL_SOURCES = ["tvq_encode.hip", "tvq_decode.hip", "tvq_device.h", "tvq_internal.h"]
+# kernel sources each counter summary depends on: a summary is quoted only while they are
+# unchanged
+CODEC_SOURCES = ["tvq_encode.hip", "tvq_decode.hip", "tvq_codes.h", "tvq_device.h",
+                 "tvq_internal.h"]
+ATTENTION_SOURCES = ["tvq_attention.hip", "tvq_codes.h", "tvq_device.h", "tvq_internal.h"]
+ATTENTION_COUNTERS = os.path.join(ROOT, "profiles", "longctx_c5_attention_counters.json")
+ATTN_GROUP = 4          # query heads per KV head (32 query heads over 8 KV heads)
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(names=None) -> str:
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in names or CODEC_SOURCES:
         with open(os.path.join(ROOT, "paper_2603_27467_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -68,17 +74,18 @@ def algorithmic_bytes(w: workloads.Workload) -> dict:
             "vectors": 2 * w.L * w.B * w.H * w.T}
 
 
-def profile_entry(kernel: str):
-    """The committed counter summary of `kernel` ("tvq_encode" / "tvq_decode"): HBM bytes per
-    launch from rocprofv3 FETCH_SIZE / WRITE_SIZE scaled by the same counters on a copy of known
-    size, VALU instructions per launch and VALU busy.  None when absent or when the kernel
-    sources have changed since the counters were taken."""
+def profile_entry(kernel: str, path: str = PROFILE_COUNTERS, sources=None):
+    """The committed counter summary of `kernel` ("tvq_encode" / "tvq_decode" in the codec
+    summary, "tvq_attention" in the long-context one): HBM bytes per launch from rocprofv3
+    FETCH_SIZE / WRITE_SIZE scaled by the same counters on a copy of known size, VALU
+    instructions per launch and VALU busy.  None when absent or when the kernel sources have
+    changed since the counters were taken."""
     try:
-        with open(PROFILE_COUNTERS) as f:
+        with open(path) as f:
             d = json.load(f)
     except (OSError, ValueError):
         return None
-    if d.get("kernel_source_hash") != kernel_source_hash():
+    if d.get("kernel_source_hash") != kernel_source_hash(sources):
         return None
     return d.get("kernels", {}).get(kernel)
 
@@ -164,6 +171,10 @@ def _short(name: str) -> str:
         return "tvq_encode"
     if "decode_" in name and "tvq" in name:
         return "tvq_decode"
+    if "attn_chunk" in name and "tvq" in name:
+        return "tvq_attention_chunk"
+    if "attn_merge" in name and "tvq" in name:
+        return "tvq_attention_merge"
     if "copyBuffer" in name:
         return "copy"
     return name
@@ -271,6 +282,132 @@ def summarize_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, comman
     return 0
 
 
+def copy_calibration() -> None:
+    """A plain 1 GiB device copy: what FETCH_SIZE and WRITE_SIZE read for it scales them."""
+    import torch
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def longctx_bytes(w: workloads.Workload):
+    """(compressed bytes of one token position over all layers, kinds, sequences and KV heads;
+    bf16 K + V bytes of one token position; bf16 query + output bytes of one attention step)."""
+    P = w.d // 2
+    rec_tok = 0
+    for t in w.table:
+        for n, mode, bits in ((t.n_k, t.norm_mode_k, t.norm_bits_k),
+                              (t.n_v, t.norm_mode_v, t.norm_bits_v)):
+            wbits = int(np.ceil(np.log2(n)))
+            rec_tok += (P * wbits // 8 + (4 * P if mode == 0 else P * bits // 8 + 8)) * w.B * w.H
+    kv_tok = 2 * w.L * w.B * w.H * w.d * 2
+    qo = 2 * w.L * w.B * w.H * ATTN_GROUP * w.d * 2
+    return rec_tok, kv_tok, qo
+
+
+def summarize_attention_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, commands,
+                                 steps_total: int) -> int:
+    """Counter summary of the long-context attention step (the runs of `commands`, each with
+    `steps_total` = warmup + timed steps): per chunk-kernel instantiation and for the merge
+    kernel, HBM bytes per dispatch (FETCH_SIZE / WRITE_SIZE scaled by the 1 GiB copy), VALU and
+    LDS instructions, bank-conflict cycles and VALU busy; and the HBM bytes of one step."""
+    w = workloads.get("C5")
+    rec_tok, _, qo = longctx_bytes(w)
+    t_mean = w.T + (steps_total + 1) / 2            # tokens attended per step, mean
+    per = {}
+
+    def add(kind, rows, counter):
+        for r in rows:
+            if r["Counter_Name"] != counter:
+                continue
+            k = _short(r["Kernel_Name"])
+            if k.startswith("tvq_attention"):
+                k = _kernel_label(r["Kernel_Name"])
+            per.setdefault(k, {}).setdefault(kind, []).append(float(r["Counter_Value"]))
+
+    add("fetch_kib", _csv(_find(fetch_dir, "counter_collection.csv")), "FETCH_SIZE")
+    add("write_kib", _csv(_find(write_dir, "counter_collection.csv")), "WRITE_SIZE")
+    sq = _csv(_find(sq_dir, "counter_collection.csv"))
+    for c in ("SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_WAVES"):
+        add(c, sq, c)
+    add("VALUBusy", _csv(_find(valu_dir, "counter_collection.csv")), "VALUBusy")
+    fetch_scale = float(1 << 30) / 1024.0 / max(per["copy"]["fetch_kib"])
+    write_scale = float(1 << 30) / 1024.0 / max(per["copy"]["write_kib"])
+    trace = {}
+    for r in _csv(_find(trace_dir, "kernel_stats.csv")):
+        if _short(r["Name"]).startswith("tvq_attention"):
+            trace[_kernel_label(r["Name"])] = {"calls": int(r["Calls"]),
+                                              "avg_ns": float(r["AverageNs"]),
+                                              "min_ns": float(r["MinNs"]),
+                                              "max_ns": float(r["MaxNs"])}
+    kernels, hbm_step, valu_step, conf_step, busy = {}, 0.0, 0.0, 0.0, []
+    for k, d in sorted(per.items()):
+        if "attn_" not in k:
+            continue
+        per_step = len(d["fetch_kib"]) / steps_total
+        fetch = float(np.median(d["fetch_kib"])) * 1024.0 * fetch_scale
+        write = float(np.median(d["write_kib"])) * 1024.0 * write_scale
+        kernels[k] = {"dispatches_per_step": per_step,
+                      "fetch_bytes_per_dispatch": int(round(fetch)),
+                      "write_bytes_per_dispatch": int(round(write)),
+                      "valu_insts_per_dispatch": int(np.median(d["SQ_INSTS_VALU"])),
+                      "lds_insts_per_dispatch": int(np.median(d["SQ_INSTS_LDS"])),
+                      "lds_bank_conflict_cycles_per_dispatch":
+                          int(np.median(d["SQ_LDS_BANK_CONFLICT"])),
+                      "waves_per_dispatch": int(np.median(d["SQ_WAVES"])),
+                      "valu_busy_pct": round(float(np.median(d["VALUBusy"])), 2)}
+        hbm_step += per_step * (fetch + write)
+        if "chunk" in k:
+            valu_step += per_step * float(np.median(d["SQ_INSTS_VALU"]))
+            conf_step += per_step * float(np.median(d["SQ_LDS_BANK_CONFLICT"]))
+            busy += [float(np.median(d["VALUBusy"]))] * int(round(per_step))
+    tiles_step = w.L * w.B * w.H * t_mean / (64 // (w.d // 32))
+    ent = {"hbm_bytes_per_step": int(round(hbm_step)),
+           "algorithmic_bytes_per_step": int(round(rec_tok * t_mean + qo)),
+           "valu_insts_per_tile": round(valu_step / tiles_step, 1),
+           "lds_bank_conflict_cycles_per_tile": round(conf_step / tiles_step, 1),
+           "valu_busy_pct": round(float(np.mean(busy)), 2),
+           "per_kernel": kernels, "trace": trace}
+    out = {"kernel_source_hash": kernel_source_hash(ATTENTION_SOURCES), "workload": w.name,
+           "query_heads_per_kv_head": ATTN_GROUP, "tokens_attended_mean": t_mean,
+           "fetch_scale_from_copy": round(fetch_scale, 4),
+           "write_scale_from_copy": round(write_scale, 4), "commands": commands,
+           "kernels": {"tvq_attention": ent}}
+    lines = [f"# Counter summary: attention over the compressed cache, {w.name} (L={w.L}, "
+             f"B={w.B}, KV heads={w.H}, query heads={w.H * ATTN_GROUP}, T={w.T}, d={w.d})",
+             "", "Commands (run from /tmp, repository root $R):", ""]
+    lines += [f"    {c}" for c in commands]
+    lines += ["", f"FETCH_SIZE scale from the 1 GiB copy: {fetch_scale:.4f}; WRITE_SIZE scale: "
+              f"{write_scale:.4f}; tokens attended per step (mean): {t_mean}", "",
+              f"Per step (32 layer calls): HBM {ent['hbm_bytes_per_step']} B by counters vs "
+              f"{ent['algorithmic_bytes_per_step']} B algorithmic; VALU {ent['valu_insts_per_tile']}"
+              f" instructions per tile of 16 tokens; LDS bank-conflict cycles per tile "
+              f"{ent['lds_bank_conflict_cycles_per_tile']}; VALUBusy {ent['valu_busy_pct']} %", "",
+              "| kernel | dispatches/step | avg ns (trace) | fetch B/dispatch | write B/dispatch | "
+              "VALU/dispatch | LDS/dispatch | bank-conflict cycles | VALUBusy % |",
+              "|---|---|---|---|---|---|---|---|---|"]
+    for k, e in kernels.items():
+        tr = trace.get(k, {})
+        lines.append(f"| {k} | {e['dispatches_per_step']:.0f} | {tr.get('avg_ns', 0):.0f} | "
+                     f"{e['fetch_bytes_per_dispatch']} | {e['write_bytes_per_dispatch']} | "
+                     f"{e['valu_insts_per_dispatch']} | {e['lds_insts_per_dispatch']} | "
+                     f"{e['lds_bank_conflict_cycles_per_dispatch']} | {e['valu_busy_pct']} |")
+    lines += ["", "rocprofv3 --kernel-trace --stats summary of the first command "
+              "(kernel_stats.csv, codec and attention kernels):", "", "```"]
+    with open(_find(trace_dir, "kernel_stats.csv")) as f:
+        rows = [ln.rstrip("\n") for ln in f]
+    lines += [rows[0]] + [r for r in rows[1:] if "tvq::" in r]
+    lines += ["```"]
+    with open(ATTENTION_COUNTERS, "w") as f:
+        json.dump(out, f, indent=1)
+    with open(ATTENTION_COUNTERS.replace("_counters.json", "_counters.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
+
+
 def run_longctx(w: workloads.Workload, args) -> dict:
     """Long-context step: the cache already holds T tokens of B sequences (every layer, K and
     V); one step encodes one new token per sequence and layer into slot T + i and decodes
@@ -303,8 +440,18 @@ def run_longctx(w: workloads.Workload, args) -> dict:
     workloads.fill_device(w, "K", kn, token_part=1)
     vn = torch.empty_like(kn)
     workloads.fill_device(w, "V", vn, token_part=1)
-    ko = torch.empty((w.L, w.B, w.H, cap, w.d), dtype=torch.bfloat16, device="cuda")
-    vo = torch.empty_like(ko)
+    if args.attention:
+        Hq = w.H * ATTN_GROUP
+        g = torch.Generator(device="cuda")
+        g.manual_seed(w.data_seed + 7)
+        qs = torch.randn((w.L, w.B, Hq, w.d), generator=g, device="cuda").to(torch.bfloat16)
+        os_ = torch.empty_like(qs)
+        ws = torch.empty(codec.attention_workspace_bytes(w.B, Hq, cap), dtype=torch.uint8,
+                         device="cuda")
+        scale = 1.0 / float(np.sqrt(w.d))
+    else:
+        ko = torch.empty((w.L, w.B, w.H, cap, w.d), dtype=torch.bfloat16, device="cuda")
+        vo = torch.empty_like(ko)
 
     def step(i, ev=None):
         t = w.T + i
@@ -313,7 +460,13 @@ def run_longctx(w: workloads.Workload, args) -> dict:
         codec.encode(kn[:, :, :, i:i + 1], vn[:, :, :, i:i + 1], cache, lay, t, stream)
         if ev is not None:
             ev[1].record(stream)
-        codec.decode(cache, lay, 0, t + 1, ko[:, :, :, :t + 1], vo[:, :, :, :t + 1], stream)
+        if args.attention:
+            for layer in range(w.L):
+                codec.attention(cache, lay, layer, t + 1, qs[layer], os_[layer], scale, ws,
+                                stream)
+        else:
+            codec.decode(cache, lay, 0, t + 1, ko[:, :, :, :t + 1], vo[:, :, :, :t + 1],
+                         stream)
         if ev is not None:
             ev[2].record(stream)
 
@@ -321,6 +474,8 @@ def run_longctx(w: workloads.Workload, args) -> dict:
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
+    if args.copy_calibration:
+        copy_calibration()
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     print(f"# timing {args.steps} steps", file=sys.stderr, flush=True)
     t_wall = time.perf_counter()
@@ -333,20 +488,47 @@ def run_longctx(w: workloads.Workload, args) -> dict:
     span_ms = ev[0][0].elapsed_time(ev[-1][2]) / args.steps
     ms_per_step = max(span_ms, float(enc.mean() + dec.mean()))
     # bytes of the timed steps, per step on average (the decoded range grows by one token)
-    P = w.d // 2
-    rec_tok = 0                       # compressed bytes of one token position, all (b, h)
-    for t in w.table:
-        for n, mode, bits in ((t.n_k, t.norm_mode_k, t.norm_bits_k),
-                              (t.n_v, t.norm_mode_v, t.norm_bits_v)):
-            wbits = int(np.ceil(np.log2(n)))
-            rec_tok += (P * wbits // 8 + (4 * P if mode == 0 else P * bits // 8 + 8)) * w.B * w.H
-    kv_tok = 2 * w.L * w.B * w.H * w.d * 2          # bf16 K + V bytes of one token position
+    rec_tok, kv_tok, qo = longctx_bytes(w)
     t_mean = w.T + args.warmup + (args.steps - 1) / 2 + 1    # tokens decoded per step, mean
-    dec_bytes = (rec_tok + kv_tok) * t_mean
     enc_bytes = rec_tok + kv_tok
     dec_ms = float(dec.mean())
-    dec_gbs = dec_bytes / (dec_ms * 1e-3) / 1e9
     value = (kv_tok + kv_tok * t_mean) / (ms_per_step * 1e-3) / 1e9
+    if args.attention:
+        # codes of every cached token once, plus the bf16 queries and outputs of every layer
+        att_bytes = rec_tok * t_mean + qo
+        prof = profile_entry("tvq_attention", ATTENTION_COUNTERS, ATTENTION_SOURCES)
+        att_gbs = att_bytes / (dec_ms * 1e-3) / 1e9
+        return {
+            "metric": "attention over the compressed cache: bf16-equivalent KV GB/s consumed",
+            "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "f32", "data": "synthetic",
+            "config": {"workload": w.name, "layers": w.L, "batch": w.B, "kv_heads": w.H,
+                       "q_heads": w.H * ATTN_GROUP, "tokens_cached": w.T, "head_dim": w.d,
+                       "io_dtype": w.dtype, "table": w.notes,
+                       "step": "encode 1 token per sequence and layer, then attention of one "
+                               "query token per sequence over the whole cache, every layer",
+                       "compressed_bytes_per_token": rec_tok},
+            "roofline": {"bound": "hbm", "kernel": "tvq_attention (chunk + merge)",
+                         "achieved": round(att_gbs, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                         "frac": round(att_gbs / HBM_PEAK_GBPS, 4),
+                         "traffic": None if prof is None else prof["hbm_bytes_per_step"],
+                         "algorithmic_bytes_per_step": int(att_bytes)},
+            "encode": {"ms": round(float(enc.mean()), 5), "ms_min": round(float(enc.min()), 5)},
+            "attention": {"ms": round(dec_ms, 5), "ms_median": round(float(np.median(dec)), 5),
+                          "ms_min": round(float(dec.min()), 5),
+                          "ms_per_layer": round(dec_ms / w.L, 5),
+                          "hbm_GBps_algorithmic": round(att_gbs, 2)},
+            "counters": None if prof is None else {
+                k: prof[k] for k in ("hbm_bytes_per_step", "algorithmic_bytes_per_step",
+                                     "valu_insts_per_tile", "valu_busy_pct",
+                                     "lds_bank_conflict_cycles_per_tile")},
+            "wall_s_timed": round(wall_s, 4),
+            "kernel_source_hash": kernel_source_hash(ATTENTION_SOURCES),
+        }
+    dec_bytes = (rec_tok + kv_tok) * t_mean
+    dec_gbs = dec_bytes / (dec_ms * 1e-3) / 1e9
     return {
         "metric": METRIC,
         "value": round(value, 2),
@@ -388,16 +570,26 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="C2")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--attention", action="store_true",
+                    help="long-context workload: attention over the compressed cache in place "
+                         "of the full decode")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for counter scaling)")
     ap.add_argument("--summarize-profiles", nargs=5,
                     metavar=("TRACE", "FETCH", "WRITE", "SQ", "VALU"),
                     help="write the profiles/ counter summary from rocprofv3 output dirs")
+    ap.add_argument("--summarize-attention-profiles", nargs=6,
+                    metavar=("TRACE", "FETCH", "WRITE", "SQ", "VALU", "STEPS_TOTAL"),
+                    help="write the profiles/ counter summary of the long-context attention "
+                         "step from rocprofv3 output dirs")
     ap.add_argument("--commands", nargs="*", default=[],
                     help="the profiling commands, recorded in the summary")
     args = ap.parse_args()
     if args.summarize_profiles:
         return summarize_profiles(*args.summarize_profiles, args.commands)
+    if args.summarize_attention_profiles:
+        a = args.summarize_attention_profiles
+        return summarize_attention_profiles(*a[:5], args.commands, int(a[5]))
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the codec is per-vector and this build measures "
               "one GPU's share; --gpus above 1 is not supported", file=sys.stderr)
@@ -453,11 +645,7 @@ def main() -> int:
     torch.cuda.synchronize()
 
     if args.copy_calibration:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        copy_calibration()
 
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     print(f"# timing {args.steps} steps", file=sys.stderr, flush=True)

@@ -156,9 +156,13 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
  *   t_end      1 .. lay->capacity_tokens tokens attended (slots [0, t_end))
  *   workspace  device scratch of at least tvq_attention_workspace(...) bytes, 16-byte
  *              aligned, owned by the caller; its contents are overwritten
- * Arithmetic is fp32 (expect ~1e-5 relative to an fp64 evaluation).  Supported: d = 64 or
- * 128, G <= 8, and for both K and V of the layer n = 64 or 256 with 8-bit linear or 4-bit
- * log-space norms (TVQ_ERR_UNSUPPORTED otherwise).  Launches two kernels on `stream`. */
+ * The token range is split into chunks (a power of two of at least 4 tiles, sized from B, H,
+ * G and t_end); the workspace holds one partial (max, sum, d accumulators) per query head and
+ * chunk.  Query heads are processed up to 4 per pass over the codes (G > 4 reads them
+ * ceil(G/4) times).  Arithmetic is fp32 (expect ~1e-5 relative to an fp64 evaluation).
+ * Supported: d = 64 or 128, G <= 64, and for both K and V of the layer n = 64 or 256 with
+ * 8-bit linear or 4-bit log-space norms (TVQ_ERR_UNSUPPORTED otherwise).  Launches two
+ * kernels on `stream`. */
 tvq_status tvq_attention_workspace(const tvq_codec* c, int64_t batch, int32_t num_q_heads,
                                    int64_t t_end, int64_t* bytes);
 tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq_layout* lay,

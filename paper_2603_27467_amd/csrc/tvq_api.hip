@@ -490,34 +490,45 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
 
 // Tokens per chunk wave of the attention kernels: chunk_tokens * G <= kAttnChunkHeadTokens,
 // a multiple of the tile (64 / (d/32) tokens), at least one tile.
-static uint32_t attn_chunk_tokens(int d, uint32_t G) {
-  const uint32_t vpw = (uint32_t)(tvq::kWave / (d / tvq::kElemsPerLane));
-  uint32_t ch = tvq::kAttnChunkHeadTokens / G;
-  ch -= ch % vpw;
-  return ch < vpw ? vpw : ch;
+// Tokens per chunk wave: a power of two (at least 4 tiles) chosen so that a launch has about
+// kAttnTargetWaves chunk waves, at most 4096.
+static uint32_t attn_chunk_tokens(int d, int64_t waves_per_chunk_row, int64_t t_end) {
+  const int64_t vpw = tvq::kWave / (d / tvq::kElemsPerLane);
+  const int64_t want = waves_per_chunk_row * t_end / (int64_t)tvq::kAttnTargetWaves;
+  int64_t ch = 4 * vpw;
+  while (ch < 4096 && 2 * ch <= want) ch *= 2;
+  return (uint32_t)ch;
 }
 
+struct AttnPlan {
+  uint32_t G, pass_heads, n_pass, chunk, n_chunks;
+  int64_t acc_bytes, ws_bytes;
+};
+
 static tvq_status attn_plan(const tvq_codec* c, int64_t batch, int32_t num_q_heads,
-                            int64_t t_end, uint32_t* chunk, uint32_t* n_chunks,
-                            int64_t* ws_bytes) {
+                            int64_t t_end, AttnPlan* p) {
   if (!c || batch < 1 || t_end < 1 || num_q_heads < c->H || num_q_heads % c->H != 0)
     return TVQ_ERR_INVALID_ARG;
   if (c->d != 64 && c->d != 128) return TVQ_ERR_UNSUPPORTED;
-  const uint32_t G = (uint32_t)(num_q_heads / c->H);
-  if (G > tvq::kAttnMaxGroup) return TVQ_ERR_UNSUPPORTED;
-  *chunk = attn_chunk_tokens(c->d, G);
-  *n_chunks = (uint32_t)((t_end + *chunk - 1) / *chunk);
-  const int64_t parts = batch * num_q_heads * (int64_t)*n_chunks;
-  const int64_t acc_bytes = (parts * c->d * 4 + 255) / 256 * 256;
-  *ws_bytes = acc_bytes + parts * 2 * 4;
+  p->G = (uint32_t)(num_q_heads / c->H);
+  if (p->G > tvq::kAttnMaxGroup) return TVQ_ERR_UNSUPPORTED;
+  p->n_pass = (p->G + tvq::kAttnPassHeads - 1) / tvq::kAttnPassHeads;
+  p->pass_heads = (p->G + p->n_pass - 1) / p->n_pass;          // balanced passes
+  p->chunk = attn_chunk_tokens(c->d, batch * c->H * p->n_pass, t_end);
+  p->n_chunks = (uint32_t)((t_end + p->chunk - 1) / p->chunk);
+  const int64_t parts = batch * num_q_heads * (int64_t)p->n_chunks;
+  p->acc_bytes = (parts * c->d * 4 + 255) / 256 * 256;
+  p->ws_bytes = p->acc_bytes + parts * 2 * 4;
   return TVQ_OK;
 }
 
 tvq_status tvq_attention_workspace(const tvq_codec* c, int64_t batch, int32_t num_q_heads,
                                    int64_t t_end, int64_t* bytes) {
   if (!bytes) return TVQ_ERR_INVALID_ARG;
-  uint32_t chunk, n_chunks;
-  return attn_plan(c, batch, num_q_heads, t_end, &chunk, &n_chunks, bytes);
+  AttnPlan p;
+  const tvq_status st = attn_plan(c, batch, num_q_heads, t_end, &p);
+  if (st == TVQ_OK) *bytes = p.ws_bytes;
+  return st;
 }
 
 tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq_layout* lay,
@@ -529,18 +540,20 @@ tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq
   if ((q_dtype != TVQ_BF16 && q_dtype != TVQ_F32) || (o_dtype != TVQ_BF16 && o_dtype != TVQ_F32))
     return TVQ_ERR_INVALID_ARG;
   if (!(scale == scale) || scale > 3.0e38f || scale < -3.0e38f) return TVQ_ERR_INVALID_ARG;
-  uint32_t chunk, n_chunks;
-  int64_t need;
-  const tvq_status st = attn_plan(c, lay->batch, num_q_heads, t_end, &chunk, &n_chunks, &need);
+  AttnPlan p;
+  const tvq_status st = attn_plan(c, lay->batch, num_q_heads, t_end, &p);
   if (st != TVQ_OK) return st;
+  int fmt[2];
   for (int kind = 0; kind < 2; ++kind) {
     const tvq::SegParams& sp = c->segs[2 * layer + kind];
     if (!tvq::fast_format(sp.n, sp.mode, sp.bits)) return TVQ_ERR_UNSUPPORTED;
+    fmt[kind] = (sp.n == 256 ? 1 : 0) | (sp.mode == 2 ? 2 : 0);
   }
   if (!cache || !q || !o || !workspace || !aligned16(cache) || !aligned16(q) || !aligned16(o) ||
-      !aligned16(workspace) || workspace_bytes < need)
+      !aligned16(workspace) || workspace_bytes < p.ws_bytes)
     return TVQ_ERR_INVALID_ARG;
-  if ((int64_t)lay->batch * num_q_heads * n_chunks * c->d >= (1ll << 31))
+  if ((int64_t)lay->batch * num_q_heads * p.n_chunks * c->d >= (1ll << 31) ||
+      (int64_t)lay->batch * c->H * p.n_chunks * p.n_pass >= (1ll << 31))
     return TVQ_ERR_INVALID_ARG;
 
   tvq::AttnArgs a;
@@ -553,21 +566,21 @@ tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq
   a.lut = c->d_lut;
   a.q = q;
   a.o = o;
-  const int64_t parts = lay->batch * num_q_heads * (int64_t)n_chunks;
   a.ws_acc = (float*)workspace;
-  a.ws_ml = (float*)((char*)workspace + (parts * c->d * 4 + 255) / 256 * 256);
+  a.ws_ml = (float*)((char*)workspace + p.acc_bytes);
   a.layer = (uint32_t)layer;
   a.B = (uint32_t)lay->batch;
   a.H = (uint32_t)c->H;
-  a.G = (uint32_t)(num_q_heads / c->H);
+  a.G = p.G;
   a.Hq = (uint32_t)num_q_heads;
   a.t_end = (uint32_t)t_end;
-  a.chunk_tokens = chunk;
-  a.n_chunks = n_chunks;
-  const uint32_t vpw = (uint32_t)(tvq::kWave / (c->d / tvq::kElemsPerLane));
-  a.lds_floats_per_wave = 4 * 256 + a.G * c->d + a.G * chunk + vpw * 16;
+  a.chunk_tokens = p.chunk;
+  a.n_chunks = p.n_chunks;
+  a.pass_heads = p.pass_heads;
+  a.n_pass = p.n_pass;
+  a.q_f32 = q_dtype == TVQ_F32 ? 1u : 0u;
   a.qscale = scale * 1.4426950408889634f;          // scores in log2 units
-  const int rc = tvq_launch_attention(a, c->d, q_dtype == TVQ_F32, o_dtype == TVQ_F32, stream);
+  const int rc = tvq_launch_attention(a, c->d, fmt[0], fmt[1], o_dtype == TVQ_F32, stream);
   if (rc == -1) return TVQ_ERR_UNSUPPORTED;
   return rc == 0 ? TVQ_OK : TVQ_ERR_HIP;
 }

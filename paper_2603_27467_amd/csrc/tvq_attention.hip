@@ -13,17 +13,18 @@
 // form it (same tables, same fp32 operation order).
 //
 // Split over tokens (split-K): a chunk wave takes `chunk_tokens` tokens of one (sequence, KV
-// head) for all G query heads.
-//   prologue  q^_g = scale * log2(e) * W D q_g into LDS (the d/32 lanes of "vector" g)
-//   pass 1    per tile of 64/(d/32) tokens: y'_K from the K codes, scores s = q^_g . y'_K
-//             (each lane its 32 elements, then a sum over the vector's lanes) into LDS
-//   pass 2    per pair of query heads: m = max s over the chunk, then per tile y'_V from the
-//             V codes, acc += 2^(s - m) y'_V and l += 2^(s - m), summed over the wave at the end
-//   out       (m, l, acc[d]) per query head and chunk into the workspace
-// The merge kernel combines the chunks of each output, M = max m_c, L = sum l_c 2^(m_c - M),
-// A = sum acc_c 2^(m_c - M), and stores D W (A / L).  Both passes load the next tile's codes
-// while working on the current one.  All arithmetic is fp32; scores are in log2 units so the
-// weights are one v_exp_f32 each.
+// head) for up to four of the G query heads (G > 4 runs in passes of balanced size).
+//   prologue  q^_g = scale * log2(e) * W D q_g into LDS (the d/32 lanes of vector slot g)
+//   per tile  of 64/(d/32) tokens, one token per vector slot: y'_K from the K codes, the
+//             scores s_g = q^_g . y'_K, then y'_V from the V codes and, per head,
+//             acc_g += 2^(s_g - m_g) y'_V and l_g += 2^(s_g - m_g)
+//   out       (m, l, acc[d]) per query head and chunk into the workspace, summed over the slots
+// m_g is a reference point shared by the wave, not the running maximum: it is raised (and acc,
+// l rescaled) only when a score exceeds it by more than kLazyLog2, so every weight stays below
+// 2^kLazyLog2 and the rescale runs on a few tiles of a chunk.  The merge kernel combines the
+// chunks of each output, M = max m_c, L = sum l_c 2^(m_c - M), A = sum acc_c 2^(m_c - M), and
+// stores D W (A / L).  The next tile's codes load while the current one is worked on.  All
+// arithmetic is fp32; scores are in log2 units so each weight is one v_exp_f32.
 #include <float.h>
 #include <hip/hip_runtime.h>
 
@@ -34,7 +35,12 @@
 namespace tvq {
 namespace {
 
-constexpr int kLut = 256;   // entries of each staged table (the formats here have n <= 256)
+constexpr int kLut = 256;            // entries of each staged table (the formats here: n <= 256)
+constexpr float kLazyLog2 = 8.0f;    // weights 2^(s - m) stay below 2^8 between rescales
+// q^ in LDS: each lane's 32 elements of a head at a pitch of 36 floats, so the d/32 distinct
+// 16-byte reads of a wave (one per lane of a vector, broadcast over the vector slots) fall in
+// distinct banks
+constexpr int kQPitch = kElemsPerLane + 4;
 
 template <int LPV>
 __device__ __forceinline__ float vec_sum(float v) {
@@ -49,59 +55,84 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Sum over the wave's vector slots (lanes sub, sub + LPV, ...): every lane gets its sub's sum.
+template <int LPV>
+__device__ __forceinline__ float slot_sum(float v) {
+#pragma unroll
+  for (int o = LPV; o < kWave; o <<= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
 template <int D>
 struct AttnWave {
   static constexpr int LPV = D / kElemsPerLane;
   static constexpr int VPW = kWave / LPV;
   int lane, sub, vslot;
-  uint32_t b, h, chunk;
+  uint32_t b, h, chunk, g0, gc;  // query heads g0 .. g0 + gc - 1 of KV head h
   uint32_t t0, ntok;             // the chunk's tokens [t0, t0 + ntok)
   uint32_t row;                  // cache slot of token 0 of (b, h)
   SegParams sp[2];               // K and V of the layer
   const uint8_t* plane[2][3];
-  float2* lut[2];                // the two cos/sin tables in LDS
-  float* qh;                     // LDS [G][D]
-  float* sc;                     // LDS [G][chunk_tokens]
-  float* lvl;                    // LDS level table, 16 per vector
 };
 
-template <int D>
-__device__ __forceinline__ bool attn_setup(const AttnArgs& a, AttnWave<D>& w, float* lds) {
-  w.lane = threadIdx.x & (kWave - 1);
-  w.sub = w.lane % AttnWave<D>::LPV;
-  w.vslot = w.lane / AttnWave<D>::LPV;
-  const uint32_t wib = threadIdx.x / kWave;
-  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + wib);
-  if (wave >= a.B * a.H * a.n_chunks) return false;
-  const uint32_t bh = wave / a.n_chunks;
-  w.chunk = wave - bh * a.n_chunks;
-  w.b = bh / a.H;
-  w.h = bh - w.b * a.H;
-  w.t0 = w.chunk * a.chunk_tokens;
-  w.ntok = min(a.chunk_tokens, a.t_end - w.t0);
-  w.row = bh * a.cap;
-  float* base = lds + wib * a.lds_floats_per_wave;
-  w.lut[0] = (float2*)base;
-  w.lut[1] = w.lut[0] + kLut;
-  w.qh = (float*)(w.lut[1] + kLut);
-  w.sc = w.qh + a.G * D;
-  w.lvl = w.sc + a.G * a.chunk_tokens;
-  for (int kind = 0; kind < 2; ++kind) {
-    w.sp[kind] = a.segs[2 * a.layer + kind];
-    for (int p = 0; p < 3; ++p) w.plane[kind][p] = a.cache + a.n_slots * w.sp[kind].pre[p];
-    const float2* src = (const float2*)a.lut + w.sp[kind].lut_off;
-    for (uint32_t e = w.lane; e < w.sp[kind].n; e += kWave) w.lut[kind][e] = src[e];
+// y' of this lane's 32 elements of a token from its codes, in the decode kernels' operation
+// order: r^ from the norm codes, y'_2i = RN(r^_i C'[k_i]), y'_2i+1 = RN(r^_i S'[k_i]).  `lvl`
+// is the vector slot's 16-entry level table (log-space norms).
+template <int LPV, int WA, int NB>
+__device__ __forceinline__ void code_vector(const TileCodes<WA, NB>& c, const float2* lut,
+                                            float* lvl, int sub, float (&y)[kElemsPerLane]) {
+  constexpr uint32_t kLevels = (1u << NB) - 1u;
+  uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
+  unpack16_index<WA>(c.ang, kc);
+  if constexpr (NB == 8) unpack16<NB>(c.nrm, qc);
+  else unpack16_index<NB>(c.nrm, qc);
+  const float rmin = __uint_as_float(c.hdr.x), rmax = __uint_as_float(c.hdr.y);
+  float r[kPairsPerLane];
+  if constexpr (NB == 8) {
+    const float step = rmax == rmin ? 0.0f : (rmax - rmin) / (float)kLevels;
+#pragma unroll
+    for (int i = 0; i < kPairsPerLane; ++i) r[i] = __builtin_fmaf((float)qc[i], step, rmin);
+  } else {
+    wave_lds_sync();                    // the previous tile's reads of the table are done
+    log_level_ladder<LPV>(lvl, sub, rmin, rmax, kLevels);
+    wave_lds_sync();
+#pragma unroll
+    for (int i = 0; i < kPairsPerLane; ++i) r[i] = lvl[qc[i]];
   }
-  return true;
+#pragma unroll
+  for (int i = 0; i < kPairsPerLane; ++i) {
+    const float2 cs = lut[kc[i]];
+    y[2 * i] = r[i] * cs.x;
+    y[2 * i + 1] = r[i] * cs.y;
+  }
 }
 
-// q^_g = scale * log2(e) * W D q_g of the G query heads into LDS: head g on the lanes of
-// vector slot g (the other slots repeat head 0 and store nothing).
+template <int KW, int KN, int VW, int VN>
+struct TilePair {
+  TileCodes<KW, KN> k;
+  TileCodes<VW, VN> v;
+};
+
+template <int D, int KW, int KN, int VW, int VN>
+__device__ __forceinline__ TilePair<KW, KN, VW, VN> tile_pair(const AttnWave<D>& w,
+                                                              uint32_t tile) {
+  // slots past the chunk read its last token (in bounds) and get weight 0
+  const uint32_t j = min(tile * AttnWave<D>::VPW + w.vslot, w.ntok - 1);
+  const uint32_t slot = w.row + w.t0 + j;
+  TilePair<KW, KN, VW, VN> p;
+  p.k = load_codes_at<KW, KN>(w.plane[0], w.sp[0].rec, slot, w.sub);
+  p.v = load_codes_at<VW, VN>(w.plane[1], w.sp[1].rec, slot, w.sub);
+  return p;
+}
+
+// q^_g = scale * log2(e) * W D q_g of the pass's query heads into LDS: head g0 + g on the lanes
+// of vector slot g (the other slots repeat the first head and store nothing).
 template <int D, bool F32Q>
-__device__ __forceinline__ void query_transform(const AttnArgs& a, const AttnWave<D>& w) {
+__device__ __forceinline__ void query_transform(const AttnArgs& a, const AttnWave<D>& w,
+                                                float* qh) {
   constexpr int LPV = AttnWave<D>::LPV;
-  const uint32_t g = (uint32_t)w.vslot < a.G ? (uint32_t)w.vslot : 0u;
-  const uint64_t elem = ((uint64_t)w.b * a.Hq + w.h * a.G + g) * D + w.sub * kElemsPerLane;
+  const uint32_t g = (uint32_t)w.vslot < w.gc ? (uint32_t)w.vslot : 0u;
+  const uint64_t elem = ((uint64_t)w.b * a.Hq + w.h * a.G + w.g0 + g) * D + w.sub * kElemsPerLane;
   uint32_t sm[16];
   load_words<16>(a.sign_masks + (size_t)a.layer * (D / 2) + w.sub * 16, sm);
   float x[kElemsPerLane];
@@ -126,84 +157,33 @@ __device__ __forceinline__ void query_transform(const AttnArgs& a, const AttnWav
   fwht_in_lane(x);
   fwht_cross_lane_signed<LPV>(x, w.sub);          // sigma * W D q
   const float mul = lane_negated<LPV>(w.sub) ? -a.qscale : a.qscale;
-  if ((uint32_t)w.vslot < a.G) {
-    float* dst = w.qh + g * D + w.sub * kElemsPerLane;
+  if ((uint32_t)w.vslot < w.gc) {
+    float* dst = qh + (g * LPV + w.sub) * kQPitch;
 #pragma unroll
     for (int i = 0; i < kElemsPerLane; i += 4)
       *(float4*)(dst + i) = make_float4(x[i] * mul, x[i + 1] * mul, x[i + 2] * mul, x[i + 3] * mul);
   }
 }
 
-// y' of this lane's 32 elements of a token from its codes (kind 0 = K, 1 = V), in the decode
-// kernels' operation order: r^ from the norm codes, y'_2i = RN(r^_i C'[k_i]), y'_2i+1 =
-// RN(r^_i S'[k_i]).
-template <int D, int WA, int NB>
-__device__ __forceinline__ void code_vector(const AttnWave<D>& w, int kind,
-                                            const TileCodes<WA, NB>& c, float (&y)[kElemsPerLane]) {
-  constexpr uint32_t kLevels = (1u << NB) - 1u;
-  uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
-  unpack16_index<WA>(c.ang, kc);
-  if constexpr (NB == 8) unpack16<NB>(c.nrm, qc);
-  else unpack16_index<NB>(c.nrm, qc);
-  const float rmin = __uint_as_float(c.hdr.x), rmax = __uint_as_float(c.hdr.y);
-  float r[kPairsPerLane];
-  if constexpr (NB == 8) {
-    const float step = rmax == rmin ? 0.0f : (rmax - rmin) / (float)kLevels;
-#pragma unroll
-    for (int i = 0; i < kPairsPerLane; ++i) r[i] = __builtin_fmaf((float)qc[i], step, rmin);
-  } else {
-    float* tab = w.lvl + (w.vslot << 4);
-    wave_lds_sync();                    // earlier reads of the level table are done
-    log_level_ladder<AttnWave<D>::LPV>(tab, w.sub, rmin, rmax, kLevels);
-    wave_lds_sync();
-#pragma unroll
-    for (int i = 0; i < kPairsPerLane; ++i) r[i] = tab[qc[i]];
-  }
-  const float2* lut = w.lut[kind];
-#pragma unroll
-  for (int i = 0; i < kPairsPerLane; ++i) {
-    const float2 cs = lut[kc[i]];
-    y[2 * i] = r[i] * cs.x;
-    y[2 * i + 1] = r[i] * cs.y;
-  }
-}
-
-template <int D, int WA, int NB>
-__device__ __forceinline__ TileCodes<WA, NB> tile_codes(const AttnWave<D>& w, int kind,
-                                                        uint32_t tile) {
-  // tokens past the chunk read its last token (in bounds) and are not counted
-  const uint32_t j = min(tile * AttnWave<D>::VPW + w.vslot, w.ntok - 1);
-  return load_codes_at<WA, NB>(w.plane[kind], w.sp[kind].rec, w.row + w.t0 + j, w.sub);
-}
-
-// Tiles 0 .. ntiles-1 of one kind, two per iteration from two code buffers: each tile's codes
-// load while the tile before it is processed.
-template <int D, int WA, int NB, class Body>
-__device__ __forceinline__ void for_tiles(const AttnWave<D>& w, int kind, uint32_t ntiles,
-                                          Body body) {
-  const uint32_t last = ntiles - 1;
-  TileCodes<WA, NB> ca = tile_codes<D, WA, NB>(w, kind, 0);
-  for (uint32_t t = 0; t <= last; t += 2) {
-    const uint32_t t1 = min(t + 1, last);
-    const TileCodes<WA, NB> cb = tile_codes<D, WA, NB>(w, kind, t1);
-    body(ca, t);
-    ca = tile_codes<D, WA, NB>(w, kind, min(t + 2, last));
-    if (t1 != t) body(cb, t1);
-  }
-}
-
-// Pass 1: the scores of the chunk's tokens for the G query heads, in log2 units, into LDS
-// (-inf for the slots past the chunk's last token).
-template <int D, int WA, int NB>
-__device__ void pass_scores(const AttnArgs& a, const AttnWave<D>& w, uint32_t ntiles) {
+// One tile: scores of the slot's token for the pass's heads, then the weighted V sum.
+template <int D, int KW, int KN, int VW, int VN>
+__device__ __forceinline__ void attend_tile(const AttnWave<D>& w, const TilePair<KW, KN, VW, VN>& c,
+                                            uint32_t tile, const float2* lut_k,
+                                            const float2* lut_v, const float* qh, float* lvl,
+                                            float (&m)[kAttnPassHeads], float (&l)[kAttnPassHeads],
+                                            float (&acc)[kAttnPassHeads][kElemsPerLane]) {
   constexpr int LPV = AttnWave<D>::LPV;
   constexpr int VPW = AttnWave<D>::VPW;
-  for_tiles<D, WA, NB>(w, 0, ntiles, [&](const TileCodes<WA, NB>& c, uint32_t tile) {
-    float y[kElemsPerLane];
-    code_vector<D, WA, NB>(w, 0, c, y);
-    const uint32_t j = tile * VPW + w.vslot;
-    for (uint32_t g = 0; g < a.G; ++g) {
-      const float* qr = w.qh + g * D + w.sub * kElemsPerLane;
+  float y[kElemsPerLane];
+  code_vector<LPV, KW, KN>(c.k, lut_k, lvl, w.sub, y);
+  const bool live = tile * VPW + w.vslot < w.ntok;
+  float s[kAttnPassHeads];
+  bool raise = false;
+#pragma unroll
+  for (int g = 0; g < kAttnPassHeads; ++g) {
+    s[g] = -INFINITY;
+    if ((uint32_t)g < w.gc) {
+      const float* qr = qh + (g * LPV + w.sub) * kQPitch;
       float part = 0.0f;
 #pragma unroll
       for (int i = 0; i < kElemsPerLane; i += 4) {
@@ -213,131 +193,142 @@ __device__ void pass_scores(const AttnArgs& a, const AttnWave<D>& w, uint32_t nt
         part = __builtin_fmaf(qv.z, y[i + 2], part);
         part = __builtin_fmaf(qv.w, y[i + 3], part);
       }
-      const float s = vec_sum<LPV>(part);
-      if (w.sub == 0) w.sc[g * a.chunk_tokens + j] = j < w.ntok ? s : -INFINITY;
+      const float sv = vec_sum<LPV>(part);
+      s[g] = live ? sv : -INFINITY;
+      raise = raise || s[g] > m[g] + kLazyLog2;
     }
-  });
-}
-
-// Pass 2 for query heads g0 .. g0+ng-1 (ng <= 2): acc += 2^(s - m) y'_V, l += 2^(s - m) over
-// this lane's tokens.
-template <int D, int WA, int NB>
-__device__ void pass_values(const AttnArgs& a, const AttnWave<D>& w, uint32_t ntiles,
-                            uint32_t g0, uint32_t ng, const float (&m)[2],
-                            float (&acc)[2][kElemsPerLane], float (&l)[2]) {
-  constexpr int VPW = AttnWave<D>::VPW;
-#pragma unroll
-  for (int gg = 0; gg < 2; ++gg) {
-    l[gg] = 0.0f;
-#pragma unroll
-    for (int i = 0; i < kElemsPerLane; ++i) acc[gg][i] = 0.0f;
   }
-  for_tiles<D, WA, NB>(w, 1, ntiles, [&](const TileCodes<WA, NB>& c, uint32_t tile) {
-    float y[kElemsPerLane];
-    code_vector<D, WA, NB>(w, 1, c, y);
-    const uint32_t j = tile * VPW + w.vslot;     // slots past the chunk hold -inf: weight 0
+  if (__builtin_amdgcn_ballot_w64(raise) != 0) {   // a new reference point (wave-uniform)
 #pragma unroll
-    for (int gg = 0; gg < 2; ++gg) {
-      if ((uint32_t)gg < ng) {
-        const float p = __builtin_amdgcn_exp2f(w.sc[(g0 + gg) * a.chunk_tokens + j] - m[gg]);
-        l[gg] += p;
+    for (int g = 0; g < kAttnPassHeads; ++g) {
+      if ((uint32_t)g < w.gc) {
+        const float mn = fmaxf(m[g], wave_max(s[g]));
+        const float f = __builtin_amdgcn_exp2f(m[g] - mn);   // 0 on the first raise
+        l[g] *= f;
 #pragma unroll
-        for (int i = 0; i < kElemsPerLane; ++i) acc[gg][i] = __builtin_fmaf(p, y[i], acc[gg][i]);
+        for (int i = 0; i < kElemsPerLane; ++i) acc[g][i] *= f;
+        m[g] = mn;
       }
     }
-  });
+  }
+  code_vector<LPV, VW, VN>(c.v, lut_v, lvl + 16 * VPW, w.sub, y);
+#pragma unroll
+  for (int g = 0; g < kAttnPassHeads; ++g) {
+    if ((uint32_t)g < w.gc) {
+      const float p = __builtin_amdgcn_exp2f(s[g] - m[g]);
+      l[g] += p;
+#pragma unroll
+      for (int i = 0; i < kElemsPerLane; ++i) acc[g][i] = __builtin_fmaf(p, y[i], acc[g][i]);
+    }
+  }
 }
 
-template <int D>
-__device__ __forceinline__ float chunk_max(const AttnArgs& a, const AttnWave<D>& w, uint32_t g) {
-  float m = -INFINITY;
-  for (uint32_t k = w.lane; k < w.ntok; k += kWave) m = fmaxf(m, w.sc[g * a.chunk_tokens + k]);
-  return wave_max(m);
-}
-
-template <int D, bool F32Q>
+template <int D, int KW, int KN, int VW, int VN>
 __global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
-  extern __shared__ float4 s_dyn[];
   constexpr int LPV = AttnWave<D>::LPV;
   constexpr int VPW = AttnWave<D>::VPW;
+  __shared__ float2 s_lut[2][kLut];
+  __shared__ float4 s_q[kWavesPerBlock][kAttnPassHeads * LPV * kQPitch / 4];
+  __shared__ float s_lvl[kWavesPerBlock][2 * 16 * VPW];
+
+  // the layer's K and V tables, shared by the block (before any wave leaves)
+  const SegParams spk = a.segs[2 * a.layer], spv = a.segs[2 * a.layer + 1];
+  for (uint32_t e = threadIdx.x; e < spk.n; e += kBlockThreads)
+    s_lut[0][e] = ((const float2*)a.lut)[spk.lut_off + e];
+  for (uint32_t e = threadIdx.x; e < spv.n; e += kBlockThreads)
+    s_lut[1][e] = ((const float2*)a.lut)[spv.lut_off + e];
+  __syncthreads();
+
   AttnWave<D> w;
-  if (!attn_setup<D>(a, w, (float*)s_dyn)) return;
-  query_transform<D, F32Q>(a, w);
-  wave_lds_sync();                                // tables and q^ visible to every lane
-  const uint32_t ntiles = (w.ntok + VPW - 1) / VPW;
-  const bool k_wide = w.sp[0].w == 8, v_wide = w.sp[1].w == 8;
-  if (w.sp[0].mode == 1) {
-    if (k_wide) pass_scores<D, 8, 8>(a, w, ntiles);
-    else pass_scores<D, 6, 8>(a, w, ntiles);
-  } else {
-    if (k_wide) pass_scores<D, 8, 4>(a, w, ntiles);
-    else pass_scores<D, 6, 4>(a, w, ntiles);
+  w.lane = threadIdx.x & (kWave - 1);
+  w.sub = w.lane % LPV;
+  w.vslot = w.lane / LPV;
+  const uint32_t wib = threadIdx.x / kWave;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + wib);
+  if (wave >= a.B * a.H * a.n_chunks * a.n_pass) return;
+  const uint32_t pass = wave % a.n_pass;
+  const uint32_t bhc = wave / a.n_pass;
+  const uint32_t bh = bhc / a.n_chunks;
+  w.chunk = bhc - bh * a.n_chunks;
+  w.b = bh / a.H;
+  w.h = bh - w.b * a.H;
+  w.g0 = pass * a.pass_heads;
+  w.gc = min(a.pass_heads, a.G - w.g0);
+  w.t0 = w.chunk * a.chunk_tokens;
+  w.ntok = min(a.chunk_tokens, a.t_end - w.t0);
+  w.row = bh * a.cap;
+  w.sp[0] = spk;
+  w.sp[1] = spv;
+  for (int kind = 0; kind < 2; ++kind)
+    for (int p = 0; p < 3; ++p) w.plane[kind][p] = a.cache + a.n_slots * w.sp[kind].pre[p];
+  float* qh = (float*)s_q[wib];
+  float* lvl = s_lvl[wib] + 16 * w.vslot;
+  if (a.q_f32) query_transform<D, true>(a, w, qh);
+  else query_transform<D, false>(a, w, qh);
+  wave_lds_sync();                                 // q^ visible to every lane
+
+  float m[kAttnPassHeads], l[kAttnPassHeads], acc[kAttnPassHeads][kElemsPerLane];
+#pragma unroll
+  for (int g = 0; g < kAttnPassHeads; ++g) {
+    m[g] = -INFINITY;
+    l[g] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kElemsPerLane; ++i) acc[g][i] = 0.0f;
   }
-  wave_lds_sync();                                // scores visible to every lane
-  for (uint32_t g0 = 0; g0 < a.G; g0 += 2) {
-    const uint32_t ng = min(2u, a.G - g0);
-    float m[2];
-    m[0] = chunk_max<D>(a, w, g0);
-    m[1] = ng > 1 ? chunk_max<D>(a, w, g0 + 1) : 0.0f;
-    float acc[2][kElemsPerLane], l[2];
-    if (w.sp[1].mode == 1) {
-      if (v_wide) pass_values<D, 8, 8>(a, w, ntiles, g0, ng, m, acc, l);
-      else pass_values<D, 6, 8>(a, w, ntiles, g0, ng, m, acc, l);
-    } else {
-      if (v_wide) pass_values<D, 8, 4>(a, w, ntiles, g0, ng, m, acc, l);
-      else pass_values<D, 6, 4>(a, w, ntiles, g0, ng, m, acc, l);
-    }
-    // every vector slot of the wave summed into slot 0 (lanes 0 .. LPV-1)
+  // tiles two at a time from two code buffers: each tile's codes load while the one before
+  // it is worked on
+  const uint32_t last = (w.ntok + VPW - 1) / VPW - 1;
+  TilePair<KW, KN, VW, VN> ca = tile_pair<D, KW, KN, VW, VN>(w, 0);
+  for (uint32_t t = 0; t <= last; t += 2) {
+    const uint32_t t1 = min(t + 1, last);
+    const TilePair<KW, KN, VW, VN> cb = tile_pair<D, KW, KN, VW, VN>(w, t1);
+    attend_tile<D>(w, ca, t, s_lut[0], s_lut[1], qh, lvl, m, l, acc);
+    ca = tile_pair<D, KW, KN, VW, VN>(w, min(t + 2, last));
+    if (t1 != t) attend_tile<D>(w, cb, t1, s_lut[0], s_lut[1], qh, lvl, m, l, acc);
+  }
+
+  // slots summed (they share m); slot 0 writes (m, l, acc) of each head
 #pragma unroll
-    for (int gg = 0; gg < 2; ++gg) {
+  for (int g = 0; g < kAttnPassHeads; ++g) {
+    if ((uint32_t)g < w.gc) {
+      const float lg = slot_sum<LPV>(l[g]);
 #pragma unroll
-      for (int o = LPV; o < kWave; o <<= 1) {
-        l[gg] += __shfl_xor(l[gg], o);
+      for (int i = 0; i < kElemsPerLane; ++i) acc[g][i] = slot_sum<LPV>(acc[g][i]);
+      if (w.vslot == 0) {
+        const uint64_t idx =
+            ((uint64_t)w.b * a.Hq + w.h * a.G + w.g0 + g) * a.n_chunks + w.chunk;
+        float* dst = a.ws_acc + idx * D + w.sub * kElemsPerLane;
 #pragma unroll
-        for (int i = 0; i < kElemsPerLane; ++i) acc[gg][i] += __shfl_xor(acc[gg][i], o);
-      }
-    }
-    if (w.vslot == 0) {
-#pragma unroll
-      for (int gg = 0; gg < 2; ++gg) {
-        if ((uint32_t)gg < ng) {
-          const uint64_t idx = ((uint64_t)w.b * a.Hq + w.h * a.G + g0 + gg) * a.n_chunks + w.chunk;
-          float* dst = a.ws_acc + idx * D + w.sub * kElemsPerLane;
-#pragma unroll
-          for (int i = 0; i < kElemsPerLane; i += 4)
-            *(float4*)(dst + i) = make_float4(acc[gg][i], acc[gg][i + 1], acc[gg][i + 2],
-                                              acc[gg][i + 3]);
-          if (w.sub == 0) *(float2*)(a.ws_ml + idx * 2) = make_float2(m[gg], l[gg]);
-        }
+        for (int i = 0; i < kElemsPerLane; i += 4)
+          *(float4*)(dst + i) = make_float4(acc[g][i], acc[g][i + 1], acc[g][i + 2], acc[g][i + 3]);
+        if (w.sub == 0) *(float2*)(a.ws_ml + idx * 2) = make_float2(m[g], lg);
       }
     }
   }
 }
 
-// One output per vector slot: merge its chunks, then o = D W (A / L).
+// One output per wave: vector slot k merges chunks k, k + VPW, ..., the slots are summed, and
+// o = D W (A / L).
 template <int D, bool F32OUT>
 __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
   constexpr int LPV = D / kElemsPerLane;
   constexpr int VPW = kWave / LPV;
   const int lane = threadIdx.x & (kWave - 1);
   const int sub = lane % LPV;
-  const int vslot = lane / LPV;
-  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock +
-                                                        threadIdx.x / kWave);
-  const uint32_t nout = a.B * a.Hq;
-  const uint32_t j0 = wave * VPW;
-  if (j0 >= nout) return;
-  const bool valid = j0 + vslot < nout;
-  const uint32_t j = valid ? j0 + vslot : j0;
+  const uint32_t vslot = (uint32_t)(lane / LPV);
+  const uint32_t j = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock +
+                                                     threadIdx.x / kWave);
+  if (j >= a.B * a.Hq) return;
   const float* ml = a.ws_ml + (size_t)j * a.n_chunks * 2;
   float M = -INFINITY;
-  for (uint32_t c = 0; c < a.n_chunks; ++c) M = fmaxf(M, ml[2 * c]);
+  for (uint32_t c = vslot; c < a.n_chunks; c += VPW) M = fmaxf(M, ml[2 * c]);
+  M = wave_max(M);
   float L = 0.0f;
   float x[kElemsPerLane];
 #pragma unroll
   for (int i = 0; i < kElemsPerLane; ++i) x[i] = 0.0f;
   const float* acc = a.ws_acc + (size_t)j * a.n_chunks * D + sub * kElemsPerLane;
-  for (uint32_t c = 0; c < a.n_chunks; ++c) {
+  for (uint32_t c = vslot; c < a.n_chunks; c += VPW) {
     const float f = __builtin_amdgcn_exp2f(ml[2 * c] - M);
     L = __builtin_fmaf(ml[2 * c + 1], f, L);
 #pragma unroll
@@ -349,6 +340,9 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
       x[i + 3] = __builtin_fmaf(v.w, f, x[i + 3]);
     }
   }
+  L = slot_sum<LPV>(L);
+#pragma unroll
+  for (int i = 0; i < kElemsPerLane; ++i) x[i] = slot_sum<LPV>(x[i]);
   const float inv = 1.0f / L;
 #pragma unroll
   for (int i = 0; i < kElemsPerLane; ++i) x[i] *= inv;
@@ -357,7 +351,7 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
   uint32_t sm[16];
   load_words<16>(a.sign_masks + (size_t)a.layer * (D / 2) + sub * 16, sm);
   const uint32_t neg = lane_negated<LPV>(sub) ? 0x80008000u : 0u;
-  if (!valid) return;
+  if (vslot != 0) return;
   const uint64_t elem = (uint64_t)j * D + sub * kElemsPerLane;
   if constexpr (F32OUT) {
     uint32_t o[32];
@@ -376,29 +370,54 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
   }
 }
 
+template <int D, int KW, int KN, int VW, int VN>
+void launch_chunk(const AttnArgs& a, dim3 grid, hipStream_t s) {
+  hipLaunchKernelGGL((attn_chunk_kernel<D, KW, KN, VW, VN>), grid, dim3(kBlockThreads), 0, s, a);
+}
+
+// format index: bit 0 = 8-bit angle codes (n = 256), bit 1 = 4-bit log norms
+template <int D, int KF>
+void launch_chunk_v(const AttnArgs& a, int vf, dim3 grid, hipStream_t s) {
+  constexpr int KW = (KF & 1) ? 8 : 6, KN = (KF & 2) ? 4 : 8;
+  switch (vf) {
+    case 0: launch_chunk<D, KW, KN, 6, 8>(a, grid, s); break;
+    case 1: launch_chunk<D, KW, KN, 8, 8>(a, grid, s); break;
+    case 2: launch_chunk<D, KW, KN, 6, 4>(a, grid, s); break;
+    default: launch_chunk<D, KW, KN, 8, 4>(a, grid, s); break;
+  }
+}
+
+template <int D>
+void launch_chunk_kv(const AttnArgs& a, int kf, int vf, dim3 grid, hipStream_t s) {
+  switch (kf) {
+    case 0: launch_chunk_v<D, 0>(a, vf, grid, s); break;
+    case 1: launch_chunk_v<D, 1>(a, vf, grid, s); break;
+    case 2: launch_chunk_v<D, 2>(a, vf, grid, s); break;
+    default: launch_chunk_v<D, 3>(a, vf, grid, s); break;
+  }
+}
+
 }  // namespace
 }  // namespace tvq
 
-int tvq_launch_attention(const tvq::AttnArgs& a, int d, int q_f32, int o_f32, void* stream) {
+int tvq_launch_attention(const tvq::AttnArgs& a, int d, int k_format, int v_format, int o_f32,
+                         void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  const dim3 block(tvq::kBlockThreads);
-  const uint64_t chunk_waves = (uint64_t)a.B * a.H * a.n_chunks;
+  const uint64_t chunk_waves = (uint64_t)a.B * a.H * a.n_chunks * a.n_pass;
   const dim3 grid1((unsigned)((chunk_waves + tvq::kWavesPerBlock - 1) / tvq::kWavesPerBlock));
-  const size_t lds = (size_t)tvq::kWavesPerBlock * a.lds_floats_per_wave * sizeof(float);
-  const int vpw = tvq::kWave / (d / tvq::kElemsPerLane);
-  const uint64_t merge_waves = ((uint64_t)a.B * a.Hq + vpw - 1) / vpw;
+  const uint64_t merge_waves = (uint64_t)a.B * a.Hq;
   const dim3 grid2((unsigned)((merge_waves + tvq::kWavesPerBlock - 1) / tvq::kWavesPerBlock));
-#define TVQ_LAUNCH_ATTN(D)                                                                      \
-  do {                                                                                          \
-    if (q_f32) hipLaunchKernelGGL((tvq::attn_chunk_kernel<D, true>), grid1, block, lds, s, a);  \
-    else hipLaunchKernelGGL((tvq::attn_chunk_kernel<D, false>), grid1, block, lds, s, a);       \
-    if (hipGetLastError() != hipSuccess) return -2;                                             \
-    if (o_f32) hipLaunchKernelGGL((tvq::attn_merge_kernel<D, true>), grid2, block, 0, s, a);    \
-    else hipLaunchKernelGGL((tvq::attn_merge_kernel<D, false>), grid2, block, 0, s, a);         \
-  } while (0)
-  if (d == 128) TVQ_LAUNCH_ATTN(128);
-  else if (d == 64) TVQ_LAUNCH_ATTN(64);
+  const dim3 block(tvq::kBlockThreads);
+  if (d == 128) tvq::launch_chunk_kv<128>(a, k_format, v_format, grid1, s);
+  else if (d == 64) tvq::launch_chunk_kv<64>(a, k_format, v_format, grid1, s);
   else return -1;
-#undef TVQ_LAUNCH_ATTN
+  if (hipGetLastError() != hipSuccess) return -2;
+  if (d == 128) {
+    if (o_f32) hipLaunchKernelGGL((tvq::attn_merge_kernel<128, true>), grid2, block, 0, s, a);
+    else hipLaunchKernelGGL((tvq::attn_merge_kernel<128, false>), grid2, block, 0, s, a);
+  } else {
+    if (o_f32) hipLaunchKernelGGL((tvq::attn_merge_kernel<64, true>), grid2, block, 0, s, a);
+    else hipLaunchKernelGGL((tvq::attn_merge_kernel<64, false>), grid2, block, 0, s, a);
+  }
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }

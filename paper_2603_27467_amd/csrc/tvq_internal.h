@@ -105,12 +105,14 @@ struct AttnArgs {
   float* ws_ml;          // [B*Hq][n_chunks][2]
   uint32_t layer, B, H, G, Hq;
   uint32_t t_end, chunk_tokens, n_chunks;
-  uint32_t lds_floats_per_wave;
+  uint32_t pass_heads, n_pass;  // query heads per chunk wave (<= kAttnPassHeads), passes over G
+  uint32_t q_f32;        // query dtype: 1 = fp32, 0 = bf16
   float qscale;          // scale * log2(e): scores in log2 units
 };
 
-constexpr uint32_t kAttnMaxGroup = 8;         // query heads per KV head (LDS: 52 KiB per block)
-constexpr uint32_t kAttnChunkHeadTokens = 1024;   // chunk_tokens * G
+constexpr int kAttnPassHeads = 4;           // accumulators of 4 query heads per wave
+constexpr uint32_t kAttnMaxGroup = 64;      // query heads per KV head
+constexpr uint64_t kAttnTargetWaves = 8192; // chunk waves per launch the token split aims at
 
 // Segments the multi-tile encode and decode kernels handle: n = 64 or 256 (6- or 8-bit angle
 // codes, every code a valid bin) with 8-bit linear or 4-bit log-space norms.  Other formats go
@@ -128,4 +130,6 @@ int tvq_launch_encode(const tvq::EncodeArgs& a, int d, int in_f32, bool fast, un
                       void* stream);
 int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, unsigned grid,
                       void* stream);
-int tvq_launch_attention(const tvq::AttnArgs& a, int d, int q_f32, int o_f32, void* stream);
+// k_format / v_format: bit 0 set for 8-bit angle codes (n = 256), bit 1 for 4-bit log norms.
+int tvq_launch_attention(const tvq::AttnArgs& a, int d, int k_format, int v_format, int o_f32,
+                         void* stream);
