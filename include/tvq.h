@@ -170,6 +170,53 @@ tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq
                                 tvq_dtype q_dtype, const void* q, tvq_dtype o_dtype, void* o,
                                 void* workspace, int64_t workspace_bytes, void* stream);
 
+/* ---- paged caches (serving) ----
+ * A paged pool holds fixed-size blocks of cache slots shared by many sequences.  Its byte
+ * layout is that of tvq_cache_layout(c, n_blocks, block_tokens): block j plays the part of
+ * "sequence" j, so the record of (block j, head h, row r) sits at ((j*H + h)*block_tokens + r)
+ * in every plane.  block_tokens is a power of two in [32, 65536].  A block table, device int32
+ * [B][max_blocks] with max_blocks * block_tokens < 2^31, maps position t of sequence b to
+ * pool block table[b][t / block_tokens], row t % block_tokens.  Per-sequence positions and
+ * lengths are device data too, so one call serves every step of a decode loop and can be
+ * captured in a HIP graph and replayed while the caller advances them on the device.
+ * Positions past a sequence's table row, or whose entry holds no pool block (< 0 or
+ * >= n_blocks), are skipped by encode and decode to zeros.  Attention reads positions below
+ * each context, clipped to max_blocks * block_tokens; they must lie in blocks the table
+ * holds: an entry holding no pool block is read as pool block 0 (memory-safe, meaningless
+ * values). */
+
+/* Encode (as tvq_encode) in->tokens tokens of each of the in->batch sequences into a paged
+ * pool: token t of sequence b goes to position positions[b] + t through the block table
+ * (positions: device int32 [in->batch]; a negative position writes nothing).  One or two
+ * kernel launches (as tvq_encode); with in->tokens == 1 this is the per-step append. */
+tvq_status tvq_encode_paged(const tvq_codec* c, tvq_dtype in_dtype, const void* k, const void* v,
+                            const tvq_tensor_desc* in, const int32_t* positions,
+                            const int32_t* block_table, int32_t max_blocks, void* pool,
+                            const tvq_layout* pool_layout, void* stream);
+
+/* Decode (as tvq_decode) positions [t_begin, t_end) of the out->batch sequences of a paged
+ * pool into k_out / v_out (out->tokens == t_end - t_begin, t_end <= max_blocks *
+ * block_tokens).  One launch of the any-format decode kernel. */
+tvq_status tvq_decode_paged(const tvq_codec* c, const void* pool, const tvq_layout* pool_layout,
+                            const int32_t* block_table, int32_t max_blocks, int64_t t_begin,
+                            int64_t t_end, tvq_dtype out_dtype, void* k_out, void* v_out,
+                            const tvq_tensor_desc* out, void* stream);
+
+/* Attention (as tvq_attention_decode) of `batch` sequences over a paged pool: sequence b
+ * attends its positions [0, min(ctx_lens[b], max_ctx)) (ctx_lens: device int32 [batch];
+ * <= 0 gives a zero output).  max_ctx (host, 1 .. max_blocks * block_tokens) bounds every
+ * context and fixes the launch shape, so the call can be replayed as the lengths grow.  The
+ * workspace is at least tvq_attention_paged_workspace(c, batch, num_q_heads, max_ctx,
+ * block_tokens) bytes.  Two kernel launches on `stream`. */
+tvq_status tvq_attention_paged_workspace(const tvq_codec* c, int64_t batch, int32_t num_q_heads,
+                                         int64_t max_ctx, int64_t block_tokens, int64_t* bytes);
+tvq_status tvq_attention_paged(const tvq_codec* c, const void* pool, const tvq_layout* pool_layout,
+                               const int32_t* block_table, int32_t max_blocks,
+                               const int32_t* ctx_lens, int64_t max_ctx, int64_t batch,
+                               int32_t layer, int32_t num_q_heads, float scale, tvq_dtype q_dtype,
+                               const void* q, tvq_dtype o_dtype, void* o, void* workspace,
+                               int64_t workspace_bytes, void* stream);
+
 /* Bits per element of the codec, averaged over layers and over K and V.
  * accounting 0: the paper's -- eq. (1) angle bits (log2 n)/2 (fractional for non-power-of-
  *               two n) plus, per eq. (3), b_norm/2 + 64/d for quantized norms or 16 for

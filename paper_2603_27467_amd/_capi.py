@@ -82,6 +82,18 @@ def load_library():
     L.tvq_attention_decode.argtypes = [vp, vp, ctypes.POINTER(tvq_layout), i32, i64, i32,
                                        ctypes.c_float, ctypes.c_int, vp, ctypes.c_int, vp, vp, i64,
                                        vp]
+    L.tvq_encode_paged.restype = ctypes.c_int
+    L.tvq_encode_paged.argtypes = [vp, ctypes.c_int, vp, vp, ctypes.POINTER(tvq_tensor_desc),
+                                   vp, vp, i32, vp, ctypes.POINTER(tvq_layout), vp]
+    L.tvq_decode_paged.restype = ctypes.c_int
+    L.tvq_decode_paged.argtypes = [vp, vp, ctypes.POINTER(tvq_layout), vp, i32, i64, i64,
+                                   ctypes.c_int, vp, vp, ctypes.POINTER(tvq_tensor_desc), vp]
+    L.tvq_attention_paged_workspace.restype = ctypes.c_int
+    L.tvq_attention_paged_workspace.argtypes = [vp, i64, i32, i64, i64, ctypes.POINTER(i64)]
+    L.tvq_attention_paged.restype = ctypes.c_int
+    L.tvq_attention_paged.argtypes = [vp, vp, ctypes.POINTER(tvq_layout), vp, i32, vp, i64, i64,
+                                      i32, i32, ctypes.c_float, ctypes.c_int, vp, ctypes.c_int,
+                                      vp, vp, i64, vp]
     L.tvq_bits_per_element.restype = ctypes.c_double
     L.tvq_bits_per_element.argtypes = [vp, ctypes.c_int]
     L.tvq_status_string.restype = ctypes.c_char_p
@@ -176,6 +188,47 @@ def tvq_attention_decode(handle: int, cache_ptr: int, lay: tvq_layout, layer: in
         num_q_heads, ctypes.c_float(scale), q_dtype, ctypes.c_void_p(q_ptr), o_dtype,
         ctypes.c_void_p(o_ptr), ctypes.c_void_p(ws_ptr), ws_bytes, ctypes.c_void_p(stream)),
         "tvq_attention_decode")
+
+
+def tvq_encode_paged(handle: int, in_dtype: int, k_ptr: int, v_ptr: int, desc: tvq_tensor_desc,
+                     positions_ptr: int, table_ptr: int, max_blocks: int, pool_ptr: int,
+                     pool_lay: tvq_layout, stream: int = 0) -> None:
+    _check(load_library().tvq_encode_paged(
+        ctypes.c_void_p(handle), in_dtype, ctypes.c_void_p(k_ptr), ctypes.c_void_p(v_ptr),
+        ctypes.byref(desc), ctypes.c_void_p(positions_ptr), ctypes.c_void_p(table_ptr),
+        max_blocks, ctypes.c_void_p(pool_ptr), ctypes.byref(pool_lay), ctypes.c_void_p(stream)),
+        "tvq_encode_paged")
+
+
+def tvq_decode_paged(handle: int, pool_ptr: int, pool_lay: tvq_layout, table_ptr: int,
+                     max_blocks: int, t_begin: int, t_end: int, out_dtype: int, k_ptr: int,
+                     v_ptr: int, desc: tvq_tensor_desc, stream: int = 0) -> None:
+    _check(load_library().tvq_decode_paged(
+        ctypes.c_void_p(handle), ctypes.c_void_p(pool_ptr), ctypes.byref(pool_lay),
+        ctypes.c_void_p(table_ptr), max_blocks, t_begin, t_end, out_dtype,
+        ctypes.c_void_p(k_ptr), ctypes.c_void_p(v_ptr), ctypes.byref(desc),
+        ctypes.c_void_p(stream)), "tvq_decode_paged")
+
+
+def tvq_attention_paged_workspace(handle: int, batch: int, num_q_heads: int, max_ctx: int,
+                                  block_tokens: int) -> int:
+    out = ctypes.c_int64(0)
+    _check(load_library().tvq_attention_paged_workspace(
+        ctypes.c_void_p(handle), batch, num_q_heads, max_ctx, block_tokens, ctypes.byref(out)),
+        "tvq_attention_paged_workspace")
+    return int(out.value)
+
+
+def tvq_attention_paged(handle: int, pool_ptr: int, pool_lay: tvq_layout, table_ptr: int,
+                        max_blocks: int, ctx_ptr: int, max_ctx: int, batch: int, layer: int,
+                        num_q_heads: int, scale: float, q_dtype: int, q_ptr: int, o_dtype: int,
+                        o_ptr: int, ws_ptr: int, ws_bytes: int, stream: int = 0) -> None:
+    _check(load_library().tvq_attention_paged(
+        ctypes.c_void_p(handle), ctypes.c_void_p(pool_ptr), ctypes.byref(pool_lay),
+        ctypes.c_void_p(table_ptr), max_blocks, ctypes.c_void_p(ctx_ptr), max_ctx, batch, layer,
+        num_q_heads, ctypes.c_float(scale), q_dtype, ctypes.c_void_p(q_ptr), o_dtype,
+        ctypes.c_void_p(o_ptr), ctypes.c_void_p(ws_ptr), ws_bytes, ctypes.c_void_p(stream)),
+        "tvq_attention_paged")
 
 
 def tvq_bits_per_element(handle: int, accounting: int) -> float:

@@ -120,5 +120,79 @@ class Codec:
                                scale, dts[q.dtype], q.data_ptr(), dts[out.dtype], out.data_ptr(),
                                workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
 
+    # ---- paged pools (tvq_encode_paged / tvq_decode_paged / tvq_attention_paged) ----
+    def pool_layout(self, n_blocks: int, block_tokens: int) -> C.tvq_layout:
+        """Layout of a paged pool of n_blocks blocks of block_tokens slots."""
+        return C.tvq_cache_layout(self.handle, n_blocks, block_tokens)
+
+    @staticmethod
+    def _i32(t, what):
+        import torch
+        if t.dtype != torch.int32 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{what} must be a contiguous int32 GPU tensor")
+        return t.data_ptr()
+
+    def encode_paged(self, k, v, positions, block_table, pool, pool_lay: C.tvq_layout,
+                     stream=None) -> None:
+        """k, v: [L, B, T, ...] as for encode; token t of sequence b goes to position
+        positions[b] + t through block_table ([B, max_blocks] int32)."""
+        import torch
+        if k.shape != v.shape or k.stride() != v.stride() or k.dtype != v.dtype:
+            raise ValueError("k and v must share shape, strides and dtype")
+        dt = {torch.bfloat16: C.TVQ_BF16, torch.float32: C.TVQ_F32}.get(k.dtype)
+        if dt is None:
+            raise ValueError("k/v must be bf16 or fp32")
+        if block_table.dim() != 2 or positions.shape != (k.shape[1],) or \
+                block_table.shape[0] != k.shape[1]:
+            raise ValueError("positions [B] and block_table [B, max_blocks] must match k")
+        C.tvq_encode_paged(self.handle, dt, k.data_ptr(), v.data_ptr(), desc_of(k),
+                           self._i32(positions, "positions"),
+                           self._i32(block_table, "block_table"), block_table.shape[1],
+                           pool.data_ptr(), pool_lay, _stream_handle(stream))
+
+    def decode_paged(self, pool, pool_lay: C.tvq_layout, block_table, t_begin: int, t_end: int,
+                     k_out, v_out, stream=None) -> None:
+        import torch
+        if k_out.shape != v_out.shape or k_out.stride() != v_out.stride() or \
+                k_out.dtype != v_out.dtype:
+            raise ValueError("k_out and v_out must share shape, strides and dtype")
+        dt = {torch.bfloat16: C.TVQ_BF16, torch.float32: C.TVQ_F32}.get(k_out.dtype)
+        if dt is None:
+            raise ValueError("outputs must be bf16 or fp32")
+        if block_table.dim() != 2 or block_table.shape[0] != k_out.shape[1]:
+            raise ValueError("block_table must be [B, max_blocks]")
+        C.tvq_decode_paged(self.handle, pool.data_ptr(), pool_lay,
+                           self._i32(block_table, "block_table"), block_table.shape[1], t_begin,
+                           t_end, dt, k_out.data_ptr(), v_out.data_ptr(), desc_of(k_out),
+                           _stream_handle(stream))
+
+    def attention_paged_workspace_bytes(self, batch: int, num_q_heads: int, max_ctx: int,
+                                        block_tokens: int) -> int:
+        return C.tvq_attention_paged_workspace(self.handle, batch, num_q_heads, max_ctx,
+                                               block_tokens)
+
+    def attention_paged(self, pool, pool_lay: C.tvq_layout, block_table, ctx_lens, max_ctx: int,
+                        layer: int, q, out, scale: float, workspace=None, stream=None) -> None:
+        """Attention of q ([B, Hq, d]) of sequence b over its positions [0, ctx_lens[b])."""
+        import torch
+        if q.dim() != 3 or out.shape != q.shape or not q.is_contiguous() or \
+                not out.is_contiguous():
+            raise ValueError("q and out must be contiguous [B, Hq, d] tensors")
+        dts = {torch.bfloat16: C.TVQ_BF16, torch.float32: C.TVQ_F32}
+        if q.dtype not in dts or out.dtype not in dts:
+            raise ValueError("q/out must be bf16 or fp32")
+        B = q.shape[0]
+        if block_table.dim() != 2 or block_table.shape[0] != B or ctx_lens.shape != (B,):
+            raise ValueError("block_table [B, max_blocks] and ctx_lens [B] must match q")
+        need = self.attention_paged_workspace_bytes(B, q.shape[1], max_ctx,
+                                                    pool_lay.capacity_tokens)
+        if workspace is None:
+            workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        C.tvq_attention_paged(self.handle, pool.data_ptr(), pool_lay,
+                              self._i32(block_table, "block_table"), block_table.shape[1],
+                              self._i32(ctx_lens, "ctx_lens"), max_ctx, B, layer, q.shape[1],
+                              scale, dts[q.dtype], q.data_ptr(), dts[out.dtype], out.data_ptr(),
+                              workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
+
     def bits_per_element(self, accounting: int = 0) -> float:
         return C.tvq_bits_per_element(self.handle, accounting)

@@ -384,6 +384,63 @@ tvq_status tvq_cache_layout(const tvq_codec* c, int64_t batch, int64_t capacity_
   return TVQ_OK;
 }
 
+// Checks of a paged pool: its layout is the codec's for n_blocks sequences of block_tokens
+// slots, block_tokens a power of two in [32, 65536], and the tables' positions fit in 31 bits.
+static bool paging_valid(const tvq_codec* c, const tvq_layout* pool, const int32_t* table,
+                         int32_t max_blocks, tvq::Paging* pg) {
+  if (!pool || !layout_matches(c, pool) || !table || ((uintptr_t)table & 3u) != 0) return false;
+  const int64_t bt = pool->capacity_tokens;
+  if (bt < 32 || bt > 65536 || (bt & (bt - 1)) != 0) return false;
+  if (max_blocks < 1 || (int64_t)max_blocks * bt >= (1ll << 31)) return false;
+  uint32_t lg = 0;
+  while ((1ll << lg) < bt) ++lg;
+  pg->table = table;
+  pg->max_blocks = (uint32_t)max_blocks;
+  pg->n_blocks = (uint32_t)pool->batch;
+  pg->block_log2 = lg;
+  return true;
+}
+
+// Encode launches over the segment lists; `a` holds the source view and destination.
+static tvq_status encode_launch(const tvq_codec* c, tvq::EncodeArgs& a, const tvq_tensor_desc* in,
+                                bool f32, void* stream) {
+  a.segs = c->d_segs;
+  a.sign_masks = c->d_sign_masks;
+  a.div_t = make_div((uint32_t)in->tokens);
+  a.div_h = make_div((uint32_t)c->H);
+  a.H = (uint32_t)c->H;
+  a.nvec = (uint32_t)(in->batch * c->H * in->tokens);
+  a.inv_d = 1.0f / (float)c->d;
+  const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
+  // bf16 input of the common formats goes to the multi-tile kernel, the rest to the generic
+  // one (the segment list holds the common formats first, so all of it is every segment)
+  const uint32_t n_fast = f32 ? 0u : c->n_fast;
+  const struct { uint32_t first, count, tpw; bool fast; } launches[2] = {
+      {0, n_fast, tvq::kFastTilesPerWave, true},
+      {n_fast, c->n_fast + c->n_generic - n_fast, 1, false}};
+  for (const auto& l : launches) {
+    if (l.count == 0) continue;
+    a.seg_list = c->d_seg_lists + l.first;
+    a.num_segs = l.count;
+    const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave,
+                                    l.tpw);
+    const int rc = tvq_launch_encode(a, c->d, f32, l.fast, grid, stream);
+    if (rc == -1) return TVQ_ERR_UNSUPPORTED;
+    if (rc != 0) return TVQ_ERR_HIP;
+  }
+  return TVQ_OK;
+}
+
+static void encode_source(tvq::EncodeArgs& a, const void* k, const void* v,
+                          const tvq_tensor_desc* in) {
+  a.k = k;
+  a.v = v;
+  a.stride_l = in->stride_l;
+  a.stride_b = (uint32_t)in->stride_b;
+  a.stride_h = (uint32_t)in->stride_h;
+  a.stride_t = (uint32_t)in->stride_t;
+}
+
 tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, const void* v,
                       const tvq_tensor_desc* in, int64_t t_begin, void* cache,
                       const tvq_layout* lay, void* stream) {
@@ -399,28 +456,58 @@ tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, con
 
   tvq::EncodeArgs a;
   std::memset(&a, 0, sizeof(a));
-  a.k = k;
-  a.v = v;
-  a.stride_l = in->stride_l;
-  a.stride_b = (uint32_t)in->stride_b;
-  a.stride_h = (uint32_t)in->stride_h;
-  a.stride_t = (uint32_t)in->stride_t;
+  encode_source(a, k, v, in);
   a.cache = (uint8_t*)cache;
   a.n_slots = lay->batch * c->H * lay->capacity_tokens;
   a.cap = (uint32_t)lay->capacity_tokens;
   a.t_begin = (uint32_t)t_begin;
+  return encode_launch(c, a, in, in_dtype == TVQ_F32, stream);
+}
+
+tvq_status tvq_encode_paged(const tvq_codec* c, tvq_dtype in_dtype, const void* k, const void* v,
+                            const tvq_tensor_desc* in, const int32_t* positions,
+                            const int32_t* block_table, int32_t max_blocks, void* pool,
+                            const tvq_layout* pool_layout, void* stream) {
+  if (!c || !in) return TVQ_ERR_INVALID_ARG;
+  if (in_dtype != TVQ_BF16 && in_dtype != TVQ_F32) return TVQ_ERR_INVALID_ARG;
+  const int eb = in_dtype == TVQ_F32 ? 4 : 2;
+  if (!desc_valid(c, in, eb)) return TVQ_ERR_INVALID_ARG;
+  tvq::EncodeArgs a;
+  std::memset(&a, 0, sizeof(a));
+  if (!paging_valid(c, pool_layout, block_table, max_blocks, &a.pg)) return TVQ_ERR_INVALID_ARG;
+  if (!positions || ((uintptr_t)positions & 3u) != 0) return TVQ_ERR_INVALID_ARG;
+  if (in->tokens == 0) return TVQ_OK;
+  if (!k || !v || !pool || !aligned16(k) || !aligned16(v) || !aligned16(pool))
+    return TVQ_ERR_INVALID_ARG;
+  encode_source(a, k, v, in);
+  a.pg.seq = positions;
+  a.cache = (uint8_t*)pool;
+  a.n_slots = pool_layout->batch * c->H * pool_layout->capacity_tokens;
+  a.cap = (uint32_t)pool_layout->capacity_tokens;
+  return encode_launch(c, a, in, in_dtype == TVQ_F32, stream);
+}
+
+static tvq_status decode_launch(const tvq_codec* c, tvq::DecodeArgs& a,
+                                const tvq_tensor_desc* out, tvq_dtype out_dtype, void* k_out,
+                                void* v_out, void* stream) {
+  a.k_out = k_out;
+  a.v_out = v_out;
+  a.stride_l = out->stride_l;
+  a.stride_b = (uint32_t)out->stride_b;
+  a.stride_h = (uint32_t)out->stride_h;
+  a.stride_t = (uint32_t)out->stride_t;
   a.segs = c->d_segs;
   a.sign_masks = c->d_sign_masks;
-  a.div_t = make_div((uint32_t)in->tokens);
+  a.lut = c->d_lut;
+  a.div_t = make_div((uint32_t)out->tokens);
   a.div_h = make_div((uint32_t)c->H);
   a.H = (uint32_t)c->H;
-  a.nvec = (uint32_t)(in->batch * c->H * in->tokens);
-  a.inv_d = 1.0f / (float)c->d;
+  a.nvec = (uint32_t)(out->batch * c->H * out->tokens);
   const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
-  // bf16 input of the common formats goes to the multi-tile kernel, the rest to the generic
-  // one (the segment list holds the common formats first, so all of it is every segment)
-  const bool f32 = in_dtype == TVQ_F32;
-  const uint32_t n_fast = f32 ? 0u : c->n_fast;
+  // the common formats go to the multi-tile kernel, the rest to the generic one; a paged
+  // source goes to the generic kernel whole
+  const bool paged = a.pg.table != nullptr;
+  const uint32_t n_fast = paged ? 0u : c->n_fast;
   const struct { uint32_t first, count, tpw; bool fast; } launches[2] = {
       {0, n_fast, tvq::kFastTilesPerWave, true},
       {n_fast, c->n_fast + c->n_generic - n_fast, 1, false}};
@@ -430,7 +517,7 @@ tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, con
     a.num_segs = l.count;
     const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave,
                                     l.tpw);
-    const int rc = tvq_launch_encode(a, c->d, f32, l.fast, grid, stream);
+    const int rc = tvq_launch_decode(a, c->d, out_dtype == TVQ_F32, l.fast, grid, stream);
     if (rc == -1) return TVQ_ERR_UNSUPPORTED;
     if (rc != 0) return TVQ_ERR_HIP;
   }
@@ -454,49 +541,44 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
   tvq::DecodeArgs a;
   std::memset(&a, 0, sizeof(a));
   a.cache = (const uint8_t*)cache;
-  a.k_out = k_out;
-  a.v_out = v_out;
-  a.stride_l = out->stride_l;
-  a.stride_b = (uint32_t)out->stride_b;
-  a.stride_h = (uint32_t)out->stride_h;
-  a.stride_t = (uint32_t)out->stride_t;
   a.n_slots = lay->batch * c->H * lay->capacity_tokens;
   a.cap = (uint32_t)lay->capacity_tokens;
   a.t_begin = (uint32_t)t_begin;
-  a.segs = c->d_segs;
-  a.sign_masks = c->d_sign_masks;
-  a.lut = c->d_lut;
-  a.div_t = make_div((uint32_t)out->tokens);
-  a.div_h = make_div((uint32_t)c->H);
-  a.H = (uint32_t)c->H;
-  a.nvec = (uint32_t)(out->batch * c->H * out->tokens);
-  const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
-  // the common formats go to the multi-tile kernel, the rest to the generic one
-  const struct { uint32_t first, count, tpw; bool fast; } launches[2] = {
-      {0, c->n_fast, tvq::kFastTilesPerWave, true},
-      {c->n_fast, c->n_generic, 1, false}};
-  for (const auto& l : launches) {
-    if (l.count == 0) continue;
-    a.seg_list = c->d_seg_lists + l.first;
-    a.num_segs = l.count;
-    const unsigned grid = plan_grid(a.nvec, vpw, a.num_segs, &a.waves_per_seg, &a.tiles_per_wave,
-                                    l.tpw);
-    const int rc = tvq_launch_decode(a, c->d, out_dtype == TVQ_F32, l.fast, grid, stream);
-    if (rc == -1) return TVQ_ERR_UNSUPPORTED;
-    if (rc != 0) return TVQ_ERR_HIP;
-  }
-  return TVQ_OK;
+  return decode_launch(c, a, out, out_dtype, k_out, v_out, stream);
 }
 
-// Tokens per chunk wave of the attention kernels: chunk_tokens * G <= kAttnChunkHeadTokens,
-// a multiple of the tile (64 / (d/32) tokens), at least one tile.
+tvq_status tvq_decode_paged(const tvq_codec* c, const void* pool, const tvq_layout* pool_layout,
+                            const int32_t* block_table, int32_t max_blocks, int64_t t_begin,
+                            int64_t t_end, tvq_dtype out_dtype, void* k_out, void* v_out,
+                            const tvq_tensor_desc* out, void* stream) {
+  if (!c || !out) return TVQ_ERR_INVALID_ARG;
+  if (out_dtype != TVQ_BF16 && out_dtype != TVQ_F32) return TVQ_ERR_INVALID_ARG;
+  const int eb = out_dtype == TVQ_F32 ? 4 : 2;
+  if (!desc_valid(c, out, eb)) return TVQ_ERR_INVALID_ARG;
+  tvq::DecodeArgs a;
+  std::memset(&a, 0, sizeof(a));
+  if (!paging_valid(c, pool_layout, block_table, max_blocks, &a.pg)) return TVQ_ERR_INVALID_ARG;
+  if (t_begin < 0 || t_end < t_begin || t_end > (int64_t)max_blocks * pool_layout->capacity_tokens)
+    return TVQ_ERR_INVALID_ARG;
+  if (out->tokens != t_end - t_begin) return TVQ_ERR_INVALID_ARG;
+  if (out->tokens == 0) return TVQ_OK;
+  if (!k_out || !v_out || !pool || !aligned16(k_out) || !aligned16(v_out) || !aligned16(pool))
+    return TVQ_ERR_INVALID_ARG;
+  a.cache = (const uint8_t*)pool;
+  a.n_slots = pool_layout->batch * c->H * pool_layout->capacity_tokens;
+  a.cap = (uint32_t)pool_layout->capacity_tokens;
+  a.t_begin = (uint32_t)t_begin;
+  return decode_launch(c, a, out, out_dtype, k_out, v_out, stream);
+}
+
 // Tokens per chunk wave: a power of two (at least 4 tiles) chosen so that a launch has about
-// kAttnTargetWaves chunk waves, at most 4096.
-static uint32_t attn_chunk_tokens(int d, int64_t waves_per_chunk_row, int64_t t_end) {
+// kAttnTargetWaves chunk waves, at most `max_chunk` (4096; 64 blocks of a paged pool).
+static uint32_t attn_chunk_tokens(int d, int64_t waves_per_chunk_row, int64_t t_end,
+                                  int64_t max_chunk) {
   const int64_t vpw = tvq::kWave / (d / tvq::kElemsPerLane);
   const int64_t want = waves_per_chunk_row * t_end / (int64_t)tvq::kAttnTargetWaves;
   int64_t ch = 4 * vpw;
-  while (ch < 4096 && 2 * ch <= want) ch *= 2;
+  while (ch < max_chunk && 2 * ch <= want) ch *= 2;
   return (uint32_t)ch;
 }
 
@@ -505,8 +587,10 @@ struct AttnPlan {
   int64_t acc_bytes, ws_bytes;
 };
 
+// block_tokens: 0 for the contiguous layout, else the pool's block size (a chunk then spans
+// at most 64 blocks, one per lane of the wave that fetches their pool indices).
 static tvq_status attn_plan(const tvq_codec* c, int64_t batch, int32_t num_q_heads,
-                            int64_t t_end, AttnPlan* p) {
+                            int64_t t_end, int64_t block_tokens, AttnPlan* p) {
   if (!c || batch < 1 || t_end < 1 || num_q_heads < c->H || num_q_heads % c->H != 0)
     return TVQ_ERR_INVALID_ARG;
   if (c->d != 64 && c->d != 128) return TVQ_ERR_UNSUPPORTED;
@@ -514,7 +598,9 @@ static tvq_status attn_plan(const tvq_codec* c, int64_t batch, int32_t num_q_hea
   if (p->G > tvq::kAttnMaxGroup) return TVQ_ERR_UNSUPPORTED;
   p->n_pass = (p->G + tvq::kAttnPassHeads - 1) / tvq::kAttnPassHeads;
   p->pass_heads = (p->G + p->n_pass - 1) / p->n_pass;          // balanced passes
-  p->chunk = attn_chunk_tokens(c->d, batch * c->H * p->n_pass, t_end);
+  const int64_t max_chunk = block_tokens > 0 && 64 * block_tokens < 4096 ? 64 * block_tokens
+                                                                          : 4096;
+  p->chunk = attn_chunk_tokens(c->d, batch * c->H * p->n_pass, t_end, max_chunk);
   p->n_chunks = (uint32_t)((t_end + p->chunk - 1) / p->chunk);
   const int64_t parts = batch * num_q_heads * (int64_t)p->n_chunks;
   p->acc_bytes = (parts * c->d * 4 + 255) / 256 * 256;
@@ -526,22 +612,35 @@ tvq_status tvq_attention_workspace(const tvq_codec* c, int64_t batch, int32_t nu
                                    int64_t t_end, int64_t* bytes) {
   if (!bytes) return TVQ_ERR_INVALID_ARG;
   AttnPlan p;
-  const tvq_status st = attn_plan(c, batch, num_q_heads, t_end, &p);
+  const tvq_status st = attn_plan(c, batch, num_q_heads, t_end, 0, &p);
   if (st == TVQ_OK) *bytes = p.ws_bytes;
   return st;
 }
 
-tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq_layout* lay,
-                                int32_t layer, int64_t t_end, int32_t num_q_heads, float scale,
-                                tvq_dtype q_dtype, const void* q, tvq_dtype o_dtype, void* o,
-                                void* workspace, int64_t workspace_bytes, void* stream) {
-  if (!c || !lay || !layout_matches(c, lay)) return TVQ_ERR_INVALID_ARG;
-  if (layer < 0 || layer >= c->L || t_end > lay->capacity_tokens) return TVQ_ERR_INVALID_ARG;
+tvq_status tvq_attention_paged_workspace(const tvq_codec* c, int64_t batch, int32_t num_q_heads,
+                                         int64_t max_ctx, int64_t block_tokens, int64_t* bytes) {
+  if (!bytes || block_tokens < 32 || block_tokens > 65536 ||
+      (block_tokens & (block_tokens - 1)) != 0)
+    return TVQ_ERR_INVALID_ARG;
+  AttnPlan p;
+  const tvq_status st = attn_plan(c, batch, num_q_heads, max_ctx, block_tokens, &p);
+  if (st == TVQ_OK) *bytes = p.ws_bytes;
+  return st;
+}
+
+// The shared body of the two attention entry points: `a` holds the cache, its geometry and
+// the paging (if any); t_end bounds every sequence's context.
+static tvq_status attention_launch(const tvq_codec* c, tvq::AttnArgs& a, int64_t batch,
+                                   int32_t layer, int64_t t_end, int64_t block_tokens,
+                                   int32_t num_q_heads, float scale, tvq_dtype q_dtype,
+                                   const void* q, tvq_dtype o_dtype, void* o, void* workspace,
+                                   int64_t workspace_bytes, void* stream) {
+  if (layer < 0 || layer >= c->L) return TVQ_ERR_INVALID_ARG;
   if ((q_dtype != TVQ_BF16 && q_dtype != TVQ_F32) || (o_dtype != TVQ_BF16 && o_dtype != TVQ_F32))
     return TVQ_ERR_INVALID_ARG;
   if (!(scale == scale) || scale > 3.0e38f || scale < -3.0e38f) return TVQ_ERR_INVALID_ARG;
   AttnPlan p;
-  const tvq_status st = attn_plan(c, lay->batch, num_q_heads, t_end, &p);
+  const tvq_status st = attn_plan(c, batch, num_q_heads, t_end, block_tokens, &p);
   if (st != TVQ_OK) return st;
   int fmt[2];
   for (int kind = 0; kind < 2; ++kind) {
@@ -549,18 +648,12 @@ tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq
     if (!tvq::fast_format(sp.n, sp.mode, sp.bits)) return TVQ_ERR_UNSUPPORTED;
     fmt[kind] = (sp.n == 256 ? 1 : 0) | (sp.mode == 2 ? 2 : 0);
   }
-  if (!cache || !q || !o || !workspace || !aligned16(cache) || !aligned16(q) || !aligned16(o) ||
-      !aligned16(workspace) || workspace_bytes < p.ws_bytes)
+  if (!a.cache || !q || !o || !workspace || !aligned16(a.cache) || !aligned16(q) ||
+      !aligned16(o) || !aligned16(workspace) || workspace_bytes < p.ws_bytes)
     return TVQ_ERR_INVALID_ARG;
-  if ((int64_t)lay->batch * num_q_heads * p.n_chunks * c->d >= (1ll << 31) ||
-      (int64_t)lay->batch * c->H * p.n_chunks * p.n_pass >= (1ll << 31))
+  if (batch * num_q_heads * p.n_chunks * c->d >= (1ll << 31) ||
+      batch * c->H * p.n_chunks * p.n_pass >= (1ll << 31))
     return TVQ_ERR_INVALID_ARG;
-
-  tvq::AttnArgs a;
-  std::memset(&a, 0, sizeof(a));
-  a.cache = (const uint8_t*)cache;
-  a.n_slots = lay->batch * c->H * lay->capacity_tokens;
-  a.cap = (uint32_t)lay->capacity_tokens;
   a.segs = c->d_segs;
   a.sign_masks = c->d_sign_masks;
   a.lut = c->d_lut;
@@ -569,7 +662,7 @@ tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq
   a.ws_acc = (float*)workspace;
   a.ws_ml = (float*)((char*)workspace + p.acc_bytes);
   a.layer = (uint32_t)layer;
-  a.B = (uint32_t)lay->batch;
+  a.B = (uint32_t)batch;
   a.H = (uint32_t)c->H;
   a.G = p.G;
   a.Hq = (uint32_t)num_q_heads;
@@ -583,6 +676,41 @@ tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq
   const int rc = tvq_launch_attention(a, c->d, fmt[0], fmt[1], o_dtype == TVQ_F32, stream);
   if (rc == -1) return TVQ_ERR_UNSUPPORTED;
   return rc == 0 ? TVQ_OK : TVQ_ERR_HIP;
+}
+
+tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq_layout* lay,
+                                int32_t layer, int64_t t_end, int32_t num_q_heads, float scale,
+                                tvq_dtype q_dtype, const void* q, tvq_dtype o_dtype, void* o,
+                                void* workspace, int64_t workspace_bytes, void* stream) {
+  if (!c || !lay || !layout_matches(c, lay)) return TVQ_ERR_INVALID_ARG;
+  if (t_end > lay->capacity_tokens) return TVQ_ERR_INVALID_ARG;
+  tvq::AttnArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.cache = (const uint8_t*)cache;
+  a.n_slots = lay->batch * c->H * lay->capacity_tokens;
+  a.cap = (uint32_t)lay->capacity_tokens;
+  return attention_launch(c, a, lay->batch, layer, t_end, 0, num_q_heads, scale, q_dtype, q,
+                          o_dtype, o, workspace, workspace_bytes, stream);
+}
+
+tvq_status tvq_attention_paged(const tvq_codec* c, const void* pool, const tvq_layout* pool_layout,
+                               const int32_t* block_table, int32_t max_blocks,
+                               const int32_t* ctx_lens, int64_t max_ctx, int64_t batch,
+                               int32_t layer, int32_t num_q_heads, float scale, tvq_dtype q_dtype,
+                               const void* q, tvq_dtype o_dtype, void* o, void* workspace,
+                               int64_t workspace_bytes, void* stream) {
+  if (!c) return TVQ_ERR_INVALID_ARG;
+  tvq::AttnArgs a;
+  std::memset(&a, 0, sizeof(a));
+  if (!paging_valid(c, pool_layout, block_table, max_blocks, &a.pg)) return TVQ_ERR_INVALID_ARG;
+  if (!ctx_lens || ((uintptr_t)ctx_lens & 3u) != 0) return TVQ_ERR_INVALID_ARG;
+  if (max_ctx > (int64_t)max_blocks * pool_layout->capacity_tokens) return TVQ_ERR_INVALID_ARG;
+  a.pg.seq = ctx_lens;
+  a.cache = (const uint8_t*)pool;
+  a.n_slots = pool_layout->batch * c->H * pool_layout->capacity_tokens;
+  a.cap = (uint32_t)pool_layout->capacity_tokens;
+  return attention_launch(c, a, batch, layer, max_ctx, pool_layout->capacity_tokens, num_q_heads,
+                          scale, q_dtype, q, o_dtype, o, workspace, workspace_bytes, stream);
 }
 
 double tvq_bits_per_element_config(const tvq_config* cfg, int accounting) {

@@ -70,7 +70,8 @@ struct AttnWave {
   int lane, sub, vslot;
   uint32_t b, h, chunk, g0, gc;  // query heads g0 .. g0 + gc - 1 of KV head h
   uint32_t t0, ntok;             // the chunk's tokens [t0, t0 + ntok)
-  uint32_t row;                  // cache slot of token 0 of (b, h)
+  uint32_t row;                  // cache slot of token 0 of (b, h) (contiguous layout)
+  uint32_t blk;                  // paged: lane i holds the pool block of the chunk's i-th block
   SegParams sp[2];               // K and V of the layer
   const uint8_t* plane[2][3];
 };
@@ -113,12 +114,25 @@ struct TilePair {
   TileCodes<VW, VN> v;
 };
 
+// Pool record of the chunk's token j in a paged cache: a tile lies inside one block (blocks
+// hold a multiple of a tile's tokens), whose pool index comes from lane i of w.blk.
+template <int D>
+__device__ __forceinline__ uint32_t paged_record(const AttnArgs& a, const AttnWave<D>& w,
+                                                 uint32_t tile, uint32_t j) {
+  const uint32_t first = (w.t0 + tile * AttnWave<D>::VPW) >> a.pg.block_log2;
+  const uint32_t i = first - (w.t0 >> a.pg.block_log2);
+  const uint32_t blk = (uint32_t)__builtin_amdgcn_readlane((int)w.blk, (int)i);
+  const uint32_t tok = w.t0 + j;
+  return ((blk * a.H + w.h) << a.pg.block_log2) + (tok & ((1u << a.pg.block_log2) - 1u));
+}
+
 template <int D, int KW, int KN, int VW, int VN>
-__device__ __forceinline__ TilePair<KW, KN, VW, VN> tile_pair(const AttnWave<D>& w,
+__device__ __forceinline__ TilePair<KW, KN, VW, VN> tile_pair(const AttnArgs& a,
+                                                              const AttnWave<D>& w,
                                                               uint32_t tile) {
   // slots past the chunk read its last token (in bounds) and get weight 0
   const uint32_t j = min(tile * AttnWave<D>::VPW + w.vslot, w.ntok - 1);
-  const uint32_t slot = w.row + w.t0 + j;
+  const uint32_t slot = a.pg.table ? paged_record<D>(a, w, tile, j) : w.row + w.t0 + j;
   TilePair<KW, KN, VW, VN> p;
   p.k = load_codes_at<KW, KN>(w.plane[0], w.sp[0].rec, slot, w.sub);
   p.v = load_codes_at<VW, VN>(w.plane[1], w.sp[1].rec, slot, w.sub);
@@ -255,8 +269,36 @@ __global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
   w.g0 = pass * a.pass_heads;
   w.gc = min(a.pass_heads, a.G - w.g0);
   w.t0 = w.chunk * a.chunk_tokens;
-  w.ntok = min(a.chunk_tokens, a.t_end - w.t0);
+  // the sequence's context: t_end, or its own length (paged), at most what its table covers
+  uint32_t ctx = a.t_end;
+  if (a.pg.seq) {
+    const int32_t len = a.pg.seq[w.b];
+    ctx = len <= 0 ? 0u : min((uint32_t)len, a.t_end);
+  }
+  if (w.t0 >= ctx) {
+    // nothing to attend in this chunk: a partial of weight 0 for the merge
+    if (w.vslot == 0) {
+      for (uint32_t g = 0; g < w.gc; ++g) {
+        const uint64_t idx =
+            ((uint64_t)w.b * a.Hq + w.h * a.G + w.g0 + g) * a.n_chunks + w.chunk;
+        float* dst = a.ws_acc + idx * D + w.sub * kElemsPerLane;
+        for (int i = 0; i < kElemsPerLane; i += 4) *(float4*)(dst + i) = make_float4(0, 0, 0, 0);
+        if (w.sub == 0) *(float2*)(a.ws_ml + idx * 2) = make_float2(-INFINITY, 0.0f);
+      }
+    }
+    return;
+  }
+  w.ntok = min(a.chunk_tokens, ctx - w.t0);
   w.row = bh * a.cap;
+  w.blk = 0;
+  if (a.pg.table) {
+    // lane i: the pool block of the chunk's i-th block (entries past the table or naming no
+    // pool block read block 0, so a corrupt table stays inside the pool)
+    const uint32_t i = (w.t0 >> a.pg.block_log2) + (uint32_t)w.lane;
+    const uint32_t blk = i < a.pg.max_blocks
+                             ? (uint32_t)a.pg.table[(size_t)w.b * a.pg.max_blocks + i] : 0u;
+    w.blk = blk < a.pg.n_blocks ? blk : 0u;
+  }
   w.sp[0] = spk;
   w.sp[1] = spv;
   for (int kind = 0; kind < 2; ++kind)
@@ -278,12 +320,12 @@ __global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
   // tiles two at a time from two code buffers: each tile's codes load while the one before
   // it is worked on
   const uint32_t last = (w.ntok + VPW - 1) / VPW - 1;
-  TilePair<KW, KN, VW, VN> ca = tile_pair<D, KW, KN, VW, VN>(w, 0);
+  TilePair<KW, KN, VW, VN> ca = tile_pair<D, KW, KN, VW, VN>(a, w, 0);
   for (uint32_t t = 0; t <= last; t += 2) {
     const uint32_t t1 = min(t + 1, last);
-    const TilePair<KW, KN, VW, VN> cb = tile_pair<D, KW, KN, VW, VN>(w, t1);
+    const TilePair<KW, KN, VW, VN> cb = tile_pair<D, KW, KN, VW, VN>(a, w, t1);
     attend_tile<D>(w, ca, t, s_lut[0], s_lut[1], qh, lvl, m, l, acc);
-    ca = tile_pair<D, KW, KN, VW, VN>(w, min(t + 2, last));
+    ca = tile_pair<D, KW, KN, VW, VN>(a, w, min(t + 2, last));
     if (t1 != t) attend_tile<D>(w, cb, t1, s_lut[0], s_lut[1], qh, lvl, m, l, acc);
   }
 
@@ -329,7 +371,8 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
   for (int i = 0; i < kElemsPerLane; ++i) x[i] = 0.0f;
   const float* acc = a.ws_acc + (size_t)j * a.n_chunks * D + sub * kElemsPerLane;
   for (uint32_t c = vslot; c < a.n_chunks; c += VPW) {
-    const float f = __builtin_amdgcn_exp2f(ml[2 * c] - M);
+    // empty chunks carry m = -inf and weight 0; with no token at all, M is -inf too
+    const float f = M == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(ml[2 * c] - M);
     L = __builtin_fmaf(ml[2 * c + 1], f, L);
 #pragma unroll
     for (int i = 0; i < kElemsPerLane; i += 4) {
@@ -343,7 +386,7 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
   L = slot_sum<LPV>(L);
 #pragma unroll
   for (int i = 0; i < kElemsPerLane; ++i) x[i] = slot_sum<LPV>(x[i]);
-  const float inv = 1.0f / L;
+  const float inv = M == -INFINITY ? 0.0f : 1.0f / L;   // no token attended: zeros
 #pragma unroll
   for (int i = 0; i < kElemsPerLane; ++i) x[i] *= inv;
   fwht_in_lane(x);

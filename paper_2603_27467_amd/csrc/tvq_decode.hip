@@ -52,10 +52,13 @@ constexpr int kLvlPerWave = 32 * (1 << kLvlBits);   // vectors per wave (d = 64)
 
 struct TilePos {
   uint32_t bh, t, b, h;
-  uint32_t slot;             // (b*H + h)*capacity + t_begin + t < 2^31
+  uint32_t slot;             // (b*H + h)*capacity + t_begin + t < 2^31, or the pool record
   bool valid;
+  bool present;              // paged: the table holds a block for the position
 };
 
+// PAGED: position t_begin + t of sequence b through the block table.
+template <bool PAGED = false>
 __device__ __forceinline__ TilePos tile_pos(const DecodeArgs& a, uint32_t j0, int vslot) {
   TilePos p;
   const uint32_t j = j0 + vslot;
@@ -65,7 +68,12 @@ __device__ __forceinline__ TilePos tile_pos(const DecodeArgs& a, uint32_t j0, in
   p.t = jj - p.bh * a.div_t.div;
   p.b = fast_div(p.bh, a.div_h);
   p.h = p.bh - p.b * a.H;
-  p.slot = p.bh * a.cap + a.t_begin + p.t;
+  if constexpr (PAGED) {
+    p.slot = paged_slot(a.pg, p.b, p.h, a.H, a.t_begin + p.t, p.present);
+  } else {
+    p.slot = p.bh * a.cap + a.t_begin + p.t;
+    p.present = true;
+  }
   return p;
 }
 
@@ -316,8 +324,9 @@ __global__ __launch_bounds__(kBlockThreads) void decode_fast_kernel(DecodeArgs a
   }
 }
 
-// Any code widths and norm modes, one tile per wave.
-template <int D, bool F32OUT>
+// Any code widths and norm modes, one tile per wave.  PAGED: the source is a paged pool, and
+// positions without a block decode to zeros.
+template <int D, bool F32OUT, bool PAGED>
 __global__ __launch_bounds__(kBlockThreads) void decode_generic_kernel(DecodeArgs a) {
   constexpr int VPW = WaveState<D>::VPW;
   __shared__ float2 s_lut[kWavesPerBlock * kLutGeneric];
@@ -325,7 +334,7 @@ __global__ __launch_bounds__(kBlockThreads) void decode_generic_kernel(DecodeArg
   WaveState<D> w;
   uint32_t tile0, ntiles;
   if (!wave_setup<D>(a, w, s_lut, kLutGeneric, tile0, ntiles)) return;
-  const TilePos pos = tile_pos(a, tile0 * VPW, w.vslot);
+  const TilePos pos = tile_pos<PAGED>(a, tile0 * VPW, w.vslot);
   uint32_t kc[kPairsPerLane];
   load_codes_any(w.plane[0] + (uint64_t)pos.slot * w.sp.rec[0], w.sub, w.sp.w, kc);
   if (!w.sp.mask) {
@@ -373,6 +382,12 @@ __global__ __launch_bounds__(kBlockThreads) void decode_generic_kernel(DecodeArg
   uint32_t o[OutWords<F32OUT>::NW];
   if (w.lut_s) reconstruct<D, F32OUT, true>(a, w, kc, r, o);
   else reconstruct<D, F32OUT, false>(a, w, kc, r, o);
+  if constexpr (PAGED) {
+    if (!pos.present) {
+#pragma unroll
+      for (int i = 0; i < OutWords<F32OUT>::NW; ++i) o[i] = 0u;
+    }
+  }
   store_direct<D, F32OUT>(a, w, pos, o);
 }
 
@@ -383,6 +398,8 @@ int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, u
                       void* stream) {
   hipStream_t s = (hipStream_t)stream;
   const dim3 block(tvq::kBlockThreads);
+  const bool paged = a.pg.table != nullptr;
+  if (paged && fast) return -1;       // a paged source goes to the generic kernel
   const bool multi = a.tiles_per_wave > 1;
 #define TVQ_LAUNCH_DEC(D, F32)                                                                  \
   do {                                                                                          \
@@ -390,8 +407,10 @@ int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, u
       hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true>), dim3(grid), block, 0, s, a);  \
     else if (fast)                                                                              \
       hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, false>), dim3(grid), block, 0, s, a); \
+    else if (paged)                                                                             \
+      hipLaunchKernelGGL((tvq::decode_generic_kernel<D, F32, true>), dim3(grid), block, 0, s, a); \
     else                                                                                        \
-      hipLaunchKernelGGL((tvq::decode_generic_kernel<D, F32>), dim3(grid), block, 0, s, a);     \
+      hipLaunchKernelGGL((tvq::decode_generic_kernel<D, F32, false>), dim3(grid), block, 0, s, a);\
   } while (0)
   if (d == 128) {
     if (out_f32) TVQ_LAUNCH_DEC(128, true);

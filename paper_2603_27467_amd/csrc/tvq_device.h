@@ -29,6 +29,19 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Pool record of token `tok` of (sequence b, head h) in a paged cache (see Paging).  `ok` is
+// false, and record 0 returned, when tok lies past the sequence's table or its entry is not a
+// pool block (the caller then neither stores nor uses what it reads).
+__device__ __forceinline__ uint32_t paged_slot(const Paging& pg, uint32_t b, uint32_t h,
+                                               uint32_t H, uint32_t tok, bool& ok) {
+  const uint32_t i = tok >> pg.block_log2;
+  const bool in_table = i < pg.max_blocks;
+  const uint32_t blk =
+      (uint32_t)pg.table[(size_t)b * pg.max_blocks + (in_table ? i : 0u)];
+  ok = in_table && blk < pg.n_blocks;
+  return ok ? ((blk * H + h) << pg.block_log2) + (tok & ((1u << pg.block_log2) - 1u)) : 0u;
+}
+
 __device__ __forceinline__ uint32_t fast_div(uint32_t x, const FastDiv& d) {
   return (uint32_t)(((uint64_t)x * d.m) >> d.s);
 }

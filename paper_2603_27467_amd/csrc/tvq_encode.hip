@@ -201,10 +201,12 @@ __device__ __forceinline__ bool enc_wave_setup(const EncodeArgs& a, EncWave<D>& 
 template <bool F32IN>
 struct TileIn {
   Raw<F32IN> raw;
-  uint32_t slot;              // (b*H + h)*capacity + t_begin + t < 2^31
+  uint32_t slot;              // (b*H + h)*capacity + t_begin + t < 2^31, or the pool record
+  bool ok;                    // paged: the destination exists (else nothing is stored)
 };
 
-template <int D, bool F32IN>
+// PAGED: token t of sequence b goes to position seq[b] + t through the block table.
+template <int D, bool F32IN, bool PAGED>
 __device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const EncWave<D>& w,
                                                    uint32_t tile) {
   const uint32_t j0 = tile * EncWave<D>::VPW;
@@ -217,16 +219,25 @@ __device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const En
   TileIn<F32IN> in;
   in.raw = load_raw<F32IN>(w.src, w.layer_off + (uint64_t)b * a.stride_b +
                                       (uint64_t)h * a.stride_h + (uint64_t)t * a.stride_t);
-  in.slot = bh * a.cap + a.t_begin + t;
+  if constexpr (PAGED) {
+    const int32_t p0 = a.pg.seq[b];
+    bool ok;
+    in.slot = paged_slot(a.pg, b, h, a.H, (uint32_t)p0 + t, ok);
+    in.ok = ok && p0 >= 0 && (uint32_t)p0 + t >= (uint32_t)p0;
+  } else {
+    in.slot = bh * a.cap + a.t_begin + t;
+    in.ok = true;
+  }
   return in;
 }
 
 // Encode one tile.  WA = angle code width and NB = norm code width of a format fixed at
 // compile time (NB = 8: linear norms, NB = 4: log-space norms; the angle codebook is then
 // n = 2^WA), or WA = NB = 0 for the segment's run-time format.
-template <int D, bool F32IN, int WA, int NB>
+template <int D, bool F32IN, int WA, int NB, bool PAGED>
 __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D>& w,
                                             const TileIn<F32IN>& in) {
+  const bool store = !PAGED || in.ok;
   constexpr int LPV = EncWave<D>::LPV;
   constexpr bool kFixed = WA != 0;
   static_assert(!kFixed || ((WA == 6 || WA == 8) && (NB == 8 || NB == 4)), "fixed formats");
@@ -289,7 +300,7 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
 #pragma unroll
     for (int i = 0; i < kPairsPerLane; ++i)
       rn[i] = __float_as_uint((float)pair_norm_f64(x[2 * i], x[2 * i + 1], inv_sqrt_d));
-    store_words<16>((uint32_t*)rec_nrm + 16 * w.sub, rn);
+    if (store) store_words<16>((uint32_t*)rec_nrm + 16 * w.sub, rn);
   } else {
     // qc: bits of t + 1.5*2^23, t the code coordinate of each pair (eq. (2) or its log
     // variant); t stays within [-eps, 2^b - 1 + eps], so the low b bits are the code
@@ -353,10 +364,13 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
               __builtin_fmaf(fmaxf(log2f(fmaxf(rf[i], FLT_MIN) * rc), 0.0f), scale, kRoundShift));
       }
     }
-    if constexpr (kFixed) store_codes<NB>(rec_nrm, w.sub, qc);
-    else store_codes_any(rec_nrm, w.sub, nbits, qc);
-    // every lane of the vector writes the same header bytes
-    *(u32x2*)(w.plane[2] + (uint64_t)in.slot * 8) = u32x2{__float_as_uint(rmin), __float_as_uint(rmax)};
+    if (store) {
+      if constexpr (kFixed) store_codes<NB>(rec_nrm, w.sub, qc);
+      else store_codes_any(rec_nrm, w.sub, nbits, qc);
+      // every lane of the vector writes the same header bytes
+      *(u32x2*)(w.plane[2] + (uint64_t)in.slot * 8) =
+          u32x2{__float_as_uint(rmin), __float_as_uint(rmax)};
+    }
   }
 
   // ---- angle codes ----
@@ -384,8 +398,10 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
                                  __uint_as_float(__float_as_uint(x[2 * i + 1]) ^ flip), nf, n);
   }
   uint8_t* rec_ang = w.plane[0] + (uint64_t)in.slot * sp.rec[0];
-  if constexpr (kFixed) store_codes<WA>(rec_ang, w.sub, kc);
-  else store_codes_any(rec_ang, w.sub, sp.w, kc);
+  if (store) {
+    if constexpr (kFixed) store_codes<WA>(rec_ang, w.sub, kc);
+    else store_codes_any(rec_ang, w.sub, sp.w, kc);
+  }
 }
 
 // Tiles tile0 .. tile0 + ntiles - 1.  MULTI: two per iteration from two input buffers, each
@@ -394,24 +410,24 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
 // addresses) and the loads past the end read lines already in cache.  Launches of one tile
 // per wave use the instantiation without the loop (a separate copy of the tile code inside
 // the same kernel would raise its register count).
-template <int D, bool MULTI, int WA, int NB>
+template <int D, bool MULTI, int WA, int NB, bool PAGED>
 __device__ void encode_tiles_fast(const EncodeArgs& a, const EncWave<D>& w, uint32_t tile0,
                                   uint32_t ntiles) {
   const uint32_t last = tile0 + ntiles - 1;
-  TileIn<false> ia = load_tile<D, false>(a, w, tile0);
+  TileIn<false> ia = load_tile<D, false, PAGED>(a, w, tile0);
   if constexpr (!MULTI) {
-    encode_tile<D, false, WA, NB>(a, w, ia);
+    encode_tile<D, false, WA, NB, PAGED>(a, w, ia);
     return;
   }
   for (uint32_t t = tile0; t <= last; t += 2) {
-    const TileIn<false> ib = load_tile<D, false>(a, w, min(t + 1, last));
-    encode_tile<D, false, WA, NB>(a, w, ia);
-    ia = load_tile<D, false>(a, w, min(t + 2, last));
-    encode_tile<D, false, WA, NB>(a, w, ib);
+    const TileIn<false> ib = load_tile<D, false, PAGED>(a, w, min(t + 1, last));
+    encode_tile<D, false, WA, NB, PAGED>(a, w, ia);
+    ia = load_tile<D, false, PAGED>(a, w, min(t + 2, last));
+    encode_tile<D, false, WA, NB, PAGED>(a, w, ib);
   }
 }
 
-template <int D, bool MULTI>
+template <int D, bool MULTI, bool PAGED>
 __global__ __launch_bounds__(kBlockThreads) void encode_fast_kernel(EncodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t s_sm[kWavesPerBlock][D / 2];
   EncWave<D> w;
@@ -419,22 +435,36 @@ __global__ __launch_bounds__(kBlockThreads) void encode_fast_kernel(EncodeArgs a
   if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles)) return;
   const bool wide = w.sp.w == 8;
   if (w.sp.mode == 1) {
-    if (wide) encode_tiles_fast<D, MULTI, 8, 8>(a, w, tile0, ntiles);
-    else encode_tiles_fast<D, MULTI, 6, 8>(a, w, tile0, ntiles);
+    if (wide) encode_tiles_fast<D, MULTI, 8, 8, PAGED>(a, w, tile0, ntiles);
+    else encode_tiles_fast<D, MULTI, 6, 8, PAGED>(a, w, tile0, ntiles);
   } else {
-    if (wide) encode_tiles_fast<D, MULTI, 8, 4>(a, w, tile0, ntiles);
-    else encode_tiles_fast<D, MULTI, 6, 4>(a, w, tile0, ntiles);
+    if (wide) encode_tiles_fast<D, MULTI, 8, 4, PAGED>(a, w, tile0, ntiles);
+    else encode_tiles_fast<D, MULTI, 6, 4, PAGED>(a, w, tile0, ntiles);
   }
 }
 
 // Any format, bf16 or fp32 input; one tile per wave.
-template <int D, bool F32IN>
+template <int D, bool F32IN, bool PAGED>
 __global__ __launch_bounds__(kBlockThreads) void encode_generic_kernel(EncodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t s_sm[kWavesPerBlock][D / 2];
   EncWave<D> w;
   uint32_t tile0, ntiles;
   if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles)) return;
-  encode_tile<D, F32IN, 0, 0>(a, w, load_tile<D, F32IN>(a, w, tile0));
+  encode_tile<D, F32IN, 0, 0, PAGED>(a, w, load_tile<D, F32IN, PAGED>(a, w, tile0));
+}
+
+template <int D, bool PAGED>
+void launch_encode(const EncodeArgs& a, int in_f32, bool fast, unsigned grid, hipStream_t s) {
+  const dim3 block(kBlockThreads);
+  const bool multi = a.tiles_per_wave > 1;
+  if (fast && multi)
+    hipLaunchKernelGGL((encode_fast_kernel<D, true, PAGED>), dim3(grid), block, 0, s, a);
+  else if (fast)
+    hipLaunchKernelGGL((encode_fast_kernel<D, false, PAGED>), dim3(grid), block, 0, s, a);
+  else if (in_f32)
+    hipLaunchKernelGGL((encode_generic_kernel<D, true, PAGED>), dim3(grid), block, 0, s, a);
+  else
+    hipLaunchKernelGGL((encode_generic_kernel<D, false, PAGED>), dim3(grid), block, 0, s, a);
 }
 
 }  // namespace
@@ -443,23 +473,16 @@ __global__ __launch_bounds__(kBlockThreads) void encode_generic_kernel(EncodeArg
 int tvq_launch_encode(const tvq::EncodeArgs& a, int d, int in_f32, bool fast, unsigned grid,
                       void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  const dim3 block(tvq::kBlockThreads);
   if (fast && in_f32) return -1;      // the multi-tile kernel reads bf16 only
-  const bool multi = a.tiles_per_wave > 1;
-#define TVQ_LAUNCH_ENC(D)                                                                    \
-  do {                                                                                       \
-    if (fast && multi)                                                                       \
-      hipLaunchKernelGGL((tvq::encode_fast_kernel<D, true>), dim3(grid), block, 0, s, a);    \
-    else if (fast)                                                                           \
-      hipLaunchKernelGGL((tvq::encode_fast_kernel<D, false>), dim3(grid), block, 0, s, a);   \
-    else if (in_f32)                                                                         \
-      hipLaunchKernelGGL((tvq::encode_generic_kernel<D, true>), dim3(grid), block, 0, s, a); \
-    else                                                                                     \
-      hipLaunchKernelGGL((tvq::encode_generic_kernel<D, false>), dim3(grid), block, 0, s, a);\
-  } while (0)
-  if (d == 128) TVQ_LAUNCH_ENC(128);
-  else if (d == 64) TVQ_LAUNCH_ENC(64);
-  else return -1;
-#undef TVQ_LAUNCH_ENC
+  const bool paged = a.pg.table != nullptr;
+  if (d == 128) {
+    if (paged) tvq::launch_encode<128, true>(a, in_f32, fast, grid, s);
+    else tvq::launch_encode<128, false>(a, in_f32, fast, grid, s);
+  } else if (d == 64) {
+    if (paged) tvq::launch_encode<64, true>(a, in_f32, fast, grid, s);
+    else tvq::launch_encode<64, false>(a, in_f32, fast, grid, s);
+  } else {
+    return -1;
+  }
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }

@@ -45,6 +45,16 @@ struct FastDiv {
   uint32_t div;
 };
 
+// Paged cache: the pool has the layout of a cache of `n_blocks` sequences of 2^block_log2
+// tokens, and token t of sequence b lives in pool block table[b * max_blocks + (t >> block_log2)],
+// row t & (2^block_log2 - 1).  table == nullptr: the contiguous layout.  `seq` is per-sequence
+// device data: the first position written (encode) or the context length (attention).
+struct Paging {
+  const int32_t* table;
+  const int32_t* seq;
+  uint32_t max_blocks, n_blocks, block_log2;
+};
+
 struct EncodeArgs {
   const void* k;
   const void* v;
@@ -64,6 +74,7 @@ struct EncodeArgs {
   uint32_t tiles_per_wave;
   uint32_t num_segs;
   float inv_d;           // 1/d (exact)
+  Paging pg;             // paged destination (the paged entry point only)
 };
 
 struct DecodeArgs {
@@ -85,6 +96,7 @@ struct DecodeArgs {
   uint32_t waves_per_seg;
   uint32_t tiles_per_wave;
   uint32_t num_segs;
+  Paging pg;             // paged source (the paged entry point only)
 };
 
 // Attention of one query token per sequence over one layer of the cache (tvq_attention_decode).
@@ -108,6 +120,7 @@ struct AttnArgs {
   uint32_t pass_heads, n_pass;  // query heads per chunk wave (<= kAttnPassHeads), passes over G
   uint32_t q_f32;        // query dtype: 1 = fp32, 0 = bf16
   float qscale;          // scale * log2(e): scores in log2 units
+  Paging pg;             // pg.seq: context length per sequence (nullptr: t_end for all)
 };
 
 constexpr int kAttnPassHeads = 4;           // accumulators of 4 query heads per wave
@@ -126,6 +139,7 @@ constexpr uint32_t kFastTilesPerWave = 4;
 }  // namespace tvq
 
 // Kernel launchers (defined in the .hip kernel files).
+// `a.pg.table` selects the paged instantiations (decode: the generic kernel only).
 int tvq_launch_encode(const tvq::EncodeArgs& a, int d, int in_f32, bool fast, unsigned grid,
                       void* stream);
 int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, unsigned grid,

@@ -256,3 +256,55 @@ def compare_decode(s: Setup, cache_dev, lay, B, t0, t1) -> DecodeReport:
             rep.bf16_max_ulp = int(du.max(initial=0))
             rep.bf16_mismatch_elems = int((du > 0).sum())
     return rep
+
+
+def gather_paged(pool: np.ndarray, s: Setup, n_blocks: int, block_tokens: int,
+                 table_row, poison: int) -> np.ndarray:
+    """The bytes of one sequence's cache in the contiguous layout (one sequence of
+    len(table_row) * block_tokens slots), taken from a paged pool (the layout of n_blocks
+    sequences of block_tokens slots) through the sequence's block table row.  Positions whose
+    entry names no pool block hold `poison`."""
+    max_blocks = len(table_row)
+    cap = max_blocks * block_tokens
+    total_c, off_c = s.orc.layout(1, cap)
+    _, off_p = s.orc.layout(n_blocks, block_tokens)
+    out = np.full(total_c, poison, np.uint8)
+    for l in range(s.L):
+        for kind in range(2):
+            rec = s.orc.record_bytes(l, kind)
+            for p in range(3):
+                if rec[p] == 0:
+                    continue
+                n_src = n_blocks * s.H * block_tokens * rec[p]
+                src = pool[off_p[l, kind, p]: off_p[l, kind, p] + n_src].reshape(
+                    n_blocks, s.H, block_tokens, rec[p])
+                dst = out[off_c[l, kind, p]: off_c[l, kind, p] + s.H * cap * rec[p]].reshape(
+                    s.H, max_blocks, block_tokens, rec[p])
+                for i, blk in enumerate(table_row):
+                    if 0 <= blk < n_blocks:
+                        dst[:, i] = src[blk]
+    return out
+
+
+def attention_error_bar(s: Setup, host_cache: np.ndarray, B: int, T_cap: int, layer: int,
+                        t_end: int, q64: np.ndarray, scale: float, ref: np.ndarray,
+                        f32_out: bool) -> np.ndarray:
+    """Per output vector, the bar for GPU attention against the oracle's fp64 attention over
+    the same cache bytes (u = 2^-24, the fp32 unit roundoff):
+      |o_gpu - o_ref| <= (2 ds + 64 u) max_t |v^_t|  (+ 2^-9 |o_ref| for a bf16 output)
+    with ds = 4 u sqrt(d) |scale| |q| max_t |k^_t| a bound on the score error: the fp32 decode
+    of k^ and the d-term dot product each round ~sqrt(d) times at u relative to |q||k^| (random
+    walk, x4 margin).  A score error ds moves the normalized weights by <= 2 ds relative, i.e.
+    o by <= 2 ds max|v^|; the weighted sums and the chunk merge add a few u each.  Normalizing
+    by max|v^| rather than |o| keeps the bar meaningful where the average cancels."""
+    Hq = q64.shape[1]
+    G = Hq // s.H
+    dec = s.orc.decode_cache(host_cache, B, T_cap, 0, t_end)[layer]      # [2][B][H][t][d]
+    kmax = np.repeat(np.linalg.norm(dec[0], axis=-1).max(axis=-1), G, axis=1)   # [B][Hq]
+    vmax = np.repeat(np.linalg.norm(dec[1], axis=-1).max(axis=-1), G, axis=1)
+    u = 2.0 ** -24
+    ds = 4 * u * np.sqrt(s.d) * abs(scale) * np.linalg.norm(q64, axis=-1) * kmax
+    bar = (2 * ds + 64 * u) * vmax
+    if not f32_out:
+        bar = bar + 2.0 ** -9 * np.linalg.norm(ref, axis=-1)
+    return bar

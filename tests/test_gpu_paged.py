@@ -1,0 +1,307 @@
+"""GPU parity of the paged-cache entry points (tvq_encode_paged, tvq_decode_paged,
+tvq_attention_paged), called through the C ABI, against the oracle on the contiguous cache
+that a sequence's block table describes (gathered on the host), and replay of a
+graph-captured decode step against the same step run eagerly.
+
+Bars: as for the contiguous entry points (codes bit-exact except flagged pairs, fp32 decode
+bit-exact against the oracle's fixed-order decode, attention within
+parity.attention_error_bar); positions without a pool block are never written and decode to
+zeros; pool blocks no table names keep their bytes; graph replays equal eager runs bit for
+bit."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from workloads import LayerCfg, NORM_LINEAR, NORM_LOG
+
+from parity import (Setup, attention_error_bar, bf16_bits_to_torch, compare_encode,
+                    gather_paged, torch_to_np)
+
+pytestmark = pytest.mark.gpu
+
+POISON = 0xAB
+P = 32                   # tokens per block
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _draw(L, B, H, T, d, seed):
+    w = workloads.get("C2")
+    ww = workloads.Workload(w.name, L, B, H, T, d, "bf16", w.table[:L], seed, w.sign_seed,
+                            w.k_dist, w.v_dist, w.n_outlier, w.outlier_scale)
+    return workloads.generate(ww, "K"), workloads.generate(ww, "V")
+
+
+class PagedCase:
+    """3 sequences over a pool of 14 blocks of 32 slots, max 5 blocks per sequence.
+    Sequence 0 holds 5 blocks, sequence 1 holds 4 (its last entry -1), sequence 2 holds 3 (then
+    -1 and 99, which is past the pool); two pool blocks belong to no sequence."""
+
+    def __init__(self, d, table, seed):
+        import torch
+        self.L, self.H, self.d = len(table), 2, d
+        self.s = Setup(self.L, self.H, d, table, workloads.sign_table(seed, self.L, d)).build()
+        self.B, self.max_blocks, self.n_blocks = 3, 5, 14
+        perm = np.random.default_rng(seed).permutation(self.n_blocks)
+        self.table = np.array([perm[0:5], list(perm[5:9]) + [-1], list(perm[9:12]) + [-1, 99]],
+                              np.int32)
+        self.unused = perm[12:]
+        self.cap = self.max_blocks * P
+        self.pool_lay = self.s.gpu.pool_layout(self.n_blocks, P)
+        self.pool = torch.full((self.pool_lay.total_bytes,), POISON, dtype=torch.uint8,
+                               device="cuda")
+        self.table_dev = torch.from_numpy(self.table).cuda()
+        # the oracle's picture: one contiguous cache per sequence, and the slots written
+        self.ocache = [np.full(self.s.orc.layout(1, self.cap)[0], POISON, np.uint8)
+                       for _ in range(self.B)]
+        self.written = [np.zeros(self.cap, bool) for _ in range(self.B)]
+        self.steps = []          # (b, t_begin, T, u, t) of every oracle encode
+
+    def allocated(self, b, pos):
+        blk = self.table[b, pos // P] if pos < self.cap else -1
+        return 0 <= blk < self.n_blocks
+
+    def encode(self, positions, T, seed):
+        """Encode T tokens per sequence at positions[b] on the GPU (paged) and, for the
+        positions that have a pool block, on the oracle."""
+        import torch
+        k, v = _draw(self.L, self.B, self.H, T, self.d, seed)
+        pos = torch.tensor(positions, dtype=torch.int32, device="cuda")
+        self.s.gpu.encode_paged(bf16_bits_to_torch(k).cuda(), bf16_bits_to_torch(v).cuda(), pos,
+                                self.table_dev, self.pool, self.pool_lay)
+        for b, p0 in enumerate(positions):
+            if p0 < 0:
+                continue
+            ok = [self.allocated(b, p0 + t) for t in range(T)]
+            # the oracle encodes each maximal run of allocated positions
+            t = 0
+            while t < T:
+                if not ok[t]:
+                    t += 1
+                    continue
+                e = t
+                while e < T and ok[e]:
+                    e += 1
+                u, tt = self.s.orc.encode_cache(np.ascontiguousarray(k[:, b:b + 1, :, t:e]),
+                                                np.ascontiguousarray(v[:, b:b + 1, :, t:e]),
+                                                p0 + t, self.cap, self.ocache[b])
+                self.steps.append((b, p0 + t, e - t, u, tt))
+                self.written[b][p0 + t:p0 + e] = True
+                t = e
+        torch.cuda.synchronize()
+
+    def gathered(self):
+        host = torch_to_np(self.pool)
+        return host, [gather_paged(host, self.s, self.n_blocks, P, self.table[b], POISON)
+                      for b in range(self.B)]
+
+
+def _check_codes(case, name):
+    host, gath = case.gathered()
+    flagged = 0
+    for b, t0, T, u, t in case.steps:
+        rep = compare_encode(case.s, gath[b], case.ocache[b], u, t, 1, T, case.cap, t0)
+        flagged += rep.angle_flagged + rep.norm_flagged
+        for note in rep.notes[:20]:
+            _say("   " + note)
+        assert rep.angle_unflagged_mismatch == 0 and rep.norm_unflagged_mismatch == 0
+        assert rep.header_max_ulp <= 2 and rep.f32norm_max_ulp <= 2
+    _say(f"[{name}] {len(case.steps)} encode runs checked, flagged pairs {flagged}")
+    # positions never written keep the poison, and so do the pool blocks no sequence holds
+    for b in range(case.B):
+        _, off = case.s.orc.layout(1, case.cap)
+        for l in range(case.L):
+            for kind in range(2):
+                rec = case.s.orc.record_bytes(l, kind)
+                for p in range(3):
+                    if rec[p] == 0:
+                        continue
+                    plane = gath[b][off[l, kind, p]: off[l, kind, p] + case.H * case.cap * rec[p]]
+                    plane = plane.reshape(case.H, case.cap, rec[p])
+                    assert np.all(plane[:, ~case.written[b]] == POISON)
+    _, offp = case.s.orc.layout(case.n_blocks, P)
+    for l in range(case.L):
+        for kind in range(2):
+            rec = case.s.orc.record_bytes(l, kind)
+            for p in range(3):
+                if rec[p] == 0:
+                    continue
+                n = case.n_blocks * case.H * P * rec[p]
+                plane = host[offp[l, kind, p]: offp[l, kind, p] + n].reshape(
+                    case.n_blocks, case.H, P, rec[p])
+                assert np.all(plane[case.unused] == POISON)
+    return host, gath
+
+
+@pytest.mark.parametrize("d", [128, 64])
+def test_paged_encode_decode(gpu, d):
+    """Prefill, a ragged second prefill that runs into a missing block, per-sequence appends
+    (one into a missing block), and negative / past-the-table positions; then the paged decode
+    of every position, fp32 and bf16."""
+    import torch
+    table = [LayerCfg(64, 64), LayerCfg(256, 64), LayerCfg(48, 128, 5, 3, NORM_LINEAR, NORM_LOG)]
+    case = PagedCase(d, table, seed=31 + d)
+    case.encode([0, 0, 0], 70, seed=1)
+    case.encode([70, 70, 70], 30, seed=2)        # sequence 2 runs into its missing 4th block
+    case.encode([100, 127, 96], 1, seed=3)       # appends; sequence 2's lands on no block
+    case.encode([-1, 128, 97], 1, seed=4)        # nothing has a block
+    _, gath = _check_codes(case, f"paged-encode-d{d}")
+
+    # decode every position of every sequence through the table
+    shape = (case.L, case.B, case.H, case.cap, d)
+    for dt in (torch.float32, torch.bfloat16):
+        ko = torch.full(shape, float("nan"), dtype=dt, device="cuda")
+        vo = torch.full(shape, float("nan"), dtype=dt, device="cuda")
+        case.s.gpu.decode_paged(case.pool, case.pool_lay, case.table_dev, 0, case.cap, ko, vo)
+        torch.cuda.synchronize()
+        g = np.stack([torch_to_np(ko), torch_to_np(vo)], axis=1)       # [L,2,B,H,T,d]
+        for b in range(case.B):
+            gb = g[:, :, b]
+            has = np.array([case.allocated(b, t) for t in range(case.cap)])
+            # the oracle decodes the written runs only (unwritten slots hold poison bytes)
+            w = case.written[b].astype(np.int8)
+            edges = np.flatnonzero(np.diff(np.concatenate([[0], w, [0]])))
+            for a, e in zip(edges[0::2], edges[1::2]):
+                ref = case.s.orc.decode_cache(gath[b], 1, case.cap, a, e, "f32")[:, :, 0]
+                gw = gb[..., a:e, :]
+                if dt == torch.float32:
+                    same = (gw.view(np.uint32) == ref.view(np.uint32)) | ((gw == 0) & (ref == 0))
+                    assert same.all(), f"sequence {b} [{a}, {e}): fp32 decode differs"
+                else:
+                    rb = oracle.f32_to_bf16(ref)
+                    zero = ((gw & 0x7FFF) == 0) & ((rb & 0x7FFF) == 0)
+                    assert np.all((gw == rb) | zero), f"sequence {b} [{a}, {e}): bf16 differs"
+            if dt == torch.float32:
+                assert np.all(gb[..., ~has, :] == 0)
+            else:
+                assert np.all((gb[..., ~has, :] & 0x7FFF) == 0)
+    _say(f"[paged-decode-d{d}] fp32 bit-exact on written positions, zeros without a block")
+
+
+@pytest.mark.parametrize("d,G", [(128, 4), (64, 3)])
+def test_paged_attention(gpu, d, G):
+    """Attention with a different context length per sequence (one of them 0), through the
+    block tables, against the oracle on each sequence's gathered cache; then the same with a
+    smaller max_ctx, which clips the longer contexts."""
+    import torch
+    table = [LayerCfg(64, 64), LayerCfg(256, 256, 4, 8, NORM_LOG, NORM_LINEAR)]
+    case = PagedCase(d, table, seed=17 + d)
+    case.encode([0, 0, 0], 96, seed=5)
+    case.encode([96, 96, 96], 40, seed=6)        # sequence 2 has no block past 95
+    _, gath = _check_codes(case, f"paged-attn-setup-d{d}")
+    Hq = case.H * G
+    rng = np.random.default_rng(d + G)
+    q = (rng.standard_normal((case.B, Hq, d)) * 2.0).astype(np.float32)
+    qd = torch.from_numpy(q).cuda()
+    scale = 1.0 / np.sqrt(d)
+    for max_ctx, lens in ((case.cap, [136, 57, 0]), (64, [136, 57, 40])):
+        ctx = torch.tensor(lens, dtype=torch.int32, device="cuda")
+        for layer in range(case.L):
+            out = torch.full((case.B, Hq, d), float("nan"), dtype=torch.float32, device="cuda")
+            case.s.gpu.attention_paged(case.pool, case.pool_lay, case.table_dev, ctx, max_ctx,
+                                       layer, qd, out, scale)
+            torch.cuda.synchronize()
+            got = out.cpu().numpy().astype(np.float64)
+            for b in range(case.B):
+                n = min(lens[b], max_ctx)
+                if n <= 0:
+                    assert np.all(got[b] == 0), "an empty context gives zeros"
+                    continue
+                q64 = q[b:b + 1].astype(np.float64)
+                ref = case.s.orc.attention_decode(gath[b], 1, case.cap, layer, n, q64, scale)
+                bar = attention_error_bar(case.s, gath[b], 1, case.cap, layer, n, q64, scale,
+                                          ref, True)
+                err = np.linalg.norm(got[b:b + 1] - ref, axis=-1)
+                _say(f"[paged-attn d={d} G={G} layer={layer} max_ctx={max_ctx} seq={b} "
+                     f"ctx={n}] max |err|/bar = {(err / bar).max():.3f}")
+                assert np.isfinite(got[b]).all() and (err <= bar).all()
+
+
+def test_paged_step_graph_replay(gpu):
+    """A decode step -- append one token per sequence and layer, then attention of every
+    layer with contexts one past the appended positions, then advance the positions on the
+    device -- captured once in a HIP graph and replayed four times, each replay checked bit for
+    bit against the same step run eagerly on a copy of the pool, with new inputs and eager
+    work between the replays."""
+    import torch
+    d, G = 128, 4
+    table = [LayerCfg(64, 64), LayerCfg(256, 64)]
+    case = PagedCase(d, table, seed=77)
+    case.encode([0, 0, 0], 60, seed=8)
+    L, B, H, Hq = case.L, case.B, case.H, case.H * G
+    max_ctx = 96                                  # every sequence holds blocks for [0, 96)
+    s = case.s.gpu
+    pool_e = case.pool.clone()                    # eager copy
+    pool_g = case.pool                            # graph copy
+    kin = torch.empty((L, B, H, 1, d), dtype=torch.bfloat16, device="cuda")
+    vin = torch.empty_like(kin)
+    q = torch.randn((L, B, Hq, d), generator=torch.Generator(device="cuda").manual_seed(3),
+                    device="cuda")
+    ws_bytes = s.attention_paged_workspace_bytes(B, Hq, max_ctx, P)
+
+    def buffers():
+        return {"pos": torch.tensor([60, 61, 62], dtype=torch.int32, device="cuda"),
+                "ctx": torch.zeros(B, dtype=torch.int32, device="cuda"),
+                "out": torch.zeros((L, B, Hq, d), dtype=torch.float32, device="cuda"),
+                "ws": torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")}
+
+    def step(pool, bf):
+        s.encode_paged(kin, vin, bf["pos"], case.table_dev, pool, case.pool_lay)
+        torch.add(bf["pos"], 1, out=bf["ctx"])
+        for layer in range(L):
+            s.attention_paged(pool, case.pool_lay, case.table_dev, bf["ctx"], max_ctx, layer,
+                              q[layer], bf["out"][layer], 1.0 / np.sqrt(d), workspace=bf["ws"])
+        bf["pos"].add_(1)
+
+    be, bg = buffers(), buffers()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(pool_g, bg)
+    torch.cuda.synchronize()
+    for r in range(4):
+        k, v = _draw(L, B, H, 1, d, seed=100 + r)
+        kin.copy_(bf16_bits_to_torch(k).cuda())
+        vin.copy_(bf16_bits_to_torch(v).cuda())
+        step(pool_e, be)                         # eager
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(be["pos"], bg["pos"]) and torch.equal(be["ctx"], bg["ctx"])
+        assert torch.equal(pool_e, pool_g), f"replay {r}: pool differs from the eager step"
+        assert torch.equal(be["out"].view(torch.int32), bg["out"].view(torch.int32)), \
+            f"replay {r}: attention output differs from the eager step"
+        assert torch.isfinite(bg["out"]).all()
+        _say(f"[paged-graph] replay {r}: positions {bg['pos'].tolist()}, pool and outputs "
+             f"equal to the eager step")
+
+
+def test_paged_api_errors(gpu):
+    """Bad pools, tables and sizes are rejected before any launch."""
+    import torch
+    import paper_2603_27467_amd as tvq
+    case = PagedCase(128, [LayerCfg(64, 64)], seed=3)
+    s = case.s.gpu
+    k = torch.zeros((1, 3, 2, 1, 128), dtype=torch.bfloat16, device="cuda")
+    pos = torch.zeros(3, dtype=torch.int32, device="cuda")
+    bad_lay = s.pool_layout(case.n_blocks, 48)            # block size not a power of two
+    with pytest.raises(tvq.TvqError):
+        s.encode_paged(k, k, pos, case.table_dev, case.pool, bad_lay)
+    small = s.pool_layout(case.n_blocks, 16)              # below 32 slots
+    with pytest.raises(tvq.TvqError):
+        s.encode_paged(k, k, pos, case.table_dev, case.pool, small)
+    with pytest.raises(ValueError):
+        s.encode_paged(k, k, pos.long(), case.table_dev, case.pool, case.pool_lay)
+    q = torch.zeros((3, 8, 128), dtype=torch.float32, device="cuda")
+    with pytest.raises(tvq.TvqError):                    # max_ctx past the table
+        s.attention_paged(case.pool, case.pool_lay, case.table_dev, pos, case.cap + 1, 0, q,
+                          torch.empty_like(q), 0.1)
+    with pytest.raises(tvq.TvqError):                    # layer out of range
+        s.attention_paged(case.pool, case.pool_lay, case.table_dev, pos, case.cap, 1, q,
+                          torch.empty_like(q), 0.1)

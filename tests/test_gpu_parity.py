@@ -21,8 +21,9 @@ import oracle
 import workloads
 from workloads import LayerCfg, NORM_F32, NORM_LINEAR, NORM_LOG
 
-from parity import (Setup, bf16_bits_to_torch, bf16_differ, compare_decode, compare_encode,
-                    run_encode, setup_from_workload, torch_to_np, untouched_outside)
+from parity import (Setup, attention_error_bar, bf16_bits_to_torch, bf16_differ, compare_decode,
+                    compare_encode, run_encode, setup_from_workload, torch_to_np,
+                    untouched_outside)
 
 pytestmark = pytest.mark.gpu
 
@@ -470,20 +471,12 @@ def _attention_case(d, G, T, table, seed, q_bf16=False):
 
 
 def _attention_check(s, lay, cache, q, layer, t_end, scale, name, q_dtype=None, o_dtype=None):
-    """GPU attention against the oracle's fp64 attention over the same cache bytes.
-
-    Bar, per output vector o of query q (u = 2^-24, fp32 unit roundoff):
-      |o_gpu - o_ref| <= (2 ds + 64 u) max_t |v^_t|  (+ 2^-9 |o_ref| for a bf16 output)
-    where ds = 4 u sqrt(d) |scale| |q| max_t |k^_t| bounds the score error: the fp32 decode of
-    k^ and the d-term dot product each round ~sqrt(d) times at u relative to |q||k^| (random
-    walk, x4 margin).  A score error ds moves the normalized weights by <= 2 ds relative, i.e.
-    o by <= 2 ds max|v^|; the weighted sums and the chunk merge add a few u each.  Normalizing
-    by max|v^| rather than |o| keeps the bar meaningful where the average cancels."""
+    """GPU attention against the oracle's fp64 attention over the same cache bytes, per output
+    vector within parity.attention_error_bar (derived from fp32 rounding of the scores)."""
     import torch
     q_dtype = q_dtype or torch.float32
     o_dtype = o_dtype or torch.float32
     B, Hq, d = q.shape
-    G = Hq // s.H
     qd = torch.from_numpy(q).to(q_dtype).cuda()
     out = torch.full((B, Hq, d), float("nan"), dtype=o_dtype, device="cuda")
     s.gpu.attention(cache, lay, layer, t_end, qd, out, scale)
@@ -492,16 +485,8 @@ def _attention_check(s, lay, cache, q, layer, t_end, scale, name, q_dtype=None, 
     host = torch_to_np(cache)
     q64 = qd.float().cpu().numpy().astype(np.float64)
     ref = s.orc.attention_decode(host, B, lay.capacity_tokens, layer, t_end, q64, scale)
-    dec = s.orc.decode_cache(host, B, lay.capacity_tokens, 0, t_end)[layer]   # [2][B][H][t][d]
-    kmax = np.linalg.norm(dec[0], axis=-1).max(axis=-1)                      # [B][H]
-    vmax = np.linalg.norm(dec[1], axis=-1).max(axis=-1)
-    kmax = np.repeat(kmax, G, axis=1)                                         # [B][Hq]
-    vmax = np.repeat(vmax, G, axis=1)
-    u = 2.0 ** -24
-    ds = 4 * u * np.sqrt(d) * abs(scale) * np.linalg.norm(q64, axis=-1) * kmax
-    bar = (2 * ds + 64 * u) * vmax
-    if o_dtype != torch.float32:
-        bar = bar + 2.0 ** -9 * np.linalg.norm(ref, axis=-1)
+    bar = attention_error_bar(s, host, B, lay.capacity_tokens, layer, t_end, q64, scale, ref,
+                              o_dtype == torch.float32)
     err = np.linalg.norm(got - ref, axis=-1)
     rel = err / np.linalg.norm(ref, axis=-1)
     _say(f"[{name}] t_end={t_end} max |err|/bar = {(err / bar).max():.3f}, max rel L2 "
