@@ -47,6 +47,7 @@ CODEC_SOURCES = ["tvq_encode.hip", "tvq_decode.hip", "tvq_codes.h", "tvq_device.
 ATTENTION_SOURCES = ["tvq_attention.hip", "tvq_codes.h", "tvq_device.h", "tvq_internal.h"]
 ATTENTION_COUNTERS = os.path.join(ROOT, "profiles", "longctx_c5_attention_counters.json")
 ATTN_GROUP = 4          # query heads per KV head (32 query heads over 8 KV heads)
+PAGE_TOKENS = 256       # slots per block of the paged pool
 
 
 def kernel_source_hash(names=None) -> str:
@@ -426,13 +427,28 @@ def run_longctx(w: workloads.Workload, args) -> dict:
     shape = (w.L, w.B, w.H, w.T, w.d)
     print(f"# workload {w.name}: drawing {2 * np.prod(shape) * 2 / 1e9:.1f} GB of bf16 on the "
           f"GPU, cache {lay.total_bytes / 1e9:.1f} GB", file=sys.stderr, flush=True)
-    cache = torch.empty(lay.total_bytes, dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
+    if args.paged:
+        # a pool of PAGE_TOKENS-slot blocks, handed to the sequences in a shuffled order
+        max_blocks = -(-cap // PAGE_TOKENS)
+        n_blocks = w.B * max_blocks
+        pool_lay = codec.pool_layout(n_blocks, PAGE_TOKENS)
+        perm = np.random.default_rng(w.data_seed).permutation(n_blocks).astype(np.int32)
+        table = torch.from_numpy(perm.reshape(w.B, max_blocks)).cuda()
+        cache = torch.empty(pool_lay.total_bytes, dtype=torch.uint8, device="cuda")
+        pos = torch.zeros(w.B, dtype=torch.int32, device="cuda")
+        ctx = torch.zeros(w.B, dtype=torch.int32, device="cuda")
+    else:
+        cache = torch.empty(lay.total_bytes, dtype=torch.uint8, device="cuda")
     k = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
     workloads.fill_device(w, "K", k)
     v = torch.empty_like(k)
     workloads.fill_device(w, "V", v)
-    codec.encode(k, v, cache, lay, 0, stream)
+    if args.paged:
+        codec.encode_paged(k, v, pos, table, cache, pool_lay, stream)
+        pos.fill_(w.T)
+    else:
+        codec.encode(k, v, cache, lay, 0, stream)
     torch.cuda.synchronize()
     del k, v
     torch.cuda.empty_cache()
@@ -446,15 +462,53 @@ def run_longctx(w: workloads.Workload, args) -> dict:
         g.manual_seed(w.data_seed + 7)
         qs = torch.randn((w.L, w.B, Hq, w.d), generator=g, device="cuda").to(torch.bfloat16)
         os_ = torch.empty_like(qs)
-        ws = torch.empty(codec.attention_workspace_bytes(w.B, Hq, cap), dtype=torch.uint8,
-                         device="cuda")
+        ws_bytes = (codec.attention_paged_workspace_bytes(w.B, Hq, cap, PAGE_TOKENS)
+                    if args.paged else codec.attention_workspace_bytes(w.B, Hq, cap))
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
         scale = 1.0 / float(np.sqrt(w.d))
     else:
         ko = torch.empty((w.L, w.B, w.H, cap, w.d), dtype=torch.bfloat16, device="cuda")
         vo = torch.empty_like(ko)
 
+    if args.paged:
+        # the serving step: every step-varying value (positions, context lengths) lives on
+        # the device, so the step can be captured once and replayed
+        kin = torch.empty((w.L, w.B, w.H, 1, w.d), dtype=torch.bfloat16, device="cuda")
+        vin = torch.empty_like(kin)
+
+        def paged_step():
+            # stream=None: the current stream when called (the capture stream under capture)
+            codec.encode_paged(kin, vin, pos, table, cache, pool_lay)
+            torch.add(pos, 1, out=ctx)
+            for layer in range(w.L):
+                codec.attention_paged(cache, pool_lay, table, ctx, cap, layer, qs[layer],
+                                      os_[layer], scale, ws)
+            pos.add_(1)
+
+        graph = None
+        if args.graph:
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                paged_step()
+            torch.cuda.synchronize()
+
     def step(i, ev=None):
         t = w.T + i
+        if args.paged:
+            if ev is not None:
+                ev[0].record(stream)
+            kin.copy_(kn[:, :, :, i:i + 1])
+            vin.copy_(vn[:, :, :, i:i + 1])
+            if ev is not None:
+                ev[1].record(stream)
+            if graph is not None:
+                graph.replay()
+            else:
+                paged_step()
+            if ev is not None:
+                ev[2].record(stream)
+            return
         if ev is not None:
             ev[0].record(stream)
         codec.encode(kn[:, :, :, i:i + 1], vn[:, :, :, i:i + 1], cache, lay, t, stream)
@@ -507,15 +561,24 @@ def run_longctx(w: workloads.Workload, args) -> dict:
             "config": {"workload": w.name, "layers": w.L, "batch": w.B, "kv_heads": w.H,
                        "q_heads": w.H * ATTN_GROUP, "tokens_cached": w.T, "head_dim": w.d,
                        "io_dtype": w.dtype, "table": w.notes,
-                       "step": "encode 1 token per sequence and layer, then attention of one "
-                               "query token per sequence over the whole cache, every layer",
+                       "step": ("paged pool of %d-slot blocks (shuffled block tables), "
+                                "%s: append 1 token per sequence and layer at device-side "
+                                "positions, then attention of every layer over device-side "
+                                "context lengths" % (PAGE_TOKENS, "one graph replay"
+                                                     if args.graph else "eager launches")
+                                if args.paged else
+                                "encode 1 token per sequence and layer, then attention of "
+                                "one query token per sequence over the whole cache, every "
+                                "layer"),
                        "compressed_bytes_per_token": rec_tok},
             "roofline": {"bound": "hbm", "kernel": "tvq_attention (chunk + merge)",
                          "achieved": round(att_gbs, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": round(att_gbs / HBM_PEAK_GBPS, 4),
                          "traffic": None if prof is None else prof["hbm_bytes_per_step"],
                          "algorithmic_bytes_per_step": int(att_bytes)},
-            "encode": {"ms": round(float(enc.mean()), 5), "ms_min": round(float(enc.min()), 5)},
+            "encode": ({"input_copy_ms": round(float(enc.mean()), 5)} if args.paged else
+                       {"ms": round(float(enc.mean()), 5),
+                        "ms_min": round(float(enc.min()), 5)}),
             "attention": {"ms": round(dec_ms, 5), "ms_median": round(float(np.median(dec)), 5),
                           "ms_min": round(float(dec.min()), 5),
                           "ms_per_layer": round(dec_ms / w.L, 5),
@@ -573,6 +636,10 @@ def main() -> int:
     ap.add_argument("--attention", action="store_true",
                     help="long-context workload: attention over the compressed cache in place "
                          "of the full decode")
+    ap.add_argument("--paged", action="store_true",
+                    help="long-context attention step over a paged pool (implies --attention)")
+    ap.add_argument("--graph", action="store_true",
+                    help="with --paged: capture the step once and replay it")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for counter scaling)")
     ap.add_argument("--summarize-profiles", nargs=5,
@@ -585,6 +652,8 @@ def main() -> int:
     ap.add_argument("--commands", nargs="*", default=[],
                     help="the profiling commands, recorded in the summary")
     args = ap.parse_args()
+    if args.paged:
+        args.attention = True
     if args.summarize_profiles:
         return summarize_profiles(*args.summarize_profiles, args.commands)
     if args.summarize_attention_profiles:
