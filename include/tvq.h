@@ -133,6 +133,18 @@ tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, con
                       const tvq_tensor_desc* in, int64_t t_begin, void* cache,
                       const tvq_layout* lay, void* stream);
 
+/* tvq_encode for bf16 input at d = 128 with a different transform schedule, for comparison:
+ * in the layers whose formats have the dedicated kernel (n = 64/256, 8-bit linear or 4-bit
+ * log norms), the butterfly stages over element bits 0, 1, 5 and 6 run as one 16-point
+ * Hadamard product per 16 vectors on the matrix cores (bf16 operands, fp32 accumulation) and
+ * the other three stages follow in registers.  Every stage of W is applied, but not in the
+ * canonical ascending order, so a code can differ from tvq_encode's where rounding moves the
+ * angle or norm coordinate across a bin boundary (inside the 1e-6-of-range flag zone of the
+ * parity rule); other layers are encoded as by tvq_encode.  TVQ_ERR_UNSUPPORTED for d != 128. */
+tvq_status tvq_encode_mfma(const tvq_codec* c, const void* k, const void* v,
+                           const tvq_tensor_desc* in, int64_t t_begin, void* cache,
+                           const tvq_layout* lay, void* stream);
+
 /* Decode (section 3.1, reconstruction) cache slots [t_begin, t_end) of every (layer, batch,
  * head) into k_out / v_out, described by `out` (out->tokens == t_end - t_begin,
  * out->batch == lay->batch), as `out_dtype` (bf16 rounded to nearest even, or fp32).

@@ -82,6 +82,9 @@ def load_library():
     L.tvq_attention_decode.argtypes = [vp, vp, ctypes.POINTER(tvq_layout), i32, i64, i32,
                                        ctypes.c_float, ctypes.c_int, vp, ctypes.c_int, vp, vp, i64,
                                        vp]
+    L.tvq_encode_mfma.restype = ctypes.c_int
+    L.tvq_encode_mfma.argtypes = [vp, vp, vp, ctypes.POINTER(tvq_tensor_desc), i64, vp,
+                                  ctypes.POINTER(tvq_layout), vp]
     L.tvq_encode_paged.restype = ctypes.c_int
     L.tvq_encode_paged.argtypes = [vp, ctypes.c_int, vp, vp, ctypes.POINTER(tvq_tensor_desc),
                                    vp, vp, i32, vp, ctypes.POINTER(tvq_layout), vp]
@@ -188,6 +191,14 @@ def tvq_attention_decode(handle: int, cache_ptr: int, lay: tvq_layout, layer: in
         num_q_heads, ctypes.c_float(scale), q_dtype, ctypes.c_void_p(q_ptr), o_dtype,
         ctypes.c_void_p(o_ptr), ctypes.c_void_p(ws_ptr), ws_bytes, ctypes.c_void_p(stream)),
         "tvq_attention_decode")
+
+
+def tvq_encode_mfma(handle: int, k_ptr: int, v_ptr: int, desc: tvq_tensor_desc, t_begin: int,
+                    cache_ptr: int, lay: tvq_layout, stream: int = 0) -> None:
+    _check(load_library().tvq_encode_mfma(
+        ctypes.c_void_p(handle), ctypes.c_void_p(k_ptr), ctypes.c_void_p(v_ptr),
+        ctypes.byref(desc), t_begin, ctypes.c_void_p(cache_ptr), ctypes.byref(lay),
+        ctypes.c_void_p(stream)), "tvq_encode_mfma")
 
 
 def tvq_encode_paged(handle: int, in_dtype: int, k_ptr: int, v_ptr: int, desc: tvq_tensor_desc,

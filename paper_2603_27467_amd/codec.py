@@ -86,6 +86,16 @@ class Codec:
         C.tvq_encode(self.handle, dt, k.data_ptr(), v.data_ptr(), desc_of(k), t_begin,
                      cache.data_ptr(), lay, _stream_handle(stream))
 
+    def encode_mfma(self, k, v, cache, lay: C.tvq_layout, t_begin: int = 0,
+                    stream=None) -> None:
+        """encode with the matrix-core transform schedule (tvq_encode_mfma; bf16, d = 128)."""
+        import torch
+        if k.shape != v.shape or k.stride() != v.stride() or k.dtype != torch.bfloat16 or \
+                v.dtype != torch.bfloat16:
+            raise ValueError("k and v must be bf16 and share shape and strides")
+        C.tvq_encode_mfma(self.handle, k.data_ptr(), v.data_ptr(), desc_of(k), t_begin,
+                          cache.data_ptr(), lay, _stream_handle(stream))
+
     def decode(self, cache, lay: C.tvq_layout, t_begin: int, t_end: int, k_out, v_out,
                stream=None) -> None:
         import torch

@@ -464,6 +464,28 @@ tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, con
   return encode_launch(c, a, in, in_dtype == TVQ_F32, stream);
 }
 
+tvq_status tvq_encode_mfma(const tvq_codec* c, const void* k, const void* v,
+                           const tvq_tensor_desc* in, int64_t t_begin, void* cache,
+                           const tvq_layout* lay, void* stream) {
+  if (!c || !in || !lay) return TVQ_ERR_INVALID_ARG;
+  if (c->d != 128) return TVQ_ERR_UNSUPPORTED;
+  if (!desc_valid(c, in, 2) || !layout_matches(c, lay)) return TVQ_ERR_INVALID_ARG;
+  if (in->batch != lay->batch) return TVQ_ERR_INVALID_ARG;
+  if (t_begin < 0 || t_begin + in->tokens > lay->capacity_tokens) return TVQ_ERR_INVALID_ARG;
+  if (in->tokens == 0) return TVQ_OK;
+  if (!k || !v || !cache || !aligned16(k) || !aligned16(v) || !aligned16(cache))
+    return TVQ_ERR_INVALID_ARG;
+  tvq::EncodeArgs a;
+  std::memset(&a, 0, sizeof(a));
+  encode_source(a, k, v, in);
+  a.cache = (uint8_t*)cache;
+  a.n_slots = lay->batch * c->H * lay->capacity_tokens;
+  a.cap = (uint32_t)lay->capacity_tokens;
+  a.t_begin = (uint32_t)t_begin;
+  a.mfma_front = 1;
+  return encode_launch(c, a, in, false, stream);
+}
+
 tvq_status tvq_encode_paged(const tvq_codec* c, tvq_dtype in_dtype, const void* k, const void* v,
                             const tvq_tensor_desc* in, const int32_t* positions,
                             const int32_t* block_table, int32_t max_blocks, void* pool,

@@ -12,6 +12,9 @@
 //                          several consecutive tiles, loading the next tile's input while it
 //                          encodes the current one, and amortizes its set-up over them.
 //   encode_generic_kernel  every other format and fp32 input, one tile per wave.
+//   encode_mfma_kernel     (tvq_encode_mfma, d = 128, bf16, the formats of the fast kernel)
+//                          the first four butterfly stages as one 16-point Hadamard product
+//                          per 16 vectors on the matrix cores; see front_mfma.
 //
 // The kernels are bound by VALU issue, so the per-pair path is kept branch-free and short:
 // codes are rounded by the 1.5*2^23 shift and handed to the packer as raw float bits, whose
@@ -162,15 +165,18 @@ struct EncWave {
   uint32_t unneg;             // sign flip that undoes the negation (odd n)
 };
 
-template <int D>
+// MF: the lane mapping of the matrix-core front end (d = 128): vector slot lane % 16 and
+// element slice lane / 16, instead of a vector per lane quad.
+template <int D, bool MF = false>
 __device__ __forceinline__ bool enc_wave_setup(const EncodeArgs& a, EncWave<D>& w,
                                                uint32_t (*sm_rows)[D / 2], uint32_t& tile0,
                                                uint32_t& ntiles) {
   constexpr int LPV = EncWave<D>::LPV;
   constexpr int VPW = EncWave<D>::VPW;
+  static_assert(!MF || D == 128, "the matrix-core front end is built for d = 128");
   const int lane = threadIdx.x & (kWave - 1);
-  w.sub = lane % LPV;
-  w.vslot = lane / LPV;
+  w.sub = MF ? lane / VPW : lane % LPV;
+  w.vslot = MF ? lane % VPW : lane / LPV;
   const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock +
                                                         (threadIdx.x / kWave));
   const uint32_t li = wave / a.waves_per_seg;
@@ -189,7 +195,7 @@ __device__ __forceinline__ bool enc_wave_setup(const EncodeArgs& a, EncWave<D>& 
   if (lane < D / 2) row[lane] = a.sign_masks[(size_t)w.sp.layer * (D / 2) + lane];
   wave_lds_sync();
   w.sm = row + w.sub * 16;
-  w.negated = lane_negated<LPV>(w.sub);
+  w.negated = MF ? false : lane_negated<LPV>(w.sub);
   const bool odd_n = (w.sp.n & 1u) != 0;
   w.shift = (w.negated && !odd_n) ? kRoundShift - 0.5f * w.sp.nf : kRoundShift;
   w.unneg = (w.negated && odd_n) ? 0x80000000u : 0u;
@@ -234,9 +240,75 @@ __device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const En
 // Encode one tile.  WA = angle code width and NB = norm code width of a format fixed at
 // compile time (NB = 8: linear norms, NB = 4: log-space norms; the angle codebook is then
 // n = 2^WA), or WA = NB = 0 for the segment's run-time format.
-template <int D, bool F32IN, int WA, int NB, bool PAGED>
+// Matrix-core front end (d = 128, bf16): the lane holds elements 32 s .. 32 s + 31 of vector
+// slot v (s = lane / 16, v = lane % 16).  For each m = 0..7, v_mfma_f32_16x16x16_bf16 with
+// A[i][k] = (-1)^popcount(i & k) and B[k][v] = element 32 (k >> 2) + 4 m + (k & 3) of vector v
+// gives the 16-point Hadamard transform over element bits 0, 1, 5 and 6; the lane receives
+// outputs 32 s + 4 m + r, r = 0..3 (the operand layout of the instruction: A and B from lane l
+// at [l % 16][4 (l / 16) + q] and [4 (l / 16) + q][l % 16], C at [4 (l / 16) + r][l % 16]).
+// The products are exact (bf16 times +-1).  The butterfly stages over bits 2, 3 and 4 then
+// run in registers, so every stage of W is applied, in an order other than the canonical one:
+// the result equals the canonical butterfly's whenever the partial sums are exact in fp32,
+// and otherwise differs by rounding.
+__device__ __forceinline__ void front_mfma(const uint32_t (&raw)[16], const uint32_t (&sm)[16],
+                                           float (&x)[kElemsPerLane]) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  typedef float v4f __attribute__((ext_vector_type(4)));
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t i = (uint32_t)lane & 15u, k0 = 4u * ((uint32_t)lane >> 4);
+  v4s amat;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    amat[q] = (__builtin_popcount(i & (k0 + q)) & 1) ? (short)0xBF80 : (short)0x3F80;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    const uint32_t w0 = raw[2 * m] ^ sm[2 * m], w1 = raw[2 * m + 1] ^ sm[2 * m + 1];
+    v4s bmat;
+    bmat[0] = (short)(w0 & 0xFFFFu);
+    bmat[1] = (short)(w0 >> 16);
+    bmat[2] = (short)(w1 & 0xFFFFu);
+    bmat[3] = (short)(w1 >> 16);
+    const v4f c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(amat, bmat, (v4f){0, 0, 0, 0}, 0, 0, 0);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) x[4 * m + r] = c[r];
+  }
+  // element bits 2, 3, 4: (a, b) -> (a + b, a - b) with the partner h = 4, 8, 16 apart
+#pragma unroll
+  for (int h = 4; h <= 16; h <<= 1) {
+#pragma unroll
+    for (int e = 0; e < kElemsPerLane; ++e) {
+      if (e & h) continue;
+      const float p = x[e], q = x[e + h];
+      x[e] = p + q;
+      x[e + h] = p - q;
+    }
+  }
+}
+
+template <bool MF, int LPV>
+__device__ __forceinline__ float vector_min(float v) {
+  if constexpr (MF) {
+    v = fminf(v, __shfl_xor(v, 16));
+    return fminf(v, __shfl_xor(v, 32));
+  } else {
+    return vec_min<LPV>(v);
+  }
+}
+
+template <bool MF, int LPV>
+__device__ __forceinline__ float vector_max(float v) {
+  if constexpr (MF) {
+    v = fmaxf(v, __shfl_xor(v, 16));
+    return fmaxf(v, __shfl_xor(v, 32));
+  } else {
+    return vec_max<LPV>(v);
+  }
+}
+
+template <int D, bool F32IN, int WA, int NB, bool PAGED, bool MF = false>
 __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D>& w,
                                             const TileIn<F32IN>& in) {
+  static_assert(!MF || (D == 128 && !F32IN), "matrix-core front end: d = 128, bf16 input");
   const bool store = !PAGED || in.ok;
   constexpr int LPV = EncWave<D>::LPV;
   constexpr bool kFixed = WA != 0;
@@ -257,24 +329,28 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
     sm[4 * q] = v.x, sm[4 * q + 1] = v.y, sm[4 * q + 2] = v.z, sm[4 * q + 3] = v.w;
   }
   float x[kElemsPerLane];
-  if constexpr (F32IN) {
-#pragma unroll
-    for (int m = 0; m < 16; ++m) {
-      x[2 * m] = __uint_as_float(in.raw.w[2 * m] ^ (sm[m] << 16));
-      x[2 * m + 1] = __uint_as_float(in.raw.w[2 * m + 1] ^ (sm[m] & 0x80000000u));
-    }
+  if constexpr (MF) {
+    front_mfma(in.raw.w, sm, x);           // this lane holds z (no negated lanes)
   } else {
+    if constexpr (F32IN) {
 #pragma unroll
-    for (int m = 0; m < 16; ++m) {
-      const uint32_t wv = in.raw.w[m] ^ sm[m];
-      x[2 * m] = __uint_as_float(wv << 16);
-      x[2 * m + 1] = __uint_as_float(wv & 0xFFFF0000u);
+      for (int m = 0; m < 16; ++m) {
+        x[2 * m] = __uint_as_float(in.raw.w[2 * m] ^ (sm[m] << 16));
+        x[2 * m + 1] = __uint_as_float(in.raw.w[2 * m + 1] ^ (sm[m] & 0x80000000u));
+      }
+    } else {
+#pragma unroll
+      for (int m = 0; m < 16; ++m) {
+        const uint32_t wv = in.raw.w[m] ^ sm[m];
+        x[2 * m] = __uint_as_float(wv << 16);
+        x[2 * m + 1] = __uint_as_float(wv & 0xFFFF0000u);
+      }
     }
-  }
 
-  // ---- Walsh-Hadamard butterfly, stages h = 1 .. d/2 in ascending order ----
-  fwht_in_lane(x);
-  fwht_cross_lane_signed<LPV>(x, w.sub);   // this lane now holds sigma * z
+    // ---- Walsh-Hadamard butterfly, stages h = 1 .. d/2 in ascending order ----
+    fwht_in_lane(x);
+    fwht_cross_lane_signed<LPV>(x, w.sub);   // this lane now holds sigma * z
+  }
 
   // ---- squared pair norms and the vector's extremes ----
   float s2[kPairsPerLane];
@@ -286,8 +362,8 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
     lmin = fminf(lmin, s2[i]);
     lmax = fmaxf(lmax, s2[i]);
   }
-  const float smin = vec_min<LPV>(lmin);
-  const float smax = vec_max<LPV>(lmax);
+  const float smin = vector_min<MF, LPV>(lmin);
+  const float smax = vector_max<MF, LPV>(lmax);
   // the fast formulas need every pair's max(|a|,|b|) inside [2^-61, 2^60]
   const bool fast = __all(smin >= 0x1p-120f && smax <= 0x1p120f);
 
@@ -346,8 +422,8 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
         l0 = fminf(l0, rf[i]);
         l1 = fmaxf(l1, rf[i]);
       }
-      rmin = vec_min<LPV>(l0);
-      rmax = vec_max<LPV>(l1);
+      rmin = vector_min<MF, LPV>(l0);
+      rmax = vector_max<MF, LPV>(l1);
       if (mode == 1) {
         const float scale = (rmax == rmin) ? 0.0f : levels / (rmax - rmin);
 #pragma unroll
@@ -410,20 +486,37 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
 // addresses) and the loads past the end read lines already in cache.  Launches of one tile
 // per wave use the instantiation without the loop (a separate copy of the tile code inside
 // the same kernel would raise its register count).
-template <int D, bool MULTI, int WA, int NB, bool PAGED>
+template <int D, bool MULTI, int WA, int NB, bool PAGED, bool MF = false>
 __device__ void encode_tiles_fast(const EncodeArgs& a, const EncWave<D>& w, uint32_t tile0,
                                   uint32_t ntiles) {
   const uint32_t last = tile0 + ntiles - 1;
   TileIn<false> ia = load_tile<D, false, PAGED>(a, w, tile0);
   if constexpr (!MULTI) {
-    encode_tile<D, false, WA, NB, PAGED>(a, w, ia);
+    encode_tile<D, false, WA, NB, PAGED, MF>(a, w, ia);
     return;
   }
   for (uint32_t t = tile0; t <= last; t += 2) {
     const TileIn<false> ib = load_tile<D, false, PAGED>(a, w, min(t + 1, last));
-    encode_tile<D, false, WA, NB, PAGED>(a, w, ia);
+    encode_tile<D, false, WA, NB, PAGED, MF>(a, w, ia);
     ia = load_tile<D, false, PAGED>(a, w, min(t + 2, last));
-    encode_tile<D, false, WA, NB, PAGED>(a, w, ib);
+    encode_tile<D, false, WA, NB, PAGED, MF>(a, w, ib);
+  }
+}
+
+// The fast kernel with the matrix-core front end (d = 128, bf16, contiguous cache).
+template <bool MULTI>
+__global__ __launch_bounds__(kBlockThreads) void encode_mfma_kernel(EncodeArgs a) {
+  __shared__ __attribute__((aligned(16))) uint32_t s_sm[kWavesPerBlock][64];
+  EncWave<128> w;
+  uint32_t tile0, ntiles;
+  if (!enc_wave_setup<128, true>(a, w, s_sm, tile0, ntiles)) return;
+  const bool wide = w.sp.w == 8;
+  if (w.sp.mode == 1) {
+    if (wide) encode_tiles_fast<128, MULTI, 8, 8, false, true>(a, w, tile0, ntiles);
+    else encode_tiles_fast<128, MULTI, 6, 8, false, true>(a, w, tile0, ntiles);
+  } else {
+    if (wide) encode_tiles_fast<128, MULTI, 8, 4, false, true>(a, w, tile0, ntiles);
+    else encode_tiles_fast<128, MULTI, 6, 4, false, true>(a, w, tile0, ntiles);
   }
 }
 
@@ -457,6 +550,13 @@ template <int D, bool PAGED>
 void launch_encode(const EncodeArgs& a, int in_f32, bool fast, unsigned grid, hipStream_t s) {
   const dim3 block(kBlockThreads);
   const bool multi = a.tiles_per_wave > 1;
+  if constexpr (D == 128 && !PAGED) {
+    if (fast && a.mfma_front) {
+      if (multi) hipLaunchKernelGGL((encode_mfma_kernel<true>), dim3(grid), block, 0, s, a);
+      else hipLaunchKernelGGL((encode_mfma_kernel<false>), dim3(grid), block, 0, s, a);
+      return;
+    }
+  }
   if (fast && multi)
     hipLaunchKernelGGL((encode_fast_kernel<D, true, PAGED>), dim3(grid), block, 0, s, a);
   else if (fast)
@@ -475,6 +575,7 @@ int tvq_launch_encode(const tvq::EncodeArgs& a, int d, int in_f32, bool fast, un
   hipStream_t s = (hipStream_t)stream;
   if (fast && in_f32) return -1;      // the multi-tile kernel reads bf16 only
   const bool paged = a.pg.table != nullptr;
+  if (a.mfma_front && (d != 128 || paged)) return -1;
   if (d == 128) {
     if (paged) tvq::launch_encode<128, true>(a, in_f32, fast, grid, s);
     else tvq::launch_encode<128, false>(a, in_f32, fast, grid, s);

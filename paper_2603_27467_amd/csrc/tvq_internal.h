@@ -75,6 +75,7 @@ struct EncodeArgs {
   uint32_t num_segs;
   float inv_d;           // 1/d (exact)
   Paging pg;             // paged destination (the paged entry point only)
+  uint32_t mfma_front;   // fast formats through the matrix-core front end (tvq_encode_mfma)
 };
 
 struct DecodeArgs {
