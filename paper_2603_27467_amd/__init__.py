@@ -18,3 +18,4 @@ from ._capi import (  # noqa: F401
     tvq_abi_version, library_path, load_library,
 )
 from .codec import Codec, LayerCfg, desc_of  # noqa: F401
+from .presets import TABLE3, boosted_table, early_boost, table3_preset  # noqa: F401
