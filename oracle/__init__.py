@@ -39,7 +39,8 @@ class _Kind(ctypes.Structure):
 
 class _Codec(ctypes.Structure):
     _fields_ = [("L", ctypes.c_int), ("H", ctypes.c_int), ("d", ctypes.c_int),
-                ("kinds", ctypes.POINTER(_Kind)), ("signs", ctypes.POINTER(ctypes.c_int8))]
+                ("kinds", ctypes.POINTER(_Kind)), ("signs", ctypes.POINTER(ctypes.c_int8)),
+                ("packing", ctypes.c_int)]
 
 
 _lib = None
@@ -72,6 +73,10 @@ def lib():
         L.or_decode_vector_f32.argtypes = [ctypes.c_int, ctypes.POINTER(_Kind)] + [vp] * 6
         L.or_pack_bits.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp]
         L.or_unpack_bits.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp]
+        L.or_group_size.argtypes = [ctypes.c_int]
+        L.or_group_bits.argtypes = [ctypes.c_int, ctypes.c_int]
+        L.or_pack_groups.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp]
+        L.or_unpack_groups.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp]
         L.or_record_bytes.argtypes = [ctypes.POINTER(_Codec), ctypes.c_int, ctypes.c_int, vp]
         L.or_cache_layout.restype = ctypes.c_int64
         L.or_cache_layout.argtypes = [ctypes.POINTER(_Codec), ctypes.c_int64, ctypes.c_int64, vp]
@@ -262,19 +267,52 @@ def unpack_bits(buf, count: int, w: int) -> np.ndarray:
     return out
 
 
+def group_size(n: int) -> int:
+    """Codes per group of the group packing (0: n is a power of two, no grouping)."""
+    return int(lib().or_group_size(n))
+
+
+def group_bits(n: int, g: int) -> int:
+    return int(lib().or_group_bits(n, g))
+
+
+def pack_groups(codes, n: int) -> np.ndarray:
+    codes = np.ascontiguousarray(codes, np.uint32)
+    g = group_size(n)
+    out = np.zeros(((codes.size // g) * group_bits(n, g) + 7) // 8, np.uint8)
+    lib().or_pack_groups(_p(codes), codes.size, n, _p(out))
+    return out
+
+
+def unpack_groups(buf, count: int, n: int) -> np.ndarray:
+    buf = np.ascontiguousarray(buf, np.uint8)
+    out = np.zeros(count, np.uint32)
+    lib().or_unpack_groups(_p(buf), count, n, _p(out))
+    return out
+
+
 # ---------------------------------------------------------------- whole cache
 class Codec:
     """Oracle-side codec description: L layers, H heads, head dim d, per-(layer, kind)
     (n, norm mode, norm bits) and a [L][d] sign table."""
 
-    def __init__(self, L: int, H: int, d: int, kinds, sign_table: np.ndarray):
+    def __init__(self, L: int, H: int, d: int, kinds, sign_table: np.ndarray, packing: int = 0):
         self.L, self.H, self.d = L, H, d
+        self.packing = packing    # 1: group packing of non-power-of-two codebooks
         self.kinds = list(kinds)  # length 2L: [l*2 + 0] = K, [l*2 + 1] = V
         assert len(self.kinds) == 2 * L
         self._karr = (_Kind * (2 * L))(*[k.c() for k in self.kinds])
         self.signs = np.ascontiguousarray(sign_table, np.int8).reshape(L, d)
         self._c = _Codec(L, H, d, self._karr,
-                         self.signs.ctypes.data_as(ctypes.POINTER(ctypes.c_int8)))
+                         self.signs.ctypes.data_as(ctypes.POINTER(ctypes.c_int8)), packing)
+
+    def unpack_angles(self, layer: int, kind: int, rec) -> np.ndarray:
+        """The d/2 angle codes of one angle-plane record of (layer, kind)."""
+        n = self.kinds[2 * layer + kind].n
+        P = self.d // 2
+        if self.packing and group_size(n) > 0:
+            return unpack_groups(rec, P, n)
+        return unpack_bits(rec, P, angle_width(n))
 
     def record_bytes(self, layer: int, kind: int):
         rec = np.zeros(3, np.int64)

@@ -357,6 +357,61 @@ void or_unpack_bits(const uint8_t* in, int count, int w, uint32_t* codes) {
 }
 
 /* ------------------------------------------------------------------------------------ */
+/* Group packing of non-power-of-two codebooks: groups of g codes as base-n numbers.       */
+/* ------------------------------------------------------------------------------------ */
+int or_group_size(int n) {
+  if (n < 2 || (n & (n - 1)) == 0) return 0;
+  return n <= 255 ? 8 : 4;
+}
+
+int or_group_bits(int n, int g) {
+  uint64_t p = 1;                      /* n^g: below 2^64 for the group sizes above */
+  for (int i = 0; i < g; i++) p *= (uint64_t)n;
+  int W = 0;
+  while (W < 64 && (((uint64_t)1) << W) < p) W++;
+  return W;
+}
+
+void or_pack_groups(const uint32_t* codes, int count, int n, uint8_t* out) {
+  const int g = or_group_size(n);
+  const int W = or_group_bits(n, g);
+  const int groups = count / g;
+  memset(out, 0, ((size_t)groups * (size_t)W + 7) / 8);
+  for (int j = 0; j < groups; j++) {
+    uint64_t v = 0, place = 1;
+    for (int i = 0; i < g; i++) {
+      v += (uint64_t)codes[j * g + i] * place;
+      place *= (uint64_t)n;
+    }
+    for (int b = 0; b < W; b++) {
+      size_t bit = (size_t)j * (size_t)W + (size_t)b;
+      if ((v >> b) & 1u) out[bit / 8] |= (uint8_t)(1u << (bit % 8));
+    }
+  }
+}
+
+void or_unpack_groups(const uint8_t* in, int count, int n, uint32_t* codes) {
+  const int g = or_group_size(n);
+  const int W = or_group_bits(n, g);
+  const int groups = count / g;
+  for (int j = 0; j < groups; j++) {
+    uint64_t v = 0;
+    for (int b = 0; b < W; b++) {
+      size_t bit = (size_t)j * (size_t)W + (size_t)b;
+      v |= (uint64_t)((in[bit / 8] >> (bit % 8)) & 1u) << b;
+    }
+    for (int i = 0; i < g; i++) {
+      codes[j * g + i] = (uint32_t)(v % (uint64_t)n);
+      v /= (uint64_t)n;
+    }
+  }
+}
+
+static int grouped(const or_codec* c, const or_kind* kd) {
+  return c->packing && or_group_size(kd->n) > 0;
+}
+
+/* ------------------------------------------------------------------------------------ */
 /* Cache layout: for each (layer, kind) three planes -- angle codes, norm data, header -- */
 /* each indexed [B][H][T_cap] by record.  Planes follow each other in (layer, kind,      */
 /* plane) order with no padding between them.                                           */
@@ -364,7 +419,12 @@ void or_unpack_bits(const uint8_t* in, int count, int w, uint32_t* codes) {
 void or_record_bytes(const or_codec* c, int layer, int kind, int64_t rec[3]) {
   const or_kind* kd = &c->kinds[2 * layer + kind];
   int64_t P = c->d / 2;
-  rec[0] = (P * or_angle_width(kd->n) + 7) / 8;
+  if (grouped(c, kd)) {
+    const int g = or_group_size(kd->n);
+    rec[0] = ((P / g) * or_group_bits(kd->n, g) + 7) / 8;
+  } else {
+    rec[0] = (P * or_angle_width(kd->n) + 7) / 8;
+  }
   if (kd->norm_mode == OR_NORM_F32) {
     rec[1] = 4 * P;
     rec[2] = 0;
@@ -443,7 +503,8 @@ int or_encode_cache(const or_codec* c, int in_bf16, const void* k_in, const void
             if (rc) break;
             uint8_t* ang = cache + off[(l * 2 + kind) * 3 + 0] + slot * rec[0];
             uint8_t* nrm = cache + off[(l * 2 + kind) * 3 + 1] + slot * rec[1];
-            or_pack_bits(kc, P, w, ang);
+            if (grouped(c, kd)) or_pack_groups(kc, P, kd->n, ang);
+            else or_pack_bits(kc, P, w, ang);
             if (kd->norm_mode == OR_NORM_F32) {
               memcpy(nrm, rn, sizeof(float) * (size_t)P);
             } else {
@@ -470,8 +531,11 @@ int or_read_vector(const or_codec* c, const uint8_t* cache, int64_t B, int64_t T
   int64_t rec[3];
   or_record_bytes(c, layer, kind, rec);
   int64_t slot = (b * c->H + h) * T_cap + t;
-  or_unpack_bits(cache + off[(layer * 2 + kind) * 3 + 0] + slot * rec[0], P,
-                 or_angle_width(kd->n), k);
+  if (grouped(c, kd))
+    or_unpack_groups(cache + off[(layer * 2 + kind) * 3 + 0] + slot * rec[0], P, kd->n, k);
+  else
+    or_unpack_bits(cache + off[(layer * 2 + kind) * 3 + 0] + slot * rec[0], P,
+                   or_angle_width(kd->n), k);
   const uint8_t* nrm = cache + off[(layer * 2 + kind) * 3 + 1] + slot * rec[1];
   if (kd->norm_mode == OR_NORM_F32) {
     if (rn) memcpy(rn, nrm, sizeof(float) * (size_t)P);

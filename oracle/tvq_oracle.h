@@ -138,15 +138,29 @@ void or_decode_vector_f32(int d, const or_kind* kind, const int8_t* signs,
 void or_pack_bits(const uint32_t* codes, int count, int w, uint8_t* out);
 void or_unpack_bits(const uint8_t* in, int count, int w, uint32_t* codes);
 
+/* Group packing of the angle codes of a non-power-of-two n (the paper counts log2(n)/2 bits
+ * per element, section 3.1 "Rate accounting"; storing ceil(log2 n) bits per code spends more).
+ * Codes go in groups of g consecutive codes (g = 8 for n <= 255, 4 above), each group the
+ * base-n number V = sum_i c_(g*j+i) n^i stored in W = ceil(log2(n^g)) bits (the smallest W with
+ * n^g <= 2^W) at bits [j*W, (j+1)*W) of the LSB-first bitstream.  g = 0 (no grouping) for a
+ * power-of-two n.  Parity unpinned (the format is this project's): checked against a
+ * hand-packed example, by round trip and against the exact bit count. */
+int or_group_size(int n);
+int or_group_bits(int n, int g);
+void or_pack_groups(const uint32_t* codes, int count, int n, uint8_t* out);
+void or_unpack_groups(const uint8_t* in, int count, int n, uint32_t* codes);
+
 /* ---- the whole cache ---- */
 typedef struct {
   int L, H, d;
   const or_kind* kinds;   /* [L][2]: index 2*l + 0 = K, 2*l + 1 = V */
   const int8_t* signs;    /* [L][d] of +-1 */
+  int packing;            /* 0: ceil(log2 n) bits per angle code; 1: group packing */
 } or_codec;
 
 /* Record sizes (bytes per vector) of the three planes of (layer, kind):
- * plane 0 angle codes P*w/8, plane 1 norm data P*b/8 (4P for F32), plane 2 header 8 (0 for F32). */
+ * plane 0 angle codes P*w/8 (group packing: (P/g)*W/8), plane 1 norm data P*b/8 (4P for F32),
+ * plane 2 header 8 (0 for F32); each rounded up to whole bytes. */
 void or_record_bytes(const or_codec* c, int layer, int kind, int64_t rec[3]);
 /* Byte offset of every plane: planes follow each other in (layer, kind, plane) order with no
  * padding; plane size = B * H * T_cap * record.  Returns the total size.  Parity unpinned

@@ -125,10 +125,9 @@ def compare_encode(s: Setup, gcache: np.ndarray, ocache: np.ndarray, u, t, B, T,
             rep.records_checked += len(slots)
             fl = oracle.angle_flags(uu, kd.n)
             rep.angle_flagged += int(fl.sum())
-            w = oracle.angle_width(kd.n)
             for r in np.nonzero((g != o).any(axis=1))[0]:
-                kg = oracle.unpack_bits(g[r], P, w)
-                ko = oracle.unpack_bits(o[r], P, w)
+                kg = s.orc.unpack_angles(l, kind, g[r])
+                ko = s.orc.unpack_angles(l, kind, o[r])
                 bad = kg != ko
                 rep.angle_mismatch += int(bad.sum())
                 ub = bad & ~fl[r]

@@ -621,3 +621,70 @@ def test_attention_in_the_rotated_domain(orc):
             a = sum(p[t] * ydash(1, b, h, t) for t in range(T)) / p.sum()
             o = sgn[layer] * orc.fwht_f64(a)                              # D W a
             assert np.allclose(o, out[b, h], rtol=1e-12, atol=1e-12)
+
+
+# ---------------------------------------------------------------- group packing
+def test_group_packing_hand_example(orc):
+    """n = 3: groups of 8 codes in W = 13 bits (3^8 = 6561 lies in (2^12, 2^13]).  Codes
+    1,2,0,1,2,0,1,2 give 1 + 2*3 + 1*27 + 2*81 + 1*729 + 2*2187 = 5299; eight 2s give
+    3^8 - 1 = 6560.  The stream 5299 + 6560 * 2^13 = 53744819 = 0x033414B3, least significant
+    byte first."""
+    codes = [1, 2, 0, 1, 2, 0, 1, 2] + [2] * 8
+    assert orc.group_size(3) == 8 and orc.group_bits(3, 8) == 13
+    out = orc.pack_groups(codes, 3)
+    assert list(out) == [0xB3, 0x14, 0x34, 0x03]
+    assert list(orc.unpack_groups(out, 16, 3)) == codes
+
+
+@pytest.mark.parametrize("n,g,W", [(3, 8, 13), (48, 8, 45), (56, 8, 47), (100, 8, 54),
+                                   (255, 8, 64), (300, 4, 33), (4095, 4, 48), (64, 0, 0),
+                                   (256, 0, 0)])
+def test_group_sizes(orc, n, g, W):
+    """Group sizes and widths: 48^8 = 2.82e13 in (2^44, 2^45]; 56^8 = 9.67e13 in (2^46, 2^47];
+    100^8 = 1e16 in (2^53, 2^54]; 255^8 = 1.78e19 in (2^63, 2^64); 300^4 = 8.1e9 in
+    (2^32, 2^33]; 4095^4 = 2.81e14 in (2^47, 2^48); powers of two are not grouped."""
+    assert orc.group_size(n) == g
+    if g:
+        assert orc.group_bits(n, g) == W
+
+
+@pytest.mark.parametrize("n", [3, 5, 12, 48, 56, 100, 200, 255, 300, 1000, 4095])
+def test_group_packing_round_trip_and_rate(orc, n):
+    """unpack(pack(c)) = c for random codes; the packed size is at most one bit per group
+    above the information content P log2 n, and never above the fixed-width size."""
+    rng = np.random.default_rng(n)
+    for P in (32, 64):
+        codes = rng.integers(0, n, P, dtype=np.uint32)
+        codes[:3] = [0, n - 1, n - 1]
+        buf = orc.pack_groups(codes, n)
+        assert np.array_equal(orc.unpack_groups(buf, P, n), codes)
+        g = orc.group_size(n)
+        assert buf.size <= int(np.ceil((P * np.log2(n) + P // g) / 8))
+        assert buf.size <= (P * orc.angle_width(n) + 7) // 8
+
+
+def test_group_packed_cache_decodes_the_same(orc):
+    """The same vectors encoded with and without group packing decode to the same values (the
+    packing changes bytes, not codes); record sizes: n = 48 takes 45 bytes at d = 128 against
+    48 at 6 bits per code, and 23 bytes at d = 64."""
+    rng = np.random.default_rng(5)
+    d, T = 128, 9
+    kinds = [orc.Kind(48, orc.NORM_LINEAR, 8), orc.Kind(100, orc.NORM_LOG, 4)]
+    sg = np.where(rng.random((1, d)) < 0.5, -1, 1).astype(np.int8)
+    x = rng.standard_normal((1, 1, 2, T, d)).astype(np.float32)
+    caches = []
+    for packing in (0, 1):
+        c = orc.Codec(1, 2, d, kinds, sg, packing=packing)
+        total, _ = c.layout(1, T)
+        buf = np.zeros(total, np.uint8)
+        c.encode_cache(x, -x, 0, T, buf)
+        caches.append((c, buf))
+    (c0, b0), (c1, b1) = caches
+    assert c0.record_bytes(0, 0)[0] == 48 and c1.record_bytes(0, 0)[0] == 45
+    assert c1.record_bytes(0, 1)[0] == 54                    # n = 100: W = 54 per 8 codes
+    assert b1.size < b0.size
+    for prec in ("f64", "f32"):
+        assert np.array_equal(c0.decode_cache(b0, 1, T, 0, T, prec),
+                              c1.decode_cache(b1, 1, T, 0, T, prec))
+    c64 = orc.Codec(1, 2, 64, kinds, sg[:, :64], packing=1)
+    assert c64.record_bytes(0, 0)[0] == 23
