@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define TVQ_ABI_VERSION 1
+#define TVQ_ABI_VERSION 2
 #define TVQ_MAX_LAYERS 256
 
 typedef enum {
@@ -71,13 +71,20 @@ typedef struct {
  *               NULL: drawn from `seed` with SplitMix64 (Steele, Lea and Flood 2014) as
  *               tvq_make_signs describes.  The paper samples D once from a seeded PRNG and
  *               shares it across layers (section 3.1 "Implementation"); shared_signs = 1 gives
- *               that, shared_signs = 0 draws an independent D per layer.               */
+ *               that, shared_signs = 0 draws an independent D per layer.
+ *   angle_packing  0: every angle code in ceil(log2 n) bits; 1: group packing for a
+ *               non-power-of-two n (the paper counts log2(n)/2 bits per element, section 3.1
+ *               "Rate accounting"): groups of g = 8 codes (g = 4 for n > 255) stored as the
+ *               base-n number sum_i c_(g*j+i) n^i in W = ceil(log2(n^g)) bits, group j at bits
+ *               [j*W, (j+1)*W) of the record.  n = 48 takes 45 bytes per d = 128 vector
+ *               instead of 48.  Powers of two are stored the same way under both settings. */
 typedef struct {
   int32_t num_layers, num_heads, head_dim;
   int32_t shared_signs;
   uint64_t seed;
   const tvq_layer_cfg* layers;
   const int8_t* signs;
+  int32_t angle_packing;
 } tvq_config;
 
 /* A strided [L][B][H][T][d] view of K and V (the same strides for both), in elements, with
@@ -91,7 +98,8 @@ typedef struct {
 
 /* Compressed cache layout (this project's; the paper only counts bits, section 3.1 "Rate
  * accounting" and eq. (3)).  For each layer l and kind (0 = K, 1 = V) there are three planes:
- *   plane 0  angle codes   P*ceil(log2 n)/8 bytes per vector (P = d/2 pairs)
+ *   plane 0  angle codes   P*ceil(log2 n)/8 bytes per vector (P = d/2 pairs), or with group
+ *                          packing (P/g)*W/8, rounded up to whole bytes
  *   plane 1  norm data     P*b/8 bytes (LINEAR/LOG codes) or 4P bytes (fp32 norms)
  *   plane 2  header        8 bytes (fp32 r_min, r_max), absent (0 bytes) for fp32 norms
  * Each plane holds B*H*capacity records indexed ((b*H + h)*capacity + t).  Planes follow each

@@ -6,7 +6,7 @@ import os
 
 import numpy as np
 
-TVQ_ABI_VERSION = 1
+TVQ_ABI_VERSION = 2
 TVQ_MAX_LAYERS = 256
 TVQ_OK, TVQ_ERR_INVALID_ARG, TVQ_ERR_UNSUPPORTED, TVQ_ERR_HIP, TVQ_ERR_ALLOC = 0, -1, -2, -3, -4
 TVQ_BF16, TVQ_F32 = 0, 1
@@ -35,7 +35,7 @@ class tvq_config(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("num_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("shared_signs", ctypes.c_int32),
                 ("seed", ctypes.c_uint64), ("layers", ctypes.POINTER(tvq_layer_cfg)),
-                ("signs", ctypes.POINTER(ctypes.c_int8))]
+                ("signs", ctypes.POINTER(ctypes.c_int8)), ("angle_packing", ctypes.c_int32)]
 
 
 class tvq_tensor_desc(ctypes.Structure):

@@ -39,7 +39,8 @@ def desc_of(t, layers: Optional[int] = None) -> C.tvq_tensor_desc:
 class Codec:
     def __init__(self, num_layers: int, num_heads: int, head_dim: int,
                  layers: Sequence, seed: int = 0, shared_signs: bool = False,
-                 signs: Optional[np.ndarray] = None):
+                 signs: Optional[np.ndarray] = None, angle_packing: int = 0):
+        """angle_packing = 1: group packing of non-power-of-two codebooks (tvq_config)."""
         self.L, self.H, self.d = num_layers, num_heads, head_dim
         self.layers = list(layers)
         arr = (C.tvq_layer_cfg * num_layers)()
@@ -53,7 +54,7 @@ class Codec:
             self._signs = np.ascontiguousarray(signs, np.int8)
             sp = self._signs.ctypes.data_as(ctypes.POINTER(ctypes.c_int8))
         self.cfg = C.tvq_config(num_layers, num_heads, head_dim, 1 if shared_signs else 0,
-                                seed & (2**64 - 1), arr, sp)
+                                seed & (2**64 - 1), arr, sp, angle_packing)
         self.handle = C.tvq_create(self.cfg)
 
     def close(self):

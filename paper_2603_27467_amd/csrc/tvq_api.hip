@@ -16,6 +16,7 @@
 
 struct tvq_codec {
   int32_t L = 0, H = 0, d = 0;
+  int32_t packing = 0;                       // tvq_config::angle_packing
   std::vector<tvq_layer_cfg> layers;
   std::vector<int8_t> signs;                 // [L][d]
   std::vector<tvq::SegParams> segs;          // [2L]
@@ -62,6 +63,7 @@ tvq_status validate_config(const tvq_config* cfg) {
     if (!kind_valid(c.n_k, c.norm_bits_k, c.norm_mode_k)) return TVQ_ERR_INVALID_ARG;
     if (!kind_valid(c.n_v, c.norm_bits_v, c.norm_mode_v)) return TVQ_ERR_INVALID_ARG;
   }
+  if (cfg->angle_packing != 0 && cfg->angle_packing != 1) return TVQ_ERR_INVALID_ARG;
   if (cfg->signs) {
     const int rows = cfg->shared_signs ? 1 : cfg->num_layers;
     for (int i = 0; i < rows * d; ++i)
@@ -70,10 +72,28 @@ tvq_status validate_config(const tvq_config* cfg) {
   return TVQ_OK;
 }
 
+// Group packing of a non-power-of-two n: codes per group (8 while n^8 < 2^64, else 4; 0 for
+// a power of two or packing off) and the bits of a group, the bit length of n^g - 1.
+uint32_t group_codes(uint32_t n, int packing) {
+  if (!packing || (n & (n - 1)) == 0) return 0;
+  return n <= 255 ? 8u : 4u;
+}
+
+uint32_t group_width(uint32_t n, uint32_t g) {
+  uint64_t top = 1;
+  for (uint32_t i = 0; i < g; ++i) top *= n;
+  top -= 1;                                   // largest group value
+  uint32_t w = 0;
+  while (w < 64 && (top >> w) != 0) ++w;
+  return w;
+}
+
 // record bytes (angle, norm, header) of one kind
-void kind_records(int d, uint32_t n, uint32_t bits, uint32_t mode, uint32_t rec[3]) {
+void kind_records(int d, uint32_t n, uint32_t bits, uint32_t mode, int packing,
+                  uint32_t rec[3]) {
   const uint32_t P = (uint32_t)d / 2;
-  rec[0] = (P * (uint32_t)width_of(n) + 7) / 8;
+  const uint32_t g = group_codes(n, packing);
+  rec[0] = g ? ((P / g) * group_width(n, g) + 7) / 8 : (P * (uint32_t)width_of(n) + 7) / 8;
   if (mode == TVQ_NORM_F32) {
     rec[1] = 4 * P;
     rec[2] = 0;
@@ -93,8 +113,10 @@ void fill_layout(const tvq_config* cfg, int64_t batch, int64_t cap, tvq_layout* 
     const tvq_layer_cfg& c = cfg->layers[l];
     for (int kind = 0; kind < 2; ++kind) {
       uint32_t rec[3];
-      if (kind == 0) kind_records(cfg->head_dim, c.n_k, c.norm_bits_k, c.norm_mode_k, rec);
-      else kind_records(cfg->head_dim, c.n_v, c.norm_bits_v, c.norm_mode_v, rec);
+      if (kind == 0)
+        kind_records(cfg->head_dim, c.n_k, c.norm_bits_k, c.norm_mode_k, cfg->angle_packing, rec);
+      else
+        kind_records(cfg->head_dim, c.n_v, c.norm_bits_v, c.norm_mode_v, cfg->angle_packing, rec);
       for (int p = 0; p < 3; ++p) {
         out->off[l][kind][p] = pos;
         out->rec_bytes[l][kind][p] = (int32_t)rec[p];
@@ -268,6 +290,7 @@ tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out) {
   c->L = cfg->num_layers;
   c->H = cfg->num_heads;
   c->d = cfg->head_dim;
+  c->packing = cfg->angle_packing;
   c->layers.assign(cfg->layers, cfg->layers + c->L);
   const int d = c->d;
 
@@ -310,7 +333,10 @@ tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out) {
       s.w = (uint32_t)width_of(n);
       s.mode = mode;
       s.bits = bits;
-      kind_records(d, n, bits, mode, s.rec);
+      kind_records(d, n, bits, mode, c->packing, s.rec);
+      s.grp = group_codes(n, c->packing);
+      s.gw = s.grp ? group_width(n, s.grp) : 0u;
+      s.ndiv = make_div(n);
       s.layer = (uint32_t)l;
       s.kind = (uint32_t)kind;
       s.lut_off = (uint32_t)(lut.size() / 2);
@@ -380,6 +406,7 @@ tvq_status tvq_cache_layout(const tvq_codec* c, int64_t batch, int64_t capacity_
   cfg.num_heads = c->H;
   cfg.head_dim = c->d;
   cfg.layers = c->layers.data();
+  cfg.angle_packing = c->packing;
   fill_layout(&cfg, batch, capacity_tokens, out);
   return TVQ_OK;
 }
@@ -752,7 +779,7 @@ double tvq_bits_per_element_config(const tvq_config* cfg, int accounting) {
         else b += (double)bits / 2.0 + 64.0 / (double)d;            // eq. (3)
       } else {
         uint32_t rec[3];
-        kind_records(d, n, bits, mode, rec);
+        kind_records(d, n, bits, mode, cfg->angle_packing, rec);
         b = 8.0 * (double)(rec[0] + rec[1] + rec[2]) / (double)d;
       }
       total += b;
@@ -768,6 +795,7 @@ double tvq_bits_per_element(const tvq_codec* c, int accounting) {
   cfg.num_heads = c->H;
   cfg.head_dim = c->d;
   cfg.layers = c->layers.data();
+  cfg.angle_packing = c->packing;
   return tvq_bits_per_element_config(&cfg, accounting);
 }
 

@@ -336,7 +336,10 @@ __global__ __launch_bounds__(kBlockThreads) void decode_generic_kernel(DecodeArg
   if (!wave_setup<D>(a, w, s_lut, kLutGeneric, tile0, ntiles)) return;
   const TilePos pos = tile_pos<PAGED>(a, tile0 * VPW, w.vslot);
   uint32_t kc[kPairsPerLane];
-  load_codes_any(w.plane[0] + (uint64_t)pos.slot * w.sp.rec[0], w.sub, w.sp.w, kc);
+  const uint8_t* rec_ang = w.plane[0] + (uint64_t)pos.slot * w.sp.rec[0];
+  if (w.sp.grp == 8) unpack_groups_lane<8>(rec_ang, w.sub, w.sp, kc);
+  else if (w.sp.grp == 4) unpack_groups_lane<4>(rec_ang, w.sub, w.sp, kc);
+  else load_codes_any(rec_ang, w.sub, w.sp.w, kc);
   if (!w.sp.mask) {
     const uint32_t kclamp = w.sp.n - 1u;   // codes of a corrupted cache stay inside the table
 #pragma unroll

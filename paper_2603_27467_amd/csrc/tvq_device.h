@@ -46,6 +46,72 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t x, const FastDiv& d) {
   return (uint32_t)(((uint64_t)x * d.m) >> d.s);
 }
 
+// Group packing of a non-power-of-two codebook (grp codes per group, each group the base-n
+// number sum_i c_i n^i in gw bits; see SegParams).  The record spans (P/grp)*gw bits and
+// lane `sub` owns groups sub*16/grp .. sub*16/grp + 16/grp - 1, i.e. its own 16 codes.
+
+// v / n and v % n for v < 2^64 by long division in 16-bit steps: every partial dividend is
+// below n * 2^16 <= 2^28, inside fast_div's range.
+__device__ __forceinline__ uint64_t divmod_n(uint64_t v, const FastDiv& nd, uint32_t& rem) {
+  uint32_t r = 0;
+  uint64_t q = 0;
+#pragma unroll
+  for (int c = 3; c >= 0; --c) {
+    const uint32_t t = (r << 16) | (uint32_t)((v >> (16 * c)) & 0xFFFFu);
+    const uint32_t qc = fast_div(t, nd);
+    r = t - qc * nd.div;
+    q |= (uint64_t)qc << (16 * c);
+  }
+  rem = r;
+  return q;
+}
+
+// 64 bits of the window win[0..8] (bit 0 = bit 0 of win[0]) starting at bit `pos` < 224,
+// selected without indexing the array by a run-time value.
+__device__ __forceinline__ uint64_t window_bits(const uint32_t (&win)[9], uint32_t pos) {
+  const uint32_t wi = pos >> 5, sh = pos & 31u;
+  uint32_t a = 0, b = 0, c = 0;
+#pragma unroll
+  for (uint32_t k = 0; k < 7; ++k) {
+    if (k == wi) {
+      a = win[k];
+      b = win[k + 1];
+      c = win[k + 2];
+    }
+  }
+  const uint64_t lo = ((uint64_t)b << 32) | a;
+  return sh ? (lo >> sh) | ((uint64_t)c << (64 - sh)) : lo;
+}
+
+// This lane's 16 codes of a group-packed record.
+template <int G>
+__device__ __forceinline__ void unpack_groups_lane(const uint8_t* rec, int sub,
+                                                   const SegParams& sp,
+                                                   uint32_t (&kc)[kPairsPerLane]) {
+  constexpr int NG = kPairsPerLane / G;
+  const uint32_t W = sp.gw;
+  const uint32_t L = NG * W;                         // bits of this lane (<= 192)
+  const uint32_t first = ((uint32_t)sub * L) >> 3, lead = ((uint32_t)sub * L) & 7u;
+  const uint32_t nbytes = (lead + L + 7) >> 3;        // <= 25
+  uint32_t win[9];
+#pragma unroll
+  for (int k = 0; k < 9; ++k) win[k] = 0u;
+#pragma unroll
+  for (uint32_t b = 0; b < 28; ++b)
+    if (b < nbytes) win[b >> 2] |= (uint32_t)rec[first + b] << (8 * (b & 3));
+  const uint64_t mask = W >= 64 ? ~0ull : ((1ull << W) - 1);
+#pragma unroll
+  for (int j = 0; j < NG; ++j) {
+    uint64_t v = window_bits(win, lead + j * W) & mask;
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      uint32_t r;
+      v = divmod_n(v, sp.ndiv, r);
+      kc[j * G + i] = r;
+    }
+  }
+}
+
 // DPP quad permutations: 0xB1 = [1,0,3,2] (lane ^ 1), 0x4E = [2,3,0,1] (lane ^ 2).  The old
 // value is left undefined (bound_ctrl on, every quad lane is in range), which lets the
 // compiler fold the permutation into the consuming v_add/v_min/v_max as a DPP operand.

@@ -160,6 +160,7 @@ struct EncWave {
   int64_t layer_off;          // element offset of the layer and of the lane's 32 elements
   uint8_t* plane[3];
   const uint32_t* sm;         // the lane's 16 sign-mask words, in this wave's LDS
+  uint32_t* grp_lds;          // the wave's record buffer for group packing (generic kernel)
   bool negated;               // the lane holds -z after the butterfly
   float shift;                // rounding shift with the half-turn of a negated lane removed
   uint32_t unneg;             // sign flip that undoes the negation (odd n)
@@ -195,6 +196,7 @@ __device__ __forceinline__ bool enc_wave_setup(const EncodeArgs& a, EncWave<D>& 
   if (lane < D / 2) row[lane] = a.sign_masks[(size_t)w.sp.layer * (D / 2) + lane];
   wave_lds_sync();
   w.sm = row + w.sub * 16;
+  w.grp_lds = nullptr;
   w.negated = MF ? false : lane_negated<LPV>(w.sub);
   const bool odd_n = (w.sp.n & 1u) != 0;
   w.shift = (w.negated && !odd_n) ? kRoundShift - 0.5f * w.sp.nf : kRoundShift;
@@ -240,6 +242,43 @@ __device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const En
 // Encode one tile.  WA = angle code width and NB = norm code width of a format fixed at
 // compile time (NB = 8: linear norms, NB = 4: log-space norms; the angle codebook is then
 // n = 2^WA), or WA = NB = 0 for the segment's run-time format.
+// Record words per vector slot of the group-packing buffer: a group-packed record holds at
+// most 96 bytes at d = 128 (16 groups of 48 bits) and 48 at d = 64.
+template <int D>
+constexpr int kGrpRecordWords = 3 * D / 16;
+
+// Group packing of this lane's 16 angle codes (G codes per group, each group the base-n
+// number sum_i c_i n^i in sp.gw bits at bit (group index) * gw of the record): the vector's
+// lanes OR their groups into the record in LDS, then store its bytes (records of a
+// non-power-of-two n need not be word-aligned, so the stores are byte stores).
+template <int D, int G>
+__device__ __forceinline__ void store_angle_groups(const EncWave<D>& w, const SegParams& sp,
+                                                   uint8_t* rec, const uint32_t (&kc)[kPairsPerLane],
+                                                   bool store) {
+  constexpr int LPV = EncWave<D>::LPV;
+  constexpr int RW = kGrpRecordWords<D>;
+  constexpr int NG = kPairsPerLane / G;
+  uint32_t* r = w.grp_lds + w.vslot * RW;
+  for (int i = w.sub; i < RW; i += LPV) r[i] = 0u;
+  wave_lds_sync();
+  const uint32_t W = sp.gw;
+#pragma unroll
+  for (int j = 0; j < NG; ++j) {
+    uint64_t v = 0;
+#pragma unroll
+    for (int i = G - 1; i >= 0; --i) v = v * sp.n + kc[j * G + i];     // digit 0 lowest
+    const uint32_t pos = ((uint32_t)w.sub * NG + j) * W;
+    const uint32_t word = pos >> 5, sh = pos & 31u;
+    atomicOr(&r[word], (uint32_t)(v << sh));
+    if (sh + W > 32) atomicOr(&r[word + 1], (uint32_t)(sh ? v >> (32 - sh) : v >> 32));
+    if (sh + W > 64) atomicOr(&r[word + 2], (uint32_t)(v >> (64 - sh)));
+  }
+  wave_lds_sync();
+  if (store)
+    for (uint32_t b = (uint32_t)w.sub; b < sp.rec[0]; b += LPV)
+      rec[b] = (uint8_t)(r[b >> 2] >> (8 * (b & 3u)));
+}
+
 // Matrix-core front end (d = 128, bf16): the lane holds elements 32 s .. 32 s + 31 of vector
 // slot v (s = lane / 16, v = lane % 16).  For each m = 0..7, v_mfma_f32_16x16x16_bf16 with
 // A[i][k] = (-1)^popcount(i & k) and B[k][v] = element 32 (k >> 2) + 4 m + (k & 3) of vector v
@@ -474,6 +513,16 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
                                  __uint_as_float(__float_as_uint(x[2 * i + 1]) ^ flip), nf, n);
   }
   uint8_t* rec_ang = w.plane[0] + (uint64_t)in.slot * sp.rec[0];
+  if constexpr (!kFixed) {
+    if (sp.grp == 8) {
+      store_angle_groups<D, 8>(w, sp, rec_ang, kc, store);
+      return;
+    }
+    if (sp.grp == 4) {
+      store_angle_groups<D, 4>(w, sp, rec_ang, kc, store);
+      return;
+    }
+  }
   if (store) {
     if constexpr (kFixed) store_codes<WA>(rec_ang, w.sub, kc);
     else store_codes_any(rec_ang, w.sub, sp.w, kc);
@@ -540,9 +589,11 @@ __global__ __launch_bounds__(kBlockThreads) void encode_fast_kernel(EncodeArgs a
 template <int D, bool F32IN, bool PAGED>
 __global__ __launch_bounds__(kBlockThreads) void encode_generic_kernel(EncodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t s_sm[kWavesPerBlock][D / 2];
+  __shared__ uint32_t s_grp[kWavesPerBlock][EncWave<D>::VPW * kGrpRecordWords<D>];
   EncWave<D> w;
   uint32_t tile0, ntiles;
   if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles)) return;
+  w.grp_lds = s_grp[threadIdx.x / kWave];
   encode_tile<D, F32IN, 0, 0, PAGED>(a, w, load_tile<D, F32IN, PAGED>(a, w, tile0));
 }
 

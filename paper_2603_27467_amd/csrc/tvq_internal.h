@@ -21,6 +21,16 @@ constexpr int kWavesPerBlock = kBlockThreads / kWave;
 // Per-(layer, kind) parameters.  Plane p of a segment starts at n_slots * pre[p] bytes,
 // where n_slots = B * H * capacity: the layout puts planes back to back, so the prefix of
 // record bytes over all earlier planes scales to the byte offset for any (B, capacity).
+// Unsigned division by a runtime constant for numerators x below 2^31:
+// q = (x * m) >> s with s = 31 + ceil(log2 div) and m = ceil(2^s / div) < 2^32.  With
+// e = m * div - 2^s < div <= 2^(s-31), x * e < 2^s, so the product never reaches the next
+// multiple of 2^s and q = floor(x / div).
+struct FastDiv {
+  uint32_t m;
+  uint32_t s;
+  uint32_t div;
+};
+
 struct SegParams {
   float nf;            // n as float
   uint32_t n;          // angle bins
@@ -33,17 +43,12 @@ struct SegParams {
   uint32_t kind;
   uint32_t lut_off;    // first entry of this codebook in the trig LUT
   uint64_t pre[3];     // record-byte prefix of the three planes
+  uint32_t grp;        // group packing: codes per group (8 or 4), 0 = fixed width
+  uint32_t gw;         // group packing: bits per group
+  FastDiv ndiv;        // division by n (group unpacking)
 };
 
-// Unsigned division by a runtime constant for numerators x below 2^31:
-// q = (x * m) >> s with s = 31 + ceil(log2 div) and m = ceil(2^s / div) < 2^32.  With
-// e = m * div - 2^s < div <= 2^(s-31), x * e < 2^s, so the product never reaches the next
-// multiple of 2^s and q = floor(x / div).
-struct FastDiv {
-  uint32_t m;
-  uint32_t s;
-  uint32_t div;
-};
+
 
 // Paged cache: the pool has the layout of a cache of `n_blocks` sequences of 2^block_log2
 // tokens, and token t of sequence b lives in pool block table[b * max_blocks + (t >> block_log2)],

@@ -52,6 +52,7 @@ class Setup:
     seed_mode: bool = False
     seed: int = 0
     shared: bool = False
+    packing: int = 0         # 1: group packing of non-power-of-two codebooks
     gpu: object = None
     orc: object = None
 
@@ -65,13 +66,14 @@ class Setup:
             kinds.append(oracle.Kind(t.n_v, t.norm_mode_v, t.norm_bits_v))
         if self.seed_mode:
             self.gpu = tvq.Codec(self.L, self.H, self.d, layers, seed=self.seed,
-                                 shared_signs=self.shared)
+                                 shared_signs=self.shared, angle_packing=self.packing)
             rows = [oracle.signs(self.seed, 0 if self.shared else l, self.d)
                     for l in range(self.L)]
             self.signs = np.stack(rows)
         else:
-            self.gpu = tvq.Codec(self.L, self.H, self.d, layers, signs=self.signs)
-        self.orc = oracle.Codec(self.L, self.H, self.d, kinds, self.signs)
+            self.gpu = tvq.Codec(self.L, self.H, self.d, layers, signs=self.signs,
+                                 angle_packing=self.packing)
+        self.orc = oracle.Codec(self.L, self.H, self.d, kinds, self.signs, packing=self.packing)
         return self
 
 

@@ -30,7 +30,8 @@ def test_library_exports_every_declared_symbol(tvq):
     lib = ctypes.CDLL(tvq.library_path())
     missing = [s for s in syms if not hasattr(lib, s)]
     assert not missing, missing
-    assert tvq.tvq_abi_version() == 1
+    header = open(os.path.join(ROOT, "include", "tvq.h")).read()
+    assert tvq.tvq_abi_version() == int(re.search(r"#define TVQ_ABI_VERSION (\d+)", header).group(1))
 
 
 def test_status_strings(tvq):
@@ -66,7 +67,7 @@ def test_decode_table_agrees_with_oracle(tvq, orc):
             assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32)), (n, d)
 
 
-def _cfg(tvq, table, L, H, d, seed=0, shared=0, signs=None):
+def _cfg(tvq, table, L, H, d, seed=0, shared=0, signs=None, packing=0):
     arr = (tvq.tvq_layer_cfg * max(len(table), 1))()
     for i, t in enumerate(table):
         arr[i] = tvq.tvq_layer_cfg(*t)
@@ -74,7 +75,7 @@ def _cfg(tvq, table, L, H, d, seed=0, shared=0, signs=None):
     if signs is not None:
         signs = np.ascontiguousarray(signs, np.int8)
         sp = signs.ctypes.data_as(ctypes.POINTER(ctypes.c_int8))
-    cfg = tvq.tvq_config(L, H, d, shared, seed, arr, sp)
+    cfg = tvq.tvq_config(L, H, d, shared, seed, arr, sp, packing)
     cfg._keep = (arr, signs)
     return cfg
 
@@ -95,18 +96,20 @@ def _random_table(rng, L):
 
 @pytest.mark.parametrize("seed", range(6))
 def test_layout_agrees_with_oracle(tvq, orc, seed):
+    """Layouts of random tables, with and without group packing (odd seeds)."""
     rng = np.random.default_rng(seed)
+    packing = seed % 2
     L = int(rng.integers(1, 9))
     H = int(rng.integers(1, 9))
     d = int(rng.choice([64, 128]))
     B = int(rng.integers(1, 4))
     T = int(rng.integers(1, 300))
     table = _random_table(rng, L)
-    lay = tvq.tvq_layout_for_config(_cfg(tvq, table, L, H, d), B, T)
+    lay = tvq.tvq_layout_for_config(_cfg(tvq, table, L, H, d, packing=packing), B, T)
     kinds = []
     for (nk, nv, bk, bv, mk, mv) in table:
         kinds += [orc.Kind(nk, mk, bk), orc.Kind(nv, mv, bv)]
-    oc = orc.Codec(L, H, d, kinds, np.ones((L, d), np.int8))
+    oc = orc.Codec(L, H, d, kinds, np.ones((L, d), np.int8), packing=packing)
     total, off = oc.layout(B, T)
     assert lay.total_bytes == total
     assert lay.batch == B and lay.capacity_tokens == T
@@ -204,6 +207,21 @@ def test_null_codec_calls_rejected(tvq):
     assert lib.tvq_cache_layout(None, 1, 1, ctypes.byref(lay)) == -1
     assert lib.tvq_bits_per_element(None, 0) < 0
     lib.tvq_destroy(None)
+
+
+def test_group_packing_storage(tvq):
+    """Group packing at n = 48 (d = 128): 45-byte angle records instead of 48, and the
+    actual-storage rate drops by 3 * 8 / 128 bits per element; powers of two are unchanged;
+    an unknown packing value is rejected."""
+    t48 = [(48, 64, 8, 4, 1, 2)]
+    plain = tvq.tvq_layout_for_config(_cfg(tvq, t48, 1, 8, 128), 1, 16)
+    packed = tvq.tvq_layout_for_config(_cfg(tvq, t48, 1, 8, 128, packing=1), 1, 16)
+    assert plain.rec_bytes[0][0][0] == 48 and packed.rec_bytes[0][0][0] == 45
+    assert plain.rec_bytes[0][1][0] == packed.rec_bytes[0][1][0] == 48     # n = 64
+    r0 = tvq.tvq_bits_per_element_config(_cfg(tvq, t48, 1, 8, 128), 1)
+    r1 = tvq.tvq_bits_per_element_config(_cfg(tvq, t48, 1, 8, 128, packing=1), 1)
+    assert r0 - r1 == pytest.approx(3 * 8 / 128 / 2)        # averaged over K and V
+    assert tvq.tvq_bits_per_element_config(_cfg(tvq, t48, 1, 8, 128, packing=2), 1) < 0
 
 
 def test_layout_limits(tvq):

@@ -130,6 +130,24 @@ def test_odd_widths_and_norm_modes(gpu, d):
     _roundtrip(s, k, v, 1, 33, 40, 3, f"odd-widths-d{d}")
 
 
+@pytest.mark.parametrize("d", [64, 128])
+def test_group_packing(gpu, d):
+    """Group packing of non-power-of-two codebooks: n = 48 and 56 (8 codes per group in 45
+    and 47 bits), 100 with fp32 norms, 3 (13 bits per 8 codes), 300 and 4095 (4 codes per
+    group), next to a power of two that keeps its fixed width; fp32 and bf16 inputs, a
+    ragged token count written at slot 4."""
+    table = [LayerCfg(48, 56, 8, 4, NORM_LINEAR, NORM_LOG),
+             LayerCfg(100, 3, 32, 6, NORM_F32, NORM_LINEAR),
+             LayerCfg(300, 4095, 5, 8, NORM_LOG, NORM_LINEAR),
+             LayerCfg(64, 48)]
+    s = Setup(4, 2, d, table, workloads.sign_table(13, 4, d), packing=1).build()
+    assert s.orc.record_bytes(0, 0)[0] == (45 if d == 128 else 23)
+    w = workloads.get("C2")
+    for dtype, seed in (("f32", 6), ("bf16", 7)):
+        k, v = _draw(w, 4, 2, 2, 29, d, dtype, seed)
+        _roundtrip(s, k, v, 2, 29, 40, 4, f"group-packing-d{d}-{dtype}")
+
+
 def test_seeded_signs(gpu):
     """The codec draws D itself from a seed (per layer, and shared across layers as the paper
     does); the oracle draws it with its own SplitMix64."""
