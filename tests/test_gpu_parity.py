@@ -568,3 +568,92 @@ def test_attention_api_errors(gpu):
     small = torch.empty(16, dtype=torch.uint8, device="cuda")
     with pytest.raises(tvq.TvqError):
         s.gpu.attention(cache, lay, 0, 40, qd, out, 0.1, workspace=small)
+
+
+def test_long_context_attention_full_size_sampled(gpu):
+    """Attention at the long-context benchmark's shape and launch plan: 16 sequences x 32768
+    cached tokens + 1 appended, 32 layers x 8 KV heads, 32 query heads, d = 128, layers 0-3 at
+    n = 256.  Contiguous cache and paged pool (256-slot blocks, shuffled tables) encoded from the
+    same draw; attention of a boosted and a base layer.  The paged outputs equal the contiguous
+    ones bit for bit (same chunk plan, same codes); sampled (sequence, KV head) rows are checked
+    against the oracle's fp64 attention over that row's records (gathered on the GPU), under
+    parity.attention_error_bar.  Needs ~140 GB of device memory."""
+    import types
+    import torch
+    w = workloads.get("C5")
+    free, _ = torch.cuda.mem_get_info()
+    if free < 140e9:
+        pytest.skip(f"needs ~140 GB of free device memory, {free / 1e9:.0f} GB free")
+    s = setup_from_workload(w)
+    cap = w.T + 1
+    G, P_blk = 4, 256
+    Hq = w.H * G
+    lay = s.gpu.layout(w.B, cap)
+    cache = torch.empty((lay.total_bytes,), dtype=torch.uint8, device="cuda")
+    max_blocks = -(-cap // P_blk)
+    n_blocks = w.B * max_blocks
+    pool_lay = s.gpu.pool_layout(n_blocks, P_blk)
+    pool = torch.empty((pool_lay.total_bytes,), dtype=torch.uint8, device="cuda")
+    perm = np.random.default_rng(9).permutation(n_blocks).astype(np.int32)
+    table = torch.from_numpy(perm.reshape(w.B, max_blocks)).cuda()
+    shape = (w.L, w.B, w.H, w.T, w.d)
+    src = {}
+    for kind, name in ((0, "K"), (1, "V")):
+        x = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+        workloads.fill_device(w, name, x)
+        src[kind] = x
+    zeros = torch.zeros(w.B, dtype=torch.int32, device="cuda")
+    s.gpu.encode(src[0], src[1], cache, lay, 0)
+    s.gpu.encode_paged(src[0], src[1], zeros, table, pool, pool_lay)
+    del src
+    torch.cuda.empty_cache()
+    new = {}
+    for kind, name in ((0, "K"), (1, "V")):
+        xn = torch.empty((w.L, w.B, w.H, 1, w.d), dtype=torch.bfloat16, device="cuda")
+        workloads.fill_device(w, name, xn, token_part=1)
+        new[kind] = xn
+    s.gpu.encode(new[0], new[1], cache, lay, w.T)
+    s.gpu.encode_paged(new[0], new[1], torch.full((w.B,), w.T, dtype=torch.int32, device="cuda"),
+                       table, pool, pool_lay)
+    ctx = torch.full((w.B,), cap, dtype=torch.int32, device="cuda")
+    gq = torch.Generator(device="cuda").manual_seed(11)
+    scale = 1.0 / np.sqrt(w.d)
+    rng = np.random.default_rng(3)
+    rows = [(0, 0), (w.B - 1, w.H - 1)] + [(int(rng.integers(0, w.B)), int(rng.integers(0, w.H)))
+                                          for _ in range(2)]
+    worst = 0.0
+    for layer in (0, w.L - 1):
+        q = torch.randn((w.B, Hq, w.d), generator=gq, device="cuda").to(torch.bfloat16)
+        out = torch.full((w.B, Hq, w.d), float("nan"), dtype=torch.float32, device="cuda")
+        outp = torch.full_like(out, float("nan"))
+        s.gpu.attention(cache, lay, layer, cap, q, out, scale)
+        s.gpu.attention_paged(pool, pool_lay, table, ctx, cap, layer, q, outp, scale)
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int32), outp.view(torch.int32)), \
+            f"layer {layer}: paged attention differs from the contiguous cache's"
+        got = out.cpu().numpy().astype(np.float64)
+        q64 = q.float().cpu().numpy().astype(np.float64)
+        # one (sequence, KV head) row of the layer as a one-head, one-layer oracle cache
+        kinds = [s.orc.kinds[2 * layer], s.orc.kinds[2 * layer + 1]]
+        mini = oracle.Codec(1, 1, w.d, kinds, s.signs[layer:layer + 1])
+        mtotal, moff = mini.layout(1, cap)
+        for b, h in rows:
+            buf = np.zeros(mtotal, np.uint8)
+            row = (b * w.H + h) * cap
+            for kind in range(2):
+                for p in range(3):
+                    rb = lay.rec_bytes[layer][kind][p]
+                    if rb == 0:
+                        continue
+                    start = lay.off[layer][kind][p] + row * rb
+                    buf[moff[0, kind, p]: moff[0, kind, p] + cap * rb] = \
+                        torch_to_np(cache[start: start + cap * rb])
+            qr = q64[b:b + 1, h * G:(h + 1) * G]
+            ref = mini.attention_decode(buf, 1, cap, 0, cap, qr, scale)
+            bar = attention_error_bar(types.SimpleNamespace(orc=mini, H=1, d=w.d), buf, 1, cap,
+                                      0, cap, qr, scale, ref, True)
+            err = np.linalg.norm(got[b:b + 1, h * G:(h + 1) * G] - ref, axis=-1)
+            worst = max(worst, float((err / bar).max()))
+            _say(f"[attn-full layer={layer} b={b} h={h}] max |err|/bar = {(err / bar).max():.3f}")
+            assert np.isfinite(got[b]).all() and (err <= bar).all()
+    _say(f"[attn-full] paged == contiguous bit for bit; worst |err|/bar {worst:.3f}")
