@@ -41,6 +41,11 @@ constexpr float kLazyLog2 = 8.0f;    // weights 2^(s - m) stay below 2^8 between
 // 16-byte reads of a wave (one per lane of a vector, broadcast over the vector slots) fall in
 // distinct banks
 constexpr int kQPitch = kElemsPerLane + 4;
+// Value staging of the d = 128 matrix-core kernel: pair p of token t at word 16 p + t +
+// kVRowSkew (p / 16).  The skew puts the 16 tokens x 4 slices of a store, and the 16 lanes of
+// each quarter of a rotated 16-byte read, in distinct banks.
+constexpr int kVRowSkew = 16;
+constexpr int kVPairWords = 16 * 64 + kVRowSkew * 3;
 
 template <int LPV>
 __device__ __forceinline__ float vec_sum(float v) {
@@ -53,6 +58,30 @@ __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
   return v;
+}
+
+// Rotation inside each row of 16 lanes (DPP row_ror: a register operation, no LDS traffic).
+template <int N>
+__device__ __forceinline__ uint32_t row_ror(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x120 + N, 0xF, 0xF, true);
+}
+template <int N>
+__device__ __forceinline__ float row_ror(float v) {
+  return __uint_as_float(row_ror<N>(__float_as_uint(v)));
+}
+
+// v[l] + v[l ^ 16] and v[l] + v[l ^ 32] on every lane: v_permlane16_swap exchanges rows 2i and
+// 2i + 1 between two copies of v, v_permlane32_swap the two halves; both lanes of a pair add the
+// same two values, so they hold the same sum.
+__device__ __forceinline__ float sum_xor16(float v) {
+  const auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(t[0]) + __uint_as_float(t[1]);
+}
+__device__ __forceinline__ float sum_xor32(float v) {
+  const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(t[0]) + __uint_as_float(t[1]);
 }
 
 // Sum over the wave's vector slots (lanes sub, sub + LPV, ...): every lane gets its sub's sum.
@@ -237,6 +266,55 @@ __device__ __forceinline__ void attend_tile(const AttnWave<D>& w, const TilePair
   }
 }
 
+// The chunk wave's work: (sequence, KV head, chunk, pass of query heads), the chunk's tokens
+// (the sequence's own context with per-sequence lengths) and, for a paged cache, the pool
+// blocks of the chunk (lane i: its i-th block).  A chunk with no token writes partials of
+// weight 0 and returns false, as does a wave past the grid's work.
+template <int D>
+__device__ __forceinline__ bool chunk_setup(const AttnArgs& a, AttnWave<D>& w, uint32_t wib) {
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + wib);
+  if (wave >= a.B * a.H * a.n_chunks * a.n_pass) return false;
+  const uint32_t pass = wave % a.n_pass;
+  const uint32_t bhc = wave / a.n_pass;
+  const uint32_t bh = bhc / a.n_chunks;
+  w.chunk = bhc - bh * a.n_chunks;
+  w.b = bh / a.H;
+  w.h = bh - w.b * a.H;
+  w.g0 = pass * a.pass_heads;
+  w.gc = min(a.pass_heads, a.G - w.g0);
+  w.t0 = w.chunk * a.chunk_tokens;
+  // the sequence's context: t_end, or its own length (paged), at most what its table covers
+  uint32_t ctx = a.t_end;
+  if (a.pg.seq) {
+    const int32_t len = a.pg.seq[w.b];
+    ctx = len <= 0 ? 0u : min((uint32_t)len, a.t_end);
+  }
+  if (w.t0 >= ctx) {
+    // nothing to attend in this chunk: a partial of weight 0 for the merge
+    for (uint32_t g = 0; g < w.gc; ++g) {
+      const uint64_t idx = ((uint64_t)w.b * a.Hq + w.h * a.G + w.g0 + g) * a.n_chunks + w.chunk;
+      if (w.lane < D / 4)
+        *(float4*)(a.ws_acc + idx * D + 4 * w.lane) = make_float4(0, 0, 0, 0);
+      if (w.lane == 0) *(float2*)(a.ws_ml + idx * 2) = make_float2(-INFINITY, 0.0f);
+    }
+    return false;
+  }
+  w.ntok = min(a.chunk_tokens, ctx - w.t0);
+  w.row = bh * a.cap;
+  w.blk = 0;
+  if (a.pg.table) {
+    // lane i: the pool block of the chunk's i-th block (entries past the table or naming no
+    // pool block read block 0, so a corrupt table stays inside the pool)
+    const uint32_t i = (w.t0 >> a.pg.block_log2) + (uint32_t)w.lane;
+    const uint32_t blk = i < a.pg.max_blocks
+                             ? (uint32_t)a.pg.table[(size_t)w.b * a.pg.max_blocks + i] : 0u;
+    w.blk = blk < a.pg.n_blocks ? blk : 0u;
+  }
+  for (int kind = 0; kind < 2; ++kind)
+    for (int p = 0; p < 3; ++p) w.plane[kind][p] = a.cache + a.n_slots * w.sp[kind].pre[p];
+  return true;
+}
+
 template <int D, int KW, int KN, int VW, int VN>
 __global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
   constexpr int LPV = AttnWave<D>::LPV;
@@ -258,51 +336,9 @@ __global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
   w.sub = w.lane % LPV;
   w.vslot = w.lane / LPV;
   const uint32_t wib = threadIdx.x / kWave;
-  const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock + wib);
-  if (wave >= a.B * a.H * a.n_chunks * a.n_pass) return;
-  const uint32_t pass = wave % a.n_pass;
-  const uint32_t bhc = wave / a.n_pass;
-  const uint32_t bh = bhc / a.n_chunks;
-  w.chunk = bhc - bh * a.n_chunks;
-  w.b = bh / a.H;
-  w.h = bh - w.b * a.H;
-  w.g0 = pass * a.pass_heads;
-  w.gc = min(a.pass_heads, a.G - w.g0);
-  w.t0 = w.chunk * a.chunk_tokens;
-  // the sequence's context: t_end, or its own length (paged), at most what its table covers
-  uint32_t ctx = a.t_end;
-  if (a.pg.seq) {
-    const int32_t len = a.pg.seq[w.b];
-    ctx = len <= 0 ? 0u : min((uint32_t)len, a.t_end);
-  }
-  if (w.t0 >= ctx) {
-    // nothing to attend in this chunk: a partial of weight 0 for the merge
-    if (w.vslot == 0) {
-      for (uint32_t g = 0; g < w.gc; ++g) {
-        const uint64_t idx =
-            ((uint64_t)w.b * a.Hq + w.h * a.G + w.g0 + g) * a.n_chunks + w.chunk;
-        float* dst = a.ws_acc + idx * D + w.sub * kElemsPerLane;
-        for (int i = 0; i < kElemsPerLane; i += 4) *(float4*)(dst + i) = make_float4(0, 0, 0, 0);
-        if (w.sub == 0) *(float2*)(a.ws_ml + idx * 2) = make_float2(-INFINITY, 0.0f);
-      }
-    }
-    return;
-  }
-  w.ntok = min(a.chunk_tokens, ctx - w.t0);
-  w.row = bh * a.cap;
-  w.blk = 0;
-  if (a.pg.table) {
-    // lane i: the pool block of the chunk's i-th block (entries past the table or naming no
-    // pool block read block 0, so a corrupt table stays inside the pool)
-    const uint32_t i = (w.t0 >> a.pg.block_log2) + (uint32_t)w.lane;
-    const uint32_t blk = i < a.pg.max_blocks
-                             ? (uint32_t)a.pg.table[(size_t)w.b * a.pg.max_blocks + i] : 0u;
-    w.blk = blk < a.pg.n_blocks ? blk : 0u;
-  }
   w.sp[0] = spk;
   w.sp[1] = spv;
-  for (int kind = 0; kind < 2; ++kind)
-    for (int p = 0; p < 3; ++p) w.plane[kind][p] = a.cache + a.n_slots * w.sp[kind].pre[p];
+  if (!chunk_setup<D>(a, w, wib)) return;
   float* qh = (float*)s_q[wib];
   float* lvl = s_lvl[wib] + 16 * w.vslot;
   if (a.q_f32) query_transform<D, true>(a, w, qh);
@@ -346,6 +382,206 @@ __global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
         if (w.sub == 0) *(float2*)(a.ws_ml + idx * 2) = make_float2(m[g], lg);
       }
     }
+  }
+}
+
+// The chunk kernel at d = 128 with the two contractions on the matrix cores
+// (v_mfma_f32_4x4x1f32: 16 blocks b = lane / 4; block b's C[r][j] += A[lane 4b + r] *
+// B[lane 4b + j], kept by lane 4b + j in its register r).
+//   scores  lane l decodes y'_K of token t = l % 16, elements 32 s .. 32 s + 31 (s = l / 16),
+//           and holds q^ of query head j = l % 4 on the same elements.  Over those 32 elements
+//           block b = l / 4 (tokens 4 ((l / 4) % 4) + r) accumulates the partial scores of 4
+//           tokens x 4 heads; the four element slices s are summed across lanes, so every row
+//           of 16 lanes holds all 16 scores and lane l the weights of tokens 4 tq .. 4 tq + 3
+//           (tq = (l / 4) % 4) for head j.
+//   values  the V codes of the tile go through LDS so that lane l reads pair l (elements 2l,
+//           2l + 1) of any token; in each of 16 steps block b = l / 4 adds y'_V(k, pair
+//           4b + r) * p(k, head j) for one token k, the blocks of a row taking their tokens in
+//           rotated order so that the weights move by row rotations instead of LDS; lane
+//           4b + j accumulates pairs 4b .. 4b + 3 of head j: 8 registers for the whole
+//           (4 heads x 128 elements) accumulator.
+// The reference point m, the sum l and the accumulator of head j live on the lanes with
+// lane % 4 == j.  y' is rebuilt exactly as decode rebuilds it.
+template <int KW, int KN, int VW, int VN>
+__global__ __launch_bounds__(kBlockThreads) void attn_mfma_chunk_kernel(AttnArgs a) {
+  constexpr int D = 128;
+  typedef float v4f __attribute__((ext_vector_type(4)));
+  __shared__ float2 s_lut[2][kLut];
+  // level tables of log-space norms (none for linear norms): K as 16 rows of 16 levels, V with
+  // level q of token t at word 32 q + 2 t + c in two copies c, read by the lanes of even and odd
+  // slices, so that the 32 lanes of each half of a read use 32 distinct banks
+  constexpr int kLvlK = KN == 8 ? 0 : 16 * 16, kLvlV = VN == 8 ? 0 : 16 * 32;
+  __shared__ float s_lvl[kWavesPerBlock][kLvlK + kLvlV + 1];
+  // per wave: q^ of the pass's heads while it is read into registers, then per pair and token
+  // the two elements of y'_V
+  static_assert(kAttnPassHeads * 4 * kQPitch <= 2 * kVPairWords, "q^ fits the value staging");
+  __shared__ __attribute__((aligned(16))) float s_stage[kWavesPerBlock][2 * kVPairWords];
+
+  const SegParams spk = a.segs[2 * a.layer], spv = a.segs[2 * a.layer + 1];
+  for (uint32_t e = threadIdx.x; e < spk.n; e += kBlockThreads)
+    s_lut[0][e] = ((const float2*)a.lut)[spk.lut_off + e];
+  for (uint32_t e = threadIdx.x; e < spv.n; e += kBlockThreads)
+    s_lut[1][e] = ((const float2*)a.lut)[spv.lut_off + e];
+  __syncthreads();
+
+  const uint32_t wib = threadIdx.x / kWave;
+  const int lane = threadIdx.x & (kWave - 1);
+  AttnWave<D> w;
+  w.lane = lane;
+  w.sp[0] = spk;
+  w.sp[1] = spv;
+  if (!chunk_setup<D>(a, w, wib)) return;
+
+  // q^ of the pass's heads: computed in the quad layout (vector slot g = head g), read back as
+  // head j = lane % 4 on elements 32 s .. 32 s + 31 (zero for heads past the pass)
+  float* qh = s_stage[wib];
+  {
+    AttnWave<D> wq = w;
+    wq.sub = lane % 4;
+    wq.vslot = lane / 4;
+    if (a.q_f32) query_transform<D, true>(a, wq, qh);
+    else query_transform<D, false>(a, wq, qh);
+  }
+  wave_lds_sync();
+  const int j = lane & 3, s = lane >> 4, tq = (lane >> 2) & 3;
+  float qr[kElemsPerLane];
+#pragma unroll
+  for (int i = 0; i < kElemsPerLane; i += 4) {
+    const float4 v = (uint32_t)j < w.gc ? *(const float4*)(qh + (j * 4 + s) * kQPitch + i)
+                                        : make_float4(0, 0, 0, 0);
+    qr[i] = v.x, qr[i + 1] = v.y, qr[i + 2] = v.z, qr[i + 3] = v.w;
+  }
+  // the K layout: token t = lane % 16, slice s (tile loads and the K decode use it)
+  w.sub = s;
+  w.vslot = lane & 15;
+  float* lvl_k = s_lvl[wib] + 16 * w.vslot;
+  float* lvl_v = s_lvl[wib] + kLvlK + 2 * w.vslot;
+  float* vy0 = s_stage[wib];
+  float* vy1 = s_stage[wib] + kVPairWords;
+  // this lane's pair (pair `lane`) in the value layout: 16 tokens from word 16 pair + skew
+  const float* vy0_row = vy0 + 16 * lane + kVRowSkew * (lane >> 4);
+  const float* vy1_row = vy1 + 16 * lane + kVRowSkew * (lane >> 4);
+  // token groups of the weights that row rotations by 0, 4, 8 and 12 lanes bring to this lane
+  // (found by rotating the lane's own group number the same way)
+  const uint32_t grp[4] = {(uint32_t)tq, row_ror<4>((uint32_t)tq), row_ror<8>((uint32_t)tq),
+                           row_ror<12>((uint32_t)tq)};
+
+  float m = -INFINITY, lsum = 0.0f;
+  // accumulators of element 0 and 1 of each pair
+  v4f acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
+  constexpr uint32_t kVLevels = (1u << VN) - 1u;
+
+  const uint32_t last = (w.ntok + 15) / 16 - 1;
+  auto tile_work = [&](const TilePair<KW, KN, VW, VN>& c, uint32_t tile) {
+    // ---- scores: y'_K on this lane's slice, then 32 matrix products over the slice ----
+    float y[kElemsPerLane];
+    code_vector<4, KW, KN>(c.k, s_lut[0], lvl_k, s, y);
+    v4f sc = {0, 0, 0, 0};
+#pragma unroll
+    for (int n = 0; n < kElemsPerLane; ++n)
+      sc = __builtin_amdgcn_mfma_f32_4x4x1f32(y[n], qr[n], sc, 0, 0, 0);
+    // the four slices summed: every row of 16 lanes now holds the scores of tokens 4 tq + r
+    // (register r) for head j
+    float sv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float tot = sum_xor32(sum_xor16(sc[r]));
+      sv[r] = tile * 16 + 4 * tq + r < w.ntok ? tot : -INFINITY;
+    }
+    const float smax = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+    if (__builtin_amdgcn_ballot_w64(smax > m + kLazyLog2) != 0) {   // a new reference point
+      float mx = fmaxf(smax, __shfl_xor(smax, 4));
+      mx = fmaxf(mx, __shfl_xor(mx, 8));
+      const float mn = fmaxf(m, mx);
+      const float f = __builtin_amdgcn_exp2f(m - mn);          // 0 on the first raise
+      lsum *= f;
+      acc0 *= f;
+      acc1 *= f;
+      m = mn;
+    }
+    float p[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) p[r] = __builtin_amdgcn_exp2f(sv[r] - m);
+    lsum += (p[0] + p[1]) + (p[2] + p[3]);
+
+    // ---- values: y'_V of every pair to the pair layout through LDS ----
+    {
+      const float rmin = __uint_as_float(c.v.hdr.x), rmax = __uint_as_float(c.v.hdr.y);
+      uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
+      unpack16_index<VW>(c.v.ang, kc);
+      wave_lds_sync();                       // the previous tile's reads of vy and lvl are done
+      float step = 0.0f;
+      if constexpr (VN == 8) {
+        unpack16<VN>(c.v.nrm, qc);
+        step = rmax == rmin ? 0.0f : (rmax - rmin) / (float)kVLevels;
+      } else {
+        unpack16_index<VN>(c.v.nrm, qc);
+        log_level_ladder_each<4>(
+            [lvl_v](uint32_t q, float v) {
+              lvl_v[32 * q] = v;
+              lvl_v[32 * q + 1] = v;
+            },
+            s, rmin, rmax, kVLevels);
+        wave_lds_sync();
+      }
+      float* d0 = vy0 + kVRowSkew * s + w.vslot;
+      float* d1 = vy1 + kVRowSkew * s + w.vslot;
+#pragma unroll
+      for (int i = 0; i < kPairsPerLane; ++i) {
+        const int pr = 16 * s + i;             // row of pair 16 s + i, before the slice skew
+        const float r =
+            VN == 8 ? __builtin_fmaf((float)qc[i], step, rmin) : lvl_v[32 * qc[i] + (s & 1)];
+        const float2 cs = s_lut[1][kc[i]];
+        d0[16 * pr] = r * cs.x;
+        d1[16 * pr] = r * cs.y;
+      }
+      wave_lds_sync();
+    }
+    // step 4 x + r of the products takes, in block b, token 4 grp[x] + r: the weights come from
+    // the lanes 4 x further round the row (so every block of 4 lanes sees all 16 tokens over the
+    // 16 steps), y'_V from LDS at that block's own token
+    float pw[16];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      pw[r] = p[r];
+      pw[4 + r] = row_ror<4>(p[r]);
+      pw[8 + r] = row_ror<8>(p[r]);
+      pw[12 + r] = row_ror<12>(p[r]);
+    }
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const float4 v0 = *(const float4*)(vy0_row + 4 * grp[x]);
+      const float4 v1 = *(const float4*)(vy1_row + 4 * grp[x]);
+      acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(v0.x, pw[4 * x], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(v1.x, pw[4 * x], acc1, 0, 0, 0);
+      acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(v0.y, pw[4 * x + 1], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(v1.y, pw[4 * x + 1], acc1, 0, 0, 0);
+      acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(v0.z, pw[4 * x + 2], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(v1.z, pw[4 * x + 2], acc1, 0, 0, 0);
+      acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(v0.w, pw[4 * x + 3], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(v1.w, pw[4 * x + 3], acc1, 0, 0, 0);
+    }
+  };
+
+  TilePair<KW, KN, VW, VN> ca = tile_pair<D, KW, KN, VW, VN>(a, w, 0);
+  for (uint32_t t = 0; t <= last; t += 2) {
+    const uint32_t t1 = min(t + 1, last);
+    const TilePair<KW, KN, VW, VN> cb = tile_pair<D, KW, KN, VW, VN>(a, w, t1);
+    tile_work(ca, t);
+    ca = tile_pair<D, KW, KN, VW, VN>(a, w, min(t + 2, last));
+    if (t1 != t) tile_work(cb, t1);
+  }
+
+  // l of head j: every row holds the same partial sums, so the row's four token groups are
+  // added; lane 4b + j stores elements 8b .. 8b + 7 of head j
+  lsum += __shfl_xor(lsum, 4);
+  lsum += __shfl_xor(lsum, 8);
+  if ((uint32_t)j < w.gc) {
+    const uint64_t idx = ((uint64_t)w.b * a.Hq + w.h * a.G + w.g0 + j) * a.n_chunks + w.chunk;
+    float* dst = a.ws_acc + idx * D + 8 * (lane >> 2);
+    *(float4*)dst = make_float4(acc0[0], acc1[0], acc0[1], acc1[1]);
+    *(float4*)(dst + 4) = make_float4(acc0[2], acc1[2], acc0[3], acc1[3]);
+    if (lane < 4) *(float2*)(a.ws_ml + idx * 2) = make_float2(m, lsum);
   }
 }
 
@@ -415,7 +651,10 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
 
 template <int D, int KW, int KN, int VW, int VN>
 void launch_chunk(const AttnArgs& a, dim3 grid, hipStream_t s) {
-  hipLaunchKernelGGL((attn_chunk_kernel<D, KW, KN, VW, VN>), grid, dim3(kBlockThreads), 0, s, a);
+  if constexpr (D == 128)
+    hipLaunchKernelGGL((attn_mfma_chunk_kernel<KW, KN, VW, VN>), grid, dim3(kBlockThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_chunk_kernel<D, KW, KN, VW, VN>), grid, dim3(kBlockThreads), 0, s, a);
 }
 
 // format index: bit 0 = 8-bit angle codes (n = 256), bit 1 = 4-bit log norms

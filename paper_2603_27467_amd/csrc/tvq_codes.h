@@ -95,13 +95,14 @@ __device__ __forceinline__ double ladder_ratio(float lo_c, float hi_c, uint32_t 
   return rho;
 }
 
-// The levels of one vector into `tab` (2^b <= 16 entries), split over the vector's LPV lanes:
+// The levels of one vector (2^b <= 16 entries), split over the vector's LPV lanes, handed to
+// store(q, level) (log_level_ladder: into tab[q]):
 // level q = RN32(R'min * rho^q).  Level 0 is R'min exactly and RN32 brings the top level back
 // to R'max.  Vectors with R'min == R'max get Rmin at every level.  The caller orders the LDS
 // writes against other lanes' reads.
-template <int LPV>
-__device__ __forceinline__ void log_level_ladder(float* tab, int sub, float rmin, float rmax,
-                                                 uint32_t qlevels) {
+template <int LPV, class Store>
+__device__ __forceinline__ void log_level_ladder_each(Store&& store, int sub, float rmin,
+                                                      float rmax, uint32_t qlevels) {
   const float lo_c = fmaxf(rmin, FLT_MIN), hi_c = fmaxf(rmax, FLT_MIN);
   const bool deg = lo_c == hi_c;
   const double rho = deg ? 1.0 : ladder_ratio(lo_c, hi_c, qlevels);
@@ -111,9 +112,15 @@ __device__ __forceinline__ void log_level_ladder(float* tab, int sub, float rmin
   const double step = (LPV >= 4) ? rho2 * rho2 : rho2;    // rho^LPV
   double v = (double)lo_c * pw;
   for (uint32_t q = sub; q <= qlevels; q += LPV) {
-    tab[q] = deg ? rmin : (float)v;
+    store(q, deg ? rmin : (float)v);
     v *= step;
   }
+}
+template <int LPV>
+__device__ __forceinline__ void log_level_ladder(float* tab, int sub, float rmin, float rmax,
+                                                 uint32_t qlevels) {
+  log_level_ladder_each<LPV>([tab](uint32_t q, float v) { tab[q] = v; }, sub, rmin, rmax,
+                             qlevels);
 }
 
 // Raw code words of one vector's lane for n = 64/256 angle codes (WA = 6/8 bits) and NB = 8
