@@ -403,7 +403,7 @@ __global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
 // The reference point m, the sum l and the accumulator of head j live on the lanes with
 // lane % 4 == j.  y' is rebuilt exactly as decode rebuilds it.
 template <int KW, int KN, int VW, int VN>
-__global__ __launch_bounds__(kBlockThreads) void attn_mfma_chunk_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kBlockThreads, 3) void attn_mfma_chunk_kernel(AttnArgs a) {
   constexpr int D = 128;
   typedef float v4f __attribute__((ext_vector_type(4)));
   __shared__ float2 s_lut[2][kLut];
