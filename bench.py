@@ -172,7 +172,7 @@ def _short(name: str) -> str:
         return "tvq_encode"
     if "decode_" in name and "tvq" in name:
         return "tvq_decode"
-    if "attn_chunk" in name and "tvq" in name:
+    if "attn_" in name and "chunk_kernel" in name and "tvq" in name:
         return "tvq_attention_chunk"
     if "attn_merge" in name and "tvq" in name:
         return "tvq_attention_merge"
