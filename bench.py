@@ -150,14 +150,25 @@ def cpu_baseline(w: workloads.Workload, budget_s: float = 15.0) -> dict:
             vecs += sum(ex.map(run, jobs))
             passes += 1
     wall = time.perf_counter() - s
+    # the same jobs on one thread, for about a fifth of the budget
+    vecs1 = 0
+    s1 = time.perf_counter()
+    for job in jobs:
+        vecs1 += run(job)
+        if time.perf_counter() - s1 > budget_s / 5:
+            break
+    wall1 = time.perf_counter() - s1
     elem_bytes = 2 if w.dtype == "bf16" else 4
     kv_bytes = vecs * w.d * elem_bytes
     return {"value": round(2 * kv_bytes / wall / 1e9, 4), "unit": "GB/s", "cores": cores,
+            "value_1core": round(2 * vecs1 * w.d * elem_bytes / wall1 / 1e9, 4),
             "kind": "oracle",
             "sample": f"{len(tasks)} chunks of {chunk} tokens x {w.B * w.H} (batch, head) rows "
                       f"x (K, V) spread over all {w.L} layers, {vecs // passes} vectors, encoded "
                       f"and decoded {passes} times: {vecs} vectors in {wall:.1f} s on {cores} "
-                      f"threads; same unit as value (bf16 KV bytes encoded + decoded per second)"}
+                      f"threads; value_1core: {vecs1} vectors of the same jobs in {wall1:.1f} s "
+                      f"on one thread; same unit as value (bf16 KV bytes encoded + decoded per "
+                      f"second)"}
 
 
 def _csv(path):
@@ -291,6 +302,30 @@ def copy_calibration() -> None:
     dst.copy_(src)
     torch.cuda.synchronize()
     del src, dst
+
+
+def copy_peak(nbytes: int = 1 << 30, reps: int = 10) -> dict:
+    """The achievable streaming rate on this GPU: a plain elementwise read + write pass
+    (torch.add of 0 from one fp32 buffer of `nbytes` into another; it streams faster than the
+    runtime's device-to-device blit), timed with events over `reps` runs after a warm-up run.
+    Bytes moved per run = 2 * nbytes."""
+    import torch
+    src = torch.zeros(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.add(src, 0.0, out=dst)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for i in range(reps):
+        torch.add(src, 0.0, out=dst)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    ms = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)])
+    del src, dst
+    return {"kernel": "elementwise fp32 read + write (torch.add of 0)",
+            "bytes_per_run": 2 * nbytes,
+            "GBps_mean": round(2 * nbytes / (float(ms.mean()) * 1e-3) / 1e9, 1),
+            "GBps_max": round(2 * nbytes / (float(ms.min()) * 1e-3) / 1e9, 1)}
 
 
 def longctx_bytes(w: workloads.Workload):
@@ -728,6 +763,8 @@ def main() -> int:
         step(args.warmup + i, ev[i])
     torch.cuda.synchronize()
     wall_s = time.perf_counter() - t_wall
+    print("# streaming copy", file=sys.stderr, flush=True)
+    copy = copy_peak()
     enc = np.array([e[0].elapsed_time(e[1]) for e in ev])
     dec = np.array([e[1].elapsed_time(e[2]) for e in ev])
     span_ms = ev[0][0].elapsed_time(ev[-1][2]) / args.steps
@@ -746,6 +783,7 @@ def main() -> int:
                "frac_of_peak": round(gbs / HBM_PEAK_GBPS, 4),
                "frac_of_peak_at_min": round(ab["per_launch"] / (ms_all.min() * 1e-3) / 1e9
                                             / HBM_PEAK_GBPS, 4),
+               "frac_of_copy_peak": round(gbs / copy["GBps_mean"], 4),
                "vectors_per_s": round(ab["vectors"] / (ms * 1e-3), 1),
                "traffic_bytes_per_launch": None if prof is None else prof["hbm_bytes_per_launch"]}
         if prof is not None:
@@ -787,6 +825,7 @@ def main() -> int:
         "encode": e_leg,
         "decode": d_leg,
         "wall_s_timed": round(wall_s, 4),
+        "copy_peak": copy,
         "kernel_source_hash": kernel_source_hash(),
     }
     if "valu" in dom:
