@@ -155,6 +155,22 @@ __device__ __forceinline__ uint32_t paged_record(const AttnArgs& a, const AttnWa
   return ((blk * a.H + w.h) << a.pg.block_log2) + (tok & ((1u << a.pg.block_log2) - 1u));
 }
 
+// The V header (R'min, R'max) of this lane's token (vector slot) in `tile`, where the tile
+// may differ between lanes: the paged block id comes from its lane by a cross-lane read.
+template <int D>
+__device__ __forceinline__ u32x2 v_header(const AttnArgs& a, const AttnWave<D>& w,
+                                          uint32_t tile) {
+  const uint32_t j = min(tile * AttnWave<D>::VPW + w.vslot, w.ntok - 1);
+  uint32_t slot = w.row + w.t0 + j;
+  if (a.pg.table) {
+    const uint32_t first = (w.t0 + tile * AttnWave<D>::VPW) >> a.pg.block_log2;
+    const uint32_t blk = (uint32_t)__shfl((int)w.blk, (int)(first - (w.t0 >> a.pg.block_log2)));
+    const uint32_t tok = w.t0 + j;
+    slot = ((blk * a.H + w.h) << a.pg.block_log2) + (tok & ((1u << a.pg.block_log2) - 1u));
+  }
+  return *(const u32x2*)(w.plane[1][2] + (uint64_t)slot * 8);
+}
+
 template <int D, int KW, int KN, int VW, int VN>
 __device__ __forceinline__ TilePair<KW, KN, VW, VN> tile_pair(const AttnArgs& a,
                                                               const AttnWave<D>& w,
@@ -472,6 +488,12 @@ __global__ __launch_bounds__(kBlockThreads, 3) void attn_mfma_chunk_kernel(AttnA
   constexpr uint32_t kVLevels = (1u << VN) - 1u;
 
   const uint32_t last = (w.ntok + 15) / 16 - 1;
+  // log-space V norms: the ladder ratio of each token, computed for four tiles at once (the
+  // four lanes of a token would otherwise compute the same one): lane (t, s) holds that of
+  // token t in tile 4 k + s, and tile 4 k + x reads it from lane t + 16 x
+  double vrho = 1.0;
+  u32x2 vh = {0u, 0u};
+  if constexpr (VN != 8) vh = v_header<D>(a, w, min((uint32_t)s, last));
   auto tile_work = [&](const TilePair<KW, KN, VW, VN>& c, uint32_t tile) {
     // ---- scores: y'_K on this lane's slice, then 32 matrix products over the slice ----
     float y[kElemsPerLane];
@@ -516,12 +538,17 @@ __global__ __launch_bounds__(kBlockThreads, 3) void attn_mfma_chunk_kernel(AttnA
         step = rmax == rmin ? 0.0f : (rmax - rmin) / (float)kVLevels;
       } else {
         unpack16_index<VN>(c.v.nrm, qc);
-        log_level_ladder_each<4>(
+        if ((tile & 3u) == 0) {
+          vrho = ladder_rho(__uint_as_float(vh.x), __uint_as_float(vh.y), kVLevels);
+          vh = v_header<D>(a, w, min(tile + 4u + (uint32_t)s, last));   // the next group's
+        }
+        const double rho = __shfl(vrho, w.vslot + 16 * (int)(tile & 3u));
+        ladder_levels_each<4>(
             [lvl_v](uint32_t q, float v) {
               lvl_v[32 * q] = v;
               lvl_v[32 * q + 1] = v;
             },
-            s, rmin, rmax, kVLevels);
+            s, rmin, rmax, rho, kVLevels);
         wave_lds_sync();
       }
       float* d0 = vy0 + kVRowSkew * s + w.vslot;

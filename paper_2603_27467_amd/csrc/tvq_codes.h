@@ -95,17 +95,22 @@ __device__ __forceinline__ double ladder_ratio(float lo_c, float hi_c, uint32_t 
   return rho;
 }
 
-// The levels of one vector (2^b <= 16 entries), split over the vector's LPV lanes, handed to
-// store(q, level) (log_level_ladder: into tab[q]):
-// level q = RN32(R'min * rho^q).  Level 0 is R'min exactly and RN32 brings the top level back
-// to R'max.  Vectors with R'min == R'max get Rmin at every level.  The caller orders the LDS
-// writes against other lanes' reads.
+// The levels of one vector (2^b <= 16 entries): level q = RN32(R'min * rho^q).  Level 0 is
+// R'min exactly and RN32 brings the top level back to R'max.  Vectors with R'min == R'max get
+// Rmin at every level.  ladder_rho gives rho (1 for those vectors); ladder_levels_each hands
+// the levels q = sub, sub + LPV, ... of one of the vector's LPV lanes to store(q, level);
+// log_level_ladder_each does both, log_level_ladder stores into tab[q].  The caller orders
+// the LDS writes against other lanes' reads.
+__device__ __forceinline__ double ladder_rho(float rmin, float rmax, uint32_t qlevels) {
+  const float lo_c = fmaxf(rmin, FLT_MIN), hi_c = fmaxf(rmax, FLT_MIN);
+  return lo_c == hi_c ? 1.0 : ladder_ratio(lo_c, hi_c, qlevels);
+}
+
 template <int LPV, class Store>
-__device__ __forceinline__ void log_level_ladder_each(Store&& store, int sub, float rmin,
-                                                      float rmax, uint32_t qlevels) {
+__device__ __forceinline__ void ladder_levels_each(Store&& store, int sub, float rmin, float rmax,
+                                                   double rho, uint32_t qlevels) {
   const float lo_c = fmaxf(rmin, FLT_MIN), hi_c = fmaxf(rmax, FLT_MIN);
   const bool deg = lo_c == hi_c;
-  const double rho = deg ? 1.0 : ladder_ratio(lo_c, hi_c, qlevels);
   const double rho2 = rho * rho;
   double pw = (sub & 1) ? rho : 1.0;          // rho^sub
   if constexpr (LPV >= 4) pw = (sub & 2) ? pw * rho2 : pw;
@@ -115,6 +120,12 @@ __device__ __forceinline__ void log_level_ladder_each(Store&& store, int sub, fl
     store(q, deg ? rmin : (float)v);
     v *= step;
   }
+}
+
+template <int LPV, class Store>
+__device__ __forceinline__ void log_level_ladder_each(Store&& store, int sub, float rmin,
+                                                      float rmax, uint32_t qlevels) {
+  ladder_levels_each<LPV>(store, sub, rmin, rmax, ladder_rho(rmin, rmax, qlevels), qlevels);
 }
 template <int LPV>
 __device__ __forceinline__ void log_level_ladder(float* tab, int sub, float rmin, float rmax,
