@@ -132,13 +132,46 @@ __device__ __forceinline__ bool wave_setup(const DecodeArgs& a, WaveState<D>& w,
 // Rmin at every level.
 template <int D>
 __device__ __forceinline__ const float* build_log_levels(const WaveState<D>& w, float* lvl,
-                                                         float rmin, float rmax, uint32_t qlevels) {
+                                                         float rmin, float rmax, double rho,
+                                                         uint32_t qlevels) {
   float* tab = lvl + (w.vslot << kLvlBits);
   wave_lds_sync();             // earlier reads of this LDS area are done
-  log_level_ladder<WaveState<D>::LPV>(tab, w.sub, rmin, rmax, qlevels);
+  ladder_levels_each<WaveState<D>::LPV>([tab](uint32_t q, float v) { tab[q] = v; }, w.sub, rmin,
+                                        rmax, rho, qlevels);
   wave_lds_sync();
   return tab;
 }
+template <int D>
+__device__ __forceinline__ const float* build_log_levels(const WaveState<D>& w, float* lvl,
+                                                         float rmin, float rmax, uint32_t qlevels) {
+  return build_log_levels<D>(w, lvl, rmin, rmax, ladder_rho(rmin, rmax, qlevels), qlevels);
+}
+
+// Ladder ratios of the fast kernel's log-space norms, computed for LPV tiles at once (the LPV
+// lanes of a vector would otherwise compute the same one): lane (v, s) holds the ratio of
+// vector v in tile g + s of the group starting at tile g, from headers loaded a group ahead,
+// and tile g + x reads it from lane LPV v + x.
+template <int D>
+struct LadderGroups {
+  double rho = 1.0;
+  u32x2 next = {0u, 0u};
+  __device__ __forceinline__ void load(const DecodeArgs& a, const WaveState<D>& w,
+                                       const uint8_t* hdr_plane, uint32_t tile, uint32_t last) {
+    const TilePos p = tile_pos(a, min(tile + (uint32_t)w.sub, last) * WaveState<D>::VPW,
+                               w.vslot);
+    next = *(const u32x2*)(hdr_plane + (uint64_t)p.slot * 8);
+  }
+  // the ratio for tile `tile`, x = tile - (first tile of its group)
+  __device__ __forceinline__ double at(const DecodeArgs& a, const WaveState<D>& w, uint32_t tile,
+                                       uint32_t x, uint32_t last, uint32_t qlevels) {
+    constexpr int LPV = WaveState<D>::LPV;
+    if (x == 0) {
+      rho = ladder_rho(__uint_as_float(next.x), __uint_as_float(next.y), qlevels);
+      load(a, w, w.plane[2], tile + LPV, last);
+    }
+    return __shfl(rho, w.lane - w.sub + (int)x);
+  }
+};
 
 template <bool F32OUT>
 struct OutWords {
@@ -255,7 +288,7 @@ __device__ __forceinline__ TileCodes<WA, NB> load_tile_codes(const DecodeArgs& a
 template <int D, bool F32OUT, int WA, int NB>
 __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState<D>& w,
                                             uint32_t* stg, const TileCodes<WA, NB>& c,
-                                            uint32_t tile) {
+                                            uint32_t tile, double rho) {
   constexpr uint32_t kLevels = (1u << NB) - 1u;
   uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
   unpack16_index<WA>(c.ang, kc);
@@ -269,7 +302,7 @@ __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState
 #pragma unroll
     for (int i = 0; i < kPairsPerLane; ++i) r[i] = __builtin_fmaf((float)qc[i], step, rmin);
   } else {
-    const float* tab = build_log_levels<D>(w, (float*)stg, rmin, rmax, kLevels);
+    const float* tab = build_log_levels<D>(w, (float*)stg, rmin, rmax, rho, kLevels);
 #pragma unroll
     for (int i = 0; i < kPairsPerLane; ++i) r[i] = tab[qc[i]];
   }
@@ -288,18 +321,30 @@ __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState
 template <int D, bool F32OUT, bool MULTI, int WA, int NB>
 __device__ void decode_tiles_prefetch(const DecodeArgs& a, const WaveState<D>& w, uint32_t* stg,
                                       uint32_t tile0, uint32_t ntiles) {
+  constexpr int LPV = WaveState<D>::LPV;
+  constexpr uint32_t kLevels = (1u << NB) - 1u;
   const uint32_t last = tile0 + ntiles - 1;
   TileCodes<WA, NB> ca = load_tile_codes<D, WA, NB>(a, w, tile0);
   if constexpr (!MULTI) {
-    decode_tile<D, F32OUT>(a, w, stg, ca, tile0);
+    const float rmin = __uint_as_float(ca.hdr.x), rmax = __uint_as_float(ca.hdr.y);
+    decode_tile<D, F32OUT>(a, w, stg, ca, tile0,
+                           NB == 8 ? 1.0 : ladder_rho(rmin, rmax, kLevels));
     return;
   }
+  LadderGroups<D> lg;
+  if constexpr (NB != 8) lg.load(a, w, w.plane[2], tile0, last);
   for (uint32_t t = tile0; t <= last; t += 2) {
     const uint32_t t1 = min(t + 1, last);
     const TileCodes<WA, NB> cb = load_tile_codes<D, WA, NB>(a, w, t1);
-    decode_tile<D, F32OUT>(a, w, stg, ca, t);
+    double rho = 1.0;
+    if constexpr (NB != 8) rho = lg.at(a, w, t, (t - tile0) % LPV, last, kLevels);
+    decode_tile<D, F32OUT>(a, w, stg, ca, t, rho);
     ca = load_tile_codes<D, WA, NB>(a, w, min(t + 2, last));
-    decode_tile<D, F32OUT>(a, w, stg, cb, t1);
+    // t1 == t (the last tile again) keeps the ratio of tile t
+    if constexpr (NB != 8) {
+      if (t1 != t) rho = lg.at(a, w, t1, (t1 - tile0) % LPV, last, kLevels);
+    }
+    decode_tile<D, F32OUT>(a, w, stg, cb, t1, rho);
   }
 }
 
