@@ -264,6 +264,18 @@ tvq_status tvq_make_trig_table(int32_t n, float* cos_out, float* sin_out);
  * cos_out[k] = RN32(cos(2 pi k/n) / sqrt(d)), sin_out[k] likewise.  Host-only. */
 tvq_status tvq_make_decode_table(int32_t n, int32_t head_dim, float* cos_out, float* sin_out);
 
+/* The angle bins the encode kernels read for an n-bin codebook, n a power of two in
+ * [16, 256] (Algorithm 1: k = round(n theta / 2 pi) mod n, round = floor(u + 1/2)).  A pair
+ * (a, b) is placed by p' = sign(a) b / (|a| + |b|) in [-1, 1]: for each sign of a (h = 0 for a
+ * sign bit of 0, h = 1 for 1) p' moves monotonically over half a turn of angles.  With
+ * K = n - 3 equal cells of [-1, 1], entry h n + i covers: i = 0, p' < -1 (a rounding
+ * overshoot); i = 1 .. K, cell i - 1, p' in [-1 + 2 (i - 1) / K, -1 + 2 i / K); i = K + 1,
+ * p' >= 1; i > K + 1 repeats entry K + 1.  code_out[h n + i] is the code at the entry's lowest
+ * p'; bound_out[h n + i] the fp32 rounding of the p' of the one bin boundary inside the cell,
+ * from which the code is one more (mod n), or 3 where the cell holds none.  Both arrays hold
+ * 2 n entries.  Host-only; TVQ_ERR_INVALID_ARG for other n or null pointers. */
+tvq_status tvq_make_angle_bins(int32_t n, uint32_t* code_out, float* bound_out);
+
 /* Layout of a configuration without creating a codec (same result as tvq_cache_layout). */
 tvq_status tvq_layout_for_config(const tvq_config* cfg, int64_t batch, int64_t capacity_tokens,
                                  tvq_layout* out);

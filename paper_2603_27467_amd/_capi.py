@@ -107,6 +107,8 @@ def load_library():
     L.tvq_make_trig_table.argtypes = [i32, vp, vp]
     L.tvq_make_decode_table.restype = ctypes.c_int
     L.tvq_make_decode_table.argtypes = [i32, i32, vp, vp]
+    L.tvq_make_angle_bins.restype = ctypes.c_int
+    L.tvq_make_angle_bins.argtypes = [i32, vp, vp]
     L.tvq_layout_for_config.restype = ctypes.c_int
     L.tvq_layout_for_config.argtypes = [ctypes.POINTER(tvq_config), i64, i64,
                                         ctypes.POINTER(tvq_layout)]
@@ -264,6 +266,16 @@ def tvq_make_decode_table(n: int, head_dim: int):
                                                 s.ctypes.data_as(ctypes.c_void_p)),
            "tvq_make_decode_table")
     return c, s
+
+
+def tvq_make_angle_bins(n: int):
+    """(code, bound) arrays of 2 n entries: the angle bins the encode kernels read."""
+    code = np.zeros(2 * n, np.uint32)
+    bound = np.zeros(2 * n, np.float32)
+    _check(load_library().tvq_make_angle_bins(n, code.ctypes.data_as(ctypes.c_void_p),
+                                              bound.ctypes.data_as(ctypes.c_void_p)),
+           "tvq_make_angle_bins")
+    return code, bound
 
 
 def tvq_make_trig_table(n: int):

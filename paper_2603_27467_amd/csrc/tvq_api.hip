@@ -25,6 +25,7 @@ struct tvq_codec {
   tvq::SegParams* d_segs = nullptr;
   uint32_t* d_sign_masks = nullptr;
   float* d_lut = nullptr;
+  uint32_t* d_abins = nullptr;               // angle bins of n = 64, then n = 256 (pairs)
   uint32_t* d_seg_lists = nullptr;           // fast-format segment ids, then the others
   uint32_t n_fast = 0, n_generic = 0;
 };
@@ -256,6 +257,57 @@ tvq_status tvq_make_trig_table(int32_t n, float* cos_out, float* sin_out) {
   return TVQ_OK;
 }
 
+// Angle bins of an n-bin codebook (n a power of two, 16..256) over the direction parameter
+// p' = sign(a) b / (|a| + |b|), one half of the table per sign of a.  In each half p' runs
+// from -1 to 1 while the angle runs monotonically over a half turn (a >= 0: -1/4 .. 1/4 turn;
+// a < 0: 1/4 .. 3/4 turn), and K = n - 3 equal cells of [-1, 1] are narrow enough (the angle
+// moves by at most 2 rad per unit of p', a bin is 2 pi / n wide) that each holds at most one
+// bin boundary.  Entry i of a half: i = 0 is p' below -1 (a rounding overshoot), i = 1 .. K
+// is cell i - 1, i = K + 1 is p' = 1 and above, the rest repeat it.  code_out = the code of
+// the entry's lowest p' (round(n theta / 2 pi) mod n, round = floor(u + 1/2)); bound_out =
+// the p' of the bin boundary inside the cell, rounded to fp32, from which the code is one
+// more, or 3 where there is none.
+tvq_status tvq_make_angle_bins(int32_t n, uint32_t* code_out, float* bound_out) {
+  if (n < 16 || n > 256 || (n & (n - 1)) || !code_out || !bound_out) return TVQ_ERR_INVALID_ARG;
+  const double two_pi = 6.283185307179586;
+  const int32_t K = n - 3;
+  for (int h = 0; h < 2; ++h) {
+    // the angle coordinate u = n theta / 2 pi of p' in half h, continuous across the half
+    auto coord = [&](double pp) {
+      const double p = h ? -pp : pp;
+      const double r = 1.0 - std::fabs(p);
+      double th = std::atan2(p, h ? -r : r);
+      if (h && th < 0.0) th += two_pi;
+      return (double)n * th / two_pi;
+    };
+    auto code_of = [&](double u) {
+      long long k = (long long)std::floor(u + 0.5) % n;
+      if (k < 0) k += n;
+      return (uint32_t)k;
+    };
+    for (int32_t i = 0; i < n; ++i) {
+      const int32_t j = i <= K + 1 ? i - 1 : K;       // cell; -1 below, K the point p' = 1
+      const double lo = j < 0 ? -1.0 : -1.0 + 2.0 * j / K;
+      uint32_t code = code_of(coord(lo));
+      float bound = 3.0f;
+      if (j >= 0 && j < K) {
+        const double hi = -1.0 + 2.0 * (j + 1) / K;
+        const double u0 = coord(lo), u1 = coord(hi);
+        const double m = std::floor(u0 + 0.5);        // the next boundary is at u = m + 1/2
+        if (m + 0.5 < u1) {
+          const double th = two_pi * (m + 0.5) / (double)n;
+          const double cs = std::cos(th), sn = std::sin(th);
+          const double p = sn / (std::fabs(cs) + std::fabs(sn));
+          bound = (float)(h ? -p : p);
+        }
+      }
+      code_out[h * n + i] = code;
+      bound_out[h * n + i] = bound;
+    }
+  }
+  return TVQ_OK;
+}
+
 tvq_status tvq_make_decode_table(int32_t n, int32_t head_dim, float* cos_out, float* sin_out) {
   if (n < 2 || n > 4096 || head_dim < 1 || !cos_out || !sin_out) return TVQ_ERR_INVALID_ARG;
   const double root = std::sqrt((double)head_dim);
@@ -369,7 +421,22 @@ tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out) {
   const size_t seg_bytes = c->segs.size() * sizeof(tvq::SegParams);
   const size_t mask_bytes = masks.size() * sizeof(uint32_t);
   const size_t lut_bytes = lut.size() * sizeof(float);
+  // angle bins of the fast formats' codebooks, as (code, boundary bits) pairs
+  std::vector<uint32_t> abins;
+  for (int32_t n : {64, 256}) {
+    std::vector<uint32_t> code(2 * n);
+    std::vector<float> bound(2 * n);
+    tvq_make_angle_bins(n, code.data(), bound.data());
+    for (int32_t i = 0; i < 2 * n; ++i) {
+      uint32_t b;
+      std::memcpy(&b, &bound[i], 4);
+      abins.push_back(code[i]);
+      abins.push_back(b);
+    }
+  }
+  const size_t abin_bytes = abins.size() * sizeof(uint32_t);
   if (hipMalloc((void**)&c->d_segs, seg_bytes) != hipSuccess ||
+      hipMalloc((void**)&c->d_abins, abin_bytes) != hipSuccess ||
       hipMalloc((void**)&c->d_sign_masks, mask_bytes) != hipSuccess ||
       hipMalloc((void**)&c->d_lut, lut_bytes) != hipSuccess ||
       hipMalloc((void**)&c->d_seg_lists, list_bytes) != hipSuccess) {
@@ -379,6 +446,7 @@ tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out) {
   if (hipMemcpy(c->d_segs, c->segs.data(), seg_bytes, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(c->d_sign_masks, masks.data(), mask_bytes, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(c->d_lut, lut.data(), lut_bytes, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(c->d_abins, abins.data(), abin_bytes, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(c->d_seg_lists, lists.data(), list_bytes, hipMemcpyHostToDevice) != hipSuccess) {
     tvq_destroy(c);
     return TVQ_ERR_HIP;
@@ -392,6 +460,7 @@ void tvq_destroy(tvq_codec* c) {
   if (c->d_segs) (void)hipFree(c->d_segs);
   if (c->d_sign_masks) (void)hipFree(c->d_sign_masks);
   if (c->d_lut) (void)hipFree(c->d_lut);
+  if (c->d_abins) (void)hipFree(c->d_abins);
   if (c->d_seg_lists) (void)hipFree(c->d_seg_lists);
   delete c;
 }
@@ -433,6 +502,7 @@ static tvq_status encode_launch(const tvq_codec* c, tvq::EncodeArgs& a, const tv
                                 bool f32, void* stream) {
   a.segs = c->d_segs;
   a.sign_masks = c->d_sign_masks;
+  a.abins = c->d_abins;
   a.div_t = make_div((uint32_t)in->tokens);
   a.div_h = make_div((uint32_t)c->H);
   a.H = (uint32_t)c->H;

@@ -74,6 +74,34 @@ __device__ __forceinline__ uint32_t angle_bits(float a, float b, float nf, float
   return __float_as_uint(__builtin_fmaf(copysignf(h, b), nf, shift));
 }
 
+// Angle code of (a, b) for n = 2^WA (16..256) from the angle bins (tvq_make_angle_bins):
+// p' = sign(a) b / (|a| + |b|) (one reciprocal; the sign of a goes into it), its entry in the
+// half of the table for the sign of a (the fma rounds once, to floor((p' + 1) K / 2) + 1 with
+// K = n - 3 cells), and the entry's code plus one when p' is at or past the cell's boundary.
+// `lane_off` (n/2 on lanes holding -z) turns the code by half a turn; the packer keeps the low
+// WA bits, which is the mod n.  Same range requirement as angle_bits.
+typedef const u32x2 __attribute__((address_space(3)))* lds_bins_ptr;
+
+template <int WA>
+__device__ __forceinline__ uint32_t angle_code_bins(float a, float b, uint32_t bins_addr,
+                                                    uint32_t lane_off) {
+  constexpr float kHalfCells = 0.5f * (float)((1u << WA) - 3u);
+  const uint32_t sa = __float_as_uint(a) >> 31;
+  const float r = __uint_as_float(__float_as_uint(__builtin_amdgcn_rcpf(fabsf(a) + fabsf(b))) |
+                                  (sa << 31));
+  const float p = b * r;
+  // the fma's bits are kRoundShiftBits + (entry within the half)
+  const uint32_t bits = __float_as_uint(__builtin_fmaf(p, kHalfCells, kHalfCells + 0.5f +
+                                                                        kRoundShift));
+  // entry + kRoundShiftBits, then its LDS address against bins_addr (the table's address less
+  // 8 kRoundShiftBits, modulo 2^32): one instruction each (left to itself the compiler shifts
+  // and masks the sign of a separately and adds the parts in three more)
+  uint32_t idx;
+  asm("v_lshl_add_u32 %0, %1, %2, %3" : "=v"(idx) : "v"(sa), "i"(WA), "v"(bits));
+  const u32x2 e = *(lds_bins_ptr)(uintptr_t)(bins_addr + (idx << 3));
+  return e.x + (p >= __uint_as_float(e.y) ? 1u : 0u) + lane_off;
+}
+
 // Code in [0, n) from angle_bits with shift = 1.5*2^23 + off, off in {0, -n/2}: the signed
 // bin plus n lies in [0, 3n/2], and one conditional subtraction of n (as an unsigned min)
 // wraps it.
@@ -161,6 +189,9 @@ struct EncWave {
   uint8_t* plane[3];
   const uint32_t* sm;         // the lane's 16 sign-mask words, in this wave's LDS
   uint32_t* grp_lds;          // the wave's record buffer for group packing (generic kernel)
+  uint32_t bins_addr;         // LDS address of the segment's angle bins in this wave's rows
+                              // less 8 kRoundShiftBits, modulo 2^32 (fast formats)
+  uint32_t bins_off;          // n/2 on lanes holding -z (the half turn), else 0
   bool negated;               // the lane holds -z after the butterfly
   float shift;                // rounding shift with the half-turn of a negated lane removed
   uint32_t unneg;             // sign flip that undoes the negation (odd n)
@@ -168,10 +199,13 @@ struct EncWave {
 
 // MF: the lane mapping of the matrix-core front end (d = 128): vector slot lane % 16 and
 // element slice lane / 16, instead of a vector per lane quad.
+// bins_rows: per wave, room for the angle bins of n = 256 (the fast kernels), or null.
+constexpr int kBinRows = 2 * 256;
 template <int D, bool MF = false>
 __device__ __forceinline__ bool enc_wave_setup(const EncodeArgs& a, EncWave<D>& w,
                                                uint32_t (*sm_rows)[D / 2], uint32_t& tile0,
-                                               uint32_t& ntiles) {
+                                               uint32_t& ntiles,
+                                               u32x2 (*bins_rows)[kBinRows] = nullptr) {
   constexpr int LPV = EncWave<D>::LPV;
   constexpr int VPW = EncWave<D>::VPW;
   static_assert(!MF || D == 128, "the matrix-core front end is built for d = 128");
@@ -194,11 +228,21 @@ __device__ __forceinline__ bool enc_wave_setup(const EncodeArgs& a, EncWave<D>& 
   // the layer's sign masks into LDS (registers would hold them through the whole tile loop)
   uint32_t* row = sm_rows[threadIdx.x / kWave];
   if (lane < D / 2) row[lane] = a.sign_masks[(size_t)w.sp.layer * (D / 2) + lane];
+  w.bins_addr = 0;
+  w.bins_off = 0;
+  if (bins_rows != nullptr && (w.sp.n == 64 || w.sp.n == 256)) {
+    // the segment's angle bins (2 n entries) into the wave's rows
+    u32x2* brow = bins_rows[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];   // uniform
+    const u32x2* src = (const u32x2*)a.abins + (w.sp.n == 64 ? 0 : 2 * 64);
+    for (uint32_t e = (uint32_t)lane; e < 2 * w.sp.n; e += kWave) brow[e] = src[e];
+    w.bins_addr = (uint32_t)(uintptr_t)(lds_bins_ptr)brow - 8u * kRoundShiftBits;
+  }
   wave_lds_sync();
   w.sm = row + w.sub * 16;
   w.grp_lds = nullptr;
   w.negated = MF ? false : lane_negated<LPV>(w.sub);
   const bool odd_n = (w.sp.n & 1u) != 0;
+  w.bins_off = w.negated ? w.sp.n / 2 : 0u;
   w.shift = (w.negated && !odd_n) ? kRoundShift - 0.5f * w.sp.nf : kRoundShift;
   w.unneg = (w.negated && odd_n) ? 0x80000000u : 0u;
   return true;
@@ -493,7 +537,11 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
   // removed by starting the rounding shift n/2 lower; for odd n the pair is negated back.
   uint32_t kc[kPairsPerLane];
   if (fast) {
-    if (pow2) {
+    if constexpr (kFixed) {
+#pragma unroll
+      for (int i = 0; i < kPairsPerLane; ++i)
+        kc[i] = angle_code_bins<WA>(x[2 * i], x[2 * i + 1], w.bins_addr, w.bins_off);
+    } else if (pow2) {
 #pragma unroll
       for (int i = 0; i < kPairsPerLane; ++i)
         kc[i] = angle_bits(x[2 * i], x[2 * i + 1], nf, w.shift);
@@ -556,9 +604,10 @@ __device__ void encode_tiles_fast(const EncodeArgs& a, const EncWave<D>& w, uint
 template <bool MULTI>
 __global__ __launch_bounds__(kBlockThreads) void encode_mfma_kernel(EncodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t s_sm[kWavesPerBlock][64];
+  __shared__ u32x2 s_bins[kWavesPerBlock][kBinRows];
   EncWave<128> w;
   uint32_t tile0, ntiles;
-  if (!enc_wave_setup<128, true>(a, w, s_sm, tile0, ntiles)) return;
+  if (!enc_wave_setup<128, true>(a, w, s_sm, tile0, ntiles, s_bins)) return;
   const bool wide = w.sp.w == 8;
   if (w.sp.mode == 1) {
     if (wide) encode_tiles_fast<128, MULTI, 8, 8, false, true>(a, w, tile0, ntiles);
@@ -572,9 +621,10 @@ __global__ __launch_bounds__(kBlockThreads) void encode_mfma_kernel(EncodeArgs a
 template <int D, bool MULTI, bool PAGED>
 __global__ __launch_bounds__(kBlockThreads) void encode_fast_kernel(EncodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t s_sm[kWavesPerBlock][D / 2];
+  __shared__ u32x2 s_bins[kWavesPerBlock][kBinRows];
   EncWave<D> w;
   uint32_t tile0, ntiles;
-  if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles)) return;
+  if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles, s_bins)) return;
   const bool wide = w.sp.w == 8;
   if (w.sp.mode == 1) {
     if (wide) encode_tiles_fast<D, MULTI, 8, 8, PAGED>(a, w, tile0, ntiles);

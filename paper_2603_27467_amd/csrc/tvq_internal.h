@@ -72,6 +72,7 @@ struct EncodeArgs {
   const SegParams* segs;
   const uint32_t* seg_list;  // segment indices this launch covers
   const uint32_t* sign_masks;
+  const uint32_t* abins;  // angle bins (code, boundary) of n = 64 (2 x 64), then n = 256
   FastDiv div_t, div_h;  // by T (tokens in the call) and by H
   uint32_t H;
   uint32_t nvec;         // B * H * T vectors per segment

@@ -231,3 +231,72 @@ def test_layout_limits(tvq):
     assert lib.tvq_layout_for_config(ctypes.byref(cfg), 0, 16, ctypes.byref(lay)) == -1
     assert lib.tvq_layout_for_config(ctypes.byref(cfg), 1, 0, ctypes.byref(lay)) == -1
     assert lib.tvq_layout_for_config(ctypes.byref(cfg), 1 << 20, 1 << 12, ctypes.byref(lay)) == -1
+
+
+def _bins_code(code, bound, n, a, b, rcp_ulps=0):
+    """The fast encode kernels' table-driven angle code, step by step in fp32 (the reciprocal
+    correctly rounded, optionally moved by `rcp_ulps` units in the last place, as the
+    hardware's may be); also returns the table index, for bounds checks."""
+    a = np.asarray(a, np.float32)
+    b = np.asarray(b, np.float32)
+    s = (np.abs(a) + np.abs(b)).astype(np.float32)
+    r = (np.float32(1.0) / s).astype(np.float32)
+    for _ in range(abs(rcp_ulps)):
+        r = np.nextafter(r, np.float32(np.inf if rcp_ulps > 0 else 0)).astype(np.float32)
+    sa = a.view(np.uint32) >> np.uint32(31)
+    r = (r.view(np.uint32) | (sa << np.uint32(31))).view(np.float32)
+    p = (b * r).astype(np.float32)
+    half = (n - 3) / 2.0
+    # fma(p, K/2, K/2 + 1/2 + 1.5 * 2^23): exact in fp64, then rounded once to fp32
+    v = (p.astype(np.float64) * half + (half + 0.5 + 12582912.0)).astype(np.float32)
+    entry = v.view(np.uint32).astype(np.int64) - 0x4B400000
+    idx = entry + (sa.astype(np.int64) << int(np.log2(n)))
+    k = (code[idx] + (p >= bound[idx])) % n
+    return k.astype(np.int64), entry
+
+
+@pytest.mark.parametrize("n", [16, 64, 256])
+def test_angle_bins_reproduce_the_angle_code(tvq, orc, n):
+    """The angle bins of the fast encode kernels (p' = sign(a) b / (|a| + |b|), a cell of
+    [-1, 1] per sign of a, the code at the cell's low edge plus one past its boundary) give
+    the oracle's code round(n theta / 2 pi) mod n for every pair outside the 1e-6-turn flag
+    zone: random directions at scales 2^-40 .. 2^40, the neighbourhoods of every bin boundary,
+    the axes (signed zeros included) and the diagonals, with the reciprocal exact or one ulp
+    off either way.  The entry index stays inside the half table."""
+    code, bound = tvq.tvq_make_angle_bins(n)
+    assert code.shape == (2 * n,) and (code < n).all()
+    rng = np.random.default_rng(7 + n)
+    th = [rng.uniform(-np.pi, np.pi, 200000)]
+    edges = (np.arange(n) + 0.5) * 2 * np.pi / n
+    for off in (-1e-4, -1e-5, -3e-6, 0.0, 3e-6, 1e-5, 1e-4):
+        th.append(edges + off)
+    th.append(np.arange(8) * np.pi / 4)
+    th = np.concatenate(th)
+    scale = 2.0 ** rng.uniform(-40, 40, th.size)
+    a = (np.cos(th) * scale).astype(np.float32)
+    b = (np.sin(th) * scale).astype(np.float32)
+    z = np.float32(0.0)
+    axes_a = np.array([1, -1, z, -z, 3e-20, -3e-20, 1, 1, -1, -1], np.float32)
+    axes_b = np.array([z, z, 1, -1, z, -z, -z, 1, 1, -1], np.float32)
+    a = np.concatenate([a, axes_a])
+    b = np.concatenate([b, axes_b])
+    u = n * np.arctan2(b.astype(np.float64), a.astype(np.float64)) / (2 * np.pi)
+    want = np.mod(np.floor(u + 0.5), n).astype(np.int64)
+    for i in rng.choice(u.size, 200, replace=False):
+        assert want[i] == orc.angle_code(float(u[i]), n)
+    ok = ~orc.angle_flags(u, n)
+    for ulps in (0, 1, -1):
+        got, entry = _bins_code(code, bound, n, a, b, ulps)
+        assert entry.min() >= 0 and entry.max() <= n - 2
+        bad = np.nonzero(ok & (got != want))[0]
+        assert bad.size == 0, (n, ulps, bad[:5], a[bad[:5]], b[bad[:5]], got[bad[:5]], want[bad[:5]])
+
+
+def test_angle_bins_reject_other_n(tvq):
+    lib = tvq.load_library()
+    buf = np.zeros(1024, np.uint32)
+    fb = np.zeros(1024, np.float32)
+    for n in (8, 48, 512, 0):
+        assert lib.tvq_make_angle_bins(n, buf.ctypes.data_as(ctypes.c_void_p),
+                                       fb.ctypes.data_as(ctypes.c_void_p)) == -1
+    assert lib.tvq_make_angle_bins(64, None, None) == -1
