@@ -5,8 +5,9 @@
 // consecutive pairs, uniform angle bins, per-vector min-max norm codes, bit-packing.
 //
 // A lane computes 32 consecutive elements of a vector (d/32 lanes per vector, 64/(d/32)
-// vectors per wave, a "tile").  No LDS, no barriers: every wave is independent.  Two kernels,
-// each launched over its own list of (layer, kind) segments:
+// vectors per wave, a "tile").  LDS holds per-wave tables only (the layer's sign masks, the
+// angle bins of the fast formats); no barriers: every wave is independent.  Two kernels, each
+// launched over its own list of (layer, kind) segments:
 //   encode_fast_kernel     bf16 input, n = 64 or 256 with 8-bit linear or 4-bit log norms,
 //                          every format constant known at compile time.  A wave encodes
 //                          several consecutive tiles, loading the next tile's input while it
@@ -19,9 +20,10 @@
 // The kernels are bound by VALU issue, so the per-pair path is kept branch-free and short:
 // codes are rounded by the 1.5*2^23 shift and handed to the packer as raw float bits, whose
 // low bits are the code (the packer masks them to the code width, which is the "mod n" for n
-// a power of two).  The two cross-lane butterfly stages take one instruction per element and
-// leave some lanes holding the negated transform; for the angle that is a half-turn rotation,
-// folded into the rounding shift.  Stores are unconditional: a lane past the end of the
+// a power of two); the fast formats look their angle codes up in a table of bins instead of
+// evaluating the angle.  The two cross-lane butterfly stages take one instruction per element
+// and leave some lanes holding the negated transform; for the angle that is a half-turn
+// rotation, folded into the rounding shift or added to the looked-up code.  Stores are unconditional: a lane past the end of the
 // segment works on the tile's first vector and stores the same bytes as that vector's own
 // lane, so no path of a tile loop skips a store (which would make the compiler wait for every
 // outstanding store before using a prefetched load).
@@ -74,13 +76,14 @@ __device__ __forceinline__ uint32_t angle_bits(float a, float b, float nf, float
   return __float_as_uint(__builtin_fmaf(copysignf(h, b), nf, shift));
 }
 
+typedef const u32x2 __attribute__((address_space(3)))* lds_bins_ptr;
+
 // Angle code of (a, b) for n = 2^WA (16..256) from the angle bins (tvq_make_angle_bins):
 // p' = sign(a) b / (|a| + |b|) (one reciprocal; the sign of a goes into it), its entry in the
 // half of the table for the sign of a (the fma rounds once, to floor((p' + 1) K / 2) + 1 with
 // K = n - 3 cells), and the entry's code plus one when p' is at or past the cell's boundary.
 // `lane_off` (n/2 on lanes holding -z) turns the code by half a turn; the packer keeps the low
 // WA bits, which is the mod n.  Same range requirement as angle_bits.
-typedef const u32x2 __attribute__((address_space(3)))* lds_bins_ptr;
 
 template <int WA>
 __device__ __forceinline__ uint32_t angle_code_bins(float a, float b, uint32_t bins_addr,
@@ -197,10 +200,11 @@ struct EncWave {
   uint32_t unneg;             // sign flip that undoes the negation (odd n)
 };
 
+constexpr int kBinRows = 2 * 256;    // angle-bin entries of n = 256, the largest fast n
+
 // MF: the lane mapping of the matrix-core front end (d = 128): vector slot lane % 16 and
-// element slice lane / 16, instead of a vector per lane quad.
-// bins_rows: per wave, room for the angle bins of n = 256 (the fast kernels), or null.
-constexpr int kBinRows = 2 * 256;
+// element slice lane / 16, instead of a vector per lane quad.  bins_rows: per wave, room for
+// the segment's angle bins (the fast kernels), or null.
 template <int D, bool MF = false>
 __device__ __forceinline__ bool enc_wave_setup(const EncodeArgs& a, EncWave<D>& w,
                                                uint32_t (*sm_rows)[D / 2], uint32_t& tile0,
@@ -534,7 +538,8 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
 
   // ---- angle codes ----
   // A lane holding -z sees every pair rotated by half a turn: for even n that is n/2 bins,
-  // removed by starting the rounding shift n/2 lower; for odd n the pair is negated back.
+  // added to the looked-up code or removed by starting the rounding shift n/2 lower; for odd
+  // n the pair is negated back.
   uint32_t kc[kPairsPerLane];
   if (fast) {
     if constexpr (kFixed) {
