@@ -23,10 +23,11 @@
 // a power of two); the fast formats look their angle codes up in a table of bins instead of
 // evaluating the angle.  The two cross-lane butterfly stages take one instruction per element
 // and leave some lanes holding the negated transform; for the angle that is a half-turn
-// rotation, folded into the rounding shift or added to the looked-up code.  Stores are unconditional: a lane past the end of the
-// segment works on the tile's first vector and stores the same bytes as that vector's own
-// lane, so no path of a tile loop skips a store (which would make the compiler wait for every
-// outstanding store before using a prefetched load).
+// rotation, folded into the rounding shift or added to the looked-up code.  Stores are
+// unconditional: a lane past the end of the segment works on the tile's first vector and
+// stores the same bytes as that vector's own lane, so no path of a tile loop skips a store
+// (which would make the compiler wait for every outstanding store before using a prefetched
+// load).
 #include <float.h>
 #include <hip/hip_runtime.h>
 
@@ -191,6 +192,8 @@ struct EncWave {
   int64_t layer_off;          // element offset of the layer and of the lane's 32 elements
   uint8_t* plane[3];
   const uint32_t* sm;         // the lane's 16 sign-mask words, in this wave's LDS
+  uint32_t* sm_row;           // the wave's sign-mask row (D/2 words), filled by stage_tables
+  u32x2* bins_row;            // the wave's angle-bin rows, or null
   uint32_t* grp_lds;          // the wave's record buffer for group packing (generic kernel)
   uint32_t bins_addr;         // LDS address of the segment's angle bins in this wave's rows
                               // less 8 kRoundShiftBits, modulo 2^32 (fast formats)
@@ -229,20 +232,17 @@ __device__ __forceinline__ bool enc_wave_setup(const EncodeArgs& a, EncWave<D>& 
   w.src = w.sp.kind ? a.v : a.k;
   w.layer_off = (int64_t)w.sp.layer * a.stride_l + w.sub * kElemsPerLane;
   for (int p = 0; p < 3; ++p) w.plane[p] = a.cache + a.n_slots * w.sp.pre[p];
-  // the layer's sign masks into LDS (registers would hold them through the whole tile loop)
-  uint32_t* row = sm_rows[threadIdx.x / kWave];
-  if (lane < D / 2) row[lane] = a.sign_masks[(size_t)w.sp.layer * (D / 2) + lane];
+  // the wave's LDS rows for the layer's sign masks (registers would hold them through the
+  // whole tile loop) and the segment's angle bins; stage_tables fills them
+  w.sm_row = sm_rows[threadIdx.x / kWave];
+  w.sm = w.sm_row + w.sub * 16;
+  w.bins_row = nullptr;
   w.bins_addr = 0;
   w.bins_off = 0;
   if (bins_rows != nullptr && (w.sp.n == 64 || w.sp.n == 256)) {
-    // the segment's angle bins (2 n entries) into the wave's rows
-    u32x2* brow = bins_rows[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];   // uniform
-    const u32x2* src = (const u32x2*)a.abins + (w.sp.n == 64 ? 0 : 2 * 64);
-    for (uint32_t e = (uint32_t)lane; e < 2 * w.sp.n; e += kWave) brow[e] = src[e];
-    w.bins_addr = (uint32_t)(uintptr_t)(lds_bins_ptr)brow - 8u * kRoundShiftBits;
+    w.bins_row = bins_rows[__builtin_amdgcn_readfirstlane(threadIdx.x / kWave)];   // uniform
+    w.bins_addr = (uint32_t)(uintptr_t)(lds_bins_ptr)w.bins_row - 8u * kRoundShiftBits;
   }
-  wave_lds_sync();
-  w.sm = row + w.sub * 16;
   w.grp_lds = nullptr;
   w.negated = MF ? false : lane_negated<LPV>(w.sub);
   const bool odd_n = (w.sp.n & 1u) != 0;
@@ -250,6 +250,19 @@ __device__ __forceinline__ bool enc_wave_setup(const EncodeArgs& a, EncWave<D>& 
   w.shift = (w.negated && !odd_n) ? kRoundShift - 0.5f * w.sp.nf : kRoundShift;
   w.unneg = (w.negated && odd_n) ? 0x80000000u : 0u;
   return true;
+}
+
+// Fill the wave's sign-mask row and angle bins (2 n entries of the segment's n).  Called after
+// the first tile's input load is issued, so the two loads' latencies overlap.
+template <int D>
+__device__ __forceinline__ void stage_tables(const EncodeArgs& a, const EncWave<D>& w) {
+  const int lane = threadIdx.x & (kWave - 1);
+  if (lane < D / 2) w.sm_row[lane] = a.sign_masks[(size_t)w.sp.layer * (D / 2) + lane];
+  if (w.bins_row != nullptr) {
+    const u32x2* src = (const u32x2*)a.abins + (w.sp.n == 64 ? 0 : 2 * 64);
+    for (uint32_t e = (uint32_t)lane; e < 2 * w.sp.n; e += kWave) w.bins_row[e] = src[e];
+  }
+  wave_lds_sync();
 }
 
 // A tile's input for one lane and the lane's cache slot.  A lane past the end of the segment
@@ -392,7 +405,7 @@ __device__ __forceinline__ float vector_max(float v) {
   }
 }
 
-template <int D, bool F32IN, int WA, int NB, bool PAGED, bool MF = false>
+template <int D, bool F32IN, int WA, int NB, bool PAGED, bool MF = false, bool BINS = false>
 __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D>& w,
                                             const TileIn<F32IN>& in) {
   static_assert(!MF || (D == 128 && !F32IN), "matrix-core front end: d = 128, bf16 input");
@@ -542,7 +555,7 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
   // n the pair is negated back.
   uint32_t kc[kPairsPerLane];
   if (fast) {
-    if constexpr (kFixed) {
+    if constexpr (kFixed && BINS) {
 #pragma unroll
       for (int i = 0; i < kPairsPerLane; ++i)
         kc[i] = angle_code_bins<WA>(x[2 * i], x[2 * i + 1], w.bins_addr, w.bins_off);
@@ -587,21 +600,24 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
 // last tile, so an odd count encodes the last tile twice (the same bytes to the same
 // addresses) and the loads past the end read lines already in cache.  Launches of one tile
 // per wave use the instantiation without the loop (a separate copy of the tile code inside
-// the same kernel would raise its register count).
+// the same kernel would raise its register count); it evaluates the angles (angle_bits)
+// rather than staging the bin table for a single tile, which made those short launches ~30%
+// slower.  Both give the exact code outside the flag zone.
 template <int D, bool MULTI, int WA, int NB, bool PAGED, bool MF = false>
 __device__ void encode_tiles_fast(const EncodeArgs& a, const EncWave<D>& w, uint32_t tile0,
                                   uint32_t ntiles) {
   const uint32_t last = tile0 + ntiles - 1;
   TileIn<false> ia = load_tile<D, false, PAGED>(a, w, tile0);
+  stage_tables<D>(a, w);
   if constexpr (!MULTI) {
-    encode_tile<D, false, WA, NB, PAGED, MF>(a, w, ia);
+    encode_tile<D, false, WA, NB, PAGED, MF, false>(a, w, ia);
     return;
   }
   for (uint32_t t = tile0; t <= last; t += 2) {
     const TileIn<false> ib = load_tile<D, false, PAGED>(a, w, min(t + 1, last));
-    encode_tile<D, false, WA, NB, PAGED, MF>(a, w, ia);
+    encode_tile<D, false, WA, NB, PAGED, MF, true>(a, w, ia);
     ia = load_tile<D, false, PAGED>(a, w, min(t + 2, last));
-    encode_tile<D, false, WA, NB, PAGED, MF>(a, w, ib);
+    encode_tile<D, false, WA, NB, PAGED, MF, true>(a, w, ib);
   }
 }
 
@@ -612,7 +628,7 @@ __global__ __launch_bounds__(kBlockThreads) void encode_mfma_kernel(EncodeArgs a
   __shared__ u32x2 s_bins[kWavesPerBlock][kBinRows];
   EncWave<128> w;
   uint32_t tile0, ntiles;
-  if (!enc_wave_setup<128, true>(a, w, s_sm, tile0, ntiles, s_bins)) return;
+  if (!enc_wave_setup<128, true>(a, w, s_sm, tile0, ntiles, MULTI ? s_bins : nullptr)) return;
   const bool wide = w.sp.w == 8;
   if (w.sp.mode == 1) {
     if (wide) encode_tiles_fast<128, MULTI, 8, 8, false, true>(a, w, tile0, ntiles);
@@ -629,7 +645,7 @@ __global__ __launch_bounds__(kBlockThreads) void encode_fast_kernel(EncodeArgs a
   __shared__ u32x2 s_bins[kWavesPerBlock][kBinRows];
   EncWave<D> w;
   uint32_t tile0, ntiles;
-  if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles, s_bins)) return;
+  if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles, MULTI ? s_bins : nullptr)) return;
   const bool wide = w.sp.w == 8;
   if (w.sp.mode == 1) {
     if (wide) encode_tiles_fast<D, MULTI, 8, 8, PAGED>(a, w, tile0, ntiles);
@@ -649,7 +665,9 @@ __global__ __launch_bounds__(kBlockThreads) void encode_generic_kernel(EncodeArg
   uint32_t tile0, ntiles;
   if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles)) return;
   w.grp_lds = s_grp[threadIdx.x / kWave];
-  encode_tile<D, F32IN, 0, 0, PAGED>(a, w, load_tile<D, F32IN, PAGED>(a, w, tile0));
+  const TileIn<F32IN> in = load_tile<D, F32IN, PAGED>(a, w, tile0);
+  stage_tables<D>(a, w);
+  encode_tile<D, F32IN, 0, 0, PAGED>(a, w, in);
 }
 
 template <int D, bool PAGED>
