@@ -15,10 +15,12 @@
 // Split over tokens (split-K): a chunk wave takes `chunk_tokens` tokens of one (sequence, KV
 // head) for up to four of the G query heads (G > 4 runs in passes of balanced size).
 //   prologue  q^_g = scale * log2(e) * W D q_g into LDS (the d/32 lanes of vector slot g)
-//   per tile  of 64/(d/32) tokens, one token per vector slot: y'_K from the K codes, the
-//             scores s_g = q^_g . y'_K, then y'_V from the V codes and, per head,
-//             acc_g += 2^(s_g - m_g) y'_V and l_g += 2^(s_g - m_g)
-//   out       (m, l, acc[d]) per query head and chunk into the workspace, summed over the slots
+//   per tile  y'_K from the K codes, the scores s_g = q^_g . y'_K, then y'_V from the V codes
+//             and, per head, acc_g += 2^(s_g - m_g) y'_V and l_g += 2^(s_g - m_g)
+//   out       (m, l, acc[d]) per query head and chunk into the workspace
+// Two chunk kernels: attn_chunk_kernel (d = 64) does the contractions as per-lane FMAs, one
+// token per vector slot of a 32-token tile; attn_mfma_chunk_kernel (d = 128) does them on
+// the matrix cores, 16 tokens x 4 heads per tile (its layouts are described where it is).
 // m_g is a reference point shared by the wave, not the running maximum: it is raised (and acc,
 // l rescaled) only when a score exceeds it by more than kLazyLog2, so every weight stays below
 // 2^kLazyLog2 and the rescale runs on a few tiles of a chunk.  The merge kernel combines the
@@ -410,12 +412,13 @@ __global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
 //           tokens x 4 heads; the four element slices s are summed across lanes, so every row
 //           of 16 lanes holds all 16 scores and lane l the weights of tokens 4 tq .. 4 tq + 3
 //           (tq = (l / 4) % 4) for head j.
-//   values  the V codes of the tile go through LDS so that lane l reads pair l (elements 2l,
-//           2l + 1) of any token; in each of 16 steps block b = l / 4 adds y'_V(k, pair
-//           4b + r) * p(k, head j) for one token k, the blocks of a row taking their tokens in
-//           rotated order so that the weights move by row rotations instead of LDS; lane
-//           4b + j accumulates pairs 4b .. 4b + 3 of head j: 8 registers for the whole
-//           (4 heads x 128 elements) accumulator.
+//   values  the lane that loaded a token's V codes (token l % 16, slice s) rebuilds y'_V of
+//           its 16 pairs and stores them to LDS pair-major, so that lane l reads pair l
+//           (elements 2l, 2l + 1) of any token; in each of 16 steps block b = l / 4 adds
+//           y'_V(k, pair 4b + r) * p(k, head j) for one token k, the blocks of a row taking
+//           their tokens in rotated order so that the weights move by row rotations instead
+//           of LDS; lane 4b + j accumulates pairs 4b .. 4b + 3 of head j: 8 registers for the
+//           whole (4 heads x 128 elements) accumulator.
 // The reference point m, the sum l and the accumulator of head j live on the lanes with
 // lane % 4 == j.  y' is rebuilt exactly as decode rebuilds it.
 template <int KW, int KN, int VW, int VN>
