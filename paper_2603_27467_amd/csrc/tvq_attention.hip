@@ -627,26 +627,52 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
   const uint32_t j = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock +
                                                      threadIdx.x / kWave);
   if (j >= a.B * a.Hq) return;
-  const float* ml = a.ws_ml + (size_t)j * a.n_chunks * 2;
+  // Chunks are taken kMergeBatch at a time per slot with every load of a batch issued before
+  // its first use, so a slot waits for one memory latency per batch rather than per chunk.
+  constexpr uint32_t kMergeBatch = 4;
+  const float2* ml = (const float2*)(a.ws_ml + (size_t)j * a.n_chunks * 2);
   float M = -INFINITY;
-  for (uint32_t c = vslot; c < a.n_chunks; c += VPW) M = fmaxf(M, ml[2 * c]);
+  for (uint32_t c0 = vslot; c0 < a.n_chunks; c0 += kMergeBatch * VPW) {
+    float mb[kMergeBatch];
+#pragma unroll
+    for (uint32_t k = 0; k < kMergeBatch; ++k) {
+      const uint32_t c = c0 + k * VPW;
+      mb[k] = c < a.n_chunks ? ml[c].x : -INFINITY;
+    }
+#pragma unroll
+    for (uint32_t k = 0; k < kMergeBatch; ++k) M = fmaxf(M, mb[k]);
+  }
   M = wave_max(M);
   float L = 0.0f;
   float x[kElemsPerLane];
 #pragma unroll
   for (int i = 0; i < kElemsPerLane; ++i) x[i] = 0.0f;
   const float* acc = a.ws_acc + (size_t)j * a.n_chunks * D + sub * kElemsPerLane;
-  for (uint32_t c = vslot; c < a.n_chunks; c += VPW) {
-    // empty chunks carry m = -inf and weight 0; with no token at all, M is -inf too
-    const float f = M == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(ml[2 * c] - M);
-    L = __builtin_fmaf(ml[2 * c + 1], f, L);
+  for (uint32_t c0 = vslot; c0 < a.n_chunks; c0 += kMergeBatch * VPW) {
+    float2 mlb[kMergeBatch];
+    float4 vb[kMergeBatch][kElemsPerLane / 4];
 #pragma unroll
-    for (int i = 0; i < kElemsPerLane; i += 4) {
-      const float4 v = *(const float4*)(acc + (size_t)c * D + i);
-      x[i] = __builtin_fmaf(v.x, f, x[i]);
-      x[i + 1] = __builtin_fmaf(v.y, f, x[i + 1]);
-      x[i + 2] = __builtin_fmaf(v.z, f, x[i + 2]);
-      x[i + 3] = __builtin_fmaf(v.w, f, x[i + 3]);
+    for (uint32_t k = 0; k < kMergeBatch; ++k) {
+      const uint32_t c = min(c0 + k * VPW, a.n_chunks - 1);     // in bounds; weight 0 below
+      mlb[k] = ml[c];
+#pragma unroll
+      for (int i = 0; i < kElemsPerLane / 4; ++i)
+        vb[k][i] = *(const float4*)(acc + (size_t)c * D + 4 * i);
+    }
+#pragma unroll
+    for (uint32_t k = 0; k < kMergeBatch; ++k) {
+      // empty chunks carry m = -inf and weight 0; with no token at all, M is -inf too; a
+      // batch entry past the last chunk also gets weight 0
+      const bool live = c0 + k * VPW < a.n_chunks && M != -INFINITY;
+      const float f = live ? __builtin_amdgcn_exp2f(mlb[k].x - M) : 0.0f;
+      L = __builtin_fmaf(mlb[k].y, f, L);
+#pragma unroll
+      for (int i = 0; i < kElemsPerLane / 4; ++i) {
+        x[4 * i] = __builtin_fmaf(vb[k][i].x, f, x[4 * i]);
+        x[4 * i + 1] = __builtin_fmaf(vb[k][i].y, f, x[4 * i + 1]);
+        x[4 * i + 2] = __builtin_fmaf(vb[k][i].z, f, x[4 * i + 2]);
+        x[4 * i + 3] = __builtin_fmaf(vb[k][i].w, f, x[4 * i + 3]);
+      }
     }
   }
   L = slot_sum<LPV>(L);
