@@ -627,23 +627,16 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
   const uint32_t j = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock +
                                                      threadIdx.x / kWave);
   if (j >= a.B * a.Hq) return;
+  // The layer's sign masks are loaded first, to arrive under the chunk reads.
+  uint32_t sm[16];
+  load_words<16>(a.sign_masks + (size_t)a.layer * (D / 2) + sub * 16, sm);
   // Chunks are taken kMergeBatch at a time per slot with every load of a batch issued before
   // its first use, so a slot waits for one memory latency per batch rather than per chunk.
+  // Each slot keeps its own reference point Ms (raised batch by batch, the slot's sums
+  // rescaled), and the slots are brought to the wave's M before they are added.
   constexpr uint32_t kMergeBatch = 4;
   const float2* ml = (const float2*)(a.ws_ml + (size_t)j * a.n_chunks * 2);
-  float M = -INFINITY;
-  for (uint32_t c0 = vslot; c0 < a.n_chunks; c0 += kMergeBatch * VPW) {
-    float mb[kMergeBatch];
-#pragma unroll
-    for (uint32_t k = 0; k < kMergeBatch; ++k) {
-      const uint32_t c = c0 + k * VPW;
-      mb[k] = c < a.n_chunks ? ml[c].x : -INFINITY;
-    }
-#pragma unroll
-    for (uint32_t k = 0; k < kMergeBatch; ++k) M = fmaxf(M, mb[k]);
-  }
-  M = wave_max(M);
-  float L = 0.0f;
+  float Ms = -INFINITY, L = 0.0f;
   float x[kElemsPerLane];
 #pragma unroll
   for (int i = 0; i < kElemsPerLane; ++i) x[i] = 0.0f;
@@ -659,12 +652,24 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
       for (int i = 0; i < kElemsPerLane / 4; ++i)
         vb[k][i] = *(const float4*)(acc + (size_t)c * D + 4 * i);
     }
+    // empty chunks carry m = -inf and weight 0, and so does a batch entry past the last chunk
+    float mk[kMergeBatch];
+    float bm = Ms;
 #pragma unroll
     for (uint32_t k = 0; k < kMergeBatch; ++k) {
-      // empty chunks carry m = -inf and weight 0; with no token at all, M is -inf too; a
-      // batch entry past the last chunk also gets weight 0
-      const bool live = c0 + k * VPW < a.n_chunks && M != -INFINITY;
-      const float f = live ? __builtin_amdgcn_exp2f(mlb[k].x - M) : 0.0f;
+      mk[k] = c0 + k * VPW < a.n_chunks ? mlb[k].x : -INFINITY;
+      bm = fmaxf(bm, mk[k]);
+    }
+    if (bm != -INFINITY) {
+      const float sc = __builtin_amdgcn_exp2f(Ms - bm);      // 0 while Ms is -inf
+      L *= sc;
+#pragma unroll
+      for (int i = 0; i < kElemsPerLane; ++i) x[i] *= sc;
+      Ms = bm;
+    }
+#pragma unroll
+    for (uint32_t k = 0; k < kMergeBatch; ++k) {
+      const float f = mk[k] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mk[k] - Ms);
       L = __builtin_fmaf(mlb[k].y, f, L);
 #pragma unroll
       for (int i = 0; i < kElemsPerLane / 4; ++i) {
@@ -675,6 +680,12 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
       }
     }
   }
+  // with no token at all M is -inf and every slot contributes 0
+  const float M = wave_max(Ms);
+  const float g = Ms == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(Ms - M);
+  L *= g;
+#pragma unroll
+  for (int i = 0; i < kElemsPerLane; ++i) x[i] *= g;
   L = slot_sum<LPV>(L);
 #pragma unroll
   for (int i = 0; i < kElemsPerLane; ++i) x[i] = slot_sum<LPV>(x[i]);
@@ -683,8 +694,6 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
   for (int i = 0; i < kElemsPerLane; ++i) x[i] *= inv;
   fwht_in_lane(x);
   fwht_cross_lane_signed<LPV>(x, sub);            // sigma * W A / L
-  uint32_t sm[16];
-  load_words<16>(a.sign_masks + (size_t)a.layer * (D / 2) + sub * 16, sm);
   const uint32_t neg = lane_negated<LPV>(sub) ? 0x80008000u : 0u;
   if (vslot != 0) return;
   const uint64_t elem = (uint64_t)j * D + sub * kElemsPerLane;
