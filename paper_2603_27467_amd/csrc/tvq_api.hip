@@ -5,6 +5,7 @@
 // on the host and enqueue exactly one kernel each, with no allocation and no synchronization.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -22,6 +23,7 @@ struct tvq_codec {
   std::vector<tvq::SegParams> segs;          // [2L]
   uint64_t rec_total = 0;                    // record bytes of all planes, per slot
   int device = 0;
+  int64_t attn_slots = 0;                    // chunk waves the device holds at once (d = 64, 128)
   tvq::SegParams* d_segs = nullptr;
   uint32_t* d_sign_masks = nullptr;
   float* d_lut = nullptr;
@@ -409,6 +411,16 @@ tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out) {
     delete c;
     return TVQ_ERR_HIP;
   }
+  if (d == 64 || d == 128) {
+    int n_cu = 0;
+    const int blocks = tvq_attention_blocks_per_cu(d);
+    if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, c->device) !=
+            hipSuccess || n_cu < 1 || blocks < 1) {
+      delete c;
+      return TVQ_ERR_HIP;
+    }
+    c->attn_slots = (int64_t)n_cu * blocks * tvq::kWavesPerBlock;
+  }
   // segment lists of the two decode kernels
   std::vector<uint32_t> lists;
   for (uint32_t i = 0; i < c->segs.size(); ++i)
@@ -690,15 +702,18 @@ tvq_status tvq_decode_paged(const tvq_codec* c, const void* pool, const tvq_layo
   return decode_launch(c, a, out, out_dtype, k_out, v_out, stream);
 }
 
-// Tokens per chunk wave: a power of two (at least 4 tiles) chosen so that a launch has about
-// kAttnTargetWaves chunk waves, at most `max_chunk` (4096; 64 blocks of a paged pool).
-static uint32_t attn_chunk_tokens(int d, int64_t waves_per_chunk_row, int64_t t_end,
+// Tokens per chunk wave.  The rows (sequence, KV head, pass over the query heads) split into
+// equal chunks so that the launch has about kAttnRounds x `slots` chunk waves (`slots`: the
+// chunk waves the device holds at once).  A chunk holds whole tile pairs, at least four tiles,
+// and at most `max_chunk` tokens.
+static uint32_t attn_chunk_tokens(int d, int64_t rows, int64_t t_end, int64_t slots,
                                   int64_t max_chunk) {
   const int64_t vpw = tvq::kWave / (d / tvq::kElemsPerLane);
-  const int64_t want = waves_per_chunk_row * t_end / (int64_t)tvq::kAttnTargetWaves;
-  int64_t ch = 4 * vpw;
-  while (ch < max_chunk && 2 * ch <= want) ch *= 2;
-  return (uint32_t)ch;
+  const int64_t step = 2 * vpw;
+  const int64_t per_row = std::max<int64_t>(1, slots * tvq::kAttnRounds / rows);
+  int64_t ch = (t_end + per_row - 1) / per_row;
+  ch = std::max<int64_t>((ch + step - 1) / step * step, 4 * vpw);
+  return (uint32_t)std::min(ch, max_chunk / step * step);
 }
 
 struct AttnPlan {
@@ -717,9 +732,10 @@ static tvq_status attn_plan(const tvq_codec* c, int64_t batch, int32_t num_q_hea
   if (p->G > tvq::kAttnMaxGroup) return TVQ_ERR_UNSUPPORTED;
   p->n_pass = (p->G + tvq::kAttnPassHeads - 1) / tvq::kAttnPassHeads;
   p->pass_heads = (p->G + p->n_pass - 1) / p->n_pass;          // balanced passes
-  const int64_t max_chunk = block_tokens > 0 && 64 * block_tokens < 4096 ? 64 * block_tokens
-                                                                          : 4096;
-  p->chunk = attn_chunk_tokens(c->d, batch * c->H * p->n_pass, t_end, max_chunk);
+  // paged: a chunk may start inside a block, so 63 blocks' tokens keep it within the 64
+  // blocks whose pool indices one wave fetches
+  const int64_t max_chunk = block_tokens > 0 ? std::min<int64_t>(4096, 63 * block_tokens) : 4096;
+  p->chunk = attn_chunk_tokens(c->d, batch * c->H * p->n_pass, t_end, c->attn_slots, max_chunk);
   p->n_chunks = (uint32_t)((t_end + p->chunk - 1) / p->chunk);
   const int64_t parts = batch * num_q_heads * (int64_t)p->n_chunks;
   p->acc_bytes = (parts * c->d * 4 + 255) / 256 * 256;

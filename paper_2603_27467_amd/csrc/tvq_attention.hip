@@ -13,7 +13,8 @@
 // form it (same tables, same fp32 operation order).
 //
 // Split over tokens (split-K): a chunk wave takes `chunk_tokens` tokens of one (sequence, KV
-// head) for up to four of the G query heads (G > 4 runs in passes of balanced size).
+// head) for up to four of the G query heads (G > 4 runs in passes of balanced size).  The host
+// sizes the chunks so that a launch has about one chunk wave per wave slot of the device.
 //   prologue  q^_g = scale * log2(e) * W D q_g into LDS (the d/32 lanes of vector slot g)
 //   per tile  y'_K from the K codes, the scores s_g = q^_g . y'_K, then y'_V from the V codes
 //             and, per head, acc_g += 2^(s_g - m_g) y'_V and l_g += 2^(s_g - m_g)
@@ -734,6 +735,42 @@ void launch_chunk_v(const AttnArgs& a, int vf, dim3 grid, hipStream_t s) {
   }
 }
 
+// Fewest workgroups of the chunk kernel per compute unit over the four value formats that
+// follow key format KF; 0 on a HIP error.
+template <int D, int KF>
+int chunk_blocks_v() {
+  constexpr int KW = (KF & 1) ? 8 : 6, KN = (KF & 2) ? 4 : 8;
+  const void* f[4];
+  if constexpr (D == 128) {
+    f[0] = (const void*)attn_mfma_chunk_kernel<KW, KN, 6, 8>;
+    f[1] = (const void*)attn_mfma_chunk_kernel<KW, KN, 8, 8>;
+    f[2] = (const void*)attn_mfma_chunk_kernel<KW, KN, 6, 4>;
+    f[3] = (const void*)attn_mfma_chunk_kernel<KW, KN, 8, 4>;
+  } else {
+    f[0] = (const void*)attn_chunk_kernel<D, KW, KN, 6, 8>;
+    f[1] = (const void*)attn_chunk_kernel<D, KW, KN, 8, 8>;
+    f[2] = (const void*)attn_chunk_kernel<D, KW, KN, 6, 4>;
+    f[3] = (const void*)attn_chunk_kernel<D, KW, KN, 8, 4>;
+  }
+  int fewest = 1 << 30;
+  for (const void* k : f) {
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k, kBlockThreads, 0) != hipSuccess)
+      return 0;
+    fewest = nb < fewest ? nb : fewest;
+  }
+  return fewest;
+}
+
+template <int D>
+int chunk_blocks() {
+  const int b[4] = {chunk_blocks_v<D, 0>(), chunk_blocks_v<D, 1>(), chunk_blocks_v<D, 2>(),
+                    chunk_blocks_v<D, 3>()};
+  int fewest = b[0];
+  for (int x : b) fewest = x < fewest ? x : fewest;
+  return fewest;
+}
+
 template <int D>
 void launch_chunk_kv(const AttnArgs& a, int kf, int vf, dim3 grid, hipStream_t s) {
   switch (kf) {
@@ -746,6 +783,11 @@ void launch_chunk_kv(const AttnArgs& a, int kf, int vf, dim3 grid, hipStream_t s
 
 }  // namespace
 }  // namespace tvq
+
+int tvq_attention_blocks_per_cu(int d) {
+  const int nb = d == 128 ? tvq::chunk_blocks<128>() : d == 64 ? tvq::chunk_blocks<64>() : 0;
+  return nb > 0 ? nb : -1;
+}
 
 int tvq_launch_attention(const tvq::AttnArgs& a, int d, int k_format, int v_format, int o_f32,
                          void* stream) {

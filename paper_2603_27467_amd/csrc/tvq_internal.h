@@ -132,7 +132,9 @@ struct AttnArgs {
 
 constexpr int kAttnPassHeads = 4;           // accumulators of 4 query heads per wave
 constexpr uint32_t kAttnMaxGroup = 64;      // query heads per KV head
-constexpr uint64_t kAttnTargetWaves = 8192; // chunk waves per launch the token split aims at
+// The token split gives a launch about kAttnRounds times as many chunk waves as the device
+// holds at once, so that every wave slot stays busy until the launch's end.
+constexpr int64_t kAttnRounds = 1;
 
 // Segments the multi-tile encode and decode kernels handle: n = 64 or 256 (6- or 8-bit angle
 // codes, every code a valid bin) with 8-bit linear or 4-bit log-space norms.  Other formats go
@@ -154,3 +156,6 @@ int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, u
 // k_format / v_format: bit 0 set for 8-bit angle codes (n = 256), bit 1 for 4-bit log norms.
 int tvq_launch_attention(const tvq::AttnArgs& a, int d, int k_format, int v_format, int o_f32,
                          void* stream);
+// Chunk-kernel workgroups of head dimension d that one compute unit holds at once (the
+// fewest over the formats), or -1 on a HIP error.
+int tvq_attention_blocks_per_cu(int d);
