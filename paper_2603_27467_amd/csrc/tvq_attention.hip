@@ -122,7 +122,7 @@ __device__ __forceinline__ void code_vector(const TileCodes<WA, NB>& c, const fl
   const float rmin = __uint_as_float(c.hdr.x), rmax = __uint_as_float(c.hdr.y);
   float r[kPairsPerLane];
   if constexpr (NB == 8) {
-    const float step = rmax == rmin ? 0.0f : (rmax - rmin) / (float)kLevels;
+    const float step = linear_step255(rmin, rmax);
 #pragma unroll
     for (int i = 0; i < kPairsPerLane; ++i) r[i] = __builtin_fmaf((float)qc[i], step, rmin);
   } else {
@@ -539,7 +539,7 @@ __global__ __launch_bounds__(kBlockThreads, 3) void attn_mfma_chunk_kernel(AttnA
       float step = 0.0f;
       if constexpr (VN == 8) {
         unpack16<VN>(c.v.nrm, qc);
-        step = rmax == rmin ? 0.0f : (rmax - rmin) / (float)kVLevels;
+        step = linear_step255(rmin, rmax);
       } else {
         unpack16_index<VN>(c.v.nrm, qc);
         if ((tile & 3u) == 0) {

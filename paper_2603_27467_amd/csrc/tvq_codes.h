@@ -95,6 +95,20 @@ __device__ __forceinline__ double ladder_ratio(float lo_c, float hi_c, uint32_t 
   return rho;
 }
 
+// Level spacing of 8-bit linear norms, (R'max - R'min) / 255 as the IEEE fp32 division rounds
+// it, and 0 when R'max == R'min (also both infinite).  For finite x = R'max - R'min the product
+// q = RN(x RN(1/255)) is corrected once by its exact residual, RN(q + RN(x - 255 q) RN(1/255))
+// (Markstein's correction step); an exhaustive check over every fp32 x finds it equal to
+// RN(x / 255), where the division sequence takes 12 instructions.  Infinite or NaN x is what
+// the division gives for it.
+__device__ __forceinline__ float linear_step255(float rmin, float rmax) {
+  constexpr float kInv = 1.0f / 255.0f;
+  const float x = rmax - rmin;
+  const float q = x * kInv;
+  const float s = __builtin_fmaf(__builtin_fmaf(-q, 255.0f, x), kInv, q);
+  return rmax == rmin ? 0.0f : (__builtin_isfinite(x) ? s : x);
+}
+
 // The levels of one vector (2^b <= 16 entries): level q = RN32(R'min * rho^q).  Level 0 is
 // R'min exactly and RN32 brings the top level back to R'max.  Vectors with R'min == R'max get
 // Rmin at every level.  ladder_rho gives rho (1 for those vectors); ladder_levels_each hands

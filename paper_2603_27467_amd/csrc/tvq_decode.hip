@@ -298,7 +298,7 @@ __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState
   float r[kPairsPerLane];
   if constexpr (NB == 8) {
     // R^max == R^min (also both infinite) decodes to R^min: q * 0 + R^min
-    const float step = rmax == rmin ? 0.0f : (rmax - rmin) / (float)kLevels;
+    const float step = linear_step255(rmin, rmax);
 #pragma unroll
     for (int i = 0; i < kPairsPerLane; ++i) r[i] = __builtin_fmaf((float)qc[i], step, rmin);
   } else {
