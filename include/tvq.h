@@ -116,7 +116,8 @@ typedef struct tvq_codec tvq_codec;
 
 /* Create a codec: validates `cfg`, builds the sign table, the per-(layer, kind) parameters
  * and the reconstruction cos/sin tables (section 3.1, "trigonometric lookup") and uploads
- * them to the current HIP device.  *out receives the handle (NULL on error).
+ * them to the current HIP device, whose compute-unit count and attention-kernel occupancy it
+ * records for the attention chunk plan.  *out receives the handle (NULL on error).
  * Returns TVQ_ERR_INVALID_ARG (bad config), TVQ_ERR_UNSUPPORTED (d not 64/128),
  * TVQ_ERR_ALLOC or TVQ_ERR_HIP. */
 tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out);
@@ -176,9 +177,11 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
  *   t_end      1 .. lay->capacity_tokens tokens attended (slots [0, t_end))
  *   workspace  device scratch of at least tvq_attention_workspace(...) bytes, 16-byte
  *              aligned, owned by the caller; its contents are overwritten
- * The token range is split into chunks (a power of two of at least 4 tiles, sized from B, H,
- * G and t_end); the workspace holds one partial (max, sum, d accumulators) per query head and
- * chunk.  Query heads are processed up to 4 per pass over the codes (G > 4 reads them
+ * The token range is split into equal chunks (whole tile pairs, at least 4 tiles) so that a
+ * launch has about one chunk wave per wave slot of the codec's device (its compute units
+ * times the chunk kernel's resident waves per compute unit, taken at tvq_create); the
+ * workspace holds one partial (max, sum, d accumulators) per query head and chunk, so its
+ * size depends on the device the codec was created on.  Query heads are processed up to 4 per pass over the codes (G > 4 reads them
  * ceil(G/4) times).  Arithmetic is fp32 (expect ~1e-5 relative to an fp64 evaluation).
  * Supported: d = 64 or 128, G <= 64, and for both K and V of the layer n = 64 or 256 with
  * 8-bit linear or 4-bit log-space norms (TVQ_ERR_UNSUPPORTED otherwise).  Launches two
