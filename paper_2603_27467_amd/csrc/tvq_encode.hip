@@ -133,6 +133,32 @@ __device__ __forceinline__ double pair_norm_f64(float a, float b, double inv_sqr
   return sqrt(ad * ad + bd * bd) * inv_sqrt_d;
 }
 
+// c[15:0] * m[15:0] + acc in one instruction (m from a scalar register)
+__device__ __forceinline__ uint32_t mad_lo16(uint32_t c, uint32_t m, uint32_t acc) {
+  uint32_t r;
+  asm("v_mad_u32_u16 %0, %1, %2, %3" : "=v"(r) : "v"(c), "s"(m), "v"(acc));
+  return r;
+}
+
+// 16 four-bit codes whose low 16 bits are the code (the rounded float bits of the norm
+// codes): each half word gathers four codes by multiply-adds of the low 16 bits onto the
+// first code's bits (whose upper half is dropped), and one byte permutation joins two half
+// words.  Seven instructions per word instead of a shift and a mask per code.
+__device__ __forceinline__ Chunk<4> pack16_nibbles(const uint32_t (&c)[kPairsPerLane]) {
+  Chunk<4> o;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    uint32_t h[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int b = 8 * j + 4 * k;
+      h[k] = mad_lo16(c[b + 3], 4096u, mad_lo16(c[b + 2], 256u, mad_lo16(c[b + 1], 16u, c[b])));
+    }
+    o.w[j] = __builtin_amdgcn_perm(h[1], h[0], 0x05040100u);
+  }
+  return o;
+}
+
 template <int W>
 __device__ __forceinline__ void store_codes(uint8_t* rec, int sub, const uint32_t (&c)[kPairsPerLane]) {
   store_chunk<W>(rec + 2 * W * sub, pack16<W>(c));
@@ -190,6 +216,8 @@ struct EncWave {
   SegParams sp;
   const void* src;
   int64_t layer_off;          // element offset of the layer and of the lane's 32 elements
+  uint32_t lane_in_bytes;     // aligned tiles: byte offset of the lane's input from the
+                              // tile's first vector
   uint8_t* plane[3];
   const uint32_t* sm;         // the lane's 16 sign-mask words, in this wave's LDS
   uint32_t* sm_row;           // the wave's sign-mask row (D/2 words), filled by stage_tables
@@ -231,6 +259,7 @@ __device__ __forceinline__ bool enc_wave_setup(const EncodeArgs& a, EncWave<D>& 
   w.sp = a.segs[a.seg_list[li]];
   w.src = w.sp.kind ? a.v : a.k;
   w.layer_off = (int64_t)w.sp.layer * a.stride_l + w.sub * kElemsPerLane;
+  w.lane_in_bytes = (uint32_t)(w.sub * kElemsPerLane + w.vslot * a.stride_t) * 2u;
   for (int p = 0; p < 3; ++p) w.plane[p] = a.cache + a.n_slots * w.sp.pre[p];
   // the wave's LDS rows for the layer's sign masks (registers would hold them through the
   // whole tile loop) and the segment's angle bins; stage_tables fills them
@@ -275,10 +304,29 @@ struct TileIn {
 };
 
 // PAGED: token t of sequence b goes to position seq[b] + t through the block table.
-template <int D, bool F32IN, bool PAGED>
+// ALIGNED (bf16, contiguous cache, T a multiple of the tile's vector count): the tile's
+// vectors are consecutive tokens of one (batch, head), so its position is wave-uniform
+// (scalar arithmetic) and each lane adds a fixed offset; `slot` is then the slot of the
+// tile's first vector.
+template <int D, bool F32IN, bool PAGED, bool ALIGNED = false>
 __device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const EncWave<D>& w,
                                                    uint32_t tile) {
   const uint32_t j0 = tile * EncWave<D>::VPW;
+  if constexpr (ALIGNED) {
+    static_assert(!F32IN && !PAGED, "aligned tiles: bf16 input, contiguous cache");
+    const uint32_t bh = fast_div(j0, a.div_t);
+    const uint32_t t = j0 - bh * a.div_t.div;
+    const uint32_t b = fast_div(bh, a.div_h);
+    const uint32_t h = bh - b * a.H;
+    const uint16_t* base = (const uint16_t*)w.src + (int64_t)w.sp.layer * a.stride_l +
+                           (uint64_t)b * a.stride_b + (uint64_t)h * a.stride_h +
+                           (uint64_t)t * a.stride_t;
+    TileIn<F32IN> in;
+    load_words<16>((const uint32_t*)((const uint8_t*)base + w.lane_in_bytes), in.raw.w);
+    in.slot = bh * a.cap + a.t_begin + t;
+    in.ok = true;
+    return in;
+  }
   const uint32_t j = j0 + w.vslot;
   const uint32_t jj = j < a.nvec ? j : j0;
   const uint32_t bh = fast_div(jj, a.div_t);
@@ -385,6 +433,19 @@ __device__ __forceinline__ void front_mfma(const uint32_t (&raw)[16], const uint
   }
 }
 
+// Extremes over the vector's lanes of non-negative float bit patterns.
+template <bool MF, int LPV>
+__device__ __forceinline__ void vector_minmax_bits(uint32_t& mn, uint32_t& mx) {
+  if constexpr (MF) {
+    mn = min(mn, (uint32_t)__shfl_xor((int)mn, 16));
+    mx = max(mx, (uint32_t)__shfl_xor((int)mx, 16));
+    mn = min(mn, (uint32_t)__shfl_xor((int)mn, 32));
+    mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32));
+  } else {
+    vec_minmax_bits<LPV>(mn, mx);
+  }
+}
+
 template <bool MF, int LPV>
 __device__ __forceinline__ float vector_min(float v) {
   if constexpr (MF) {
@@ -405,7 +466,8 @@ __device__ __forceinline__ float vector_max(float v) {
   }
 }
 
-template <int D, bool F32IN, int WA, int NB, bool PAGED, bool MF = false, bool BINS = false>
+template <int D, bool F32IN, int WA, int NB, bool PAGED, bool MF = false, bool BINS = false,
+          bool ALIGNED = false>
 __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D>& w,
                                             const TileIn<F32IN>& in) {
   static_assert(!MF || (D == 128 && !F32IN), "matrix-core front end: d = 128, bf16 input");
@@ -453,22 +515,31 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
   }
 
   // ---- squared pair norms and the vector's extremes ----
+  // s2 >= +0 (never -0), so its bit patterns order like its values: the extremes are taken
+  // as unsigned integers, starting from FLT_MAX and +0
   float s2[kPairsPerLane];
-  float lmin = FLT_MAX, lmax = 0.0f;
+  uint32_t bmin = 0x7F7FFFFFu, bmax = 0u;
 #pragma unroll
   for (int i = 0; i < kPairsPerLane; ++i) {
     const float p = x[2 * i], q = x[2 * i + 1];
     s2[i] = __builtin_fmaf(p, p, q * q);
-    lmin = fminf(lmin, s2[i]);
-    lmax = fmaxf(lmax, s2[i]);
+    bmin = min(bmin, __float_as_uint(s2[i]));
+    bmax = max(bmax, __float_as_uint(s2[i]));
   }
-  const float smin = vector_min<MF, LPV>(lmin);
-  const float smax = vector_max<MF, LPV>(lmax);
-  // the fast formulas need every pair's max(|a|,|b|) inside [2^-61, 2^60]
-  const bool fast = __all(smin >= 0x1p-120f && smax <= 0x1p120f);
+  vector_minmax_bits<MF, LPV>(bmin, bmax);
+  const float smin = __uint_as_float(bmin);
+  const float smax = __uint_as_float(bmax);
+  // the fast formulas need every pair's max(|a|,|b|) inside [2^-61, 2^60] (every lane of the
+  // wave is active here)
+  const bool fast = __builtin_amdgcn_ballot_w64(bmin < 0x03800000u || bmax > 0x7B800000u) == 0;
 
   // ---- norms (first: the squared norms are then dead before the angle codes exist) ----
+  // aligned tiles: the tile's records are consecutive, from the uniform record of its first
+  // vector (the lane's offset is added as a 32-bit offset to that scalar address)
+  static_assert(!ALIGNED || (kFixed && !MF && !PAGED), "aligned tiles: fast formats");
   uint8_t* rec_nrm = w.plane[1] + (uint64_t)in.slot * sp.rec[1];
+  const uint32_t lane_nrm = ALIGNED ? (uint32_t)w.vslot * sp.rec[1] : 0u;
+  const uint32_t lane_hdr = ALIGNED ? (uint32_t)w.vslot * 8u : 0u;
   if (!kFixed && mode == 0) {
     // fp32 norms, rounded once from the fp64 value
     const double inv_sqrt_d = 1.0 / sqrt((double)D);
@@ -541,10 +612,12 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
       }
     }
     if (store) {
-      if constexpr (kFixed) store_codes<NB>(rec_nrm, w.sub, qc);
+      if constexpr (kFixed && NB == 4)
+        store_chunk<4>(rec_nrm + (lane_nrm + 8u * (uint32_t)w.sub), pack16_nibbles(qc));
+      else if constexpr (kFixed) store_chunk<NB>(rec_nrm + (lane_nrm + 2u * NB * (uint32_t)w.sub), pack16<NB>(qc));
       else store_codes_any(rec_nrm, w.sub, nbits, qc);
       // every lane of the vector writes the same header bytes
-      *(u32x2*)(w.plane[2] + (uint64_t)in.slot * 8) =
+      *(u32x2*)(w.plane[2] + (uint64_t)in.slot * 8 + lane_hdr) =
           u32x2{__float_as_uint(rmin), __float_as_uint(rmax)};
     }
   }
@@ -590,8 +663,12 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
     }
   }
   if (store) {
-    if constexpr (kFixed) store_codes<WA>(rec_ang, w.sub, kc);
-    else store_codes_any(rec_ang, w.sub, sp.w, kc);
+    if constexpr (kFixed) {
+      const uint32_t lane_ang = ALIGNED ? (uint32_t)w.vslot * sp.rec[0] : 0u;
+      store_chunk<WA>(rec_ang + (lane_ang + 2u * WA * (uint32_t)w.sub), pack16<WA>(kc));
+    } else {
+      store_codes_any(rec_ang, w.sub, sp.w, kc);
+    }
   }
 }
 
@@ -603,21 +680,21 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
 // the same kernel would raise its register count); it evaluates the angles (angle_bits)
 // rather than staging the bin table for a single tile, which made those short launches ~30%
 // slower.  Both give the exact code outside the flag zone.
-template <int D, bool MULTI, int WA, int NB, bool PAGED, bool MF = false>
+template <int D, bool MULTI, int WA, int NB, bool PAGED, bool MF = false, bool ALIGNED = false>
 __device__ void encode_tiles_fast(const EncodeArgs& a, const EncWave<D>& w, uint32_t tile0,
                                   uint32_t ntiles) {
   const uint32_t last = tile0 + ntiles - 1;
-  TileIn<false> ia = load_tile<D, false, PAGED>(a, w, tile0);
+  TileIn<false> ia = load_tile<D, false, PAGED, ALIGNED>(a, w, tile0);
   stage_tables<D>(a, w);
   if constexpr (!MULTI) {
-    encode_tile<D, false, WA, NB, PAGED, MF, false>(a, w, ia);
+    encode_tile<D, false, WA, NB, PAGED, MF, false, ALIGNED>(a, w, ia);
     return;
   }
   for (uint32_t t = tile0; t <= last; t += 2) {
-    const TileIn<false> ib = load_tile<D, false, PAGED>(a, w, min(t + 1, last));
-    encode_tile<D, false, WA, NB, PAGED, MF, true>(a, w, ia);
-    ia = load_tile<D, false, PAGED>(a, w, min(t + 2, last));
-    encode_tile<D, false, WA, NB, PAGED, MF, true>(a, w, ib);
+    const TileIn<false> ib = load_tile<D, false, PAGED, ALIGNED>(a, w, min(t + 1, last));
+    encode_tile<D, false, WA, NB, PAGED, MF, true, ALIGNED>(a, w, ia);
+    ia = load_tile<D, false, PAGED, ALIGNED>(a, w, min(t + 2, last));
+    encode_tile<D, false, WA, NB, PAGED, MF, true, ALIGNED>(a, w, ib);
   }
 }
 
@@ -639,7 +716,8 @@ __global__ __launch_bounds__(kBlockThreads) void encode_mfma_kernel(EncodeArgs a
   }
 }
 
-template <int D, bool MULTI, bool PAGED>
+// ALIGNED: see load_tile (multi-tile launches only).
+template <int D, bool MULTI, bool PAGED, bool ALIGNED = false>
 __global__ __launch_bounds__(kBlockThreads) void encode_fast_kernel(EncodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t s_sm[kWavesPerBlock][D / 2];
   __shared__ u32x2 s_bins[kWavesPerBlock][kBinRows];
@@ -648,11 +726,11 @@ __global__ __launch_bounds__(kBlockThreads) void encode_fast_kernel(EncodeArgs a
   if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles, MULTI ? s_bins : nullptr)) return;
   const bool wide = w.sp.w == 8;
   if (w.sp.mode == 1) {
-    if (wide) encode_tiles_fast<D, MULTI, 8, 8, PAGED>(a, w, tile0, ntiles);
-    else encode_tiles_fast<D, MULTI, 6, 8, PAGED>(a, w, tile0, ntiles);
+    if (wide) encode_tiles_fast<D, MULTI, 8, 8, PAGED, false, ALIGNED>(a, w, tile0, ntiles);
+    else encode_tiles_fast<D, MULTI, 6, 8, PAGED, false, ALIGNED>(a, w, tile0, ntiles);
   } else {
-    if (wide) encode_tiles_fast<D, MULTI, 8, 4, PAGED>(a, w, tile0, ntiles);
-    else encode_tiles_fast<D, MULTI, 6, 4, PAGED>(a, w, tile0, ntiles);
+    if (wide) encode_tiles_fast<D, MULTI, 8, 4, PAGED, false, ALIGNED>(a, w, tile0, ntiles);
+    else encode_tiles_fast<D, MULTI, 6, 4, PAGED, false, ALIGNED>(a, w, tile0, ntiles);
   }
 }
 
@@ -681,7 +759,14 @@ void launch_encode(const EncodeArgs& a, int in_f32, bool fast, unsigned grid, hi
       return;
     }
   }
-  if (fast && multi)
+  // aligned tiles: whole tiles per (batch, head), and every lane's input offset from its
+  // tile's first vector, (VPW - 1) * stride_t + d elements of bf16, inside 32 bits
+  constexpr uint32_t VPW = EncWave<D>::VPW;
+  const bool aligned = !PAGED && a.div_t.div % VPW == 0 &&
+                       (uint64_t)a.stride_t * VPW * 2u < (1ull << 31);
+  if (fast && multi && aligned)
+    hipLaunchKernelGGL((encode_fast_kernel<D, true, PAGED, !PAGED>), dim3(grid), block, 0, s, a);
+  else if (fast && multi)
     hipLaunchKernelGGL((encode_fast_kernel<D, true, PAGED>), dim3(grid), block, 0, s, a);
   else if (fast)
     hipLaunchKernelGGL((encode_fast_kernel<D, false, PAGED>), dim3(grid), block, 0, s, a);

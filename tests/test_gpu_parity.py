@@ -308,6 +308,67 @@ def test_multi_tile_decode_ragged(gpu, d, L, B, T):
 
 
 # ---------------------------------------------------------------------------- full size
+@pytest.mark.parametrize("d,L,B,T,t_begin,pad", [
+    (128, 4, 1, 4112, 5, 0),     # whole tiles per (batch, head): the scalar-addressed tiles
+    (128, 4, 1, 4112, 7, 64),    # the same through a strided view (token stride d + 64)
+    (128, 4, 1, 4100, 3, 0),     # tiles that cross (batch, head) rows, ragged last tile
+    (64, 2, 2, 8192, 3, 32),     # d = 64 whole tiles, strided
+    (64, 2, 2, 8190, 0, 0),      # d = 64 tiles crossing rows
+])
+def test_multi_tile_encode_sampled(gpu, d, L, B, T, t_begin, pad):
+    """Encode launches of 2 tiles per wave (the multi-tile kernel) with and without tiles that
+    stay within one (batch, head) row, into a cache of capacity T + 16 at token offset t_begin,
+    from a contiguous or a strided input view.  The codes and header of the last three tiles of
+    every (layer, kind) and of 1500 random vectors against the oracle's encode of the same
+    input, and every slot outside [t_begin, t_begin + T) untouched."""
+    import torch
+    w = workloads.get("C2")
+    table = [LayerCfg(64, 64), LayerCfg(256, 256), LayerCfg(64, 256), LayerCfg(256, 64)][:L]
+    s = Setup(L, 8, d, table, workloads.sign_table(13, L, d)).build()
+    k, v = _draw(w, L, B, 8, T, d, "bf16", 14)
+    T_cap = T + 16
+    lay = s.gpu.layout(B, T_cap)
+    cache = torch.full((lay.total_bytes,), 0xAB, dtype=torch.uint8, device="cuda")
+    views = []
+    for x in (k, v):
+        full = torch.zeros((L, B, 8, T, d + pad), dtype=torch.bfloat16, device="cuda")
+        full[..., :d] = bf16_bits_to_torch(x).cuda()
+        views.append(full[..., :d])
+    _say(f"[multi-tile encode d={d} L={L} B={B} T={T} t_begin={t_begin} pad={pad}] "
+         f"strides {views[0].stride()}")
+    s.gpu.encode(views[0], views[1], cache, lay, t_begin=t_begin)
+    torch.cuda.synchronize()
+    host = torch_to_np(cache)
+    assert untouched_outside(host, s, B, T, T_cap, t_begin, 0xAB)
+    nvec = B * 8 * T
+    vpw = 64 // (d // 32)
+    tail = range(max(0, (nvec - 1) // vpw - 2) * vpw, nvec)
+    rng = np.random.default_rng(2)
+    picks = [(l, kind, j) for l in range(L) for kind in range(2) for j in tail]
+    picks += [(int(rng.integers(0, L)), int(rng.integers(0, 2)), int(rng.integers(0, nvec)))
+              for _ in range(1500)]
+    stats = dict(angle_mismatch=0, angle_unflagged=0, norm_mismatch=0, norm_unflagged=0,
+                 hdr_ulp=0)
+    for l, kind, j in picks:
+        bh, t = divmod(j, T)
+        b, h = divmod(bh, 8)
+        x = ((k if kind == 0 else v)[l, b, h, t].astype(np.uint32) << 16).view(np.float32)
+        kd_ = s.orc.kinds[2 * l + kind]
+        ref = oracle.encode_vector(x, s.signs[l], kd_)
+        kg, qg, _, hg = s.orc.read_vector(host, B, T_cap, l, kind, b, h, t_begin + t)
+        fa = oracle.angle_flags(ref.u, kd_.n)
+        fn = oracle.norm_flags(ref.t, kd_.norm_bits)
+        stats["angle_mismatch"] += int((kg != ref.k).sum())
+        stats["angle_unflagged"] += int(((kg != ref.k) & ~fa).sum())
+        stats["norm_mismatch"] += int((qg != ref.q).sum())
+        stats["norm_unflagged"] += int(((qg != ref.q) & ~fn).sum())
+        du = np.abs(hg.view(np.int32).astype(np.int64) - ref.hdr.view(np.int32).astype(np.int64))
+        stats["hdr_ulp"] = max(stats["hdr_ulp"], int(du.max()))
+    _say(f"   {len(picks)} vectors: {stats}")
+    assert stats["angle_unflagged"] == 0 and stats["norm_unflagged"] == 0
+    assert stats["hdr_ulp"] <= 2
+
+
 @pytest.mark.parametrize("cfg", ["C2", "C3", "C4"])
 def test_cache_full_size_sampled(gpu, cfg):
     """A benchmark workload at full size in the launch configuration the benchmark times:
