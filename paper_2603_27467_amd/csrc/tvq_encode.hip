@@ -433,6 +433,29 @@ __device__ __forceinline__ void front_mfma(const uint32_t (&raw)[16], const uint
   }
 }
 
+// Minimum and maximum over a vector's lanes of the bit patterns of non-negative floats, which
+// order like the floats themselves: one DPP min and one DPP max per stage (the float forms
+// need a canonicalizing copy of the permuted operand).  The s_nop keeps the DPP sources two
+// wait states after the VALU instructions that wrote them.
+#define TVQ_MINMAX_DPP(P)                                                                  \
+  "s_nop 1\n\tv_min_u32_dpp %0, %2, %2 " P " row_mask:0xf bank_mask:0xf\n\t"              \
+  "v_max_u32_dpp %1, %3, %3 " P " row_mask:0xf bank_mask:0xf"
+
+template <int LPV>
+__device__ __forceinline__ void vec_minmax_bits(uint32_t& mn, uint32_t& mx) {
+  static_assert(LPV == 1 || LPV == 2 || LPV == 4, "d must be 32, 64 or 128");
+  if constexpr (LPV >= 2) {
+    uint32_t a, b;
+    asm volatile(TVQ_MINMAX_DPP("quad_perm:[1,0,3,2]") : "=&v"(a), "=&v"(b) : "v"(mn), "v"(mx));
+    mn = a, mx = b;
+  }
+  if constexpr (LPV >= 4) {
+    uint32_t a, b;
+    asm volatile(TVQ_MINMAX_DPP("quad_perm:[2,3,0,1]") : "=&v"(a), "=&v"(b) : "v"(mn), "v"(mx));
+    mn = a, mx = b;
+  }
+}
+
 // Extremes over the vector's lanes of non-negative float bit patterns.
 template <bool MF, int LPV>
 __device__ __forceinline__ void vector_minmax_bits(uint32_t& mn, uint32_t& mx) {
