@@ -300,3 +300,26 @@ def test_angle_bins_reject_other_n(tvq):
         assert lib.tvq_make_angle_bins(n, buf.ctypes.data_as(ctypes.c_void_p),
                                        fb.ctypes.data_as(ctypes.c_void_p)) == -1
     assert lib.tvq_make_angle_bins(64, None, None) == -1
+
+
+def test_binding_raises_without_the_library(tmp_path):
+    """A copy of the package without libtvq.so: constructing a codec raises ImportError naming
+    the missing library (there is no fallback path to run instead)."""
+    import shutil
+    import subprocess
+    import sys
+    src = os.path.join(ROOT, "paper_2603_27467_amd")
+    dst = tmp_path / "paper_2603_27467_amd"
+    shutil.copytree(src, dst, ignore=shutil.ignore_patterns("*.so", "*.so.*", "csrc",
+                                                            "__pycache__"))
+    code = ("import paper_2603_27467_amd as t\n"
+            "try:\n"
+            "    t.Codec(1, 1, 128, [t.LayerCfg(64, 64)])\n"
+            "except ImportError as e:\n"
+            "    print('raised:', e)\n"
+            "else:\n"
+            "    print('no error')\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=tmp_path, capture_output=True,
+                       text=True, timeout=120, env={**os.environ, "PYTHONPATH": str(tmp_path)})
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.startswith("raised:") and "libtvq.so is missing" in r.stdout, r.stdout
