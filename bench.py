@@ -75,18 +75,18 @@ def algorithmic_bytes(w: workloads.Workload) -> dict:
             "vectors": 2 * w.L * w.B * w.H * w.T}
 
 
-def profile_entry(kernel: str, path: str = PROFILE_COUNTERS, sources=None):
+def profile_entry(kernel: str, workload: str, path: str = PROFILE_COUNTERS, sources=None):
     """The committed counter summary of `kernel` ("tvq_encode" / "tvq_decode" in the codec
     summary, "tvq_attention" in the long-context one): HBM bytes per launch from rocprofv3
     FETCH_SIZE / WRITE_SIZE scaled by the same counters on a copy of known size, VALU
-    instructions per launch and VALU busy.  None when absent or when the kernel sources have
-    changed since the counters were taken."""
+    instructions per launch and VALU busy.  None when absent, when the counters were taken on
+    another workload, or when the kernel sources have changed since they were taken."""
     try:
         with open(path) as f:
             d = json.load(f)
     except (OSError, ValueError):
         return None
-    if d.get("kernel_source_hash") != kernel_source_hash(sources):
+    if d.get("kernel_source_hash") != kernel_source_hash(sources) or d.get("workload") != workload:
         return None
     return d.get("kernels", {}).get(kernel)
 
@@ -585,7 +585,7 @@ def run_longctx(w: workloads.Workload, args) -> dict:
     if args.attention:
         # codes of every cached token once, plus the bf16 queries and outputs of every layer
         att_bytes = rec_tok * t_mean + qo
-        prof = profile_entry("tvq_attention", ATTENTION_COUNTERS, ATTENTION_SOURCES)
+        prof = profile_entry("tvq_attention", w.name, ATTENTION_COUNTERS, ATTENTION_SOURCES)
         att_gbs = att_bytes / (dec_ms * 1e-3) / 1e9
         return {
             "metric": "attention over the compressed cache: bf16-equivalent KV GB/s consumed",
@@ -775,7 +775,7 @@ def main() -> int:
         ms = float(ms_all.mean())
         gbs = ab["per_launch"] / (ms * 1e-3) / 1e9
         # the committed counters cover the canonical-schedule encode only
-        prof = None if (args.encode_mfma and name == "encode") else profile_entry(kern)
+        prof = None if (args.encode_mfma and name == "encode") else profile_entry(kern, w.name)
         out = {"ms": round(ms, 5), "ms_median": round(float(np.median(ms_all)), 5),
                "ms_min": round(float(ms_all.min()), 5),
                "kv_GBps": round(ab["kv"] / (ms * 1e-3) / 1e9, 2),
