@@ -313,7 +313,7 @@ def test_multi_tile_decode_ragged(gpu, d, L, B, T):
     (128, 4, 1, 4112, 7, 64),    # the same through a strided view (token stride d + 64)
     (128, 4, 1, 4100, 3, 0),     # tiles that cross (batch, head) rows, ragged last tile
     (64, 2, 2, 8192, 3, 32),     # d = 64 whole tiles, strided
-    (64, 2, 2, 8190, 0, 0),      # d = 64 tiles crossing rows
+    (64, 2, 2, 8194, 0, 0),      # d = 64 tiles crossing rows
 ])
 def test_multi_tile_encode_sampled(gpu, d, L, B, T, t_begin, pad):
     """Encode launches of 2 tiles per wave (the multi-tile kernel) with and without tiles that
