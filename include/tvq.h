@@ -279,6 +279,17 @@ tvq_status tvq_make_decode_table(int32_t n, int32_t head_dim, float* cos_out, fl
  * 2 n entries.  Host-only; TVQ_ERR_INVALID_ARG for other n or null pointers. */
 tvq_status tvq_make_angle_bins(int32_t n, uint32_t* code_out, float* bound_out);
 
+/* The constants of the encode kernels' fp32 arithmetic, so that a host program can run the
+ * same steps (Algorithm 1, the angle quantizer; section 3.3, eq. (2) and its log-space variant):
+ *   poly_out[6]   the coefficients of atan(t)/(2 pi) = t * p(t^2), t in [0, 1], from the
+ *                 highest power of t^2 down, that the evaluated angle path uses;
+ *   spread_out[2] the range [lo, hi) of bits(s2_max) - bits(s2_min) (the bit patterns of a
+ *                 vector's largest and smallest squared pair norm) inside which a vector's norm
+ *                 codes come from fp32 formulas; a tile holding any other vector takes its
+ *                 norm codes from fp64.
+ * Host-only.  TVQ_ERR_INVALID_ARG for null pointers. */
+tvq_status tvq_encode_constants(float* poly_out, uint32_t* spread_out);
+
 /* Layout of a configuration without creating a codec (same result as tvq_cache_layout). */
 tvq_status tvq_layout_for_config(const tvq_config* cfg, int64_t batch, int64_t capacity_tokens,
                                  tvq_layout* out);

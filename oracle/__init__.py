@@ -391,11 +391,42 @@ def angle_flags(u: np.ndarray, n) -> np.ndarray:
     return np.abs(frac - 0.5) < FLAG_REL * np.asarray(n, np.float64)
 
 
-def norm_flags(t: np.ndarray, bits) -> np.ndarray:
-    """True where the norm coordinate lies within 1e-6 of the code range (2^b - 1) of a
-    rounding boundary; NaN (degenerate / fp32 norms) is never flagged."""
+def norm_flags_range(t: np.ndarray, bits) -> np.ndarray:
+    """True where the norm coordinate t (eq. (2) or its log variant) lies within 1e-6 of the
+    code range (2^b - 1) of a rounding boundary; NaN (degenerate / fp32 norms) is never
+    flagged."""
     levels = (2.0 ** np.asarray(bits, np.float64)) - 1.0
     frac = t - np.floor(t)
     with np.errstate(invalid="ignore"):
         f = np.abs(frac - 0.5) < FLAG_REL * levels
     return np.where(np.isnan(t), False, f)
+
+
+def norm_flags_value(t: np.ndarray, bits, hdr: np.ndarray, mode) -> np.ndarray:
+    """True where the pair norm r lies within 1e-6 relative of the norm r_b of the nearest
+    rounding boundary, |r - r_b| < 1e-6 r_b.  t: [..., P] coordinates, hdr: [..., 2] the
+    stored (Rmin, Rmax) of each vector, mode NORM_LINEAR or NORM_LOG.  With Delta the code
+    step, linear: r - r_b = (t - t_b) Delta_r, r_b = Rmin + t_b Delta_r; log: ln r - ln r_b =
+    (t - t_b) Delta_ln (section 3.3 inverted at the boundary t_b = floor(t) + 1/2)."""
+    t = np.asarray(t, np.float64)
+    levels = (2.0 ** np.asarray(bits, np.float64)) - 1.0
+    hdr = np.asarray(hdr, np.float64)
+    r0, r1 = hdr[..., 0:1], hdr[..., 1:2]
+    tb = np.floor(t) + 0.5
+    with np.errstate(invalid="ignore", divide="ignore", over="ignore"):
+        if mode == NORM_LINEAR:
+            step = (r1 - r0) / levels
+            f = np.abs(t - tb) * step < FLAG_REL * (r0 + tb * step)
+        else:
+            tiny = float(np.finfo(np.float32).tiny)
+            step = (np.log(np.maximum(r1, tiny)) - np.log(np.maximum(r0, tiny))) / levels
+            f = np.abs(np.expm1((t - tb) * step)) < FLAG_REL
+    return np.where(np.isnan(t), False, f)
+
+
+def norm_flags(t: np.ndarray, bits, hdr: np.ndarray, mode) -> np.ndarray:
+    """The flag rule of the norm codes: a pair is near a bin boundary when its coordinate lies
+    within 1e-6 of the code range of the boundary (norm_flags_range) or its norm within 1e-6
+    relative of the boundary's norm (norm_flags_value).  Pairs so flagged are counted and
+    reported; every other pair's code must match exactly."""
+    return norm_flags_range(t, bits) | norm_flags_value(t, bits, hdr, mode)

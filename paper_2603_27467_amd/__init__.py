@@ -13,7 +13,8 @@ from ._capi import (  # noqa: F401
     TvqError, tvq_layer_cfg, tvq_config, tvq_tensor_desc, tvq_layout,
     tvq_create, tvq_destroy, tvq_cache_layout, tvq_encode, tvq_decode, tvq_bits_per_element,
     tvq_status_string, tvq_make_signs, tvq_bits_per_element_config, tvq_make_trig_table,
-    tvq_make_decode_table, tvq_make_angle_bins, tvq_layout_for_config, tvq_attention_workspace,
+    tvq_make_decode_table, tvq_make_angle_bins, tvq_encode_constants, tvq_layout_for_config,
+    tvq_attention_workspace,
     tvq_attention_decode,
     tvq_encode_mfma, tvq_encode_paged, tvq_decode_paged, tvq_attention_paged_workspace, tvq_attention_paged,
     tvq_abi_version, library_path, load_library,

@@ -109,6 +109,8 @@ def load_library():
     L.tvq_make_decode_table.argtypes = [i32, i32, vp, vp]
     L.tvq_make_angle_bins.restype = ctypes.c_int
     L.tvq_make_angle_bins.argtypes = [i32, vp, vp]
+    L.tvq_encode_constants.restype = ctypes.c_int
+    L.tvq_encode_constants.argtypes = [vp, vp]
     L.tvq_layout_for_config.restype = ctypes.c_int
     L.tvq_layout_for_config.argtypes = [ctypes.POINTER(tvq_config), i64, i64,
                                         ctypes.POINTER(tvq_layout)]
@@ -276,6 +278,17 @@ def tvq_make_angle_bins(n: int):
                                               bound.ctypes.data_as(ctypes.c_void_p)),
            "tvq_make_angle_bins")
     return code, bound
+
+
+def tvq_encode_constants():
+    """(atan polynomial coefficients [6] fp32, fp32-norm spread limits [2] uint32) of the
+    encode kernels."""
+    poly = np.zeros(6, np.float32)
+    spread = np.zeros(2, np.uint32)
+    _check(load_library().tvq_encode_constants(poly.ctypes.data_as(ctypes.c_void_p),
+                                               spread.ctypes.data_as(ctypes.c_void_p)),
+           "tvq_encode_constants")
+    return poly, spread
 
 
 def tvq_make_trig_table(n: int):

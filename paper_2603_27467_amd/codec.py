@@ -36,6 +36,21 @@ def desc_of(t, layers: Optional[int] = None) -> C.tvq_tensor_desc:
     return C.tvq_tensor_desc(t.shape[1], t.shape[3], s[0], s[1], s[2], s[3])
 
 
+def _check_bytes(buf, lay: C.tvq_layout, what: str) -> None:
+    """buf must be a contiguous uint8 GPU tensor holding at least the layout's bytes (the
+    kernels address it from the layout alone)."""
+    import torch
+    if buf.dtype != torch.uint8 or not buf.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous uint8 GPU tensor")
+    if buf.numel() < lay.total_bytes:
+        raise ValueError(f"{what} holds {buf.numel()} bytes, the layout needs {lay.total_bytes}")
+
+
+def _on_gpu(*tensors) -> None:
+    if not all(t.is_cuda for t in tensors):
+        raise ValueError("tensors must be on the GPU")
+
+
 class Codec:
     def __init__(self, num_layers: int, num_heads: int, head_dim: int,
                  layers: Sequence, seed: int = 0, shared_signs: bool = False,
@@ -68,6 +83,22 @@ class Codec:
         except Exception:
             pass
 
+    def _check_kv(self, t, what: str) -> None:
+        """t must be a [L, B, H, T, d] GPU tensor of this codec's L, H and d (the kernels take
+        L, H and d from the codec, so a smaller tensor would be read or written past its end)."""
+        if t.dim() != 5:
+            raise ValueError(f"{what} must be a [L, B, H, T, d] GPU tensor")
+        if t.shape[0] != self.L or t.shape[2] != self.H or t.shape[4] != self.d:
+            raise ValueError(f"{what} has shape {tuple(t.shape)}; the codec needs "
+                             f"[{self.L}, B, {self.H}, T, {self.d}]")
+
+    def _check_q(self, q, out) -> None:
+        if q.dim() != 3 or out.shape != q.shape or not q.is_contiguous() or \
+                not out.is_contiguous():
+            raise ValueError("q and out must be contiguous [B, Hq, d] GPU tensors")
+        if q.shape[2] != self.d:
+            raise ValueError(f"q has head dim {q.shape[2]}, the codec {self.d}")
+
     def layout(self, batch: int, capacity_tokens: int) -> C.tvq_layout:
         return C.tvq_cache_layout(self.handle, batch, capacity_tokens)
 
@@ -82,8 +113,9 @@ class Codec:
         dt = {torch.bfloat16: C.TVQ_BF16, torch.float32: C.TVQ_F32}.get(k.dtype)
         if dt is None:
             raise ValueError("k/v must be bf16 or fp32")
-        if not (k.is_cuda and v.is_cuda and cache.is_cuda):
-            raise ValueError("tensors must be on the GPU")
+        self._check_kv(k, "k")
+        _check_bytes(cache, lay, "cache")
+        _on_gpu(k, v, cache)
         C.tvq_encode(self.handle, dt, k.data_ptr(), v.data_ptr(), desc_of(k), t_begin,
                      cache.data_ptr(), lay, _stream_handle(stream))
 
@@ -94,6 +126,9 @@ class Codec:
         if k.shape != v.shape or k.stride() != v.stride() or k.dtype != torch.bfloat16 or \
                 v.dtype != torch.bfloat16:
             raise ValueError("k and v must be bf16 and share shape and strides")
+        self._check_kv(k, "k")
+        _check_bytes(cache, lay, "cache")
+        _on_gpu(k, v, cache)
         C.tvq_encode_mfma(self.handle, k.data_ptr(), v.data_ptr(), desc_of(k), t_begin,
                           cache.data_ptr(), lay, _stream_handle(stream))
 
@@ -106,6 +141,9 @@ class Codec:
         dt = {torch.bfloat16: C.TVQ_BF16, torch.float32: C.TVQ_F32}.get(k_out.dtype)
         if dt is None:
             raise ValueError("outputs must be bf16 or fp32")
+        self._check_kv(k_out, "k_out")
+        _check_bytes(cache, lay, "cache")
+        _on_gpu(k_out, v_out, cache)
         C.tvq_decode(self.handle, cache.data_ptr(), lay, t_begin, t_end, dt, k_out.data_ptr(),
                      v_out.data_ptr(), desc_of(k_out), _stream_handle(stream))
 
@@ -118,15 +156,18 @@ class Codec:
         codes (tvq_attention_decode).  `workspace` (a uint8 device tensor) is allocated when
         not given."""
         import torch
-        if q.dim() != 3 or out.shape != q.shape or not q.is_contiguous() or \
-                not out.is_contiguous():
-            raise ValueError("q and out must be contiguous [B, Hq, d] tensors")
+        self._check_q(q, out)
+        _check_bytes(cache, lay, "cache")
+        _on_gpu(q, out, cache)
         dts = {torch.bfloat16: C.TVQ_BF16, torch.float32: C.TVQ_F32}
         if q.dtype not in dts or out.dtype not in dts:
             raise ValueError("q/out must be bf16 or fp32")
         need = self.attention_workspace_bytes(q.shape[0], q.shape[1], t_end)
         if workspace is None:
             workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        elif workspace.dtype != torch.uint8 or not workspace.is_cuda or \
+                not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous uint8 GPU tensor")
         C.tvq_attention_decode(self.handle, cache.data_ptr(), lay, layer, t_end, q.shape[1],
                                scale, dts[q.dtype], q.data_ptr(), dts[out.dtype], out.data_ptr(),
                                workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
@@ -153,6 +194,9 @@ class Codec:
         dt = {torch.bfloat16: C.TVQ_BF16, torch.float32: C.TVQ_F32}.get(k.dtype)
         if dt is None:
             raise ValueError("k/v must be bf16 or fp32")
+        self._check_kv(k, "k")
+        _check_bytes(pool, pool_lay, "pool")
+        _on_gpu(k, v, pool)
         if block_table.dim() != 2 or positions.shape != (k.shape[1],) or \
                 block_table.shape[0] != k.shape[1]:
             raise ValueError("positions [B] and block_table [B, max_blocks] must match k")
@@ -170,6 +214,9 @@ class Codec:
         dt = {torch.bfloat16: C.TVQ_BF16, torch.float32: C.TVQ_F32}.get(k_out.dtype)
         if dt is None:
             raise ValueError("outputs must be bf16 or fp32")
+        self._check_kv(k_out, "k_out")
+        _check_bytes(pool, pool_lay, "pool")
+        _on_gpu(k_out, v_out, pool)
         if block_table.dim() != 2 or block_table.shape[0] != k_out.shape[1]:
             raise ValueError("block_table must be [B, max_blocks]")
         C.tvq_decode_paged(self.handle, pool.data_ptr(), pool_lay,
@@ -186,9 +233,9 @@ class Codec:
                         layer: int, q, out, scale: float, workspace=None, stream=None) -> None:
         """Attention of q ([B, Hq, d]) of sequence b over its positions [0, ctx_lens[b])."""
         import torch
-        if q.dim() != 3 or out.shape != q.shape or not q.is_contiguous() or \
-                not out.is_contiguous():
-            raise ValueError("q and out must be contiguous [B, Hq, d] tensors")
+        self._check_q(q, out)
+        _check_bytes(pool, pool_lay, "pool")
+        _on_gpu(q, out, pool, block_table, ctx_lens)
         dts = {torch.bfloat16: C.TVQ_BF16, torch.float32: C.TVQ_F32}
         if q.dtype not in dts or out.dtype not in dts:
             raise ValueError("q/out must be bf16 or fp32")
@@ -199,6 +246,9 @@ class Codec:
                                                     pool_lay.capacity_tokens)
         if workspace is None:
             workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        elif workspace.dtype != torch.uint8 or not workspace.is_cuda or \
+                not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous uint8 GPU tensor")
         C.tvq_attention_paged(self.handle, pool.data_ptr(), pool_lay,
                               self._i32(block_table, "block_table"), block_table.shape[1],
                               self._i32(ctx_lens, "ctx_lens"), max_ctx, B, layer, q.shape[1],

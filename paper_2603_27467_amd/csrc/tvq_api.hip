@@ -310,6 +310,14 @@ tvq_status tvq_make_angle_bins(int32_t n, uint32_t* code_out, float* bound_out) 
   return TVQ_OK;
 }
 
+tvq_status tvq_encode_constants(float* poly_out, uint32_t* spread_out) {
+  if (!poly_out || !spread_out) return TVQ_ERR_INVALID_ARG;
+  for (int i = 0; i < 6; ++i) poly_out[i] = tvq::kAtanTurnsPoly[i];
+  spread_out[0] = tvq::kNormSpreadMinBits;
+  spread_out[1] = tvq::kNormSpreadMaxBits;
+  return TVQ_OK;
+}
+
 tvq_status tvq_make_decode_table(int32_t n, int32_t head_dim, float* cos_out, float* sin_out) {
   if (n < 2 || n > 4096 || head_dim < 1 || !cos_out || !sin_out) return TVQ_ERR_INVALID_ARG;
   const double root = std::sqrt((double)head_dim);

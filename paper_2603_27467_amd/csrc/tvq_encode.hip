@@ -40,37 +40,25 @@ namespace {
 constexpr float kRoundShift = 12582912.0f;    // 1.5 * 2^23
 constexpr uint32_t kRoundShiftBits = 0x4B400000u;
 
-// atan(t) / (2 pi) for t in [0, 1] as t * p(t^2), degree-11 odd polynomial fitted for minimum
-// maximum error: 2.8e-7 of a turn when evaluated in fp32, inside the 1e-6 of a turn that
-// separates an unflagged pair from a bin boundary.
-__device__ __forceinline__ float atan_turns01(float t) {
-  const float s = t * t;
-  float p = -1.865156344e-03f;
-  p = __builtin_fmaf(p, s, 8.379081264e-03f);
-  p = __builtin_fmaf(p, s, -1.852984540e-02f);
-  p = __builtin_fmaf(p, s, 3.080290556e-02f);
-  p = __builtin_fmaf(p, s, -5.293856561e-02f);
-  p = __builtin_fmaf(p, s, 1.591513157e-01f);
-  return t * p;
-}
-
 // Angle bin of the pair (a, b) as the bits of round(n * atan2(b, a) / 2pi) + `shift`, where
 // shift = 1.5*2^23 (+ a whole number of bins): the low bits hold the signed bin (two's
 // complement), so masking them to ceil(log2 n) bits gives the bin mod n when n is a power
 // of two.  Reduction: in the first quadrant the angle is pi/4 + atan(t) with
-// t = (|b| - |a|) / (|b| + |a|) in [-1, 1]; the reflection into the left half plane flips the
-// sign of (angle - 1/4 turn), and the sign of b gives the lower half plane.  Requires
-// |a| + |b| in [2^-61, 2^62] (the caller checks) so rcp stays normal.
+// t = (|b| - |a|) / (|b| + |a|) in [-1, 1], atan(t) / 2pi from the polynomial kAtanTurnsPoly
+// (2.8e-7 of a turn, inside the 1e-6 of a turn that separates an unflagged pair from a bin
+// boundary); the reflection into the left half plane flips the sign of (angle - 1/4 turn),
+// and the sign of b gives the lower half plane.  Requires |a| + |b| in [2^-61, 2^62] (the
+// caller checks) so rcp stays normal.
 __device__ __forceinline__ uint32_t angle_bits(float a, float b, float nf, float shift) {
   const float ax = fabsf(a), ay = fabsf(b);
   const float t = (ay - ax) * __builtin_amdgcn_rcpf(ay + ax);
   const float s = t * t;
-  float p = -1.865156344e-03f;
-  p = __builtin_fmaf(p, s, 8.379081264e-03f);
-  p = __builtin_fmaf(p, s, -1.852984540e-02f);
-  p = __builtin_fmaf(p, s, 3.080290556e-02f);
-  p = __builtin_fmaf(p, s, -5.293856561e-02f);
-  p = __builtin_fmaf(p, s, 1.591513157e-01f);
+  float p = kAtanTurnsPoly[0];
+  p = __builtin_fmaf(p, s, kAtanTurnsPoly[1]);
+  p = __builtin_fmaf(p, s, kAtanTurnsPoly[2]);
+  p = __builtin_fmaf(p, s, kAtanTurnsPoly[3]);
+  p = __builtin_fmaf(p, s, kAtanTurnsPoly[4]);
+  p = __builtin_fmaf(p, s, kAtanTurnsPoly[5]);
   const float g = __builtin_fmaf(t, p, -0.125f);            // first-quadrant angle - 1/4, turns
   const float gr = __uint_as_float(__float_as_uint(g) ^ (__float_as_uint(a) & 0x80000000u));
   const float h = 0.25f + gr;                                // upper half plane, [0, 1/2]
@@ -131,6 +119,69 @@ __device__ __forceinline__ uint32_t angle_code_careful(float a, float b, float n
 __device__ __forceinline__ double pair_norm_f64(float a, float b, double inv_sqrt_d) {
   const double ad = (double)a, bd = (double)b;
   return sqrt(ad * ad + bd * bd) * inv_sqrt_d;
+}
+
+// Compact fp64 helpers of the encode's fp64 norm path.  The library sqrt and log expand to
+// sequences whose temporaries, unrolled over a lane's 16 pairs, raise the register count of
+// the whole encode kernel (and so cost a wave per SIMD in every tile); these use few registers
+// and stay within about an ulp of the correctly rounded results.
+
+// sqrt(s) for s = 0 or s in [2^-300, 2^300]: the hardware reciprocal square root estimate,
+// one Goldschmidt step (g ~ sqrt(s), h ~ 1/(2 sqrt(s))) and two corrections by the residual
+// s - g^2, each of which roughly squares the relative error.
+__device__ __forceinline__ double sqrt_f64_lean(double s) {
+  const double y = __builtin_amdgcn_rsq(s);
+  double g = s * y, h = 0.5 * y;
+  const double r = __builtin_fma(-g, h, 0.5);
+  g = __builtin_fma(g, r, g);
+  h = __builtin_fma(h, r, h);
+  g = __builtin_fma(__builtin_fma(-g, g, s), h, g);
+  g = __builtin_fma(__builtin_fma(-g, g, s), h, g);
+  return s == 0.0 ? 0.0 : g;
+}
+
+// |(a, b)| / sqrt(d) in fp64: a^2 and b^2 are exact for fp32 a, b, their sum rounds once.
+__device__ __forceinline__ double pair_norm_f64_lean(float a, float b, double inv_sqrt_d) {
+  const double ad = (double)a, bd = (double)b;
+  return sqrt_f64_lean(ad * ad + bd * bd) * inv_sqrt_d;
+}
+
+// ln(x) for a normal fp64 x > 0: x = m 2^e with m in [sqrt(1/2), sqrt(2)), ln m = 2 atanh(s),
+// s = (m - 1)/(m + 1), |s| <= 0.172, summed as 2 s (1 + s^2/3 + s^4/5 + ... + s^20/21) (the
+// next term is below 1e-17 relative); e ln 2 in two parts, the first exact for |e| < 2^11.
+__device__ __forceinline__ double ln_f64_lean(double x) {
+  int e = __builtin_amdgcn_frexp_exp(x);
+  double m = __builtin_amdgcn_frexp_mant(x);          // [1/2, 1)
+  const bool low = m < 0.70710678118654752440;
+  m = low ? 2.0 * m : m;
+  e = low ? e - 1 : e;
+  const double num = m - 1.0, den = m + 1.0;            // num exact (Sterbenz)
+  double y = __builtin_amdgcn_rcp(den);
+  y = __builtin_fma(__builtin_fma(-den, y, 1.0), y, y);
+  y = __builtin_fma(__builtin_fma(-den, y, 1.0), y, y);
+  double s = num * y;
+  s = __builtin_fma(__builtin_fma(-den, s, num), y, s);
+  const double z = s * s;
+  double p = 2.0 / 21.0;
+  p = __builtin_fma(p, z, 2.0 / 19.0);
+  p = __builtin_fma(p, z, 2.0 / 17.0);
+  p = __builtin_fma(p, z, 2.0 / 15.0);
+  p = __builtin_fma(p, z, 2.0 / 13.0);
+  p = __builtin_fma(p, z, 2.0 / 11.0);
+  p = __builtin_fma(p, z, 2.0 / 9.0);
+  p = __builtin_fma(p, z, 2.0 / 7.0);
+  p = __builtin_fma(p, z, 2.0 / 5.0);
+  p = __builtin_fma(p, z, 2.0 / 3.0);
+  const double ln_m = __builtin_fma(s * z, p, 2.0 * s);
+  const double ed = (double)e;
+  return __builtin_fma(ed, 6.93147180369123816490e-01,
+                       __builtin_fma(ed, 1.90821492927058770002e-10, ln_m));
+}
+
+// Norm code of the fp64 code coordinate t (eq. (2)): clamp(floor(t + 1/2), 0, levels); a NaN
+// coordinate (non-finite input) gives 0.
+__device__ __forceinline__ uint32_t code_of_t(double t, double levels) {
+  return (uint32_t)fmin(fmax(floor(t + 0.5), 0.0), levels);
 }
 
 // c[15:0] * m[15:0] + acc in one instruction (m from a scalar register)
@@ -350,7 +401,8 @@ __device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const En
 
 // Encode one tile.  WA = angle code width and NB = norm code width of a format fixed at
 // compile time (NB = 8: linear norms, NB = 4: log-space norms; the angle codebook is then
-// n = 2^WA), or WA = NB = 0 for the segment's run-time format.
+// n = 2^WA), or WA = NB = 0 for the segment's run-time format.  Returns true (wave-uniform) when
+// the tile's norm codes need the fp64 norm pass (encode_norms_f64).
 // Record words per vector slot of the group-packing buffer: a group-packed record holds at
 // most 96 bytes at d = 128 (16 groups of 48 bits) and 48 at d = 64.
 template <int D>
@@ -489,9 +541,112 @@ __device__ __forceinline__ float vector_max(float v) {
   }
 }
 
+// Sign flip (sign-bit XOR, exact), widening to fp32 and the Walsh-Hadamard butterfly (stages
+// h = 1 .. d/2 in ascending order) of a lane's 32 elements.  Afterwards the lane holds
+// sigma * z (see fwht_cross_lane_signed), or z with the matrix-core front end.
+template <int D, bool F32IN, bool MF>
+__device__ __forceinline__ void transform_tile(const EncWave<D>& w, const Raw<F32IN>& raw,
+                                               float (&x)[kElemsPerLane]) {
+  constexpr int LPV = EncWave<D>::LPV;
+  uint32_t sm[16];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const u32x4a v = *(const u32x4a*)(w.sm + 4 * q);
+    sm[4 * q] = v.x, sm[4 * q + 1] = v.y, sm[4 * q + 2] = v.z, sm[4 * q + 3] = v.w;
+  }
+  if constexpr (MF) {
+    front_mfma(raw.w, sm, x);
+  } else {
+    if constexpr (F32IN) {
+#pragma unroll
+      for (int m = 0; m < 16; ++m) {
+        x[2 * m] = __uint_as_float(raw.w[2 * m] ^ (sm[m] << 16));
+        x[2 * m + 1] = __uint_as_float(raw.w[2 * m + 1] ^ (sm[m] & 0x80000000u));
+      }
+    } else {
+#pragma unroll
+      for (int m = 0; m < 16; ++m) {
+        const uint32_t wv = raw.w[m] ^ sm[m];
+        x[2 * m] = __uint_as_float(wv << 16);
+        x[2 * m + 1] = __uint_as_float(wv & 0xFFFF0000u);
+      }
+    }
+    fwht_in_lane(x);
+    fwht_cross_lane_signed<LPV>(x, w.sub);
+  }
+}
+
+// Store a lane's 16 norm codes (low bits of qc) and its vector's header.  ALIGNED: the tile's
+// records are consecutive from the uniform record of its first vector (the lane's offset is
+// added as a 32-bit offset to that scalar address).
+template <int D, int NB, bool ALIGNED>
+__device__ __forceinline__ void store_norms(const EncWave<D>& w, uint32_t slot, uint32_t nbits,
+                                            const uint32_t (&qc)[kPairsPerLane], float rmin,
+                                            float rmax) {
+  uint8_t* rec_nrm = w.plane[1] + (uint64_t)slot * w.sp.rec[1];
+  const uint32_t lane_nrm = ALIGNED ? (uint32_t)w.vslot * w.sp.rec[1] : 0u;
+  const uint32_t lane_hdr = ALIGNED ? (uint32_t)w.vslot * 8u : 0u;
+  if constexpr (NB == 4)
+    store_chunk<4>(rec_nrm + (lane_nrm + 8u * (uint32_t)w.sub), pack16_nibbles(qc));
+  else if constexpr (NB == 8)
+    store_chunk<8>(rec_nrm + (lane_nrm + 16u * (uint32_t)w.sub), pack16<8>(qc));
+  else
+    store_codes_any(rec_nrm, w.sub, nbits, qc);
+  // every lane of the vector writes the same header bytes
+  *(u32x2*)(w.plane[2] + (uint64_t)slot * 8 + lane_hdr) =
+      u32x2{__float_as_uint(rmin), __float_as_uint(rmax)};
+}
+
+// The fp64 norm pass of a tile (norm modes 1 and 2), for tiles whose vectors have a narrow
+// spread of pair norms or values near the ends of the fp32 range, and zero and one-hot
+// vectors (encode_tile tells which): the pair norms in fp64 as the definition forms them (no
+// overflow or underflow of a^2 + b^2), the header their fp32 roundings, and t of eq. (2) (or of
+// its log-space variant, as ln(r / R'min)) in fp64.  Its error is then ~1e-16 relative to the
+// norm, so even the narrowest range (one fp32 ulp) leaves it far inside the flag zone.  It runs
+// after the tile loop, on the tile's input loaded again, and overwrites the codes and header
+// the loop stored: its temporaries and constants then stay out of the loop's registers.  The
+// norms are formed twice (for the extremes, then for the codes) rather than kept.
+template <int D, bool F32IN, int NB, bool PAGED, bool MF, bool ALIGNED>
+__device__ __forceinline__ void encode_norms_f64(const EncWave<D>& w, const TileIn<F32IN>& in) {
+  constexpr int LPV = EncWave<D>::LPV;
+  const uint32_t nbits = NB ? (uint32_t)NB : w.sp.bits;
+  const uint32_t mode = NB ? (NB == 8 ? 1u : 2u) : w.sp.mode;
+  float x[kElemsPerLane];
+  transform_tile<D, F32IN, MF>(w, in.raw, x);
+  const double inv_sqrt_d = 1.0 / sqrt((double)D);
+  float l0 = FLT_MAX, l1 = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kPairsPerLane; ++i) {
+    const float rf = (float)pair_norm_f64_lean(x[2 * i], x[2 * i + 1], inv_sqrt_d);
+    l0 = fminf(l0, rf);
+    l1 = fmaxf(l1, rf);
+  }
+  const float rmin = vector_min<MF, LPV>(l0);
+  const float rmax = vector_max<MF, LPV>(l1);
+  const double lv = (double)((1u << (nbits & 31u)) - 1u);
+  const double r0 = (double)rmin;
+  uint32_t qc[kPairsPerLane];
+  if (mode == 1) {
+    const double scale = (rmax == rmin) ? 0.0 : lv / ((double)rmax - r0);
+#pragma unroll
+    for (int i = 0; i < kPairsPerLane; ++i)
+      qc[i] = code_of_t((pair_norm_f64_lean(x[2 * i], x[2 * i + 1], inv_sqrt_d) - r0) * scale, lv);
+  } else {
+    const double c0 = fmax(r0, (double)FLT_MIN), c1 = fmax((double)rmax, (double)FLT_MIN);
+    const double rc = 1.0 / c0;
+    const double scale = (c1 == c0) ? 0.0 : lv / ln_f64_lean(c1 * rc);
+#pragma unroll
+    for (int i = 0; i < kPairsPerLane; ++i) {
+      const double r = fmax(pair_norm_f64_lean(x[2 * i], x[2 * i + 1], inv_sqrt_d), (double)FLT_MIN);
+      qc[i] = code_of_t(ln_f64_lean(r * rc) * scale, lv);
+    }
+  }
+  if (!PAGED || in.ok) store_norms<D, NB, ALIGNED>(w, in.slot, nbits, qc, rmin, rmax);
+}
+
 template <int D, bool F32IN, int WA, int NB, bool PAGED, bool MF = false, bool BINS = false,
           bool ALIGNED = false>
-__device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D>& w,
+__device__ __forceinline__ bool encode_tile(const EncodeArgs& a, const EncWave<D>& w,
                                             const TileIn<F32IN>& in) {
   static_assert(!MF || (D == 128 && !F32IN), "matrix-core front end: d = 128, bf16 input");
   const bool store = !PAGED || in.ok;
@@ -506,36 +661,8 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
   const uint32_t nbits = kFixed ? (uint32_t)NB : sp.bits;
   const float levels = (float)((1u << (nbits & 31u)) - 1u);
 
-  // ---- sign flip (sign-bit XOR, exact), widen to fp32 ----
-  uint32_t sm[16];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const u32x4a v = *(const u32x4a*)(w.sm + 4 * q);
-    sm[4 * q] = v.x, sm[4 * q + 1] = v.y, sm[4 * q + 2] = v.z, sm[4 * q + 3] = v.w;
-  }
   float x[kElemsPerLane];
-  if constexpr (MF) {
-    front_mfma(in.raw.w, sm, x);           // this lane holds z (no negated lanes)
-  } else {
-    if constexpr (F32IN) {
-#pragma unroll
-      for (int m = 0; m < 16; ++m) {
-        x[2 * m] = __uint_as_float(in.raw.w[2 * m] ^ (sm[m] << 16));
-        x[2 * m + 1] = __uint_as_float(in.raw.w[2 * m + 1] ^ (sm[m] & 0x80000000u));
-      }
-    } else {
-#pragma unroll
-      for (int m = 0; m < 16; ++m) {
-        const uint32_t wv = in.raw.w[m] ^ sm[m];
-        x[2 * m] = __uint_as_float(wv << 16);
-        x[2 * m + 1] = __uint_as_float(wv & 0xFFFF0000u);
-      }
-    }
-
-    // ---- Walsh-Hadamard butterfly, stages h = 1 .. d/2 in ascending order ----
-    fwht_in_lane(x);
-    fwht_cross_lane_signed<LPV>(x, w.sub);   // this lane now holds sigma * z
-  }
+  transform_tile<D, F32IN, MF>(w, in.raw, x);    // this lane holds sigma * z (or z)
 
   // ---- squared pair norms and the vector's extremes ----
   // s2 >= +0 (never -0), so its bit patterns order like its values: the extremes are taken
@@ -552,19 +679,21 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
   vector_minmax_bits<MF, LPV>(bmin, bmax);
   const float smin = __uint_as_float(bmin);
   const float smax = __uint_as_float(bmax);
-  // the fast formulas need every pair's max(|a|,|b|) inside [2^-61, 2^60] (every lane of the
-  // wave is active here)
+  // the fast angle and norm formulas need every pair's max(|a|,|b|) inside [2^-61, 2^60];
+  // the fp32 norm codes also need pair norms that are not all nearly equal, in every vector
+  // of the wave (kNormSpreadMinBits): otherwise the fp64 norm pass (every lane of the wave is
+  // active here)
   const bool fast = __builtin_amdgcn_ballot_w64(bmin < 0x03800000u || bmax > 0x7B800000u) == 0;
+  const bool fast_norm =
+      fast && __builtin_amdgcn_ballot_w64(bmax - bmin - kNormSpreadMinBits >=
+                                          kNormSpreadMaxBits - kNormSpreadMinBits) == 0;
+  const bool f64_norms = (kFixed || mode != 0) && !fast_norm;   // the caller's fp64 norm pass
 
   // ---- norms (first: the squared norms are then dead before the angle codes exist) ----
-  // aligned tiles: the tile's records are consecutive, from the uniform record of its first
-  // vector (the lane's offset is added as a 32-bit offset to that scalar address)
   static_assert(!ALIGNED || (kFixed && !MF && !PAGED), "aligned tiles: fast formats");
-  uint8_t* rec_nrm = w.plane[1] + (uint64_t)in.slot * sp.rec[1];
-  const uint32_t lane_nrm = ALIGNED ? (uint32_t)w.vslot * sp.rec[1] : 0u;
-  const uint32_t lane_hdr = ALIGNED ? (uint32_t)w.vslot * 8u : 0u;
   if (!kFixed && mode == 0) {
     // fp32 norms, rounded once from the fp64 value
+    uint8_t* rec_nrm = w.plane[1] + (uint64_t)in.slot * sp.rec[1];
     const double inv_sqrt_d = 1.0 / sqrt((double)D);
     uint32_t rn[kPairsPerLane];
 #pragma unroll
@@ -573,76 +702,36 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
     if (store) store_words<16>((uint32_t*)rec_nrm + 16 * w.sub, rn);
   } else {
     // qc: bits of t + 1.5*2^23, t the code coordinate of each pair (eq. (2) or its log
-    // variant); t stays within [-eps, 2^b - 1 + eps], so the low b bits are the code
+    // variant); t stays within [-eps, 2^b - 1 + eps], so the low b bits are the code.  The
+    // fp32 roundings of s2, of its square root or log and of the scale (a few units of 2^-24
+    // each) move t by a small fraction of the width of a bin boundary's flag zone while every
+    // vector's squared norms span a ratio in [2^-126, ~0.84] (kNormSpreadMinBits).  Otherwise
+    // (fast_norm false) what is stored here is replaced by the fp64 norm pass
+    // (encode_norms_f64), which the caller runs for this tile after its tile loop.
     uint32_t qc[kPairsPerLane];
-    float rmin, rmax;
-    if (fast) {
-      rmin = __builtin_amdgcn_sqrtf(smin * a.inv_d);
-      rmax = __builtin_amdgcn_sqrtf(smax * a.inv_d);
-      const bool degenerate = rmax == rmin;
-      if (mode == 1) {
-        // linear in r: sqrt(s2) is r * sqrt(d), the same affine map up to a common factor
-        // scale by rcp (1 ulp): t moves by < 2^-22 * levels, a tenth of the flag zone
-        const float k0 = __builtin_amdgcn_sqrtf(smin), k1 = __builtin_amdgcn_sqrtf(smax);
-        const float scale =
-            (degenerate || !(k1 > k0)) ? 0.0f : levels * __builtin_amdgcn_rcpf(k1 - k0);
+    const float rmin = __builtin_amdgcn_sqrtf(smin * a.inv_d);
+    const float rmax = __builtin_amdgcn_sqrtf(smax * a.inv_d);
+    if (mode == 1) {
+      // linear in r: sqrt(s2) is r * sqrt(d), the same affine map up to a common factor
+      const float k0 = __builtin_amdgcn_sqrtf(smin), k1 = __builtin_amdgcn_sqrtf(smax);
+      const float scale = levels * __builtin_amdgcn_rcpf(k1 - k0);
 #pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i)
-          qc[i] = __float_as_uint(
-              __builtin_fmaf(__builtin_amdgcn_sqrtf(s2[i]) - k0, scale, kRoundShift));
-      } else {
-        // log space: log2(s2 / smin) = 2 log2(r / Rmin) starts near 0, so the fp32 log
-        // outputs keep their precision (no cancellation against a large log of smin)
-        const float rs = __builtin_amdgcn_rcpf(smin);
-        const float k0 = __builtin_amdgcn_logf(smin * rs);   // ~0: rcp is not exact
-        const float k1 = __builtin_amdgcn_logf(smax * rs);
-        const float scale =
-            (degenerate || !(k1 > k0)) ? 0.0f : levels * __builtin_amdgcn_rcpf(k1 - k0);
-#pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i)
-          qc[i] = __float_as_uint(
-              __builtin_fmaf(__builtin_amdgcn_logf(s2[i] * rs) - k0, scale, kRoundShift));
-      }
+      for (int i = 0; i < kPairsPerLane; ++i)
+        qc[i] = __float_as_uint(
+            __builtin_fmaf(__builtin_amdgcn_sqrtf(s2[i]) - k0, scale, kRoundShift));
     } else {
-      // careful path: norms from fp64 (no overflow or underflow of a^2 + b^2), rounded once
-      // to fp32; the affine maps on r and on log r (as a ratio to the minimum, so the log
-      // input is >= 1) in fp32
-      const double inv_sqrt_d = 1.0 / sqrt((double)D);
-      float rf[kPairsPerLane];
-      float l0 = FLT_MAX, l1 = 0.0f;
+      // log space: log2(s2 / smin) = 2 log2(r / Rmin) starts near 0, so the fp32 log
+      // outputs keep their precision (no cancellation against a large log of smin)
+      const float rs = __builtin_amdgcn_rcpf(smin);
+      const float k0 = __builtin_amdgcn_logf(smin * rs);   // ~0: rcp is not exact
+      const float k1 = __builtin_amdgcn_logf(smax * rs);
+      const float scale = levels * __builtin_amdgcn_rcpf(k1 - k0);
 #pragma unroll
-      for (int i = 0; i < kPairsPerLane; ++i) {
-        rf[i] = (float)pair_norm_f64(x[2 * i], x[2 * i + 1], inv_sqrt_d);
-        l0 = fminf(l0, rf[i]);
-        l1 = fmaxf(l1, rf[i]);
-      }
-      rmin = vector_min<MF, LPV>(l0);
-      rmax = vector_max<MF, LPV>(l1);
-      if (mode == 1) {
-        const float scale = (rmax == rmin) ? 0.0f : levels / (rmax - rmin);
-#pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i)
-          qc[i] = __float_as_uint(__builtin_fmaf(rf[i] - rmin, scale, kRoundShift));
-      } else {
-        const float c0 = fmaxf(rmin, FLT_MIN);
-        const float rc = 1.0f / c0;
-        const float k1 = log2f(fmaxf(rmax, FLT_MIN) * rc);
-        const float scale = (fmaxf(rmax, FLT_MIN) == c0 || !(k1 > 0.0f)) ? 0.0f : levels / k1;
-#pragma unroll
-        for (int i = 0; i < kPairsPerLane; ++i)
-          qc[i] = __float_as_uint(
-              __builtin_fmaf(fmaxf(log2f(fmaxf(rf[i], FLT_MIN) * rc), 0.0f), scale, kRoundShift));
-      }
+      for (int i = 0; i < kPairsPerLane; ++i)
+        qc[i] = __float_as_uint(
+            __builtin_fmaf(__builtin_amdgcn_logf(s2[i] * rs) - k0, scale, kRoundShift));
     }
-    if (store) {
-      if constexpr (kFixed && NB == 4)
-        store_chunk<4>(rec_nrm + (lane_nrm + 8u * (uint32_t)w.sub), pack16_nibbles(qc));
-      else if constexpr (kFixed) store_chunk<NB>(rec_nrm + (lane_nrm + 2u * NB * (uint32_t)w.sub), pack16<NB>(qc));
-      else store_codes_any(rec_nrm, w.sub, nbits, qc);
-      // every lane of the vector writes the same header bytes
-      *(u32x2*)(w.plane[2] + (uint64_t)in.slot * 8 + lane_hdr) =
-          u32x2{__float_as_uint(rmin), __float_as_uint(rmax)};
-    }
+    if (store) store_norms<D, kFixed ? NB : 0, ALIGNED>(w, in.slot, nbits, qc, rmin, rmax);
   }
 
   // ---- angle codes ----
@@ -678,11 +767,11 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
   if constexpr (!kFixed) {
     if (sp.grp == 8) {
       store_angle_groups<D, 8>(w, sp, rec_ang, kc, store);
-      return;
+      return f64_norms;
     }
     if (sp.grp == 4) {
       store_angle_groups<D, 4>(w, sp, rec_ang, kc, store);
-      return;
+      return f64_norms;
     }
   }
   if (store) {
@@ -693,6 +782,7 @@ __device__ __forceinline__ void encode_tile(const EncodeArgs& a, const EncWave<D
       store_codes_any(rec_ang, w.sub, sp.w, kc);
     }
   }
+  return f64_norms;
 }
 
 // Tiles tile0 .. tile0 + ntiles - 1.  MULTI: two per iteration from two input buffers, each
@@ -710,14 +800,23 @@ __device__ void encode_tiles_fast(const EncodeArgs& a, const EncWave<D>& w, uint
   TileIn<false> ia = load_tile<D, false, PAGED, ALIGNED>(a, w, tile0);
   stage_tables<D>(a, w);
   if constexpr (!MULTI) {
-    encode_tile<D, false, WA, NB, PAGED, MF, false, ALIGNED>(a, w, ia);
+    if (encode_tile<D, false, WA, NB, PAGED, MF, false, ALIGNED>(a, w, ia))
+      encode_norms_f64<D, false, NB, PAGED, MF, ALIGNED>(w, ia);
     return;
   }
+  uint32_t redo = 0;    // tiles (bit tile - tile0) whose norms take the fp64 pass
   for (uint32_t t = tile0; t <= last; t += 2) {
-    const TileIn<false> ib = load_tile<D, false, PAGED, ALIGNED>(a, w, min(t + 1, last));
-    encode_tile<D, false, WA, NB, PAGED, MF, true, ALIGNED>(a, w, ia);
+    const uint32_t t1 = min(t + 1, last);
+    const TileIn<false> ib = load_tile<D, false, PAGED, ALIGNED>(a, w, t1);
+    if (encode_tile<D, false, WA, NB, PAGED, MF, true, ALIGNED>(a, w, ia)) redo |= 1u << (t - tile0);
     ia = load_tile<D, false, PAGED, ALIGNED>(a, w, min(t + 2, last));
-    encode_tile<D, false, WA, NB, PAGED, MF, true, ALIGNED>(a, w, ib);
+    if (encode_tile<D, false, WA, NB, PAGED, MF, true, ALIGNED>(a, w, ib)) redo |= 1u << (t1 - tile0);
+  }
+  while (redo != 0) {
+    const uint32_t k = __builtin_ctz(redo);
+    redo &= redo - 1;
+    encode_norms_f64<D, false, NB, PAGED, MF, ALIGNED>(
+        w, load_tile<D, false, PAGED, ALIGNED>(a, w, tile0 + k));
   }
 }
 
@@ -768,7 +867,8 @@ __global__ __launch_bounds__(kBlockThreads) void encode_generic_kernel(EncodeArg
   w.grp_lds = s_grp[threadIdx.x / kWave];
   const TileIn<F32IN> in = load_tile<D, F32IN, PAGED>(a, w, tile0);
   stage_tables<D>(a, w);
-  encode_tile<D, F32IN, 0, 0, PAGED>(a, w, in);
+  if (encode_tile<D, F32IN, 0, 0, PAGED>(a, w, in))
+    encode_norms_f64<D, F32IN, 0, PAGED, false, false>(w, in);
 }
 
 template <int D, bool PAGED>

@@ -145,6 +145,23 @@ inline bool fast_format(uint32_t n, uint32_t mode, uint32_t bits) {
 
 constexpr uint32_t kFastTilesPerWave = 4;
 
+// atan(t) / (2 pi) for t in [0, 1] as t * p(t^2), p of degree 5 in t^2 (an odd polynomial of
+// degree 11 fitted for minimum maximum error, 2.8e-7 of a turn in fp32).  Coefficients from
+// the highest power of t^2 down to the constant term.
+constexpr float kAtanTurnsPoly[6] = {-1.865156344e-03f, 8.379081264e-03f, -1.852984540e-02f,
+                                     3.080290556e-02f, -5.293856561e-02f, 1.591513157e-01f};
+
+// Spread rule of the fp32 norm-code formulas of the encode.  bits(s2_max) - bits(s2_min), the
+// difference of the bit patterns of a vector's largest and smallest squared pair norms, is
+// 2^23 log2(s2_max / s2_min) to within 0.09 * 2^23.  The fp32 formulas are used when it lies in
+// [kNormSpreadMinBits, kNormSpreadMaxBits): a ratio s2_min / s2_max below ~0.84 (nearer to 1 the
+// code coordinate of eq. (2) divides the rounding error of the norms by a vanishing range, and
+// equal norms give no range at all) and above 2^-126 (the log formulas' s2 / s2_min stays
+// finite).  Vectors outside it, and tiles with values near the ends of the fp32 range, take
+// their norm codes from the fp64 pass.
+constexpr uint32_t kNormSpreadMinBits = 1u << 21;
+constexpr uint32_t kNormSpreadMaxBits = 126u << 23;
+
 }  // namespace tvq
 
 // Kernel launchers (defined in the .hip kernel files).

@@ -323,3 +323,37 @@ def test_binding_raises_without_the_library(tmp_path):
                        text=True, timeout=120, env={**os.environ, "PYTHONPATH": str(tmp_path)})
     assert r.returncode == 0, r.stderr
     assert r.stdout.startswith("raised:") and "libtvq.so is missing" in r.stdout, r.stdout
+
+
+def test_binding_checks_extents_before_any_call(tvq):
+    """The binding rejects, before it calls the library, tensors whose layers, heads or head
+    dim differ from the codec's, caches and pools smaller than their layout, and queries of
+    another head dim: the kernels size their accesses from the codec and the layout, so such a
+    tensor would be read or written past its end.  (A codec object without a device handle
+    stands in for a live one; each call must fail in the binding.)"""
+    import torch
+    c = tvq.Codec.__new__(tvq.Codec)
+    c.L, c.H, c.d, c.handle = 2, 4, 128, 0
+    lay = tvq.tvq_layout()
+    lay.total_bytes, lay.batch, lay.capacity_tokens = 4096, 1, 8
+    cache = torch.zeros(4096, dtype=torch.uint8)
+    good = torch.zeros((2, 1, 4, 8, 128), dtype=torch.bfloat16)
+    for bad in (torch.zeros((1, 1, 4, 8, 128), dtype=torch.bfloat16),     # fewer layers
+                torch.zeros((2, 1, 3, 8, 128), dtype=torch.bfloat16),     # fewer heads
+                torch.zeros((2, 1, 4, 8, 64), dtype=torch.bfloat16)):     # other head dim
+        with pytest.raises(ValueError, match="codec needs"):
+            c.encode(bad, bad, cache, lay)
+        with pytest.raises(ValueError, match="codec needs"):
+            c.decode(cache, lay, 0, 8, bad, bad)
+    for small in (torch.zeros(4095, dtype=torch.uint8), torch.zeros(4096, dtype=torch.int8),
+                  torch.zeros(8192, dtype=torch.uint8)[::2]):
+        with pytest.raises(ValueError, match="cache"):
+            c.encode(good, good, small, lay)
+        with pytest.raises(ValueError, match="cache"):
+            c.decode(small, lay, 0, 8, good, good)
+    q = torch.zeros((1, 8, 64))
+    with pytest.raises(ValueError, match="head dim"):
+        c.attention(cache, lay, 0, 8, q, torch.zeros_like(q), 0.1)
+    q = torch.zeros((1, 8, 128))
+    with pytest.raises(ValueError, match="cache"):
+        c.attention(torch.zeros(100, dtype=torch.uint8), lay, 0, 8, q, torch.zeros_like(q), 0.1)

@@ -17,8 +17,8 @@ import oracle
 import workloads
 from workloads import LayerCfg, NORM_LINEAR, NORM_LOG
 
-from parity import (Setup, attention_error_bar, bf16_bits_to_torch, compare_encode,
-                    gather_paged, torch_to_np)
+from parity import (DecodeCheck, Setup, attention_error_bar, bf16_bits_to_torch,
+                    check_decoded, compare_encode, gather_paged, torch_to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -155,6 +155,7 @@ def test_paged_encode_decode(gpu, d):
 
     # decode every position of every sequence through the table
     shape = (case.L, case.B, case.H, case.cap, d)
+    chk, chk16 = DecodeCheck(), DecodeCheck()
     for dt in (torch.float32, torch.bfloat16):
         ko = torch.full(shape, float("nan"), dtype=dt, device="cuda")
         vo = torch.full(shape, float("nan"), dtype=dt, device="cuda")
@@ -168,20 +169,20 @@ def test_paged_encode_decode(gpu, d):
             w = case.written[b].astype(np.int8)
             edges = np.flatnonzero(np.diff(np.concatenate([[0], w, [0]])))
             for a, e in zip(edges[0::2], edges[1::2]):
-                ref = case.s.orc.decode_cache(gath[b], 1, case.cap, a, e, "f32")[:, :, 0]
+                ref64 = case.s.orc.decode_cache(gath[b], 1, case.cap, a, e, "f64")[:, :, 0]
+                mirror = case.s.orc.decode_cache(gath[b], 1, case.cap, a, e, "f32")[:, :, 0]
                 gw = gb[..., a:e, :]
                 if dt == torch.float32:
-                    same = (gw.view(np.uint32) == ref.view(np.uint32)) | ((gw == 0) & (ref == 0))
-                    assert same.all(), f"sequence {b} [{a}, {e}): fp32 decode differs"
+                    check_decoded(chk, ref64, d, g32=gw, mirror32=mirror)
                 else:
-                    rb = oracle.f32_to_bf16(ref)
-                    zero = ((gw & 0x7FFF) == 0) & ((rb & 0x7FFF) == 0)
-                    assert np.all((gw == rb) | zero), f"sequence {b} [{a}, {e}): bf16 differs"
+                    check_decoded(chk16, ref64, d, g16=gw)
+                assert chk.ok() and chk16.ok(), f"sequence {b} [{a}, {e}): {chk.line()} / {chk16.line()}"
             if dt == torch.float32:
                 assert np.all(gb[..., ~has, :] == 0)
             else:
                 assert np.all((gb[..., ~has, :] & 0x7FFF) == 0)
-    _say(f"[paged-decode-d{d}] fp32 bit-exact on written positions, zeros without a block")
+    _say(f"[paged-decode-d{d}] written positions against the fp64 decode: fp32 {chk.line()}; "
+         f"bf16 {chk16.line()}; zeros without a block")
 
 
 @pytest.mark.parametrize("d,G", [(128, 4), (64, 3)])
@@ -292,6 +293,9 @@ def test_paged_api_errors(gpu):
     pos = torch.zeros(3, dtype=torch.int32, device="cuda")
     bad_lay = s.pool_layout(case.n_blocks, 48)            # block size not a power of two
     with pytest.raises(tvq.TvqError):
+        s.encode_paged(k, k, pos, case.table_dev,
+                       torch.zeros(bad_lay.total_bytes, dtype=torch.uint8, device="cuda"), bad_lay)
+    with pytest.raises(ValueError, match="pool"):         # a pool smaller than its layout
         s.encode_paged(k, k, pos, case.table_dev, case.pool, bad_lay)
     small = s.pool_layout(case.n_blocks, 16)              # below 32 slots
     with pytest.raises(tvq.TvqError):

@@ -688,3 +688,63 @@ def test_group_packed_cache_decodes_the_same(orc):
                               c1.decode_cache(b1, 1, T, 0, T, prec))
     c64 = orc.Codec(1, 2, 64, kinds, sg[:, :64], packing=1)
     assert c64.record_bytes(0, 0)[0] == 23
+
+
+# --------------------------------------------------------------------------- norm flag rule
+def test_norm_flag_zones_worked_examples(orc):
+    """The two zones the norm flag rule joins, on hand-worked cases (section 3.3, eq. (2) and
+    its log variant inverted at a boundary t_b = m + 1/2):
+    linear, R = [1, 2], 8 bits (step 1/255):
+      t = 0.5 + 1e-4: |r - r_b| = 1e-4/255 = 3.9e-7 of r_b = 1.00196 -> both zones;
+      t = 0.5 + 3e-4: 3e-4 > 2.55e-4 (code range) and 1.17e-6 of r_b -> neither;
+    linear, R = [1, 1.001] (step 3.92e-6): t = 100.5 + 0.1 is 0.1 code units (outside the
+      code-range zone) but 3.9e-7 of r_b -> the norm-relative zone only; t = 100.8 neither;
+    log, R = [1, e^15], 4 bits (one unit of ln r per code):
+      t = 3.5 + 5e-7: ln r - ln r_b = 5e-7 -> both; t = 3.5 + 2e-6: 2e-6 > 1e-6 relative
+      but inside 1.5e-5 of the code range -> the code-range zone only;
+    a NaN coordinate (degenerate vector) and t just below 0 (no boundary) are never flagged."""
+    L8, LOG = orc.NORM_LINEAR, orc.NORM_LOG
+    h12 = np.array([[1.0, 2.0]], np.float32)
+    t = np.array([[0.5 + 1e-4, 0.5 + 3e-4, np.nan, -1e-9]])
+    assert orc.norm_flags_range(t, 8).tolist() == [[True, False, False, False]]
+    assert orc.norm_flags_value(t, 8, h12, L8).tolist() == [[True, False, False, False]]
+    narrow = np.array([[1.0, 1.001]], np.float32)
+    t = np.array([[100.6, 100.8]])
+    assert orc.norm_flags_range(t, 8).tolist() == [[False, False]]
+    assert orc.norm_flags_value(t, 8, narrow, L8).tolist() == [[True, False]]
+    assert orc.norm_flags(t, 8, narrow, L8).tolist() == [[True, False]]
+    hl = np.array([[1.0, np.exp(15.0)]], np.float32)
+    step = (np.log(np.float64(hl[0, 1])) - 0.0) / 15
+    t = np.array([[3.5 + 5e-7 / step, 3.5 + 2e-6 / step, 3.5 + 2e-5 / step]])
+    assert orc.norm_flags_value(t, 4, hl, LOG).tolist() == [[True, False, False]]
+    assert orc.norm_flags_range(t, 4).tolist() == [[True, True, False]]
+    assert orc.norm_flags(t, 4, hl, LOG).tolist() == [[True, True, False]]
+
+
+def test_norm_flag_value_zone_matches_the_definition(orc):
+    """The norm-relative zone equals its definition written out on random vectors: the
+    boundary norm r_b of the nearest rounding boundary formed from the stored header, and
+    |r - r_b| < 1e-6 r_b with r = sqrt(a^2 + b^2)/sqrt(d) of the fp32 butterfly output (the
+    oracle's own t is not used for r)."""
+    rng = np.random.default_rng(17)
+    d = 64
+    s = orc.signs(3, 0, d)
+    for mode, bits in ((orc.NORM_LINEAR, 8), (orc.NORM_LOG, 4)):
+        for c in (0.0, 30.0, 300.0):
+            x = rng.standard_normal(d).astype(np.float32)
+            x[5] += np.float32(c)
+            v = orc.encode_vector(x, s, orc.Kind(64, mode, bits))
+            z = v.z.astype(np.float64)
+            r = np.sqrt(z[0::2] ** 2 + z[1::2] ** 2) / np.sqrt(d)
+            R0, R1 = float(v.hdr[0]), float(v.hdr[1])
+            lv = 2 ** bits - 1
+            tb = np.floor(v.t) + 0.5
+            if mode == orc.NORM_LINEAR:
+                rb = R0 + tb * (R1 - R0) / lv
+            else:
+                rb = np.exp(np.log(R0) + tb * (np.log(R1) - np.log(R0)) / lv)
+            want = np.abs(r - rb) < 1e-6 * rb
+            got = orc.norm_flags_value(v.t, bits, v.hdr, mode)
+            # agree except where |r - r_b| / r_b sits within rounding of 1e-6
+            close = np.abs(np.abs(r - rb) / rb - 1e-6) < 1e-12
+            assert np.array_equal(got[~close], want[~close])
