@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define TVQ_ABI_VERSION 2
+#define TVQ_ABI_VERSION 3
 #define TVQ_MAX_LAYERS 256
 
 typedef enum {
@@ -43,7 +43,9 @@ typedef enum {
   TVQ_ERR_INVALID_ARG = -1,  /* a pointer, size, stride, alignment or config value is bad */
   TVQ_ERR_UNSUPPORTED = -2,  /* valid for the method but not built for the GPU (e.g. d=32) */
   TVQ_ERR_HIP = -3,          /* a HIP runtime call or kernel launch failed */
-  TVQ_ERR_ALLOC = -4         /* tvq_create could not allocate its device tables */
+  TVQ_ERR_ALLOC = -4,        /* tvq_create could not allocate its device tables */
+  TVQ_ERR_SCRATCH = -5       /* the call needs more scratch than the library's static buffer
+                                holds (tvq_attention_decode_noalloc) */
 } tvq_status;
 
 typedef enum { TVQ_BF16 = 0, TVQ_F32 = 1 } tvq_dtype;
@@ -192,6 +194,27 @@ tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq
                                 int32_t layer, int64_t t_end, int32_t num_q_heads, float scale,
                                 tvq_dtype q_dtype, const void* q, tvq_dtype o_dtype, void* o,
                                 void* workspace, int64_t workspace_bytes, void* stream);
+
+/* Bytes of the device scratch that tvq_attention_decode_noalloc uses in place of a workspace:
+ * one static array per GPU, held from the library's first use of that GPU until the process
+ * ends (16 MiB; the long-context shape of 16 sequences x 32 query heads x 32K tokens at d = 128
+ * needs 6.4 MB). */
+#define TVQ_ATTENTION_SCRATCH_BYTES (16 * 1024 * 1024)
+
+/* tvq_attention_decode without the workspace argument, for callers that cannot allocate
+ * device memory (code under graph capture, serving loops that forbid allocation): the
+ * per-chunk partials go to the library's static scratch on the codec's device.  Allocates
+ * nothing and calls no allocating routine; arguments, results and launches are those of
+ * tvq_attention_decode.  TVQ_ERR_SCRATCH, with nothing launched, when the call's partials
+ * (tvq_attention_workspace) exceed TVQ_ATTENTION_SCRATCH_BYTES; TVQ_ERR_HIP when the scratch's
+ * device address could not be obtained at tvq_create.  Every call on one GPU shares that
+ * scratch: calls that overlap in time on one GPU (concurrent streams, or host threads each
+ * launching) race on it and must be ordered by the caller.  The scratch needs no clearing:
+ * each call writes every partial it reads. */
+tvq_status tvq_attention_decode_noalloc(const tvq_codec* c, const void* cache,
+                                        const tvq_layout* lay, int32_t layer, int64_t t_end,
+                                        int32_t num_q_heads, float scale, tvq_dtype q_dtype,
+                                        const void* q, tvq_dtype o_dtype, void* o, void* stream);
 
 /* ---- paged caches (serving) ----
  * A paged pool holds fixed-size blocks of cache slots shared by many sequences.  Its byte

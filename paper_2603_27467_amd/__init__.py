@@ -15,7 +15,8 @@ from ._capi import (  # noqa: F401
     tvq_status_string, tvq_make_signs, tvq_bits_per_element_config, tvq_make_trig_table,
     tvq_make_decode_table, tvq_make_angle_bins, tvq_encode_constants, tvq_layout_for_config,
     tvq_attention_workspace,
-    tvq_attention_decode,
+    tvq_attention_decode, tvq_attention_decode_noalloc, TVQ_ERR_SCRATCH,
+    TVQ_ATTENTION_SCRATCH_BYTES,
     tvq_encode_mfma, tvq_encode_paged, tvq_decode_paged, tvq_attention_paged_workspace, tvq_attention_paged,
     tvq_abi_version, library_path, load_library,
 )

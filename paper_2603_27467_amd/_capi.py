@@ -6,9 +6,11 @@ import os
 
 import numpy as np
 
-TVQ_ABI_VERSION = 2
+TVQ_ABI_VERSION = 3
 TVQ_MAX_LAYERS = 256
 TVQ_OK, TVQ_ERR_INVALID_ARG, TVQ_ERR_UNSUPPORTED, TVQ_ERR_HIP, TVQ_ERR_ALLOC = 0, -1, -2, -3, -4
+TVQ_ERR_SCRATCH = -5
+TVQ_ATTENTION_SCRATCH_BYTES = 16 * 1024 * 1024
 TVQ_BF16, TVQ_F32 = 0, 1
 TVQ_NORM_F32, TVQ_NORM_LINEAR, TVQ_NORM_LOG = 0, 1, 2
 
@@ -82,6 +84,10 @@ def load_library():
     L.tvq_attention_decode.argtypes = [vp, vp, ctypes.POINTER(tvq_layout), i32, i64, i32,
                                        ctypes.c_float, ctypes.c_int, vp, ctypes.c_int, vp, vp, i64,
                                        vp]
+    L.tvq_attention_decode_noalloc.restype = ctypes.c_int
+    L.tvq_attention_decode_noalloc.argtypes = [vp, vp, ctypes.POINTER(tvq_layout), i32, i64, i32,
+                                               ctypes.c_float, ctypes.c_int, vp, ctypes.c_int,
+                                               vp, vp]
     L.tvq_encode_mfma.restype = ctypes.c_int
     L.tvq_encode_mfma.argtypes = [vp, vp, vp, ctypes.POINTER(tvq_tensor_desc), i64, vp,
                                   ctypes.POINTER(tvq_layout), vp]
@@ -195,6 +201,15 @@ def tvq_attention_decode(handle: int, cache_ptr: int, lay: tvq_layout, layer: in
         num_q_heads, ctypes.c_float(scale), q_dtype, ctypes.c_void_p(q_ptr), o_dtype,
         ctypes.c_void_p(o_ptr), ctypes.c_void_p(ws_ptr), ws_bytes, ctypes.c_void_p(stream)),
         "tvq_attention_decode")
+
+
+def tvq_attention_decode_noalloc(handle: int, cache_ptr: int, lay: tvq_layout, layer: int,
+                                 t_end: int, num_q_heads: int, scale: float, q_dtype: int,
+                                 q_ptr: int, o_dtype: int, o_ptr: int, stream: int = 0) -> None:
+    _check(load_library().tvq_attention_decode_noalloc(
+        ctypes.c_void_p(handle), ctypes.c_void_p(cache_ptr), ctypes.byref(lay), layer, t_end,
+        num_q_heads, ctypes.c_float(scale), q_dtype, ctypes.c_void_p(q_ptr), o_dtype,
+        ctypes.c_void_p(o_ptr), ctypes.c_void_p(stream)), "tvq_attention_decode_noalloc")
 
 
 def tvq_encode_mfma(handle: int, k_ptr: int, v_ptr: int, desc: tvq_tensor_desc, t_begin: int,

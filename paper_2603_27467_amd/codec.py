@@ -172,6 +172,21 @@ class Codec:
                                scale, dts[q.dtype], q.data_ptr(), dts[out.dtype], out.data_ptr(),
                                workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
 
+    def attention_noalloc(self, cache, lay: C.tvq_layout, layer: int, t_end: int, q, out,
+                          scale: float, stream=None) -> None:
+        """attention without a workspace (tvq_attention_decode_noalloc): the partials go to
+        the library's static scratch; nothing is allocated, by the library or here."""
+        import torch
+        self._check_q(q, out)
+        _check_bytes(cache, lay, "cache")
+        _on_gpu(q, out, cache)
+        dts = {torch.bfloat16: C.TVQ_BF16, torch.float32: C.TVQ_F32}
+        if q.dtype not in dts or out.dtype not in dts:
+            raise ValueError("q/out must be bf16 or fp32")
+        C.tvq_attention_decode_noalloc(self.handle, cache.data_ptr(), lay, layer, t_end,
+                                       q.shape[1], scale, dts[q.dtype], q.data_ptr(),
+                                       dts[out.dtype], out.data_ptr(), _stream_handle(stream))
+
     # ---- paged pools (tvq_encode_paged / tvq_decode_paged / tvq_attention_paged) ----
     def pool_layout(self, n_blocks: int, block_tokens: int) -> C.tvq_layout:
         """Layout of a paged pool of n_blocks blocks of block_tokens slots."""

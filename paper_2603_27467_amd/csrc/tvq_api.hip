@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -23,6 +24,7 @@ struct tvq_codec {
   std::vector<tvq::SegParams> segs;          // [2L]
   uint64_t rec_total = 0;                    // record bytes of all planes, per slot
   int device = 0;
+  void* scratch = nullptr;                   // the static attention scratch on `device`
   int64_t attn_slots = 0;                    // chunk waves the device holds at once (d = 64, 128)
   tvq::SegParams* d_segs = nullptr;
   uint32_t* d_sign_masks = nullptr;
@@ -32,7 +34,34 @@ struct tvq_codec {
   uint32_t n_fast = 0, n_generic = 0;
 };
 
+// Scratch of tvq_attention_decode_noalloc: the attention partials of one call, in a static
+// device array instead of a caller's workspace.  Each GPU holds its own copy at its own
+// address; host code never uses the array's name as a device address (it is a host-side
+// stand-in), only the per-device address that hipGetSymbolAddress returns with that device
+// current (scratch_address).
+static __device__ __align__(256) uint8_t scratch[TVQ_ATTENTION_SCRATCH_BYTES];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// The scratch's address on `device`, which must be the current device; looked up once per
+// device.  nullptr on a HIP error.
+void* scratch_address(int device) {
+  if (device < 0 || device >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[device]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch[device] = p;
+  }
+  return g_scratch[device];
+}
 
 constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ULL;
 
@@ -232,6 +261,7 @@ const char* tvq_status_string(tvq_status s) {
     case TVQ_ERR_UNSUPPORTED: return "unsupported configuration";
     case TVQ_ERR_HIP: return "HIP runtime error";
     case TVQ_ERR_ALLOC: return "device allocation failed";
+    case TVQ_ERR_SCRATCH: return "needs more scratch than the static buffer holds";
   }
   return "unknown status";
 }
@@ -419,6 +449,9 @@ tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out) {
     delete c;
     return TVQ_ERR_HIP;
   }
+  // the static attention scratch of this device (tvq_attention_decode_noalloc); a failure
+  // leaves it null and only that entry point reports it
+  c->scratch = scratch_address(c->device);
   if (d == 64 || d == 128) {
     int n_cu = 0;
     const int blocks = tvq_attention_blocks_per_cu(d);
@@ -834,6 +867,20 @@ tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq
   a.cap = (uint32_t)lay->capacity_tokens;
   return attention_launch(c, a, lay->batch, layer, t_end, 0, num_q_heads, scale, q_dtype, q,
                           o_dtype, o, workspace, workspace_bytes, stream);
+}
+
+tvq_status tvq_attention_decode_noalloc(const tvq_codec* c, const void* cache,
+                                        const tvq_layout* lay, int32_t layer, int64_t t_end,
+                                        int32_t num_q_heads, float scale, tvq_dtype q_dtype,
+                                        const void* q, tvq_dtype o_dtype, void* o, void* stream) {
+  if (!c || !lay) return TVQ_ERR_INVALID_ARG;
+  AttnPlan p;
+  const tvq_status st = attn_plan(c, lay->batch, num_q_heads, t_end, 0, &p);
+  if (st != TVQ_OK) return st;
+  if (p.ws_bytes > (int64_t)TVQ_ATTENTION_SCRATCH_BYTES) return TVQ_ERR_SCRATCH;
+  if (!c->scratch) return TVQ_ERR_HIP;
+  return tvq_attention_decode(c, cache, lay, layer, t_end, num_q_heads, scale, q_dtype, q,
+                              o_dtype, o, c->scratch, TVQ_ATTENTION_SCRATCH_BYTES, stream);
 }
 
 tvq_status tvq_attention_paged(const tvq_codec* c, const void* pool, const tvq_layout* pool_layout,
