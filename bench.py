@@ -207,6 +207,60 @@ def _find(dirpath: str, suffix: str) -> str:
     raise FileNotFoundError(f"no *{suffix} under {dirpath}")
 
 
+# dispatches of each codec kernel in the kernel-trace run that are timed steps (the last 20 of
+# `bench.py --steps 20 --warmup 3`: before them the encode fills two caches and both directions
+# run the warm-up steps)
+TRACE_TIMED_DISPATCHES = 20
+
+
+def shader_engines(trace_dir):
+    """(shader engines, XCDs) of the GPU agent (rocprofv3 agent_info.csv, the agent with
+    compute units)."""
+    try:
+        rows = _csv(_find(trace_dir, "agent_info.csv"))
+    except (OSError, FileNotFoundError, StopIteration):
+        return 32, 8
+    gpu = max(rows, key=lambda r: int(r.get("Cu_Count") or 0))
+    return int(gpu.get("Array_Count") or 32) or 32, int(gpu.get("Num_Xcc") or 8) or 8
+
+
+def dispatch_timeline(trace_dir) -> dict:
+    """Per codec entry point, the durations (ns) of its dispatches in issue order
+    (kernel_trace.csv)."""
+    rows = _csv(_find(trace_dir, "kernel_trace.csv"))
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    out = {}
+    for r in rows:
+        k = _short(r["Kernel_Name"])
+        if k in ("tvq_encode", "tvq_decode", "tvq_attention"):
+            out.setdefault(k, []).append(float(r["End_Timestamp"]) - float(r["Start_Timestamp"]))
+    return out
+
+
+def clock_fields(d: dict, topo, durations, timed: int) -> dict:
+    """The shader clock of an entry point's kernel.  GRBM_GUI_ACTIVE counts the cycles the
+    graphics engine is active, summed over the XCDs: per XCD over the duration of a counted
+    dispatch (which runs alone in the counter run) it is the clock of that dispatch.  Over the
+    mean of the timed dispatches of the kernel-trace run, where launches follow each other, the
+    same cycle count gives the clock those launches sustained (the cycles of an issue-bound
+    launch do not depend on the clock).  SQ_BUSY_CYCLES per shader engine (the cycles the
+    shader arrays are busy, ~90% of the active ones) gives the same ratio and is recorded
+    beside it."""
+    n_se, n_xcc = topo
+    sq = float(np.median(d["SQ_BUSY_CYCLES"])) / n_se
+    pmc_ns = float(np.median(d["pmc_ns"]))
+    grbm = float(np.median(d["GRBM_GUI_ACTIVE"])) / n_xcc if d.get("GRBM_GUI_ACTIVE") else float("nan")
+    tl = list(durations)[-timed:] if durations else []
+    t_avg = float(np.mean(tl)) if tl else float("nan")
+    return {"grbm_active_cycles_per_xcd": int(round(grbm)) if grbm == grbm else None,
+            "sq_busy_cycles_per_se": int(round(sq)), "pmc_dispatch_ns": pmc_ns,
+            "clock_ghz_pmc": round(grbm / pmc_ns, 3), "clock_ghz_pmc_sq_busy": round(sq / pmc_ns, 3),
+            "trace_timed_avg_ns": round(t_avg, 1), "trace_timed_dispatches": len(tl),
+            "clock_ghz_sustained": round(grbm / t_avg, 3) if tl and grbm == grbm else None,
+            "clock_ghz_sustained_sq_busy": round(sq / t_avg, 3) if tl else None,
+            "dispatch_ns": [round(x) for x in durations]}
+
+
 def summarize_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, commands) -> int:
     """Turn the rocprofv3 output of the profiling runs (kernel trace, FETCH_SIZE, WRITE_SIZE,
     SQ instruction counts, VALU busy) into the counter summary bench.py reads and a readable
@@ -227,8 +281,15 @@ def summarize_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, comman
     add("write_kib", _csv(_find(write_dir, "counter_collection.csv")), "WRITE_SIZE")
     sq = _csv(_find(sq_dir, "counter_collection.csv"))
     for c in ("SQ_INSTS_VALU", "SQ_INSTS_SALU", "SQ_INSTS_LDS", "SQ_INSTS_VMEM_RD",
-              "SQ_INSTS_VMEM_WR", "SQ_WAVES"):
+              "SQ_INSTS_VMEM_WR", "SQ_WAVES", "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE"):
         add(c, sq, c)
+    # the duration of each counted dispatch, for the clocks below
+    for r in sq:
+        if r["Counter_Name"] == "SQ_BUSY_CYCLES":
+            per.setdefault(_short(r["Kernel_Name"]), {}).setdefault("pmc_ns", []).append(
+                float(r["End_Timestamp"]) - float(r["Start_Timestamp"]))
+    topo = shader_engines(trace_dir)
+    timeline = dispatch_timeline(trace_dir)
     add("VALUBusy", _csv(_find(valu_dir, "counter_collection.csv")), "VALUBusy")
     stats = {}
     for r in _csv(_find(trace_dir, "kernel_stats.csv")):
@@ -271,6 +332,7 @@ def summarize_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, comman
                "vmem_wr_insts_per_launch": int(np.median(d["SQ_INSTS_VMEM_WR"])),
                "waves_per_launch": int(np.median(d["SQ_WAVES"])),
                "valu_busy_pct": round(float(np.median(d["VALUBusy"])), 2),
+               **clock_fields(d, topo, timeline.get(k, []), TRACE_TIMED_DISPATCHES),
                "trace": [{"kernel": r["Name"], "calls": int(r["Calls"]),
                           "avg_ns": float(r["AverageNs"]), "min_ns": float(r["MinNs"]),
                           "max_ns": float(r["MaxNs"])} for r in stats.get(k, [])]}
@@ -280,6 +342,23 @@ def summarize_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, comman
         lines.append(f"| {k} | {ks} | {ent['hbm_bytes_per_launch']} | {ab['per_launch']} | "
                      f"{ent['valu_insts_per_launch']} | {ent['valu_insts_per_tile']} | "
                      f"{ent['valu_busy_pct']} |")
+    lines += ["", f"Clock and trace figures ({topo[1]} XCDs, {topo[0]} shader engines; "
+              "GRBM_GUI_ACTIVE and SQ_BUSY_CYCLES from the counter run, whose dispatches run one "
+              f"at a time; the trace mean over the last {TRACE_TIMED_DISPATCHES} dispatches of "
+              "the kernel-trace run, the timed steps):", "",
+              "| entry point | active cycles per XCD (busy per shader engine) | counted dispatch "
+              "(us) | clock of the counted dispatch (GHz) | trace mean of the timed dispatches "
+              "(us) | sustained clock = active cycles / trace mean (GHz) | fraction of the "
+              "roofline at the trace mean |", "|---|---|---|---|---|---|---|"]
+    for k in ("tvq_encode", "tvq_decode"):
+        e = out["kernels"][k]
+        lines.append(f"| {k} | {e['grbm_active_cycles_per_xcd']} ({e['sq_busy_cycles_per_se']}) | "
+                     f"{e['pmc_dispatch_ns'] / 1e3:.1f} | {e['clock_ghz_pmc']} | "
+                     f"{e['trace_timed_avg_ns'] / 1e3:.1f} | {e['clock_ghz_sustained']} | "
+                     f"{ab['per_launch'] / (e['trace_timed_avg_ns'] * 1e-9) / 1e9 / HBM_PEAK_GBPS:.4f} |")
+    lines += ["", "Dispatch durations of the kernel-trace run in issue order (us):", ""]
+    for k in ("tvq_encode", "tvq_decode"):
+        lines.append(f"    {k}: " + ", ".join(f"{x / 1e3:.1f}" for x in timeline.get(k, [])))
     lines += ["", "rocprofv3 --kernel-trace --stats summary of the first command "
               "(kernel_stats.csv):", "", "```"]
     with open(_find(trace_dir, "kernel_stats.csv")) as f:
@@ -787,12 +866,24 @@ def main() -> int:
                "vectors_per_s": round(ab["vectors"] / (ms * 1e-3), 1),
                "traffic_bytes_per_launch": None if prof is None else prof["hbm_bytes_per_launch"]}
         if prof is not None:
-            # VALU issue: instructions of one launch (counters) over this run's launch time
+            # VALU issue: instructions of one launch (counters) over this run's launch time, at
+            # the 2.4 GHz peak clock and at the clock the profiled launches sustained
+            clk = prof.get("clock_ghz_sustained")
             out["valu"] = {"insts_per_launch": prof["valu_insts_per_launch"],
                            "insts_per_tile": prof["valu_insts_per_tile"],
                            "busy_pct_profiled": prof["valu_busy_pct"],
                            "issue_frac": round(prof["valu_insts_per_launch"] / (ms * 1e-3)
                                                / VALU_ISSUE_PEAK, 4)}
+            if clk:
+                out["valu"]["issue_frac_at_clock"] = round(
+                    prof["valu_insts_per_launch"] / (ms * 1e-3) / (VALU_ISSUE_PEAK * clk / 2.4), 4)
+                t_ns = prof["trace_timed_avg_ns"]
+                out["profiled"] = {
+                    "trace_timed_avg_us": round(t_ns / 1e3, 2),
+                    "frac_of_peak_trace_timed": round(ab["per_launch"] / (t_ns * 1e-9) / 1e9
+                                                      / HBM_PEAK_GBPS, 4),
+                    "clock_ghz_sustained": clk, "clock_ghz_single_dispatch":
+                        prof["clock_ghz_pmc"]}
         return out
 
     e_leg, d_leg = leg(enc, "encode"), leg(dec, "decode")
@@ -830,6 +921,14 @@ def main() -> int:
     }
     if "valu" in dom:
         out["roofline"]["valu_issue_frac"] = dom["valu"]["issue_frac"]
+        if "issue_frac_at_clock" in dom["valu"]:
+            out["roofline"]["valu_issue_frac_at_clock"] = dom["valu"]["issue_frac_at_clock"]
+    if "profiled" in dom:
+        # the committed kernel trace of the same kernel: its timed dispatches' mean duration,
+        # the fraction of the roofline at it, and the shader clock it implies
+        out["roofline"]["frac_trace"] = dom["profiled"]["frac_of_peak_trace_timed"]
+        out["roofline"]["trace_avg_us"] = dom["profiled"]["trace_timed_avg_us"]
+        out["roofline"]["clock_ghz"] = dom["profiled"]["clock_ghz_sustained"]
     if not args.no_cpu_baseline:
         print("# cpu baseline (oracle on host cores)", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w)
