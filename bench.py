@@ -445,8 +445,15 @@ def summarize_attention_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_d
     add("fetch_kib", _csv(_find(fetch_dir, "counter_collection.csv")), "FETCH_SIZE")
     add("write_kib", _csv(_find(write_dir, "counter_collection.csv")), "WRITE_SIZE")
     sq = _csv(_find(sq_dir, "counter_collection.csv"))
-    for c in ("SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_WAVES"):
+    for c in ("SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_WAVES", "SQ_INSTS_MFMA",
+              "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE"):
         add(c, sq, c)
+    n_se, n_xcc = shader_engines(trace_dir)
+    try:
+        agent = max(_csv(_find(trace_dir, "agent_info.csv")), key=lambda r: int(r.get("Cu_Count") or 0))
+        n_simd = int(agent.get("Simd_Count") or 1024)
+    except (OSError, FileNotFoundError, StopIteration):
+        n_simd = 1024
     add("VALUBusy", _csv(_find(valu_dir, "counter_collection.csv")), "VALUBusy")
     fetch_scale = float(1 << 30) / 1024.0 / max(per["copy"]["fetch_kib"])
     write_scale = float(1 << 30) / 1024.0 / max(per["copy"]["write_kib"])
@@ -473,6 +480,15 @@ def summarize_attention_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_d
                           int(np.median(d["SQ_LDS_BANK_CONFLICT"])),
                       "waves_per_dispatch": int(np.median(d["SQ_WAVES"])),
                       "valu_busy_pct": round(float(np.median(d["VALUBusy"])), 2)}
+        if d.get("SQ_INSTS_MFMA") and d.get("GRBM_GUI_ACTIVE"):
+            # matrix-core busy cycles per SIMD over the dispatch's active cycles per XCD: the
+            # share of the SIMDs' time the matrix instructions hold
+            active = float(np.median(d["GRBM_GUI_ACTIVE"])) / n_xcc
+            mf_busy = float(np.median(d["SQ_VALU_MFMA_BUSY_CYCLES"])) / n_simd
+            kernels[k].update({"mfma_insts_per_dispatch": int(np.median(d["SQ_INSTS_MFMA"])),
+                               "active_cycles_per_xcd": int(round(active)),
+                               "mfma_busy_cycles_per_simd": int(round(mf_busy)),
+                               "mfma_busy_pct": round(100.0 * mf_busy / active, 2) if active else None})
         hbm_step += per_step * (fetch + write)
         if "chunk" in k:
             valu_step += per_step * float(np.median(d["SQ_INSTS_VALU"]))
@@ -501,14 +517,17 @@ def summarize_attention_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_d
               f" instructions per tile of 16 tokens; LDS bank-conflict cycles per tile "
               f"{ent['lds_bank_conflict_cycles_per_tile']}; VALUBusy {ent['valu_busy_pct']} %", "",
               "| kernel | dispatches/step | avg ns (trace) | fetch B/dispatch | write B/dispatch | "
-              "VALU/dispatch | LDS/dispatch | bank-conflict cycles | VALUBusy % |",
-              "|---|---|---|---|---|---|---|---|---|"]
+              "VALU/dispatch (incl. MFMA) | MFMA/dispatch | LDS/dispatch | bank-conflict cycles | "
+              "VALUBusy % | MFMA busy % of active cycles |",
+              "|---|---|---|---|---|---|---|---|---|---|---|"]
     for k, e in kernels.items():
         tr = trace.get(k, {})
         lines.append(f"| {k} | {e['dispatches_per_step']:.0f} | {tr.get('avg_ns', 0):.0f} | "
                      f"{e['fetch_bytes_per_dispatch']} | {e['write_bytes_per_dispatch']} | "
-                     f"{e['valu_insts_per_dispatch']} | {e['lds_insts_per_dispatch']} | "
-                     f"{e['lds_bank_conflict_cycles_per_dispatch']} | {e['valu_busy_pct']} |")
+                     f"{e['valu_insts_per_dispatch']} | {e.get('mfma_insts_per_dispatch', '-')} | "
+                     f"{e['lds_insts_per_dispatch']} | "
+                     f"{e['lds_bank_conflict_cycles_per_dispatch']} | {e['valu_busy_pct']} | "
+                     f"{e.get('mfma_busy_pct', '-')} |")
     lines += ["", "rocprofv3 --kernel-trace --stats summary of the first command "
               "(kernel_stats.csv, codec and attention kernels):", "", "```"]
     with open(_find(trace_dir, "kernel_stats.csv")) as f:

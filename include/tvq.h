@@ -181,10 +181,12 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
  *              aligned, owned by the caller; its contents are overwritten
  * The token range is split into equal chunks (whole tile pairs, at least 4 tiles) so that a
  * launch has about one chunk wave per wave slot of the codec's device (its compute units
- * times the chunk kernel's resident waves per compute unit, taken at tvq_create); the
- * workspace holds one partial (max, sum, d accumulators) per query head and chunk, so its
- * size depends on the device the codec was created on.  Query heads are processed up to 4 per pass over the codes (G > 4 reads them
- * ceil(G/4) times).  Arithmetic is fp32 (expect ~1e-5 relative to an fp64 evaluation).
+ * times the resident waves per compute unit of the chunk kernel of the layer's formats, taken
+ * at tvq_create); the workspace holds one partial (max, sum, d accumulators) per query head
+ * and chunk, so its size depends on the device the codec was created on.
+ * tvq_attention_workspace names no layer and gives the size for the formats with the most
+ * chunks, which covers every layer.  Query heads are processed up to 4 per pass over the
+ * codes (G > 4 reads them ceil(G/4) times).  Arithmetic is fp32 (expect ~1e-5 relative to an fp64 evaluation).
  * Supported: d = 64 or 128, G <= 64, and for both K and V of the layer n = 64 or 256 with
  * 8-bit linear or 4-bit log-space norms (TVQ_ERR_UNSUPPORTED otherwise).  Launches two
  * kernels on `stream`. */
@@ -198,7 +200,7 @@ tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq
 /* Bytes of the device scratch that tvq_attention_decode_noalloc uses in place of a workspace:
  * one static array per GPU, held from the library's first use of that GPU until the process
  * ends (16 MiB; the long-context shape of 16 sequences x 32 query heads x 32K tokens at d = 128
- * needs 6.4 MB). */
+ * needs 8.5 MB). */
 #define TVQ_ATTENTION_SCRATCH_BYTES (16 * 1024 * 1024)
 
 /* tvq_attention_decode without the workspace argument, for callers that cannot allocate
@@ -206,7 +208,7 @@ tvq_status tvq_attention_decode(const tvq_codec* c, const void* cache, const tvq
  * per-chunk partials go to the library's static scratch on the codec's device.  Allocates
  * nothing and calls no allocating routine; arguments, results and launches are those of
  * tvq_attention_decode.  TVQ_ERR_SCRATCH, with nothing launched, when the call's partials
- * (tvq_attention_workspace) exceed TVQ_ATTENTION_SCRATCH_BYTES; TVQ_ERR_HIP when the scratch's
+ * (the chunks planned for this layer's formats) exceed TVQ_ATTENTION_SCRATCH_BYTES; TVQ_ERR_HIP when the scratch's
  * device address could not be obtained at tvq_create.  Every call on one GPU shares that
  * scratch: calls that overlap in time on one GPU (concurrent streams, or host threads each
  * launching) race on it and must be ordered by the caller.  The scratch needs no clearing:

@@ -25,7 +25,10 @@ struct tvq_codec {
   uint64_t rec_total = 0;                    // record bytes of all planes, per slot
   int device = 0;
   void* scratch = nullptr;                   // the static attention scratch on `device`
-  int64_t attn_slots = 0;                    // chunk waves the device holds at once (d = 64, 128)
+  // chunk waves of the attention the device holds at once (d = 64, 128), per key and value
+  // format (bit 0: 8-bit angle codes, bit 1: 4-bit log norms), and the most over the formats
+  int64_t attn_slots[4][4] = {};
+  int64_t attn_slots_max = 0;
   tvq::SegParams* d_segs = nullptr;
   uint32_t* d_sign_masks = nullptr;
   float* d_lut = nullptr;
@@ -454,13 +457,21 @@ tvq_status tvq_create(const tvq_config* cfg, tvq_codec** out) {
   c->scratch = scratch_address(c->device);
   if (d == 64 || d == 128) {
     int n_cu = 0;
-    const int blocks = tvq_attention_blocks_per_cu(d);
     if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, c->device) !=
-            hipSuccess || n_cu < 1 || blocks < 1) {
+            hipSuccess || n_cu < 1) {
       delete c;
       return TVQ_ERR_HIP;
     }
-    c->attn_slots = (int64_t)n_cu * blocks * tvq::kWavesPerBlock;
+    for (int kf = 0; kf < 4; ++kf)
+      for (int vf = 0; vf < 4; ++vf) {
+        const int blocks = tvq_attention_blocks_per_cu(d, kf, vf);
+        if (blocks < 1) {
+          delete c;
+          return TVQ_ERR_HIP;
+        }
+        c->attn_slots[kf][vf] = (int64_t)n_cu * blocks * tvq::kWavesPerBlock;
+        c->attn_slots_max = std::max(c->attn_slots_max, c->attn_slots[kf][vf]);
+      }
   }
   // segment lists of the two decode kernels
   std::vector<uint32_t> lists;
@@ -762,10 +773,23 @@ struct AttnPlan {
   int64_t acc_bytes, ws_bytes;
 };
 
+// The attention formats of `layer`'s keys and values (bit 0: n = 256, bit 1: 4-bit log norms).
+static tvq_status attn_formats(const tvq_codec* c, int32_t layer, int (&fmt)[2]) {
+  if (layer < 0 || layer >= c->L) return TVQ_ERR_INVALID_ARG;
+  for (int kind = 0; kind < 2; ++kind) {
+    const tvq::SegParams& sp = c->segs[2 * layer + kind];
+    if (!tvq::fast_format(sp.n, sp.mode, sp.bits)) return TVQ_ERR_UNSUPPORTED;
+    fmt[kind] = (sp.n == 256 ? 1 : 0) | (sp.mode == 2 ? 2 : 0);
+  }
+  return TVQ_OK;
+}
+
 // block_tokens: 0 for the contiguous layout, else the pool's block size (a chunk then spans
-// at most 64 blocks, one per lane of the wave that fetches their pool indices).
+// at most 64 blocks, one per lane of the wave that fetches their pool indices).  fmt: the
+// layer's formats, or nullptr for the plan with the most chunks over the formats (the
+// workspace queries, which name no layer: a layer's plan never has more chunks).
 static tvq_status attn_plan(const tvq_codec* c, int64_t batch, int32_t num_q_heads,
-                            int64_t t_end, int64_t block_tokens, AttnPlan* p) {
+                            int64_t t_end, int64_t block_tokens, const int* fmt, AttnPlan* p) {
   if (!c || batch < 1 || t_end < 1 || num_q_heads < c->H || num_q_heads % c->H != 0)
     return TVQ_ERR_INVALID_ARG;
   if (c->d != 64 && c->d != 128) return TVQ_ERR_UNSUPPORTED;
@@ -776,7 +800,8 @@ static tvq_status attn_plan(const tvq_codec* c, int64_t batch, int32_t num_q_hea
   // paged: a chunk may start inside a block, so 63 blocks' tokens keep it within the 64
   // blocks whose pool indices one wave fetches
   const int64_t max_chunk = block_tokens > 0 ? std::min<int64_t>(4096, 63 * block_tokens) : 4096;
-  p->chunk = attn_chunk_tokens(c->d, batch * c->H * p->n_pass, t_end, c->attn_slots, max_chunk);
+  const int64_t slots = fmt ? c->attn_slots[fmt[0]][fmt[1]] : c->attn_slots_max;
+  p->chunk = attn_chunk_tokens(c->d, batch * c->H * p->n_pass, t_end, slots, max_chunk);
   p->n_chunks = (uint32_t)((t_end + p->chunk - 1) / p->chunk);
   const int64_t parts = batch * num_q_heads * (int64_t)p->n_chunks;
   p->acc_bytes = (parts * c->d * 4 + 255) / 256 * 256;
@@ -788,7 +813,7 @@ tvq_status tvq_attention_workspace(const tvq_codec* c, int64_t batch, int32_t nu
                                    int64_t t_end, int64_t* bytes) {
   if (!bytes) return TVQ_ERR_INVALID_ARG;
   AttnPlan p;
-  const tvq_status st = attn_plan(c, batch, num_q_heads, t_end, 0, &p);
+  const tvq_status st = attn_plan(c, batch, num_q_heads, t_end, 0, nullptr, &p);
   if (st == TVQ_OK) *bytes = p.ws_bytes;
   return st;
 }
@@ -799,7 +824,7 @@ tvq_status tvq_attention_paged_workspace(const tvq_codec* c, int64_t batch, int3
       (block_tokens & (block_tokens - 1)) != 0)
     return TVQ_ERR_INVALID_ARG;
   AttnPlan p;
-  const tvq_status st = attn_plan(c, batch, num_q_heads, max_ctx, block_tokens, &p);
+  const tvq_status st = attn_plan(c, batch, num_q_heads, max_ctx, block_tokens, nullptr, &p);
   if (st == TVQ_OK) *bytes = p.ws_bytes;
   return st;
 }
@@ -815,15 +840,12 @@ static tvq_status attention_launch(const tvq_codec* c, tvq::AttnArgs& a, int64_t
   if ((q_dtype != TVQ_BF16 && q_dtype != TVQ_F32) || (o_dtype != TVQ_BF16 && o_dtype != TVQ_F32))
     return TVQ_ERR_INVALID_ARG;
   if (!(scale == scale) || scale > 3.0e38f || scale < -3.0e38f) return TVQ_ERR_INVALID_ARG;
-  AttnPlan p;
-  const tvq_status st = attn_plan(c, batch, num_q_heads, t_end, block_tokens, &p);
-  if (st != TVQ_OK) return st;
   int fmt[2];
-  for (int kind = 0; kind < 2; ++kind) {
-    const tvq::SegParams& sp = c->segs[2 * layer + kind];
-    if (!tvq::fast_format(sp.n, sp.mode, sp.bits)) return TVQ_ERR_UNSUPPORTED;
-    fmt[kind] = (sp.n == 256 ? 1 : 0) | (sp.mode == 2 ? 2 : 0);
-  }
+  tvq_status st = attn_formats(c, layer, fmt);
+  if (st != TVQ_OK) return st;
+  AttnPlan p;
+  st = attn_plan(c, batch, num_q_heads, t_end, block_tokens, fmt, &p);
+  if (st != TVQ_OK) return st;
   if (!a.cache || !q || !o || !workspace || !aligned16(a.cache) || !aligned16(q) ||
       !aligned16(o) || !aligned16(workspace) || workspace_bytes < p.ws_bytes)
     return TVQ_ERR_INVALID_ARG;
@@ -874,8 +896,11 @@ tvq_status tvq_attention_decode_noalloc(const tvq_codec* c, const void* cache,
                                         int32_t num_q_heads, float scale, tvq_dtype q_dtype,
                                         const void* q, tvq_dtype o_dtype, void* o, void* stream) {
   if (!c || !lay) return TVQ_ERR_INVALID_ARG;
+  int fmt[2];
+  tvq_status st = attn_formats(c, layer, fmt);
+  if (st != TVQ_OK) return st;
   AttnPlan p;
-  const tvq_status st = attn_plan(c, lay->batch, num_q_heads, t_end, 0, &p);
+  st = attn_plan(c, lay->batch, num_q_heads, t_end, 0, fmt, &p);
   if (st != TVQ_OK) return st;
   if (p.ws_bytes > (int64_t)TVQ_ATTENTION_SCRATCH_BYTES) return TVQ_ERR_SCRATCH;
   if (!c->scratch) return TVQ_ERR_HIP;

@@ -44,12 +44,6 @@ constexpr float kLazyLog2 = 8.0f;    // weights 2^(s - m) stay below 2^8 between
 // 16-byte reads of a wave (one per lane of a vector, broadcast over the vector slots) fall in
 // distinct banks
 constexpr int kQPitch = kElemsPerLane + 4;
-// Value staging of the d = 128 matrix-core kernel: pair p of token t at word 16 p + t +
-// kVRowSkew (p / 16).  The skew puts the 16 tokens x 4 slices of a store, and the 16 lanes of
-// each quarter of a rotated 16-byte read, in distinct banks.
-constexpr int kVRowSkew = 16;
-constexpr int kVPairWords = 16 * 64 + kVRowSkew * 3;
-
 template <int LPV>
 __device__ __forceinline__ float vec_sum(float v) {
   if constexpr (LPV >= 2) v += quad_perm<0xB1>(v);
@@ -146,18 +140,6 @@ struct TilePair {
   TileCodes<VW, VN> v;
 };
 
-// Pool record of the chunk's token j in a paged cache: a tile lies inside one block (blocks
-// hold a multiple of a tile's tokens), whose pool index comes from lane i of w.blk.
-template <int D>
-__device__ __forceinline__ uint32_t paged_record(const AttnArgs& a, const AttnWave<D>& w,
-                                                 uint32_t tile, uint32_t j) {
-  const uint32_t first = (w.t0 + tile * AttnWave<D>::VPW) >> a.pg.block_log2;
-  const uint32_t i = first - (w.t0 >> a.pg.block_log2);
-  const uint32_t blk = (uint32_t)__builtin_amdgcn_readlane((int)w.blk, (int)i);
-  const uint32_t tok = w.t0 + j;
-  return ((blk * a.H + w.h) << a.pg.block_log2) + (tok & ((1u << a.pg.block_log2) - 1u));
-}
-
 // The V header (R'min, R'max) of this lane's token (vector slot) in `tile`, where the tile
 // may differ between lanes: the paged block id comes from its lane by a cross-lane read.
 template <int D>
@@ -174,16 +156,29 @@ __device__ __forceinline__ u32x2 v_header(const AttnArgs& a, const AttnWave<D>& 
   return *(const u32x2*)(w.plane[1][2] + (uint64_t)slot * 8);
 }
 
+// The codes of `tile`: this lane's token (vector slot) and slice.  The tile's first token is
+// the same for the whole wave, and a tile lies inside one pool block of a paged cache (blocks
+// hold a multiple of a tile's tokens; the block's pool index comes from lane i of w.blk), so
+// the record addresses of its first token are scalar and a lane adds its own token's offset.
+// Slots past the chunk read its last token (in bounds) and get weight 0.
 template <int D, int KW, int KN, int VW, int VN>
 __device__ __forceinline__ TilePair<KW, KN, VW, VN> tile_pair(const AttnArgs& a,
                                                               const AttnWave<D>& w,
                                                               uint32_t tile) {
-  // slots past the chunk read its last token (in bounds) and get weight 0
-  const uint32_t j = min(tile * AttnWave<D>::VPW + w.vslot, w.ntok - 1);
-  const uint32_t slot = a.pg.table ? paged_record<D>(a, w, tile, j) : w.row + w.t0 + j;
+  constexpr uint32_t VPW = AttnWave<D>::VPW;
+  const uint32_t first = tile * VPW;
+  uint32_t j = (uint32_t)w.vslot;
+  if (first + VPW > w.ntok) j = min(j, w.ntok - 1 - first);
+  uint32_t slot0 = w.row + w.t0 + first;
+  if (a.pg.table) {
+    const uint32_t tok = w.t0 + first;
+    const uint32_t i = (tok >> a.pg.block_log2) - (w.t0 >> a.pg.block_log2);
+    const uint32_t blk = (uint32_t)__builtin_amdgcn_readlane((int)w.blk, (int)i);
+    slot0 = ((blk * a.H + w.h) << a.pg.block_log2) + (tok & ((1u << a.pg.block_log2) - 1u));
+  }
   TilePair<KW, KN, VW, VN> p;
-  p.k = load_codes_at<KW, KN>(w.plane[0], w.sp[0].rec, slot, w.sub);
-  p.v = load_codes_at<VW, VN>(w.plane[1], w.sp[1].rec, slot, w.sub);
+  p.k = load_codes_from<KW, KN>(w.plane[0], w.sp[0].rec, slot0, j, w.sub);
+  p.v = load_codes_from<VW, VN>(w.plane[1], w.sp[1].rec, slot0, j, w.sub);
   return p;
 }
 
@@ -405,43 +400,89 @@ __global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
 }
 
 // The chunk kernel at d = 128 with the two contractions on the matrix cores
-// (v_mfma_f32_4x4x1f32: 16 blocks b = lane / 4; block b's C[r][j] += A[lane 4b + r] *
-// B[lane 4b + j], kept by lane 4b + j in its register r).
-//   scores  lane l decodes y'_K of token t = l % 16, elements 32 s .. 32 s + 31 (s = l / 16),
-//           and holds q^ of query head j = l % 4 on the same elements.  Over those 32 elements
-//           block b = l / 4 (tokens 4 ((l / 4) % 4) + r) accumulates the partial scores of 4
-//           tokens x 4 heads; the four element slices s are summed across lanes, so every row
-//           of 16 lanes holds all 16 scores and lane l the weights of tokens 4 tq .. 4 tq + 3
-//           (tq = (l / 4) % 4) for head j.
-//   values  the lane that loaded a token's V codes (token l % 16, slice s) rebuilds y'_V of
-//           its 16 pairs and stores them to LDS pair-major, so that lane l reads pair l
-//           (elements 2l, 2l + 1) of any token; in each of 16 steps block b = l / 4 adds
-//           y'_V(k, pair 4b + r) * p(k, head j) for one token k, the blocks of a row taking
-//           their tokens in rotated order so that the weights move by row rotations instead
-//           of LDS; lane 4b + j accumulates pairs 4b .. 4b + 3 of head j: 8 registers for the
-//           whole (4 heads x 128 elements) accumulator.
-// The reference point m, the sum l and the accumulator of head j live on the lanes with
-// lane % 4 == j.  y' is rebuilt exactly as decode rebuilds it.
-template <int KW, int KN, int VW, int VN>
-__global__ __launch_bounds__(kBlockThreads, 3) void attn_mfma_chunk_kernel(AttnArgs a) {
-  constexpr int D = 128;
-  typedef float v4f __attribute__((ext_vector_type(4)));
-  __shared__ float2 s_lut[2][kLut];
-  // level tables of log-space norms (none for linear norms): K as 16 rows of 16 levels, V with
-  // level q of token t at word 32 q + 2 t + c in two copies c, read by the lanes of even and odd
-  // slices, so that the 32 lanes of each half of a read use 32 distinct banks
-  constexpr int kLvlK = KN == 8 ? 0 : 16 * 16, kLvlV = VN == 8 ? 0 : 16 * 32;
-  __shared__ float s_lvl[kWavesPerBlock][kLvlK + kLvlV + 1];
-  // per wave: q^ of the pass's heads while it is read into registers, then per pair and token
-  // the two elements of y'_V
-  static_assert(kAttnPassHeads * 4 * kQPitch <= 2 * kVPairWords, "q^ fits the value staging");
-  __shared__ __attribute__((aligned(16))) float s_stage[kWavesPerBlock][2 * kVPairWords];
+// (v_mfma_f32_4x4x1f32: 16 blocks of 4 lanes, block b = lane / 4; block b's C[r][j] +=
+// A[lane 4b + r] * B[lane 4b + j], kept by lane 4b + j in its register r; operand `blgp` 4 + u
+// makes every block take B from the lanes of row u, lanes 16u .. 16u + 15, instead of its own).
+// Lane l sits in row R = l / 16, column c = (l / 4) % 4 and position x = l % 4.
+//   codes   lane l reads and rebuilds token 4R + x of the 16-token tile on slice c (pairs
+//           16c .. 16c + 15, elements 32c .. 32c + 31), for K and for V.
+//   scores  the products take q^ of query head x on the same 32 elements.  q^ is the same
+//           for the four rows, so row u keeps elements 8u .. 8u + 7 of each slice and the
+//           products over those take B from row u.  Block 4R + c accumulates the partial
+//           scores of tokens 4R + r for heads j; two row rotations add the four slices, after
+//           which lane l holds the weights of tokens 4R + r (register r) for head x, as does
+//           every column of the row.
+//   values  y'_V goes through LDS so that lane l holds pair l of the 16 tokens, both
+//           elements.  The product for token 4u + k takes the weights from register k of row u
+//           (B broadcast from row u), so block b adds y'_V(token, pair 4b + r, element e) *
+//           p(token, head j) over all 16 tokens: lane 4b + j accumulates pairs 4b .. 4b + 3 of
+//           head j in 8 registers.
+// The reference point m, the sum l and the accumulator of head x live on the lanes with
+// lane % 4 == x.  y'_V is rebuilt before the softmax step, which it does not depend on, so
+// that its arithmetic can overlap the score products.  y' is rebuilt exactly as decode
+// rebuilds it.
+//
+// Per-wave LDS of this kernel, in floats.  Value staging: pair l from word kPairPitch l +
+// kHalfSkew (l / 32), in it token t and element e at 2t + e; the lane that rebuilt (token t,
+// pair l) stores both elements with one 8-byte write.  The pitch keeps the four lanes of each
+// quad of a 16-byte read on distinct banks, the skew spreads the 8-byte stores of the lanes of
+// one column over two bank halves (layouts chosen by timing the access patterns on gfx950).
+// Level tables of log-space norms, one per kind: level q of token t at word 32q + 2t + h, in
+// two copies h = c % 2 that the lanes of even and odd columns read.  The tables share the
+// staging's words: each is written, read into registers, and then overwritten by the same
+// tile's staging.
+constexpr int kPairPitch = 36;
+constexpr int kHalfSkew = 16;
+constexpr int kStageWords = 64 * kPairPitch + kHalfSkew + 16;
+constexpr int kLvlWords = 16 * 32;
+static_assert(2 * kLvlWords <= kStageWords, "both level tables fit the staging words");
+static_assert(kAttnPassHeads * 4 * kQPitch <= kStageWords, "q^ fits the staging words");
 
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// Products over elements 8 RHO .. 8 RHO + 7 of the lane's slice (pairs 4 RHO .. 4 RHO + 3),
+// q^ from row RHO.
+template <int RHO>
+__device__ __forceinline__ v4f score_quarter(const float (&r)[kPairsPerLane],
+                                             const uint32_t (&kc)[kPairsPerLane],
+                                             const float2* lut, const float (&qr)[8], v4f sc) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const float2 cs = lut[kc[4 * RHO + u]];
+    sc = __builtin_amdgcn_mfma_f32_4x4x1f32(r[4 * RHO + u] * cs.x, qr[2 * u], sc, 0, 0, 4 + RHO);
+    sc = __builtin_amdgcn_mfma_f32_4x4x1f32(r[4 * RHO + u] * cs.y, qr[2 * u + 1], sc, 0, 0,
+                                            4 + RHO);
+  }
+  return sc;
+}
+
+// Value products of tokens 2N and 2N + 1 of the tile: words 4N .. 4N + 3 of the lane's staged
+// pair are (token 2N, e 0), (2N, 1), (2N + 1, 0), (2N + 1, 1); the weights of token 4u + k are
+// register k of row u.
+template <int N>
+__device__ __forceinline__ void value_pair(const float* stage_r, const float (&p)[4], v4f& acc0,
+                                           v4f& acc1) {
+  constexpr int t0 = 2 * N, t1 = 2 * N + 1;
+  const float4 v = *(const float4*)(stage_r + 4 * N);
+  acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(v.x, p[t0 & 3], acc0, 0, 0, 4 + t0 / 4);
+  acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(v.y, p[t0 & 3], acc1, 0, 0, 4 + t0 / 4);
+  acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(v.z, p[t1 & 3], acc0, 0, 0, 4 + t1 / 4);
+  acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(v.w, p[t1 & 3], acc1, 0, 0, 4 + t1 / 4);
+}
+
+template <int KW, int KN, int VW, int VN>
+__global__ __launch_bounds__(kBlockThreads, 4) void attn_mfma_chunk_kernel(AttnArgs a) {
+  constexpr int D = 128;
+  __shared__ float2 s_lut_k[1 << KW];
+  __shared__ float2 s_lut_v[1 << VW];
+  __shared__ __attribute__((aligned(16))) float s_wave[kWavesPerBlock][kStageWords];
+
+  // the layer's K and V tables (n = 2^KW and 2^VW entries: the host dispatches on n)
   const SegParams spk = a.segs[2 * a.layer], spv = a.segs[2 * a.layer + 1];
-  for (uint32_t e = threadIdx.x; e < spk.n; e += kBlockThreads)
-    s_lut[0][e] = ((const float2*)a.lut)[spk.lut_off + e];
-  for (uint32_t e = threadIdx.x; e < spv.n; e += kBlockThreads)
-    s_lut[1][e] = ((const float2*)a.lut)[spv.lut_off + e];
+  for (uint32_t e = threadIdx.x; e < (1u << KW); e += kBlockThreads)
+    s_lut_k[e] = ((const float2*)a.lut)[spk.lut_off + e];
+  for (uint32_t e = threadIdx.x; e < (1u << VW); e += kBlockThreads)
+    s_lut_v[e] = ((const float2*)a.lut)[spv.lut_off + e];
   __syncthreads();
 
   const uint32_t wib = threadIdx.x / kWave;
@@ -451,73 +492,134 @@ __global__ __launch_bounds__(kBlockThreads, 3) void attn_mfma_chunk_kernel(AttnA
   w.sp[0] = spk;
   w.sp[1] = spv;
   if (!chunk_setup<D>(a, w, wib)) return;
+  float* const lds = s_wave[wib];
 
   // q^ of the pass's heads: computed in the quad layout (vector slot g = head g), read back as
-  // head j = lane % 4 on elements 32 s .. 32 s + 31 (zero for heads past the pass)
-  float* qh = s_stage[wib];
+  // head x on slice c (zero for heads past the pass)
   {
     AttnWave<D> wq = w;
     wq.sub = lane % 4;
     wq.vslot = lane / 4;
-    if (a.q_f32) query_transform<D, true>(a, wq, qh);
-    else query_transform<D, false>(a, wq, qh);
+    if (a.q_f32) query_transform<D, true>(a, wq, lds);
+    else query_transform<D, false>(a, wq, lds);
   }
   wave_lds_sync();
-  const int j = lane & 3, s = lane >> 4, tq = (lane >> 2) & 3;
-  float qr[kElemsPerLane];
+  // q^ is the same on the four rows, so each row keeps a quarter of it: lane (R, c, x) holds
+  // elements 32c + 8R .. 32c + 8R + 7 of head x, and the product over element n takes its
+  // B operand from row n / 8 (the lane-group broadcast of the matrix instruction, blgp 4 + n / 8)
+  const int x = lane & 3, c = (lane >> 2) & 3, R = lane >> 4;
+  float qr[8];
 #pragma unroll
-  for (int i = 0; i < kElemsPerLane; i += 4) {
-    const float4 v = (uint32_t)j < w.gc ? *(const float4*)(qh + (j * 4 + s) * kQPitch + i)
+  for (int i = 0; i < 8; i += 4) {
+    const float4 v = (uint32_t)x < w.gc ? *(const float4*)(lds + (x * 4 + c) * kQPitch + 8 * R + i)
                                         : make_float4(0, 0, 0, 0);
     qr[i] = v.x, qr[i + 1] = v.y, qr[i + 2] = v.z, qr[i + 3] = v.w;
   }
-  // the K layout: token t = lane % 16, slice s (tile loads and the K decode use it)
-  w.sub = s;
-  w.vslot = lane & 15;
-  float* lvl_k = s_lvl[wib] + 16 * w.vslot;
-  float* lvl_v = s_lvl[wib] + kLvlK + 2 * w.vslot;
-  float* vy0 = s_stage[wib];
-  float* vy1 = s_stage[wib] + kVPairWords;
-  // this lane's pair (pair `lane`) in the value layout: 16 tokens from word 16 pair + skew
-  const float* vy0_row = vy0 + 16 * lane + kVRowSkew * (lane >> 4);
-  const float* vy1_row = vy1 + 16 * lane + kVRowSkew * (lane >> 4);
-  // token groups of the weights that row rotations by 0, 4, 8 and 12 lanes bring to this lane
-  // (found by rotating the lane's own group number the same way)
-  const uint32_t grp[4] = {(uint32_t)tq, row_ror<4>((uint32_t)tq), row_ror<8>((uint32_t)tq),
-                           row_ror<12>((uint32_t)tq)};
+  // the code layout: token 4R + x of the tile, slice c (tile loads and both rebuilds use it)
+  w.sub = c;
+  w.vslot = 4 * R + x;
+  const int tok = w.vslot;
+  const float* const lvl_v = lds + 2 * tok + (c & 1);           // level q at + 32 q
+  const float* const lvl_k = lds + kLvlWords + 2 * tok + (c & 1);
+  float* const lvl_v_w = lds + 2 * tok;                         // the two copies of level q
+  float* const lvl_k_w = lds + kLvlWords + 2 * tok;
+  float* const stage_w = lds + 16 * kPairPitch * c + kHalfSkew * (c >> 1) + 2 * tok;   // + pitch i
+  const float* const stage_r = lds + kPairPitch * lane + kHalfSkew * (lane >> 5);
 
   float m = -INFINITY, lsum = 0.0f;
-  // accumulators of element 0 and 1 of each pair
+  // accumulators of element 0 and 1 of pairs 4b + r (register r), head x
   v4f acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
-  constexpr uint32_t kVLevels = (1u << VN) - 1u;
+  constexpr uint32_t kKLevels = (1u << KN) - 1u, kVLevels = (1u << VN) - 1u;
 
   const uint32_t last = (w.ntok + 15) / 16 - 1;
+  const bool ragged = (w.ntok & 15u) != 0;
   // log-space V norms: the ladder ratio of each token, computed for four tiles at once (the
-  // four lanes of a token would otherwise compute the same one): lane (t, s) holds that of
-  // token t in tile 4 k + s, and tile 4 k + x reads it from lane t + 16 x
+  // four lanes of a token would otherwise compute the same one): lane (token t, column c)
+  // holds that of token t in tile 4k + c, and tile 4k + u reads it from column u
   double vrho = 1.0;
   u32x2 vh = {0u, 0u};
-  if constexpr (VN != 8) vh = v_header<D>(a, w, min((uint32_t)s, last));
-  auto tile_work = [&](const TilePair<KW, KN, VW, VN>& c, uint32_t tile) {
-    // ---- scores: y'_K on this lane's slice, then 32 matrix products over the slice ----
-    float y[kElemsPerLane];
-    code_vector<4, KW, KN>(c.k, s_lut[0], lvl_k, s, y);
+  if constexpr (VN != 8) vh = v_header<D>(a, w, min((uint32_t)c, last));
+  auto tile_work = [&](const TilePair<KW, KN, VW, VN>& cd, uint32_t tile) {
+    // ---- scores: y'_K on this lane's slice, 32 matrix products over the slice ----
     v4f sc = {0, 0, 0, 0};
+    {
+      const float rmin = __uint_as_float(cd.k.hdr.x), rmax = __uint_as_float(cd.k.hdr.y);
+      uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
+      unpack16_index<KW>(cd.k.ang, kc);
+      float r[kPairsPerLane];
+      if constexpr (KN == 8) {
+        unpack16<KN>(cd.k.nrm, qc);
+        const float step = linear_step255(rmin, rmax);
 #pragma unroll
-    for (int n = 0; n < kElemsPerLane; ++n)
-      sc = __builtin_amdgcn_mfma_f32_4x4x1f32(y[n], qr[n], sc, 0, 0, 0);
-    // the four slices summed: every row of 16 lanes now holds the scores of tokens 4 tq + r
-    // (register r) for head j
+        for (int i = 0; i < kPairsPerLane; ++i) r[i] = __builtin_fmaf((float)qc[i], step, rmin);
+      } else {
+        unpack16_index<KN>(cd.k.nrm, qc);
+        wave_lds_sync();                       // the previous tile's reads of these words are done
+        static_assert(KN == 4, "log-space norms here: 16 levels, four per lane");
+        log_level_ladder_each<4, 4>(
+            [lvl_k_w](uint32_t q, float v) { lvl_k_w[32 * q] = v; lvl_k_w[32 * q + 1] = v; },
+            c, rmin, rmax, kKLevels);
+        wave_lds_sync();
+#pragma unroll
+        for (int i = 0; i < kPairsPerLane; ++i) r[i] = lvl_k[32 * qc[i]];
+      }
+      sc = score_quarter<0>(r, kc, s_lut_k, qr, sc);
+      sc = score_quarter<1>(r, kc, s_lut_k, qr, sc);
+      sc = score_quarter<2>(r, kc, s_lut_k, qr, sc);
+      sc = score_quarter<3>(r, kc, s_lut_k, qr, sc);
+    }
+    // ---- values: y'_V of the lane's 16 pairs to the staging ----
+    {
+      const float rmin = __uint_as_float(cd.v.hdr.x), rmax = __uint_as_float(cd.v.hdr.y);
+      uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
+      unpack16_index<VW>(cd.v.ang, kc);
+      float r[kPairsPerLane];
+      if constexpr (VN == 8) {
+        unpack16<VN>(cd.v.nrm, qc);
+        const float step = linear_step255(rmin, rmax);
+#pragma unroll
+        for (int i = 0; i < kPairsPerLane; ++i) r[i] = __builtin_fmaf((float)qc[i], step, rmin);
+        wave_lds_sync();                       // the previous tile's staging reads are done
+      } else {
+        unpack16_index<VN>(cd.v.nrm, qc);
+        if ((tile & 3u) == 0) {
+          vrho = ladder_rho(__uint_as_float(vh.x), __uint_as_float(vh.y), kVLevels);
+          vh = v_header<D>(a, w, min(tile + 4u + (uint32_t)c, last));   // the next group's
+        }
+        const double rho = __shfl(vrho, (lane & 0x33) | (int)((tile & 3u) << 2));
+        wave_lds_sync();                       // the previous tile's staging reads are done
+        static_assert(VN == 4, "log-space norms here: 16 levels, four per lane");
+        ladder_levels_each<4, 4>(
+            [lvl_v_w](uint32_t q, float v) { lvl_v_w[32 * q] = v; lvl_v_w[32 * q + 1] = v; },
+            c, rmin, rmax, rho, kVLevels);
+        wave_lds_sync();
+#pragma unroll
+        for (int i = 0; i < kPairsPerLane; ++i) r[i] = lvl_v[32 * qc[i]];
+        wave_lds_sync();                       // every lane's level reads are done
+      }
+#pragma unroll
+      for (int i = 0; i < kPairsPerLane; ++i) {
+        const float2 cs = s_lut_v[kc[i]];
+        *(float2*)(stage_w + kPairPitch * i) = make_float2(r[i] * cs.x, r[i] * cs.y);
+      }
+    }
+    // ---- softmax step: the slices added across the row's columns, the weights ----
     float sv[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float tot = sum_xor32(sum_xor16(sc[r]));
-      sv[r] = tile * 16 + 4 * tq + r < w.ntok ? tot : -INFINITY;
+    for (int q = 0; q < 4; ++q) {
+      float v = sc[q];
+      v += row_ror<8>(v);
+      v += row_ror<4>(v);
+      sv[q] = v;
+    }
+    if (ragged && tile == last) {              // tokens past the chunk weigh 0
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sv[q] = tile * 16 + 4 * R + q < w.ntok ? sv[q] : -INFINITY;
     }
     const float smax = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
     if (__builtin_amdgcn_ballot_w64(smax > m + kLazyLog2) != 0) {   // a new reference point
-      float mx = fmaxf(smax, __shfl_xor(smax, 4));
-      mx = fmaxf(mx, __shfl_xor(mx, 8));
+      float mx = fmaxf(smax, __shfl_xor(smax, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
       const float mn = fmaxf(m, mx);
       const float f = __builtin_amdgcn_exp2f(m - mn);          // 0 on the first raise
       lsum *= f;
@@ -527,73 +629,22 @@ __global__ __launch_bounds__(kBlockThreads, 3) void attn_mfma_chunk_kernel(AttnA
     }
     float p[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) p[r] = __builtin_amdgcn_exp2f(sv[r] - m);
+    for (int q = 0; q < 4; ++q) p[q] = __builtin_amdgcn_exp2f(sv[q] - m);
     lsum += (p[0] + p[1]) + (p[2] + p[3]);
-
-    // ---- values: y'_V of every pair to the pair layout through LDS ----
-    {
-      const float rmin = __uint_as_float(c.v.hdr.x), rmax = __uint_as_float(c.v.hdr.y);
-      uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
-      unpack16_index<VW>(c.v.ang, kc);
-      wave_lds_sync();                       // the previous tile's reads of vy and lvl are done
-      float step = 0.0f;
-      if constexpr (VN == 8) {
-        unpack16<VN>(c.v.nrm, qc);
-        step = linear_step255(rmin, rmax);
-      } else {
-        unpack16_index<VN>(c.v.nrm, qc);
-        if ((tile & 3u) == 0) {
-          vrho = ladder_rho(__uint_as_float(vh.x), __uint_as_float(vh.y), kVLevels);
-          vh = v_header<D>(a, w, min(tile + 4u + (uint32_t)s, last));   // the next group's
-        }
-        const double rho = __shfl(vrho, w.vslot + 16 * (int)(tile & 3u));
-        ladder_levels_each<4>(
-            [lvl_v](uint32_t q, float v) {
-              lvl_v[32 * q] = v;
-              lvl_v[32 * q + 1] = v;
-            },
-            s, rmin, rmax, rho, kVLevels);
-        wave_lds_sync();
-      }
-      float* d0 = vy0 + kVRowSkew * s + w.vslot;
-      float* d1 = vy1 + kVRowSkew * s + w.vslot;
-#pragma unroll
-      for (int i = 0; i < kPairsPerLane; ++i) {
-        const int pr = 16 * s + i;             // row of pair 16 s + i, before the slice skew
-        const float r =
-            VN == 8 ? __builtin_fmaf((float)qc[i], step, rmin) : lvl_v[32 * qc[i] + (s & 1)];
-        const float2 cs = s_lut[1][kc[i]];
-        d0[16 * pr] = r * cs.x;
-        d1[16 * pr] = r * cs.y;
-      }
-      wave_lds_sync();
-    }
-    // step 4 x + r of the products takes, in block b, token 4 grp[x] + r: the weights come from
-    // the lanes 4 x further round the row (so every block of 4 lanes sees all 16 tokens over the
-    // 16 steps), y'_V from LDS at that block's own token
-    float pw[16];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      pw[r] = p[r];
-      pw[4 + r] = row_ror<4>(p[r]);
-      pw[8 + r] = row_ror<8>(p[r]);
-      pw[12 + r] = row_ror<12>(p[r]);
-    }
-#pragma unroll
-    for (int x = 0; x < 4; ++x) {
-      const float4 v0 = *(const float4*)(vy0_row + 4 * grp[x]);
-      const float4 v1 = *(const float4*)(vy1_row + 4 * grp[x]);
-      acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(v0.x, pw[4 * x], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(v1.x, pw[4 * x], acc1, 0, 0, 0);
-      acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(v0.y, pw[4 * x + 1], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(v1.y, pw[4 * x + 1], acc1, 0, 0, 0);
-      acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(v0.z, pw[4 * x + 2], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(v1.z, pw[4 * x + 2], acc1, 0, 0, 0);
-      acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(v0.w, pw[4 * x + 3], acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(v1.w, pw[4 * x + 3], acc1, 0, 0, 0);
-    }
+    // ---- value products: tokens 2n and 2n + 1, both elements, from one 16-byte read ----
+    wave_lds_sync();                           // every lane's staging is written
+    value_pair<0>(stage_r, p, acc0, acc1);
+    value_pair<1>(stage_r, p, acc0, acc1);
+    value_pair<2>(stage_r, p, acc0, acc1);
+    value_pair<3>(stage_r, p, acc0, acc1);
+    value_pair<4>(stage_r, p, acc0, acc1);
+    value_pair<5>(stage_r, p, acc0, acc1);
+    value_pair<6>(stage_r, p, acc0, acc1);
+    value_pair<7>(stage_r, p, acc0, acc1);
   };
 
+  // tiles two at a time from two code buffers: each tile's codes load while the one before
+  // it is worked on
   TilePair<KW, KN, VW, VN> ca = tile_pair<D, KW, KN, VW, VN>(a, w, 0);
   for (uint32_t t = 0; t <= last; t += 2) {
     const uint32_t t1 = min(t + 1, last);
@@ -603,12 +654,12 @@ __global__ __launch_bounds__(kBlockThreads, 3) void attn_mfma_chunk_kernel(AttnA
     if (t1 != t) tile_work(cb, t1);
   }
 
-  // l of head j: every row holds the same partial sums, so the row's four token groups are
-  // added; lane 4b + j stores elements 8b .. 8b + 7 of head j
-  lsum += __shfl_xor(lsum, 4);
-  lsum += __shfl_xor(lsum, 8);
-  if ((uint32_t)j < w.gc) {
-    const uint64_t idx = ((uint64_t)w.b * a.Hq + w.h * a.G + w.g0 + j) * a.n_chunks + w.chunk;
+  // l of head x: the rows hold different tokens (the columns of a row the same sums); lane
+  // 4b + j stores elements 8b .. 8b + 7 of head j
+  lsum += __shfl_xor(lsum, 16);
+  lsum += __shfl_xor(lsum, 32);
+  if ((uint32_t)x < w.gc) {
+    const uint64_t idx = ((uint64_t)w.b * a.Hq + w.h * a.G + w.g0 + x) * a.n_chunks + w.chunk;
     float* dst = a.ws_acc + idx * D + 8 * (lane >> 2);
     *(float4*)dst = make_float4(acc0[0], acc1[0], acc0[1], acc1[1]);
     *(float4*)(dst + 4) = make_float4(acc0[2], acc1[2], acc0[3], acc1[3]);
@@ -735,10 +786,10 @@ void launch_chunk_v(const AttnArgs& a, int vf, dim3 grid, hipStream_t s) {
   }
 }
 
-// Fewest workgroups of the chunk kernel per compute unit over the four value formats that
-// follow key format KF; 0 on a HIP error.
+// Workgroups of the chunk kernel for key format KF and value format vf that one compute unit
+// holds at once; 0 on a HIP error.
 template <int D, int KF>
-int chunk_blocks_v() {
+int chunk_blocks_v(int vf) {
   constexpr int KW = (KF & 1) ? 8 : 6, KN = (KF & 2) ? 4 : 8;
   const void* f[4];
   if constexpr (D == 128) {
@@ -752,23 +803,20 @@ int chunk_blocks_v() {
     f[2] = (const void*)attn_chunk_kernel<D, KW, KN, 6, 4>;
     f[3] = (const void*)attn_chunk_kernel<D, KW, KN, 8, 4>;
   }
-  int fewest = 1 << 30;
-  for (const void* k : f) {
-    int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k, kBlockThreads, 0) != hipSuccess)
-      return 0;
-    fewest = nb < fewest ? nb : fewest;
-  }
-  return fewest;
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, f[vf & 3], kBlockThreads, 0) != hipSuccess)
+    return 0;
+  return nb;
 }
 
 template <int D>
-int chunk_blocks() {
-  const int b[4] = {chunk_blocks_v<D, 0>(), chunk_blocks_v<D, 1>(), chunk_blocks_v<D, 2>(),
-                    chunk_blocks_v<D, 3>()};
-  int fewest = b[0];
-  for (int x : b) fewest = x < fewest ? x : fewest;
-  return fewest;
+int chunk_blocks(int kf, int vf) {
+  switch (kf & 3) {
+    case 0: return chunk_blocks_v<D, 0>(vf);
+    case 1: return chunk_blocks_v<D, 1>(vf);
+    case 2: return chunk_blocks_v<D, 2>(vf);
+    default: return chunk_blocks_v<D, 3>(vf);
+  }
 }
 
 template <int D>
@@ -784,8 +832,9 @@ void launch_chunk_kv(const AttnArgs& a, int kf, int vf, dim3 grid, hipStream_t s
 }  // namespace
 }  // namespace tvq
 
-int tvq_attention_blocks_per_cu(int d) {
-  const int nb = d == 128 ? tvq::chunk_blocks<128>() : d == 64 ? tvq::chunk_blocks<64>() : 0;
+int tvq_attention_blocks_per_cu(int d, int k_format, int v_format) {
+  const int nb = d == 128 ? tvq::chunk_blocks<128>(k_format, v_format)
+                          : d == 64 ? tvq::chunk_blocks<64>(k_format, v_format) : 0;
   return nb > 0 ? nb : -1;
 }
 

@@ -120,7 +120,9 @@ __device__ __forceinline__ double ladder_rho(float rmin, float rmax, uint32_t ql
   return lo_c == hi_c ? 1.0 : ladder_ratio(lo_c, hi_c, qlevels);
 }
 
-template <int LPV, class Store>
+// COUNT > 0: the caller knows that every lane stores COUNT levels (qlevels + 1 = COUNT * LPV),
+// and the loop is unrolled.
+template <int LPV, int COUNT = 0, class Store>
 __device__ __forceinline__ void ladder_levels_each(Store&& store, int sub, float rmin, float rmax,
                                                    double rho, uint32_t qlevels) {
   const float lo_c = fmaxf(rmin, FLT_MIN), hi_c = fmaxf(rmax, FLT_MIN);
@@ -130,16 +132,24 @@ __device__ __forceinline__ void ladder_levels_each(Store&& store, int sub, float
   if constexpr (LPV >= 4) pw = (sub & 2) ? pw * rho2 : pw;
   const double step = (LPV >= 4) ? rho2 * rho2 : rho2;    // rho^LPV
   double v = (double)lo_c * pw;
-  for (uint32_t q = sub; q <= qlevels; q += LPV) {
-    store(q, deg ? rmin : (float)v);
-    v *= step;
+  if constexpr (COUNT > 0) {
+#pragma unroll
+    for (int k = 0; k < COUNT; ++k) {
+      store(sub + LPV * k, deg ? rmin : (float)v);
+      v *= step;
+    }
+  } else {
+    for (uint32_t q = sub; q <= qlevels; q += LPV) {
+      store(q, deg ? rmin : (float)v);
+      v *= step;
+    }
   }
 }
 
-template <int LPV, class Store>
+template <int LPV, int COUNT = 0, class Store>
 __device__ __forceinline__ void log_level_ladder_each(Store&& store, int sub, float rmin,
                                                       float rmax, uint32_t qlevels) {
-  ladder_levels_each<LPV>(store, sub, rmin, rmax, ladder_rho(rmin, rmax, qlevels), qlevels);
+  ladder_levels_each<LPV, COUNT>(store, sub, rmin, rmax, ladder_rho(rmin, rmax, qlevels), qlevels);
 }
 template <int LPV>
 __device__ __forceinline__ void log_level_ladder(float* tab, int sub, float rmin, float rmax,
@@ -165,6 +175,20 @@ __device__ __forceinline__ TileCodes<WA, NB> load_codes_at(const uint8_t* const 
   c.ang = load_chunk<WA>(plane[0] + (uint64_t)slot * rec[0] + 2 * WA * sub);
   c.nrm = load_chunk<NB>(plane[1] + (uint64_t)slot * rec[1] + 2 * NB * sub);
   c.hdr = *(const u32x2*)(plane[2] + (uint64_t)slot * 8);
+  return c;
+}
+
+// load_codes_at for slot slot0 + j, where slot0 is the same for the whole wave: the record
+// addresses of slot0 stay scalar and each lane adds a 32-bit offset (j * rec <= 2^31 here: j
+// indexes a tile, rec is at most a few hundred bytes).
+template <int WA, int NB>
+__device__ __forceinline__ TileCodes<WA, NB> load_codes_from(const uint8_t* const (&plane)[3],
+                                                             const uint32_t (&rec)[3],
+                                                             uint32_t slot0, uint32_t j, int sub) {
+  TileCodes<WA, NB> c;
+  c.ang = load_chunk<WA>(plane[0] + (uint64_t)slot0 * rec[0] + (j * rec[0] + 2 * WA * sub));
+  c.nrm = load_chunk<NB>(plane[1] + (uint64_t)slot0 * rec[1] + (j * rec[1] + 2 * NB * sub));
+  c.hdr = *(const u32x2*)(plane[2] + (uint64_t)slot0 * 8 + j * 8);
   return c;
 }
 

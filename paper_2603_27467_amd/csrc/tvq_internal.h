@@ -173,6 +173,6 @@ int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, u
 // k_format / v_format: bit 0 set for 8-bit angle codes (n = 256), bit 1 for 4-bit log norms.
 int tvq_launch_attention(const tvq::AttnArgs& a, int d, int k_format, int v_format, int o_f32,
                          void* stream);
-// Chunk-kernel workgroups of head dimension d that one compute unit holds at once (the
-// fewest over the formats), or -1 on a HIP error.
-int tvq_attention_blocks_per_cu(int d);
+// Chunk-kernel workgroups of head dimension d and the given key and value formats (as for
+// tvq_launch_attention) that one compute unit holds at once, or -1 on a HIP error.
+int tvq_attention_blocks_per_cu(int d, int k_format, int v_format);
