@@ -473,16 +473,21 @@ __device__ __forceinline__ void value_pair(const float* stage_r, const float (&p
 template <int KW, int KN, int VW, int VN>
 __global__ __launch_bounds__(kBlockThreads, 4) void attn_mfma_chunk_kernel(AttnArgs a) {
   constexpr int D = 128;
+  // the layer's K and V tables (n = 2^KW and 2^VW entries: the host dispatches on n).  A table
+  // depends only on n and d, so K and V with the same n share one (at n = 256 the second copy
+  // would keep the fourth block of the compute unit out of the LDS).
+  constexpr bool kShared = KW == VW;
   __shared__ float2 s_lut_k[1 << KW];
-  __shared__ float2 s_lut_v[1 << VW];
+  __shared__ float2 s_lut_v[kShared ? 1 : (1 << VW)];
   __shared__ __attribute__((aligned(16))) float s_wave[kWavesPerBlock][kStageWords];
-
-  // the layer's K and V tables (n = 2^KW and 2^VW entries: the host dispatches on n)
   const SegParams spk = a.segs[2 * a.layer], spv = a.segs[2 * a.layer + 1];
   for (uint32_t e = threadIdx.x; e < (1u << KW); e += kBlockThreads)
     s_lut_k[e] = ((const float2*)a.lut)[spk.lut_off + e];
-  for (uint32_t e = threadIdx.x; e < (1u << VW); e += kBlockThreads)
-    s_lut_v[e] = ((const float2*)a.lut)[spv.lut_off + e];
+  if constexpr (!kShared) {
+    for (uint32_t e = threadIdx.x; e < (1u << VW); e += kBlockThreads)
+      s_lut_v[e] = ((const float2*)a.lut)[spv.lut_off + e];
+  }
+  const float2* const lut_v = kShared ? s_lut_k : s_lut_v;
   __syncthreads();
 
   const uint32_t wib = threadIdx.x / kWave;
@@ -599,7 +604,7 @@ __global__ __launch_bounds__(kBlockThreads, 4) void attn_mfma_chunk_kernel(AttnA
       }
 #pragma unroll
       for (int i = 0; i < kPairsPerLane; ++i) {
-        const float2 cs = s_lut_v[kc[i]];
+        const float2 cs = lut_v[kc[i]];
         *(float2*)(stage_w + kPairPitch * i) = make_float2(r[i] * cs.x, r[i] * cs.y);
       }
     }
