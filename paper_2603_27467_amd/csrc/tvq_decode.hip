@@ -77,6 +77,21 @@ __device__ __forceinline__ TilePos tile_pos(const DecodeArgs& a, uint32_t j0, in
   return p;
 }
 
+// Whole-tile rows (the call's token count a multiple of the tile's vector count, contiguous
+// cache): a tile's vectors are consecutive tokens of one (batch, head), so the position of its
+// first vector is wave-uniform -- computed once per tile in scalar registers -- and a lane's
+// vector is that position plus its vector slot.
+__device__ __forceinline__ TilePos tile_pos_rows(const DecodeArgs& a, uint32_t j0) {
+  TilePos p;
+  p.bh = fast_div(j0, a.div_t);
+  p.t = j0 - p.bh * a.div_t.div;
+  p.b = fast_div(p.bh, a.div_h);
+  p.h = p.bh - p.b * a.H;
+  p.slot = p.bh * a.cap + a.t_begin + p.t;
+  p.valid = p.present = true;
+  return p;
+}
+
 // Per-wave state shared by every tile of the wave's segment.
 template <int D>
 struct WaveState {
@@ -241,7 +256,9 @@ __device__ __forceinline__ void store_direct(const DecodeArgs& a, const WaveStat
 // codes can leave this tile's stores in flight.  A lane past the end (its position is that of
 // the tile's first vector) stores the first vector's block again: the same bytes to the same
 // address.
-template <int D, bool F32OUT>
+// ROWS: `pos` is the tile's first vector (tile_pos_rows), every lane's vector is in range, and
+// the host has checked that (VPW - 1) * stride_t elements fit a 32-bit byte offset.
+template <int D, bool F32OUT, bool ROWS = false>
 __device__ __forceinline__ void store_staged(const DecodeArgs& a, const WaveState<D>& w,
                                              const TilePos& pos,
                                              const uint32_t (&o)[OutWords<F32OUT>::NW],
@@ -258,17 +275,29 @@ __device__ __forceinline__ void store_staged(const DecodeArgs& a, const WaveStat
   for (int q = 0; q < NBL; ++q)
     *(u32x4a*)(row + 4 * q) = u32x4a{o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]};
   wave_lds_sync();
-  const bool lane_ok = pos.valid && pos.t >= (uint32_t)w.vslot &&
-                       pos.t - w.vslot + VPW <= a.div_t.div;
-  const bool contig = a.stride_t == (uint32_t)D && __all(lane_ok);
-  const int vs = pos.valid ? w.vslot : 0;
-  uint8_t* vec = (uint8_t*)(w.sp.kind ? a.v_out : a.k_out) + out_elem(a, w.sp.layer, pos) * EB;
+  bool contig;
+  int vs;
+  uint8_t* dst0;
+  uint8_t* const out = (uint8_t*)(w.sp.kind ? a.v_out : a.k_out);
+  if constexpr (ROWS) {
+    contig = a.stride_t == (uint32_t)D;
+    vs = w.vslot;
+    uint8_t* const vec0 = out + out_elem(a, w.sp.layer, pos) * EB;      // wave-uniform
+    dst0 = contig ? vec0 + w.lane * 16
+                  : vec0 + ((uint32_t)w.vslot * a.stride_t * (uint32_t)EB + w.sub * 16);
+  } else {
+    const bool lane_ok = pos.valid && pos.t >= (uint32_t)w.vslot &&
+                         pos.t - w.vslot + VPW <= a.div_t.div;
+    contig = a.stride_t == (uint32_t)D && __all(lane_ok);
+    vs = pos.valid ? w.vslot : 0;
+    uint8_t* vec = out + out_elem(a, w.sp.layer, pos) * EB;
+    dst0 = contig ? vec - (size_t)w.vslot * D * EB + w.lane * 16 : vec + w.sub * 16;
+  }
   // contiguous: block 64 k + L is word (64 k + L) % NBL * 4 of lane (64 k + L) / NBL;
   // per vector: block k LPV + sub is word ((k LPV) % NBL + sub) * 4 of lane
   // vs LPV + k LPV / NBL
   const uint32_t lds0 = contig ? (w.lane / NBL) * PITCH + (w.lane % NBL) * 4
                                : vs * LPV * PITCH + w.sub * 4;
-  uint8_t* dst0 = contig ? vec - (size_t)w.vslot * D * EB + w.lane * 16 : vec + w.sub * 16;
   const size_t dst_step = contig ? kWave * 16 : LPV * 16;
 #pragma unroll
   for (int k = 0; k < NBL; ++k) {
@@ -278,14 +307,18 @@ __device__ __forceinline__ void store_staged(const DecodeArgs& a, const WaveStat
   }
 }
 
-template <int D, int WA, int NB>
+template <int D, int WA, int NB, bool ROWS = false>
 __device__ __forceinline__ TileCodes<WA, NB> load_tile_codes(const DecodeArgs& a,
                                                               const WaveState<D>& w, uint32_t tile) {
+  if constexpr (ROWS) {
+    const TilePos p0 = tile_pos_rows(a, tile * WaveState<D>::VPW);
+    return load_codes_from<WA, NB>(w.plane, w.sp.rec, p0.slot, (uint32_t)w.vslot, w.sub);
+  }
   const TilePos p = tile_pos(a, tile * WaveState<D>::VPW, w.vslot);
   return load_codes_at<WA, NB>(w.plane, w.sp.rec, p.slot, w.sub);
 }
 
-template <int D, bool F32OUT, int WA, int NB>
+template <int D, bool F32OUT, int WA, int NB, bool ROWS = false>
 __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState<D>& w,
                                             uint32_t* stg, const TileCodes<WA, NB>& c,
                                             uint32_t tile, double rho) {
@@ -308,7 +341,10 @@ __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState
   }
   uint32_t o[OutWords<F32OUT>::NW];
   reconstruct<D, F32OUT, true>(a, w, kc, r, o);
-  store_staged<D, F32OUT>(a, w, tile_pos(a, tile * WaveState<D>::VPW, w.vslot), o, stg);
+  if constexpr (ROWS)
+    store_staged<D, F32OUT, true>(a, w, tile_pos_rows(a, tile * WaveState<D>::VPW), o, stg);
+  else
+    store_staged<D, F32OUT>(a, w, tile_pos(a, tile * WaveState<D>::VPW, w.vslot), o, stg);
 }
 
 // Tiles tile0 .. tile0 + ntiles - 1.  MULTI: two per iteration from two code buffers, each
@@ -318,13 +354,13 @@ __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState
 // has no branch around a load or a store, and nothing has to wait for a load before its data
 // is used.  Launches of one tile per wave use the instantiation without the loop (a separate
 // copy of the tile code inside the same kernel would raise its register count).
-template <int D, bool F32OUT, bool MULTI, int WA, int NB>
+template <int D, bool F32OUT, bool MULTI, int WA, int NB, bool ROWS = false>
 __device__ void decode_tiles_prefetch(const DecodeArgs& a, const WaveState<D>& w, uint32_t* stg,
                                       uint32_t tile0, uint32_t ntiles) {
   constexpr int LPV = WaveState<D>::LPV;
   constexpr uint32_t kLevels = (1u << NB) - 1u;
   const uint32_t last = tile0 + ntiles - 1;
-  TileCodes<WA, NB> ca = load_tile_codes<D, WA, NB>(a, w, tile0);
+  TileCodes<WA, NB> ca = load_tile_codes<D, WA, NB, ROWS>(a, w, tile0);
   if constexpr (!MULTI) {
     const float rmin = __uint_as_float(ca.hdr.x), rmax = __uint_as_float(ca.hdr.y);
     decode_tile<D, F32OUT>(a, w, stg, ca, tile0,
@@ -335,20 +371,20 @@ __device__ void decode_tiles_prefetch(const DecodeArgs& a, const WaveState<D>& w
   if constexpr (NB != 8) lg.load(a, w, w.plane[2], tile0, last);
   for (uint32_t t = tile0; t <= last; t += 2) {
     const uint32_t t1 = min(t + 1, last);
-    const TileCodes<WA, NB> cb = load_tile_codes<D, WA, NB>(a, w, t1);
+    const TileCodes<WA, NB> cb = load_tile_codes<D, WA, NB, ROWS>(a, w, t1);
     double rho = 1.0;
     if constexpr (NB != 8) rho = lg.at(a, w, t, (t - tile0) % LPV, last, kLevels);
-    decode_tile<D, F32OUT>(a, w, stg, ca, t, rho);
-    ca = load_tile_codes<D, WA, NB>(a, w, min(t + 2, last));
+    decode_tile<D, F32OUT, WA, NB, ROWS>(a, w, stg, ca, t, rho);
+    ca = load_tile_codes<D, WA, NB, ROWS>(a, w, min(t + 2, last));
     // t1 == t (the last tile again) keeps the ratio of tile t
     if constexpr (NB != 8) {
       if (t1 != t) rho = lg.at(a, w, t1, (t1 - tile0) % LPV, last, kLevels);
     }
-    decode_tile<D, F32OUT>(a, w, stg, cb, t1, rho);
+    decode_tile<D, F32OUT, WA, NB, ROWS>(a, w, stg, cb, t1, rho);
   }
 }
 
-template <int D, bool F32OUT, bool MULTI>
+template <int D, bool F32OUT, bool MULTI, bool ROWS = false>
 __global__ __launch_bounds__(kBlockThreads) void decode_fast_kernel(DecodeArgs a) {
   constexpr int kStageWords = kWave * OutWords<F32OUT>::PITCH;
   static_assert(kStageWords >= kLvlPerWave, "the level table shares the staging area");
@@ -361,11 +397,11 @@ __global__ __launch_bounds__(kBlockThreads) void decode_fast_kernel(DecodeArgs a
   uint32_t* stg = s_stg[w.wib];
   const bool wide = w.sp.w == 8;
   if (w.sp.mode == 1) {
-    if (wide) decode_tiles_prefetch<D, F32OUT, MULTI, 8, 8>(a, w, stg, tile0, ntiles);
-    else decode_tiles_prefetch<D, F32OUT, MULTI, 6, 8>(a, w, stg, tile0, ntiles);
+    if (wide) decode_tiles_prefetch<D, F32OUT, MULTI, 8, 8, ROWS>(a, w, stg, tile0, ntiles);
+    else decode_tiles_prefetch<D, F32OUT, MULTI, 6, 8, ROWS>(a, w, stg, tile0, ntiles);
   } else {
-    if (wide) decode_tiles_prefetch<D, F32OUT, MULTI, 8, 4>(a, w, stg, tile0, ntiles);
-    else decode_tiles_prefetch<D, F32OUT, MULTI, 6, 4>(a, w, stg, tile0, ntiles);
+    if (wide) decode_tiles_prefetch<D, F32OUT, MULTI, 8, 4, ROWS>(a, w, stg, tile0, ntiles);
+    else decode_tiles_prefetch<D, F32OUT, MULTI, 6, 4, ROWS>(a, w, stg, tile0, ntiles);
   }
 }
 
@@ -449,9 +485,16 @@ int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, u
   const bool paged = a.pg.table != nullptr;
   if (paged && fast) return -1;       // a paged source goes to the generic kernel
   const bool multi = a.tiles_per_wave > 1;
+  // whole-tile rows: every tile's vectors consecutive tokens of one (batch, head), and a lane's
+  // output offset within its tile, (VPW - 1) * stride_t elements, inside 32 bits
+  const uint32_t vpw = d == 128 ? 16u : 32u;
+  const bool rows = !paged && a.div_t.div % vpw == 0 &&
+                    (uint64_t)a.stride_t * vpw * (out_f32 ? 4u : 2u) < (1ull << 31);
 #define TVQ_LAUNCH_DEC(D, F32)                                                                  \
   do {                                                                                          \
-    if (fast && multi)                                                                          \
+    if (fast && multi && rows)                                                                  \
+      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true, true>), dim3(grid), block, 0, s, a); \
+    else if (fast && multi)                                                                     \
       hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true>), dim3(grid), block, 0, s, a);  \
     else if (fast)                                                                              \
       hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, false>), dim3(grid), block, 0, s, a); \
