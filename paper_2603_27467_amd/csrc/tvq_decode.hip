@@ -145,14 +145,15 @@ __device__ __forceinline__ bool wave_setup(const DecodeArgs& a, WaveState<D>& w,
 // (16 per vector): the ladder R'min * rho^q, split over the vector's LPV lanes.  Level 0 is
 // R'min exactly and RN32 brings the top level back to R'max.  Vectors with R'min == R'max get
 // Rmin at every level.
-template <int D>
+// COUNT > 0: every lane stores COUNT levels (qlevels + 1 = COUNT * LPV), the loop unrolled.
+template <int D, int COUNT = 0>
 __device__ __forceinline__ const float* build_log_levels(const WaveState<D>& w, float* lvl,
                                                          float rmin, float rmax, double rho,
                                                          uint32_t qlevels) {
   float* tab = lvl + (w.vslot << kLvlBits);
   wave_lds_sync();             // earlier reads of this LDS area are done
-  ladder_levels_each<WaveState<D>::LPV>([tab](uint32_t q, float v) { tab[q] = v; }, w.sub, rmin,
-                                        rmax, rho, qlevels);
+  ladder_levels_each<WaveState<D>::LPV, COUNT>([tab](uint32_t q, float v) { tab[q] = v; }, w.sub,
+                                               rmin, rmax, rho, qlevels);
   wave_lds_sync();
   return tab;
 }
@@ -335,7 +336,8 @@ __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState
 #pragma unroll
     for (int i = 0; i < kPairsPerLane; ++i) r[i] = __builtin_fmaf((float)qc[i], step, rmin);
   } else {
-    const float* tab = build_log_levels<D>(w, (float*)stg, rmin, rmax, rho, kLevels);
+    constexpr int kPerLane = (int)(kLevels + 1u) / WaveState<D>::LPV;
+    const float* tab = build_log_levels<D, kPerLane>(w, (float*)stg, rmin, rmax, rho, kLevels);
 #pragma unroll
     for (int i = 0; i < kPairsPerLane; ++i) r[i] = tab[qc[i]];
   }
