@@ -67,20 +67,6 @@ __device__ __forceinline__ float row_ror(float v) {
   return __uint_as_float(row_ror<N>(__float_as_uint(v)));
 }
 
-// v[l] + v[l ^ 16] and v[l] + v[l ^ 32] on every lane: v_permlane16_swap exchanges rows 2i and
-// 2i + 1 between two copies of v, v_permlane32_swap the two halves; both lanes of a pair add the
-// same two values, so they hold the same sum.
-__device__ __forceinline__ float sum_xor16(float v) {
-  const auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
-                                                  false);
-  return __uint_as_float(t[0]) + __uint_as_float(t[1]);
-}
-__device__ __forceinline__ float sum_xor32(float v) {
-  const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
-                                                  false);
-  return __uint_as_float(t[0]) + __uint_as_float(t[1]);
-}
-
 // Sum over the wave's vector slots (lanes sub, sub + LPV, ...): every lane gets its sub's sum.
 template <int LPV>
 __device__ __forceinline__ float slot_sum(float v) {
