@@ -795,7 +795,7 @@ def main() -> int:
         a = args.summarize_attention_profiles
         return summarize_attention_profiles(*a[:5], args.commands, int(a[5]))
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: the codec is per-vector and this build measures "
+        print("bench.py runs on one GPU only: the codec is per-vector and the bench measures "
               "one GPU's share; --gpus above 1 is not supported", file=sys.stderr)
         return 2
 
