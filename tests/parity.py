@@ -273,17 +273,23 @@ class DecodeCheck:
     bf16_undecided: int = 0
     bf16_undecided_max_over_bound: float = 0.0
     mirror_mismatch_elems: int = 0      # against the fixed-order fp32 decode (reported only)
+    f32_elems: int = 0                  # elements checked in each output type
+    bf16_elems: int = 0
 
     def ok(self) -> bool:
         return (self.f32_max_rel_l2 <= 1e-5 and self.f32_max_elem_over_bound <= 1.0 and
                 self.bf16_max_ulp <= 1 and self.bf16_undecided_max_over_bound <= 1.0)
 
     def line(self) -> str:
-        return (f"vectors={self.vectors} fp32: max rel L2 {self.f32_max_rel_l2:.2e}, max "
-                f"|err|/bound {self.f32_max_elem_over_bound:.3f}; bf16: max ulp vs RNE(fp64) "
-                f"{self.bf16_max_ulp}, undecided elements {self.bf16_undecided} (max "
-                f"|err|/(E+ulp) {self.bf16_undecided_max_over_bound:.3f}); fixed-order fp32 "
-                f"decode differs in {self.mirror_mismatch_elems} elements (reported)")
+        f32 = (f"fp32 ({self.f32_elems} elements): max rel L2 {self.f32_max_rel_l2:.2e}, max "
+               f"|err|/bound {self.f32_max_elem_over_bound:.3f}" if self.f32_elems
+               else "fp32: not checked")
+        bf16 = (f"bf16 ({self.bf16_elems} elements): max ulp vs RNE(fp64) {self.bf16_max_ulp}, "
+                f"undecided elements {self.bf16_undecided} (max |err|/(E+ulp) "
+                f"{self.bf16_undecided_max_over_bound:.3f})" if self.bf16_elems
+                else "bf16: not checked")
+        return (f"vectors={self.vectors} {f32}; {bf16}; fixed-order fp32 decode differs in "
+                f"{self.mirror_mismatch_elems} elements (reported)")
 
 
 def check_decoded(chk: DecodeCheck, ref64: np.ndarray, d: int, g32=None, g16=None,
@@ -295,6 +301,7 @@ def check_decoded(chk: DecodeCheck, ref64: np.ndarray, d: int, g32=None, g16=Non
     E = decode_error_bound(ref64, d)
     chk.vectors += int(np.prod(ref64.shape[:-1]))
     if g32 is not None:
+        chk.f32_elems += int(ref64.size)
         g = np.asarray(g32, np.float32).astype(np.float64)
         err = np.abs(g - ref64)
         chk.f32_max_elem_over_bound = max(chk.f32_max_elem_over_bound, float((err / E).max(initial=0)))
@@ -309,6 +316,7 @@ def check_decoded(chk: DecodeCheck, ref64: np.ndarray, d: int, g32=None, g16=Non
             chk.mirror_mismatch_elems += int(np.count_nonzero(
                 (gg.view(np.uint32) != m.view(np.uint32)) & ~((gg == 0) & (m == 0))))
     if g16 is not None:
+        chk.bf16_elems += int(ref64.size)
         g16 = np.asarray(g16, np.uint16)
         rne = f64_to_bf16(ref64)
         decided = np.abs(ref64) >= 2.0 ** 9 * E

@@ -68,6 +68,10 @@ def test_faithful_fp32_decode_meets_the_bars(d):
     assert chk.ok(), chk.line()
     assert chk.mirror_mismatch_elems == 0
     assert chk.f32_max_elem_over_bound < 0.25
+    assert chk.f32_elems == chk.bf16_elems == ref.size
+    # a check that saw one output type says so instead of reporting zeros for the other
+    only16 = check_decoded(DecodeCheck(), ref, d, g16=oracle.f32_to_bf16(f32))
+    assert "fp32: not checked" in only16.line() and only16.f32_elems == 0
 
 
 @pytest.mark.parametrize("d", [64, 128])
