@@ -45,7 +45,14 @@ VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4
 CODEC_SOURCES = ["tvq_encode.hip", "tvq_decode.hip", "tvq_codes.h", "tvq_device.h",
                  "tvq_internal.h"]
 ATTENTION_SOURCES = ["tvq_attention.hip", "tvq_codes.h", "tvq_device.h", "tvq_internal.h"]
-ATTENTION_COUNTERS = os.path.join(ROOT, "profiles", "longctx_c5_attention_counters.json")
+# the attention counter summary of each workload the attention step runs on
+ATTENTION_COUNTER_FILES = {"C5": "longctx_c5_attention_counters.json",
+                           "C4": "d64_batch8_c4_attention_counters.json"}
+
+
+def attention_counters(workload_key: str):
+    name = ATTENTION_COUNTER_FILES.get(workload_key)
+    return None if name is None else os.path.join(ROOT, "profiles", name)
 ATTN_GROUP = 4          # query heads per KV head (32 query heads over 8 KV heads)
 PAGE_TOKENS = 256       # slots per block of the paged pool
 
@@ -423,12 +430,14 @@ def longctx_bytes(w: workloads.Workload):
 
 
 def summarize_attention_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, commands,
-                                 steps_total: int) -> int:
-    """Counter summary of the long-context attention step (the runs of `commands`, each with
-    `steps_total` = warmup + timed steps): per chunk-kernel instantiation and for the merge
-    kernel, HBM bytes per dispatch (FETCH_SIZE / WRITE_SIZE scaled by the 1 GiB copy), VALU and
-    LDS instructions, bank-conflict cycles and VALU busy; and the HBM bytes of one step."""
-    w = workloads.get("C5")
+                                 steps_total: int, workload_key: str = "C5") -> int:
+    """Counter summary of the attention step over the cache of `workload_key` (the runs of
+    `commands`, each with `steps_total` = warmup + timed steps): per chunk-kernel instantiation
+    and for the merge kernel, HBM bytes per dispatch (FETCH_SIZE / WRITE_SIZE scaled by the
+    1 GiB copy), VALU and LDS instructions, bank-conflict cycles and VALU busy; and the HBM
+    bytes of one step."""
+    w = workloads.get(workload_key)
+    counters_path = attention_counters(workload_key)
     rec_tok, _, qo = longctx_bytes(w)
     t_mean = w.T + (steps_total + 1) / 2            # tokens attended per step, mean
     per = {}
@@ -512,9 +521,10 @@ def summarize_attention_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_d
     lines += [f"    {c}" for c in commands]
     lines += ["", f"FETCH_SIZE scale from the 1 GiB copy: {fetch_scale:.4f}; WRITE_SIZE scale: "
               f"{write_scale:.4f}; tokens attended per step (mean): {t_mean}", "",
-              f"Per step (32 layer calls): HBM {ent['hbm_bytes_per_step']} B by counters vs "
+              f"Per step ({w.L} layer calls): HBM {ent['hbm_bytes_per_step']} B by counters vs "
               f"{ent['algorithmic_bytes_per_step']} B algorithmic; VALU {ent['valu_insts_per_tile']}"
-              f" instructions per tile of 16 tokens; LDS bank-conflict cycles per tile "
+              f" instructions per tile of {64 // (w.d // 32)} tokens; LDS bank-conflict cycles "
+              f"per tile "
               f"{ent['lds_bank_conflict_cycles_per_tile']}; VALUBusy {ent['valu_busy_pct']} %", "",
               "| kernel | dispatches/step | avg ns (trace) | fetch B/dispatch | write B/dispatch | "
               "VALU/dispatch (incl. MFMA) | MFMA/dispatch | LDS/dispatch | bank-conflict cycles | "
@@ -534,9 +544,9 @@ def summarize_attention_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_d
         rows = [ln.rstrip("\n") for ln in f]
     lines += [rows[0]] + [r for r in rows[1:] if "tvq::" in r]
     lines += ["```"]
-    with open(ATTENTION_COUNTERS, "w") as f:
+    with open(counters_path, "w") as f:
         json.dump(out, f, indent=1)
-    with open(ATTENTION_COUNTERS.replace("_counters.json", "_counters.md"), "w") as f:
+    with open(counters_path.replace("_counters.json", "_counters.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
     return 0
@@ -683,7 +693,9 @@ def run_longctx(w: workloads.Workload, args) -> dict:
     if args.attention:
         # codes of every cached token once, plus the bf16 queries and outputs of every layer
         att_bytes = rec_tok * t_mean + qo
-        prof = profile_entry("tvq_attention", w.name, ATTENTION_COUNTERS, ATTENTION_SOURCES)
+        path = attention_counters(args.workload)
+        prof = None if path is None else profile_entry("tvq_attention", w.name, path,
+                                                       ATTENTION_SOURCES)
         att_gbs = att_bytes / (dec_ms * 1e-3) / 1e9
         return {
             "metric": "attention over the compressed cache: bf16-equivalent KV GB/s consumed",
@@ -767,8 +779,8 @@ def main() -> int:
     ap.add_argument("--workload", default="C2")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--attention", action="store_true",
-                    help="long-context workload: attention over the compressed cache in place "
-                         "of the full decode")
+                    help="attention over the compressed cache in place of the full decode "
+                         "(the long-context cache of C5, or the cache of the workload named)")
     ap.add_argument("--encode-mfma", action="store_true",
                     help="encode with the matrix-core transform schedule (comparison)")
     ap.add_argument("--paged", action="store_true",
@@ -782,8 +794,8 @@ def main() -> int:
                     help="write the profiles/ counter summary from rocprofv3 output dirs")
     ap.add_argument("--summarize-attention-profiles", nargs=6,
                     metavar=("TRACE", "FETCH", "WRITE", "SQ", "VALU", "STEPS_TOTAL"),
-                    help="write the profiles/ counter summary of the long-context attention "
-                         "step from rocprofv3 output dirs")
+                    help="write the profiles/ counter summary of the attention step over "
+                         "the --workload cache (C5 or C4) from rocprofv3 output dirs")
     ap.add_argument("--commands", nargs="*", default=[],
                     help="the profiling commands, recorded in the summary")
     args = ap.parse_args()
@@ -793,7 +805,7 @@ def main() -> int:
         return summarize_profiles(*args.summarize_profiles, args.commands)
     if args.summarize_attention_profiles:
         a = args.summarize_attention_profiles
-        return summarize_attention_profiles(*a[:5], args.commands, int(a[5]))
+        return summarize_attention_profiles(*a[:5], args.commands, int(a[5]), args.workload)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the codec is per-vector and the bench measures "
               "one GPU's share; --gpus above 1 is not supported", file=sys.stderr)
@@ -806,7 +818,9 @@ def main() -> int:
         print("no GPU visible", file=sys.stderr)
         return 1
     w = workloads.get(args.workload)
-    if args.workload == "C5":
+    if args.workload == "C5" or args.attention:
+        # the serving step over a cache of the workload's shape (C5: the long-context cache;
+        # --attention on another workload: attention over that workload's cache, e.g. d = 64)
         out = run_longctx(w, args)
         if not args.no_cpu_baseline:
             print("# cpu baseline (oracle on host cores)", file=sys.stderr, flush=True)

@@ -19,9 +19,9 @@
 //   per tile  y'_K from the K codes, the scores s_g = q^_g . y'_K, then y'_V from the V codes
 //             and, per head, acc_g += 2^(s_g - m_g) y'_V and l_g += 2^(s_g - m_g)
 //   out       (m, l, acc[d]) per query head and chunk into the workspace
-// Two chunk kernels: attn_chunk_kernel (d = 64) does the contractions as per-lane FMAs, one
-// token per vector slot of a 32-token tile; attn_mfma_chunk_kernel (d = 128) does them on
-// the matrix cores, 16 tokens x 4 heads per tile (its layouts are described where it is).
+// The chunk kernel (attn_mfma_chunk_kernel) does both contractions on the matrix cores, 16
+// tokens (d = 128) or 32 tokens (d = 64) x 4 heads per tile; its layouts are described where
+// it is.
 // m_g is a reference point shared by the wave, not the running maximum: it is raised (and acc,
 // l rescaled) only when a score exceeds it by more than kLazyLog2, so every weight stays below
 // 2^kLazyLog2 and the rescale runs on a few tiles of a chunk.  The merge kernel combines the
@@ -38,19 +38,11 @@
 namespace tvq {
 namespace {
 
-constexpr int kLut = 256;            // entries of each staged table (the formats here: n <= 256)
 constexpr float kLazyLog2 = 8.0f;    // weights 2^(s - m) stay below 2^8 between rescales
 // q^ in LDS: each lane's 32 elements of a head at a pitch of 36 floats, so the d/32 distinct
 // 16-byte reads of a wave (one per lane of a vector, broadcast over the vector slots) fall in
 // distinct banks
 constexpr int kQPitch = kElemsPerLane + 4;
-template <int LPV>
-__device__ __forceinline__ float vec_sum(float v) {
-  if constexpr (LPV >= 2) v += quad_perm<0xB1>(v);
-  if constexpr (LPV >= 4) v += quad_perm<0x4E>(v);
-  return v;
-}
-
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
@@ -87,38 +79,6 @@ struct AttnWave {
   SegParams sp[2];               // K and V of the layer
   const uint8_t* plane[2][3];
 };
-
-// y' of this lane's 32 elements of a token from its codes, in the decode kernels' operation
-// order: r^ from the norm codes, y'_2i = RN(r^_i C'[k_i]), y'_2i+1 = RN(r^_i S'[k_i]).  `lvl`
-// is the vector slot's 16-entry level table (log-space norms).
-template <int LPV, int WA, int NB>
-__device__ __forceinline__ void code_vector(const TileCodes<WA, NB>& c, const float2* lut,
-                                            float* lvl, int sub, float (&y)[kElemsPerLane]) {
-  constexpr uint32_t kLevels = (1u << NB) - 1u;
-  uint32_t kc[kPairsPerLane], qc[kPairsPerLane];
-  unpack16_index<WA>(c.ang, kc);
-  if constexpr (NB == 8) unpack16<NB>(c.nrm, qc);
-  else unpack16_index<NB>(c.nrm, qc);
-  const float rmin = __uint_as_float(c.hdr.x), rmax = __uint_as_float(c.hdr.y);
-  float r[kPairsPerLane];
-  if constexpr (NB == 8) {
-    const float step = linear_step255(rmin, rmax);
-#pragma unroll
-    for (int i = 0; i < kPairsPerLane; ++i) r[i] = __builtin_fmaf((float)qc[i], step, rmin);
-  } else {
-    wave_lds_sync();                    // the previous tile's reads of the table are done
-    log_level_ladder<LPV>(lvl, sub, rmin, rmax, kLevels);
-    wave_lds_sync();
-#pragma unroll
-    for (int i = 0; i < kPairsPerLane; ++i) r[i] = lvl[qc[i]];
-  }
-#pragma unroll
-  for (int i = 0; i < kPairsPerLane; ++i) {
-    const float2 cs = lut[kc[i]];
-    y[2 * i] = r[i] * cs.x;
-    y[2 * i + 1] = r[i] * cs.y;
-  }
-}
 
 template <int KW, int KN, int VW, int VN>
 struct TilePair {
@@ -208,64 +168,6 @@ __device__ __forceinline__ void query_transform(const AttnArgs& a, const AttnWav
   }
 }
 
-// One tile: scores of the slot's token for the pass's heads, then the weighted V sum.
-template <int D, int KW, int KN, int VW, int VN>
-__device__ __forceinline__ void attend_tile(const AttnWave<D>& w, const TilePair<KW, KN, VW, VN>& c,
-                                            uint32_t tile, const float2* lut_k,
-                                            const float2* lut_v, const float* qh, float* lvl,
-                                            float (&m)[kAttnPassHeads], float (&l)[kAttnPassHeads],
-                                            float (&acc)[kAttnPassHeads][kElemsPerLane]) {
-  constexpr int LPV = AttnWave<D>::LPV;
-  constexpr int VPW = AttnWave<D>::VPW;
-  float y[kElemsPerLane];
-  code_vector<LPV, KW, KN>(c.k, lut_k, lvl, w.sub, y);
-  const bool live = tile * VPW + w.vslot < w.ntok;
-  float s[kAttnPassHeads];
-  bool raise = false;
-#pragma unroll
-  for (int g = 0; g < kAttnPassHeads; ++g) {
-    s[g] = -INFINITY;
-    if ((uint32_t)g < w.gc) {
-      const float* qr = qh + (g * LPV + w.sub) * kQPitch;
-      float part = 0.0f;
-#pragma unroll
-      for (int i = 0; i < kElemsPerLane; i += 4) {
-        const float4 qv = *(const float4*)(qr + i);
-        part = __builtin_fmaf(qv.x, y[i], part);
-        part = __builtin_fmaf(qv.y, y[i + 1], part);
-        part = __builtin_fmaf(qv.z, y[i + 2], part);
-        part = __builtin_fmaf(qv.w, y[i + 3], part);
-      }
-      const float sv = vec_sum<LPV>(part);
-      s[g] = live ? sv : -INFINITY;
-      raise = raise || s[g] > m[g] + kLazyLog2;
-    }
-  }
-  if (__builtin_amdgcn_ballot_w64(raise) != 0) {   // a new reference point (wave-uniform)
-#pragma unroll
-    for (int g = 0; g < kAttnPassHeads; ++g) {
-      if ((uint32_t)g < w.gc) {
-        const float mn = fmaxf(m[g], wave_max(s[g]));
-        const float f = __builtin_amdgcn_exp2f(m[g] - mn);   // 0 on the first raise
-        l[g] *= f;
-#pragma unroll
-        for (int i = 0; i < kElemsPerLane; ++i) acc[g][i] *= f;
-        m[g] = mn;
-      }
-    }
-  }
-  code_vector<LPV, VW, VN>(c.v, lut_v, lvl + 16 * VPW, w.sub, y);
-#pragma unroll
-  for (int g = 0; g < kAttnPassHeads; ++g) {
-    if ((uint32_t)g < w.gc) {
-      const float p = __builtin_amdgcn_exp2f(s[g] - m[g]);
-      l[g] += p;
-#pragma unroll
-      for (int i = 0; i < kElemsPerLane; ++i) acc[g][i] = __builtin_fmaf(p, y[i], acc[g][i]);
-    }
-  }
-}
-
 // The chunk wave's work: (sequence, KV head, chunk, pass of query heads), the chunk's tokens
 // (the sequence's own context with per-sequence lengths) and, for a paged cache, the pool
 // blocks of the chunk (lane i: its i-th block).  A chunk with no token writes partials of
@@ -315,81 +217,11 @@ __device__ __forceinline__ bool chunk_setup(const AttnArgs& a, AttnWave<D>& w, u
   return true;
 }
 
-template <int D, int KW, int KN, int VW, int VN>
-__global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
-  constexpr int LPV = AttnWave<D>::LPV;
-  constexpr int VPW = AttnWave<D>::VPW;
-  __shared__ float2 s_lut[2][kLut];
-  __shared__ float4 s_q[kWavesPerBlock][kAttnPassHeads * LPV * kQPitch / 4];
-  __shared__ float s_lvl[kWavesPerBlock][2 * 16 * VPW];
-
-  // the layer's K and V tables, shared by the block (before any wave leaves)
-  const SegParams spk = a.segs[2 * a.layer], spv = a.segs[2 * a.layer + 1];
-  for (uint32_t e = threadIdx.x; e < spk.n; e += kBlockThreads)
-    s_lut[0][e] = ((const float2*)a.lut)[spk.lut_off + e];
-  for (uint32_t e = threadIdx.x; e < spv.n; e += kBlockThreads)
-    s_lut[1][e] = ((const float2*)a.lut)[spv.lut_off + e];
-  __syncthreads();
-
-  AttnWave<D> w;
-  w.lane = threadIdx.x & (kWave - 1);
-  w.sub = w.lane % LPV;
-  w.vslot = w.lane / LPV;
-  const uint32_t wib = threadIdx.x / kWave;
-  w.sp[0] = spk;
-  w.sp[1] = spv;
-  if (!chunk_setup<D>(a, w, wib)) return;
-  float* qh = (float*)s_q[wib];
-  float* lvl = s_lvl[wib] + 16 * w.vslot;
-  if (a.q_f32) query_transform<D, true>(a, w, qh);
-  else query_transform<D, false>(a, w, qh);
-  wave_lds_sync();                                 // q^ visible to every lane
-
-  float m[kAttnPassHeads], l[kAttnPassHeads], acc[kAttnPassHeads][kElemsPerLane];
-#pragma unroll
-  for (int g = 0; g < kAttnPassHeads; ++g) {
-    m[g] = -INFINITY;
-    l[g] = 0.0f;
-#pragma unroll
-    for (int i = 0; i < kElemsPerLane; ++i) acc[g][i] = 0.0f;
-  }
-  // tiles two at a time from two code buffers: each tile's codes load while the one before
-  // it is worked on
-  const uint32_t last = (w.ntok + VPW - 1) / VPW - 1;
-  TilePair<KW, KN, VW, VN> ca = tile_pair<D, KW, KN, VW, VN>(a, w, 0);
-  for (uint32_t t = 0; t <= last; t += 2) {
-    const uint32_t t1 = min(t + 1, last);
-    const TilePair<KW, KN, VW, VN> cb = tile_pair<D, KW, KN, VW, VN>(a, w, t1);
-    attend_tile<D>(w, ca, t, s_lut[0], s_lut[1], qh, lvl, m, l, acc);
-    ca = tile_pair<D, KW, KN, VW, VN>(a, w, min(t + 2, last));
-    if (t1 != t) attend_tile<D>(w, cb, t1, s_lut[0], s_lut[1], qh, lvl, m, l, acc);
-  }
-
-  // slots summed (they share m); slot 0 writes (m, l, acc) of each head
-#pragma unroll
-  for (int g = 0; g < kAttnPassHeads; ++g) {
-    if ((uint32_t)g < w.gc) {
-      const float lg = slot_sum<LPV>(l[g]);
-#pragma unroll
-      for (int i = 0; i < kElemsPerLane; ++i) acc[g][i] = slot_sum<LPV>(acc[g][i]);
-      if (w.vslot == 0) {
-        const uint64_t idx =
-            ((uint64_t)w.b * a.Hq + w.h * a.G + w.g0 + g) * a.n_chunks + w.chunk;
-        float* dst = a.ws_acc + idx * D + w.sub * kElemsPerLane;
-#pragma unroll
-        for (int i = 0; i < kElemsPerLane; i += 4)
-          *(float4*)(dst + i) = make_float4(acc[g][i], acc[g][i + 1], acc[g][i + 2], acc[g][i + 3]);
-        if (w.sub == 0) *(float2*)(a.ws_ml + idx * 2) = make_float2(m[g], lg);
-      }
-    }
-  }
-}
-
-// The chunk kernel at d = 128 with the two contractions on the matrix cores
-// (v_mfma_f32_4x4x1f32: 16 blocks of 4 lanes, block b = lane / 4; block b's C[r][j] +=
-// A[lane 4b + r] * B[lane 4b + j], kept by lane 4b + j in its register r; operand `blgp` 4 + u
-// makes every block take B from the lanes of row u, lanes 16u .. 16u + 15, instead of its own).
-// Lane l sits in row R = l / 16, column c = (l / 4) % 4 and position x = l % 4.
+// The chunk kernel, with the two contractions on the matrix cores (v_mfma_f32_4x4x1f32: 16
+// blocks of 4 lanes, block b = lane / 4; block b's C[r][j] += A[lane 4b + r] * B[lane 4b + j],
+// kept by lane 4b + j in its register r; operand `blgp` 4 + u makes every block take B from
+// the lanes of row u, lanes 16u .. 16u + 15, instead of its own).  Lane l sits in row
+// R = l / 16, column c = (l / 4) % 4 and position x = l % 4.  At d = 128:
 //   codes   lane l reads and rebuilds token 4R + x of the 16-token tile on slice c (pairs
 //           16c .. 16c + 15, elements 32c .. 32c + 31), for K and for V.
 //   scores  the products take q^ of query head x on the same 32 elements.  q^ is the same
@@ -408,7 +240,7 @@ __global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
 // that its arithmetic can overlap the score products.  y' is rebuilt exactly as decode
 // rebuilds it.
 //
-// Per-wave LDS of this kernel, in floats.  Value staging: pair l from word kPairPitch l +
+// Per-wave LDS at d = 128, in floats.  Value staging: pair l from word kPairPitch l +
 // kHalfSkew (l / 32), in it token t and element e at 2t + e; the lane that rebuilt (token t,
 // pair l) stores both elements with one 8-byte write.  The pitch keeps the four lanes of each
 // quad of a 16-byte read on distinct banks, the skew spreads the 8-byte stores of the lanes of
@@ -417,12 +249,27 @@ __global__ __launch_bounds__(kBlockThreads) void attn_chunk_kernel(AttnArgs a) {
 // two copies h = c % 2 that the lanes of even and odd columns read.  The tables share the
 // staging's words: each is written, read into registers, and then overwritten by the same
 // tile's staging.
+//
+// At d = 64 a tile holds 32 tokens, two lanes per token: lane l rebuilds token 8R + 4(c % 2) + x
+// on slice c / 2, so the blocks of columns c and c + 2 hold the two slices of the same four
+// tokens (one row rotation adds them) and those of columns c and c + 1 different tokens.  The
+// value products then need the weights of every token of a row in every column: P_h holds
+// those of tokens 8R + 4h + k (register k), taken from the column itself or its neighbour.
+// Block b accumulates elements 4b .. 4b + 3 (pair 2b + r / 2, element r % 2 in register r) of
+// head j over the 32 tokens.  Staging: pair p at word 64 p, element e at + 32 e, token t at
+// + (t + 16 (p % 2)) % 32, so the four lanes of a quad read 16-byte groups on distinct banks.
+// Level tables: level q of token t at word 32 q + t, one copy.
 constexpr int kPairPitch = 36;
 constexpr int kHalfSkew = 16;
 constexpr int kStageWords = 64 * kPairPitch + kHalfSkew + 16;
+constexpr int kStageWords64 = 32 * 64;
+template <int D>
+constexpr int kStageWordsOf = D == 128 ? kStageWords : kStageWords64;
 constexpr int kLvlWords = 16 * 32;
-static_assert(2 * kLvlWords <= kStageWords, "both level tables fit the staging words");
-static_assert(kAttnPassHeads * 4 * kQPitch <= kStageWords, "q^ fits the staging words");
+static_assert(2 * kLvlWords <= kStageWords && 2 * kLvlWords <= kStageWords64,
+              "both level tables fit the staging words");
+static_assert(kAttnPassHeads * 4 * kQPitch <= kStageWords &&
+              kAttnPassHeads * 2 * kQPitch <= kStageWords64, "q^ fits the staging words");
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
@@ -456,16 +303,34 @@ __device__ __forceinline__ void value_pair(const float* stage_r, const float (&p
   acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(v.w, p[t1 & 3], acc1, 0, 0, 4 + t1 / 4);
 }
 
-template <int KW, int KN, int VW, int VN>
+// d = 64: value products of tokens 4N .. 4N + 3 of the tile (token 8u + 4h + k with u = N / 2,
+// h = N % 2) on this lane's (pair, element), one 16-byte read: the weights of token 8u + 4h + k
+// are register k of P_h in row u.  `lo` and `hi` address tokens 0 .. 15 and 16 .. 31 of the
+// lane's staged row (its rotation by 16 tokens folded in).
+template <int N>
+__device__ __forceinline__ v4f value_quad(const float* lo, const float* hi, const float (&p0)[4],
+                                          const float (&p1)[4], v4f acc) {
+  const float4 v = *(const float4*)((N < 4 ? lo : hi) + 4 * (N & 3));
+  const float(&pw)[4] = (N & 1) ? p1 : p0;
+  acc = __builtin_amdgcn_mfma_f32_4x4x1f32(v.x, pw[0], acc, 0, 0, 4 + N / 2);
+  acc = __builtin_amdgcn_mfma_f32_4x4x1f32(v.y, pw[1], acc, 0, 0, 4 + N / 2);
+  acc = __builtin_amdgcn_mfma_f32_4x4x1f32(v.z, pw[2], acc, 0, 0, 4 + N / 2);
+  acc = __builtin_amdgcn_mfma_f32_4x4x1f32(v.w, pw[3], acc, 0, 0, 4 + N / 2);
+  return acc;
+}
+
+template <int D, int KW, int KN, int VW, int VN>
 __global__ __launch_bounds__(kBlockThreads, 4) void attn_mfma_chunk_kernel(AttnArgs a) {
-  constexpr int D = 128;
+  static_assert(D == 64 || D == 128, "d = 64 or 128");
+  constexpr int LPV = AttnWave<D>::LPV;
+  constexpr int VPW = AttnWave<D>::VPW;     // tokens per tile: 16 (d = 128) or 32 (d = 64)
   // the layer's K and V tables (n = 2^KW and 2^VW entries: the host dispatches on n).  A table
   // depends only on n and d, so K and V with the same n share one (at n = 256 the second copy
   // would keep the fourth block of the compute unit out of the LDS).
   constexpr bool kShared = KW == VW;
   __shared__ float2 s_lut_k[1 << KW];
   __shared__ float2 s_lut_v[kShared ? 1 : (1 << VW)];
-  __shared__ __attribute__((aligned(16))) float s_wave[kWavesPerBlock][kStageWords];
+  __shared__ __attribute__((aligned(16))) float s_wave[kWavesPerBlock][kStageWordsOf<D>];
   const SegParams spk = a.segs[2 * a.layer], spv = a.segs[2 * a.layer + 1];
   for (uint32_t e = threadIdx.x; e < (1u << KW); e += kBlockThreads)
     s_lut_k[e] = ((const float2*)a.lut)[spk.lut_off + e];
@@ -485,51 +350,64 @@ __global__ __launch_bounds__(kBlockThreads, 4) void attn_mfma_chunk_kernel(AttnA
   if (!chunk_setup<D>(a, w, wib)) return;
   float* const lds = s_wave[wib];
 
-  // q^ of the pass's heads: computed in the quad layout (vector slot g = head g), read back as
-  // head x on slice c (zero for heads past the pass)
+  // q^ of the pass's heads: computed in the layout of vector slot g = head g, read back as
+  // head x on the lane's slice (zero for heads past the pass)
   {
     AttnWave<D> wq = w;
-    wq.sub = lane % 4;
-    wq.vslot = lane / 4;
+    wq.sub = lane % LPV;
+    wq.vslot = lane / LPV;
     if (a.q_f32) query_transform<D, true>(a, wq, lds);
     else query_transform<D, false>(a, wq, lds);
   }
   wave_lds_sync();
-  // q^ is the same on the four rows, so each row keeps a quarter of it: lane (R, c, x) holds
-  // elements 32c + 8R .. 32c + 8R + 7 of head x, and the product over element n takes its
-  // B operand from row n / 8 (the lane-group broadcast of the matrix instruction, blgp 4 + n / 8)
+  // the code layout: token tok of the tile on slice sl (tile loads and both rebuilds use it)
   const int x = lane & 3, c = (lane >> 2) & 3, R = lane >> 4;
+  const int sl = D == 128 ? c : c >> 1;
+  const int tok = D == 128 ? 4 * R + x : 8 * R + 4 * (c & 1) + x;
+  // q^ is the same on the four rows, so each row keeps a quarter of it: lane (R, c, x) holds
+  // elements 32 sl + 8R .. 32 sl + 8R + 7 of head x, and the product over element n takes its
+  // B operand from row n / 8 (the lane-group broadcast of the matrix instruction, blgp 4 + n / 8)
   float qr[8];
 #pragma unroll
   for (int i = 0; i < 8; i += 4) {
-    const float4 v = (uint32_t)x < w.gc ? *(const float4*)(lds + (x * 4 + c) * kQPitch + 8 * R + i)
-                                        : make_float4(0, 0, 0, 0);
+    const float4 v = (uint32_t)x < w.gc
+                         ? *(const float4*)(lds + (x * LPV + sl) * kQPitch + 8 * R + i)
+                         : make_float4(0, 0, 0, 0);
     qr[i] = v.x, qr[i + 1] = v.y, qr[i + 2] = v.z, qr[i + 3] = v.w;
   }
-  // the code layout: token 4R + x of the tile, slice c (tile loads and both rebuilds use it)
-  w.sub = c;
-  w.vslot = 4 * R + x;
-  const int tok = w.vslot;
-  const float* const lvl_v = lds + 2 * tok + (c & 1);           // level q at + 32 q
-  const float* const lvl_k = lds + kLvlWords + 2 * tok + (c & 1);
-  float* const lvl_v_w = lds + 2 * tok;                         // the two copies of level q
-  float* const lvl_k_w = lds + kLvlWords + 2 * tok;
-  float* const stage_w = lds + 16 * kPairPitch * c + kHalfSkew * (c >> 1) + 2 * tok;   // + pitch i
-  const float* const stage_r = lds + kPairPitch * lane + kHalfSkew * (lane >> 5);
+  w.sub = sl;
+  w.vslot = tok;
+  // level q of the lane's token at + 32 q (d = 128: two copies, read by even and odd columns)
+  const float* const lvl_v = lds + (D == 128 ? 2 * tok + (c & 1) : tok);
+  const float* const lvl_k = lvl_v + kLvlWords;
+  float* const lvl_v_w = lds + (D == 128 ? 2 * tok : tok);
+  float* const lvl_k_w = lvl_v_w + kLvlWords;
+  // staging of y'_V: the lane's pair i at stage_w + kPairPitch i (d = 128) or, at d = 64, at
+  // (i even ? stage_w : stage_w1) + 64 i; the lane's (pair, element) row at stage_r (d = 128),
+  // or its tokens 0 .. 15 at stage_r and 16 .. 31 at stage_r1 (d = 64)
+  float* const stage_w = D == 128 ? lds + 16 * kPairPitch * c + kHalfSkew * (c >> 1) + 2 * tok
+                                  : lds + 1024 * sl + tok;
+  float* const stage_w1 = lds + 1024 * sl + (tok ^ 16);
+  const int skew = 16 * ((lane >> 1) & 1);
+  const float* const stage_r =
+      D == 128 ? lds + kPairPitch * lane + kHalfSkew * (lane >> 5)
+               : lds + 64 * (lane >> 1) + 32 * (lane & 1) + skew;
+  const float* const stage_r1 = lds + 64 * (lane >> 1) + 32 * (lane & 1) + (skew ^ 16);
 
   float m = -INFINITY, lsum = 0.0f;
-  // accumulators of element 0 and 1 of pairs 4b + r (register r), head x
+  // d = 128: accumulators of element 0 and 1 of pairs 4b + r (register r), head x; d = 64:
+  // acc0 alone, element 4b + r
   v4f acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
   constexpr uint32_t kKLevels = (1u << KN) - 1u, kVLevels = (1u << VN) - 1u;
 
-  const uint32_t last = (w.ntok + 15) / 16 - 1;
-  const bool ragged = (w.ntok & 15u) != 0;
-  // log-space V norms: the ladder ratio of each token, computed for four tiles at once (the
-  // four lanes of a token would otherwise compute the same one): lane (token t, column c)
-  // holds that of token t in tile 4k + c, and tile 4k + u reads it from column u
+  const uint32_t last = (w.ntok + VPW - 1) / VPW - 1;
+  const bool ragged = (w.ntok & (VPW - 1)) != 0;
+  // log-space V norms: the ladder ratio of each token, computed for LPV tiles at once (the LPV
+  // lanes of a token would otherwise compute the same one): the lane on slice sl holds that of
+  // its token in tile LPV k + sl, and tile LPV k + u reads it from the lane of slice u
   double vrho = 1.0;
   u32x2 vh = {0u, 0u};
-  if constexpr (VN != 8) vh = v_header<D>(a, w, min((uint32_t)c, last));
+  if constexpr (VN != 8) vh = v_header<D>(a, w, min((uint32_t)sl, last));
   auto tile_work = [&](const TilePair<KW, KN, VW, VN>& cd, uint32_t tile) {
     // ---- scores: y'_K on this lane's slice, 32 matrix products over the slice ----
     v4f sc = {0, 0, 0, 0};
@@ -546,10 +424,13 @@ __global__ __launch_bounds__(kBlockThreads, 4) void attn_mfma_chunk_kernel(AttnA
       } else {
         unpack16_index<KN>(cd.k.nrm, qc);
         wave_lds_sync();                       // the previous tile's reads of these words are done
-        static_assert(KN == 4, "log-space norms here: 16 levels, four per lane");
-        log_level_ladder_each<4, 4>(
-            [lvl_k_w](uint32_t q, float v) { lvl_k_w[32 * q] = v; lvl_k_w[32 * q + 1] = v; },
-            c, rmin, rmax, kKLevels);
+        static_assert(KN == 4, "log-space norms here: 16 levels, 16 / LPV per lane");
+        log_level_ladder_each<LPV, 16 / LPV>(
+            [lvl_k_w](uint32_t q, float v) {
+              lvl_k_w[32 * q] = v;
+              if constexpr (D == 128) lvl_k_w[32 * q + 1] = v;
+            },
+            sl, rmin, rmax, kKLevels);
         wave_lds_sync();
 #pragma unroll
         for (int i = 0; i < kPairsPerLane; ++i) r[i] = lvl_k[32 * qc[i]];
@@ -573,16 +454,22 @@ __global__ __launch_bounds__(kBlockThreads, 4) void attn_mfma_chunk_kernel(AttnA
         wave_lds_sync();                       // the previous tile's staging reads are done
       } else {
         unpack16_index<VN>(cd.v.nrm, qc);
-        if ((tile & 3u) == 0) {
+        if ((tile & (LPV - 1)) == 0) {
           vrho = ladder_rho(__uint_as_float(vh.x), __uint_as_float(vh.y), kVLevels);
-          vh = v_header<D>(a, w, min(tile + 4u + (uint32_t)c, last));   // the next group's
+          vh = v_header<D>(a, w, min(tile + LPV + (uint32_t)sl, last));   // the next group's
         }
-        const double rho = __shfl(vrho, (lane & 0x33) | (int)((tile & 3u) << 2));
+        // the lane of the same token on slice tile % LPV
+        const int src = D == 128 ? (lane & 0x33) | (int)((tile & 3u) << 2)
+                                 : (lane & 0x37) | (int)((tile & 1u) << 3);
+        const double rho = __shfl(vrho, src);
         wave_lds_sync();                       // the previous tile's staging reads are done
-        static_assert(VN == 4, "log-space norms here: 16 levels, four per lane");
-        ladder_levels_each<4, 4>(
-            [lvl_v_w](uint32_t q, float v) { lvl_v_w[32 * q] = v; lvl_v_w[32 * q + 1] = v; },
-            c, rmin, rmax, rho, kVLevels);
+        static_assert(VN == 4, "log-space norms here: 16 levels, 16 / LPV per lane");
+        ladder_levels_each<LPV, 16 / LPV>(
+            [lvl_v_w](uint32_t q, float v) {
+              lvl_v_w[32 * q] = v;
+              if constexpr (D == 128) lvl_v_w[32 * q + 1] = v;
+            },
+            sl, rmin, rmax, rho, kVLevels);
         wave_lds_sync();
 #pragma unroll
         for (int i = 0; i < kPairsPerLane; ++i) r[i] = lvl_v[32 * qc[i]];
@@ -591,25 +478,34 @@ __global__ __launch_bounds__(kBlockThreads, 4) void attn_mfma_chunk_kernel(AttnA
 #pragma unroll
       for (int i = 0; i < kPairsPerLane; ++i) {
         const float2 cs = lut_v[kc[i]];
-        *(float2*)(stage_w + kPairPitch * i) = make_float2(r[i] * cs.x, r[i] * cs.y);
+        if constexpr (D == 128) {
+          *(float2*)(stage_w + kPairPitch * i) = make_float2(r[i] * cs.x, r[i] * cs.y);
+        } else {
+          float* const dst = ((i & 1) ? stage_w1 : stage_w) + 64 * i;
+          dst[0] = r[i] * cs.x;
+          dst[32] = r[i] * cs.y;
+        }
       }
     }
     // ---- softmax step: the slices added across the row's columns, the weights ----
+    // register q: token tok - x + q (4R + q, or 8R + 4 (c % 2) + q at d = 64)
     float sv[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       float v = sc[q];
       v += row_ror<8>(v);
-      v += row_ror<4>(v);
+      if constexpr (D == 128) v += row_ror<4>(v);
       sv[q] = v;
     }
     if (ragged && tile == last) {              // tokens past the chunk weigh 0
 #pragma unroll
-      for (int q = 0; q < 4; ++q) sv[q] = tile * 16 + 4 * R + q < w.ntok ? sv[q] : -INFINITY;
+      for (int q = 0; q < 4; ++q) sv[q] = tile * VPW + (tok - x) + q < w.ntok ? sv[q] : -INFINITY;
     }
     const float smax = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
     if (__builtin_amdgcn_ballot_w64(smax > m + kLazyLog2) != 0) {   // a new reference point
-      float mx = fmaxf(smax, __shfl_xor(smax, 16));
+      float mx = smax;
+      if constexpr (D == 64) mx = fmaxf(mx, __shfl_xor(mx, 4));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       const float mn = fmaxf(m, mx);
       const float f = __builtin_amdgcn_exp2f(m - mn);          // 0 on the first raise
@@ -622,16 +518,40 @@ __global__ __launch_bounds__(kBlockThreads, 4) void attn_mfma_chunk_kernel(AttnA
 #pragma unroll
     for (int q = 0; q < 4; ++q) p[q] = __builtin_amdgcn_exp2f(sv[q] - m);
     lsum += (p[0] + p[1]) + (p[2] + p[3]);
-    // ---- value products: tokens 2n and 2n + 1, both elements, from one 16-byte read ----
-    wave_lds_sync();                           // every lane's staging is written
-    value_pair<0>(stage_r, p, acc0, acc1);
-    value_pair<1>(stage_r, p, acc0, acc1);
-    value_pair<2>(stage_r, p, acc0, acc1);
-    value_pair<3>(stage_r, p, acc0, acc1);
-    value_pair<4>(stage_r, p, acc0, acc1);
-    value_pair<5>(stage_r, p, acc0, acc1);
-    value_pair<6>(stage_r, p, acc0, acc1);
-    value_pair<7>(stage_r, p, acc0, acc1);
+    // ---- value products from 16-byte reads of the staging ----
+    if constexpr (D == 128) {
+      // tokens 2n and 2n + 1, both elements
+      wave_lds_sync();                         // every lane's staging is written
+      value_pair<0>(stage_r, p, acc0, acc1);
+      value_pair<1>(stage_r, p, acc0, acc1);
+      value_pair<2>(stage_r, p, acc0, acc1);
+      value_pair<3>(stage_r, p, acc0, acc1);
+      value_pair<4>(stage_r, p, acc0, acc1);
+      value_pair<5>(stage_r, p, acc0, acc1);
+      value_pair<6>(stage_r, p, acc0, acc1);
+      value_pair<7>(stage_r, p, acc0, acc1);
+    } else {
+      // P_h: the weights of tokens 8R + 4h + k in every column, from the lane's own column
+      // (c % 2 == h) or the one beside it (a row rotation by one column; bank_mask picks the
+      // columns that take it)
+      float p0[4], p1[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int pk = __float_as_int(p[k]);
+        p0[k] = __int_as_float(__builtin_amdgcn_update_dpp(pk, pk, 0x124, 0xF, 0xA, false));
+        p1[k] = __int_as_float(__builtin_amdgcn_update_dpp(pk, pk, 0x124, 0xF, 0x5, false));
+      }
+      // tokens 4n .. 4n + 3
+      wave_lds_sync();                         // every lane's staging is written
+      acc0 = value_quad<0>(stage_r, stage_r1, p0, p1, acc0);
+      acc0 = value_quad<1>(stage_r, stage_r1, p0, p1, acc0);
+      acc0 = value_quad<2>(stage_r, stage_r1, p0, p1, acc0);
+      acc0 = value_quad<3>(stage_r, stage_r1, p0, p1, acc0);
+      acc0 = value_quad<4>(stage_r, stage_r1, p0, p1, acc0);
+      acc0 = value_quad<5>(stage_r, stage_r1, p0, p1, acc0);
+      acc0 = value_quad<6>(stage_r, stage_r1, p0, p1, acc0);
+      acc0 = value_quad<7>(stage_r, stage_r1, p0, p1, acc0);
+    }
   };
 
   // tiles two at a time from two code buffers: each tile's codes load while the one before
@@ -645,15 +565,22 @@ __global__ __launch_bounds__(kBlockThreads, 4) void attn_mfma_chunk_kernel(AttnA
     if (t1 != t) tile_work(cb, t1);
   }
 
-  // l of head x: the rows hold different tokens (the columns of a row the same sums); lane
-  // 4b + j stores elements 8b .. 8b + 7 of head j
+  // l of head x: the rows hold different tokens, and so do the columns c and c + 1 at d = 64
+  // (the other columns of a row hold the same sums); lane 4b + j stores elements 8b .. 8b + 7
+  // (d = 128) or 4b .. 4b + 3 (d = 64) of head j
+  if constexpr (D == 64) lsum += __shfl_xor(lsum, 4);
   lsum += __shfl_xor(lsum, 16);
   lsum += __shfl_xor(lsum, 32);
   if ((uint32_t)x < w.gc) {
     const uint64_t idx = ((uint64_t)w.b * a.Hq + w.h * a.G + w.g0 + x) * a.n_chunks + w.chunk;
-    float* dst = a.ws_acc + idx * D + 8 * (lane >> 2);
-    *(float4*)dst = make_float4(acc0[0], acc1[0], acc0[1], acc1[1]);
-    *(float4*)(dst + 4) = make_float4(acc0[2], acc1[2], acc0[3], acc1[3]);
+    if constexpr (D == 128) {
+      float* dst = a.ws_acc + idx * D + 8 * (lane >> 2);
+      *(float4*)dst = make_float4(acc0[0], acc1[0], acc0[1], acc1[1]);
+      *(float4*)(dst + 4) = make_float4(acc0[2], acc1[2], acc0[3], acc1[3]);
+    } else {
+      *(float4*)(a.ws_acc + idx * D + 4 * (lane >> 2)) =
+          make_float4(acc0[0], acc0[1], acc0[2], acc0[3]);
+    }
     if (lane < 4) *(float2*)(a.ws_ml + idx * 2) = make_float2(m, lsum);
   }
 }
@@ -759,10 +686,8 @@ __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
 
 template <int D, int KW, int KN, int VW, int VN>
 void launch_chunk(const AttnArgs& a, dim3 grid, hipStream_t s) {
-  if constexpr (D == 128)
-    hipLaunchKernelGGL((attn_mfma_chunk_kernel<KW, KN, VW, VN>), grid, dim3(kBlockThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL((attn_chunk_kernel<D, KW, KN, VW, VN>), grid, dim3(kBlockThreads), 0, s, a);
+  hipLaunchKernelGGL((attn_mfma_chunk_kernel<D, KW, KN, VW, VN>), grid, dim3(kBlockThreads), 0, s,
+                     a);
 }
 
 // format index: bit 0 = 8-bit angle codes (n = 256), bit 1 = 4-bit log norms
@@ -783,17 +708,10 @@ template <int D, int KF>
 int chunk_blocks_v(int vf) {
   constexpr int KW = (KF & 1) ? 8 : 6, KN = (KF & 2) ? 4 : 8;
   const void* f[4];
-  if constexpr (D == 128) {
-    f[0] = (const void*)attn_mfma_chunk_kernel<KW, KN, 6, 8>;
-    f[1] = (const void*)attn_mfma_chunk_kernel<KW, KN, 8, 8>;
-    f[2] = (const void*)attn_mfma_chunk_kernel<KW, KN, 6, 4>;
-    f[3] = (const void*)attn_mfma_chunk_kernel<KW, KN, 8, 4>;
-  } else {
-    f[0] = (const void*)attn_chunk_kernel<D, KW, KN, 6, 8>;
-    f[1] = (const void*)attn_chunk_kernel<D, KW, KN, 8, 8>;
-    f[2] = (const void*)attn_chunk_kernel<D, KW, KN, 6, 4>;
-    f[3] = (const void*)attn_chunk_kernel<D, KW, KN, 8, 4>;
-  }
+  f[0] = (const void*)attn_mfma_chunk_kernel<D, KW, KN, 6, 8>;
+  f[1] = (const void*)attn_mfma_chunk_kernel<D, KW, KN, 8, 8>;
+  f[2] = (const void*)attn_mfma_chunk_kernel<D, KW, KN, 6, 4>;
+  f[3] = (const void*)attn_mfma_chunk_kernel<D, KW, KN, 8, 4>;
   int nb = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, f[vf & 3], kBlockThreads, 0) != hipSuccess)
     return 0;

@@ -113,8 +113,8 @@ __device__ __forceinline__ float linear_step255(float rmin, float rmax) {
 // R'min exactly and RN32 brings the top level back to R'max.  Vectors with R'min == R'max get
 // Rmin at every level.  ladder_rho gives rho (1 for those vectors); ladder_levels_each hands
 // the levels q = sub, sub + LPV, ... of one of the vector's LPV lanes to store(q, level);
-// log_level_ladder_each does both, log_level_ladder stores into tab[q].  The caller orders
-// the LDS writes against other lanes' reads.
+// log_level_ladder_each does both.  The caller orders the LDS writes against other lanes'
+// reads.
 __device__ __forceinline__ double ladder_rho(float rmin, float rmax, uint32_t qlevels) {
   const float lo_c = fmaxf(rmin, FLT_MIN), hi_c = fmaxf(rmax, FLT_MIN);
   return lo_c == hi_c ? 1.0 : ladder_ratio(lo_c, hi_c, qlevels);
@@ -150,12 +150,6 @@ template <int LPV, int COUNT = 0, class Store>
 __device__ __forceinline__ void log_level_ladder_each(Store&& store, int sub, float rmin,
                                                       float rmax, uint32_t qlevels) {
   ladder_levels_each<LPV, COUNT>(store, sub, rmin, rmax, ladder_rho(rmin, rmax, qlevels), qlevels);
-}
-template <int LPV>
-__device__ __forceinline__ void log_level_ladder(float* tab, int sub, float rmin, float rmax,
-                                                 uint32_t qlevels) {
-  log_level_ladder_each<LPV>([tab](uint32_t q, float v) { tab[q] = v; }, sub, rmin, rmax,
-                             qlevels);
 }
 
 // Raw code words of one vector's lane for n = 64/256 angle codes (WA = 6/8 bits) and NB = 8

@@ -711,12 +711,15 @@ def _attention_check(s, lay, cache, q, layer, t_end, scale, name, q_dtype=None, 
     (128, 2, 250, "n256-lin"),
     (64, 2, 700, "k256-v64"),
     (64, 3, 200, "n256-k4log-v8lin"),
+    (64, 4, 600, "n64-k8lin-v4log"),
+    (64, 6, 333, "k64log-v256log"),
+    (64, 1, 1100, "n256-lin"),
 ])
 def test_attention_matches_oracle(gpu, d, G, T, fmt):
     """Attention of one query token over the compressed cache (query heads grouped over the
     KV heads), from the codes, against the oracle's fp64 attention over the decoded cache:
     several chunks with a ragged last one, one token, and a short range.  The formats cover
-    every table of the d = 128 kernel (log-space levels of K and of V, n = 64 and 256) and G
+    every table of the kernel at both d (log-space levels of K and of V, n = 64 and 256) and G
     covers whole, partial (G = 6: two passes of 3 heads) and single-head passes."""
     tables = {
         "n64-k8lin-v4log": [LayerCfg(64, 64), LayerCfg(64, 64)],
