@@ -43,6 +43,7 @@ constexpr float kLazyLog2 = 8.0f;    // weights 2^(s - m) stay below 2^8 between
 // 16-byte reads of a wave (one per lane of a vector, broadcast over the vector slots) fall in
 // distinct banks
 constexpr int kQPitch = kElemsPerLane + 4;
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
@@ -57,14 +58,6 @@ __device__ __forceinline__ uint32_t row_ror(uint32_t v) {
 template <int N>
 __device__ __forceinline__ float row_ror(float v) {
   return __uint_as_float(row_ror<N>(__float_as_uint(v)));
-}
-
-// Sum over the wave's vector slots (lanes sub, sub + LPV, ...): every lane gets its sub's sum.
-template <int LPV>
-__device__ __forceinline__ float slot_sum(float v) {
-#pragma unroll
-  for (int o = LPV; o < kWave; o <<= 1) v += __shfl_xor(v, o);
-  return v;
 }
 
 template <int D>
@@ -585,102 +578,96 @@ __global__ __launch_bounds__(kBlockThreads, 4) void attn_mfma_chunk_kernel(AttnA
   }
 }
 
-// One output per wave: vector slot k merges chunks k, k + VPW, ..., the slots are summed, and
-// o = D W (A / L).
+// One output per wave, its elements across the lanes: lane l keeps elements EPL l .. EPL l +
+// EPL - 1 (EPL = d / 64) of A = sum_c acc_c 2^(m_c - M), so the chunks' partials are read as
+// contiguous rows and summed without any exchange between lanes.  The chunks' (m_c, l_c) are
+// read 64 at a time, one per lane: M = max m_c, then the weights 2^(m_c - M), L, and each
+// chunk's weight taken from its lane by a scalar read.  o = D W (A / L): the butterfly's
+// stages over element bits that lie across lanes are exchanges with the partner lane.
 template <int D, bool F32OUT>
 __global__ __launch_bounds__(kBlockThreads) void attn_merge_kernel(AttnArgs a) {
-  constexpr int LPV = D / kElemsPerLane;
-  constexpr int VPW = kWave / LPV;
+  constexpr int EPL = D / kWave;                      // elements per lane: 1 or 2
   const int lane = threadIdx.x & (kWave - 1);
-  const int sub = lane % LPV;
-  const uint32_t vslot = (uint32_t)(lane / LPV);
   const uint32_t j = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerBlock +
                                                      threadIdx.x / kWave);
   if (j >= a.B * a.Hq) return;
-  // The layer's sign masks are loaded first, to arrive under the chunk reads.
-  uint32_t sm[16];
-  load_words<16>(a.sign_masks + (size_t)a.layer * (D / 2) + sub * 16, sm);
-  // Chunks are taken kMergeBatch at a time per slot with every load of a batch issued before
-  // its first use, so a slot waits for one memory latency per batch rather than per chunk.
-  // Each slot keeps its own reference point Ms (raised batch by batch, the slot's sums
-  // rescaled), and the slots are brought to the wave's M before they are added.
-  constexpr uint32_t kMergeBatch = 4;
-  const float2* ml = (const float2*)(a.ws_ml + (size_t)j * a.n_chunks * 2);
-  float Ms = -INFINITY, L = 0.0f;
-  float x[kElemsPerLane];
+  const uint32_t nc = a.n_chunks;
+  const float2* const ml = (const float2*)(a.ws_ml + (size_t)j * nc * 2);
+  const float* const acc = a.ws_acc + (size_t)j * nc * D + EPL * lane;
+  // the sign bits of the lane's elements: word e / 2 of the layer's masks, bit 15 or 31
+  const uint32_t smw = a.sign_masks[(size_t)a.layer * (D / 2) + (EPL * lane) / 2];
+  // M over every chunk (an empty chunk carries m = -inf)
+  float M = -INFINITY;
+  for (uint32_t c = (uint32_t)lane; c < nc; c += kWave) M = fmaxf(M, ml[c].x);
+  M = wave_max(M);
+  float L = 0.0f;
+  float x[EPL];
 #pragma unroll
-  for (int i = 0; i < kElemsPerLane; ++i) x[i] = 0.0f;
-  const float* acc = a.ws_acc + (size_t)j * a.n_chunks * D + sub * kElemsPerLane;
-  for (uint32_t c0 = vslot; c0 < a.n_chunks; c0 += kMergeBatch * VPW) {
-    float2 mlb[kMergeBatch];
-    float4 vb[kMergeBatch][kElemsPerLane / 4];
+  for (int e = 0; e < EPL; ++e) x[e] = 0.0f;
+  if (M != -INFINITY) {
+    for (uint32_t c0 = 0; c0 < nc; c0 += kWave) {
+      const uint32_t c = c0 + (uint32_t)lane;
+      const float2 v = c < nc ? ml[c] : make_float2(-INFINITY, 0.0f);
+      const float wc = v.x == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(v.x - M);
+      L = __builtin_fmaf(v.y, wc, L);
+      const uint32_t n = min(nc - c0, (uint32_t)kWave);
+      // eight chunks' rows requested before any is used
+      for (uint32_t k0 = 0; k0 < n; k0 += 8) {
+        float r[8][EPL];
 #pragma unroll
-    for (uint32_t k = 0; k < kMergeBatch; ++k) {
-      const uint32_t c = min(c0 + k * VPW, a.n_chunks - 1);     // in bounds; weight 0 below
-      mlb[k] = ml[c];
+        for (uint32_t k = 0; k < 8; ++k) {
+          const uint32_t kk = min(k0 + k, n - 1);            // in bounds; weight 0 below
+          const float* src = acc + (size_t)(c0 + kk) * D;
+          if constexpr (EPL == 2) {
+            const float2 t = *(const float2*)src;
+            r[k][0] = t.x, r[k][1] = t.y;
+          } else {
+            r[k][0] = *src;
+          }
+        }
 #pragma unroll
-      for (int i = 0; i < kElemsPerLane / 4; ++i)
-        vb[k][i] = *(const float4*)(acc + (size_t)c * D + 4 * i);
-    }
-    // empty chunks carry m = -inf and weight 0, and so does a batch entry past the last chunk
-    float mk[kMergeBatch];
-    float bm = Ms;
+        for (uint32_t k = 0; k < 8; ++k) {
+          // chunk c0 + k0 + k's weight, from its lane (a wave-uniform index below 64)
+          const int wk = __builtin_amdgcn_readlane(__float_as_int(wc), (int)min(k0 + k, 63u));
+          const float wf = k0 + k < n ? __int_as_float(wk) : 0.0f;
 #pragma unroll
-    for (uint32_t k = 0; k < kMergeBatch; ++k) {
-      mk[k] = c0 + k * VPW < a.n_chunks ? mlb[k].x : -INFINITY;
-      bm = fmaxf(bm, mk[k]);
-    }
-    if (bm != -INFINITY) {
-      const float sc = __builtin_amdgcn_exp2f(Ms - bm);      // 0 while Ms is -inf
-      L *= sc;
-#pragma unroll
-      for (int i = 0; i < kElemsPerLane; ++i) x[i] *= sc;
-      Ms = bm;
-    }
-#pragma unroll
-    for (uint32_t k = 0; k < kMergeBatch; ++k) {
-      const float f = mk[k] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mk[k] - Ms);
-      L = __builtin_fmaf(mlb[k].y, f, L);
-#pragma unroll
-      for (int i = 0; i < kElemsPerLane / 4; ++i) {
-        x[4 * i] = __builtin_fmaf(vb[k][i].x, f, x[4 * i]);
-        x[4 * i + 1] = __builtin_fmaf(vb[k][i].y, f, x[4 * i + 1]);
-        x[4 * i + 2] = __builtin_fmaf(vb[k][i].z, f, x[4 * i + 2]);
-        x[4 * i + 3] = __builtin_fmaf(vb[k][i].w, f, x[4 * i + 3]);
+          for (int e = 0; e < EPL; ++e) x[e] = __builtin_fmaf(r[k][e], wf, x[e]);
+        }
       }
     }
   }
-  // with no token at all M is -inf and every slot contributes 0
-  const float M = wave_max(Ms);
-  const float g = Ms == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(Ms - M);
-  L *= g;
+  // L over the lanes; no token at all (M = -inf) gives zeros
 #pragma unroll
-  for (int i = 0; i < kElemsPerLane; ++i) x[i] *= g;
-  L = slot_sum<LPV>(L);
+  for (int o = 32; o >= 1; o >>= 1) L += __shfl_xor(L, o);
+  const float inv = M == -INFINITY ? 0.0f : 1.0f / L;
 #pragma unroll
-  for (int i = 0; i < kElemsPerLane; ++i) x[i] = slot_sum<LPV>(x[i]);
-  const float inv = M == -INFINITY ? 0.0f : 1.0f / L;   // no token attended: zeros
+  for (int e = 0; e < EPL; ++e) x[e] *= inv;
+  // W: the stage over element bit 0 inside the lane at d = 128, then the stages over the
+  // lane's bits: the lane with the bit clear keeps a + b, its partner a - b
+  if constexpr (EPL == 2) {
+    const float p = x[0], q = x[1];
+    x[0] = p + q;
+    x[1] = p - q;
+  }
 #pragma unroll
-  for (int i = 0; i < kElemsPerLane; ++i) x[i] *= inv;
-  fwht_in_lane(x);
-  fwht_cross_lane_signed<LPV>(x, sub);            // sigma * W A / L
-  const uint32_t neg = lane_negated<LPV>(sub) ? 0x80008000u : 0u;
-  if (vslot != 0) return;
-  const uint64_t elem = (uint64_t)j * D + sub * kElemsPerLane;
-  if constexpr (F32OUT) {
-    uint32_t o[32];
+  for (int b = 1; b < kWave; b <<= 1) {
+    const float sgn = (lane & b) ? -1.0f : 1.0f;
 #pragma unroll
-    for (int m = 0; m < 16; ++m) {
-      const uint32_t s = sm[m] ^ neg;
-      o[2 * m] = __float_as_uint(x[2 * m]) ^ (s << 16);
-      o[2 * m + 1] = __float_as_uint(x[2 * m + 1]) ^ (s & 0x80000000u);
-    }
-    store_words<32>((uint32_t*)a.o + elem, o);
+    for (int e = 0; e < EPL; ++e) x[e] = __builtin_fmaf(x[e], sgn, __shfl_xor(x[e], b));
+  }
+  // D, then the store
+  const uint64_t elem = (uint64_t)j * D + EPL * lane;
+  if constexpr (EPL == 2) {
+    const uint32_t lo = (smw << 16) & 0x80000000u, hi = smw & 0x80000000u;
+    const float o0 = __uint_as_float(__float_as_uint(x[0]) ^ lo);
+    const float o1 = __uint_as_float(__float_as_uint(x[1]) ^ hi);
+    if constexpr (F32OUT) *(float2*)((float*)a.o + elem) = make_float2(o0, o1);
+    else *(uint32_t*)((uint16_t*)a.o + elem) = bf16x2_rne(o0, o1);
   } else {
-    uint32_t o[16];
-#pragma unroll
-    for (int m = 0; m < 16; ++m) o[m] = bf16x2_rne(x[2 * m], x[2 * m + 1]) ^ sm[m] ^ neg;
-    store_words<16>((uint32_t*)((uint16_t*)a.o + elem), o);
+    const uint32_t sb = (lane & 1) ? (smw & 0x80000000u) : ((smw << 16) & 0x80000000u);
+    const float o0 = __uint_as_float(__float_as_uint(x[0]) ^ sb);
+    if constexpr (F32OUT) ((float*)a.o)[elem] = o0;
+    else ((uint16_t*)a.o)[elem] = (uint16_t)(bf16x2_rne(o0, 0.0f) & 0xFFFFu);
   }
 }
 
