@@ -768,20 +768,23 @@ def test_attention_api_errors(gpu):
         s.gpu.attention(cache, lay, 0, 40, qd, out, 0.1, workspace=small)
 
 
-def test_long_context_attention_full_size_sampled(gpu):
-    """Attention at the long-context benchmark's shape and launch plan: 16 sequences x 32768
-    cached tokens + 1 appended, 32 layers x 8 KV heads, 32 query heads, d = 128, layers 0-3 at
-    n = 256.  Contiguous cache and paged pool (256-slot blocks, shuffled tables) encoded from the
-    same draw; attention of a boosted and a base layer.  The paged outputs equal the contiguous
-    ones bit for bit (same chunk plan, same codes); sampled (sequence, KV head) rows are checked
-    against the oracle's fp64 attention over that row's records (gathered on the GPU), under
-    parity.attention_error_bar.  Needs ~140 GB of device memory."""
+@pytest.mark.parametrize("wl,need_gb", [("C5", 140), ("C4", 8)])
+def test_long_context_attention_full_size_sampled(gpu, wl, need_gb):
+    """Attention at the benchmark's attention shapes and launch plans: C5, 16 sequences x 32768
+    cached tokens + 1 appended, 32 layers x 8 KV heads, d = 128, layers 0-3 at n = 256; C4,
+    8 sequences x 8192 + 1 tokens, 16 layers x 8 KV heads, d = 64, keys of layers 0-3 at
+    n = 256; 32 query heads.  Contiguous cache and paged pool (256-slot blocks, shuffled tables)
+    encoded from the same draw; attention of a boosted and a base layer.  The paged outputs
+    equal the contiguous ones bit for bit (same chunk plan, same codes); sampled (sequence, KV
+    head) rows are checked against the oracle's fp64 attention over that row's records
+    (gathered on the GPU), under parity.attention_error_bar.  C5 needs ~140 GB of device
+    memory."""
     import types
     import torch
-    w = workloads.get("C5")
+    w = workloads.get(wl)
     free, _ = torch.cuda.mem_get_info()
-    if free < 140e9:
-        pytest.skip(f"needs ~140 GB of free device memory, {free / 1e9:.0f} GB free")
+    if free < need_gb * 1e9:
+        pytest.skip(f"needs ~{need_gb} GB of free device memory, {free / 1e9:.0f} GB free")
     s = setup_from_workload(w)
     cap = w.T + 1
     G, P_blk = 4, 256
@@ -852,6 +855,7 @@ def test_long_context_attention_full_size_sampled(gpu):
                                       0, cap, qr, scale, ref, True)
             err = np.linalg.norm(got[b:b + 1, h * G:(h + 1) * G] - ref, axis=-1)
             worst = max(worst, float((err / bar).max()))
-            _say(f"[attn-full layer={layer} b={b} h={h}] max |err|/bar = {(err / bar).max():.3f}")
+            _say(f"[attn-full {wl} layer={layer} b={b} h={h}] max |err|/bar = "
+                 f"{(err / bar).max():.3f}")
             assert np.isfinite(got[b]).all() and (err <= bar).all()
-    _say(f"[attn-full] paged == contiguous bit for bit; worst |err|/bar {worst:.3f}")
+    _say(f"[attn-full {wl}] paged == contiguous bit for bit; worst |err|/bar {worst:.3f}")
