@@ -38,10 +38,11 @@ def _case(d, B, H, T, seed):
     return s, lay, cache
 
 
-def test_noalloc_attention_matches_the_workspace_entry_point(gpu):
+@pytest.mark.parametrize("d", [128, 64])
+def test_noalloc_attention_matches_the_workspace_entry_point(gpu, d):
     import torch
     import paper_2603_27467_amd as tvq
-    d, H, G = 128, 2, 4
+    H, G = 2, 4
     s, lay, cache = _case(d, 3, H, 1500, seed=31)
     rng = np.random.default_rng(32)
     host = torch_to_np(cache)
@@ -63,7 +64,7 @@ def test_noalloc_attention_matches_the_workspace_entry_point(gpu):
         bar = attention_error_bar(s, host, 3, lay.capacity_tokens, layer, t_end, q64, scale,
                                   want, o_dtype == torch.float32)
         err = np.linalg.norm(got.float().cpu().numpy().astype(np.float64) - want, axis=-1)
-        _say(f"[noalloc layer={layer} t_end={t_end} {o_dtype}] partials {need} bytes of "
+        _say(f"[noalloc d={d} layer={layer} t_end={t_end} {o_dtype}] partials {need} bytes of "
              f"{tvq.TVQ_ATTENTION_SCRATCH_BYTES}; identical to the workspace call: {same}; "
              f"max |err|/bar vs oracle {(err / bar).max():.3f}")
         assert same
