@@ -734,6 +734,32 @@ def test_attention_matches_oracle(gpu, d, G, T, fmt):
         _attention_check(s, lay, cache, q, 1, t_end, scale, f"attn d={d} G={G} {fmt}")
 
 
+def test_attention_random_formats_and_shapes(gpu):
+    """Seeded random cases at both d: the layer's K and V formats (n = 64 or 256, 8-bit linear
+    or 4-bit log-space norms, independently), G from 1 to 16 (one to four passes), T and t_end
+    from 1 to 900 tokens, the query and output dtypes and the scale; each against the oracle's
+    fp64 attention within parity.attention_error_bar."""
+    import torch
+    rng = np.random.default_rng(2024)
+    norm = [(8, NORM_LINEAR), (4, NORM_LOG)]
+    for case in range(16):
+        d = (64, 128)[case % 2]
+        G = int(rng.choice([1, 2, 3, 4, 5, 7, 8, 9, 12, 16]))
+        T = int(rng.integers(1, 901))
+        t_end = int(rng.integers(1, T + 1))
+        nk, nv = int(rng.choice([64, 256])), int(rng.choice([64, 256]))
+        (bk, mk), (bv, mv) = norm[int(rng.integers(0, 2))], norm[int(rng.integers(0, 2))]
+        table = [LayerCfg(64, 64), LayerCfg(nk, nv, bk, bv, mk, mv)]
+        q_dtype = (torch.float32, torch.bfloat16)[int(rng.integers(0, 2))]
+        o_dtype = (torch.float32, torch.bfloat16)[int(rng.integers(0, 2))]
+        scale = float(rng.choice([1.0 / np.sqrt(d), 0.05, 2.0]))
+        s, lay, cache, q = _attention_case(d, G, T, table, seed=100 + case,
+                                           q_bf16=q_dtype == torch.bfloat16)
+        name = (f"attn random {case}: d={d} G={G} T={T} K n={nk} {bk}b V n={nv} {bv}b "
+                f"q {q_dtype} o {o_dtype} scale {scale:.3g}")
+        _attention_check(s, lay, cache, q, 1, t_end, scale, name, q_dtype, o_dtype)
+
+
 def test_attention_dtypes_and_layers(gpu):
     """bf16 queries and outputs, both layers, a large scale (peaked weights)."""
     import torch
