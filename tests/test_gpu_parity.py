@@ -130,6 +130,38 @@ def test_odd_widths_and_norm_modes(gpu, d):
     _roundtrip(s, k, v, 1, 33, 40, 3, f"odd-widths-d{d}")
 
 
+def test_codec_random_formats_and_shapes(gpu):
+    """Seeded random cases at both d: 1-3 layers whose K and V formats are drawn independently
+    (n from 2 to 4096, powers of two or not; fp32, linear or log-space norms of 1-16 bits),
+    with or without group packing, bf16 or fp32 input, 1-3 sequences x 1-4 heads x 1-300
+    tokens written at a random slot of a larger cache; encode and decode against the oracle."""
+    rng = np.random.default_rng(77)
+    ns = [2, 3, 5, 8, 17, 32, 48, 64, 100, 128, 200, 256, 300, 1000, 4095, 4096]
+    w = workloads.get("C2")
+    for case in range(12):
+        d = (64, 128)[case % 2]
+        L = int(rng.integers(1, 4))
+        B, H = int(rng.integers(1, 4)), int(rng.integers(1, 5))
+        T = int(rng.integers(1, 301))
+        t_begin = int(rng.integers(0, 50))
+        T_cap = T + t_begin + int(rng.integers(0, 20))
+        table = []
+        for _ in range(L):
+            modes = [(NORM_F32, 32)] + [(m, int(rng.integers(1, 17))) for m in (NORM_LINEAR,
+                                                                             NORM_LOG)]
+            (mk, bk), (mv, bv) = (modes[int(rng.integers(0, 3))] for _ in range(2))
+            table.append(LayerCfg(int(rng.choice(ns)), int(rng.choice(ns)), bk, bv, mk, mv))
+        packing = int(rng.integers(0, 2))
+        dtype = ("bf16", "f32")[int(rng.integers(0, 2))]
+        s = Setup(L, H, d, table, workloads.sign_table(200 + case, L, d), packing=packing).build()
+        k, v = _draw(w, L, B, H, T, d, dtype, 300 + case)
+        name = (f"codec random {case}: d={d} L={L} B={B} H={H} T={T} at {t_begin} of {T_cap} "
+                f"{dtype} packing={packing} " +
+                " ".join(f"({c.n_k},{c.n_v},{c.norm_bits_k},{c.norm_bits_v},{c.norm_mode_k},"
+                         f"{c.norm_mode_v})" for c in table))
+        _roundtrip(s, k, v, B, T, T_cap, t_begin, name)
+
+
 @pytest.mark.parametrize("d", [64, 128])
 def test_group_packing(gpu, d):
     """Group packing of non-power-of-two codebooks: n = 48 and 56 (8 codes per group in 45
