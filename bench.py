@@ -178,6 +178,70 @@ def cpu_baseline(w: workloads.Workload, budget_s: float = 15.0) -> dict:
                       f"second)"}
 
 
+def cpu_baseline_attention(w: workloads.Workload, budget_s: float = 15.0,
+                           tokens: int = 2048) -> dict:
+    """The oracle's attention (plain C, fp64, untuned) on a bounded sample of the same cache:
+    single (sequence, KV head) rows of `tokens` cached tokens, layers taken in turn, each
+    encoded by the oracle beforehand (not timed), then attention of ATTN_GROUP query heads over
+    the row, sharded over all host cores by a thread pool (ctypes releases the GIL).  The unit
+    is the attention line's: bf16-equivalent K and V bytes consumed per second."""
+    import oracle
+    from concurrent.futures import ThreadPoolExecutor
+
+    cores = os.cpu_count() or 1
+    signs = workloads.sign_table(w.sign_seed, w.L, w.d)
+    T = min(tokens, w.T)
+    scale = 1.0 / float(np.sqrt(w.d))
+    rng = np.random.default_rng(w.data_seed + 11)
+
+    def prepare(l: int):
+        t = w.table[l]
+        kinds = [oracle.Kind(t.n_k, t.norm_mode_k, t.norm_bits_k),
+                 oracle.Kind(t.n_v, t.norm_mode_v, t.norm_bits_v)]
+        c = oracle.Codec(1, 1, w.d, kinds, signs[l:l + 1])
+        k = workloads.generate(w, "K", layers=range(l, l + 1), tokens=range(0, T))
+        v = workloads.generate(w, "V", layers=range(l, l + 1), tokens=range(0, T))
+        total, _ = c.layout(1, T)
+        cache = np.zeros(total, np.uint8)
+        b, h = l % w.B, (l // w.B) % w.H
+        c.encode_cache(np.ascontiguousarray(k[:, b:b + 1, h:h + 1]),
+                       np.ascontiguousarray(v[:, b:b + 1, h:h + 1]), 0, T, cache,
+                       want_coords=False)
+        q = rng.standard_normal((1, ATTN_GROUP, w.d))
+        return c, cache, q
+
+    def run(job):
+        c, cache, q = job
+        c.attention_decode(cache, 1, T, 0, T, q, scale)
+        return T
+
+    oracle.lib()
+    layers = [l % w.L for l in range(max(cores, 8))]
+    with ThreadPoolExecutor(max_workers=cores) as ex:
+        jobs = list(ex.map(prepare, layers))
+    toks, passes = 0, 0
+    s = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=cores) as ex:
+        while time.perf_counter() - s < budget_s:
+            toks += sum(ex.map(run, jobs))
+            passes += 1
+    wall = time.perf_counter() - s
+    toks1 = 0
+    s1 = time.perf_counter()
+    while time.perf_counter() - s1 < budget_s / 5:
+        for job in jobs:
+            toks1 += run(job)
+    wall1 = time.perf_counter() - s1
+    per_tok = 2 * w.d * 2                     # bf16 K and V of one token of one KV head
+    return {"value": round(toks * per_tok / wall / 1e9, 4), "unit": "GB/s", "cores": cores,
+            "value_1core": round(toks1 * per_tok / wall1 / 1e9, 4), "kind": "oracle",
+            "sample": f"{len(jobs)} (sequence, KV head) rows of {T} cached tokens, one layer "
+                      f"each (layers in turn), {ATTN_GROUP} query heads, fp64 attention over "
+                      f"the codes, {passes} passes: {toks} tokens in {wall:.1f} s on {cores} "
+                      f"threads; value_1core: {toks1} tokens in {wall1:.1f} s on one thread; "
+                      f"same unit as value (bf16-equivalent K and V bytes consumed per second)"}
+
+
 def _csv(path):
     import csv
     with open(path) as f:
@@ -824,7 +888,8 @@ def main() -> int:
         out = run_longctx(w, args)
         if not args.no_cpu_baseline:
             print("# cpu baseline (oracle on host cores)", file=sys.stderr, flush=True)
-            out["cpu_baseline"] = cpu_baseline(w)
+            out["cpu_baseline"] = (cpu_baseline_attention(w) if args.attention
+                                   else cpu_baseline(w))
         print(json.dumps(out), flush=True)
         return 0
     ab = algorithmic_bytes(w)
