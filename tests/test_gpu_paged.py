@@ -39,21 +39,28 @@ def _draw(L, B, H, T, d, seed):
 
 
 class PagedCase:
-    """3 sequences over a pool of 14 blocks of 32 slots, max 5 blocks per sequence.
+    """By default 3 sequences over a pool of 14 blocks of 32 slots, max 5 blocks per sequence.
     Sequence 0 holds 5 blocks, sequence 1 holds 4 (its last entry -1), sequence 2 holds 3 (then
-    -1 and 99, which is past the pool); two pool blocks belong to no sequence."""
+    -1 and 99, which is past the pool); two pool blocks belong to no sequence.  `shape` =
+    (B, max_blocks, n_blocks, block tokens, table) replaces that layout (table entries -1 or
+    past the pool name no block)."""
 
-    def __init__(self, d, table, seed):
+    def __init__(self, d, table, seed, shape=None):
         import torch
         self.L, self.H, self.d = len(table), 2, d
         self.s = Setup(self.L, self.H, d, table, workloads.sign_table(seed, self.L, d)).build()
-        self.B, self.max_blocks, self.n_blocks = 3, 5, 14
-        perm = np.random.default_rng(seed).permutation(self.n_blocks)
-        self.table = np.array([perm[0:5], list(perm[5:9]) + [-1], list(perm[9:12]) + [-1, 99]],
-                              np.int32)
-        self.unused = perm[12:]
-        self.cap = self.max_blocks * P
-        self.pool_lay = self.s.gpu.pool_layout(self.n_blocks, P)
+        if shape is None:
+            self.B, self.max_blocks, self.n_blocks, self.P = 3, 5, 14, P
+            perm = np.random.default_rng(seed).permutation(self.n_blocks)
+            self.table = np.array([perm[0:5], list(perm[5:9]) + [-1],
+                                   list(perm[9:12]) + [-1, 99]], np.int32)
+        else:
+            self.B, self.max_blocks, self.n_blocks, self.P, tab = shape
+            self.table = np.asarray(tab, np.int32)
+        named = set(int(x) for x in self.table.ravel() if 0 <= x < self.n_blocks)
+        self.unused = np.array([x for x in range(self.n_blocks) if x not in named], np.int64)
+        self.cap = self.max_blocks * self.P
+        self.pool_lay = self.s.gpu.pool_layout(self.n_blocks, self.P)
         self.pool = torch.full((self.pool_lay.total_bytes,), POISON, dtype=torch.uint8,
                                device="cuda")
         self.table_dev = torch.from_numpy(self.table).cuda()
@@ -64,7 +71,7 @@ class PagedCase:
         self.steps = []          # (b, t_begin, T, u, t) of every oracle encode
 
     def allocated(self, b, pos):
-        blk = self.table[b, pos // P] if pos < self.cap else -1
+        blk = self.table[b, pos // self.P] if 0 <= pos < self.cap else -1
         return 0 <= blk < self.n_blocks
 
     def encode(self, positions, T, seed):
@@ -98,7 +105,7 @@ class PagedCase:
 
     def gathered(self):
         host = torch_to_np(self.pool)
-        return host, [gather_paged(host, self.s, self.n_blocks, P, self.table[b], POISON)
+        return host, [gather_paged(host, self.s, self.n_blocks, self.P, self.table[b], POISON)
                       for b in range(self.B)]
 
 
@@ -125,16 +132,16 @@ def _check_codes(case, name):
                     plane = gath[b][off[l, kind, p]: off[l, kind, p] + case.H * case.cap * rec[p]]
                     plane = plane.reshape(case.H, case.cap, rec[p])
                     assert np.all(plane[:, ~case.written[b]] == POISON)
-    _, offp = case.s.orc.layout(case.n_blocks, P)
+    _, offp = case.s.orc.layout(case.n_blocks, case.P)
     for l in range(case.L):
         for kind in range(2):
             rec = case.s.orc.record_bytes(l, kind)
             for p in range(3):
                 if rec[p] == 0:
                     continue
-                n = case.n_blocks * case.H * P * rec[p]
+                n = case.n_blocks * case.H * case.P * rec[p]
                 plane = host[offp[l, kind, p]: offp[l, kind, p] + n].reshape(
-                    case.n_blocks, case.H, P, rec[p])
+                    case.n_blocks, case.H, case.P, rec[p])
                 assert np.all(plane[case.unused] == POISON)
     return host, gath
 
@@ -222,6 +229,82 @@ def test_paged_attention(gpu, d, G):
                 _say(f"[paged-attn d={d} G={G} layer={layer} max_ctx={max_ctx} seq={b} "
                      f"ctx={n}] max |err|/bar = {(err / bar).max():.3f}")
                 assert np.isfinite(got[b]).all() and (err <= bar).all()
+
+
+def test_paged_random_pools(gpu):
+    """Seeded random pools at both d: block sizes of 32 to 256 slots, 1-4 sequences, tables
+    with blocks shuffled over the pool, trailing entries that name no block (-1 or past the
+    pool) and spare pool blocks; a prefill of random length, then a one-token append at each
+    sequence's own position.  Codes against the oracle on the gathered caches, pool blocks no
+    table names untouched, the paged decode (fp32) of the written positions against the fp64
+    decode, and attention with random per-sequence contexts within the written prefix."""
+    import torch
+    rng = np.random.default_rng(4242)
+    for case_no in range(8):
+        d = (64, 128)[case_no % 2]
+        Pb = int(rng.choice([32, 64, 128, 256]))
+        B = int(rng.integers(1, 5))
+        max_blocks = int(rng.integers(2, 6))
+        held = [int(rng.integers(1, max_blocks + 1)) for _ in range(B)]
+        n_blocks = sum(held) + int(rng.integers(0, 3))
+        perm = rng.permutation(n_blocks)
+        tab, k0 = [], 0
+        for b in range(B):
+            row = list(perm[k0:k0 + held[b]])
+            k0 += held[b]
+            row += [int(rng.choice([-1, n_blocks + 7])) for _ in range(max_blocks - held[b])]
+            tab.append(row)
+        fmt = [LayerCfg(int(rng.choice([64, 256])), int(rng.choice([64, 256])),
+                        *((8, 4, NORM_LINEAR, NORM_LOG) if rng.integers(0, 2)
+                          else (4, 8, NORM_LOG, NORM_LINEAR)))]
+        case = PagedCase(d, fmt, seed=500 + case_no, shape=(B, max_blocks, n_blocks, Pb, tab))
+        T = int(rng.integers(1, max(held) * Pb + 1))
+        case.encode([0] * B, T, seed=600 + case_no)
+        case.encode([min(T, held[b] * Pb) for b in range(B)], 1, seed=700 + case_no)
+        name = f"paged-random {case_no}: d={d} P={Pb} B={B} held={held} pool={n_blocks} T={T}"
+        _, gath = _check_codes(case, name)
+        # decode of the written positions
+        shape = (case.L, B, case.H, case.cap, d)
+        ko = torch.full(shape, float("nan"), dtype=torch.float32, device="cuda")
+        vo = torch.full_like(ko, float("nan"))
+        case.s.gpu.decode_paged(case.pool, case.pool_lay, case.table_dev, 0, case.cap, ko, vo)
+        torch.cuda.synchronize()
+        g = np.stack([torch_to_np(ko), torch_to_np(vo)], axis=1)
+        chk = DecodeCheck()
+        prefix = []
+        for b in range(B):
+            n = int(np.argmin(np.concatenate([case.written[b], [False]])))   # written prefix
+            prefix.append(n)
+            if n > 0:
+                ref64 = case.s.orc.decode_cache(gath[b], 1, case.cap, 0, n, "f64")[:, :, 0]
+                check_decoded(chk, ref64, d, g32=g[:, :, b, :, :n])
+        assert chk.ok(), f"{name}: {chk.line()}"
+        # attention over random contexts inside each written prefix
+        G = int(rng.integers(1, 6))
+        Hq = case.H * G
+        q = (rng.standard_normal((B, Hq, d)) * 2.0).astype(np.float32)
+        lens = [int(rng.integers(0, n + 1)) for n in prefix]
+        ctx = torch.tensor(lens, dtype=torch.int32, device="cuda")
+        out = torch.full((B, Hq, d), float("nan"), dtype=torch.float32, device="cuda")
+        case.s.gpu.attention_paged(case.pool, case.pool_lay, case.table_dev, ctx, case.cap, 0,
+                                   torch.from_numpy(q).cuda(), out, 1.0 / np.sqrt(d))
+        torch.cuda.synchronize()
+        got = out.cpu().numpy().astype(np.float64)
+        worst = 0.0
+        for b in range(B):
+            if lens[b] == 0:
+                assert np.all(got[b] == 0), f"{name}: an empty context gives zeros"
+                continue
+            q64 = q[b:b + 1].astype(np.float64)
+            ref = case.s.orc.attention_decode(gath[b], 1, case.cap, 0, lens[b], q64,
+                                              1.0 / np.sqrt(d))
+            bar = attention_error_bar(case.s, gath[b], 1, case.cap, 0, lens[b], q64,
+                                      1.0 / np.sqrt(d), ref, True)
+            err = np.linalg.norm(got[b:b + 1] - ref, axis=-1)
+            worst = max(worst, float((err / bar).max()))
+            assert np.isfinite(got[b]).all() and (err <= bar).all(), name
+        _say(f"[{name}] decode {chk.line()}; attention G={G} ctx={lens} worst |err|/bar "
+             f"{worst:.3f}")
 
 
 def test_paged_step_graph_replay(gpu):
