@@ -160,7 +160,9 @@ tvq_status tvq_encode_mfma(const tvq_codec* c, const void* k, const void* v,
  * head) into k_out / v_out, described by `out` (out->tokens == t_end - t_begin,
  * out->batch == lay->batch), as `out_dtype` (bf16 rounded to nearest even, or fp32).
  * Launches up to two kernels on `stream` (one for the layers whose formats have a dedicated
- * kernel, one for the rest); an empty range launches nothing. */
+ * kernel, one for the rest), twice over when a range of at least 2^19 vectors per kind has a
+ * token count that is not a multiple of the tile's (16 tokens at d = 128, 32 at d = 64): its
+ * whole tiles first, then the remaining tokens; an empty range launches nothing. */
 tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* lay,
                       int64_t t_begin, int64_t t_end, tvq_dtype out_dtype, void* k_out,
                       void* v_out, const tvq_tensor_desc* out, void* stream);

@@ -670,6 +670,11 @@ tvq_status tvq_encode_paged(const tvq_codec* c, tvq_dtype in_dtype, const void* 
   return encode_launch(c, a, in, in_dtype == TVQ_F32, stream);
 }
 
+// Ranges of at least this many vectors per kind whose token count is not a multiple of the
+// tile's are decoded in two parts (whole tiles, then the rest): below it the extra launch
+// costs more than the whole-tile kernel saves.
+constexpr int64_t kDecodeSplitVectors = 1 << 19;
+
 static tvq_status decode_launch(const tvq_codec* c, tvq::DecodeArgs& a,
                                 const tvq_tensor_desc* out, tvq_dtype out_dtype, void* k_out,
                                 void* v_out, void* stream) {
@@ -727,6 +732,27 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
   a.n_slots = lay->batch * c->H * lay->capacity_tokens;
   a.cap = (uint32_t)lay->capacity_tokens;
   a.t_begin = (uint32_t)t_begin;
+  // A large range whose token count is not a multiple of the tile's vectors is decoded as its
+  // whole tiles per (batch, head) row (the kernel that keeps a tile's position in scalar
+  // registers) and then the remaining tokens of every row, into the same output view.
+  const int64_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
+  const int64_t whole = out->tokens / vpw * vpw;
+  if (whole > 0 && whole != out->tokens && out->batch * c->H * whole >= kDecodeSplitVectors) {
+    tvq_tensor_desc head = *out, tail = *out;
+    head.tokens = whole;
+    tail.tokens = out->tokens - whole;
+    tvq_status st = decode_launch(c, a, &head, out_dtype, k_out, v_out, stream);
+    if (st != TVQ_OK) return st;
+    tvq::DecodeArgs b;
+    std::memset(&b, 0, sizeof(b));
+    b.cache = a.cache;
+    b.n_slots = a.n_slots;
+    b.cap = a.cap;
+    b.t_begin = (uint32_t)(t_begin + whole);
+    const int64_t skip = whole * out->stride_t * eb;   // bytes of the head's tokens in a row
+    return decode_launch(c, b, &tail, out_dtype, (char*)k_out + skip, (char*)v_out + skip,
+                         stream);
+  }
   return decode_launch(c, a, out, out_dtype, k_out, v_out, stream);
 }
 

@@ -401,14 +401,16 @@ def test_api_errors_with_live_codec(gpu):
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("d,L,B,T", [(128, 4, 1, 8197), (64, 2, 2, 8197)])
+@pytest.mark.parametrize("d,L,B,T", [(128, 4, 1, 8197), (64, 2, 2, 8197), (128, 2, 8, 8197)])
 def test_multi_tile_decode_ragged(gpu, d, L, B, T):
     """Shapes large enough that the decode gives each wave 4 (d=128) or 2 (d=64) tiles of the
     common formats (n = 64/256 with 8-bit linear K and 4-bit log V norms), with T = 8197 so
     that the last tile of every (layer, kind) is ragged, the last wave of a segment gets fewer
-    tiles (3 at d=128, 1 at d=64) and tiles both stay within and cross (batch, head) rows.
-    Every vector of the last tiles of each segment and 600 random ones, decoded to fp32 and
-    bf16, against the oracle's decode of the same cache bytes; every output element written."""
+    tiles (3 at d=128, 1 at d=64) and tiles both stay within and cross (batch, head) rows; at
+    B = 8 the range holds 2^19 whole-tile vectors per kind, so it is decoded as whole tiles
+    per row and then the last 5 tokens of every row.  Every vector of the last tiles of each
+    segment, the last tokens of some rows and 600 random ones, decoded to fp32 and bf16,
+    against the oracle's decode of the same cache bytes; every output element written."""
     import torch
     w = workloads.get("C2")
     table = [LayerCfg(64, 64), LayerCfg(256, 256), LayerCfg(64, 256), LayerCfg(256, 64)][:L]
@@ -433,6 +435,10 @@ def test_multi_tile_decode_ragged(gpu, d, L, B, T):
     picks = [(l, kind, j) for l in range(L) for kind in range(2) for j in tail]
     picks += [(int(rng.integers(0, L)), int(rng.integers(0, 2)), int(rng.integers(0, nvec)))
               for _ in range(600)]
+    for _ in range(8):                   # the last tokens of random rows, every layer and kind
+        bh = int(rng.integers(0, B * 8))
+        picks += [(l, kind, bh * T + t) for l in range(L) for kind in range(2)
+                  for t in range(T - 5, T)]
     chk32, chk16 = DecodeCheck(), DecodeCheck()
     for l, kind, j in picks:
         bh, t = divmod(j, T)
