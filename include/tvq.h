@@ -139,7 +139,9 @@ tvq_status tvq_cache_layout(const tvq_codec* c, int64_t batch, int64_t capacity_
  * Requires in->batch == lay->batch and t_begin + in->tokens <= lay->capacity_tokens.
  * k, v: device pointers; cache: device pointer to lay->total_bytes bytes.
  * Launches up to two kernels on `stream` (one for bf16 input of the layers whose formats have a
- * dedicated kernel, one for the rest); in->tokens == 0 launches nothing. */
+ * dedicated kernel, one for the rest), twice over for bf16 input of at least 2^19 vectors per
+ * kind whose token count is not a multiple of the tile's (16 tokens at d = 128, 32 at d = 64):
+ * its whole tiles first, then the remaining tokens; in->tokens == 0 launches nothing. */
 tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, const void* v,
                       const tvq_tensor_desc* in, int64_t t_begin, void* cache,
                       const tvq_layout* lay, void* stream);

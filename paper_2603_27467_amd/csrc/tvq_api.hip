@@ -592,6 +592,12 @@ static tvq_status encode_launch(const tvq_codec* c, tvq::EncodeArgs& a, const tv
   return TVQ_OK;
 }
 
+// Ranges of at least this many vectors per kind whose token count is not a multiple of the
+// tile's are encoded or decoded in two parts (whole tiles per (batch, head) row, on the
+// kernels that keep a tile's position in scalar registers, then the remaining tokens of every
+// row): below it the extra launch costs more than those kernels save.
+constexpr int64_t kSplitVectors = 1 << 19;
+
 static void encode_source(tvq::EncodeArgs& a, const void* k, const void* v,
                           const tvq_tensor_desc* in) {
   a.k = k;
@@ -615,14 +621,29 @@ tvq_status tvq_encode(const tvq_codec* c, tvq_dtype in_dtype, const void* k, con
   if (!k || !v || !cache || !aligned16(k) || !aligned16(v) || !aligned16(cache))
     return TVQ_ERR_INVALID_ARG;
 
+  const int64_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
+  const int64_t whole = in->tokens / vpw * vpw;
+  const bool split = in_dtype == TVQ_BF16 && whole > 0 && whole != in->tokens &&
+                     in->batch * c->H * whole >= kSplitVectors;
+  tvq_tensor_desc head = *in;
+  if (split) head.tokens = whole;
   tvq::EncodeArgs a;
   std::memset(&a, 0, sizeof(a));
-  encode_source(a, k, v, in);
+  encode_source(a, k, v, &head);
   a.cache = (uint8_t*)cache;
   a.n_slots = lay->batch * c->H * lay->capacity_tokens;
   a.cap = (uint32_t)lay->capacity_tokens;
   a.t_begin = (uint32_t)t_begin;
-  return encode_launch(c, a, in, in_dtype == TVQ_F32, stream);
+  tvq_status st = encode_launch(c, a, &head, in_dtype == TVQ_F32, stream);
+  if (st != TVQ_OK || !split) return st;
+  // the remaining tokens of every row, read from the same view past its whole tiles
+  tvq_tensor_desc tail = *in;
+  tail.tokens = in->tokens - whole;
+  const int64_t skip = whole * in->stride_t * eb;
+  tvq::EncodeArgs b = a;
+  encode_source(b, (const char*)k + skip, (const char*)v + skip, &tail);
+  b.t_begin = (uint32_t)(t_begin + whole);
+  return encode_launch(c, b, &tail, false, stream);
 }
 
 tvq_status tvq_encode_mfma(const tvq_codec* c, const void* k, const void* v,
@@ -669,11 +690,6 @@ tvq_status tvq_encode_paged(const tvq_codec* c, tvq_dtype in_dtype, const void* 
   a.cap = (uint32_t)pool_layout->capacity_tokens;
   return encode_launch(c, a, in, in_dtype == TVQ_F32, stream);
 }
-
-// Ranges of at least this many vectors per kind whose token count is not a multiple of the
-// tile's are decoded in two parts (whole tiles, then the rest): below it the extra launch
-// costs more than the whole-tile kernel saves.
-constexpr int64_t kDecodeSplitVectors = 1 << 19;
 
 static tvq_status decode_launch(const tvq_codec* c, tvq::DecodeArgs& a,
                                 const tvq_tensor_desc* out, tvq_dtype out_dtype, void* k_out,
@@ -737,7 +753,7 @@ tvq_status tvq_decode(const tvq_codec* c, const void* cache, const tvq_layout* l
   // registers) and then the remaining tokens of every row, into the same output view.
   const int64_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
   const int64_t whole = out->tokens / vpw * vpw;
-  if (whole > 0 && whole != out->tokens && out->batch * c->H * whole >= kDecodeSplitVectors) {
+  if (whole > 0 && whole != out->tokens && out->batch * c->H * whole >= kSplitVectors) {
     tvq_tensor_desc head = *out, tail = *out;
     head.tokens = whole;
     tail.tokens = out->tokens - whole;

@@ -462,6 +462,8 @@ def test_multi_tile_decode_ragged(gpu, d, L, B, T):
     (128, 4, 1, 4100, 3, 0),     # tiles that cross (batch, head) rows, ragged last tile
     (64, 2, 2, 8192, 3, 32),     # d = 64 whole tiles, strided
     (64, 2, 2, 8194, 0, 0),      # d = 64 tiles crossing rows
+    (128, 2, 8, 8197, 5, 32),    # 2^19 whole-tile vectors per kind: whole tiles, then the
+                                 # last 5 tokens of every row, from a strided view
 ])
 def test_multi_tile_encode_sampled(gpu, d, L, B, T, t_begin, pad):
     """Encode launches of 2 tiles per wave (the multi-tile kernel) with and without tiles that
@@ -495,6 +497,10 @@ def test_multi_tile_encode_sampled(gpu, d, L, B, T, t_begin, pad):
     picks = [(l, kind, j) for l in range(L) for kind in range(2) for j in tail]
     picks += [(int(rng.integers(0, L)), int(rng.integers(0, 2)), int(rng.integers(0, nvec)))
               for _ in range(1500)]
+    for _ in range(8):                   # the last tokens of random rows, every layer and kind
+        bh = int(rng.integers(0, B * 8))
+        picks += [(l, kind, bh * T + t) for l in range(L) for kind in range(2)
+                  for t in range(max(0, T - 5), T)]
     stats = dict(angle_mismatch=0, angle_unflagged=0, norm_mismatch=0, norm_unflagged=0,
                  hdr_ulp=0)
     for l, kind, j in picks:
