@@ -851,6 +851,9 @@ def main() -> int:
                     help="long-context attention step over a paged pool (implies --attention)")
     ap.add_argument("--graph", action="store_true",
                     help="with --paged: capture the step once and replay it")
+    ap.add_argument("--pool", action="store_true",
+                    help="encode and decode through a paged pool (blocks of PAGE_TOKENS slots "
+                         "handed out in a shuffled order) in place of a contiguous cache")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for counter scaling)")
     ap.add_argument("--summarize-profiles", nargs=5,
@@ -865,6 +868,10 @@ def main() -> int:
     args = ap.parse_args()
     if args.paged:
         args.attention = True
+    if args.pool and (args.encode_mfma or args.attention or args.workload == "C5"):
+        print("--pool runs the codec step of C1-C4 with the canonical encode only",
+              file=sys.stderr)
+        return 2
     if args.summarize_profiles:
         return summarize_profiles(*args.summarize_profiles, args.commands)
     if args.summarize_attention_profiles:
@@ -904,23 +911,43 @@ def main() -> int:
                            t.norm_mode_v) for t in w.table]
     codec = tvq.Codec(w.L, w.H, w.d, layers,
                       signs=workloads.sign_table(w.sign_seed, w.L, w.d))
-    lay = codec.layout(w.B, w.T)
+    stream = torch.cuda.current_stream()
+    if args.pool:
+        # the same records in a pool of PAGE_TOKENS-slot blocks, shuffled over the sequences
+        max_blocks = -(-w.T // PAGE_TOKENS)
+        n_blocks = w.B * max_blocks
+        lay = codec.pool_layout(n_blocks, PAGE_TOKENS)
+        perm = np.random.default_rng(w.data_seed).permutation(n_blocks).astype(np.int32)
+        table = torch.from_numpy(perm.reshape(w.B, max_blocks)).cuda()
+        pos0 = torch.zeros(w.B, dtype=torch.int32, device="cuda")
+
+        def encode_to(c):
+            codec.encode_paged(kd, vd, pos0, table, c, lay, stream)
+
+        def decode_from(c, ko, vo):
+            codec.decode_paged(c, lay, table, 0, w.T, ko, vo, stream)
+    else:
+        lay = codec.layout(w.B, w.T)
+        encode = codec.encode_mfma if args.encode_mfma else codec.encode
+
+        def encode_to(c):
+            encode(kd, vd, c, lay, 0, stream)
+
+        def decode_from(c, ko, vo):
+            codec.decode(c, lay, 0, w.T, ko, vo, stream)
     caches = [torch.empty(lay.total_bytes, dtype=torch.uint8, device="cuda") for _ in range(2)]
     outs = [(torch.empty_like(kd), torch.empty_like(vd)) for _ in range(2)]
-    stream = torch.cuda.current_stream()
     for c in caches:                        # both caches hold the encoded workload
-        codec.encode(kd, vd, c, lay, 0, stream)
-
-    encode = codec.encode_mfma if args.encode_mfma else codec.encode
+        encode_to(c)
 
     def step(i, ev=None):
         if ev is not None:
             ev[0].record(stream)
-        encode(kd, vd, caches[i % 2], lay, 0, stream)
+        encode_to(caches[i % 2])
         if ev is not None:
             ev[1].record(stream)
         ko, vo = outs[i % 2]
-        codec.decode(caches[(i + 1) % 2], lay, 0, w.T, ko, vo, stream)
+        decode_from(caches[(i + 1) % 2], ko, vo)
         if ev is not None:
             ev[2].record(stream)
 
@@ -951,8 +978,9 @@ def main() -> int:
         kern = f"tvq_{name}"
         ms = float(ms_all.mean())
         gbs = ab["per_launch"] / (ms * 1e-3) / 1e9
-        # the committed counters cover the canonical-schedule encode only
-        prof = None if (args.encode_mfma and name == "encode") else profile_entry(kern, w.name)
+        # the committed counters cover the canonical-schedule encode of a contiguous cache
+        prof = (None if (args.encode_mfma and name == "encode") or args.pool
+                else profile_entry(kern, w.name))
         out = {"ms": round(ms, 5), "ms_median": round(float(np.median(ms_all)), 5),
                "ms_min": round(float(ms_all.min()), 5),
                "kv_GBps": round(ab["kv"] / (ms * 1e-3) / 1e9, 2),
@@ -1005,7 +1033,10 @@ def main() -> int:
                    "table": w.notes, "kv_bytes_per_direction": ab["kv"],
                    "compressed_bytes": ab["compressed"],
                    "encode_schedule": ("matrix-core stages, comparison (tvq_encode_mfma)"
-                                       if args.encode_mfma else "canonical butterfly")},
+                                       if args.encode_mfma else "canonical butterfly"),
+                   "cache": (f"paged pool, {PAGE_TOKENS}-slot blocks in a shuffled order "
+                             "(tvq_encode_paged / tvq_decode_paged)" if args.pool
+                             else "contiguous")},
         "roofline": {"bound": "hbm", "kernel": f"tvq_{dom_name}",
                      "achieved": dom["hbm_GBps_algorithmic"], "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": dom["frac_of_peak"],

@@ -708,10 +708,9 @@ static tvq_status decode_launch(const tvq_codec* c, tvq::DecodeArgs& a,
   a.H = (uint32_t)c->H;
   a.nvec = (uint32_t)(out->batch * c->H * out->tokens);
   const uint32_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
-  // the common formats go to the multi-tile kernel, the rest to the generic one; a paged
-  // source goes to the generic kernel whole
-  const bool paged = a.pg.table != nullptr;
-  const uint32_t n_fast = paged ? 0u : c->n_fast;
+  // the common formats go to the multi-tile kernel (a paged source through its block
+  // table), the rest to the generic one
+  const uint32_t n_fast = c->n_fast;
   const struct { uint32_t first, count, tpw; bool fast; } launches[2] = {
       {0, n_fast, tvq::kFastTilesPerWave, true},
       {n_fast, c->n_fast + c->n_generic - n_fast, 1, false}};

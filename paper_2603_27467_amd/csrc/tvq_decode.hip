@@ -77,18 +77,26 @@ __device__ __forceinline__ TilePos tile_pos(const DecodeArgs& a, uint32_t j0, in
   return p;
 }
 
-// Whole-tile rows (the call's token count a multiple of the tile's vector count, contiguous
-// cache): a tile's vectors are consecutive tokens of one (batch, head), so the position of its
-// first vector is wave-uniform -- computed once per tile in scalar registers -- and a lane's
-// vector is that position plus its vector slot.
+// Whole-tile rows (the call's token count a multiple of the tile's vector count): a tile's
+// vectors are consecutive tokens of one (batch, head), so the position of its first vector is
+// wave-uniform -- computed once per tile in scalar registers -- and a lane's vector is that
+// position plus its vector slot.  PAGED: t_begin is a multiple of the tile's vector count too,
+// so the tile lies in one pool block (blocks hold a power of two of at least 32 tokens); without
+// a block the tile reads records 0 .. VPW - 1 of the pool (in bounds) and is stored as zeros.
+template <bool PAGED = false>
 __device__ __forceinline__ TilePos tile_pos_rows(const DecodeArgs& a, uint32_t j0) {
   TilePos p;
   p.bh = fast_div(j0, a.div_t);
   p.t = j0 - p.bh * a.div_t.div;
   p.b = fast_div(p.bh, a.div_h);
   p.h = p.bh - p.b * a.H;
-  p.slot = p.bh * a.cap + a.t_begin + p.t;
-  p.valid = p.present = true;
+  p.valid = true;
+  if constexpr (PAGED) {
+    p.slot = paged_slot(a.pg, p.b, p.h, a.H, a.t_begin + p.t, p.present);
+  } else {
+    p.slot = p.bh * a.cap + a.t_begin + p.t;
+    p.present = true;
+  }
   return p;
 }
 
@@ -103,6 +111,9 @@ struct WaveState {
   const float2* lut_g;       // the codebook's table in global memory
   float2* lut_s;             // this wave's LDS copy, or null when it does not fit
   uint32_t sm[16];           // output sign masks, with this lane's butterfly sign folded in
+  uint32_t tile0 = 0;        // the wave's first tile
+  uint32_t pslot = 0;        // paged whole-tile rows: lane x holds the pool record of the first
+                             // vector of tile tile0 + x, bit 31 set when it has no block
 };
 
 // Segment set-up common to both kernels: the wave's segment and tiles, its cos/sin table into
@@ -167,15 +178,21 @@ __device__ __forceinline__ const float* build_log_levels(const WaveState<D>& w, 
 // lanes of a vector would otherwise compute the same one): lane (v, s) holds the ratio of
 // vector v in tile g + s of the group starting at tile g, from headers loaded a group ahead,
 // and tile g + x reads it from lane LPV v + x.
-template <int D>
+// Paged whole-tile rows take the records from the wave's per-tile lookups (WaveState::pslot).
+template <int D, bool PAGED = false, bool ROWS = false>
 struct LadderGroups {
   double rho = 1.0;
   u32x2 next = {0u, 0u};
   __device__ __forceinline__ void load(const DecodeArgs& a, const WaveState<D>& w,
                                        const uint8_t* hdr_plane, uint32_t tile, uint32_t last) {
-    const TilePos p = tile_pos(a, min(tile + (uint32_t)w.sub, last) * WaveState<D>::VPW,
-                               w.vslot);
-    next = *(const u32x2*)(hdr_plane + (uint64_t)p.slot * 8);
+    const uint32_t tl = min(tile + (uint32_t)w.sub, last);
+    uint32_t slot;
+    if constexpr (PAGED && ROWS) {
+      slot = ((uint32_t)__shfl((int)w.pslot, (int)(tl - w.tile0)) & 0x7FFFFFFFu) + w.vslot;
+    } else {
+      slot = tile_pos<PAGED>(a, tl * WaveState<D>::VPW, w.vslot).slot;
+    }
+    next = *(const u32x2*)(hdr_plane + (uint64_t)slot * 8);
   }
   // the ratio for tile `tile`, x = tile - (first tile of its group)
   __device__ __forceinline__ double at(const DecodeArgs& a, const WaveState<D>& w, uint32_t tile,
@@ -308,18 +325,36 @@ __device__ __forceinline__ void store_staged(const DecodeArgs& a, const WaveStat
   }
 }
 
-template <int D, int WA, int NB, bool ROWS = false>
+// PAGED: a position without a pool block reads record 0 of the pool (in bounds); its output is
+// zeroed when stored.
+// Whole-tile rows: the position of the tile's first vector; a paged one takes its pool record
+// from the lane of the tile (looked up once per wave).
+template <int D, bool PAGED>
+__device__ __forceinline__ TilePos rows_pos(const DecodeArgs& a, const WaveState<D>& w,
+                                            uint32_t tile) {
+  if constexpr (PAGED) {
+    TilePos p = tile_pos_rows<false>(a, tile * WaveState<D>::VPW);
+    const uint32_t r = __builtin_amdgcn_readlane(w.pslot, tile - w.tile0);
+    p.present = (r >> 31) == 0u;
+    p.slot = r & 0x7FFFFFFFu;
+    return p;
+  } else {
+    return tile_pos_rows<false>(a, tile * WaveState<D>::VPW);
+  }
+}
+
+template <int D, int WA, int NB, bool ROWS = false, bool PAGED = false>
 __device__ __forceinline__ TileCodes<WA, NB> load_tile_codes(const DecodeArgs& a,
                                                               const WaveState<D>& w, uint32_t tile) {
   if constexpr (ROWS) {
-    const TilePos p0 = tile_pos_rows(a, tile * WaveState<D>::VPW);
+    const TilePos p0 = rows_pos<D, PAGED>(a, w, tile);
     return load_codes_from<WA, NB>(w.plane, w.sp.rec, p0.slot, (uint32_t)w.vslot, w.sub);
   }
-  const TilePos p = tile_pos(a, tile * WaveState<D>::VPW, w.vslot);
+  const TilePos p = tile_pos<PAGED>(a, tile * WaveState<D>::VPW, w.vslot);
   return load_codes_at<WA, NB>(w.plane, w.sp.rec, p.slot, w.sub);
 }
 
-template <int D, bool F32OUT, int WA, int NB, bool ROWS = false>
+template <int D, bool F32OUT, int WA, int NB, bool ROWS = false, bool PAGED = false>
 __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState<D>& w,
                                             uint32_t* stg, const TileCodes<WA, NB>& c,
                                             uint32_t tile, double rho) {
@@ -343,10 +378,15 @@ __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState
   }
   uint32_t o[OutWords<F32OUT>::NW];
   reconstruct<D, F32OUT, true>(a, w, kc, r, o);
-  if constexpr (ROWS)
-    store_staged<D, F32OUT, true>(a, w, tile_pos_rows(a, tile * WaveState<D>::VPW), o, stg);
-  else
-    store_staged<D, F32OUT>(a, w, tile_pos(a, tile * WaveState<D>::VPW, w.vslot), o, stg);
+  const TilePos p = ROWS ? rows_pos<D, PAGED>(a, w, tile)
+                        : tile_pos<PAGED>(a, tile * WaveState<D>::VPW, w.vslot);
+  if constexpr (PAGED) {
+    if (!p.present) {
+#pragma unroll
+      for (int i = 0; i < OutWords<F32OUT>::NW; ++i) o[i] = 0u;
+    }
+  }
+  store_staged<D, F32OUT, ROWS>(a, w, p, o, stg);
 }
 
 // Tiles tile0 .. tile0 + ntiles - 1.  MULTI: two per iteration from two code buffers, each
@@ -356,37 +396,38 @@ __device__ __forceinline__ void decode_tile(const DecodeArgs& a, const WaveState
 // has no branch around a load or a store, and nothing has to wait for a load before its data
 // is used.  Launches of one tile per wave use the instantiation without the loop (a separate
 // copy of the tile code inside the same kernel would raise its register count).
-template <int D, bool F32OUT, bool MULTI, int WA, int NB, bool ROWS = false>
+template <int D, bool F32OUT, bool MULTI, int WA, int NB, bool ROWS = false, bool PAGED = false>
 __device__ void decode_tiles_prefetch(const DecodeArgs& a, const WaveState<D>& w, uint32_t* stg,
                                       uint32_t tile0, uint32_t ntiles) {
   constexpr int LPV = WaveState<D>::LPV;
   constexpr uint32_t kLevels = (1u << NB) - 1u;
   const uint32_t last = tile0 + ntiles - 1;
-  TileCodes<WA, NB> ca = load_tile_codes<D, WA, NB, ROWS>(a, w, tile0);
+  TileCodes<WA, NB> ca = load_tile_codes<D, WA, NB, ROWS, PAGED>(a, w, tile0);
   if constexpr (!MULTI) {
     const float rmin = __uint_as_float(ca.hdr.x), rmax = __uint_as_float(ca.hdr.y);
-    decode_tile<D, F32OUT>(a, w, stg, ca, tile0,
-                           NB == 8 ? 1.0 : ladder_rho(rmin, rmax, kLevels));
+    decode_tile<D, F32OUT, WA, NB, false, PAGED>(a, w, stg, ca, tile0,
+                                                 NB == 8 ? 1.0 : ladder_rho(rmin, rmax, kLevels));
     return;
   }
-  LadderGroups<D> lg;
+  LadderGroups<D, PAGED, ROWS> lg;
   if constexpr (NB != 8) lg.load(a, w, w.plane[2], tile0, last);
   for (uint32_t t = tile0; t <= last; t += 2) {
     const uint32_t t1 = min(t + 1, last);
-    const TileCodes<WA, NB> cb = load_tile_codes<D, WA, NB, ROWS>(a, w, t1);
+    const TileCodes<WA, NB> cb = load_tile_codes<D, WA, NB, ROWS, PAGED>(a, w, t1);
     double rho = 1.0;
     if constexpr (NB != 8) rho = lg.at(a, w, t, (t - tile0) % LPV, last, kLevels);
-    decode_tile<D, F32OUT, WA, NB, ROWS>(a, w, stg, ca, t, rho);
-    ca = load_tile_codes<D, WA, NB, ROWS>(a, w, min(t + 2, last));
+    decode_tile<D, F32OUT, WA, NB, ROWS, PAGED>(a, w, stg, ca, t, rho);
+    ca = load_tile_codes<D, WA, NB, ROWS, PAGED>(a, w, min(t + 2, last));
     // t1 == t (the last tile again) keeps the ratio of tile t
     if constexpr (NB != 8) {
       if (t1 != t) rho = lg.at(a, w, t1, (t1 - tile0) % LPV, last, kLevels);
     }
-    decode_tile<D, F32OUT, WA, NB, ROWS>(a, w, stg, cb, t1, rho);
+    decode_tile<D, F32OUT, WA, NB, ROWS, PAGED>(a, w, stg, cb, t1, rho);
   }
 }
 
-template <int D, bool F32OUT, bool MULTI, bool ROWS = false>
+// PAGED: the source is a paged pool, and positions without a block decode to zeros.
+template <int D, bool F32OUT, bool MULTI, bool ROWS = false, bool PAGED = false>
 __global__ __launch_bounds__(kBlockThreads) void decode_fast_kernel(DecodeArgs a) {
   constexpr int kStageWords = kWave * OutWords<F32OUT>::PITCH;
   static_assert(kStageWords >= kLvlPerWave, "the level table shares the staging area");
@@ -395,15 +436,23 @@ __global__ __launch_bounds__(kBlockThreads) void decode_fast_kernel(DecodeArgs a
   WaveState<D> w;
   uint32_t tile0, ntiles;
   if (!wave_setup<D>(a, w, s_lut, kLutFast, tile0, ntiles)) return;
+  w.tile0 = tile0;
+  static_assert(kFastTilesPerWave <= (uint32_t)kWave, "one lane per tile of the wave");
+  if constexpr (ROWS && PAGED) {
+    // lane x: the pool record of tile tile0 + x (at most 64 tiles a wave)
+    const uint32_t x = min((uint32_t)w.lane, ntiles - 1);
+    const TilePos q = tile_pos_rows<true>(a, (tile0 + x) * WaveState<D>::VPW);
+    w.pslot = q.present ? q.slot : 0x80000000u;
+  }
   // every codebook of this kernel (n <= 256) is in LDS
   uint32_t* stg = s_stg[w.wib];
   const bool wide = w.sp.w == 8;
   if (w.sp.mode == 1) {
-    if (wide) decode_tiles_prefetch<D, F32OUT, MULTI, 8, 8, ROWS>(a, w, stg, tile0, ntiles);
-    else decode_tiles_prefetch<D, F32OUT, MULTI, 6, 8, ROWS>(a, w, stg, tile0, ntiles);
+    if (wide) decode_tiles_prefetch<D, F32OUT, MULTI, 8, 8, ROWS, PAGED>(a, w, stg, tile0, ntiles);
+    else decode_tiles_prefetch<D, F32OUT, MULTI, 6, 8, ROWS, PAGED>(a, w, stg, tile0, ntiles);
   } else {
-    if (wide) decode_tiles_prefetch<D, F32OUT, MULTI, 8, 4, ROWS>(a, w, stg, tile0, ntiles);
-    else decode_tiles_prefetch<D, F32OUT, MULTI, 6, 4, ROWS>(a, w, stg, tile0, ntiles);
+    if (wide) decode_tiles_prefetch<D, F32OUT, MULTI, 8, 4, ROWS, PAGED>(a, w, stg, tile0, ntiles);
+    else decode_tiles_prefetch<D, F32OUT, MULTI, 6, 4, ROWS, PAGED>(a, w, stg, tile0, ntiles);
   }
 }
 
@@ -485,16 +534,22 @@ int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, u
   hipStream_t s = (hipStream_t)stream;
   const dim3 block(tvq::kBlockThreads);
   const bool paged = a.pg.table != nullptr;
-  if (paged && fast) return -1;       // a paged source goes to the generic kernel
   const bool multi = a.tiles_per_wave > 1;
-  // whole-tile rows: every tile's vectors consecutive tokens of one (batch, head), and a lane's
-  // output offset within its tile, (VPW - 1) * stride_t elements, inside 32 bits
+  // whole-tile rows: every tile's vectors consecutive tokens of one (batch, head) (of one pool
+  // block when paged), and a lane's output offset within its tile, (VPW - 1) * stride_t
+  // elements, inside 32 bits
   const uint32_t vpw = d == 128 ? 16u : 32u;
-  const bool rows = !paged && a.div_t.div % vpw == 0 &&
+  const bool rows = a.div_t.div % vpw == 0 && (!paged || a.t_begin % vpw == 0) &&
                     (uint64_t)a.stride_t * vpw * (out_f32 ? 4u : 2u) < (1ull << 31);
 #define TVQ_LAUNCH_DEC(D, F32)                                                                  \
   do {                                                                                          \
-    if (fast && multi && rows)                                                                  \
+    if (fast && paged && multi && rows)                                                         \
+      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true, true, true>), dim3(grid), block, 0, s, a); \
+    else if (fast && paged && multi)                                                            \
+      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true, false, true>), dim3(grid), block, 0, s, a); \
+    else if (fast && paged)                                                                     \
+      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, false, false, true>), dim3(grid), block, 0, s, a); \
+    else if (fast && multi && rows)                                                             \
       hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true, true>), dim3(grid), block, 0, s, a); \
     else if (fast && multi)                                                                     \
       hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true>), dim3(grid), block, 0, s, a);  \

@@ -355,16 +355,17 @@ struct TileIn {
 };
 
 // PAGED: token t of sequence b goes to position seq[b] + t through the block table.
-// ALIGNED (bf16, contiguous cache, T a multiple of the tile's vector count): the tile's
-// vectors are consecutive tokens of one (batch, head), so its position is wave-uniform
-// (scalar arithmetic) and each lane adds a fixed offset; `slot` is then the slot of the
-// tile's first vector.
+// ALIGNED (bf16, T a multiple of the tile's vector count): the tile's vectors are consecutive
+// tokens of one (batch, head), so its position is wave-uniform (scalar arithmetic) and each
+// lane adds a fixed offset to its input address; `slot` is then the slot of the tile's first
+// vector in a contiguous cache, or the lane's own pool record (a tile may straddle two blocks
+// when seq[b] is not a multiple of its vector count).
 template <int D, bool F32IN, bool PAGED, bool ALIGNED = false>
 __device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const EncWave<D>& w,
                                                    uint32_t tile) {
   const uint32_t j0 = tile * EncWave<D>::VPW;
   if constexpr (ALIGNED) {
-    static_assert(!F32IN && !PAGED, "aligned tiles: bf16 input, contiguous cache");
+    static_assert(!F32IN, "aligned tiles: bf16 input");
     const uint32_t bh = fast_div(j0, a.div_t);
     const uint32_t t = j0 - bh * a.div_t.div;
     const uint32_t b = fast_div(bh, a.div_h);
@@ -374,8 +375,16 @@ __device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const En
                            (uint64_t)t * a.stride_t;
     TileIn<F32IN> in;
     load_words<16>((const uint32_t*)((const uint8_t*)base + w.lane_in_bytes), in.raw.w);
-    in.slot = bh * a.cap + a.t_begin + t;
-    in.ok = true;
+    if constexpr (PAGED) {
+      const int32_t p0 = a.pg.seq[b];
+      const uint32_t tl = t + (uint32_t)w.vslot;
+      bool ok;
+      in.slot = paged_slot(a.pg, b, h, a.H, (uint32_t)p0 + tl, ok);
+      in.ok = ok && p0 >= 0 && (uint32_t)p0 + tl >= (uint32_t)p0;
+    } else {
+      in.slot = bh * a.cap + a.t_begin + t;
+      in.ok = true;
+    }
     return in;
   }
   const uint32_t j = j0 + w.vslot;
@@ -797,25 +806,27 @@ template <int D, bool MULTI, int WA, int NB, bool PAGED, bool MF = false, bool A
 __device__ void encode_tiles_fast(const EncodeArgs& a, const EncWave<D>& w, uint32_t tile0,
                                   uint32_t ntiles) {
   const uint32_t last = tile0 + ntiles - 1;
+  // aligned pool records are per lane (load_tile): the stores then take the lane's own slot
+  constexpr bool SA = ALIGNED && !PAGED;
   TileIn<false> ia = load_tile<D, false, PAGED, ALIGNED>(a, w, tile0);
   stage_tables<D>(a, w);
   if constexpr (!MULTI) {
-    if (encode_tile<D, false, WA, NB, PAGED, MF, false, ALIGNED>(a, w, ia))
-      encode_norms_f64<D, false, NB, PAGED, MF, ALIGNED>(w, ia);
+    if (encode_tile<D, false, WA, NB, PAGED, MF, false, SA>(a, w, ia))
+      encode_norms_f64<D, false, NB, PAGED, MF, SA>(w, ia);
     return;
   }
   uint32_t redo = 0;    // tiles (bit tile - tile0) whose norms take the fp64 pass
   for (uint32_t t = tile0; t <= last; t += 2) {
     const uint32_t t1 = min(t + 1, last);
     const TileIn<false> ib = load_tile<D, false, PAGED, ALIGNED>(a, w, t1);
-    if (encode_tile<D, false, WA, NB, PAGED, MF, true, ALIGNED>(a, w, ia)) redo |= 1u << (t - tile0);
+    if (encode_tile<D, false, WA, NB, PAGED, MF, true, SA>(a, w, ia)) redo |= 1u << (t - tile0);
     ia = load_tile<D, false, PAGED, ALIGNED>(a, w, min(t + 2, last));
-    if (encode_tile<D, false, WA, NB, PAGED, MF, true, ALIGNED>(a, w, ib)) redo |= 1u << (t1 - tile0);
+    if (encode_tile<D, false, WA, NB, PAGED, MF, true, SA>(a, w, ib)) redo |= 1u << (t1 - tile0);
   }
   while (redo != 0) {
     const uint32_t k = __builtin_ctz(redo);
     redo &= redo - 1;
-    encode_norms_f64<D, false, NB, PAGED, MF, ALIGNED>(
+    encode_norms_f64<D, false, NB, PAGED, MF, SA>(
         w, load_tile<D, false, PAGED, ALIGNED>(a, w, tile0 + k));
   }
 }
@@ -885,10 +896,9 @@ void launch_encode(const EncodeArgs& a, int in_f32, bool fast, unsigned grid, hi
   // aligned tiles: whole tiles per (batch, head), and every lane's input offset from its
   // tile's first vector, (VPW - 1) * stride_t + d elements of bf16, inside 32 bits
   constexpr uint32_t VPW = EncWave<D>::VPW;
-  const bool aligned = !PAGED && a.div_t.div % VPW == 0 &&
-                       (uint64_t)a.stride_t * VPW * 2u < (1ull << 31);
+  const bool aligned = a.div_t.div % VPW == 0 && (uint64_t)a.stride_t * VPW * 2u < (1ull << 31);
   if (fast && multi && aligned)
-    hipLaunchKernelGGL((encode_fast_kernel<D, true, PAGED, !PAGED>), dim3(grid), block, 0, s, a);
+    hipLaunchKernelGGL((encode_fast_kernel<D, true, PAGED, true>), dim3(grid), block, 0, s, a);
   else if (fast && multi)
     hipLaunchKernelGGL((encode_fast_kernel<D, true, PAGED>), dim3(grid), block, 0, s, a);
   else if (fast)

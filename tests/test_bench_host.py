@@ -77,3 +77,12 @@ def test_gpu_count_above_one_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+@pytest.mark.parametrize("extra", [["--workload", "C5"], ["--attention"], ["--encode-mfma"]])
+def test_pool_takes_the_codec_step_only(extra):
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--pool", *extra],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "--pool" in r.stderr

@@ -237,7 +237,9 @@ def test_paged_random_pools(gpu):
     pool) and spare pool blocks; a prefill of random length, then a one-token append at each
     sequence's own position.  Codes against the oracle on the gathered caches, pool blocks no
     table names untouched, the paged decode (fp32) of the written positions against the fp64
-    decode, and attention with random per-sequence contexts within the written prefix."""
+    decode and zeros where the table names no block (and a window starting inside a tile equal
+    to it bit for bit), and attention with random per-sequence contexts within the written
+    prefix."""
     import torch
     rng = np.random.default_rng(4242)
     for case_no in range(8):
@@ -278,7 +280,21 @@ def test_paged_random_pools(gpu):
             if n > 0:
                 ref64 = case.s.orc.decode_cache(gath[b], 1, case.cap, 0, n, "f64")[:, :, 0]
                 check_decoded(chk, ref64, d, g32=g[:, :, b, :, :n])
+            has = np.array([case.allocated(b, t) for t in range(case.cap)])
+            assert np.all(g[:, :, b, :, ~has] == 0), f"{name}: positions without a block"
         assert chk.ok(), f"{name}: {chk.line()}"
+        # a window that starts and ends inside tiles (per-lane block lookups) against the
+        # whole-range decode above (one lookup per tile): the same values bit for bit
+        t0 = int(rng.integers(1, 16))
+        t1 = int(rng.integers(t0 + 1, case.cap + 1))
+        kw = torch.full((case.L, B, case.H, t1 - t0, d), float("nan"), dtype=torch.float32,
+                        device="cuda")
+        vw = torch.full_like(kw, float("nan"))
+        case.s.gpu.decode_paged(case.pool, case.pool_lay, case.table_dev, t0, t1, kw, vw)
+        torch.cuda.synchronize()
+        gw = np.stack([torch_to_np(kw), torch_to_np(vw)], axis=1)
+        assert np.array_equal(gw.view(np.uint32), g[..., t0:t1, :].view(np.uint32)), \
+            f"{name}: window [{t0}, {t1})"
         # attention over random contexts inside each written prefix
         G = int(rng.integers(1, 6))
         Hq = case.H * G
@@ -305,6 +321,71 @@ def test_paged_random_pools(gpu):
             assert np.isfinite(got[b]).all() and (err <= bar).all(), name
         _say(f"[{name}] decode {chk.line()}; attention G={G} ctx={lens} worst |err|/bar "
              f"{worst:.3f}")
+
+
+@pytest.mark.parametrize("d,T", [(128, 4096), (128, 4101), (64, 8192), (64, 8195)])
+def test_paged_multi_tile(gpu, d, T):
+    """Pools large enough that encode and decode give each wave 2 tiles (the multi-tile
+    kernels): 4 layers of the common formats, 4 sequences of 2 heads written from positions
+    0, 5, 32 and 300 (tiles that start inside a block and tiles that straddle two), 256-slot
+    blocks in a shuffled order, one missing block inside sequence 3's range and spare blocks.
+    T a multiple of the tile's vector count gives the tiles of one (batch, head) row (input
+    addressed once per tile), the odd T tiles that cross rows.  Checks: every code and header
+    against the oracle's encode of the same tokens at the same positions, pool blocks no table
+    names untouched; the decode of the whole table range (a multiple of the tile's count from 0:
+    one block lookup per tile) in fp32 and bf16 against the oracle's fp64 decode on the written
+    positions, zeros without a block; a window starting inside a tile (per-lane lookups) equal to
+    the whole-range decode bit for bit."""
+    import torch
+    L, B, Pb = 4, 4, 256
+    fmt = [LayerCfg(64, 64), LayerCfg(256, 256), LayerCfg(64, 256), LayerCfg(256, 64)]
+    starts = [0, 5, 32, 300]
+    need = [-(-(p0 + T) // Pb) for p0 in starts]
+    max_blocks = max(need) + 1
+    n_blocks = sum(need) - 1 + 2
+    perm = list(np.random.default_rng(77 + d).permutation(n_blocks))
+    tab = []
+    for b in range(B):
+        row = [int(perm.pop()) for _ in range(need[b] - (b == 3))]
+        if b == 3:
+            row.insert(2, -1)                              # a hole inside the written range
+        tab.append(row + [-1] * (max_blocks - len(row)))
+    # both launches take 2 tiles per wave (the host's grid plan: tiles / (256 CUs x 32 waves))
+    vpw = 64 // (d // 32)
+    for nvec in (B * 2 * T, B * 2 * max_blocks * Pb):
+        assert min(4, (-(-nvec // vpw)) * 2 * L // (256 * 32)) >= 2
+    case = PagedCase(d, fmt, seed=900 + d + T, shape=(B, max_blocks, n_blocks, Pb, tab))
+    case.encode(starts, T, seed=910 + T)
+    name = f"paged-multi d={d} T={T}"
+    _, gath = _check_codes(case, name)
+    shape = (L, B, case.H, case.cap, d)
+    full = {}
+    for dt in (torch.float32, torch.bfloat16):
+        ko = torch.full(shape, float("nan"), dtype=dt, device="cuda")
+        vo = torch.full_like(ko, float("nan"))
+        case.s.gpu.decode_paged(case.pool, case.pool_lay, case.table_dev, 0, case.cap, ko, vo)
+        torch.cuda.synchronize()
+        full[dt] = np.stack([torch_to_np(ko), torch_to_np(vo)], axis=1)   # [L,2,B,H,cap,d]
+    chk32, chk16 = DecodeCheck(), DecodeCheck()
+    for b in range(B):
+        has = np.array([case.allocated(b, t) for t in range(case.cap)])
+        assert np.all(full[torch.float32][:, :, b, :, ~has] == 0), f"{name}: no block"
+        assert np.all((full[torch.bfloat16][:, :, b, :, ~has] & 0x7FFF) == 0)
+        w = case.written[b].astype(np.int8)
+        edges = np.flatnonzero(np.diff(np.concatenate([[0], w, [0]])))
+        for a, e in zip(edges[0::2], edges[1::2]):
+            ref64 = case.s.orc.decode_cache(gath[b], 1, case.cap, a, e, "f64")[:, :, 0]
+            check_decoded(chk32, ref64, d, g32=full[torch.float32][:, :, b, :, a:e])
+            check_decoded(chk16, ref64, d, g16=full[torch.bfloat16][:, :, b, :, a:e])
+    _say(f"[{name}] decode fp32 {chk32.line()}; bf16 {chk16.line()}")
+    assert chk32.ok() and chk16.ok(), name
+    t0, t1 = 3, case.cap - 13
+    kw = torch.full((L, B, case.H, t1 - t0, d), float("nan"), dtype=torch.float32, device="cuda")
+    vw = torch.full_like(kw, float("nan"))
+    case.s.gpu.decode_paged(case.pool, case.pool_lay, case.table_dev, t0, t1, kw, vw)
+    torch.cuda.synchronize()
+    gw = np.stack([torch_to_np(kw), torch_to_np(vw)], axis=1)
+    assert np.array_equal(gw.view(np.uint32), full[torch.float32][..., t0:t1, :].view(np.uint32))
 
 
 def test_paged_step_graph_replay(gpu):
