@@ -278,6 +278,10 @@ struct EncWave {
                               // less 8 kRoundShiftBits, modulo 2^32 (fast formats)
   uint32_t bins_off;          // n/2 on lanes holding -z (the half turn), else 0
   bool negated;               // the lane holds -z after the butterfly
+  uint32_t tile0;             // aligned paged tiles: the wave's first tile, and the pool
+  uint32_t prec[2];           // records of vector c = x VPW + v (vector slot v of tile
+                              // tile0 + x), c in register c / 64 of lane c % 64 (bit 31: no
+                              // block)
   float shift;                // rounding shift with the half-turn of a negated lane removed
   uint32_t unneg;             // sign flip that undoes the negation (odd n)
 };
@@ -376,11 +380,15 @@ __device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const En
     TileIn<F32IN> in;
     load_words<16>((const uint32_t*)((const uint8_t*)base + w.lane_in_bytes), in.raw.w);
     if constexpr (PAGED) {
-      const int32_t p0 = a.pg.seq[b];
-      const uint32_t tl = t + (uint32_t)w.vslot;
-      bool ok;
-      in.slot = paged_slot(a.pg, b, h, a.H, (uint32_t)p0 + tl, ok);
-      in.ok = ok && p0 >= 0 && (uint32_t)p0 + tl >= (uint32_t)p0;
+      // looked up at the wave's start (paged_records)
+      const uint32_t c = (tile - w.tile0) * EncWave<D>::VPW + (uint32_t)w.vslot;
+      uint32_t r = (uint32_t)__shfl((int)w.prec[0], (int)(c & 63u));
+      if constexpr (EncWave<D>::VPW * kFastTilesPerWave > (uint32_t)kWave) {
+        const uint32_t r1 = (uint32_t)__shfl((int)w.prec[1], (int)(c & 63u));
+        r = c >= (uint32_t)kWave ? r1 : r;
+      }
+      in.slot = r & 0x7FFFFFFFu;
+      in.ok = (r >> 31) == 0u;
     } else {
       in.slot = bh * a.cap + a.t_begin + t;
       in.ok = true;
@@ -406,6 +414,33 @@ __device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const En
     in.ok = true;
   }
   return in;
+}
+
+// Aligned paged tiles: each lane's pool record in each of the wave's tiles, looked up before
+// the tile loop so that the table reads do not wait in the loop.
+// (Held across lanes and read back with a lane permute: an array indexed by the tile would be
+// placed in scratch memory.)  Every tile of an aligned launch is whole.
+template <int D>
+__device__ __forceinline__ void paged_records(const EncodeArgs& a, EncWave<D>& w, uint32_t tile0,
+                                              uint32_t ntiles) {
+  constexpr uint32_t VPW = EncWave<D>::VPW;
+  static_assert(VPW * kFastTilesPerWave <= 2u * kWave, "two registers of records");
+  w.tile0 = tile0;
+#pragma unroll
+  for (uint32_t k = 0; k < 2; ++k) {
+    w.prec[k] = 0x80000000u;
+    if (k * kWave >= VPW * kFastTilesPerWave) continue;
+    const uint32_t c = k * kWave + (threadIdx.x & (kWave - 1));
+    const uint32_t j = min(tile0 + c / VPW, tile0 + ntiles - 1) * VPW + c % VPW;
+    const uint32_t bh = fast_div(j, a.div_t);
+    const uint32_t t = j - bh * a.div_t.div;
+    const uint32_t b = fast_div(bh, a.div_h);
+    const uint32_t h = bh - b * a.H;
+    const int32_t p0 = a.pg.seq[b];
+    bool ok;
+    const uint32_t slot = paged_slot(a.pg, b, h, a.H, (uint32_t)p0 + t, ok);
+    w.prec[k] = ok && p0 >= 0 && (uint32_t)p0 + t >= (uint32_t)p0 ? slot : 0x80000000u;
+  }
 }
 
 // Encode one tile.  WA = angle code width and NB = norm code width of a format fixed at
@@ -857,6 +892,8 @@ __global__ __launch_bounds__(kBlockThreads) void encode_fast_kernel(EncodeArgs a
   EncWave<D> w;
   uint32_t tile0, ntiles;
   if (!enc_wave_setup<D>(a, w, s_sm, tile0, ntiles, MULTI ? s_bins : nullptr)) return;
+  static_assert(!(PAGED && ALIGNED) || MULTI, "aligned tiles: multi-tile launches");
+  if constexpr (PAGED && ALIGNED) paged_records<D>(a, w, tile0, ntiles);
   const bool wide = w.sp.w == 8;
   if (w.sp.mode == 1) {
     if (wide) encode_tiles_fast<D, MULTI, 8, 8, PAGED, false, ALIGNED>(a, w, tile0, ntiles);
