@@ -231,6 +231,12 @@ def test_layout_limits(tvq):
     assert lib.tvq_layout_for_config(ctypes.byref(cfg), 0, 16, ctypes.byref(lay)) == -1
     assert lib.tvq_layout_for_config(ctypes.byref(cfg), 1, 0, ctypes.byref(lay)) == -1
     assert lib.tvq_layout_for_config(ctypes.byref(cfg), 1 << 20, 1 << 12, ctypes.byref(lay)) == -1
+    # the largest cache: batch x heads x capacity just below 2^31 slots, sizes in 64 bits
+    assert lib.tvq_layout_for_config(ctypes.byref(cfg), (1 << 28) - 1, 1, ctypes.byref(lay)) == 0
+    slots = ((1 << 28) - 1) * 8
+    assert lay.total_bytes == slots * (120 + 88) and lay.total_bytes > 1 << 38
+    assert lay.off[0][1][0] == slots * 120               # V angle plane after K's three
+    assert lib.tvq_layout_for_config(ctypes.byref(cfg), 1 << 28, 1, ctypes.byref(lay)) == -1
 
 
 def _bins_code(code, bound, n, a, b, rcp_ulps=0):

@@ -758,13 +758,16 @@ def _attention_check(s, lay, cache, q, layer, t_end, scale, name, q_dtype=None, 
     (64, 4, 600, "n64-k8lin-v4log"),
     (64, 6, 333, "k64log-v256log"),
     (64, 1, 1100, "n256-lin"),
+    (128, 64, 200, "n64-k8lin-v4log"),     # the largest group: 16 passes of 4 heads
+    (64, 64, 150, "k256-v64"),
 ])
 def test_attention_matches_oracle(gpu, d, G, T, fmt):
     """Attention of one query token over the compressed cache (query heads grouped over the
     KV heads), from the codes, against the oracle's fp64 attention over the decoded cache:
     several chunks with a ragged last one, one token, and a short range.  The formats cover
     every table of the kernel at both d (log-space levels of K and of V, n = 64 and 256) and G
-    covers whole, partial (G = 6: two passes of 3 heads) and single-head passes."""
+    covers whole, partial (G = 6: two passes of 3 heads) and single-head passes, up to the
+    largest group the kernels take (64 query heads per KV head)."""
     tables = {
         "n64-k8lin-v4log": [LayerCfg(64, 64), LayerCfg(64, 64)],
         "n256-k4log-v8lin": [LayerCfg(64, 64), LayerCfg(256, 256, 4, 8, NORM_LOG, NORM_LINEAR)],
@@ -836,6 +839,9 @@ def test_attention_api_errors(gpu):
     small = torch.empty(16, dtype=torch.uint8, device="cuda")
     with pytest.raises(tvq.TvqError):
         s.gpu.attention(cache, lay, 0, 40, qd, out, 0.1, workspace=small)
+    big = torch.zeros((2, 2 * 65, 128), dtype=torch.float32, device="cuda")
+    with pytest.raises(tvq.TvqError, match="unsupported"):        # 65 query heads per KV head
+        s.gpu.attention(cache, lay, 0, 40, big, torch.empty_like(big), 0.1)
 
 
 @pytest.mark.parametrize("wl,need_gb", [("C5", 140), ("C4", 8)])
