@@ -325,8 +325,6 @@ __device__ __forceinline__ void store_staged(const DecodeArgs& a, const WaveStat
   }
 }
 
-// PAGED: a position without a pool block reads record 0 of the pool (in bounds); its output is
-// zeroed when stored.
 // Whole-tile rows: the position of the tile's first vector; a paged one takes its pool record
 // from the lane of the tile (looked up once per wave).
 template <int D, bool PAGED>
@@ -343,6 +341,8 @@ __device__ __forceinline__ TilePos rows_pos(const DecodeArgs& a, const WaveState
   }
 }
 
+// PAGED: a position without a pool block reads record 0 of the pool (in bounds); its output is
+// zeroed when stored.
 template <int D, int WA, int NB, bool ROWS = false, bool PAGED = false>
 __device__ __forceinline__ TileCodes<WA, NB> load_tile_codes(const DecodeArgs& a,
                                                               const WaveState<D>& w, uint32_t tile) {
@@ -526,13 +526,35 @@ __global__ __launch_bounds__(kBlockThreads) void decode_generic_kernel(DecodeArg
   store_direct<D, F32OUT>(a, w, pos, o);
 }
 
+// One launch of the instantiation that the call's shape selects.
+template <int D, bool F32>
+void launch_decode(const DecodeArgs& a, bool fast, bool paged, bool multi, bool rows,
+                   unsigned grid, hipStream_t s) {
+  const dim3 g(grid), b(kBlockThreads);
+  if (fast && paged && multi && rows)
+    hipLaunchKernelGGL((decode_fast_kernel<D, F32, true, true, true>), g, b, 0, s, a);
+  else if (fast && paged && multi)
+    hipLaunchKernelGGL((decode_fast_kernel<D, F32, true, false, true>), g, b, 0, s, a);
+  else if (fast && paged)
+    hipLaunchKernelGGL((decode_fast_kernel<D, F32, false, false, true>), g, b, 0, s, a);
+  else if (fast && multi && rows)
+    hipLaunchKernelGGL((decode_fast_kernel<D, F32, true, true>), g, b, 0, s, a);
+  else if (fast && multi)
+    hipLaunchKernelGGL((decode_fast_kernel<D, F32, true>), g, b, 0, s, a);
+  else if (fast)
+    hipLaunchKernelGGL((decode_fast_kernel<D, F32, false>), g, b, 0, s, a);
+  else if (paged)
+    hipLaunchKernelGGL((decode_generic_kernel<D, F32, true>), g, b, 0, s, a);
+  else
+    hipLaunchKernelGGL((decode_generic_kernel<D, F32, false>), g, b, 0, s, a);
+}
+
 }  // namespace
 }  // namespace tvq
 
 int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, unsigned grid,
                       void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  const dim3 block(tvq::kBlockThreads);
   const bool paged = a.pg.table != nullptr;
   const bool multi = a.tiles_per_wave > 1;
   // whole-tile rows: every tile's vectors consecutive tokens of one (batch, head) (of one pool
@@ -541,34 +563,14 @@ int tvq_launch_decode(const tvq::DecodeArgs& a, int d, int out_f32, bool fast, u
   const uint32_t vpw = d == 128 ? 16u : 32u;
   const bool rows = a.div_t.div % vpw == 0 && (!paged || a.t_begin % vpw == 0) &&
                     (uint64_t)a.stride_t * vpw * (out_f32 ? 4u : 2u) < (1ull << 31);
-#define TVQ_LAUNCH_DEC(D, F32)                                                                  \
-  do {                                                                                          \
-    if (fast && paged && multi && rows)                                                         \
-      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true, true, true>), dim3(grid), block, 0, s, a); \
-    else if (fast && paged && multi)                                                            \
-      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true, false, true>), dim3(grid), block, 0, s, a); \
-    else if (fast && paged)                                                                     \
-      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, false, false, true>), dim3(grid), block, 0, s, a); \
-    else if (fast && multi && rows)                                                             \
-      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true, true>), dim3(grid), block, 0, s, a); \
-    else if (fast && multi)                                                                     \
-      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, true>), dim3(grid), block, 0, s, a);  \
-    else if (fast)                                                                              \
-      hipLaunchKernelGGL((tvq::decode_fast_kernel<D, F32, false>), dim3(grid), block, 0, s, a); \
-    else if (paged)                                                                             \
-      hipLaunchKernelGGL((tvq::decode_generic_kernel<D, F32, true>), dim3(grid), block, 0, s, a); \
-    else                                                                                        \
-      hipLaunchKernelGGL((tvq::decode_generic_kernel<D, F32, false>), dim3(grid), block, 0, s, a);\
-  } while (0)
   if (d == 128) {
-    if (out_f32) TVQ_LAUNCH_DEC(128, true);
-    else TVQ_LAUNCH_DEC(128, false);
+    if (out_f32) tvq::launch_decode<128, true>(a, fast, paged, multi, rows, grid, s);
+    else tvq::launch_decode<128, false>(a, fast, paged, multi, rows, grid, s);
   } else if (d == 64) {
-    if (out_f32) TVQ_LAUNCH_DEC(64, true);
-    else TVQ_LAUNCH_DEC(64, false);
+    if (out_f32) tvq::launch_decode<64, true>(a, fast, paged, multi, rows, grid, s);
+    else tvq::launch_decode<64, false>(a, fast, paged, multi, rows, grid, s);
   } else {
     return -1;
   }
-#undef TVQ_LAUNCH_DEC
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }

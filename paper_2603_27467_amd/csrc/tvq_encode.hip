@@ -278,10 +278,8 @@ struct EncWave {
                               // less 8 kRoundShiftBits, modulo 2^32 (fast formats)
   uint32_t bins_off;          // n/2 on lanes holding -z (the half turn), else 0
   bool negated;               // the lane holds -z after the butterfly
-  uint32_t tile0;             // aligned paged tiles: the wave's first tile, and the pool
-  uint32_t prec[2];           // records of vector c = x VPW + v (vector slot v of tile
-                              // tile0 + x), c in register c / 64 of lane c % 64 (bit 31: no
-                              // block)
+  uint32_t tile0;             // aligned paged tiles: the wave's first tile
+  uint32_t prec[2];           // aligned paged tiles: pool records (paged_records)
   float shift;                // rounding shift with the half-turn of a negated lane removed
   uint32_t unneg;             // sign flip that undoes the negation (odd n)
 };
@@ -416,10 +414,11 @@ __device__ __forceinline__ TileIn<F32IN> load_tile(const EncodeArgs& a, const En
   return in;
 }
 
-// Aligned paged tiles: each lane's pool record in each of the wave's tiles, looked up before
-// the tile loop so that the table reads do not wait in the loop.
-// (Held across lanes and read back with a lane permute: an array indexed by the tile would be
-// placed in scratch memory.)  Every tile of an aligned launch is whole.
+// Aligned paged tiles: the pool record of every vector of the wave's tiles, looked up before
+// the tile loop so that the table reads do not wait inside it.  Vector c = x VPW + v (vector
+// slot v of tile tile0 + x) is held in register c / 64 of lane c % 64, bit 31 set when it has
+// no block, and load_tile reads it back with a lane permute (an array indexed by the tile would
+// be placed in scratch memory).  Every tile of an aligned launch is whole.
 template <int D>
 __device__ __forceinline__ void paged_records(const EncodeArgs& a, EncWave<D>& w, uint32_t tile0,
                                               uint32_t ntiles) {
