@@ -192,11 +192,12 @@ def test_paged_encode_decode(gpu, d):
          f"bf16 {chk16.line()}; zeros without a block")
 
 
-@pytest.mark.parametrize("d,G", [(128, 4), (64, 3)])
+@pytest.mark.parametrize("d,G", [(128, 4), (64, 3), (128, 64)])
 def test_paged_attention(gpu, d, G):
     """Attention with a different context length per sequence (one of them 0), through the
     block tables, against the oracle on each sequence's gathered cache; then the same with a
-    smaller max_ctx, which clips the longer contexts."""
+    smaller max_ctx, which clips the longer contexts.  G = 64 is the largest group (16
+    passes over the codes)."""
     import torch
     table = [LayerCfg(64, 64), LayerCfg(256, 256, 4, 8, NORM_LOG, NORM_LINEAR)]
     case = PagedCase(d, table, seed=17 + d)
