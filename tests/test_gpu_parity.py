@@ -807,6 +807,21 @@ def test_attention_random_formats_and_shapes(gpu):
         _attention_check(s, lay, cache, q, 1, t_end, scale, name, q_dtype, o_dtype)
 
 
+@pytest.mark.parametrize("d,T", [(128, 4480), (64, 8960)])
+def test_attention_many_chunks(gpu, d, T):
+    """Contexts split into more than 64 chunks per (sequence, KV head), so the merge takes
+    the chunks' partials in several groups of 64 (2 sequences x 2 KV heads on a device of
+    ~4096 wave slots: 64-token chunks at d = 128, 128-token chunks at d = 64)."""
+    s, lay, cache, q = _attention_case(d, 4, T, [LayerCfg(64, 64), LayerCfg(256, 64)], seed=61)
+    B, Hq = q.shape[0], q.shape[1]
+    ws = s.gpu.attention_workspace_bytes(B, Hq, T)
+    n_chunks = ws // (B * Hq * (4 * d + 8))
+    _say(f"[attn many chunks d={d}] {n_chunks} chunks per output")
+    assert n_chunks > 64
+    for t_end in (T, T - 37):
+        _attention_check(s, lay, cache, q, 1, t_end, 1.0 / np.sqrt(d), f"attn chunks d={d}")
+
+
 def test_attention_dtypes_and_layers(gpu):
     """bf16 queries and outputs, both layers, a large scale (peaked weights)."""
     import torch
