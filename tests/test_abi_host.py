@@ -363,3 +363,21 @@ def test_binding_checks_extents_before_any_call(tvq):
     q = torch.zeros((1, 8, 128))
     with pytest.raises(ValueError, match="cache"):
         c.attention(torch.zeros(100, dtype=torch.uint8), lay, 0, 8, q, torch.zeros_like(q), 0.1)
+
+
+def test_header_is_c99_and_host_calls_work_from_c(tvq, tmp_path):
+    """include/tvq.h compiles as strict C99, and a C program linked against the library gets
+    the layout, rates, signs and refusals its own checks expect (tests/native/abi_c99.c)."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc")
+    if cc is None:
+        pytest.skip("gcc not found")
+    lib = tvq.library_path()
+    exe = str(tmp_path / "abi_c99")
+    subprocess.run([cc, "-std=c99", "-pedantic", "-Wall", "-Wextra", "-Werror",
+                    "-I", os.path.join(ROOT, "include"),
+                    os.path.join(ROOT, "tests", "native", "abi_c99.c"), lib,
+                    "-Wl,-rpath," + os.path.dirname(lib), "-o", exe], check=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok"), r.stdout + r.stderr
