@@ -33,6 +33,13 @@ def build(force: bool = True) -> str:
     return _LIB_PATH
 
 
+def library_path() -> str:
+    """Path of the oracle's shared library, built first when missing or stale (for test
+    programs that link it)."""
+    lib()
+    return _LIB_PATH
+
+
 class _Kind(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int), ("norm_mode", ctypes.c_int), ("norm_bits", ctypes.c_int)]
 
