@@ -37,6 +37,15 @@ import workloads  # noqa: E402
 METRIC = "encode+decode GB/s of bf16 KV and % of HBM peak, d=128, 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "mistral7b_c2_encode_decode_counters.json")
+# the codec counter summary of each workload that has one
+CODEC_COUNTER_FILES = {"C2": "mistral7b_c2_encode_decode_counters.json",
+                       "C3": "c3_early_boost_encode_decode_counters.json",
+                       "C4": "d64_batch8_c4_encode_decode_counters.json"}
+
+
+def codec_counters(workload_key: str):
+    name = CODEC_COUNTER_FILES.get(workload_key)
+    return None if name is None else os.path.join(ROOT, "profiles", name)
 # fp32 VALU issue peak without packed-fp32 instructions: 256 CUs x 4 SIMDs, one wave64
 # instruction per SIMD every 4 cycles, 2.4 GHz
 VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4
@@ -332,12 +341,18 @@ def clock_fields(d: dict, topo, durations, timed: int) -> dict:
             "dispatch_ns": [round(x) for x in durations]}
 
 
-def summarize_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, commands) -> int:
+def summarize_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, commands,
+                       workload_key: str = "C2") -> int:
     """Turn the rocprofv3 output of the profiling runs (kernel trace, FETCH_SIZE, WRITE_SIZE,
-    SQ instruction counts, VALU busy) into the counter summary bench.py reads and a readable
-    table, both under profiles/.  FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are scaled by
-    what they read for the 1 GiB device copy the profiled runs include (--copy-calibration)."""
-    w = workloads.get("C2")
+    SQ instruction counts, VALU busy) of the codec step on `workload_key` into the counter
+    summary bench.py reads and a readable table, both under profiles/.  FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch) are scaled by what they read for the 1 GiB device copy the
+    profiled runs include (--copy-calibration)."""
+    path = codec_counters(workload_key)
+    if path is None:
+        print(f"no codec counter summary is kept for {workload_key}", file=sys.stderr)
+        return 2
+    w = workloads.get(workload_key)
     ab = algorithmic_bytes(w)
     per = {}
 
@@ -436,9 +451,9 @@ def summarize_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, comman
         lines += [ln.rstrip("\n") for ln in f]
     lines += ["```"]
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
-    with open(PROFILE_COUNTERS, "w") as f:
+    with open(path, "w") as f:
         json.dump(out, f, indent=1)
-    with open(PROFILE_COUNTERS.replace("_counters.json", "_counters.md"), "w") as f:
+    with open(path.replace("_counters.json", "_counters.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
     return 0
@@ -858,7 +873,8 @@ def main() -> int:
                     help="also run a plain 1 GiB device copy (for counter scaling)")
     ap.add_argument("--summarize-profiles", nargs=5,
                     metavar=("TRACE", "FETCH", "WRITE", "SQ", "VALU"),
-                    help="write the profiles/ counter summary from rocprofv3 output dirs")
+                    help="write the profiles/ counter summary of the --workload codec step "
+                         "(C2, C3 or C4) from rocprofv3 output dirs")
     ap.add_argument("--summarize-attention-profiles", nargs=6,
                     metavar=("TRACE", "FETCH", "WRITE", "SQ", "VALU", "STEPS_TOTAL"),
                     help="write the profiles/ counter summary of the attention step over "
@@ -873,7 +889,7 @@ def main() -> int:
               file=sys.stderr)
         return 2
     if args.summarize_profiles:
-        return summarize_profiles(*args.summarize_profiles, args.commands)
+        return summarize_profiles(*args.summarize_profiles, args.commands, args.workload)
     if args.summarize_attention_profiles:
         a = args.summarize_attention_profiles
         return summarize_attention_profiles(*a[:5], args.commands, int(a[5]), args.workload)
@@ -979,8 +995,9 @@ def main() -> int:
         ms = float(ms_all.mean())
         gbs = ab["per_launch"] / (ms * 1e-3) / 1e9
         # the committed counters cover the canonical-schedule encode of a contiguous cache
-        prof = (None if (args.encode_mfma and name == "encode") or args.pool
-                else profile_entry(kern, w.name))
+        path = codec_counters(args.workload)
+        prof = (None if (args.encode_mfma and name == "encode") or args.pool or path is None
+                else profile_entry(kern, w.name, path))
         out = {"ms": round(ms, 5), "ms_median": round(float(np.median(ms_all)), 5),
                "ms_min": round(float(ms_all.min()), 5),
                "kv_GBps": round(ab["kv"] / (ms * 1e-3) / 1e9, 2),

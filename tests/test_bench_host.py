@@ -86,3 +86,17 @@ def test_pool_takes_the_codec_step_only(extra):
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--pool", *extra],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2 and "--pool" in r.stderr
+
+
+def test_codec_counter_summaries_exist_for_their_workloads():
+    """Each workload with a codec counter summary has it committed and taken on that workload
+    (its bench line quotes it while the summary's kernel-source hash matches the tree)."""
+    import json
+    b = _bench()
+    for key in b.CODEC_COUNTER_FILES:
+        path = b.codec_counters(key)
+        d = json.load(open(path))
+        assert d["workload"] == workloads.get(key).name
+        assert len(d["kernel_source_hash"]) == 16, key
+        assert set(d["kernels"]) == {"tvq_encode", "tvq_decode"}
+    assert b.codec_counters("C5") is None
