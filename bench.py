@@ -59,6 +59,9 @@ ATTENTION_COUNTER_FILES = {"C5": "longctx_c5_attention_counters.json",
                            "C4": "d64_batch8_c4_attention_counters.json"}
 
 
+LONGCTX_DECODE_COUNTERS = os.path.join(ROOT, "profiles", "longctx_c5_decode_counters.json")
+
+
 def attention_counters(workload_key: str):
     name = ATTENTION_COUNTER_FILES.get(workload_key)
     return None if name is None else os.path.join(ROOT, "profiles", name)
@@ -508,6 +511,69 @@ def longctx_bytes(w: workloads.Workload):
     return rec_tok, kv_tok, qo
 
 
+def summarize_longctx_decode(fetch_dir, write_dir, commands, steps_total: int) -> int:
+    """HBM bytes of the long-context decode (C5: the whole cache decoded every step) from a
+    FETCH_SIZE run and a WRITE_SIZE run of `commands` (`steps_total` = warmup + timed steps,
+    with --copy-calibration): every decode dispatch's KiB scaled by what the counter reads for
+    the 1 GiB copy, summed, per step; beside the algorithmic bytes of the same steps."""
+    w = workloads.get("C5")
+    rec_tok, kv_tok, _ = longctx_bytes(w)
+    t_mean = w.T + (steps_total + 1) / 2            # tokens decoded per step, mean
+    rows = {}
+    for kind, d, counter in (("fetch_kib", fetch_dir, "FETCH_SIZE"),
+                             ("write_kib", write_dir, "WRITE_SIZE")):
+        for r in _csv(_find(d, "counter_collection.csv")):
+            if r["Counter_Name"] != counter:
+                continue
+            k = _short(r["Kernel_Name"])
+            if k == "tvq_decode":
+                k = _kernel_label(r["Kernel_Name"])
+            elif k != "copy":
+                continue
+            rows.setdefault(k, {}).setdefault(kind, []).append(float(r["Counter_Value"]))
+    copy_bytes = float(1 << 30)
+    fetch_scale = copy_bytes / 1024.0 / max(rows["copy"]["fetch_kib"])
+    write_scale = copy_bytes / 1024.0 / max(rows["copy"]["write_kib"])
+    kernels, total = {}, 0.0
+    for k, d in rows.items():
+        if k == "copy":
+            continue
+        fetch = np.array(d["fetch_kib"]) * 1024.0 * fetch_scale
+        write = np.array(d["write_kib"]) * 1024.0 * write_scale
+        total += float(fetch.sum() + write.sum())
+        kernels[k] = {"dispatches": len(fetch), "fetch_bytes_median": int(np.median(fetch)),
+                      "write_bytes_median": int(np.median(write))}
+    alg = (rec_tok + kv_tok) * t_mean
+    out = {"kernel_source_hash": kernel_source_hash(), "workload": w.name,
+           "steps_total": steps_total, "tokens_decoded_per_step_mean": t_mean,
+           "hbm_bytes_per_step": int(round(total / steps_total)),
+           "algorithmic_bytes_per_step": int(round(alg)),
+           "fetch_scale_from_copy": round(fetch_scale, 4),
+           "write_scale_from_copy": round(write_scale, 4), "kernels": kernels,
+           "commands": commands}
+    lines = [f"# Long-context decode traffic: {w.name} (L={w.L}, B={w.B}, H={w.H}, "
+             f"T={w.T} cached + 1 per step, d={w.d})", "",
+             "Commands (run from /tmp, repository root $R):", ""]
+    lines += [f"    {c}" for c in commands]
+    lines += ["", f"FETCH_SIZE scale from the 1 GiB copy: {fetch_scale:.4f}; WRITE_SIZE scale: "
+              f"{write_scale:.4f}", "",
+              "| decode kernel | dispatches | median fetch bytes | median write bytes |",
+              "|---|---|---|---|"]
+    for k, e in kernels.items():
+        lines.append(f"| {k} | {e['dispatches']} | {e['fetch_bytes_median']} | "
+                     f"{e['write_bytes_median']} |")
+    lines += ["", f"Per step ({steps_total} steps, {t_mean:.1f} tokens decoded per step on "
+              f"average): HBM {out['hbm_bytes_per_step']} bytes by the counters, "
+              f"{out['algorithmic_bytes_per_step']} algorithmic, ratio "
+              f"{out['hbm_bytes_per_step'] / out['algorithmic_bytes_per_step']:.4f}."]
+    with open(LONGCTX_DECODE_COUNTERS, "w") as f:
+        json.dump(out, f, indent=1)
+    with open(LONGCTX_DECODE_COUNTERS.replace(".json", ".md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
+
+
 def summarize_attention_profiles(trace_dir, fetch_dir, write_dir, sq_dir, valu_dir, commands,
                                  steps_total: int, workload_key: str = "C5") -> int:
     """Counter summary of the attention step over the cache of `workload_key` (the runs of
@@ -816,6 +882,16 @@ def run_longctx(w: workloads.Workload, args) -> dict:
         }
     dec_bytes = (rec_tok + kv_tok) * t_mean
     dec_gbs = dec_bytes / (dec_ms * 1e-3) / 1e9
+    # the committed decode traffic of this workload, scaled to this run's mean range
+    traffic = None
+    try:
+        with open(LONGCTX_DECODE_COUNTERS) as f:
+            cnt = json.load(f)
+        if cnt.get("workload") == w.name and cnt.get("kernel_source_hash") == kernel_source_hash():
+            traffic = int(round(cnt["hbm_bytes_per_step"] * t_mean /
+                                cnt["tokens_decoded_per_step_mean"]))
+    except (OSError, ValueError, KeyError):
+        traffic = None
     return {
         "metric": METRIC,
         "value": round(value, 2),
@@ -836,7 +912,7 @@ def run_longctx(w: workloads.Workload, args) -> dict:
                    "compressed_bytes_per_token": rec_tok},
         "roofline": {"bound": "hbm", "kernel": "tvq_decode",
                      "achieved": round(dec_gbs, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(dec_gbs / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(dec_gbs / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": int(dec_bytes)},
         "encode": {"ms": round(float(enc.mean()), 5), "ms_min": round(float(enc.min()), 5),
                    "vectors": 2 * w.L * w.B * w.H, "algorithmic_bytes": enc_bytes},
@@ -879,6 +955,9 @@ def main() -> int:
                     metavar=("TRACE", "FETCH", "WRITE", "SQ", "VALU", "STEPS_TOTAL"),
                     help="write the profiles/ counter summary of the attention step over "
                          "the --workload cache (C5 or C4) from rocprofv3 output dirs")
+    ap.add_argument("--summarize-longctx-decode", nargs=3,
+                    metavar=("FETCH", "WRITE", "STEPS_TOTAL"),
+                    help="write the profiles/ traffic summary of the long-context decode (C5)")
     ap.add_argument("--commands", nargs="*", default=[],
                     help="the profiling commands, recorded in the summary")
     args = ap.parse_args()
@@ -890,6 +969,9 @@ def main() -> int:
         return 2
     if args.summarize_profiles:
         return summarize_profiles(*args.summarize_profiles, args.commands, args.workload)
+    if args.summarize_longctx_decode:
+        a = args.summarize_longctx_decode
+        return summarize_longctx_decode(a[0], a[1], args.commands, int(a[2]))
     if args.summarize_attention_profiles:
         a = args.summarize_attention_profiles
         return summarize_attention_profiles(*a[:5], args.commands, int(a[5]), args.workload)

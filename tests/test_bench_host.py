@@ -100,3 +100,6 @@ def test_codec_counter_summaries_exist_for_their_workloads():
         assert len(d["kernel_source_hash"]) == 16, key
         assert set(d["kernels"]) == {"tvq_encode", "tvq_decode"}
     assert b.codec_counters("C5") is None
+    d = json.load(open(b.LONGCTX_DECODE_COUNTERS))
+    assert d["workload"] == workloads.get("C5").name
+    assert 1.0 <= d["hbm_bytes_per_step"] / d["algorithmic_bytes_per_step"] < 1.1
