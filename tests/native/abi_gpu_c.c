@@ -185,7 +185,7 @@ int main(void) {
               int32_t a, c;
               memcpy(&a, &hg[e], 4);
               memcpy(&c, &ho[e], 4);
-              if (abs(a - c) > 2) ++hdr_bad;
+              if (llabs((long long)a - (long long)c) > 2) ++hdr_bad;
             }
           }
 
