@@ -822,6 +822,54 @@ def test_attention_many_chunks(gpu, d, T):
         _attention_check(s, lay, cache, q, 1, t_end, 1.0 / np.sqrt(d), f"attn chunks d={d}")
 
 
+def test_concurrent_streams_match_sequential(gpu):
+    """One codec used from two streams at once (the handle is immutable): encode, decode and
+    attention of two different caches interleaved on two streams give the same bytes as the
+    same calls made one after another on the current stream."""
+    import torch
+    w = workloads.get("C2")
+    L, B, H, T, d = 2, 2, 4, 600, 128
+    table = [LayerCfg(64, 64), LayerCfg(256, 64)]
+    s = Setup(L, H, d, table, workloads.sign_table(71, L, d)).build()
+    lay = s.gpu.layout(B, T)
+    ins = []
+    for seed in (72, 73):
+        k, v = _draw(w, L, B, H, T, d, "bf16", seed)
+        ins.append((bf16_bits_to_torch(k).cuda(), bf16_bits_to_torch(v).cuda()))
+    rng = np.random.default_rng(74)
+    q = torch.from_numpy(rng.standard_normal((B, 4 * H, d)).astype(np.float32)).cuda()
+    ws = s.gpu.attention_workspace_bytes(B, 4 * H, T)
+
+    def buffers():
+        return [dict(cache=torch.zeros(lay.total_bytes, dtype=torch.uint8, device="cuda"),
+                     ko=torch.empty_like(ins[0][0]), vo=torch.empty_like(ins[0][1]),
+                     o=torch.empty_like(q),
+                     ws=torch.empty(ws, dtype=torch.uint8, device="cuda")) for _ in range(2)]
+
+    def run(i, bufs, stream):
+        bb = bufs[i]
+        s.gpu.encode(ins[i][0], ins[i][1], bb["cache"], lay, 0, stream)
+        s.gpu.decode(bb["cache"], lay, 0, T, bb["ko"], bb["vo"], stream)
+        s.gpu.attention(bb["cache"], lay, 1, T, q, bb["o"], 1.0 / np.sqrt(d), bb["ws"], stream)
+
+    ref = buffers()
+    for i in range(2):
+        run(i, ref, None)
+    torch.cuda.synchronize()
+    got = buffers()
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]        # default priority
+    for rep in range(3):
+        for i in range(2):
+            run(i, got, streams[i])
+    torch.cuda.synchronize()
+    for i in range(2):
+        for key in ("cache", "ko", "vo", "o"):
+            assert torch.equal(got[i][key].view(torch.uint8), ref[i][key].view(torch.uint8)), \
+                (i, key)
+    _say("[streams] two streams, 3 rounds: caches, decodes and attention equal the sequential calls")
+
+
 def test_attention_dtypes_and_layers(gpu):
     """bf16 queries and outputs, both layers, a large scale (peaked weights)."""
     import torch
