@@ -248,8 +248,10 @@ tvq_status tvq_encode_paged(const tvq_codec* c, tvq_dtype in_dtype, const void* 
 
 /* Decode (as tvq_decode) positions [t_begin, t_end) of the out->batch sequences of a paged
  * pool into k_out / v_out (out->tokens == t_end - t_begin, t_end <= max_blocks *
- * block_tokens).  Up to two kernel launches on `stream` (one for the layers whose formats
- * have a dedicated kernel, one for the rest); an empty range launches nothing. */
+ * block_tokens).  Launches as tvq_decode: up to two kernels on `stream` (one for the layers
+ * whose formats have a dedicated kernel, one for the rest), twice over for a range of at least
+ * 2^19 vectors per kind that starts on a multiple of the tile's token count and whose token
+ * count is not one; an empty range launches nothing. */
 tvq_status tvq_decode_paged(const tvq_codec* c, const void* pool, const tvq_layout* pool_layout,
                             const int32_t* block_table, int32_t max_blocks, int64_t t_begin,
                             int64_t t_end, tvq_dtype out_dtype, void* k_out, void* v_out,

@@ -792,6 +792,30 @@ tvq_status tvq_decode_paged(const tvq_codec* c, const void* pool, const tvq_layo
   a.n_slots = pool_layout->batch * c->H * pool_layout->capacity_tokens;
   a.cap = (uint32_t)pool_layout->capacity_tokens;
   a.t_begin = (uint32_t)t_begin;
+  // As tvq_decode: a large range from a tile boundary whose token count is not a multiple of
+  // the tile's vectors is decoded as its whole tiles per row (one block lookup per tile), then
+  // the remaining tokens of every row.
+  const int64_t vpw = tvq::kWave / (c->d / tvq::kElemsPerLane);
+  const int64_t whole = out->tokens / vpw * vpw;
+  if (t_begin % vpw == 0 && whole > 0 && whole != out->tokens &&
+      out->batch * c->H * whole >= kSplitVectors) {
+    tvq_tensor_desc head = *out, tail = *out;
+    head.tokens = whole;
+    tail.tokens = out->tokens - whole;
+    const tvq::DecodeArgs b0 = a;
+    tvq_status st = decode_launch(c, a, &head, out_dtype, k_out, v_out, stream);
+    if (st != TVQ_OK) return st;
+    tvq::DecodeArgs b;
+    std::memset(&b, 0, sizeof(b));
+    b.cache = b0.cache;
+    b.n_slots = b0.n_slots;
+    b.cap = b0.cap;
+    b.pg = b0.pg;
+    b.t_begin = (uint32_t)(t_begin + whole);
+    const int64_t skip = whole * out->stride_t * eb;   // bytes of the head's tokens in a row
+    return decode_launch(c, b, &tail, out_dtype, (char*)k_out + skip, (char*)v_out + skip,
+                         stream);
+  }
   return decode_launch(c, a, out, out_dtype, k_out, v_out, stream);
 }
 

@@ -389,6 +389,53 @@ def test_paged_multi_tile(gpu, d, T):
     assert np.array_equal(gw.view(np.uint32), full[torch.float32][..., t0:t1, :].view(np.uint32))
 
 
+def test_paged_decode_large_ragged_split(gpu):
+    """A paged decode of 2^19 + whole-tile vectors per kind whose token count is not a multiple
+    of the tile's (1 layer, 4 sequences x 8 KV heads x 16389 tokens in 256-slot shuffled
+    blocks): decoded as whole tiles per row, then the 5 remaining tokens of every row.  The
+    result equals the two parts decoded by separate calls bit for bit, and sampled vectors (the
+    last tokens of every row, 400 random ones) meet the decode bars against the oracle's fp64
+    decode of the gathered records."""
+    import torch
+    L, B, H, d, Pb, T = 1, 4, 8, 128, 256, 16389
+    vpw = 64 // (d // 32)
+    whole = T // vpw * vpw
+    assert B * H * whole >= 1 << 19 and whole != T
+    s = Setup(L, H, d, [LayerCfg(64, 64)], workloads.sign_table(81, L, d)).build()
+    max_blocks = -(-T // Pb)
+    n_blocks = B * max_blocks
+    table = np.random.default_rng(82).permutation(n_blocks).astype(np.int32).reshape(B, max_blocks)
+    pool_lay = s.gpu.pool_layout(n_blocks, Pb)
+    pool = torch.full((pool_lay.total_bytes,), POISON, dtype=torch.uint8, device="cuda")
+    table_dev = torch.from_numpy(table).cuda()
+    k, v = _draw(L, B, H, T, d, 83)
+    s.gpu.encode_paged(bf16_bits_to_torch(k).cuda(), bf16_bits_to_torch(v).cuda(),
+                       torch.zeros(B, dtype=torch.int32, device="cuda"), table_dev, pool, pool_lay)
+    shape = (L, B, H, T, d)
+    ko = torch.full(shape, float("nan"), dtype=torch.float32, device="cuda")
+    vo = torch.full_like(ko, float("nan"))
+    s.gpu.decode_paged(pool, pool_lay, table_dev, 0, T, ko, vo)              # split inside
+    k2, v2 = torch.full_like(ko, float("nan")), torch.full_like(ko, float("nan"))
+    for t0, t1 in ((0, whole), (whole, T)):                                    # two calls
+        s.gpu.decode_paged(pool, pool_lay, table_dev, t0, t1, k2[..., t0:t1, :], v2[..., t0:t1, :])
+    torch.cuda.synchronize()
+    assert torch.equal(ko.view(torch.int32), k2.view(torch.int32))
+    assert torch.equal(vo.view(torch.int32), v2.view(torch.int32))
+    host = torch_to_np(pool)
+    g = np.stack([torch_to_np(ko), torch_to_np(vo)], axis=1)                  # [L,2,B,H,T,d]
+    rng = np.random.default_rng(84)
+    chk = DecodeCheck()
+    for b in range(B):
+        gath = gather_paged(host, s, n_blocks, Pb, table[b], POISON)
+        cap = max_blocks * Pb
+        picks = list(range(T - 8, T)) + [int(x) for x in rng.integers(0, T, 100)]
+        for t in picks:
+            ref64 = s.orc.decode_cache(gath, 1, cap, t, t + 1, "f64")[:, :, 0]
+            check_decoded(chk, ref64, d, g32=g[:, :, b, :, t:t + 1])
+    _say(f"[paged split] {chk.line()}")
+    assert chk.ok()
+
+
 def test_paged_step_graph_replay(gpu):
     """A decode step -- append one token per sequence and layer, then attention of every
     layer with contexts one past the appended positions, then advance the positions on the
