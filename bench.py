@@ -69,6 +69,55 @@ ATTN_GROUP = 4          # query heads per KV head (32 query heads over 8 KV head
 PAGE_TOKENS = 256       # slots per block of the paged pool
 
 
+# HIP event flag: no system-scope fence (cache write-back and invalidation) when the event is
+# recorded.  The HIP runtime documents it for events that only time work: the default fence
+# writes the GPU's caches back between the timed kernels and slows the one that follows.
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
+
+
+class TimingEvent:
+    """A HIP timing event created with HIP_EVENT_DISABLE_SYSTEM_FENCE, recorded on a stream;
+    the interface of torch.cuda.Event that the bench uses (record, elapsed_time in ms)."""
+    _hip = None
+
+    @classmethod
+    def _lib(cls):
+        if cls._hip is None:
+            import ctypes
+            lib = ctypes.CDLL("libamdhip64.so")
+            lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                ctypes.c_void_p]
+            lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            cls._hip = lib
+        return cls._hip
+
+    def __init__(self):
+        import ctypes
+        self._ev = ctypes.c_void_p()
+        if self._lib().hipEventCreateWithFlags(ctypes.byref(self._ev),
+                                               HIP_EVENT_DISABLE_SYSTEM_FENCE) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
+
+    def record(self, stream=None):
+        import torch
+        s = stream if stream is not None else torch.cuda.current_stream()
+        if self._lib().hipEventRecord(self._ev, s.cuda_stream) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_time(self, end) -> float:
+        import ctypes
+        ms = ctypes.c_float()
+        if self._lib().hipEventElapsedTime(ctypes.byref(ms), self._ev, end._ev) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def __del__(self):
+        if self._hip is not None and self._ev:
+            self._hip.hipEventDestroy(self._ev)
+
+
 def kernel_source_hash(names=None) -> str:
     h = hashlib.sha256()
     for name in names or CODEC_SOURCES:
@@ -481,7 +530,7 @@ def copy_peak(nbytes: int = 1 << 30, reps: int = 10) -> dict:
     src = torch.zeros(nbytes // 4, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     torch.add(src, 0.0, out=dst)
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev = [TimingEvent() for _ in range(reps + 1)]
     torch.cuda.synchronize()
     ev[0].record()
     for i in range(reps):
@@ -818,7 +867,7 @@ def run_longctx(w: workloads.Workload, args) -> dict:
     torch.cuda.synchronize()
     if args.copy_calibration:
         copy_calibration()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    ev = [[TimingEvent() for _ in range(3)] for _ in range(args.steps)]
     print(f"# timing {args.steps} steps", file=sys.stderr, flush=True)
     t_wall = time.perf_counter()
     for i in range(args.steps):
@@ -1057,7 +1106,7 @@ def main() -> int:
     if args.copy_calibration:
         copy_calibration()
 
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    ev = [[TimingEvent() for _ in range(3)] for _ in range(args.steps)]
     print(f"# timing {args.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
